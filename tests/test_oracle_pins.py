@@ -1,0 +1,329 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+None of these tests touch the GPU.  Each one checks the oracle against
+something other than itself: hand-worked values, closed forms, special cases
+that reduce to a textbook rule, torch autograd, finite differences, or
+invariants stated in the paper.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from tests import torchref
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+FW_MLP, FW_SWIGLU = 0, 1
+
+
+def read_golden(name):
+    vals = {}
+    with open(os.path.join(GOLDEN, name)) as fh:
+        for line in fh:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, rhs = line.split("=", 1)
+            vals[key.strip()] = np.array([float(x) for x in rhs.split()])
+    return vals
+
+
+# --------------------------------------------------------------- scalar kernels
+@pytest.mark.parametrize("name", ["coeffs_c2.txt", "coeffs_no_momentum.txt"])
+def test_coeffs_golden(oracle, name):
+    g = read_golden(name)
+    kw, km, (cw, cm, cb) = oracle.chunk_coeffs(g["eta"], g["beta"], g["gamma"])
+    np.testing.assert_allclose(kw, g["kw"], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(km, g["km"], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose([cw, cm, cb], [g["cw"][0], g["cm"][0], g["cb"][0]], rtol=1e-14,
+                               atol=1e-15)
+
+
+@pytest.mark.parametrize("C", [1, 2, 5, 16, 64])
+def test_coeffs_unit_retention(oracle, C):
+    # App. A.2: beta = gamma = 1  =>  R_t = C - t + 1, K^W_t = eta_t (C - t + 1),
+    # K^M_t = eta_t, carries (1, C, 1).
+    rng = np.random.default_rng(C)
+    eta = rng.uniform(0.01, 0.1, C)
+    kw, km, (cw, cm, cb) = oracle.chunk_coeffs(eta, np.ones(C), np.ones(C))
+    t = np.arange(1, C + 1)
+    np.testing.assert_allclose(kw, eta * (C - t + 1), rtol=1e-14)
+    np.testing.assert_allclose(km, eta, rtol=1e-14)
+    assert (cw, cb) == (1.0, 1.0)
+    assert cm == pytest.approx(C, rel=1e-14)
+
+
+def scalar_recurrence(eta, beta, gamma):
+    """Coefficients read off the recurrence of eq. (7) run on basis vectors:
+    the state lives in span{W0, M0, G_1..G_C}."""
+    C = len(eta)
+    n = C + 2
+    W = np.zeros(n)
+    M = np.zeros(n)
+    W[0] = 1.0
+    M[1] = 1.0
+    for t in range(C):
+        G = np.zeros(n)
+        G[2 + t] = 1.0
+        M = beta[t] * M + eta[t] * G
+        W = gamma[t] * W + M
+    return W, M
+
+
+@pytest.mark.parametrize("C", [1, 3, 16, 64])
+def test_coeffs_vs_recurrence_and_ratio_form(oracle, C):
+    rng = np.random.default_rng(100 + C)
+    eta = 0.1 / (1 + np.exp(-rng.standard_normal(C)))
+    beta = 1 / (1 + np.exp(-rng.normal(1, 1, C)))
+    gamma = 1 - eta * 0.1 / (1 + np.exp(-rng.standard_normal(C)))
+    kw, km, (cw, cm, cb) = oracle.chunk_coeffs(eta, beta, gamma)
+    W, M = scalar_recurrence(eta, beta, gamma)
+    np.testing.assert_allclose(kw, W[2:], rtol=1e-12)
+    np.testing.assert_allclose(km, M[2:], rtol=1e-12, atol=1e-300)
+    np.testing.assert_allclose([cw, cm], W[:2], rtol=1e-12)
+    np.testing.assert_allclose([0.0, cb], M[:2], rtol=1e-12)
+    # The paper's own ratio form (eq. (9)-(11)), valid for beta > 0.
+    bt = np.array([np.prod(beta[t:]) for t in range(1, C + 1)])       # beta-tilde_t, t=1..C
+    gt = np.array([np.prod(gamma[t:]) for t in range(1, C + 1)])
+    R = np.array([np.sum(gt[t - 1:] / bt[t - 1:]) for t in range(1, C + 1)])
+    np.testing.assert_allclose(kw, eta * bt * R, rtol=1e-10)
+    np.testing.assert_allclose(km, eta * bt, rtol=1e-12)
+    np.testing.assert_allclose(cw, np.prod(gamma), rtol=1e-12)
+    np.testing.assert_allclose(cm, np.prod(beta) * R[0], rtol=1e-10)
+    np.testing.assert_allclose(cb, np.prod(beta), rtol=1e-12)
+
+
+def test_coeffs_bounds(oracle):
+    # App. A.2: for beta, gamma in (0, 1], 0 <= beta-tilde_t R_t <= C - t + 1
+    # and K^M_t <= eta_t.
+    rng = np.random.default_rng(7)
+    for C in (4, 64):
+        for _ in range(50):
+            eta = rng.uniform(0, 0.1, C)
+            beta = rng.uniform(0, 1, C)
+            gamma = rng.uniform(0, 1, C)
+            kw, km, _ = oracle.chunk_coeffs(eta, beta, gamma)
+            S = kw / eta
+            t = np.arange(1, C + 1)
+            assert np.all(S >= 0) and np.all(S <= C - t + 1 + 1e-12)
+            assert np.all(km <= eta + 1e-15)
+
+
+# --------------------------------------------------------------- fast-weight net
+NETS = [(FW_MLP, 0), (FW_MLP, 1), (FW_SWIGLU, 0), (FW_SWIGLU, 1)]
+
+
+@pytest.mark.parametrize("fw,flags", NETS)
+def test_net_and_gradient_vs_autograd(oracle, fw, flags):
+    d, dh = 8, 12
+    rng = np.random.default_rng(11 + fw + 2 * flags)
+    P = oracle.param_count(d, dh, fw)
+    W = rng.standard_normal(P) * 0.3
+    k = rng.standard_normal((5, d))
+    v = rng.standard_normal((5, d))
+    resln = flags == 0
+    f = oracle.net(W, k, fw=fw, dh=dh, flags=flags)
+    G = oracle.neg_grad(W, k, v, fw=fw, dh=dh, flags=flags)
+    Wt = torch.tensor(W)
+    for r in range(5):
+        ft = torchref.net(Wt, torch.tensor(k[r]), d, dh, fw, resln)
+        np.testing.assert_allclose(f[r], ft.numpy(), rtol=1e-12, atol=1e-13)
+        Gt = torchref.neg_grad(Wt, torch.tensor(k[r]), torch.tensor(v[r]), d, dh, fw, resln)
+        np.testing.assert_allclose(G[r], Gt.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def test_net_zero_first_layer(oracle):
+    # W1 = 0 => h = 0, GELU(0) = 0, y = 0, LN(0) = 0, so f(x) = x exactly.
+    d, dh = 16, 64
+    rng = np.random.default_rng(3)
+    W = np.concatenate([np.zeros(dh * d), rng.standard_normal(d * dh)])
+    x = rng.standard_normal((4, d))
+    assert np.array_equal(oracle.net(W, x, fw=FW_MLP, dh=dh), x)
+    # SwiGLU with W_down = 0: y = 0, f(x) = x.
+    W = np.concatenate([rng.standard_normal(2 * dh * d), np.zeros(d * dh)])
+    assert np.array_equal(oracle.net(W, x, fw=FW_SWIGLU, dh=dh), x)
+
+
+# --------------------------------------------------------------- forward pins
+def rand_problem(T, d, dh, fw, seed, scale=0.3, with_gamma=True, m_in=True):
+    rng = np.random.default_rng(seed)
+    P = (2 if fw == 0 else 3) * d * dh
+    x = dict(
+        q=rng.standard_normal((1, 1, T, d)), k=rng.standard_normal((1, 1, T, d)),
+        v=rng.standard_normal((1, 1, T, d)),
+        eta=rng.uniform(0.01, 0.1, (1, 1, T)), beta=rng.uniform(0.3, 0.95, (1, 1, T)),
+        gamma=rng.uniform(0.9, 1.0, (1, 1, T)) if with_gamma else None,
+        w_in=rng.standard_normal((1, 1, P)) * scale,
+        m_in=rng.standard_normal((1, 1, P)) * 0.05 if m_in else None)
+    return x
+
+
+@pytest.mark.parametrize("fw,flags", NETS)
+def test_chunk_size_one_is_online_gd_with_momentum(oracle, fw, flags):
+    # C = 1: the gradient is taken at W_{t-1}, so the method is exact online
+    # gradient descent with momentum and decay; outputs read W_{t-1}.
+    T, d, dh = 9, 6, 10
+    x = rand_problem(T, d, dh, fw, 21 + fw)
+    out, wo, mo = oracle.forward(**x, C=1, fw=fw, dh=dh, flags=flags)
+    W = torch.tensor(x["w_in"][0, 0])
+    M = torch.tensor(x["m_in"][0, 0])
+    resln = flags == 0
+    for t in range(T):
+        o = torchref.net(W, torch.tensor(x["q"][0, 0, t]), d, dh, fw, resln)
+        np.testing.assert_allclose(out[0, 0, t], o.numpy(), rtol=1e-10, atol=1e-12)
+        G = torchref.neg_grad(W, torch.tensor(x["k"][0, 0, t]), torch.tensor(x["v"][0, 0, t]), d,
+                              dh, fw, resln)
+        M = x["beta"][0, 0, t] * M + x["eta"][0, 0, t] * G
+        W = x["gamma"][0, 0, t] * W + M
+    np.testing.assert_allclose(wo[0, 0], W.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(mo[0, 0], M.numpy(), rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("fw", [FW_MLP, FW_SWIGLU])
+@pytest.mark.parametrize("C,T", [(1, 5), (2, 8), (4, 11), (8, 8), (16, 37)])
+def test_chunk_end_states_match_closed_form(oracle, fw, C, T):
+    # Prop. 1: W_C = cw W0 + cm M0 + sum K^W_t G_t, M_C = cb M0 + sum K^M_t G_t,
+    # with G_t at the chunk-start weights; ragged last chunks use their own length.
+    d, dh = 5, 7
+    x = rand_problem(T, d, dh, fw, 300 + C + T)
+    out, wo, mo = oracle.forward(**x, C=C, fw=fw, dh=dh)
+    W = x["w_in"][0, 0].copy()
+    M = x["m_in"][0, 0].copy()
+    for s0 in range(0, T, C):
+        sl = slice(s0, min(T, s0 + C))
+        eta, beta, gamma = (x[n][0, 0, sl] for n in ("eta", "beta", "gamma"))
+        L = len(eta)
+        bt = np.array([np.prod(beta[t:]) for t in range(1, L + 1)])
+        gt = np.array([np.prod(gamma[t:]) for t in range(1, L + 1)])
+        R = np.array([np.sum(gt[t - 1:] / bt[t - 1:]) for t in range(1, L + 1)])
+        G = torch.stack([torchref.neg_grad(torch.tensor(W), torch.tensor(x["k"][0, 0, t]),
+                                           torch.tensor(x["v"][0, 0, t]), d, dh, fw)
+                         for t in range(sl.start, sl.stop)]).numpy()
+        Wn = np.prod(gamma) * W + np.prod(beta) * R[0] * M + (eta * bt * R) @ G
+        M = np.prod(beta) * M + (eta * bt) @ G
+        W = Wn
+    np.testing.assert_allclose(wo[0, 0], W, rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(mo[0, 0], M, rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("fw", [FW_MLP, FW_SWIGLU])
+def test_zero_learning_rate_leaves_state(oracle, fw):
+    # eta = 0, gamma = 1, M0 = 0: W_t = W_{t-1}, M_t = 0, so the state is
+    # unchanged bitwise and every output is f_{W_in}(q_t).
+    T, d, dh = 40, 8, 16
+    x = rand_problem(T, d, dh, fw, 5, with_gamma=False, m_in=False)
+    x["eta"] = np.zeros_like(x["eta"])
+    out, wo, mo = oracle.forward(**x, C=16, fw=fw, dh=dh)
+    assert np.array_equal(wo, x["w_in"])
+    assert np.array_equal(mo, np.zeros_like(mo))
+    np.testing.assert_array_equal(out[0, 0], oracle.net(x["w_in"][0, 0], x["q"][0, 0], fw=fw, dh=dh))
+
+
+def test_zero_first_layer_chunk_zero(oracle):
+    # MLP with W1 = 0, M0 = 0: chunk 0 outputs are q_t exactly; a = GELU(0) = 0,
+    # so the W2 part of every G_t vanishes and W2_C = cw W2_0, M2_C = 0.
+    T, d, dh, C = 16, 8, 12, 16
+    x = rand_problem(T, d, dh, FW_MLP, 9, m_in=False)
+    x["w_in"][0, 0, : dh * d] = 0.0
+    out, wo, mo = oracle.forward(**x, C=C, fw=FW_MLP, dh=dh)
+    np.testing.assert_array_equal(out[0, 0], x["q"][0, 0])
+    cw = np.prod(x["gamma"][0, 0])
+    np.testing.assert_allclose(wo[0, 0, dh * d:], cw * x["w_in"][0, 0, dh * d:], rtol=1e-13)
+    assert np.all(mo[0, 0, dh * d:] == 0.0)
+
+
+@pytest.mark.parametrize("fw", [FW_MLP, FW_SWIGLU])
+def test_resume_is_exact(oracle, fw):
+    # Chunk-end states are the whole recurrent state (Sec. 3.1): running T
+    # tokens equals running T1 tokens then the remaining ones from (W, M).
+    T, T1, d, dh, C = 48, 16, 6, 9, 8
+    x = rand_problem(T, d, dh, fw, 77)
+    out, wo, mo = oracle.forward(**x, C=C, fw=fw, dh=dh)
+
+    def part(sl, w_in, m_in):
+        y = {n: (a[:, :, sl] if n not in ("w_in", "m_in") and a is not None else a)
+             for n, a in x.items()}
+        y["w_in"], y["m_in"] = w_in, m_in
+        return oracle.forward(**y, C=C, fw=fw, dh=dh)
+
+    o1, w1, m1 = part(slice(0, T1), x["w_in"], x["m_in"])
+    o2, w2, m2 = part(slice(T1, T), w1, m1)
+    assert np.array_equal(np.concatenate([o1, o2], axis=2), out)
+    assert np.array_equal(w2, wo) and np.array_equal(m2, mo)
+
+
+# --------------------------------------------------------------- backward pins
+def loss_and_grads(oracle, x, dO, dw, dm, C, fw, dh, flags=0):
+    out, wo, mo = oracle.forward(**x, C=C, fw=fw, dh=dh, flags=flags)
+    J = np.sum(dO * out) + np.sum(dw * wo) + np.sum(dm * mo)
+    return J
+
+
+@pytest.mark.parametrize("fw,flags", NETS)
+@pytest.mark.parametrize("C", [1, 2, 3, 8])
+def test_backward_finite_differences(oracle, fw, flags, C):
+    T, d, dh = 8, 4, 6
+    x = rand_problem(T, d, dh, fw, 1000 + 10 * C + fw + 2 * flags)
+    rng = np.random.default_rng(5 + C)
+    P = x["w_in"].shape[-1]
+    dO = rng.standard_normal(x["q"].shape)
+    dw = rng.standard_normal((1, 1, P))
+    dm = rng.standard_normal((1, 1, P))
+    g = oracle.backward(**x, d_out=dO, d_w_out=dw, d_m_out=dm, C=C, fw=fw, dh=dh, flags=flags)
+    names = {"q": "dq", "k": "dk", "v": "dv", "eta": "d_eta", "beta": "d_beta",
+             "gamma": "d_gamma", "w_in": "d_w_in", "m_in": "d_m_in"}
+    h = 1e-6
+    for inp, gname in names.items():
+        direction = rng.standard_normal(x[inp].shape)
+
+        def J(s):
+            xs = dict(x)
+            xs[inp] = x[inp] + s * h * direction
+            return loss_and_grads(oracle, xs, dO, dw, dm, C, fw, dh, flags)
+
+        # fourth-order central difference
+        fd = (-J(2) + 8 * J(1) - 8 * J(-1) + J(-2)) / (12 * h)
+        an = np.sum(g[gname] * direction)
+        assert abs(fd - an) <= 1e-7 * max(1.0, abs(an)), (inp, fd, an)
+
+
+@pytest.mark.parametrize("fw,flags", NETS)
+@pytest.mark.parametrize("C,T", [(4, 8), (3, 7)])
+def test_backward_vs_autograd(oracle, fw, flags, C, T):
+    # The whole chunked recurrence differentiated by torch autograd (second
+    # order through autograd.grad(create_graph=True)), in fp64.
+    d, dh = 4, 6
+    x = rand_problem(T, d, dh, fw, 2000 + C + fw + 2 * flags)
+    rng = np.random.default_rng(9)
+    P = x["w_in"].shape[-1]
+    dO = rng.standard_normal(x["q"].shape)
+    dw = rng.standard_normal((1, 1, P))
+    dm = rng.standard_normal((1, 1, P))
+    g = oracle.backward(**x, d_out=dO, d_w_out=dw, d_m_out=dm, C=C, fw=fw, dh=dh, flags=flags)
+    tx = {n: torch.tensor(a[0, 0], requires_grad=True) for n, a in x.items()}
+    out, W, M = torchref.chunked_forward(tx["q"], tx["k"], tx["v"], tx["eta"], tx["beta"],
+                                         tx["gamma"], tx["w_in"], tx["m_in"], C, d, dh, fw,
+                                         resln=flags == 0)
+    J = (torch.tensor(dO[0, 0]) * out).sum() + (torch.tensor(dw[0, 0]) * W).sum() + \
+        (torch.tensor(dm[0, 0]) * M).sum()
+    J.backward()
+    names = {"q": "dq", "k": "dk", "v": "dv", "eta": "d_eta", "beta": "d_beta",
+             "gamma": "d_gamma", "w_in": "d_w_in", "m_in": "d_m_in"}
+    for inp, gname in names.items():
+        np.testing.assert_allclose(g[gname][0, 0], tx[inp].grad.numpy(), rtol=1e-9, atol=1e-11,
+                                   err_msg=inp)
+
+
+def test_backward_without_gamma_or_state_grads(oracle):
+    # gamma = NULL means gamma = 1; missing d_w_out / d_m_out mean zero.
+    T, d, dh, C = 8, 4, 6, 4
+    x = rand_problem(T, d, dh, FW_MLP, 31)
+    dO = np.random.default_rng(1).standard_normal(x["q"].shape)
+    x1 = dict(x, gamma=None)
+    g1 = oracle.backward(**x1, d_out=dO, C=C, fw=FW_MLP, dh=dh)
+    x2 = dict(x, gamma=np.ones_like(x["eta"]))
+    g2 = oracle.backward(**x2, d_out=dO, C=C, fw=FW_MLP, dh=dh)
+    assert g1["d_gamma"] is None
+    for n in ("dq", "dk", "dv", "d_eta", "d_beta", "d_w_in", "d_m_in"):
+        np.testing.assert_array_equal(g1[n], g2[n])
