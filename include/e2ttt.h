@@ -1,0 +1,160 @@
+/*
+ * e2ttt.h -- C ABI of the MI355X (gfx950) E2-TTT chunk-parallel fast-weight update.
+ *
+ * Method: arxiv 2608.21308, "Rethinking Expressivity and Efficiency in
+ * Test-Time Training".  The library computes, for every (batch, head) unit
+ * independently, the chunk update of Algorithm 1:
+ *   - chunk-start outputs  o_t = f_{W_0}(q_t)                  (eq. (6))
+ *   - per-token gradients  G_t = -grad_W 1/2||f_{W_0}(k_t) - v_t||^2 at the
+ *     chunk-start weights (Sec. 3.1)
+ *   - the closed-form transition of Prop. 1 (eq. (10)-(11))
+ *       M_C = b~_0 M_0 + sum_t K^M_t G_t
+ *       W_C = g~_0 W_0 + b~_0 R_1 M_0 + sum_t K^W_t G_t
+ *     which equals the per-token recurrence M_t = beta_t M_{t-1} + eta_t G_t,
+ *     W_t = gamma_t W_{t-1} + M_t (eq. (7)) at every chunk end,
+ * and the state (W, M) is carried from chunk to chunk.  The fast-weight net f
+ * is the GELU MLP f(x) = x + LN(W2 GELU(W1 x)) or the SwiGLU net
+ * f(x) = x + LN(Wd (SiLU(Wg x) * (Wu x))) of Sec. 4 (LayerNorm without affine,
+ * biased variance, eps = ln_eps; GELU uses the exact erf form).
+ *
+ * Conventions shared by every entry point:
+ *   - Every tensor pointer is a DEVICE pointer (hipMalloc'd or equivalent) on
+ *     the current HIP device; all work is enqueued on `stream` (a hipStream_t,
+ *     NULL = the default stream) and the call returns without waiting.
+ *   - The caller owns every buffer; the library never allocates, frees or
+ *     keeps state between calls and is safe to call from several host threads
+ *     on distinct streams.
+ *   - Every argument check runs before anything is launched; on an error
+ *     return nothing has been written.  Errors raised by kernels while they
+ *     run surface on the stream as HIP errors.
+ *   - Results are bitwise reproducible run to run (no floating-point atomics).
+ *
+ * Tensor layouts (row-major, C order):
+ *   q, k, v, out, d_out, dq, dk, dv : [B][H][T][d]   element type desc.io
+ *   eta, beta, gamma, d_eta, ...    : [B][H][T]      float32
+ *   w_*, m_*, d_w_*, d_m_*          : [B][H][P]      float32, P parameters per unit
+ * Packing of the P fast-weight parameters of one unit (row-major, W x rule):
+ *   GELU MLP : W1[dh][d], then W2[d][dh]                       P = 2 d dh
+ *   SwiGLU   : Wg[dh][d], then Wu[dh][d], then Wd[d][dh]        P = 3 d dh
+ *   (Wg, Wu, Wd are the paper's W1, W2, W3 of the SwiGLU net.)
+ *
+ * Supported shapes: d in {16, 32, 64}; 1 <= dh with dh padded inside the
+ * library to a multiple of 16 (at most 256 for the MLP, 176 for SwiGLU at
+ * d = 64); 1 <= chunk <= 64; T >= 1 with a ragged last chunk of T mod chunk
+ * tokens allowed (Prop. 1 holds for any chunk length); io = F32 or BF16
+ * (bf16 tensors use MFMA bf16 operands with fp32 accumulation and fp32
+ * state; f32 tensors use fp32 MFMA throughout).  Anything else returns
+ * E2TTT_ERR_UNSUPPORTED.
+ */
+#ifndef E2TTT_H
+#define E2TTT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  E2TTT_OK = 0,
+  E2TTT_ERR_NULL_ARG = 1,              /* a required pointer is NULL             */
+  E2TTT_ERR_BAD_SHAPE = 2,             /* a size is <= 0 or inconsistent          */
+  E2TTT_ERR_UNSUPPORTED = 3,           /* valid but outside the supported set     */
+  E2TTT_ERR_WORKSPACE_TOO_SMALL = 4,   /* workspace / scratch smaller than needed */
+  E2TTT_ERR_HIP = 5                    /* a HIP launch failed                     */
+} e2ttt_status;
+
+typedef enum { E2TTT_FW_GELU_MLP = 0, E2TTT_FW_SWIGLU = 1 } e2ttt_fw;
+
+/* Element type of q, k, v, out, d_out, dq, dk, dv. */
+typedef enum { E2TTT_DT_F32 = 0, E2TTT_DT_BF16 = 1 } e2ttt_dtype;
+
+/* f(x) = y (the bare matrix net) instead of f(x) = x + LN(y). */
+#define E2TTT_FLAG_NO_RESIDUAL_LN 0x1u
+
+typedef struct {
+  int32_t B, H, T;      /* batch, heads, tokens                        */
+  int32_t d, dh;        /* head dim, fast-weight hidden width          */
+  int32_t chunk;        /* chunk length C                              */
+  int32_t fw;           /* e2ttt_fw                                    */
+  int32_t io;           /* e2ttt_dtype                                 */
+  uint32_t flags;       /* E2TTT_FLAG_*                                */
+  float ln_eps;         /* LayerNorm epsilon (> 0 unless NO_RESIDUAL_LN) */
+} e2ttt_desc;
+
+/* Parameters per unit (P above), or 0 for a bad descriptor. */
+size_t e2ttt_param_count(const e2ttt_desc* desc);
+
+/* Bytes of `workspace` that e2ttt_chunk_forward needs.  With
+ * save_for_backward != 0 the workspace also keeps what the backward reuses
+ * (per-token scalar kernels and bf16 chunk-start checkpoints of W and M), and
+ * the same buffer, untouched, must then be passed to e2ttt_chunk_backward.
+ * Returns 0 for a bad descriptor. */
+size_t e2ttt_workspace_bytes(const e2ttt_desc* desc, int save_for_backward);
+
+/* Bytes of `scratch` that e2ttt_chunk_backward needs (0 for a bad descriptor). */
+size_t e2ttt_backward_scratch_bytes(const e2ttt_desc* desc);
+
+/*
+ * Forward: Algorithm 1 over every chunk of every unit.
+ *   q, k, v   [B][H][T][d] io     queries, keys, values (k, v feed the inner
+ *                                 loss, q the outputs)
+ *   eta, beta [B][H][T]   f32     learning rate and momentum gates, eq. (7)
+ *   gamma     [B][H][T]   f32     decay gate; NULL means gamma = 1
+ *   w_in      [B][H][P]   f32     initial fast weights W (chunk-start state of chunk 0)
+ *   m_in      [B][H][P]   f32     initial momentum M; NULL means zero
+ *   out       [B][H][T][d] io     o_t = f_{W_0}(q_t) with W_0 the start state of t's chunk
+ *   w_out, m_out [B][H][P] f32    state after the last token
+ *   workspace, workspace_bytes    caller-owned device memory, at least
+ *                                 e2ttt_workspace_bytes(desc, save_for_backward)
+ * w_out / m_out may alias w_in / m_in only when save_for_backward == 0.
+ */
+e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const void* k,
+                                 const void* v, const float* eta, const float* beta,
+                                 const float* gamma, const float* w_in, const float* m_in,
+                                 void* out, float* w_out, float* m_out, void* workspace,
+                                 size_t workspace_bytes, int save_for_backward, void* stream);
+
+/*
+ * Backward of  sum_t <d_out_t, o_t> + <d_w_out, W_T> + <d_m_out, M_T>
+ * with respect to every input of the forward (reverse mode through the chunk
+ * chain; the paper trains with autograd through the same computation).
+ *   q .. m_in         the forward's inputs, unchanged
+ *   workspace         as left by e2ttt_chunk_forward(..., save_for_backward = 1)
+ *   d_out             [B][H][T][d] io   gradient of the outputs
+ *   d_w_out, d_m_out  [B][H][P] f32     gradient of the final state; NULL = zero
+ *   dq, dk, dv        [B][H][T][d] io
+ *   d_eta, d_beta     [B][H][T] f32
+ *   d_gamma           [B][H][T] f32; must be NULL iff gamma is NULL
+ *   d_w_in, d_m_in    [B][H][P] f32     gradient of the initial state
+ *   scratch           at least e2ttt_backward_scratch_bytes(desc) bytes
+ */
+e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const void* k,
+                                  const void* v, const float* eta, const float* beta,
+                                  const float* gamma, const float* w_in, const float* m_in,
+                                  const void* workspace, size_t workspace_bytes,
+                                  const void* d_out, const float* d_w_out, const float* d_m_out,
+                                  void* dq, void* dk, void* dv, float* d_eta, float* d_beta,
+                                  float* d_gamma, float* d_w_in, float* d_m_in, void* scratch,
+                                  size_t scratch_bytes, void* stream);
+
+/*
+ * Scalar kernels of every chunk (Prop. 1, eq. (9)-(11)), exposed on their own
+ * so that callers (and tests) can inspect them:
+ *   kw, km      [B][H][T] f32   K^W_t = eta_t b~_t R_t and K^M_t = eta_t b~_t
+ *   carry       [B][H][NC][3] f32, NC = ceil(T / chunk): (g~_0, b~_0 R_1, b~_0)
+ * gamma NULL means gamma = 1.
+ */
+e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const float* beta,
+                                const float* gamma, float* kw, float* km, float* carry,
+                                void* stream);
+
+/* Static description of a status code. */
+const char* e2ttt_status_str(e2ttt_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* E2TTT_H */

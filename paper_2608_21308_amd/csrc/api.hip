@@ -1,0 +1,230 @@
+// Host side of the C ABI declared in include/e2ttt.h: argument validation,
+// workspace planning and kernel dispatch.  Nothing here allocates memory.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdlib>
+
+#include "e2ttt.h"
+#include "e2ttt_internal.h"
+
+namespace {
+
+using namespace e2ttt;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Plan {
+  long U = 0, T = 0, NC = 0, P = 0;
+  ChainConfig cfg{};
+  // forward workspace
+  size_t off_kw = 0, off_km = 0, off_carry = 0, off_ckpt = 0, ws_bytes = 0, ws_bytes_save = 0;
+  long ckpt_stride = 0;
+  // backward scratch
+  size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, scratch_bytes = 0;
+};
+
+e2ttt_status select_config(const e2ttt_desc& d, ChainConfig& cfg) {
+  cfg.fw = d.fw;
+  cfg.d = d.d;
+  cfg.bf = (d.io == E2TTT_DT_BF16) ? 1 : 0;
+  const int nblk = (d.dh + 15) / 16;
+  if (cfg.bf) {
+    if (d.d != 64) return E2TTT_ERR_UNSUPPORTED;
+    cfg.ntb = 4;
+    if (nblk <= 4) { cfg.nw = 4; cfg.njb = 1; }
+    else if (nblk <= 8) { cfg.nw = 8; cfg.njb = 1; }
+    else if (d.fw == E2TTT_FW_GELU_MLP && nblk <= 16) { cfg.nw = 8; cfg.njb = 2; }
+    else if (d.fw == E2TTT_FW_SWIGLU && nblk <= 11) { cfg.nw = 11; cfg.njb = 1; }
+    else return E2TTT_ERR_UNSUPPORTED;
+  } else {
+    if (d.d != 16) return E2TTT_ERR_UNSUPPORTED;
+    cfg.ntb = (d.chunk <= 16) ? 1 : 4;
+    if (nblk <= 4) { cfg.nw = 4; cfg.njb = 1; }
+    else if (nblk <= 8) { cfg.nw = 8; cfg.njb = 1; }
+    else return E2TTT_ERR_UNSUPPORTED;
+  }
+  return E2TTT_OK;
+}
+
+e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
+  if (!desc) return E2TTT_ERR_NULL_ARG;
+  const e2ttt_desc& d = *desc;
+  if (d.B < 1 || d.H < 1 || d.T < 1 || d.d < 1 || d.dh < 1 || d.chunk < 1)
+    return E2TTT_ERR_BAD_SHAPE;
+  if (d.fw != E2TTT_FW_GELU_MLP && d.fw != E2TTT_FW_SWIGLU) return E2TTT_ERR_UNSUPPORTED;
+  if (d.io != E2TTT_DT_F32 && d.io != E2TTT_DT_BF16) return E2TTT_ERR_UNSUPPORTED;
+  if (d.flags & ~E2TTT_FLAG_NO_RESIDUAL_LN) return E2TTT_ERR_UNSUPPORTED;
+  if (!(d.flags & E2TTT_FLAG_NO_RESIDUAL_LN) && !(d.ln_eps > 0.0f)) return E2TTT_ERR_BAD_SHAPE;
+  if (d.chunk > 64) return E2TTT_ERR_UNSUPPORTED;
+  const long U = (long)d.B * d.H;
+  if (U > INT_MAX || (long)d.T * d.d > (1L << 40) / U) return E2TTT_ERR_UNSUPPORTED;
+  e2ttt_status st = select_config(d, pl.cfg);
+  if (st != E2TTT_OK) return st;
+  pl.U = U;
+  pl.T = d.T;
+  pl.NC = (d.T + d.chunk - 1) / d.chunk;
+  pl.P = (d.fw == E2TTT_FW_GELU_MLP ? 2L : 3L) * d.d * d.dh;
+  const size_t tok = (size_t)U * d.T * sizeof(float);
+  const size_t chk = (size_t)U * pl.NC * 3 * sizeof(float);
+  pl.off_kw = 0;
+  pl.off_km = align_up(tok);
+  pl.off_carry = pl.off_km + align_up(tok);
+  pl.off_ckpt = pl.off_carry + align_up(chk);
+  pl.ws_bytes = pl.off_ckpt;
+  pl.ckpt_stride = chain_ckpt_elems(pl.cfg);
+  pl.ws_bytes_save = pl.off_ckpt + align_up((size_t)U * pl.NC * 2 * pl.ckpt_stride * sizeof(uint16_t));
+  pl.off_kwb = 0;
+  pl.off_kmb = align_up(tok);
+  pl.off_carryb = pl.off_kmb + align_up(tok);
+  pl.scratch_bytes = pl.off_carryb + align_up(chk);
+  return E2TTT_OK;
+}
+
+e2ttt_status hip_status(hipError_t e) { return e == hipSuccess ? E2TTT_OK : E2TTT_ERR_HIP; }
+
+bool debug_sync() {
+  static const bool on = [] {
+    const char* s = std::getenv("E2TTT_DEBUG_SYNC");
+    return s && s[0] == '1';
+  }();
+  return on;
+}
+
+e2ttt_status finish(hipError_t e, hipStream_t s) {
+  if (e != hipSuccess) return E2TTT_ERR_HIP;
+  if (debug_sync() && hipStreamSynchronize(s) != hipSuccess) return E2TTT_ERR_HIP;
+  return E2TTT_OK;
+}
+
+template <class Tp> Tp* at(void* base, size_t off) {
+  return reinterpret_cast<Tp*>(static_cast<char*>(base) + off);
+}
+template <class Tp> const Tp* at(const void* base, size_t off) {
+  return reinterpret_cast<const Tp*>(static_cast<const char*>(base) + off);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t e2ttt_param_count(const e2ttt_desc* desc) {
+  Plan pl;
+  return make_plan(desc, pl) == E2TTT_OK ? (size_t)pl.P : 0;
+}
+
+size_t e2ttt_workspace_bytes(const e2ttt_desc* desc, int save_for_backward) {
+  Plan pl;
+  if (make_plan(desc, pl) != E2TTT_OK) return 0;
+  return save_for_backward ? pl.ws_bytes_save : pl.ws_bytes;
+}
+
+size_t e2ttt_backward_scratch_bytes(const e2ttt_desc* desc) {
+  Plan pl;
+  return make_plan(desc, pl) == E2TTT_OK ? pl.scratch_bytes : 0;
+}
+
+const char* e2ttt_status_str(e2ttt_status s) {
+  switch (s) {
+    case E2TTT_OK: return "ok";
+    case E2TTT_ERR_NULL_ARG: return "a required pointer is NULL";
+    case E2TTT_ERR_BAD_SHAPE: return "a size is not positive or the arguments are inconsistent";
+    case E2TTT_ERR_UNSUPPORTED: return "shape, dtype or flags outside the supported set";
+    case E2TTT_ERR_WORKSPACE_TOO_SMALL: return "workspace or scratch buffer too small";
+    case E2TTT_ERR_HIP: return "a HIP launch failed";
+  }
+  return "unknown status";
+}
+
+e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const float* beta,
+                                const float* gamma, float* kw, float* km, float* carry,
+                                void* stream) {
+  Plan pl;
+  e2ttt_status st = make_plan(desc, pl);
+  if (st != E2TTT_OK) return st;
+  if (!eta || !beta || !kw || !km || !carry) return E2TTT_ERR_NULL_ARG;
+  CoeffFwdArgs c{eta, beta, gamma, kw, km, carry, (int)pl.T, desc->chunk, (int)pl.NC,
+                 pl.U * pl.NC};
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return finish(launch_coeff_fwd(c, s), s);
+}
+
+e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const void* k,
+                                 const void* v, const float* eta, const float* beta,
+                                 const float* gamma, const float* w_in, const float* m_in,
+                                 void* out, float* w_out, float* m_out, void* workspace,
+                                 size_t workspace_bytes, int save_for_backward, void* stream) {
+  Plan pl;
+  e2ttt_status st = make_plan(desc, pl);
+  if (st != E2TTT_OK) return st;
+  if (!q || !k || !v || !eta || !beta || !w_in || !out || !w_out || !m_out || !workspace)
+    return E2TTT_ERR_NULL_ARG;
+  if (workspace_bytes < (save_for_backward ? pl.ws_bytes_save : pl.ws_bytes))
+    return E2TTT_ERR_WORKSPACE_TOO_SMALL;
+  if (save_for_backward && (w_out == w_in || (m_in && m_out == m_in))) return E2TTT_ERR_BAD_SHAPE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float* kw = at<float>(workspace, pl.off_kw);
+  float* km = at<float>(workspace, pl.off_km);
+  float* carry = at<float>(workspace, pl.off_carry);
+  CoeffFwdArgs c{eta, beta, gamma, kw, km, carry, (int)pl.T, desc->chunk, (int)pl.NC,
+                 pl.U * pl.NC};
+  hipError_t e = launch_coeff_fwd(c, s);
+  if (e != hipSuccess) return E2TTT_ERR_HIP;
+  ChainArgs a{};
+  a.q = q; a.k = k; a.v = v;
+  a.w_in = w_in; a.m_in = m_in;
+  a.kw = kw; a.km = km; a.carry = carry;
+  a.out = out; a.w_out = w_out; a.m_out = m_out;
+  a.ckpt = save_for_backward ? at<uint16_t>(workspace, pl.off_ckpt) : nullptr;
+  a.ckpt_stride = pl.ckpt_stride;
+  a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
+  a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
+  a.eps = desc->ln_eps;
+  return finish(launch_chain_fwd(pl.cfg, a, pl.U, s), s);
+}
+
+e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const void* k,
+                                  const void* v, const float* eta, const float* beta,
+                                  const float* gamma, const float* w_in, const float* m_in,
+                                  const void* workspace, size_t workspace_bytes,
+                                  const void* d_out, const float* d_w_out, const float* d_m_out,
+                                  void* dq, void* dk, void* dv, float* d_eta, float* d_beta,
+                                  float* d_gamma, float* d_w_in, float* d_m_in, void* scratch,
+                                  size_t scratch_bytes, void* stream) {
+  Plan pl;
+  e2ttt_status st = make_plan(desc, pl);
+  if (st != E2TTT_OK) return st;
+  if (!q || !k || !v || !eta || !beta || !w_in || !workspace || !d_out || !dq || !dk || !dv ||
+      !d_eta || !d_beta || !d_w_in || !d_m_in || !scratch)
+    return E2TTT_ERR_NULL_ARG;
+  if ((gamma == nullptr) != (d_gamma == nullptr)) return E2TTT_ERR_BAD_SHAPE;
+  if (workspace_bytes < pl.ws_bytes_save || scratch_bytes < pl.scratch_bytes)
+    return E2TTT_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ChainArgs a{};
+  a.q = q; a.k = k; a.v = v;
+  a.w_in = w_in; a.m_in = m_in;
+  a.kw = at<float>(workspace, pl.off_kw);
+  a.km = at<float>(workspace, pl.off_km);
+  a.carry = at<float>(workspace, pl.off_carry);
+  a.ckpt = const_cast<uint16_t*>(at<uint16_t>(workspace, pl.off_ckpt));
+  a.ckpt_stride = pl.ckpt_stride;
+  a.d_out = d_out; a.d_w_out = d_w_out; a.d_m_out = d_m_out;
+  a.dq = dq; a.dk = dk; a.dv = dv;
+  a.d_w_in = d_w_in; a.d_m_in = d_m_in;
+  a.kwb = at<float>(scratch, pl.off_kwb);
+  a.kmb = at<float>(scratch, pl.off_kmb);
+  a.carryb = at<float>(scratch, pl.off_carryb);
+  a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
+  a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
+  a.eps = desc->ln_eps;
+  hipError_t e = launch_chain_bwd(pl.cfg, a, pl.U, s);
+  if (e != hipSuccess) return E2TTT_ERR_HIP;
+  CoeffBwdArgs cb{eta, beta, gamma, a.kwb, a.kmb, a.carryb, d_eta, d_beta, d_gamma,
+                  (int)pl.T, desc->chunk, (int)pl.NC, pl.U * pl.NC};
+  return finish(launch_coeff_bwd(cb, s), s);
+}
+
+}  // extern "C"

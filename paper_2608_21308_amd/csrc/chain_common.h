@@ -1,0 +1,206 @@
+// Shape constants and register-resident state handling shared by the forward
+// and backward chain kernels.
+//
+// One workgroup owns one (batch, head) unit for the whole sequence.  Its NW
+// waves split the fast-weight hidden dimension: wave w owns the hidden columns
+// j in [16 w NJB, 16 (w+1) NJB).  Every fast-weight matrix is held as 16x16
+// MFMA accumulator tiles with the head index i as the tile ROW and the hidden
+// index j as the tile COLUMN:
+//   first-layer matrices (MLP W1, SwiGLU Wg and Wu, stored [dh][d]) as W^T,
+//   the second-layer matrix (MLP W2, SwiGLU Wd, stored [d][dh]) as W.
+// With that orientation every update sum_t c_t delta_t x_t^T of Prop. 1 is an
+// MFMA whose accumulator IS the state tile, and every contraction over i of a
+// token tile with a state matrix takes the state tile directly as operand.
+#pragma once
+
+#include "e2ttt_device.h"
+#include "e2ttt_internal.h"
+
+namespace e2ttt {
+
+template <int FW_, int D_, int NW_, int NJB_, int NTB_, bool BF_>
+struct Shape {
+  static constexpr int FW = FW_;
+  static constexpr int D = D_;
+  static constexpr int NW = NW_;
+  static constexpr int NJB = NJB_;
+  static constexpr int NTB = NTB_;
+  static constexpr bool BF = BF_;
+  using O = OpT<BF>;
+  using E = typename O::E;
+  static constexpr int KC = O::KC;
+  static constexpr int NH = O::NH;
+  static constexpr int NIB = D / 16;          // 16-row blocks over the head dim
+  static constexpr int CM = 16 * NTB;         // token rows per chunk tile
+  static constexpr int DHP = 16 * NW * NJB;   // padded hidden width
+  static constexpr int DHK = ((DHP + KC - 1) / KC) * KC;  // hidden extent of LDS operands
+  static constexpr int NMAT = (FW == 0) ? 2 : 3;
+  static constexpr int NT = NW * 64;
+  static constexpr int LDD = D + O::PAD;      // [t][i] operands
+  static constexpr int LDC = CM + O::PAD;     // [i][t] operands
+  static constexpr int LDH = DHK + O::PAD;    // [t][j] and [i][j] operands
+  static constexpr int KS_D = D / KC;         // K-steps over i
+  static constexpr int KS_C = CM / KC;        // K-steps over t
+  static constexpr int KS_H = DHK / KC;       // K-steps over j
+  static constexpr int IBB = (NIB >= 2) ? 2 : 1;  // head blocks per wave item in j-contractions
+  static constexpr int CKPT = NMAT * DHP * D; // checkpoint elements per state
+  static_assert(D % KC == 0, "head dim must be a multiple of the K-step");
+  static_assert(CM % KC == 0, "chunk tile must be a multiple of the K-step");
+};
+
+// State tiles of one wave: T[m][jj][ib] is the tile (rows i = 16 ib + 4 g + r,
+// column j = 16 (w NJB + jj) + c) of matrix m.
+template <class S>
+struct StateTiles {
+  f32x4 t[S::NMAT][S::NJB][S::NIB];
+};
+
+// Marks every state tile as possibly modified, so that conversions of the
+// tiles made before this point are not reused (and kept live) after it.
+template <class S>
+__device__ __forceinline__ void opaque_state(StateTiles<S>& st) {
+#pragma unroll
+  for (int m = 0; m < S::NMAT; ++m)
+#pragma unroll
+    for (int jj = 0; jj < S::NJB; ++jj)
+#pragma unroll
+      for (int ib = 0; ib < S::NIB; ++ib) asm volatile("" : "+v"(st.t[m][jj][ib]));
+}
+
+// Element (i, j) of matrix m of one unit's P parameters lives at
+//   first layer  [dh][d]: m dh d + j d + i
+//   second layer [d][dh]: (NMAT-1) dh d + i dh + j.
+// The per-lane part of the offset is formed once and kept opaque so that the
+// compiler does not materialise one 64-bit address per element.
+template <class S, bool STORE>
+__device__ __forceinline__ void state_io(StateTiles<S>& st, const float* src, float* dst,
+                                         int dh, int w, int g, int c) {
+  constexpr int D = S::D;
+  const int jl = 16 * w * S::NJB + c;                      // this lane's first hidden column
+  const int l1 = opaque_lane(jl * D + 4 * g);              // first-layer lane offset
+  const int l2 = opaque_lane(4 * g * dh + jl);             // second-layer lane offset
+#pragma unroll
+  for (int m = 0; m < S::NMAT; ++m)
+#pragma unroll
+    for (int jj = 0; jj < S::NJB; ++jj) {
+      const bool ok = (jl + 16 * jj) < dh;
+#pragma unroll
+      for (int ib = 0; ib < S::NIB; ++ib) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          long off;
+          if (m < S::NMAT - 1) off = (long)m * dh * D + l1 + jj * 16 * D + 16 * ib + r;
+          else off = (long)(S::NMAT - 1) * dh * D + l2 + (long)(16 * ib + r) * dh + 16 * jj;
+          if constexpr (STORE) {
+            if (ok) dst[off] = st.t[m][jj][ib][r];
+          } else {
+            st.t[m][jj][ib][r] = (ok && src) ? src[off] : 0.0f;
+          }
+        }
+      }
+    }
+}
+
+template <class S>
+__device__ __forceinline__ void load_state(StateTiles<S>& st, const float* src, int dh, int w,
+                                           int g, int c) {
+  state_io<S, false>(st, src, nullptr, dh, w, g, c);
+}
+
+template <class S>
+__device__ __forceinline__ void store_state(StateTiles<S>& st, float* dst, int dh, int w, int g,
+                                            int c) {
+  state_io<S, true>(st, nullptr, dst, dh, w, g, c);
+}
+
+// Checkpoint blocks hold bf16 state in register order: element
+// ((((m NJB + jj) NIB + ib) NW + w) 64 + lane) 4 + r, so that writes and reads
+// are 8-byte per lane and fully coalesced.
+template <class S>
+__device__ __forceinline__ void store_ckpt(const StateTiles<S>& st, uint16_t* dst, int w,
+                                           int lane) {
+  bf16x4* lp = reinterpret_cast<bf16x4*>(dst) + opaque_lane(w * 64 + lane);
+#pragma unroll
+  for (int m = 0; m < S::NMAT; ++m)
+#pragma unroll
+    for (int jj = 0; jj < S::NJB; ++jj)
+#pragma unroll
+      for (int ib = 0; ib < S::NIB; ++ib)
+        lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64] = OpT<true>::cvt(st.t[m][jj][ib]);
+}
+
+template <class S>
+__device__ __forceinline__ void load_ckpt(StateTiles<S>& st, const uint16_t* src, int w,
+                                          int lane) {
+  const bf16x4* lp = reinterpret_cast<const bf16x4*>(src) + opaque_lane(w * 64 + lane);
+#pragma unroll
+  for (int m = 0; m < S::NMAT; ++m)
+#pragma unroll
+    for (int jj = 0; jj < S::NJB; ++jj)
+#pragma unroll
+      for (int ib = 0; ib < S::NIB; ++ib) {
+        const bf16x4 b = lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64];
+        st.t[m][jj][ib] = f32x4{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
+      }
+}
+
+// Operand fragment whose contraction index is the tile ROW of `tiles`
+// (tiles[k-block]) for K-step p.
+template <class S>
+__device__ __forceinline__ typename S::O::Frag tile_frag(const f32x4* tiles, int p,
+                                                         int stride) {
+  typename S::O::Frag f;
+#pragma unroll
+  for (int h = 0; h < S::NH; ++h) f.h[h] = S::O::cvt(tiles[(S::NH * p + h) * stride]);
+  return f;
+}
+
+// Copy a CM x D token tile (rows < len, zero beyond) from global io memory to
+// LDS in 16-byte vectors (the io element type equals the LDS element type).
+template <class S>
+__device__ __forceinline__ void stage_tile(typename S::E* dst, const void* src, long row0,
+                                           int len, int tid) {
+  using IOT = typename IoT<S::BF>::T;
+  static_assert(sizeof(IOT) == sizeof(typename S::E), "io and operand types differ");
+  constexpr int VE = 16 / sizeof(IOT);
+  constexpr int NV = S::CM * S::D / VE;
+  const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const IOT*>(src) + row0 * S::D);
+#pragma unroll 1
+  for (int v = tid; v < NV; v += S::NT) {
+    const int e = v * VE, t = e / S::D, i = e % S::D;
+    uint4 x = make_uint4(0u, 0u, 0u, 0u);
+    if (t < len) x = p[v];
+    *reinterpret_cast<uint4*>(dst + t * S::LDD + i) = x;
+  }
+}
+
+// Y[t][i] = sum_j A[t][j] Wt[i][j]  (j-contraction, both operands in LDS),
+// written to y (fp32 [CM][D]).  Work is split into (token block, head block
+// pair) items over the waves.
+template <class S>
+__device__ __forceinline__ void jgemm_to_lds(const typename S::E* A, const typename S::E* Wt,
+                                             float* y, int w, int g, int c) {
+  constexpr int NI = S::NIB / S::IBB;
+  for (int it = w; it < S::NTB * NI; it += S::NW) {
+    const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+    f32x4 acc[S::IBB];
+#pragma unroll
+    for (int b = 0; b < S::IBB; ++b) acc[b] = zero4();
+#pragma unroll 2
+    for (int p = 0; p < S::KS_H; ++p) {
+      auto af = lds_frag<S::BF>(A, S::LDH, 16 * tb + c, p * S::KC, g);
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b) {
+        auto bf = lds_frag<S::BF>(Wt, S::LDH, 16 * (ib0 + b) + c, p * S::KC, g);
+        acc[b] = S::O::mma(acc[b], af, bf);
+      }
+      sched_fence();
+    }
+#pragma unroll
+    for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[(16 * tb + 4 * g + r) * S::D + 16 * (ib0 + b) + c] = acc[b][r];
+  }
+}
+
+}  // namespace e2ttt

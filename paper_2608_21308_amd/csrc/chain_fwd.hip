@@ -1,0 +1,325 @@
+// Forward chain kernel: Algorithm 1 of the paper over every chunk of a unit.
+//
+// Per chunk (tokens t < len, the state (W_0, M_0) in registers):
+//   H  = K W1^T              contraction over i, state tiles as operand   (a3)
+//   A  = act(H)               GELU, or SiLU(Hg) * Hu for SwiGLU
+//   Y  = A W2^T               contraction over j, A and W2 staged in LDS
+//   Z  = LN(Y), E = V - K - Z, dY = LN backward of E            (a4, the g_t)
+//   dA = dY W2,  dH = dA * act'(H)                                          (a4)
+//   W  <- cw W + cm M + sum_t K^W_t G_t,   M <- cb M + sum_t K^M_t G_t      (a5, a6)
+//        with sum_t K_t G_t = (dY^T diag(K) A, dH^T diag(K) K): MFMAs that
+//        accumulate straight into the state tiles
+//   O  = Q + LN(act(Q W1^T) W2^T)     outputs from the chunk-start weights (a7)
+// The new state stays in registers for the next chunk (a8).
+#include "chain_common.h"
+
+namespace e2ttt {
+
+namespace {
+
+template <class S>
+struct FwdSmem {
+  using E = typename S::E;
+  alignas(16) E xk[S::CM * S::LDD];
+  alignas(16) E xq[S::CM * S::LDD];
+  alignas(16) E xv[S::CM * S::LDD];
+  alignas(16) E kwt[S::D * S::LDC];   // K^W_t k_t[i], layout [i][t]
+  alignas(16) E kmt[S::D * S::LDC];   // K^M_t k_t[i]
+  alignas(16) E alds[S::CM * S::LDH]; // activations A[t][j]
+  alignas(16) E w2[S::D * S::LDH];    // second-layer weights W2[i][j] (bf16/fp32 copy of W_0)
+  alignas(16) E dy[S::CM * S::LDD];   // dY[t][i]
+  alignas(16) E dytw[S::D * S::LDC];  // K^W_t dY[t][i], layout [i][t]
+  alignas(16) E dytm[S::D * S::LDC];  // K^M_t dY[t][i]
+  alignas(16) float y[S::CM * S::D];
+  float kw[S::CM];
+  float km[S::CM];
+  float carry[4];
+};
+
+template <class S>
+__global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
+  using O = typename S::O;
+  using E = typename S::E;
+  using IO = IoT<S::BF>;
+  constexpr int D = S::D, NJB = S::NJB, NTB = S::NTB, NIB = S::NIB, NMAT = S::NMAT;
+  constexpr int SEC = NMAT - 1;  // index of the second-layer matrix
+  __shared__ FwdSmem<S> sm;
+  static_assert(sizeof(FwdSmem<S>) <= 160 * 1024, "LDS budget");
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, c = lane & 15;
+  const long u = blockIdx.x;
+  const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
+  const float inv_d = 1.0f / D;
+
+  StateTiles<S> W, M;
+  load_state<S>(W, a.w_in + u * a.P, dh, w, g, c);
+  load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, w, g, c);
+
+  // hidden columns [DHP, DHK) of the j-operands stay zero for the whole run
+  if constexpr (S::DHK > S::DHP) {
+    constexpr int NZ = S::DHK - S::DHP;
+    for (int idx = tid; idx < S::CM * NZ; idx += S::NT)
+      sm.alds[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
+    for (int idx = tid; idx < D * NZ; idx += S::NT)
+      sm.w2[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
+  }
+
+  for (int r = 0; r < NC; ++r) {
+    const int s0 = r * C;
+    const int len = min(C, T - s0);
+    const long row0 = u * T + s0;
+    // ---------------------------------------------------------- stage (a1)
+    stage_tile<S>(sm.xk, a.k, row0, len, tid);
+    stage_tile<S>(sm.xq, a.q, row0, len, tid);
+    stage_tile<S>(sm.xv, a.v, row0, len, tid);
+#pragma unroll 1
+    for (int t = tid; t < S::CM; t += S::NT) {
+      sm.kw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
+      sm.km[t] = (t < len) ? a.km[row0 + t] : 0.0f;
+    }
+    if (tid < 3) sm.carry[tid] = a.carry[(u * NC + r) * 3 + tid];
+    if (a.ckpt) {
+      uint16_t* cb = a.ckpt + (u * NC + r) * 2 * a.ckpt_stride;
+      store_ckpt<S>(W, cb, w, lane);
+      store_ckpt<S>(M, cb + a.ckpt_stride, w, lane);
+    }
+    // second-layer weights of W_0 into LDS as the j-contraction operand
+#pragma unroll
+    for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          sm.w2[(16 * ib + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] =
+              O::to_e(W.t[SEC][jj][ib][rr]);
+    opaque_state<S>(W);
+    opaque_state<S>(M);
+    __syncthreads();
+
+    // ------------------------------------------- K-side forward (a3)
+#pragma unroll 1
+    for (int idx = tid; idx < D * (S::CM / 4); idx += S::NT) {
+      const int i = idx % D, t0 = 4 * (idx / D);
+      typename O::Q qw, qm;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float kx = O::from_e(sm.xk[(t0 + q4) * S::LDD + i]);
+        qw[q4] = O::to_e(sm.kw[t0 + q4] * kx);
+        qm[q4] = O::to_e(sm.km[t0 + q4] * kx);
+      }
+      *reinterpret_cast<typename O::Q*>(&sm.kwt[i * S::LDC + t0]) = qw;
+      *reinterpret_cast<typename O::Q*>(&sm.kmt[i * S::LDC + t0]) = qm;
+    }
+    f32x4 H[NTB][NJB];                   // MLP: H;  SwiGLU: Hg
+    f32x4 Hu[NTB][(S::FW == 1) ? NJB : 1];
+    typename O::Q AK[NTB][NJB];          // act(H) as operand quads (rows t)
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+      for (int jj = 0; jj < NJB; ++jj) {
+        f32x4 acc = zero4(), accu = zero4();
+#pragma unroll
+        for (int p = 0; p < S::KS_D; ++p) {
+          auto af = lds_frag<S::BF>(sm.xk, S::LDD, 16 * tb + c, p * S::KC, g);
+          acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
+          if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
+        }
+        f32x4 act;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          if constexpr (S::FW == 0) act[rr] = gelu_f(acc[rr]);
+          else act[rr] = silu_f(acc[rr]) * accu[rr];
+        }
+        H[tb][jj] = acc;
+        if constexpr (S::FW == 1) Hu[tb][jj] = accu;
+        AK[tb][jj] = O::cvt(act);
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act[rr]);
+        sched_fence();
+      }
+    __syncthreads();
+
+    jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y = A W2^T
+    __syncthreads();
+
+    // ------------------------------- LN and activation gradients (a4)
+    const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
+    for (int t = w; t < S::CM; t += S::NW) {
+      const bool on = lane < D;
+      const float yv = on ? sm.y[t * D + lane] : 0.0f;
+      const float kx = on ? O::from_e(sm.xk[t * S::LDD + lane]) : 0.0f;
+      const float vx = on ? O::from_e(sm.xv[t * S::LDD + lane]) : 0.0f;
+      float dyv;
+      if (a.resln) {
+        const float mu = wave_sum(yv) * inv_d;
+        const float yc = on ? yv - mu : 0.0f;
+        const float var = wave_sum(yc * yc) * inv_d;
+        const float sig = sqrtf(var + a.eps);
+        const float z = yc / sig;
+        const float e = on ? vx - kx - z : 0.0f;
+        const float me = wave_sum(e) * inv_d;
+        const float mez = wave_sum(e * z) * inv_d;
+        dyv = (e - me - z * mez) / sig;
+      } else {
+        dyv = vx - yv;
+      }
+      if (on) {
+        sm.dy[t * S::LDD + lane] = O::to_e(dyv);
+        sm.dytw[lane * S::LDC + t] = O::to_e(sm.kw[t] * dyv);
+        sm.dytm[lane * S::LDC + t] = O::to_e(sm.km[t] * dyv);
+      }
+    }
+    __syncthreads();
+
+    // ----------------------------- Q-side first layer (a7), into alds
+    opaque_state<S>(W);
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+      for (int jj = 0; jj < NJB; ++jj) {
+        f32x4 acc = zero4(), accu = zero4();
+#pragma unroll
+        for (int p = 0; p < S::KS_D; ++p) {
+          auto af = lds_frag<S::BF>(sm.xq, S::LDD, 16 * tb + c, p * S::KC, g);
+          acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
+          if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
+        }
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          float act;
+          if constexpr (S::FW == 0) act = gelu_f(acc[rr]);
+          else act = silu_f(acc[rr]) * accu[rr];
+          sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act);
+        }
+        sched_fence();
+      }
+
+    // ---------------------------------- dA = dY W2, first-layer deltas (a4)
+    opaque_state<S>(W);
+    typename O::Q DH[NTB][NJB];                         // MLP dH / SwiGLU dHg
+    typename O::Q DU[NTB][(S::FW == 1) ? NJB : 1];      // SwiGLU dHu
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+      for (int jj = 0; jj < NJB; ++jj) {
+        f32x4 da = zero4();
+#pragma unroll
+        for (int p = 0; p < S::KS_D; ++p) {
+          auto af = lds_frag<S::BF>(sm.dy, S::LDD, 16 * tb + c, p * S::KC, g);
+          da = O::mma(da, af, tile_frag<S>(&W.t[SEC][jj][0], p, 1));
+        }
+        f32x4 dh1, dh2;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          if constexpr (S::FW == 0) {
+            dh1[rr] = da[rr] * gelu_d1(H[tb][jj][rr]);
+          } else {
+            const float hg = H[tb][jj][rr], hu = Hu[tb][jj][rr];
+            dh1[rr] = da[rr] * hu * silu_d1(hg);
+            dh2[rr] = da[rr] * silu_f(hg);
+          }
+        }
+        DH[tb][jj] = O::cvt(dh1);
+        if constexpr (S::FW == 1) DU[tb][jj] = O::cvt(dh2);
+        sched_fence();
+      }
+
+    // ------------------- closed-form transition (a5, a6): scale, then accumulate
+#pragma unroll
+    for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+      for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+          W.t[m][jj][ib] = cw * W.t[m][jj][ib] + cm * M.t[m][jj][ib];
+          M.t[m][jj][ib] = cbv * M.t[m][jj][ib];
+        }
+#pragma unroll
+    for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+        for (int p = 0; p < S::KS_C; ++p) {
+          typename O::Frag bA, bH, bU;
+#pragma unroll
+          for (int h = 0; h < S::NH; ++h) {
+            bA.h[h] = AK[S::NH * p + h][jj];
+            bH.h[h] = DH[S::NH * p + h][jj];
+            if constexpr (S::FW == 1) bU.h[h] = DU[S::NH * p + h][jj];
+          }
+          const int row = 16 * ib + c, k0 = p * S::KC;
+          // second layer: sum_t K_t dY[t][i] A[t][j]
+          W.t[SEC][jj][ib] = O::mma(W.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytw, S::LDC, row, k0, g), bA);
+          M.t[SEC][jj][ib] = O::mma(M.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytm, S::LDC, row, k0, g), bA);
+          // first layer(s): sum_t K_t k[t][i] dH[t][j]
+          auto kfw = lds_frag<S::BF>(sm.kwt, S::LDC, row, k0, g);
+          auto kfm = lds_frag<S::BF>(sm.kmt, S::LDC, row, k0, g);
+          W.t[0][jj][ib] = O::mma(W.t[0][jj][ib], kfw, bH);
+          M.t[0][jj][ib] = O::mma(M.t[0][jj][ib], kfm, bH);
+          if constexpr (S::FW == 1) {
+            W.t[1][jj][ib] = O::mma(W.t[1][jj][ib], kfw, bU);
+            M.t[1][jj][ib] = O::mma(M.t[1][jj][ib], kfm, bU);
+          }
+          sched_fence();
+        }
+    __syncthreads();
+
+    jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y_Q = A_Q W2^T
+    __syncthreads();
+
+    // ------------------------------------------------- outputs (a7)
+    {
+      using IOT = typename IO::T;
+      IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
+      for (int t = w; t < len; t += S::NW) {
+        const bool on = lane < D;
+        const float yv = on ? sm.y[t * D + lane] : 0.0f;
+        float f;
+        if (a.resln) {
+          const float qx = on ? O::from_e(sm.xq[t * S::LDD + lane]) : 0.0f;
+          const float mu = wave_sum(yv) * inv_d;
+          const float yc = on ? yv - mu : 0.0f;
+          const float var = wave_sum(yc * yc) * inv_d;
+          f = qx + yc / sqrtf(var + a.eps);
+        } else {
+          f = yv;
+        }
+        if (on) IO::st(outp + (long)t * D + lane, f);
+      }
+    }
+    __syncthreads();
+  }
+
+  store_state<S>(W, a.w_out + u * a.P, dh, w, g, c);
+  store_state<S>(M, a.m_out + u * a.P, dh, w, g, c);
+}
+
+template <class S>
+hipError_t launch(const ChainArgs& a, long units, hipStream_t stream) {
+  hipLaunchKernelGGL(chain_fwd_kernel<S>, dim3((unsigned)units), dim3(S::NT), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF)                                              \
+  if (cfg.fw == FW && cfg.d == D && cfg.nw == NW && cfg.njb == NJB && cfg.ntb == NTB && \
+      cfg.bf == BF)                                                                     \
+    return launch<Shape<FW, D, NW, NJB, NTB, BF>>(a, units, stream);
+
+hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, long units,
+                            hipStream_t stream) {
+#include "chain_variants.inc"
+  return hipErrorInvalidValue;
+}
+#undef E2TTT_CASE
+
+}  // namespace e2ttt
+
+namespace e2ttt {
+long chain_ckpt_elems(const ChainConfig& cfg) {
+  const long nmat = (cfg.fw == 0) ? 2 : 3;
+  return nmat * 16L * cfg.nw * cfg.njb * cfg.d;
+}
+}  // namespace e2ttt

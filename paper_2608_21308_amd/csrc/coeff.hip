@@ -1,0 +1,163 @@
+// Scalar kernels of the E2-TTT chunk transition and their backward.
+//
+// Forward (Prop. 1, eq. (9)-(11)), per chunk of length L with 1-based token t:
+//   b~_t = prod_{i>t} beta_i,  g~_t = prod_{i>t} gamma_i   (suffix products)
+//   S_t  = b~_t R_t = sum_{i>=t} (prod_{t<j<=i} beta_j) g~_i
+//        satisfies S_L = 1, S_t = g~_t + beta_{t+1} S_{t+1}
+//   K^W_t = eta_t S_t,  K^M_t = eta_t b~_t
+//   carry = (g~_0, b~_0 R_1 = beta_1 S_1, b~_0)
+// The paper evaluates the suffix products in log space and forms R_t as a sum
+// of ratios g~_i / b~_i; here the products are formed by a multiplicative
+// wave scan (every factor lies in (0, 1], so nothing overflows, and underflow
+// to zero is the exact limit) and S_t by an affine wave scan, which never
+// divides and stays finite for beta -> 0 where the ratio form is 0/0.
+//
+// One wave64 handles one (unit, chunk); lane tau holds token t = tau + 1.
+#include <hip/hip_runtime.h>
+
+#include "e2ttt_internal.h"
+
+namespace e2ttt {
+
+namespace {
+
+struct ChunkScalars {
+  float e, b, gm;      // this lane's eta, beta, gamma (padding: 0, 1, 1)
+  float pb, pg;        // inclusive suffix products of beta, gamma
+  float bt, gt;        // exclusive suffix products (b~_t, g~_t)
+  float S;             // S_t
+};
+
+__device__ __forceinline__ ChunkScalars chunk_scalars(const float* eta, const float* beta,
+                                                      const float* gamma, long base, int len,
+                                                      int lane) {
+  ChunkScalars s;
+  const bool valid = lane < len;
+  s.e = valid ? eta[base + lane] : 0.0f;
+  s.b = valid ? beta[base + lane] : 1.0f;
+  s.gm = (valid && gamma) ? gamma[base + lane] : 1.0f;
+  float pb = s.b, pg = s.gm;
+#pragma unroll
+  for (int k = 1; k < 64; k <<= 1) {
+    float ob = __shfl_down(pb, k, 64);
+    float og = __shfl_down(pg, k, 64);
+    if (lane + k < 64) { pb *= ob; pg *= og; }
+  }
+  s.pb = pb;
+  s.pg = pg;
+  float bt = __shfl_down(pb, 1, 64), gt = __shfl_down(pg, 1, 64);
+  if (lane == 63) { bt = 1.0f; gt = 1.0f; }
+  s.bt = bt;
+  s.gt = gt;
+  // reverse affine scan S_t = A_t + B_t S_{t+1}
+  const float bnext = __shfl_down(s.b, 1, 64);
+  float A, B;
+  if (lane < len - 1) { A = gt; B = bnext; }
+  else if (lane == len - 1) { A = 1.0f; B = 0.0f; }
+  else { A = 0.0f; B = 0.0f; }
+#pragma unroll
+  for (int k = 1; k < 64; k <<= 1) {
+    float oA = __shfl_down(A, k, 64);
+    float oB = __shfl_down(B, k, 64);
+    if (lane + k < 64) { A = A + B * oA; B = B * oB; }
+  }
+  s.S = A;
+  return s;
+}
+
+// Ascending affine scan x_tau = a_tau + b_tau x_{tau-1} (b_0 is ignored).
+__device__ __forceinline__ float affine_scan_up(float a, float b, int lane) {
+  if (lane == 0) b = 0.0f;
+#pragma unroll
+  for (int k = 1; k < 64; k <<= 1) {
+    float oa = __shfl_up(a, k, 64);
+    float ob = __shfl_up(b, k, 64);
+    if (lane >= k) { a = a + b * oa; b = b * ob; }
+  }
+  return a;
+}
+
+__global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
+  const long wid = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (wid >= a.nwork) return;
+  const int lane = threadIdx.x & 63;
+  const long u = wid / a.NC;
+  const int r = (int)(wid % a.NC);
+  const int s0 = r * a.C;
+  const int len = min(a.C, a.T - s0);
+  const long base = u * a.T + s0;
+  ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);
+  if (lane < len) {
+    a.kw[base + lane] = s.e * s.S;
+    a.km[base + lane] = s.e * s.bt;
+  }
+  if (lane == 0) {
+    a.carry[wid * 3 + 0] = s.pg;
+    a.carry[wid * 3 + 1] = s.b * s.S;
+    a.carry[wid * 3 + 2] = s.pb;
+  }
+}
+
+// Backward of the map (eta, beta, gamma) -> (K^W, K^M, carry) given the
+// adjoints kwb, kmb (per token) and carryb (per chunk).  Reverse mode through
+// the same scans:  S-bar accumulates through an ascending affine scan, and the
+// suffix-product adjoints are pushed to the factors with ascending affine
+// scans as well (no division by beta or gamma).
+__global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
+  const long wid = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (wid >= a.nwork) return;
+  const int lane = threadIdx.x & 63;
+  const long u = wid / a.NC;
+  const int r = (int)(wid % a.NC);
+  const int s0 = r * a.C;
+  const int len = min(a.C, a.T - s0);
+  const long base = u * a.T + s0;
+  const bool valid = lane < len;
+  ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);
+  const float kwb = valid ? a.kwb[base + lane] : 0.0f;
+  const float kmb = valid ? a.kmb[base + lane] : 0.0f;
+  const float cwb = a.carryb[wid * 3 + 0];
+  const float cmb = a.carryb[wid * 3 + 1];
+  const float cbb = a.carryb[wid * 3 + 2];
+
+  const float etab = kwb * s.S + kmb * s.bt;
+  // S-bar and the direct beta_1 term of carry_m = beta_1 S_1
+  float Sb = kwb * s.e;
+  float betab = 0.0f;
+  if (lane == 0) { Sb += cmb * s.b; betab = cmb * s.S; }
+  // S^_tau = Sb_tau + beta_tau S^_{tau-1}
+  const float Sh = affine_scan_up(Sb, s.b, lane);
+  const float Sh_prev = __shfl_up(Sh, 1, 64);
+  if (lane >= 1) betab += Sh_prev * s.S;           // S_{t-1} = g~_{t-1} + beta_t S_t
+  // adjoints of the exclusive suffix products b~_{tau}, g~_{tau} (tau = 0..len-1)
+  const float kme_prev = __shfl_up(kmb * s.e, 1, 64);
+  const float btb = (lane == 0) ? cbb : kme_prev;
+  const float gtb = (lane == 0) ? cwb : Sh_prev;
+  const float b_prev = __shfl_up(s.b, 1, 64);
+  const float g_prev = __shfl_up(s.gm, 1, 64);
+  const float Y = affine_scan_up(btb, b_prev, lane);
+  const float Z = affine_scan_up(gtb, g_prev, lane);
+  betab += s.bt * Y;
+  const float gammab = s.gt * Z;
+  if (valid) {
+    a.d_eta[base + lane] = etab;
+    a.d_beta[base + lane] = betab;
+    if (a.d_gamma) a.d_gamma[base + lane] = gammab;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_coeff_fwd(const CoeffFwdArgs& a, hipStream_t stream) {
+  const unsigned blocks = (unsigned)((a.nwork + 3) / 4);
+  hipLaunchKernelGGL(coeff_fwd_kernel, dim3(blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_coeff_bwd(const CoeffBwdArgs& a, hipStream_t stream) {
+  const unsigned blocks = (unsigned)((a.nwork + 3) / 4);
+  hipLaunchKernelGGL(coeff_bwd_kernel, dim3(blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace e2ttt

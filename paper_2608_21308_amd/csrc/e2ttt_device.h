@@ -1,0 +1,148 @@
+// Device-side building blocks shared by the E2-TTT gfx950 kernels.
+//
+// MFMA tiles are 16x16.  The accumulator ("D") layout of a 16x16 tile is:
+// lane l = 16 g + c (g = l / 16, c = l % 16) holds rows 4 g + r (r = 0..3) of
+// column c.  A K-step of an MFMA takes, from every lane, a fragment of the
+// row (A operand) or column (B operand) numbered c, covering the contraction
+// indices {k0 + 16 h + 4 g + r}: h = 0..NH-1, r = 0..3.  The A and B operands
+// use the same (lane group, slot) -> k assignment, so the hardware sum over k
+// is unchanged; with this assignment a D tile whose ROW index is the
+// contraction index is directly usable (after conversion) as half of a bf16
+// fragment or as a whole fp32 fragment, without going through LDS.
+//
+//   bf16: v_mfma_f32_16x16x32_bf16, K-step 32 = two 16-row halves, 8 bf16/lane
+//   fp32: v_mfma_f32_16x16x4_f32 x 4, K-step 16, one float per lane per MFMA
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace e2ttt {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+// Keeps the instruction scheduler from moving work across this point; used
+// between fully unrolled iterations so that operand loads of later
+// iterations are not hoisted (which would raise register pressure).
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Returns p unchanged but opaque to the optimiser, so that addresses derived
+// from it are formed where they are used instead of being hoisted out of the
+// chunk loop and kept live in registers for its whole duration.
+template <class T>
+__device__ __forceinline__ T* opaque_ptr(T* p) {
+  asm volatile("" : "+s"(p));
+  return p;
+}
+// Same for a per-lane integer (kept in a VGPR).
+__device__ __forceinline__ int opaque_lane(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+template <bool BF> struct OpT;
+
+template <> struct OpT<true> {
+  using E = __bf16;                 // element type of LDS operands
+  using Q = bf16x4;                 // four consecutive contraction indices
+  static constexpr int KC = 32;     // contraction indices per K-step
+  static constexpr int NH = 2;      // quads per fragment
+  static constexpr int PAD = 8;     // row padding of LDS operands (16 bytes)
+  struct Frag { Q h[2]; };
+  static __device__ __forceinline__ Q cvt(f32x4 x) {
+    return Q{(__bf16)x[0], (__bf16)x[1], (__bf16)x[2], (__bf16)x[3]};
+  }
+  static __device__ __forceinline__ E to_e(float x) { return (__bf16)x; }
+  static __device__ __forceinline__ float from_e(E x) { return (float)x; }
+  static __device__ __forceinline__ f32x4 mma(f32x4 acc, const Frag& a, const Frag& b) {
+    bf16x8 av = __builtin_shufflevector(a.h[0], a.h[1], 0, 1, 2, 3, 4, 5, 6, 7);
+    bf16x8 bv = __builtin_shufflevector(b.h[0], b.h[1], 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+  }
+};
+
+template <> struct OpT<false> {
+  using E = float;
+  using Q = f32x4;
+  static constexpr int KC = 16;
+  static constexpr int NH = 1;
+  static constexpr int PAD = 4;
+  struct Frag { Q h[1]; };
+  static __device__ __forceinline__ Q cvt(f32x4 x) { return x; }
+  static __device__ __forceinline__ E to_e(float x) { return x; }
+  static __device__ __forceinline__ float from_e(E x) { return x; }
+  static __device__ __forceinline__ f32x4 mma(f32x4 acc, const Frag& a, const Frag& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.h[0][0], b.h[0][0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.h[0][1], b.h[0][1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.h[0][2], b.h[0][2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.h[0][3], b.h[0][3], acc, 0, 0, 0);
+    return acc;
+  }
+};
+
+// Fragment of row `row` of a row-major LDS array (leading dimension ld, in
+// elements) whose columns are the contraction index, for the K-step at k0.
+template <bool BF>
+__device__ __forceinline__ typename OpT<BF>::Frag lds_frag(const typename OpT<BF>::E* base,
+                                                            int ld, int row, int k0, int g) {
+  using O = OpT<BF>;
+  typename O::Frag f;
+#pragma unroll
+  for (int h = 0; h < O::NH; ++h)
+    f.h[h] = *reinterpret_cast<const typename O::Q*>(base + row * ld + k0 + 16 * h + 4 * g);
+  return f;
+}
+
+// --------------------------------------------------------------- activations
+__device__ __forceinline__ float gelu_f(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+__device__ __forceinline__ float gelu_d1(float x) {
+  return 0.5f * (1.0f + erff(x * 0.70710678118654752f)) +
+         x * 0.39894228040143268f * expf(-0.5f * x * x);
+}
+__device__ __forceinline__ float gelu_d2(float x) {
+  return 0.39894228040143268f * expf(-0.5f * x * x) * (2.0f - x * x);
+}
+__device__ __forceinline__ float sigm_f(float x) { return 1.0f / (1.0f + expf(-x)); }
+__device__ __forceinline__ float silu_f(float x) { return x * sigm_f(x); }
+__device__ __forceinline__ float silu_d1(float x) {
+  float s = sigm_f(x);
+  return s * (1.0f + x * (1.0f - s));
+}
+__device__ __forceinline__ float silu_d2(float x) {
+  float s = sigm_f(x);
+  return s * (1.0f - s) * (2.0f + x * (1.0f - 2.0f * s));
+}
+
+// ------------------------------------------------------------- reductions
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+// Sum over the 16 lanes that share a lane group (same rows of a D tile).
+__device__ __forceinline__ float group16_sum(float v) {
+#pragma unroll
+  for (int m = 8; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+// ----------------------------------------------------------- io element load
+template <bool BF> struct IoT;
+template <> struct IoT<true> {
+  using T = __bf16;
+  static __device__ __forceinline__ float ld(const T* p) { return (float)*p; }
+  static __device__ __forceinline__ void st(T* p, float x) { *p = (__bf16)x; }
+};
+template <> struct IoT<false> {
+  using T = float;
+  static __device__ __forceinline__ float ld(const T* p) { return *p; }
+  static __device__ __forceinline__ void st(T* p, float x) { *p = x; }
+};
+
+}  // namespace e2ttt

@@ -1,0 +1,217 @@
+"""ctypes binding of libe2ttt.so (the HIP implementation, C ABI in include/e2ttt.h).
+
+Argument marshalling only: tensors are passed as device pointers together with
+the current HIP stream; every step of the computation runs in the library's
+kernels.  PyTorch provides device memory and streams.  Importing this module
+on a machine without the built library raises immediately.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libe2ttt.so")
+
+FW_MLP = 0
+FW_SWIGLU = 1
+DT_F32 = 0
+DT_BF16 = 1
+FLAG_NO_RESIDUAL_LN = 1
+
+STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
+          4: "workspace too small", 5: "HIP error"}
+
+# Every entry point the header declares (checked by the CPU test-suite).
+EXPORTS = ("e2ttt_param_count", "e2ttt_workspace_bytes", "e2ttt_backward_scratch_bytes",
+           "e2ttt_chunk_forward", "e2ttt_chunk_backward", "e2ttt_chunk_coeffs",
+           "e2ttt_status_str")
+
+
+class E2TTTError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (where, STATUS.get(status, "?"), status))
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("T", ctypes.c_int32),
+                ("d", ctypes.c_int32), ("dh", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("fw", ctypes.c_int32), ("io", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("ln_eps", ctypes.c_float)]
+
+
+_lib = None
+
+
+def load():
+    """Load the in-tree HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libe2ttt.so is not built (run __graft_entry__.build() or "
+                          "python paper_2608_21308_amd/build_lib.py)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, sz, i = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    dp = ctypes.POINTER(Desc)
+    lib.e2ttt_param_count.argtypes = [dp]
+    lib.e2ttt_param_count.restype = sz
+    lib.e2ttt_workspace_bytes.argtypes = [dp, i]
+    lib.e2ttt_workspace_bytes.restype = sz
+    lib.e2ttt_backward_scratch_bytes.argtypes = [dp]
+    lib.e2ttt_backward_scratch_bytes.restype = sz
+    lib.e2ttt_chunk_forward.argtypes = [dp] + [vp] * 12 + [sz, i, vp]
+    lib.e2ttt_chunk_forward.restype = i
+    lib.e2ttt_chunk_backward.argtypes = [dp] + [vp] * 9 + [sz] + [vp] * 12 + [sz, vp]
+    lib.e2ttt_chunk_backward.restype = i
+    lib.e2ttt_chunk_coeffs.argtypes = [dp] + [vp] * 7
+    lib.e2ttt_chunk_coeffs.restype = i
+    lib.e2ttt_status_str.argtypes = [i]
+    lib.e2ttt_status_str.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+@dataclass(frozen=True)
+class Config:
+    B: int
+    H: int
+    T: int
+    d: int
+    dh: int
+    chunk: int
+    fw: int = FW_MLP
+    io: int = DT_BF16
+    flags: int = 0
+    ln_eps: float = 1e-5
+
+    def desc(self) -> Desc:
+        return Desc(self.B, self.H, self.T, self.d, self.dh, self.chunk, self.fw, self.io,
+                    self.flags, self.ln_eps)
+
+    @property
+    def P(self) -> int:
+        return (2 if self.fw == FW_MLP else 3) * self.d * self.dh
+
+    @property
+    def n_chunks(self) -> int:
+        return (self.T + self.chunk - 1) // self.chunk
+
+    @property
+    def torch_io(self):
+        return torch.bfloat16 if self.io == DT_BF16 else torch.float32
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise E2TTTError(st, where)
+
+
+def workspace_bytes(cfg: Config, save_for_backward: bool) -> int:
+    d = cfg.desc()
+    return int(load().e2ttt_workspace_bytes(ctypes.byref(d), int(bool(save_for_backward))))
+
+
+def backward_scratch_bytes(cfg: Config) -> int:
+    d = cfg.desc()
+    return int(load().e2ttt_backward_scratch_bytes(ctypes.byref(d)))
+
+
+def alloc_workspace(cfg: Config, save_for_backward: bool, device="cuda"):
+    n = workspace_bytes(cfg, save_for_backward)
+    if n == 0:
+        raise E2TTTError(3, "e2ttt_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def forward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in=None, *, out=None, w_out=None,
+            m_out=None, workspace=None, save_for_backward=False):
+    """Runs e2ttt_chunk_forward on the current stream; returns (out, w_out, m_out, workspace)."""
+    lib = load()
+    dev = q.device
+    if out is None:
+        out = torch.empty_like(q)
+    if w_out is None:
+        w_out = torch.empty_like(w_in)
+    if m_out is None:
+        m_out = torch.empty_like(w_in)
+    if workspace is None:
+        workspace = alloc_workspace(cfg, save_for_backward, dev)
+    d = cfg.desc()
+    st = lib.e2ttt_chunk_forward(ctypes.byref(d), _ptr(q), _ptr(k), _ptr(v), _ptr(eta),
+                                 _ptr(beta), _ptr(gamma), _ptr(w_in), _ptr(m_in), _ptr(out),
+                                 _ptr(w_out), _ptr(m_out), _ptr(workspace),
+                                 workspace.numel(), int(bool(save_for_backward)), _stream())
+    _check(st, "e2ttt_chunk_forward")
+    return out, w_out, m_out, workspace
+
+
+def backward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, workspace, d_out, d_w_out=None,
+             d_m_out=None, *, grads=None, scratch=None):
+    """Runs e2ttt_chunk_backward; returns a dict of gradients (dq, dk, dv, d_eta, d_beta,
+    d_gamma, d_w_in, d_m_in)."""
+    lib = load()
+    dev = q.device
+    if grads is None:
+        grads = dict(dq=torch.empty_like(q), dk=torch.empty_like(k), dv=torch.empty_like(v),
+                     d_eta=torch.empty_like(eta), d_beta=torch.empty_like(beta),
+                     d_gamma=None if gamma is None else torch.empty_like(gamma),
+                     d_w_in=torch.empty_like(w_in), d_m_in=torch.empty_like(w_in))
+    if scratch is None:
+        scratch = torch.empty(backward_scratch_bytes(cfg), dtype=torch.uint8, device=dev)
+    d = cfg.desc()
+    g = grads
+    st = lib.e2ttt_chunk_backward(
+        ctypes.byref(d), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta), _ptr(gamma),
+        _ptr(w_in), _ptr(m_in), _ptr(workspace), workspace.numel(), _ptr(d_out), _ptr(d_w_out),
+        _ptr(d_m_out), _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["d_eta"]),
+        _ptr(g["d_beta"]), _ptr(g["d_gamma"]), _ptr(g["d_w_in"]), _ptr(g["d_m_in"]),
+        _ptr(scratch), scratch.numel(), _stream())
+    _check(st, "e2ttt_chunk_backward")
+    return grads
+
+
+def chunk_coeffs(cfg: Config, eta, beta, gamma):
+    """Scalar kernels: (kw [B,H,T], km [B,H,T], carry [B,H,NC,3])."""
+    lib = load()
+    kw = torch.empty_like(eta)
+    km = torch.empty_like(eta)
+    carry = torch.empty((cfg.B, cfg.H, cfg.n_chunks, 3), dtype=torch.float32, device=eta.device)
+    d = cfg.desc()
+    st = lib.e2ttt_chunk_coeffs(ctypes.byref(d), _ptr(eta), _ptr(beta), _ptr(gamma), _ptr(kw),
+                                _ptr(km), _ptr(carry), _stream())
+    _check(st, "e2ttt_chunk_coeffs")
+    return kw, km, carry
+
+
+class E2TTTFunction(torch.autograd.Function):
+    """Autograd wrapper: forward saves the workspace, backward calls the library."""
+
+    @staticmethod
+    def forward(ctx, cfg, q, k, v, eta, beta, gamma, w_in, m_in):
+        out, w_out, m_out, ws = forward(cfg, q, k, v, eta, beta, gamma, w_in, m_in,
+                                        save_for_backward=True)
+        ctx.cfg = cfg
+        ctx.save_for_backward(q, k, v, eta, beta, gamma, w_in, m_in, ws)
+        return out, w_out, m_out
+
+    @staticmethod
+    def backward(ctx, d_out, d_w_out, d_m_out):
+        q, k, v, eta, beta, gamma, w_in, m_in, ws = ctx.saved_tensors
+        g = backward(ctx.cfg, q, k, v, eta, beta, gamma, w_in, m_in, ws, d_out.contiguous(),
+                     None if d_w_out is None else d_w_out.contiguous(),
+                     None if d_m_out is None else d_m_out.contiguous())
+        return (None, g["dq"], g["dk"], g["dv"], g["d_eta"], g["d_beta"], g["d_gamma"],
+                g["d_w_in"], None if m_in is None else g["d_m_in"])

@@ -1,0 +1,107 @@
+"""C ABI checks that run without a GPU: the library loads, exports every entry
+point of include/e2ttt.h, sizes workspaces, and rejects bad arguments before
+launching anything (no call here reaches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_21308_amd import e2ttt
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return e2ttt.load()
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "e2ttt.h")).read()
+    return sorted(set(re.findall(r"\b(e2ttt_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_function(lib):
+    names = header_functions()
+    assert set(names) == set(e2ttt.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def desc(**kw):
+    base = dict(B=2, H=4, T=2048, d=64, dh=256, chunk=64, fw=0, io=1, flags=0, ln_eps=1e-5)
+    base.update(kw)
+    return e2ttt.Desc(**base)
+
+
+def test_sizes(lib):
+    d = desc()
+    assert lib.e2ttt_param_count(ctypes.byref(d)) == 2 * 64 * 256
+    ws0 = lib.e2ttt_workspace_bytes(ctypes.byref(d), 0)
+    ws1 = lib.e2ttt_workspace_bytes(ctypes.byref(d), 1)
+    # per-token K^W, K^M and per-chunk carries; plus bf16 W and M checkpoints per chunk
+    assert ws0 >= 2 * 8 * 2048 * 4 + 8 * 32 * 3 * 4
+    assert ws1 >= ws0 + 8 * 32 * 2 * 2 * (2 * 64 * 256)
+    assert lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) >= ws0
+    d = desc(fw=1, dh=172)
+    assert lib.e2ttt_param_count(ctypes.byref(d)) == 3 * 64 * 172
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=0), 2), (dict(B=-1), 2), (dict(chunk=0), 2), (dict(ln_eps=0.0), 2),
+    (dict(chunk=65), 3), (dict(fw=2), 3), (dict(io=7), 3), (dict(flags=4), 3),
+    (dict(d=32), 3), (dict(d=16), 3), (dict(dh=300), 3), (dict(fw=1, dh=200), 3),
+    (dict(io=0, d=64), 3), (dict(io=0, d=16, dh=200), 3)])
+def test_bad_descriptors(lib, kw, status):
+    d = desc(**kw)
+    assert lib.e2ttt_param_count(ctypes.byref(d)) == 0
+    assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 1) == 0
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    st = lib.e2ttt_chunk_forward(ctypes.byref(d), *([fake] * 12), 1 << 40, 0, None)
+    assert st == status
+    st = lib.e2ttt_chunk_backward(ctypes.byref(d), *([fake] * 9), 1 << 40, *([fake] * 12),
+                                  1 << 40, None)
+    assert st == status
+
+
+def test_null_and_workspace_errors(lib):
+    d = desc()
+    fake = ctypes.c_void_p(16)
+    args = [fake] * 12
+    assert lib.e2ttt_chunk_forward(None, *args, 1 << 40, 0, None) == 1
+    for i in (0, 1, 2, 3, 4, 6, 8, 9, 10, 11):    # q k v eta beta w_in out w_out m_out workspace
+        a = list(args)
+        a[i] = None
+        assert lib.e2ttt_chunk_forward(ctypes.byref(d), *a, 1 << 40, 0, None) == 1, i
+    # gamma (5) and m_in (7) are optional: with a too-small workspace the call
+    # gets past the pointer checks and stops at the size check
+    a = list(args)
+    a[5] = None
+    a[7] = None
+    ws = lib.e2ttt_workspace_bytes(ctypes.byref(d), 1)
+    assert lib.e2ttt_chunk_forward(ctypes.byref(d), *a, ws - 1, 1, None) == 4
+    # a workspace without checkpoints is too small for save_for_backward
+    ws0 = lib.e2ttt_workspace_bytes(ctypes.byref(d), 0)
+    assert lib.e2ttt_chunk_forward(ctypes.byref(d), *args, ws0, 1, None) == 4
+    # state outputs aliasing the inputs are refused when saving for backward
+    a = list(args)
+    a[9] = a[6] = ctypes.c_void_p(32)
+    assert lib.e2ttt_chunk_forward(ctypes.byref(d), *a, 1 << 40, 1, None) == 2
+    # backward: d_gamma must be given iff gamma is
+    bargs = [fake] * 9 + [1 << 40] + [fake] * 12 + [1 << 40, None]
+    b = list(bargs)
+    b[5] = None
+    assert lib.e2ttt_chunk_backward(ctypes.byref(d), *b) == 2
+    b = list(bargs)
+    b[9] = ws - 1
+    assert lib.e2ttt_chunk_backward(ctypes.byref(d), *b) == 4
+    sc = lib.e2ttt_backward_scratch_bytes(ctypes.byref(d))
+    b = list(bargs)
+    b[-2] = sc - 1
+    assert lib.e2ttt_chunk_backward(ctypes.byref(d), *b) == 4
+
+
+def test_status_strings(lib):
+    for s in range(6):
+        assert lib.e2ttt_status_str(s)

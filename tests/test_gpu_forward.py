@@ -1,0 +1,266 @@
+"""GPU parity of the forward path (e2ttt_chunk_forward, e2ttt_chunk_coeffs)
+against the fp64 oracle on identical seeded inputs.
+
+Tolerances: rel-L2 1e-5 for fp32 io, 2e-2 for bf16 io (per output tensor).
+The SwiGLU + residual-LayerNorm workloads are chaotic under the synthetic
+gates: a 1e-7 perturbation of the initial weights grows to O(1) within about
+eight chunks even in fp64 (test_swiglu_ln_trajectory_is_chaotic pins this on
+the oracle alone), so for them the GPU is checked chunk window by chunk
+window, starting from the oracle's own state at the window start; the bare
+SwiGLU net (no residual LN) is well conditioned and is checked end to end.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2608_21308_amd import e2ttt, workloads as WL
+from tests.gpu_util import TOL, config_of, gpu_forward, rel_l2, slice_tokens, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    e2ttt.load()
+
+
+def run_both(w, x, flags=0, m_in=None, check_state=True):
+    io = w.io
+    cfg = config_of(w, flags=flags)
+    t = to_dev(x, io)
+    if m_in is not None:
+        t["m_in"] = torch.from_numpy(np.ascontiguousarray(m_in, dtype=np.float32)).cuda()
+    out, wo, mo, _ = gpu_forward(cfg, t)
+    torch.cuda.synchronize()
+    ro, rw, rm = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"],
+                                x["w_in"], m_in, C=w.C, fw=w.fw, dh=w.dh, flags=flags)
+    errs = {"out": rel_l2(out, ro)}
+    if check_state:
+        errs["w_out"] = rel_l2(wo, rw)
+        errs["m_out"] = rel_l2(mo, rm)
+    return errs, (out, wo, mo), (ro, rw, rm)
+
+
+def assert_tol(errs, io, what=""):
+    tol = TOL[io]
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    print(what, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    assert not bad, "%s rel-L2 above %g: %s" % (what, tol, bad)
+
+
+# ------------------------------------------------------------------ scalars
+@pytest.mark.parametrize("T,C", [(256, 16), (200, 64), (64, 1), (70, 7)])
+def test_coeffs_match_oracle(T, C):
+    w = WL.WORKLOADS[1].with_(B=1, H=3, T=T, C=C)
+    x = WL.make_inputs(w, with_grads=False)
+    cfg = config_of(w)
+    t = to_dev(x, "bf16")
+    kw, km, carry = e2ttt.chunk_coeffs(cfg, t["eta"], t["beta"], t["gamma"])
+    torch.cuda.synchronize()
+    kw, km, carry = kw.cpu().numpy(), km.cpu().numpy(), carry.cpu().numpy()
+    for u in range(3):
+        for r, s0 in enumerate(range(0, T, C)):
+            sl = slice(s0, min(T, s0 + C))
+            rkw, rkm, rc = oracle.chunk_coeffs(x["eta"][0, u, sl], x["beta"][0, u, sl],
+                                               x["gamma"][0, u, sl])
+            np.testing.assert_allclose(kw[0, u, sl], rkw, rtol=2e-6, atol=1e-12)
+            np.testing.assert_allclose(km[0, u, sl], rkm, rtol=2e-6, atol=1e-30)
+            np.testing.assert_allclose(carry[0, u, r], rc, rtol=2e-6, atol=1e-30)
+
+
+def test_coeffs_degenerate_gates():
+    # beta = gamma = 1 (R_t = C - t + 1), beta = 0 (no momentum), gamma = NULL
+    T, C = 64, 64
+    w = WL.WORKLOADS[1].with_(B=1, H=1, T=T, C=C)
+    cfg = config_of(w)
+    eta = torch.linspace(0.01, 0.1, T, device="cuda").reshape(1, 1, T)
+    for beta_v, gamma_v in ((1.0, 1.0), (0.0, 0.9), (0.5, None)):
+        beta = torch.full((1, 1, T), beta_v, device="cuda")
+        gamma = None if gamma_v is None else torch.full((1, 1, T), gamma_v, device="cuda")
+        kw, km, carry = e2ttt.chunk_coeffs(cfg, eta, beta, gamma)
+        torch.cuda.synchronize()
+        e = eta.cpu().numpy()[0, 0]
+        g = None if gamma is None else gamma.cpu().numpy()[0, 0]
+        rkw, rkm, rc = oracle.chunk_coeffs(e, beta.cpu().numpy()[0, 0], g)
+        np.testing.assert_allclose(kw.cpu().numpy()[0, 0], rkw, rtol=2e-6, atol=1e-12)
+        np.testing.assert_allclose(km.cpu().numpy()[0, 0], rkm, rtol=2e-6, atol=1e-12)
+        np.testing.assert_allclose(carry.cpu().numpy()[0, 0, 0], rc, rtol=2e-6, atol=1e-12)
+
+
+# ------------------------------------------------------------ fp32 path
+def test_forward_tiny_fp32_config():
+    w = WL.WORKLOADS[0]
+    errs, _, _ = run_both(w, WL.make_inputs(w))
+    assert_tol(errs, "f32", w.name)
+
+
+@pytest.mark.parametrize("fw", [WL.FW_MLP, WL.FW_SWIGLU])
+@pytest.mark.parametrize("T,C,dh,flags", [(32, 16, 64, 0), (20, 16, 64, 0), (96, 64, 64, 0),
+                                          (12, 7, 50, 0), (3, 1, 64, 0), (32, 16, 128, 0),
+                                          (50, 32, 100, 0), (128, 16, 64, 1), (75, 7, 50, 1)])
+def test_forward_fp32_shapes(fw, T, C, dh, flags):
+    # one or two chunks (plus ragged tails) per run: over long trajectories the
+    # residual-LN dynamics amplify fp32 rounding itself past 1e-5 (a float32
+    # numpy implementation of the same closed form drifts by 4e-6 .. 1e-4 on
+    # 11 chunks of these shapes), so long-run fp32 parity is pinned on the
+    # tiny workload above and on the bare net (flags = 1) here.
+    w = WL.WORKLOADS[0].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, seed=500 + T + C + dh)
+    x = WL.make_inputs(w, with_grads=False)
+    m_in = np.random.default_rng(T).standard_normal(x["w_in"].shape).astype(np.float32) * 1e-3
+    errs, _, _ = run_both(w, x, flags=flags, m_in=m_in)
+    assert_tol(errs, "f32", "fp32 fw=%d T=%d C=%d dh=%d flags=%d" % (fw, T, C, dh, flags))
+
+
+# ------------------------------------------------------------ bf16 path
+def test_forward_mlp_bf16_config():
+    w = WL.WORKLOADS[1]
+    errs, _, _ = run_both(w, WL.make_inputs(w))
+    assert_tol(errs, "bf16", w.name)
+
+
+@pytest.mark.parametrize("T,C,dh,fw,flags", [(200, 64, 256, 0, 0), (130, 32, 256, 0, 0),
+                                             (96, 16, 64, 0, 0), (256, 64, 120, 0, 0),
+                                             (300, 64, 172, 1, 1), (64, 64, 172, 1, 0),
+                                             (192, 48, 100, 1, 1)])
+def test_forward_bf16_shapes(T, C, dh, fw, flags):
+    w = WL.WORKLOADS[1].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, seed=900 + T + dh)
+    errs, _, _ = run_both(w, WL.make_inputs(w, with_grads=False), flags=flags)
+    assert_tol(errs, "bf16", "bf16 T=%d C=%d dh=%d fw=%d flags=%d" % (T, C, dh, fw, flags))
+
+
+def test_forward_1p3b_layer_sampled_units():
+    # full launch (all 128 units) at the training shape; the oracle checks a
+    # sample of units, which are independent of each other
+    w = WL.WORKLOADS[3]
+    x = WL.make_inputs(w, with_grads=False)
+    cfg = config_of(w)
+    t = to_dev(x, "bf16")
+    out, wo, mo, _ = gpu_forward(cfg, t)
+    torch.cuda.synchronize()
+    units = [0, 77, 127]
+    xs = WL.make_inputs(w, with_grads=False, units=units)
+    ro, rw, rm = oracle.forward(xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"], xs["gamma"],
+                                xs["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
+    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units]
+    errs = {"out": rel_l2(flat(out), ro[0]), "w_out": rel_l2(flat(wo), rw[0]),
+            "m_out": rel_l2(flat(mo), rm[0])}
+    assert_tol(errs, "bf16", w.name)
+    assert torch.isfinite(out.float()).all()
+
+
+def test_swiglu_literal_net_end_to_end():
+    # the bare net f(x) = Wd (SiLU(Wg x) * Wu x) of the SwiGLU workloads
+    w = WL.WORKLOADS[2]
+    errs, _, _ = run_both(w, WL.make_inputs(w, with_grads=False), flags=e2ttt.FLAG_NO_RESIDUAL_LN)
+    assert_tol(errs, "bf16", w.name + " (bare net)")
+
+
+def test_swiglu_prefill_literal_net_sampled_units():
+    w = WL.WORKLOADS[4]
+    x = WL.make_inputs(w)
+    cfg = config_of(w, flags=e2ttt.FLAG_NO_RESIDUAL_LN)
+    t = to_dev(x, "bf16")
+    out, wo, mo, _ = gpu_forward(cfg, t)
+    torch.cuda.synchronize()
+    units = [3, 12]
+    xs = WL.make_inputs(w, units=units)
+    ro, rw, rm = oracle.forward(xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"], xs["gamma"],
+                                xs["w_in"], None, C=w.C, fw=w.fw, dh=w.dh,
+                                flags=e2ttt.FLAG_NO_RESIDUAL_LN)
+    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units]
+    errs = {"out": rel_l2(flat(out), ro[0])}
+    assert_tol(errs, "bf16", w.name + " (bare net)")
+    assert torch.isfinite(out.float()).all()
+
+
+def oracle_state_at(x, w, r, flags=0):
+    """Oracle chunk-start state (W, M) of chunk r (None, None for r = 0)."""
+    if r == 0:
+        return x["w_in"], None
+    y = slice_tokens(x, 0, r * w.C)
+    _, rw, rm = oracle.forward(y["q"], y["k"], y["v"], y["eta"], y["beta"], y["gamma"],
+                               y["w_in"], None, C=w.C, fw=w.fw, dh=w.dh, flags=flags)
+    return rw, rm
+
+
+@pytest.mark.parametrize("cfg_idx,units,starts", [(2, None, [0, 1, 3, 8, 17, 24, 31]),
+                                                  (4, [5], [0, 1, 50, 100, 300, 511])])
+def test_swiglu_ln_chunk_windows(cfg_idx, units, starts):
+    # One chunk at a time from the oracle's own chunk-start state.  The bound
+    # is 2e-2, widened only where the chunk itself is ill-conditioned: the
+    # oracle is re-run from its state rounded to bf16 (one of the roundings
+    # any bf16-operand implementation makes) and the GPU may deviate by at
+    # most 4x that intrinsic sensitivity.
+    w = WL.WORKLOADS[cfg_idx]
+    x = WL.make_inputs(w, with_grads=False, units=units)
+    wu = w.with_(B=x["q"].shape[0], H=x["q"].shape[1], T=w.C)
+    strict = 0
+    for r in starts:
+        W0, M0 = oracle_state_at(x, w.with_(B=wu.B, H=wu.H), r)
+        y = slice_tokens(x, r * w.C, (r + 1) * w.C)
+        y["w_in"] = np.ascontiguousarray(W0, dtype=np.float32)
+        m0 = None if M0 is None else np.ascontiguousarray(M0, dtype=np.float32)
+        errs, _, ref = run_both(wu, y, m_in=m0)
+        yb = dict(y)
+        yb["w_in"] = WL.round_bf16(y["w_in"])
+        mb = None if m0 is None else WL.round_bf16(m0)
+        pb = oracle.forward(yb["q"], yb["k"], yb["v"], yb["eta"], yb["beta"], yb["gamma"],
+                            yb["w_in"], mb, C=w.C, fw=w.fw, dh=w.dh)
+        sens = {n: rel_l2(a, b) for n, a, b in zip(("out", "w_out", "m_out"), pb, ref)}
+        bound = {n: max(TOL["bf16"], 4 * sens[n]) for n in errs}
+        strict += all(b == TOL["bf16"] for b in bound.values())
+        print("%s chunk %d gpu %s  bf16-state sensitivity %s" % (
+            w.name, r, {k: "%.2e" % v for k, v in errs.items()},
+            {k: "%.2e" % v for k, v in sens.items()}), flush=True)
+        bad = {n: (errs[n], bound[n]) for n in errs if not errs[n] <= bound[n]}
+        assert not bad, "chunk %d: %s" % (r, bad)
+    assert strict >= len(starts) // 2, "too few well-conditioned windows to be a check"
+
+
+# ------------------------------------------------------------ properties
+def test_forward_deterministic():
+    w = WL.WORKLOADS[1].with_(B=2, H=2, T=512)
+    cfg = config_of(w)
+    t = to_dev(WL.make_inputs(w, with_grads=False), "bf16")
+    a = gpu_forward(cfg, t)
+    b = gpu_forward(cfg, t)
+    torch.cuda.synchronize()
+    for x, y in zip(a[:3], b[:3]):
+        assert torch.equal(x, y)
+
+
+def test_zero_learning_rate_keeps_state():
+    w = WL.WORKLOADS[1].with_(B=1, H=2, T=300)
+    x = WL.make_inputs(w, with_grads=False)
+    x["eta"] = np.zeros_like(x["eta"])
+    x["gamma"] = None
+    cfg = config_of(w)
+    t = to_dev(x, "bf16")
+    out, wo, mo, _ = gpu_forward(cfg, t)
+    torch.cuda.synchronize()
+    assert torch.equal(wo, t["w_in"])
+    assert torch.count_nonzero(mo) == 0
+    ref = np.stack([oracle.net(x["w_in"][0, h], x["q"][0, h], fw=w.fw, dh=w.dh)
+                    for h in range(w.H)])[None]
+    assert rel_l2(out, ref) < TOL["bf16"]
+
+
+def test_resume_matches_single_call():
+    w = WL.WORKLOADS[1].with_(B=1, H=2, T=384)
+    x = WL.make_inputs(w, with_grads=False)
+    cfg = config_of(w)
+    t = to_dev(x, "bf16")
+    out, wo, mo, _ = gpu_forward(cfg, t)
+    T1 = 128
+    c1 = config_of(w, T=T1)
+    c2 = config_of(w, T=w.T - T1)
+    t1 = to_dev(slice_tokens(x, 0, T1), "bf16")
+    t2 = to_dev(slice_tokens(x, T1, w.T), "bf16")
+    o1, w1, m1, _ = gpu_forward(c1, t1)
+    t2["w_in"] = w1
+    o2, w2, m2, _ = gpu_forward(c2, t2, m_in=m1)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([o1, o2], dim=2), out)
+    assert torch.equal(w2, wo) and torch.equal(m2, mo)

@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+from paper_2608_21308_amd import workloads as WL
 from tests import torchref
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -327,3 +328,37 @@ def test_backward_without_gamma_or_state_grads(oracle):
     assert g1["d_gamma"] is None
     for n in ("dq", "dk", "dv", "d_eta", "d_beta", "d_w_in", "d_m_in"):
         np.testing.assert_array_equal(g1[n], g2[n])
+
+
+def rel_l2(a, b):
+    return float(np.linalg.norm(np.asarray(a) - np.asarray(b)) / np.linalg.norm(np.asarray(b)))
+
+
+def test_swiglu_ln_trajectory_is_chaotic(oracle):
+    # The fp64 trajectory of the SwiGLU + residual-LN workload (B2 H4 T2048,
+    # d 64, dh 172, C 64, synthetic gates) amplifies a 1e-7 relative
+    # perturbation of W_init to an O(1) change of the outputs, so end-to-end
+    # parity at any finite precision is not meaningful for it; the GPU tests
+    # compare it chunk window by chunk window instead.  The MLP workload of
+    # the same recipe stays at the perturbation's size.
+    w = WL.WORKLOADS[2]
+    x = WL.make_inputs(w, with_grads=False, units=[0])
+    ro, _, _ = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"], x["w_in"],
+                              None, C=w.C, fw=w.fw, dh=w.dh)
+    xp = dict(x)
+    rng = np.random.default_rng(0)
+    xp["w_in"] = x["w_in"] * (1 + 1e-7 * rng.standard_normal(x["w_in"].shape))
+    rp, _, _ = oracle.forward(xp["q"], xp["k"], xp["v"], xp["eta"], xp["beta"], xp["gamma"],
+                              xp["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
+    assert rel_l2(rp, ro) > 0.1
+    w = WL.WORKLOADS[1]
+    x = WL.make_inputs(w, with_grads=False, units=[0])
+    ro, _, _ = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"], x["w_in"],
+                              None, C=w.C, fw=w.fw, dh=w.dh)
+    xp = dict(x)
+    xp["w_in"] = x["w_in"] * (1 + 1e-7 * rng.standard_normal(x["w_in"].shape))
+    rp, _, _ = oracle.forward(xp["q"], xp["k"], xp["v"], xp["eta"], xp["beta"], xp["gamma"],
+                              xp["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
+    assert rel_l2(rp, ro) < 1e-6
+
+
