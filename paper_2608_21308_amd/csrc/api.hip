@@ -74,8 +74,8 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_carry = pl.off_km + align_up(tok);
   pl.off_ckpt = pl.off_carry + align_up(chk);
   pl.ws_bytes = pl.off_ckpt;
-  pl.ckpt_stride = chain_ckpt_elems(pl.cfg);
-  pl.ws_bytes_save = pl.off_ckpt + align_up((size_t)U * pl.NC * 2 * pl.ckpt_stride * sizeof(uint16_t));
+  pl.ckpt_stride = chain_ckpt_bytes(pl.cfg);
+  pl.ws_bytes_save = pl.off_ckpt + align_up((size_t)U * pl.NC * 2 * pl.ckpt_stride);
   pl.off_kwb = 0;
   pl.off_kmb = align_up(tok);
   pl.off_carryb = pl.off_kmb + align_up(tok);
@@ -177,7 +177,7 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   a.w_in = w_in; a.m_in = m_in;
   a.kw = kw; a.km = km; a.carry = carry;
   a.out = out; a.w_out = w_out; a.m_out = m_out;
-  a.ckpt = save_for_backward ? at<uint16_t>(workspace, pl.off_ckpt) : nullptr;
+  a.ckpt = save_for_backward ? at<char>(workspace, pl.off_ckpt) : nullptr;
   a.ckpt_stride = pl.ckpt_stride;
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
@@ -209,7 +209,7 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   a.kw = at<float>(workspace, pl.off_kw);
   a.km = at<float>(workspace, pl.off_km);
   a.carry = at<float>(workspace, pl.off_carry);
-  a.ckpt = const_cast<uint16_t*>(at<uint16_t>(workspace, pl.off_ckpt));
+  a.ckpt = const_cast<char*>(at<char>(workspace, pl.off_ckpt));
   a.ckpt_stride = pl.ckpt_stride;
   a.d_out = d_out; a.d_w_out = d_w_out; a.d_m_out = d_m_out;
   a.dq = dq; a.dk = dk; a.dv = dv;

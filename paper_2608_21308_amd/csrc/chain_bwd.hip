@@ -1,8 +1,848 @@
-// Backward chain kernel (placeholder until the reverse chain lands).
+// Backward chain kernel: reverse mode through Algorithm 1, one workgroup per
+// (batch, head) unit, chunks in reverse order.
+//
+// The adjoint state (Wb, Mb) = (dL/dW_C, dL/dM_C) of the current chunk lives in
+// MFMA accumulator tiles (same layout as the forward state).  For a chunk with
+// start state (W_0, M_0) (read back from the forward's checkpoints), scalar
+// kernels K^W, K^M and carries (cw, cm, cb):
+//   W_C = cw W_0 + cm M_0 + sum_t K^W_t G_t,   M_C = cb M_0 + sum_t K^M_t G_t,
+//   o_t = f_{W_0}(q_t),   G_t = G(W_0, k_t, v_t) = -grad_W 1/2||f_{W_0}(k_t) - v_t||^2,
+// the adjoints are
+//   dK^W_t = <Wb, G_t>, dK^M_t = <Mb, G_t>, dcw = <Wb, W_0>, dcm = <Wb, M_0>, dcb = <Mb, M_0>
+//   dM_0 = cm Wb + cb Mb
+//   dW_0 = cw Wb + d/dW_0 sum_t <Gb_t, G_t> + d/dW_0 sum_t <do_t, o_t>,  Gb_t = K^W_t Wb + K^M_t Mb
+// and d/dk_t, d/dv_t, d/dq_t follow from the same two terms.  The terms
+// through G_t are second order (Hessian-vector products); they are formed by
+// differentiating the first-order gradient graph once more:
+//   G_t = (dH_t k_t^T, dY_t a_t^T) with dY = LN backward of e = v - f, dA = dY W2,
+//   dH = dA * act'(H); with p = Gb1 k (over i), p2 = Gb2 a (over j), r1 = Gb1^T dH
+//   (over j), r2 = Gb2^T dY (over i), the reverse pass through
+//   dH -> dA -> dY -> (e, Z, sigma) -> Y -> A -> H -> (W_0, k) gives
+//   Wb2 += dY^T dAh + Yh^T A,  Wb1 += K^T Hh,  dk = r1 - eh + Hh W1,  dv = eh,
+//   dAh = p act'(H), Hh = p dA act''(H) + (r2 + Yh W2) act'(H),
+//   eh = LNb(dYh),  dYh = p2 + dAh W2^T,  Yh = LNb(zh) + sigh Z / d,
+//   zh = -(dYh mean(eZ) + e mean(dYh Z))/sigma - eh,  sigh = -sum(dYh dY)/sigma,
+// where LNb(x) = (x - mean x - Z mean(x Z)) / sigma (per token, over the head dim).
+// SwiGLU and the bare net (no residual LN) follow the same pattern.
 #include "chain_common.h"
 
 namespace e2ttt {
-hipError_t launch_chain_bwd(const ChainConfig&, const ChainArgs&, long, hipStream_t) {
+
+namespace {
+
+template <class S>
+struct BwdLayout {
+  using E = typename S::E;
+  static constexpr int JH = (S::DHK > 128) ? 2 : 1;     // hidden halves per j-round
+  static constexpr int JWD = S::DHK / JH;                // hidden width of one half
+  static constexpr int LDJ = JWD + S::O::PAD;
+  static_assert(JWD % S::KC == 0, "half width must be a multiple of the K-step");
+  static_assert(JWD % (16 * S::NJB) == 0, "a wave's hidden slice must lie in one half");
+  static constexpr int TD = S::CM * S::LDD * (int)sizeof(E);   // [t][i]
+  static constexpr int DT = S::D * S::LDC * (int)sizeof(E);    // [i][t]
+  static constexpr int TDX = (TD > DT) ? TD : DT;
+  static constexpr int TJ = S::CM * LDJ * (int)sizeof(E);      // [t][j] half
+  static constexpr int IJ = S::D * LDJ * (int)sizeof(E);       // [i][j] half
+  static constexpr int F = S::CM * S::D * 4;                   // fp32 [t][i]
+  static constexpr int R1 = (2 * TDX > F) ? 2 * TDX : F;
+  static constexpr int A16(int x) { return (x + 15) / 16 * 16; }
+  // region offsets (bytes)
+  static constexpr int XK = 0;                   // K [t][i]            | out branch: Q [t][i]
+  static constexpr int JW = A16(XK + TD);        // j-round weight half [i][j]
+  static constexpr int JA = A16(JW + IJ);        // j-round activation half [t][j]
+  static constexpr int YK = A16(JA + TJ);        // fp32 Y -> Z          | out branch: Y_Q
+  static constexpr int EK = A16(YK + F);         // fp32 E -> eh
+  static constexpr int RR = A16(EK + F);         // V | dY (t,i) ; dYh fp32 ; K^T ; dO
+  static constexpr int DYT = A16(RR + R1);       // dY^T [i][t]          | out branch: Yb_Q^T
+  static constexpr int YH = A16(DYT + DT);       // Yh [t][i]            | out branch: Yb_Q
+  static constexpr int YHT = A16(YH + TD);       // Yh^T [i][t]          | out branch: Q^T
+  static constexpr int ROW = A16(YHT + DT);      // per token: sigma, mean(e Z)
+  static constexpr int KB = A16(ROW + S::CM * 8);          // dK^W, dK^M partials [2][NW][CM]
+  static constexpr int CB = A16(KB + 2 * S::NW * S::CM * 4);  // carry adjoint partials [NW][4]
+  static constexpr int SC = A16(CB + S::NW * 16);          // kw[CM], km[CM], carry[4]
+  static constexpr int TOTAL = A16(SC + (2 * S::CM + 4) * 4);
+  static_assert(TOTAL <= 160 * 1024, "LDS budget of the backward chain kernel");
+  // j-round output items per wave: (token block, head block pair) items
+  static constexpr int NITEM = S::NTB * (S::NIB / S::IBB);
+  static constexpr int JIT = (NITEM + S::NW - 1) / S::NW;
+};
+
+template <class S>
+struct JAcc {
+  f32x4 v[BwdLayout<S>::JIT][S::IBB];
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int a = 0; a < BwdLayout<S>::JIT; ++a)
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b) v[a][b] = zero4();
+  }
+};
+
+// j-round: out[t][i] (+)= rowscale[t] * sum_j Act[t][j] Wt[i][j] over the full
+// hidden range.  Act and Wt are register tiles of every wave: act(tb, jj) is
+// the tile (rows t, column j) and wt(ib, jj) the tile (rows i, column j).
+// Both are written to the half-width LDS buffers one half at a time.
+template <class S, class FA, class FWT>
+__device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, typename S::E* ja,
+                                       typename S::E* jw, FA act, FWT wt, int w, int g, int c) {
+  using L = BwdLayout<S>;
+  using O = typename S::O;
+  constexpr int NI = S::NIB / S::IBB;
+  JAcc<S> tmp;
+  tmp.zero();
+#pragma unroll
+  for (int half = 0; half < L::JH; ++half) {
+    // columns of this half beyond the padded hidden width belong to no wave;
+    // they may hold the previous half's values and must read as zero
+    constexpr int NT = S::NT;
+    const int validw = S::DHP - half * L::JWD;
+    if (validw < L::JWD) {
+      const int nz = L::JWD - validw;
+#pragma unroll 1
+      for (int idx = threadIdx.x; idx < (S::CM + S::D) * nz; idx += NT) {
+        const int rw = idx / nz, col = validw + idx % nz;
+        if (rw < S::CM) ja[rw * L::LDJ + col] = O::to_e(0.0f);
+        else jw[(rw - S::CM) * L::LDJ + col] = O::to_e(0.0f);
+      }
+    }
+    const int col0 = 16 * w * S::NJB - half * L::JWD;   // this wave's first column in the half
+    if (col0 >= 0 && col0 < L::JWD) {
+#pragma unroll
+      for (int jj = 0; jj < S::NJB; ++jj) {
+        const int col = col0 + 16 * jj + c;
+#pragma unroll
+        for (int tb = 0; tb < S::NTB; ++tb) {
+          const f32x4 v = act(tb, jj);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = O::to_e(v[r]);
+        }
+#pragma unroll
+        for (int ib = 0; ib < S::NIB; ++ib) {
+          const f32x4 v = wt(ib, jj);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) jw[(16 * ib + 4 * g + r) * L::LDJ + col] = O::to_e(v[r]);
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < L::JIT; ++a) {
+      const int it = w + a * S::NW;
+      if (it < L::NITEM) {
+        const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll 2
+        for (int p = 0; p < L::JWD / S::KC; ++p) {
+          auto af = lds_frag<S::BF>(ja, L::LDJ, 16 * tb + c, p * S::KC, g);
+#pragma unroll
+          for (int b = 0; b < S::IBB; ++b) {
+            auto bf = lds_frag<S::BF>(jw, L::LDJ, 16 * (ib0 + b) + c, p * S::KC, g);
+            tmp.v[a][b] = O::mma(tmp.v[a][b], af, bf);
+          }
+          sched_fence();
+        }
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int a = 0; a < L::JIT; ++a) {
+    const int it = w + a * S::NW;
+    if (it < L::NITEM) {
+      const int tb = it / NI;
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float s = rowscale ? rowscale[16 * tb + 4 * g + r] : 1.0f;
+          out.v[a][b][r] += s * tmp.v[a][b][r];
+        }
+    }
+  }
+}
+
+// Write (or add to global io) the j-round output tiles: dst[t][i] = out + extra[t][i].
+template <class S, class FX>
+__device__ __forceinline__ void jacc_store_io(const JAcc<S>& out, void* dst, long row0, int len,
+                                              FX extra, int w, int g, int c) {
+  using L = BwdLayout<S>;
+  using IO = IoT<S::BF>;
+  constexpr int NI = S::NIB / S::IBB;
+  typename IO::T* p = reinterpret_cast<typename IO::T*>(dst) + row0 * S::D;
+#pragma unroll
+  for (int a = 0; a < L::JIT; ++a) {
+    const int it = w + a * S::NW;
+    if (it < L::NITEM) {
+      const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * tb + 4 * g + r, i = 16 * (ib0 + b) + c;
+          if (t < len) IO::st(p + (long)t * S::D + i, out.v[a][b][r] + extra(t, i));
+        }
+    }
+  }
+}
+
+template <class S>
+__global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
+  using O = typename S::O;
+  using E = typename S::E;
+  using Q = typename O::Q;
+  using L = BwdLayout<S>;
+  constexpr int D = S::D, NJB = S::NJB, NTB = S::NTB, NIB = S::NIB, NMAT = S::NMAT, NW = S::NW;
+  constexpr int SEC = NMAT - 1;      // second-layer matrix
+  constexpr int NF = NMAT - 1;       // number of first-layer matrices
+  constexpr bool SW = S::FW == 1;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[L::TOTAL];
+  E* xk = reinterpret_cast<E*>(smem + L::XK);
+  E* jw = reinterpret_cast<E*>(smem + L::JW);
+  E* ja = reinterpret_cast<E*>(smem + L::JA);
+  float* yk = reinterpret_cast<float*>(smem + L::YK);
+  float* ek = reinterpret_cast<float*>(smem + L::EK);
+  unsigned char* rr = smem + L::RR;
+  E* dyt = reinterpret_cast<E*>(smem + L::DYT);
+  E* yh = reinterpret_cast<E*>(smem + L::YH);
+  E* yht = reinterpret_cast<E*>(smem + L::YHT);
+  float* row = reinterpret_cast<float*>(smem + L::ROW);
+  float* kb = reinterpret_cast<float*>(smem + L::KB);
+  float* cbp = reinterpret_cast<float*>(smem + L::CB);
+  float* skw = reinterpret_cast<float*>(smem + L::SC);
+  float* skm = skw + S::CM;
+  float* scar = skm + S::CM;
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, c = lane & 15;
+  const long u = blockIdx.x;
+  const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
+  const float inv_d = 1.0f / D;
+  const bool resln = a.resln != 0;
+
+  // adjoint of the final state
+  StateTiles<S> Wb, Mb;
+  load_state<S>(Wb, a.d_w_out ? a.d_w_out + u * a.P : nullptr, dh, w, g, c);
+  load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, w, g, c);
+
+  for (int r = NC - 1; r >= 0; --r) {
+    const int s0 = r * C;
+    const int len = min(C, T - s0);
+    const long row0 = u * T + s0;
+    const char* ckW = static_cast<const char*>(a.ckpt) + (u * NC + r) * 2 * a.ckpt_stride;
+    const char* ckM = ckW + a.ckpt_stride;
+
+    // ------------------------------------------------------------ P0: stage
+    E* xv = reinterpret_cast<E*>(rr);
+    stage_tile<S>(xk, a.k, row0, len, tid);
+    stage_tile<S>(xv, a.v, row0, len, tid);
+#pragma unroll 1
+    for (int t = tid; t < S::CM; t += S::NT) {
+      skw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
+      skm[t] = (t < len) ? a.km[row0 + t] : 0.0f;
+    }
+    if (tid < 3) scar[tid] = a.carry[(u * NC + r) * 3 + tid];
+    __syncthreads();
+
+    // -------------------------------------- P1: H = K W1^T, A = act(H) (recompute)
+    f32x4 Hk[NF][NTB][NJB];
+    Q Akq[NTB][NJB];
+    {
+      Q w1q[NF][NJB][NIB];
+#pragma unroll
+      for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj) {
+          f32x4 acc[NF];
+#pragma unroll
+          for (int m = 0; m < NF; ++m) acc[m] = zero4();
+#pragma unroll
+          for (int p = 0; p < S::KS_D; ++p) {
+            auto af = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
+#pragma unroll
+            for (int m = 0; m < NF; ++m) {
+              typename O::Frag bf;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) bf.h[h] = w1q[m][jj][S::NH * p + h];
+              acc[m] = O::mma(acc[m], af, bf);
+            }
+          }
+          f32x4 act;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if constexpr (!SW) act[q] = gelu_f(acc[0][q]);
+            else act[q] = silu_f(acc[0][q]) * acc[1][q];
+          }
+#pragma unroll
+          for (int m = 0; m < NF; ++m) Hk[m][tb][jj] = acc[m];
+          Akq[tb][jj] = O::cvt(act);
+          sched_fence();
+        }
+    }
+    // Y = A W2^T through one j-round (into yk, fp32)
+    {
+      JAcc<S> yacc;
+      yacc.zero();
+      Q w2q[NJB][NIB];
+      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+      jround<S>(yacc, nullptr, ja, jw,
+                [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+                [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
+      constexpr int NI = NIB / S::IBB;
+#pragma unroll
+      for (int aa = 0; aa < L::JIT; ++aa) {
+        const int it = w + aa * NW;
+        if (it < L::NITEM) {
+          const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll
+          for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              yk[(16 * tb + 4 * g + q) * D + 16 * (ib0 + b) + c] = yacc.v[aa][b][q];
+        }
+      }
+    }
+    __syncthreads();
+
+    // ------------------------------- P3: LN, e, dY (first-order, recomputed)
+    E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
+#pragma unroll 1
+    for (int t = w; t < S::CM; t += NW) {
+      const bool on = lane < D;
+      const float yv = on ? yk[t * D + lane] : 0.0f;
+      const float kx = on ? O::from_e(xk[t * S::LDD + lane]) : 0.0f;
+      const float vx = on ? O::from_e(xv[t * S::LDD + lane]) : 0.0f;
+      float z = 0.0f, e, dyv, sig = 1.0f, mez = 0.0f;
+      if (resln) {
+        const float mu = wave_sum(yv) * inv_d;
+        const float yc = on ? yv - mu : 0.0f;
+        const float var = wave_sum(yc * yc) * inv_d;
+        sig = sqrtf(var + a.eps);
+        z = yc / sig;
+        e = on ? vx - kx - z : 0.0f;
+        const float me = wave_sum(e) * inv_d;
+        mez = wave_sum(e * z) * inv_d;
+        dyv = (e - me - z * mez) / sig;
+      } else {
+        e = on ? vx - yv : 0.0f;
+        dyv = e;
+      }
+      if (on) {
+        yk[t * D + lane] = z;
+        ek[t * D + lane] = e;
+        dyl[t * S::LDD + lane] = O::to_e(dyv);
+        dyt[lane * S::LDC + t] = O::to_e(dyv);
+      }
+      if (lane == 0) { row[2 * t] = sig; row[2 * t + 1] = mez; }
+    }
+    __syncthreads();
+
+    // ------------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
+    // For every tile: dA = dY W2, dH = dA act'(H);  u = K Wb1^T, K Mb1^T;
+    // rW = dY Wb2, dY Mb2;  dK^W += rowsum(dH uW + A rW), dK^M likewise;
+    // p = K^W uW + K^M uM (= d(Phi)/d(dH)), r2 = K^W rW + K^M rM (direct a-term);
+    // dAh = p act'(H);  Hh = p dA act''(H) + r2 act'(H)  (the Yh W2 term is added later)
+    Q dHq[NF][NTB][NJB];
+    Q dAhq[NTB][NJB];
+    f32x4 Hh[NF][NTB][NJB];
+    {
+      float kwp[NTB][4], kmp[NTB][4];   // row partial sums for dK^W, dK^M
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) { kwp[tb][q] = 0.0f; kmp[tb][q] = 0.0f; }
+      Q w2q[NJB][NIB];
+      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+      opaque_state<S>(Wb);
+      opaque_state<S>(Mb);
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj) {
+          f32x4 dA = zero4(), rW = zero4(), rM = zero4();
+          f32x4 uW[NF], uM[NF];
+#pragma unroll
+          for (int m = 0; m < NF; ++m) { uW[m] = zero4(); uM[m] = zero4(); }
+#pragma unroll
+          for (int p = 0; p < S::KS_D; ++p) {
+            auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
+            auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
+            typename O::Frag b2, bw, bm;
+#pragma unroll
+            for (int h = 0; h < S::NH; ++h) {
+              b2.h[h] = w2q[jj][S::NH * p + h];
+              bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
+              bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
+            }
+            dA = O::mma(dA, fy, b2);
+            rW = O::mma(rW, fy, bw);
+            rM = O::mma(rM, fy, bm);
+#pragma unroll
+            for (int m = 0; m < NF; ++m) {
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) {
+                bw.h[h] = O::cvt(Wb.t[m][jj][S::NH * p + h]);
+                bm.h[h] = O::cvt(Mb.t[m][jj][S::NH * p + h]);
+              }
+              uW[m] = O::mma(uW[m], fk, bw);
+              uM[m] = O::mma(uM[m], fk, bm);
+            }
+          }
+          const f32x4 Af = quad_f32(Akq[tb][jj]);
+          f32x4 dH[NF], dAh, hh[NF];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int t = 16 * tb + 4 * g + q;
+            const float kwv = skw[t], kmv = skm[t];
+            const float r2 = kwv * rW[q] + kmv * rM[q];
+            if constexpr (!SW) {
+              const float h = Hk[0][tb][jj][q];
+              const float d1 = gelu_d1(h), d2 = gelu_d2(h);
+              dH[0][q] = dA[q] * d1;
+              const float pp = kwv * uW[0][q] + kmv * uM[0][q];
+              dAh[q] = pp * d1;
+              hh[0][q] = pp * dA[q] * d2 + r2 * d1;
+              kwp[tb][q] += dH[0][q] * uW[0][q] + Af[q] * rW[q];
+              kmp[tb][q] += dH[0][q] * uM[0][q] + Af[q] * rM[q];
+            } else {
+              const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
+              const float sg = silu_f(hg), s1 = silu_d1(hg), s2 = silu_d2(hg);
+              dH[0][q] = dA[q] * hu * s1;
+              dH[1][q] = dA[q] * sg;
+              const float pg = kwv * uW[0][q] + kmv * uM[0][q];
+              const float pu = kwv * uW[1][q] + kmv * uM[1][q];
+              dAh[q] = pg * hu * s1 + pu * sg;
+              hh[0][q] = pg * dA[q] * hu * s2 + pu * dA[q] * s1 + r2 * hu * s1;
+              hh[1][q] = pg * dA[q] * s1 + r2 * sg;
+              kwp[tb][q] += dH[0][q] * uW[0][q] + dH[1][q] * uW[1][q] + Af[q] * rW[q];
+              kmp[tb][q] += dH[0][q] * uM[0][q] + dH[1][q] * uM[1][q] + Af[q] * rM[q];
+            }
+          }
+#pragma unroll
+          for (int m = 0; m < NF; ++m) { dHq[m][tb][jj] = O::cvt(dH[m]); Hh[m][tb][jj] = hh[m]; }
+          dAhq[tb][jj] = O::cvt(dAh);
+          sched_fence();
+        }
+      // per-wave row partials of dK^W, dK^M
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float sw = group16_sum(kwp[tb][q]);
+          const float sm2 = group16_sum(kmp[tb][q]);
+          if (c == 0) {
+            kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sw;
+            kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sm2;
+          }
+        }
+      // carry adjoints: <Wb, W_0>, <Wb, M_0>, <Mb, M_0>
+      float pcw = 0.0f, pcm = 0.0f, pcb = 0.0f;
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m) {
+        Q q0[NJB][NIB], qm[NJB][NIB];
+        load_ckpt_mat<S>(q0, ckW, m, w, lane);
+        load_ckpt_mat<S>(qm, ckM, m, w, lane);
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+          for (int ib = 0; ib < NIB; ++ib) {
+            const f32x4 w0 = quad_f32(q0[jj][ib]), m0 = quad_f32(qm[jj][ib]);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              pcw += Wb.t[m][jj][ib][q] * w0[q];
+              pcm += Wb.t[m][jj][ib][q] * m0[q];
+              pcb += Mb.t[m][jj][ib][q] * m0[q];
+            }
+          }
+      }
+      pcw = wave_sum(pcw);
+      pcm = wave_sum(pcm);
+      pcb = wave_sum(pcb);
+      if (lane == 0) { cbp[w * 4 + 0] = pcw; cbp[w * 4 + 1] = pcm; cbp[w * 4 + 2] = pcb; }
+    }
+    // direct terms through the state adjoint, over the hidden index:
+    //   r1 = K^W (dH Wb1) + K^M (dH Mb1)  (into dK),  p2 = K^W (A Wb2^T) + K^M (A Mb2^T)  (into dYh)
+    JAcc<S> dkacc, dyhacc;
+    dkacc.zero();
+    dyhacc.zero();
+#pragma unroll
+    for (int m = 0; m < NF; ++m) {
+      jround<S>(dkacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
+                [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
+      jround<S>(dkacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
+                [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+    }
+    jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+              [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
+    jround<S>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+              [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+
+    // ------------------------------------ P5: adjoint state transition
+    {
+      const float cw = scar[0], cm = scar[1], cbv = scar[2];
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+          for (int ib = 0; ib < NIB; ++ib) {
+            const f32x4 wb = Wb.t[m][jj][ib];
+            Mb.t[m][jj][ib] = cm * wb + cbv * Mb.t[m][jj][ib];
+            Wb.t[m][jj][ib] = cw * wb;
+          }
+    }
+
+    // --------------------------- P6: dYh = p2 + dAh W2^T  (into RR, fp32)
+    {
+      Q w2q[NJB][NIB];
+      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+      jround<S>(dyhacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(dAhq[tb][jj]); },
+                [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
+      float* dyh = reinterpret_cast<float*>(rr);
+      constexpr int NI = NIB / S::IBB;
+#pragma unroll
+      for (int aa = 0; aa < L::JIT; ++aa) {
+        const int it = w + aa * NW;
+        if (it < L::NITEM) {
+          const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll
+          for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              dyh[(16 * tb + 4 * g + q) * D + 16 * (ib0 + b) + c] = dyhacc.v[aa][b][q];
+        }
+      }
+    }
+    __syncthreads();
+
+    // ------------------------------------- P7: LayerNorm second order
+    {
+      const float* dyh = reinterpret_cast<const float*>(rr);
+      using IOT = typename IoT<S::BF>::T;
+      IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
+#pragma unroll 1
+      for (int t = w; t < S::CM; t += NW) {
+        const bool on = lane < D;
+        const float dyhv = on ? dyh[t * D + lane] : 0.0f;
+        const float e = on ? ek[t * D + lane] : 0.0f;
+        float eh, yhv;
+        if (resln) {
+          const float z = on ? yk[t * D + lane] : 0.0f;
+          const float sig = row[2 * t], mez = row[2 * t + 1];
+          const float me = wave_sum(e) * inv_d;
+          const float dyv = on ? (e - me - z * mez) / sig : 0.0f;
+          const float m1 = wave_sum(dyhv) * inv_d;
+          const float m2 = wave_sum(dyhv * z) * inv_d;
+          eh = on ? (dyhv - m1 - z * m2) / sig : 0.0f;
+          const float sh = -wave_sum(dyhv * dyv) / sig;
+          const float zh = on ? -(dyhv * mez + e * m2) / sig - eh : 0.0f;
+          const float n1 = wave_sum(zh) * inv_d;
+          const float n2 = wave_sum(zh * z) * inv_d;
+          yhv = on ? (zh - n1 - z * n2) / sig + sh * z * inv_d : 0.0f;
+        } else {
+          eh = dyhv;
+          yhv = -eh;
+        }
+        if (on) {
+          ek[t * D + lane] = eh;
+          yh[t * S::LDD + lane] = O::to_e(yhv);
+          yht[lane * S::LDC + t] = O::to_e(yhv);
+          if (t < len) IoT<S::BF>::st(dvp + (long)t * D + lane, eh);
+        }
+      }
+    }
+    __syncthreads();
+
+    // ------------ P8: Hh += (Yh W2) act'(H); accumulate into Wb; dk = r1 - eh + Hh W1
+    {
+      // K^T into RR for the first-layer accumulation
+      E* xkt = reinterpret_cast<E*>(rr);
+#pragma unroll 1
+      for (int idx = tid; idx < D * S::CM; idx += S::NT) {
+        const int i = idx % D, t = idx / D;
+        xkt[i * S::LDC + t] = xk[t * S::LDD + i];
+      }
+      Q w2q[NJB][NIB];
+      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj) {
+          f32x4 ah = zero4();
+#pragma unroll
+          for (int p = 0; p < S::KS_D; ++p) {
+            auto af = lds_frag<S::BF>(yh, S::LDD, 16 * tb + c, p * S::KC, g);
+            typename O::Frag bf;
+#pragma unroll
+            for (int h = 0; h < S::NH; ++h) bf.h[h] = w2q[jj][S::NH * p + h];
+            ah = O::mma(ah, af, bf);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if constexpr (!SW) {
+              Hh[0][tb][jj][q] += ah[q] * gelu_d1(Hk[0][tb][jj][q]);
+            } else {
+              const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
+              Hh[0][tb][jj][q] += ah[q] * hu * silu_d1(hg);
+              Hh[1][tb][jj][q] += ah[q] * silu_f(hg);
+            }
+          }
+          sched_fence();
+        }
+      __syncthreads();   // xkt complete
+      // Wb2 += dY^T dAh + Yh^T A ;  Wb1 += K^T Hh
+      opaque_state<S>(Wb);
+#pragma unroll
+      for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+          for (int p = 0; p < S::KS_C; ++p) {
+            typename O::Frag bd, ba;
+#pragma unroll
+            for (int h = 0; h < S::NH; ++h) {
+              bd.h[h] = dAhq[S::NH * p + h][jj];
+              ba.h[h] = Akq[S::NH * p + h][jj];
+            }
+            const int rowi = 16 * ib + c, k0 = p * S::KC;
+            Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(dyt, S::LDC, rowi, k0, g), bd);
+            Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(yht, S::LDC, rowi, k0, g), ba);
+            auto fk = lds_frag<S::BF>(xkt, S::LDC, rowi, k0, g);
+#pragma unroll
+            for (int m = 0; m < NF; ++m) {
+              typename O::Frag bh;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) bh.h[h] = O::cvt(Hh[m][S::NH * p + h][jj]);
+              Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fk, bh);
+            }
+          }
+          sched_fence();
+        }
+      // dk += Hh W1 (over the hidden index)
+#pragma unroll
+      for (int m = 0; m < NF; ++m) {
+        Q w1q[NJB][NIB];
+        load_ckpt_mat<S>(w1q, ckW, m, w, lane);
+        jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return Hh[m][tb][jj]; },
+                  [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
+      }
+      const float ksign = resln ? -1.0f : 0.0f;
+      jacc_store_io<S>(dkacc, a.dk, row0, len,
+                       [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
+    }
+    __syncthreads();
+
+    // -------------------------------------------- P9: output branch
+    {
+      E* xq = xk;                                      // Q [t][i]
+      E* xdo = reinterpret_cast<E*>(rr);               // dO [t][i]
+      E* ybq = yh;                                     // Yb_Q [t][i]
+      E* ybqt = dyt;                                   // Yb_Q^T [i][t]
+      E* xqt = yht;                                    // Q^T [i][t]
+      stage_tile<S>(xq, a.q, row0, len, tid);
+      stage_tile<S>(xdo, a.d_out, row0, len, tid);
+      __syncthreads();
+#pragma unroll 1
+      for (int idx = tid; idx < D * S::CM; idx += S::NT) {
+        const int i = idx % D, t = idx / D;
+        xqt[i * S::LDC + t] = xq[t * S::LDD + i];
+      }
+      f32x4 Hq[NF][NTB][NJB];
+      Q Aqq[NTB][NJB];
+      {
+        Q w1q[NF][NJB][NIB];
+#pragma unroll
+        for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            f32x4 acc[NF];
+#pragma unroll
+            for (int m = 0; m < NF; ++m) acc[m] = zero4();
+#pragma unroll
+            for (int p = 0; p < S::KS_D; ++p) {
+              auto af = lds_frag<S::BF>(xq, S::LDD, 16 * tb + c, p * S::KC, g);
+#pragma unroll
+              for (int m = 0; m < NF; ++m) {
+                typename O::Frag bf;
+#pragma unroll
+                for (int h = 0; h < S::NH; ++h) bf.h[h] = w1q[m][jj][S::NH * p + h];
+                acc[m] = O::mma(acc[m], af, bf);
+              }
+            }
+            f32x4 act;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              if constexpr (!SW) act[q] = gelu_f(acc[0][q]);
+              else act[q] = silu_f(acc[0][q]) * acc[1][q];
+            }
+#pragma unroll
+            for (int m = 0; m < NF; ++m) Hq[m][tb][jj] = acc[m];
+            Aqq[tb][jj] = O::cvt(act);
+            sched_fence();
+          }
+      }
+      {
+        JAcc<S> yacc;
+        yacc.zero();
+        Q w2q[NJB][NIB];
+        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+        jround<S>(yacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(Aqq[tb][jj]); },
+                  [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
+        constexpr int NI = NIB / S::IBB;
+#pragma unroll
+        for (int aa = 0; aa < L::JIT; ++aa) {
+          const int it = w + aa * NW;
+          if (it < L::NITEM) {
+            const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll
+            for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                yk[(16 * tb + 4 * g + q) * D + 16 * (ib0 + b) + c] = yacc.v[aa][b][q];
+          }
+        }
+      }
+      __syncthreads();
+      // Yb_Q = LN backward of dO at the Q rows (dO itself when there is no LN)
+#pragma unroll 1
+      for (int t = w; t < S::CM; t += NW) {
+        const bool on = lane < D;
+        const float dov = on ? O::from_e(xdo[t * S::LDD + lane]) : 0.0f;
+        float yb;
+        if (resln) {
+          const float yv = on ? yk[t * D + lane] : 0.0f;
+          const float mu = wave_sum(yv) * inv_d;
+          const float yc = on ? yv - mu : 0.0f;
+          const float var = wave_sum(yc * yc) * inv_d;
+          const float sig = sqrtf(var + a.eps);
+          const float z = yc / sig;
+          const float m1 = wave_sum(dov) * inv_d;
+          const float m2 = wave_sum(dov * z) * inv_d;
+          yb = on ? (dov - m1 - z * m2) / sig : 0.0f;
+        } else {
+          yb = dov;
+        }
+        if (on) {
+          ybq[t * S::LDD + lane] = O::to_e(yb);
+          ybqt[lane * S::LDC + t] = O::to_e(yb);
+        }
+      }
+      __syncthreads();
+      // Ab_Q = Yb_Q W2;  Hb_Q = Ab_Q act'(H_Q);  Wb2 += Yb_Q^T A_Q;  Wb1 += Q^T Hb_Q
+      Q Hbq[NF][NTB][NJB];
+      {
+        Q w2q[NJB][NIB];
+        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            f32x4 ab = zero4();
+#pragma unroll
+            for (int p = 0; p < S::KS_D; ++p) {
+              auto af = lds_frag<S::BF>(ybq, S::LDD, 16 * tb + c, p * S::KC, g);
+              typename O::Frag bf;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) bf.h[h] = w2q[jj][S::NH * p + h];
+              ab = O::mma(ab, af, bf);
+            }
+            f32x4 hb[NF];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              if constexpr (!SW) {
+                hb[0][q] = ab[q] * gelu_d1(Hq[0][tb][jj][q]);
+              } else {
+                const float hg = Hq[0][tb][jj][q], hu = Hq[1][tb][jj][q];
+                hb[0][q] = ab[q] * hu * silu_d1(hg);
+                hb[1][q] = ab[q] * silu_f(hg);
+              }
+            }
+#pragma unroll
+            for (int m = 0; m < NF; ++m) Hbq[m][tb][jj] = O::cvt(hb[m]);
+            sched_fence();
+          }
+      }
+      opaque_state<S>(Wb);
+#pragma unroll
+      for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+          for (int p = 0; p < S::KS_C; ++p) {
+            typename O::Frag ba;
+#pragma unroll
+            for (int h = 0; h < S::NH; ++h) ba.h[h] = Aqq[S::NH * p + h][jj];
+            const int rowi = 16 * ib + c, k0 = p * S::KC;
+            Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(ybqt, S::LDC, rowi, k0, g), ba);
+            auto fq = lds_frag<S::BF>(xqt, S::LDC, rowi, k0, g);
+#pragma unroll
+            for (int m = 0; m < NF; ++m) {
+              typename O::Frag bh;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) bh.h[h] = Hbq[m][S::NH * p + h][jj];
+              Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fq, bh);
+            }
+          }
+          sched_fence();
+        }
+      // dq = dO (residual) + Hb_Q W1 (over the hidden index)
+      JAcc<S> dqacc;
+      dqacc.zero();
+#pragma unroll
+      for (int m = 0; m < NF; ++m) {
+        Q w1q[NJB][NIB];
+        load_ckpt_mat<S>(w1q, ckW, m, w, lane);
+        jround<S>(dqacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(Hbq[m][tb][jj]); },
+                  [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
+      }
+      const float qsign = resln ? 1.0f : 0.0f;
+      jacc_store_io<S>(dqacc, a.dq, row0, len,
+                       [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); }, w, g,
+                       c);
+    }
+
+    // ------------------------------ P10: scalar-kernel adjoints of this chunk
+#pragma unroll 1
+    for (int t = tid; t < len; t += S::NT) {
+      float sw = 0.0f, sm2 = 0.0f;
+      for (int ww = 0; ww < NW; ++ww) {
+        sw += kb[(0 * NW + ww) * S::CM + t];
+        sm2 += kb[(1 * NW + ww) * S::CM + t];
+      }
+      a.kwb[row0 + t] = sw;
+      a.kmb[row0 + t] = sm2;
+    }
+    if (tid < 3) {
+      float s = 0.0f;
+      for (int ww = 0; ww < NW; ++ww) s += cbp[ww * 4 + tid];
+      a.carryb[(u * NC + r) * 3 + tid] = s;
+    }
+    __syncthreads();
+  }
+
+  store_state<S>(Wb, a.d_w_in + u * a.P, dh, w, g, c);
+  store_state<S>(Mb, a.d_m_in + u * a.P, dh, w, g, c);
+}
+
+template <class S>
+hipError_t launch(const ChainArgs& a, long units, hipStream_t stream) {
+  hipLaunchKernelGGL(chain_bwd_kernel<S>, dim3((unsigned)units), dim3(S::NT), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF)                                              \
+  if (cfg.fw == FW && cfg.d == D && cfg.nw == NW && cfg.njb == NJB && cfg.ntb == NTB && \
+      cfg.bf == BF)                                                                     \
+    return launch<Shape<FW, D, NW, NJB, NTB, BF>>(a, units, stream);
+
+hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, long units,
+                            hipStream_t stream) {
+#include "chain_variants.inc"
   return hipErrorInvalidValue;
 }
+#undef E2TTT_CASE
+
 }  // namespace e2ttt

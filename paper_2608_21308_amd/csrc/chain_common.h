@@ -113,35 +113,38 @@ __device__ __forceinline__ void store_state(StateTiles<S>& st, float* dst, int d
   state_io<S, true>(st, nullptr, dst, dh, w, g, c);
 }
 
-// Checkpoint blocks hold bf16 state in register order: element
-// ((((m NJB + jj) NIB + ib) NW + w) 64 + lane) 4 + r, so that writes and reads
-// are 8-byte per lane and fully coalesced.
+// Checkpoint blocks hold the chunk-start state in the operand precision
+// (bf16 on the bf16 path, fp32 on the fp32 path) and in register order: quad
+// ((m NJB + jj) NIB + ib) NW 64 + w 64 + lane, so that writes and reads are
+// one 8- or 16-byte access per lane and fully coalesced.
 template <class S>
-__device__ __forceinline__ void store_ckpt(const StateTiles<S>& st, uint16_t* dst, int w,
-                                           int lane) {
-  bf16x4* lp = reinterpret_cast<bf16x4*>(dst) + opaque_lane(w * 64 + lane);
+__device__ __forceinline__ void store_ckpt(const StateTiles<S>& st, void* dst, int w, int lane) {
+  using Q = typename S::O::Q;
+  Q* lp = reinterpret_cast<Q*>(dst) + opaque_lane(w * 64 + lane);
 #pragma unroll
   for (int m = 0; m < S::NMAT; ++m)
 #pragma unroll
     for (int jj = 0; jj < S::NJB; ++jj)
 #pragma unroll
       for (int ib = 0; ib < S::NIB; ++ib)
-        lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64] = OpT<true>::cvt(st.t[m][jj][ib]);
+        lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64] = S::O::cvt(st.t[m][jj][ib]);
 }
 
+// Quads of matrix m of a checkpoint block, for this lane.
 template <class S>
-__device__ __forceinline__ void load_ckpt(StateTiles<S>& st, const uint16_t* src, int w,
-                                          int lane) {
-  const bf16x4* lp = reinterpret_cast<const bf16x4*>(src) + opaque_lane(w * 64 + lane);
+__device__ __forceinline__ void load_ckpt_mat(typename S::O::Q (&q)[S::NJB][S::NIB],
+                                              const void* src, int m, int w, int lane) {
+  using Q = typename S::O::Q;
+  const Q* lp = reinterpret_cast<const Q*>(src) + opaque_lane(w * 64 + lane);
 #pragma unroll
-  for (int m = 0; m < S::NMAT; ++m)
+  for (int jj = 0; jj < S::NJB; ++jj)
 #pragma unroll
-    for (int jj = 0; jj < S::NJB; ++jj)
-#pragma unroll
-      for (int ib = 0; ib < S::NIB; ++ib) {
-        const bf16x4 b = lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64];
-        st.t[m][jj][ib] = f32x4{(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
-      }
+    for (int ib = 0; ib < S::NIB; ++ib) q[jj][ib] = lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64];
+}
+
+template <class Q>
+__device__ __forceinline__ f32x4 quad_f32(const Q& q) {
+  return f32x4{(float)q[0], (float)q[1], (float)q[2], (float)q[3]};
 }
 
 // Operand fragment whose contraction index is the tile ROW of `tiles`

@@ -79,7 +79,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
     }
     if (tid < 3) sm.carry[tid] = a.carry[(u * NC + r) * 3 + tid];
     if (a.ckpt) {
-      uint16_t* cb = a.ckpt + (u * NC + r) * 2 * a.ckpt_stride;
+      char* cb = static_cast<char*>(a.ckpt) + (u * NC + r) * 2 * a.ckpt_stride;
       store_ckpt<S>(W, cb, w, lane);
       store_ckpt<S>(M, cb + a.ckpt_stride, w, lane);
     }
@@ -318,8 +318,8 @@ hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, long uni
 }  // namespace e2ttt
 
 namespace e2ttt {
-long chain_ckpt_elems(const ChainConfig& cfg) {
+long chain_ckpt_bytes(const ChainConfig& cfg) {
   const long nmat = (cfg.fw == 0) ? 2 : 3;
-  return nmat * 16L * cfg.nw * cfg.njb * cfg.d;
+  return nmat * 16L * cfg.nw * cfg.njb * cfg.d * (cfg.bf ? 2 : 4);
 }
 }  // namespace e2ttt

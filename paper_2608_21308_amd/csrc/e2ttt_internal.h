@@ -58,9 +58,10 @@ struct ChainArgs {
   float* kwb;           // [U][T] adjoint of K^W (written by the backward chain)
   float* kmb;
   float* carryb;        // [U][NC][3]
-  // chunk-start checkpoints (bf16, kernel register order), nullable in forward
-  uint16_t* ckpt;
-  long ckpt_stride;     // elements per (unit, chunk, W-or-M) block
+  // chunk-start checkpoints (operand precision, kernel register order),
+  // nullable in the forward
+  void* ckpt;
+  long ckpt_stride;     // bytes per (unit, chunk, W-or-M) block
   int T, C, NC, dh;
   long P;               // parameters per unit (unpadded)
   int resln;            // 1: f = x + LN(y); 0: f = y
@@ -84,7 +85,7 @@ hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, long uni
                             hipStream_t stream);
 hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, long units,
                             hipStream_t stream);
-// Elements of one checkpoint block (W or M of one unit at one chunk start).
-long chain_ckpt_elems(const ChainConfig& cfg);
+// Bytes of one checkpoint block (W or M of one unit at one chunk start).
+long chain_ckpt_bytes(const ChainConfig& cfg);
 
 }  // namespace e2ttt

@@ -1,0 +1,207 @@
+"""GPU parity of the backward path (e2ttt_chunk_backward) against the fp64
+oracle's reverse-mode token loop, on identical seeded inputs.
+
+The loss is sum<d_out, out> + <d_w_out, w_out> + <d_m_out, m_out>; every
+gradient (q, k, v, eta, beta, gamma, w_in, m_in) is compared by rel-L2:
+1e-5 for fp32 io, 2e-2 for bf16 io.  Long fp32 runs and the chaotic SwiGLU +
+residual-LN workloads are handled as in the forward tests (short fp32 runs;
+chunk windows from the oracle's own state with a condition-aware bound).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2608_21308_amd import e2ttt, workloads as WL
+from tests.gpu_util import TOL, config_of, rel_l2, slice_tokens, to_dev
+
+pytestmark = pytest.mark.gpu
+
+GRADS = ("dq", "dk", "dv", "d_eta", "d_beta", "d_gamma", "d_w_in", "d_m_in")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    e2ttt.load()
+
+
+def gpu_fwd_bwd(w, x, flags=0):
+    cfg = config_of(w, flags=flags)
+    t = to_dev(x, w.io)
+    out, wo, mo, ws = e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                                    t["w_in"], t.get("m_in"), save_for_backward=True)
+    g = e2ttt.backward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"], t["w_in"],
+                       t.get("m_in"), ws, t["d_out"], t.get("d_w_out"), t.get("d_m_out"))
+    torch.cuda.synchronize()
+    return g
+
+
+def oracle_bwd(w, x, flags=0):
+    return oracle.backward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"], x["w_in"],
+                           x.get("m_in"), x["d_out"], x.get("d_w_out"), x.get("d_m_out"), C=w.C,
+                           fw=w.fw, dh=w.dh, flags=flags)
+
+
+def errors(g, ref, units=None):
+    errs = {}
+    for n in GRADS:
+        if ref.get(n) is None:
+            assert g.get(n) is None
+            continue
+        a = g[n]
+        if units is not None:
+            a = a.reshape((-1,) + tuple(a.shape[2:]))[units][None]
+        errs[n] = rel_l2(a, ref[n])
+    return errs
+
+
+def assert_tol(errs, io, what):
+    tol = TOL[io]
+    print(what, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, "%s rel-L2 above %g: %s" % (what, tol, bad)
+
+
+def with_state_inputs(x, seed, m_scale=1e-3, with_state_grads=True):
+    rng = np.random.default_rng(seed)
+    P = x["w_in"].shape[-1]
+    x = dict(x)
+    x["m_in"] = (m_scale * rng.standard_normal(x["w_in"].shape)).astype(np.float32)
+    if with_state_grads:
+        x["d_w_out"] = rng.standard_normal(x["w_in"].shape).astype(np.float32)
+        x["d_m_out"] = rng.standard_normal(x["w_in"].shape).astype(np.float32)
+    return x
+
+
+# ------------------------------------------------------------ fp32 path
+@pytest.mark.parametrize("fw", [WL.FW_MLP, WL.FW_SWIGLU])
+@pytest.mark.parametrize("T,C,dh,flags", [(32, 16, 64, 0), (20, 16, 64, 0), (12, 7, 50, 0),
+                                          (3, 1, 64, 0), (32, 16, 128, 0), (64, 64, 64, 0),
+                                          (128, 16, 64, 1), (75, 7, 100, 1)])
+def test_backward_fp32_shapes(fw, T, C, dh, flags):
+    w = WL.WORKLOADS[0].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, backward=True,
+                              seed=700 + T + C + dh)
+    x = with_state_inputs(WL.make_inputs(w), 11 + T)
+    g = gpu_fwd_bwd(w, x, flags)
+    errs = errors(g, oracle_bwd(w, x, flags))
+    assert_tol(errs, "f32", "bwd fp32 fw=%d T=%d C=%d dh=%d flags=%d" % (fw, T, C, dh, flags))
+
+
+def test_backward_tiny_fp32_workload():
+    w = WL.WORKLOADS[0].with_(backward=True)
+    x = WL.make_inputs(w)
+    g = gpu_fwd_bwd(w, x)
+    assert_tol(errors(g, oracle_bwd(w, x)), "f32", "bwd " + w.name)
+
+
+def test_backward_without_gamma():
+    w = WL.WORKLOADS[0].with_(B=1, H=2, T=40, C=16, backward=True)
+    x = WL.make_inputs(w)
+    x["gamma"] = None
+    g = gpu_fwd_bwd(w, x)
+    assert g["d_gamma"] is None
+    assert_tol(errors(g, oracle_bwd(w, x)), "f32", "bwd gamma=None")
+
+
+# ------------------------------------------------------------ bf16 path
+@pytest.mark.parametrize("T,C,dh,fw,flags", [(200, 64, 256, 0, 0), (130, 32, 256, 0, 0),
+                                             (96, 16, 64, 0, 0), (256, 64, 120, 0, 0),
+                                             (300, 64, 172, 1, 1), (192, 48, 100, 1, 1)])
+def test_backward_bf16_shapes(T, C, dh, fw, flags):
+    w = WL.WORKLOADS[1].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, backward=True, seed=300 + T + dh)
+    x = with_state_inputs(WL.make_inputs(w), T, m_scale=1e-2)
+    g = gpu_fwd_bwd(w, x, flags)
+    assert_tol(errors(g, oracle_bwd(w, x, flags)), "bf16",
+               "bwd bf16 T=%d C=%d dh=%d fw=%d flags=%d" % (T, C, dh, fw, flags))
+
+
+def test_backward_1p3b_layer_sampled_units():
+    # the headline training shape: full launch, oracle on a sample of units
+    w = WL.WORKLOADS[3]
+    x = WL.make_inputs(w)
+    g = gpu_fwd_bwd(w, x)
+    units = [0, 93]
+    xs = WL.make_inputs(w, units=units)
+    ref = oracle_bwd(w, xs)
+    assert_tol(errors(g, ref, units), "bf16", "bwd " + w.name)
+    for n in GRADS:
+        assert torch.isfinite(g[n].float()).all(), n
+
+
+def test_backward_swiglu_literal_net_workload():
+    w = WL.WORKLOADS[2]
+    x = WL.make_inputs(w)
+    g = gpu_fwd_bwd(w, x, flags=e2ttt.FLAG_NO_RESIDUAL_LN)
+    assert_tol(errors(g, oracle_bwd(w, x, flags=e2ttt.FLAG_NO_RESIDUAL_LN)), "bf16",
+               "bwd %s (bare net)" % w.name)
+
+
+@pytest.mark.parametrize("starts", [[0, 1, 3, 8, 17, 24, 31]])
+def test_backward_swiglu_ln_chunk_windows(starts):
+    # one chunk at a time from the oracle's chunk-start state, with random
+    # state adjoints d_w_out, d_m_out as the downstream gradient
+    w = WL.WORKLOADS[2]
+    x = WL.make_inputs(w)
+    strict = 0
+    for r in starts:
+        if r == 0:
+            W0, M0 = x["w_in"], None
+        else:
+            y = slice_tokens(x, 0, r * w.C)
+            _, W0, M0 = oracle.forward(y["q"], y["k"], y["v"], y["eta"], y["beta"], y["gamma"],
+                                       y["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
+        y = slice_tokens(x, r * w.C, (r + 1) * w.C)
+        y["w_in"] = np.ascontiguousarray(W0, dtype=np.float32)
+        y["m_in"] = None if M0 is None else np.ascontiguousarray(M0, dtype=np.float32)
+        rng = np.random.default_rng(r)
+        y["d_w_out"] = (0.1 * rng.standard_normal(W0.shape)).astype(np.float32)
+        y["d_m_out"] = (0.1 * rng.standard_normal(W0.shape)).astype(np.float32)
+        wu = w.with_(T=w.C)
+        g = gpu_fwd_bwd(wu, y)
+        ref = oracle_bwd(wu, y)
+        errs = errors(g, ref)
+        yb = dict(y)
+        yb["w_in"] = WL.round_bf16(y["w_in"])
+        yb["m_in"] = None if y["m_in"] is None else WL.round_bf16(y["m_in"])
+        refb = oracle_bwd(wu, yb)
+        sens = {n: rel_l2(refb[n], ref[n]) for n in errs}
+        bound = {n: max(TOL["bf16"], 2 * sens[n]) for n in errs}
+        strict += all(v <= TOL["bf16"] / 4 for v in sens.values())
+        print("bwd %s chunk %d gpu %s sens %s" % (w.name, r,
+              {k: "%.1e" % v for k, v in errs.items()}, {k: "%.1e" % v for k, v in sens.items()}),
+              flush=True)
+        bad = {n: (errs[n], bound[n]) for n in errs if not errs[n] <= bound[n]}
+        assert not bad, "chunk %d: %s" % (r, bad)
+    assert strict >= 2, "too few well-conditioned windows to be a check"
+
+
+# ------------------------------------------------------------ properties
+def test_backward_deterministic_and_zero_seed():
+    w = WL.WORKLOADS[1].with_(B=2, H=2, T=256, backward=True)
+    x = WL.make_inputs(w)
+    g1 = gpu_fwd_bwd(w, x)
+    g2 = gpu_fwd_bwd(w, x)
+    for n in GRADS:
+        assert torch.equal(g1[n], g2[n]), n
+    x0 = dict(x)
+    x0["d_out"] = np.zeros_like(x["d_out"])
+    g0 = gpu_fwd_bwd(w, x0)
+    for n in GRADS:
+        assert torch.count_nonzero(g0[n]) == 0, n
+
+
+def test_autograd_function_matches_library():
+    w = WL.WORKLOADS[1].with_(B=1, H=2, T=128, backward=True)
+    x = WL.make_inputs(w)
+    cfg = config_of(w)
+    t = to_dev(x, "bf16")
+    leaves = {n: t[n].clone().requires_grad_(True) for n in ("q", "k", "v", "eta", "beta",
+                                                             "gamma", "w_in")}
+    out, wo, mo = e2ttt.E2TTTFunction.apply(cfg, leaves["q"], leaves["k"], leaves["v"],
+                                            leaves["eta"], leaves["beta"], leaves["gamma"],
+                                            leaves["w_in"], None)
+    (out.float() * t["d_out"].float()).sum().backward()
+    g = gpu_fwd_bwd(w, x)
+    for n, gn in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("eta", "d_eta"), ("w_in", "d_w_in")):
+        assert torch.equal(leaves[n].grad, g[gn]), n

@@ -192,7 +192,8 @@ def test_swiglu_ln_chunk_windows(cfg_idx, units, starts):
     # is 2e-2, widened only where the chunk itself is ill-conditioned: the
     # oracle is re-run from its state rounded to bf16 (one of the roundings
     # any bf16-operand implementation makes) and the GPU may deviate by at
-    # most 4x that intrinsic sensitivity.
+    # most 2x that intrinsic sensitivity.  Windows whose sensitivity is below
+    # tol/4 are thereby checked at the plain tolerance; at least two must be.
     w = WL.WORKLOADS[cfg_idx]
     x = WL.make_inputs(w, with_grads=False, units=units)
     wu = w.with_(B=x["q"].shape[0], H=x["q"].shape[1], T=w.C)
@@ -209,14 +210,14 @@ def test_swiglu_ln_chunk_windows(cfg_idx, units, starts):
         pb = oracle.forward(yb["q"], yb["k"], yb["v"], yb["eta"], yb["beta"], yb["gamma"],
                             yb["w_in"], mb, C=w.C, fw=w.fw, dh=w.dh)
         sens = {n: rel_l2(a, b) for n, a, b in zip(("out", "w_out", "m_out"), pb, ref)}
-        bound = {n: max(TOL["bf16"], 4 * sens[n]) for n in errs}
-        strict += all(b == TOL["bf16"] for b in bound.values())
+        bound = {n: max(TOL["bf16"], 2 * sens[n]) for n in errs}
+        strict += all(v <= TOL["bf16"] / 4 for v in sens.values())
         print("%s chunk %d gpu %s  bf16-state sensitivity %s" % (
             w.name, r, {k: "%.2e" % v for k, v in errs.items()},
             {k: "%.2e" % v for k, v in sens.items()}), flush=True)
         bad = {n: (errs[n], bound[n]) for n in errs if not errs[n] <= bound[n]}
         assert not bad, "chunk %d: %s" % (r, bad)
-    assert strict >= len(starts) // 2, "too few well-conditioned windows to be a check"
+    assert strict >= 2, "too few well-conditioned windows to be a check"
 
 
 # ------------------------------------------------------------ properties
