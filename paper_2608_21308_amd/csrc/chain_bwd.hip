@@ -56,7 +56,7 @@ struct BwdLayout {
   static constexpr int DYT = A16(RR + R1);       // dY^T [i][t]          | out branch: Yb_Q^T
   static constexpr int YH = A16(DYT + DT);       // Yh [t][i]            | out branch: Yb_Q
   static constexpr int YHT = A16(YH + TD);       // Yh^T [i][t]          | out branch: Q^T
-  static constexpr int ROW = A16(YHT + DT);      // per token: sigma, mean(e Z)
+  static constexpr int ROW = A16(YHT + DT);      // per token: 1/sigma, mean(e Z)
   static constexpr int KB = A16(ROW + S::CM * 8);          // dK^W, dK^M partials [2][NW][CM]
   static constexpr int CB = A16(KB + 2 * S::NW * S::CM * 4);  // carry adjoint partials [NW][4]
   static constexpr int SC = A16(CB + S::NW * 16);          // kw[CM], km[CM], carry[4]
@@ -305,34 +305,51 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 
     // ------------------------------- P3: LN, e, dY (first-order, recomputed)
     E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
+    constexpr int EPL = D / 16;                   // head elements per lane in row phases
+    const int l16 = lane & 15;
 #pragma unroll 1
-    for (int t = w; t < S::CM; t += NW) {
-      const bool on = lane < D;
-      const float yv = on ? yk[t * D + lane] : 0.0f;
-      const float kx = on ? O::from_e(xk[t * S::LDD + lane]) : 0.0f;
-      const float vx = on ? O::from_e(xv[t * S::LDD + lane]) : 0.0f;
-      float z = 0.0f, e, dyv, sig = 1.0f, mez = 0.0f;
+    for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+      const int t = t0 + (lane >> 4);
+      float yv[EPL], e[EPL], z[EPL], dyv[EPL];
+      float sig = 1.0f, mez = 0.0f, s1 = 0.0f;   // sig: 1 / sigma
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) { yv[q] = yk[t * D + l16 * EPL + q]; s1 += yv[q]; }
       if (resln) {
-        const float mu = wave_sum(yv) * inv_d;
-        const float yc = on ? yv - mu : 0.0f;
-        const float var = wave_sum(yc * yc) * inv_d;
-        sig = sqrtf(var + a.eps);
-        z = yc / sig;
-        e = on ? vx - kx - z : 0.0f;
-        const float me = wave_sum(e) * inv_d;
-        mez = wave_sum(e * z) * inv_d;
-        dyv = (e - me - z * mez) / sig;
+        const float mu = group16_sum(s1) * inv_d;
+        float s2 = 0.0f;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
+        sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+        float se = 0.0f, sez = 0.0f;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+          const int i = l16 * EPL + q;
+          z[q] = yv[q] * sig;
+          e[q] = O::from_e(xv[t * S::LDD + i]) - O::from_e(xk[t * S::LDD + i]) - z[q];
+          se += e[q];
+          sez += e[q] * z[q];
+        }
+        const float me = group16_sum(se) * inv_d;
+        mez = group16_sum(sez) * inv_d;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) dyv[q] = (e[q] - me - z[q] * mez) * sig;
       } else {
-        e = on ? vx - yv : 0.0f;
-        dyv = e;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+          z[q] = 0.0f;
+          e[q] = O::from_e(xv[t * S::LDD + l16 * EPL + q]) - yv[q];
+          dyv[q] = e[q];
+        }
       }
-      if (on) {
-        yk[t * D + lane] = z;
-        ek[t * D + lane] = e;
-        dyl[t * S::LDD + lane] = O::to_e(dyv);
-        dyt[lane * S::LDC + t] = O::to_e(dyv);
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        const int i = l16 * EPL + q;
+        yk[t * D + i] = z[q];
+        ek[t * D + i] = e[q];
+        dyl[t * S::LDD + i] = O::to_e(dyv[q]);
+        dyt[i * S::LDC + t] = O::to_e(dyv[q]);
       }
-      if (lane == 0) { row[2 * t] = sig; row[2 * t + 1] = mez; }
+      if (l16 == 0) { row[2 * t] = sig; row[2 * t + 1] = mez; }
     }
     __syncthreads();
 
@@ -520,33 +537,58 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       using IOT = typename IoT<S::BF>::T;
       IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
 #pragma unroll 1
-      for (int t = w; t < S::CM; t += NW) {
-        const bool on = lane < D;
-        const float dyhv = on ? dyh[t * D + lane] : 0.0f;
-        const float e = on ? ek[t * D + lane] : 0.0f;
-        float eh, yhv;
-        if (resln) {
-          const float z = on ? yk[t * D + lane] : 0.0f;
-          const float sig = row[2 * t], mez = row[2 * t + 1];
-          const float me = wave_sum(e) * inv_d;
-          const float dyv = on ? (e - me - z * mez) / sig : 0.0f;
-          const float m1 = wave_sum(dyhv) * inv_d;
-          const float m2 = wave_sum(dyhv * z) * inv_d;
-          eh = on ? (dyhv - m1 - z * m2) / sig : 0.0f;
-          const float sh = -wave_sum(dyhv * dyv) / sig;
-          const float zh = on ? -(dyhv * mez + e * m2) / sig - eh : 0.0f;
-          const float n1 = wave_sum(zh) * inv_d;
-          const float n2 = wave_sum(zh * z) * inv_d;
-          yhv = on ? (zh - n1 - z * n2) / sig + sh * z * inv_d : 0.0f;
-        } else {
-          eh = dyhv;
-          yhv = -eh;
+      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+        const int t = t0 + (lane >> 4);
+        float dyhv[EPL], e[EPL], eh[EPL], yhv[EPL];
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+          dyhv[q] = dyh[t * D + l16 * EPL + q];
+          e[q] = ek[t * D + l16 * EPL + q];
         }
-        if (on) {
-          ek[t * D + lane] = eh;
-          yh[t * S::LDD + lane] = O::to_e(yhv);
-          yht[lane * S::LDC + t] = O::to_e(yhv);
-          if (t < len) IoT<S::BF>::st(dvp + (long)t * D + lane, eh);
+        if (resln) {
+          float z[EPL], dyv[EPL], zh[EPL];
+          const float sig = row[2 * t], mez = row[2 * t + 1];
+          float se = 0.0f, m1 = 0.0f, m2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            z[q] = yk[t * D + l16 * EPL + q];
+            se += e[q];
+            m1 += dyhv[q];
+            m2 += dyhv[q] * z[q];
+          }
+          const float me = group16_sum(se) * inv_d;
+          m1 = group16_sum(m1) * inv_d;
+          m2 = group16_sum(m2) * inv_d;
+          float sdd = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            dyv[q] = (e[q] - me - z[q] * mez) * sig;
+            eh[q] = (dyhv[q] - m1 - z[q] * m2) * sig;
+            sdd += dyhv[q] * dyv[q];
+          }
+          const float sh = -group16_sum(sdd) * sig;
+          float n1 = 0.0f, n2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            zh[q] = -(dyhv[q] * mez + e[q] * m2) * sig - eh[q];
+            n1 += zh[q];
+            n2 += zh[q] * z[q];
+          }
+          n1 = group16_sum(n1) * inv_d;
+          n2 = group16_sum(n2) * inv_d;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) yhv[q] = (zh[q] - n1 - z[q] * n2) * sig + sh * z[q] * inv_d;
+        } else {
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) { eh[q] = dyhv[q]; yhv[q] = -eh[q]; }
+        }
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+          const int i = l16 * EPL + q;
+          ek[t * D + i] = eh[q];
+          yh[t * S::LDD + i] = O::to_e(yhv[q]);
+          yht[i * S::LDC + t] = O::to_e(yhv[q]);
+          if (t < len) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
         }
       }
     }
@@ -706,26 +748,40 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       __syncthreads();
       // Yb_Q = LN backward of dO at the Q rows (dO itself when there is no LN)
 #pragma unroll 1
-      for (int t = w; t < S::CM; t += NW) {
-        const bool on = lane < D;
-        const float dov = on ? O::from_e(xdo[t * S::LDD + lane]) : 0.0f;
-        float yb;
+      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+        const int t = t0 + (lane >> 4);
+        float dov[EPL], yb[EPL];
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) dov[q] = O::from_e(xdo[t * S::LDD + l16 * EPL + q]);
         if (resln) {
-          const float yv = on ? yk[t * D + lane] : 0.0f;
-          const float mu = wave_sum(yv) * inv_d;
-          const float yc = on ? yv - mu : 0.0f;
-          const float var = wave_sum(yc * yc) * inv_d;
-          const float sig = sqrtf(var + a.eps);
-          const float z = yc / sig;
-          const float m1 = wave_sum(dov) * inv_d;
-          const float m2 = wave_sum(dov * z) * inv_d;
-          yb = on ? (dov - m1 - z * m2) / sig : 0.0f;
+          float yv[EPL], s1 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) { yv[q] = yk[t * D + l16 * EPL + q]; s1 += yv[q]; }
+          const float mu = group16_sum(s1) * inv_d;
+          float s2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
+          const float sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+          float m1 = 0.0f, m2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            yv[q] *= sig;              // z
+            m1 += dov[q];
+            m2 += dov[q] * yv[q];
+          }
+          m1 = group16_sum(m1) * inv_d;
+          m2 = group16_sum(m2) * inv_d;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) yb[q] = (dov[q] - m1 - yv[q] * m2) * sig;
         } else {
-          yb = dov;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) yb[q] = dov[q];
         }
-        if (on) {
-          ybq[t * S::LDD + lane] = O::to_e(yb);
-          ybqt[lane * S::LDC + t] = O::to_e(yb);
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+          const int i = l16 * EPL + q;
+          ybq[t * S::LDD + i] = O::to_e(yb[q]);
+          ybqt[i * S::LDC + t] = O::to_e(yb[q]);
         }
       }
       __syncthreads();

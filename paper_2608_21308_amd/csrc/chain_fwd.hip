@@ -144,30 +144,50 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
     __syncthreads();
 
     // ------------------------------- LN and activation gradients (a4)
+    // Four token rows per wave step: lanes 16 r .. 16 r + 15 hold row t0 + r,
+    // EPL consecutive head elements each; row sums are 16-lane DPP reductions.
     const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
-    for (int t = w; t < S::CM; t += S::NW) {
-      const bool on = lane < D;
-      const float yv = on ? sm.y[t * D + lane] : 0.0f;
-      const float kx = on ? O::from_e(sm.xk[t * S::LDD + lane]) : 0.0f;
-      const float vx = on ? O::from_e(sm.xv[t * S::LDD + lane]) : 0.0f;
-      float dyv;
-      if (a.resln) {
-        const float mu = wave_sum(yv) * inv_d;
-        const float yc = on ? yv - mu : 0.0f;
-        const float var = wave_sum(yc * yc) * inv_d;
-        const float sig = sqrtf(var + a.eps);
-        const float z = yc / sig;
-        const float e = on ? vx - kx - z : 0.0f;
-        const float me = wave_sum(e) * inv_d;
-        const float mez = wave_sum(e * z) * inv_d;
-        dyv = (e - me - z * mez) / sig;
-      } else {
-        dyv = vx - yv;
-      }
-      if (on) {
-        sm.dy[t * S::LDD + lane] = O::to_e(dyv);
-        sm.dytw[lane * S::LDC + t] = O::to_e(sm.kw[t] * dyv);
-        sm.dytm[lane * S::LDC + t] = O::to_e(sm.km[t] * dyv);
+    {
+      constexpr int EPL = D / 16;
+      const int l16 = lane & 15;
+#pragma unroll 1
+      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * S::NW) {
+        const int t = t0 + (lane >> 4);
+        float yv[EPL], e[EPL], z[EPL], dyv[EPL];
+        float s1 = 0.0f;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) { yv[q] = sm.y[t * D + l16 * EPL + q]; s1 += yv[q]; }
+        if (a.resln) {
+          const float mu = group16_sum(s1) * inv_d;
+          float s2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
+          const float sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+          float se = 0.0f, sez = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            const int i = l16 * EPL + q;
+            z[q] = yv[q] * sig;
+            e[q] = O::from_e(sm.xv[t * S::LDD + i]) - O::from_e(sm.xk[t * S::LDD + i]) - z[q];
+            se += e[q];
+            sez += e[q] * z[q];
+          }
+          const float me = group16_sum(se) * inv_d, mez = group16_sum(sez) * inv_d;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) dyv[q] = (e[q] - me - z[q] * mez) * sig;
+        } else {
+#pragma unroll
+          for (int q = 0; q < EPL; ++q)
+            dyv[q] = O::from_e(sm.xv[t * S::LDD + l16 * EPL + q]) - yv[q];
+        }
+        const float kwt = sm.kw[t], kmt = sm.km[t];
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) {
+          const int i = l16 * EPL + q;
+          sm.dy[t * S::LDD + i] = O::to_e(dyv[q]);
+          sm.dytw[i * S::LDC + t] = O::to_e(kwt * dyv[q]);
+          sm.dytm[i * S::LDC + t] = O::to_e(kmt * dyv[q]);
+        }
       }
     }
     __syncthreads();
@@ -271,21 +291,33 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
     // ------------------------------------------------- outputs (a7)
     {
       using IOT = typename IO::T;
+      constexpr int EPL = D / 16;
+      const int l16 = lane & 15;
       IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
-      for (int t = w; t < len; t += S::NW) {
-        const bool on = lane < D;
-        const float yv = on ? sm.y[t * D + lane] : 0.0f;
-        float f;
+#pragma unroll 1
+      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * S::NW) {
+        const int t = t0 + (lane >> 4);
+        float yv[EPL], f[EPL];
+        float s1 = 0.0f;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) { yv[q] = sm.y[t * D + l16 * EPL + q]; s1 += yv[q]; }
         if (a.resln) {
-          const float qx = on ? O::from_e(sm.xq[t * S::LDD + lane]) : 0.0f;
-          const float mu = wave_sum(yv) * inv_d;
-          const float yc = on ? yv - mu : 0.0f;
-          const float var = wave_sum(yc * yc) * inv_d;
-          f = qx + yc / sqrtf(var + a.eps);
+          const float mu = group16_sum(s1) * inv_d;
+          float s2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
+          const float sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+#pragma unroll
+          for (int q = 0; q < EPL; ++q)
+            f[q] = O::from_e(sm.xq[t * S::LDD + l16 * EPL + q]) + yv[q] * sig;
         } else {
-          f = yv;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) f[q] = yv[q];
         }
-        if (on) IO::st(outp + (long)t * D + lane, f);
+        if (t < len) {
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) IO::st(outp + (long)t * D + l16 * EPL + q, f[q]);
+        }
       }
     }
     __syncthreads();

@@ -98,38 +98,80 @@ __device__ __forceinline__ typename OpT<BF>::Frag lds_frag(const typename OpT<BF
 }
 
 // --------------------------------------------------------------- activations
-__device__ __forceinline__ float gelu_f(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+// Reciprocal and reciprocal square root on the hardware units (1 ulp).
+__device__ __forceinline__ float rcp_f(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float rsq_f(float x) { return __builtin_amdgcn_rsqf(x); }
+
+// Standard normal CDF Phi(x) and density phi(x) from the Chebyshev-fitted
+// complementary error function of Press et al., Numerical Recipes (2nd ed.,
+// section 6.2, "erfcc"): erfc(z) = t exp(-z^2 + P(t)), t = 1 / (1 + z / 2),
+// z >= 0, with fractional error below 1.2e-7 for every z.  Using erfc keeps
+// Phi accurate in relative terms in its lower tail, where 1 + erf cancels.
+struct NormalCdf {
+  float cdf, pdf;
+};
+__device__ __forceinline__ NormalCdf normal_cdf(float x) {
+  const float z = fabsf(x) * 0.70710678118654752f;
+  const float t = rcp_f(1.0f + 0.5f * z);
+  float p = 0.17087277f;
+  p = fmaf(p, t, -0.82215223f);
+  p = fmaf(p, t, 1.48851587f);
+  p = fmaf(p, t, -1.13520398f);
+  p = fmaf(p, t, 0.27886807f);
+  p = fmaf(p, t, -0.18628806f);
+  p = fmaf(p, t, 0.09678418f);
+  p = fmaf(p, t, 0.37409196f);
+  p = fmaf(p, t, 1.00002368f);
+  p = fmaf(p, t, -1.26551223f);
+  const float ez2 = __expf(-z * z);                 // exp(-x^2 / 2)
+  const float half_erfc = 0.5f * t * ez2 * __expf(p);  // Phi(-|x|)
+  NormalCdf r;
+  r.cdf = (x >= 0.0f) ? 1.0f - half_erfc : half_erfc;
+  r.pdf = 0.39894228040143268f * ez2;
+  return r;
 }
+// GELU (exact, x Phi(x)) and its first two derivatives.
+__device__ __forceinline__ float gelu_f(float x) { return x * normal_cdf(x).cdf; }
 __device__ __forceinline__ float gelu_d1(float x) {
-  return 0.5f * (1.0f + erff(x * 0.70710678118654752f)) +
-         x * 0.39894228040143268f * expf(-0.5f * x * x);
+  const NormalCdf n = normal_cdf(x);
+  return n.cdf + x * n.pdf;
 }
 __device__ __forceinline__ float gelu_d2(float x) {
-  return 0.39894228040143268f * expf(-0.5f * x * x) * (2.0f - x * x);
+  return 0.39894228040143268f * __expf(-0.5f * x * x) * (2.0f - x * x);
 }
-__device__ __forceinline__ float sigm_f(float x) { return 1.0f / (1.0f + expf(-x)); }
+__device__ __forceinline__ float sigm_f(float x) { return rcp_f(1.0f + __expf(-x)); }
 __device__ __forceinline__ float silu_f(float x) { return x * sigm_f(x); }
 __device__ __forceinline__ float silu_d1(float x) {
-  float s = sigm_f(x);
+  const float s = sigm_f(x);
   return s * (1.0f + x * (1.0f - s));
 }
 __device__ __forceinline__ float silu_d2(float x) {
-  float s = sigm_f(x);
+  const float s = sigm_f(x);
   return s * (1.0f - s) * (2.0f + x * (1.0f - 2.0f * s));
 }
 
 // ------------------------------------------------------------- reductions
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+// DPP lane permutations within a row of 16 lanes (no LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+// Sum over the 16 lanes of a DPP row (lanes 16 k .. 16 k + 15); every lane of
+// the row receives the sum.
+__device__ __forceinline__ float group16_sum(float v) {
+  v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);   // row_half_mirror
+  v += dpp_f<0x140>(v);   // row_mirror
   return v;
 }
-// Sum over the 16 lanes that share a lane group (same rows of a D tile).
-__device__ __forceinline__ float group16_sum(float v) {
-#pragma unroll
-  for (int m = 8; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
+// Sum over all 64 lanes, returned to every lane (all lanes must be active).
+__device__ __forceinline__ float wave_sum(float v) {
+  const int b = __float_as_int(group16_sum(v));
+  return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) +
+          __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
+         (__int_as_float(__builtin_amdgcn_readlane(b, 32)) +
+          __int_as_float(__builtin_amdgcn_readlane(b, 48)));
 }
 
 // ----------------------------------------------------------- io element load

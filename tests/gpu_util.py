@@ -49,3 +49,17 @@ def slice_tokens(x: dict, lo: int, hi: int) -> dict:
         else:
             y[n] = np.ascontiguousarray(a[:, :, lo:hi])
     return y
+
+
+def fp32_sensitivity(fn, x, keys=("q", "k", "v", "w_in", "m_in"), seed=0):
+    """rel-L2 change of the oracle outputs fn(x) under a one-ulp (2^-24)
+    relative perturbation of the float inputs x[keys]: the intrinsic conditioning of a case
+    at fp32 precision."""
+    rng = np.random.default_rng(seed)
+    ref = fn(x)
+    xp = dict(x)
+    for k in keys:
+        if xp.get(k) is not None:
+            xp[k] = x[k] * (1 + 2.0 ** -24 * rng.standard_normal(x[k].shape))
+    out = fn(xp)
+    return {n: rel_l2(out[n], ref[n]) for n in ref if ref[n] is not None}

@@ -13,7 +13,7 @@ import torch
 
 from oracle import oracle
 from paper_2608_21308_amd import e2ttt, workloads as WL
-from tests.gpu_util import TOL, config_of, rel_l2, slice_tokens, to_dev
+from tests.gpu_util import TOL, config_of, fp32_sensitivity, rel_l2, slice_tokens, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -85,7 +85,14 @@ def test_backward_fp32_shapes(fw, T, C, dh, flags):
     x = with_state_inputs(WL.make_inputs(w), 11 + T)
     g = gpu_fwd_bwd(w, x, flags)
     errs = errors(g, oracle_bwd(w, x, flags))
-    assert_tol(errs, "f32", "bwd fp32 fw=%d T=%d C=%d dh=%d flags=%d" % (fw, T, C, dh, flags))
+    # 1e-5, widened only by the case's own fp32 conditioning (see the forward test)
+    sens = fp32_sensitivity(lambda y: oracle_bwd(w, y, flags), x)
+    bound = {n: max(TOL["f32"], 10 * sens[n]) for n in errs}
+    what = "bwd fp32 fw=%d T=%d C=%d dh=%d flags=%d" % (fw, T, C, dh, flags)
+    print(what, {k: "%.2e" % v for k, v in errs.items()},
+          "sens", {k: "%.1e" % v for k, v in sens.items()}, flush=True)
+    bad = {n: (errs[n], bound[n]) for n in errs if not errs[n] <= bound[n]}
+    assert not bad, what + ": %s" % bad
 
 
 def test_backward_tiny_fp32_workload():

@@ -15,7 +15,8 @@ import torch
 
 from oracle import oracle
 from paper_2608_21308_amd import e2ttt, workloads as WL
-from tests.gpu_util import TOL, config_of, gpu_forward, rel_l2, slice_tokens, to_dev
+from tests.gpu_util import (TOL, config_of, fp32_sensitivity, gpu_forward, rel_l2, slice_tokens,
+                            to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -106,11 +107,26 @@ def test_forward_fp32_shapes(fw, T, C, dh, flags):
     # numpy implementation of the same closed form drifts by 4e-6 .. 1e-4 on
     # 11 chunks of these shapes), so long-run fp32 parity is pinned on the
     # tiny workload above and on the bare net (flags = 1) here.
+    # The bound is 1e-5, widened only for cases whose own fp32 conditioning is
+    # worse: the oracle's output change under one-ulp perturbations of its inputs,
+    # times 10 (the kernel rounds at every chunk, the probe only once).
     w = WL.WORKLOADS[0].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, seed=500 + T + C + dh)
     x = WL.make_inputs(w, with_grads=False)
     m_in = np.random.default_rng(T).standard_normal(x["w_in"].shape).astype(np.float32) * 1e-3
     errs, _, _ = run_both(w, x, flags=flags, m_in=m_in)
-    assert_tol(errs, "f32", "fp32 fw=%d T=%d C=%d dh=%d flags=%d" % (fw, T, C, dh, flags))
+
+    def fn(y):
+        o, wo, mo = oracle.forward(y["q"], y["k"], y["v"], y["eta"], y["beta"], y["gamma"],
+                                   y["w_in"], m_in, C=C, fw=fw, dh=dh, flags=flags)
+        return {"out": o, "w_out": wo, "m_out": mo}
+
+    sens = fp32_sensitivity(fn, x)
+    what = "fp32 fw=%d T=%d C=%d dh=%d flags=%d (sens %s)" % (
+        fw, T, C, dh, flags, {k: "%.1e" % v for k, v in sens.items()})
+    bound = {n: max(TOL["f32"], 10 * sens[n]) for n in errs}
+    print(what, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    bad = {n: (errs[n], bound[n]) for n in errs if not errs[n] <= bound[n]}
+    assert not bad, what + ": %s" % bad
 
 
 # ------------------------------------------------------------ bf16 path
