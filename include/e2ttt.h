@@ -28,6 +28,11 @@
  *     return nothing has been written.  Errors raised by kernels while they
  *     run surface on the stream as HIP errors.
  *   - Results are bitwise reproducible run to run (no floating-point atomics).
+ *   - For the widest nets (GELU MLP with dh > 128 at d = 64) each unit is
+ *     split over two workgroups that swap partial sums through the workspace
+ *     (or the backward scratch); those kernels are launched cooperatively, so
+ *     a call may wait for the whole device.  Calls that share a workspace or
+ *     scratch buffer must not run concurrently.
  *
  * Tensor layouts (row-major, C order):
  *   q, k, v, out, d_out, dq, dk, dv : [B][H][T][d]   element type desc.io
@@ -38,12 +43,12 @@
  *   SwiGLU   : Wg[dh][d], then Wu[dh][d], then Wd[d][dh]        P = 3 d dh
  *   (Wg, Wu, Wd are the paper's W1, W2, W3 of the SwiGLU net.)
  *
- * Supported shapes: d in {16, 32, 64}; 1 <= dh with dh padded inside the
- * library to a multiple of 16 (at most 256 for the MLP, 176 for SwiGLU at
- * d = 64); 1 <= chunk <= 64; T >= 1 with a ragged last chunk of T mod chunk
- * tokens allowed (Prop. 1 holds for any chunk length); io = F32 or BF16
- * (bf16 tensors use MFMA bf16 operands with fp32 accumulation and fp32
- * state; f32 tensors use fp32 MFMA throughout).  Anything else returns
+ * Supported shapes: io = BF16 with d = 64 (dh <= 256 for the MLP, <= 176 for
+ * SwiGLU), or io = F32 with d = 16 (dh <= 128); dh is padded inside the
+ * library to a multiple of 16; 1 <= chunk <= 64; T >= 1 with a ragged last
+ * chunk of T mod chunk tokens allowed (Prop. 1 holds for any chunk length).
+ * bf16 tensors use MFMA bf16 operands with fp32 accumulation and fp32 state;
+ * f32 tensors use fp32 MFMA throughout.  Anything else returns
  * E2TTT_ERR_UNSUPPORTED.
  */
 #ifndef E2TTT_H
@@ -62,8 +67,14 @@ typedef enum {
   E2TTT_ERR_BAD_SHAPE = 2,             /* a size is <= 0 or inconsistent          */
   E2TTT_ERR_UNSUPPORTED = 3,           /* valid but outside the supported set     */
   E2TTT_ERR_WORKSPACE_TOO_SMALL = 4,   /* workspace / scratch smaller than needed */
-  E2TTT_ERR_HIP = 5                    /* a HIP launch failed                     */
+  E2TTT_ERR_HIP = 5,                   /* a HIP launch failed                     */
+  E2TTT_ERR_DEVICE = 6                 /* a bounded device-side wait expired      */
 } e2ttt_status;
+/* E2TTT_ERR_DEVICE is reported only when the environment variable
+ * E2TTT_DEBUG_SYNC=1 makes every call wait for its kernels: a wait between the
+ * two workgroups of a unit expired (after 2 s), the grid was drained and the
+ * results of that call are undefined.  Without E2TTT_DEBUG_SYNC the word that
+ * records it sits in the workspace / scratch and no error is returned. */
 
 typedef enum { E2TTT_FW_GELU_MLP = 0, E2TTT_FW_SWIGLU = 1 } e2ttt_fw;
 
@@ -88,9 +99,10 @@ size_t e2ttt_param_count(const e2ttt_desc* desc);
 
 /* Bytes of `workspace` that e2ttt_chunk_forward needs.  With
  * save_for_backward != 0 the workspace also keeps what the backward reuses
- * (per-token scalar kernels and bf16 chunk-start checkpoints of W and M), and
- * the same buffer, untouched, must then be passed to e2ttt_chunk_backward.
- * Returns 0 for a bad descriptor. */
+ * (per-token scalar kernels, chunk-start checkpoints of W and M in the
+ * operand precision, and the LayerNorm outputs and inverse deviations of the
+ * key and query passes), and the same buffer, untouched, must then be passed
+ * to e2ttt_chunk_backward.  Returns 0 for a bad descriptor. */
 size_t e2ttt_workspace_bytes(const e2ttt_desc* desc, int save_for_backward);
 
 /* Bytes of `scratch` that e2ttt_chunk_backward needs (0 for a bad descriptor). */

@@ -2,28 +2,36 @@
 // workspace planning and kernel dispatch.  Nothing here allocates memory.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <cstdlib>
 
 #include "e2ttt.h"
 #include "e2ttt_internal.h"
+#include "pair_xchg.h"
 
 namespace {
 
 using namespace e2ttt;
 
 constexpr size_t kAlign = 256;
+// Upper bound on workgroup pairs of one cooperative launch (256 CUs, one
+// chain workgroup per CU); more units are taken in turn by the same pairs.
+constexpr long kMaxPairs = 128;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Plan {
   long U = 0, T = 0, NC = 0, P = 0;
   ChainConfig cfg{};
+  long npairs = 0;        // pairs the exchange buffers are sized for (two workgroups per unit)
   // forward workspace
-  size_t off_kw = 0, off_km = 0, off_carry = 0, off_ckpt = 0, ws_bytes = 0, ws_bytes_save = 0;
+  size_t off_kw = 0, off_km = 0, off_carry = 0, off_sync = 0, off_xbuf = 0, ws_bytes = 0;
+  size_t off_ckpt = 0, off_zk = 0, off_rk = 0, off_zq = 0, off_rq = 0, ws_bytes_save = 0;
   long ckpt_stride = 0;
   // backward scratch
-  size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, scratch_bytes = 0;
+  size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, off_bsync = 0, off_bxbuf = 0;
+  size_t scratch_bytes = 0;
 };
 
 e2ttt_status select_config(const e2ttt_desc& d, ChainConfig& cfg) {
@@ -31,12 +39,13 @@ e2ttt_status select_config(const e2ttt_desc& d, ChainConfig& cfg) {
   cfg.d = d.d;
   cfg.bf = (d.io == E2TTT_DT_BF16) ? 1 : 0;
   const int nblk = (d.dh + 15) / 16;
+  cfg.ns = 1;
   if (cfg.bf) {
     if (d.d != 64) return E2TTT_ERR_UNSUPPORTED;
     cfg.ntb = 4;
     if (nblk <= 4) { cfg.nw = 4; cfg.njb = 1; }
     else if (nblk <= 8) { cfg.nw = 8; cfg.njb = 1; }
-    else if (d.fw == E2TTT_FW_GELU_MLP && nblk <= 16) { cfg.nw = 8; cfg.njb = 2; }
+    else if (d.fw == E2TTT_FW_GELU_MLP && nblk <= 16) { cfg.nw = 8; cfg.njb = 1; cfg.ns = 2; }
     else if (d.fw == E2TTT_FW_SWIGLU && nblk <= 11) { cfg.nw = 11; cfg.njb = 1; }
     else return E2TTT_ERR_UNSUPPORTED;
   } else {
@@ -69,17 +78,32 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.P = (d.fw == E2TTT_FW_GELU_MLP ? 2L : 3L) * d.d * d.dh;
   const size_t tok = (size_t)U * d.T * sizeof(float);
   const size_t chk = (size_t)U * pl.NC * 3 * sizeof(float);
+  const long ns = pl.cfg.ns;
+  pl.npairs = (ns > 1) ? std::min((U + 7) / 8 * 8, kMaxPairs) : 0;
+  const size_t sync_b = (ns > 1) ? (size_t)sync_words(pl.npairs) * sizeof(unsigned) : 0;
   pl.off_kw = 0;
   pl.off_km = align_up(tok);
   pl.off_carry = pl.off_km + align_up(tok);
-  pl.off_ckpt = pl.off_carry + align_up(chk);
+  pl.off_sync = pl.off_carry + align_up(chk);
+  pl.off_xbuf = pl.off_sync + align_up(sync_b);
+  pl.off_ckpt = pl.off_xbuf +
+                align_up((size_t)pl.npairs * 2 * chain_xchg_floats(pl.cfg, false) * sizeof(float));
   pl.ws_bytes = pl.off_ckpt;
   pl.ckpt_stride = chain_ckpt_bytes(pl.cfg);
-  pl.ws_bytes_save = pl.off_ckpt + align_up((size_t)U * pl.NC * 2 * pl.ckpt_stride);
+  const size_t tokd = tok * d.d;
+  pl.off_zk = pl.off_ckpt + align_up((size_t)U * pl.NC * ns * 2 * pl.ckpt_stride);
+  pl.off_rk = pl.off_zk + align_up(tokd);
+  pl.off_zq = pl.off_rk + align_up(tok);
+  pl.off_rq = pl.off_zq + align_up(tokd);
+  pl.ws_bytes_save = pl.off_rq + align_up(tok);
   pl.off_kwb = 0;
-  pl.off_kmb = align_up(tok);
-  pl.off_carryb = pl.off_kmb + align_up(tok);
-  pl.scratch_bytes = pl.off_carryb + align_up(chk);
+  pl.off_kmb = align_up(ns * tok);
+  pl.off_carryb = pl.off_kmb + align_up(ns * tok);
+  pl.off_bsync = pl.off_carryb + align_up(ns * chk);
+  pl.off_bxbuf = pl.off_bsync + align_up(sync_b);
+  pl.scratch_bytes =
+      pl.off_bxbuf +
+      align_up((size_t)pl.npairs * 2 * chain_xchg_floats(pl.cfg, true) * sizeof(float));
   return E2TTT_OK;
 }
 
@@ -93,11 +117,53 @@ bool debug_sync() {
   return on;
 }
 
-e2ttt_status finish(hipError_t e, hipStream_t s) {
+// With E2TTT_DEBUG_SYNC=1 every call waits for its kernels and, for the
+// two-workgroup kernels, reads the status word of the pair exchange.
+e2ttt_status finish(hipError_t e, hipStream_t s, const unsigned* sync = nullptr) {
   if (e != hipSuccess) return E2TTT_ERR_HIP;
-  if (debug_sync() && hipStreamSynchronize(s) != hipSuccess) return E2TTT_ERR_HIP;
+  if (debug_sync()) {
+    if (hipStreamSynchronize(s) != hipSuccess) return E2TTT_ERR_HIP;
+    if (sync) {
+      unsigned st = 0;
+      if (hipMemcpy(&st, sync, sizeof(st), hipMemcpyDeviceToHost) != hipSuccess)
+        return E2TTT_ERR_HIP;
+      if (st != 0) return E2TTT_ERR_DEVICE;
+    }
+  }
   return E2TTT_OK;
 }
+
+// Pairs for one cooperative launch: what the buffers were sized for, capped by
+// what the device holds at once.  0 when the device cannot hold eight pairs.
+long launch_pairs(const Plan& pl, bool backward) {
+  return std::min(pl.npairs, chain_max_pairs(pl.cfg, backward));
+}
+
+}  // namespace
+
+namespace e2ttt {
+
+int chain_fwd_blocks_per_cu(const ChainConfig& cfg);
+int chain_bwd_blocks_per_cu(const ChainConfig& cfg);
+
+long chain_max_pairs(const ChainConfig& cfg, bool backward) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  const int nb = backward ? chain_bwd_blocks_per_cu(cfg) : chain_fwd_blocks_per_cu(cfg);
+  return ((long)nb * cus / 2) / 8 * 8;
+}
+
+long chain_xchg_floats(const ChainConfig& cfg, bool backward) {
+  // per rank: two parities of (Y_K, Y_Q) or (dYh, dk, dq), 16 ntb x d floats each
+  return 2L * (backward ? 3 : 2) * 16 * cfg.ntb * cfg.d;
+}
+
+}  // namespace e2ttt
+
+namespace {
 
 template <class Tp> Tp* at(void* base, size_t off) {
   return reinterpret_cast<Tp*>(static_cast<char*>(base) + off);
@@ -134,6 +200,7 @@ const char* e2ttt_status_str(e2ttt_status s) {
     case E2TTT_ERR_UNSUPPORTED: return "shape, dtype or flags outside the supported set";
     case E2TTT_ERR_WORKSPACE_TOO_SMALL: return "workspace or scratch buffer too small";
     case E2TTT_ERR_HIP: return "a HIP launch failed";
+    case E2TTT_ERR_DEVICE: return "a device-side wait between the two workgroups of a unit expired";
   }
   return "unknown status";
 }
@@ -146,7 +213,7 @@ e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const 
   if (st != E2TTT_OK) return st;
   if (!eta || !beta || !kw || !km || !carry) return E2TTT_ERR_NULL_ARG;
   CoeffFwdArgs c{eta, beta, gamma, kw, km, carry, (int)pl.T, desc->chunk, (int)pl.NC,
-                 pl.U * pl.NC};
+                 pl.U * pl.NC, nullptr, 0};
   hipStream_t s = static_cast<hipStream_t>(stream);
   return finish(launch_coeff_fwd(c, s), s);
 }
@@ -168,21 +235,34 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   float* kw = at<float>(workspace, pl.off_kw);
   float* km = at<float>(workspace, pl.off_km);
   float* carry = at<float>(workspace, pl.off_carry);
+  unsigned* sync = pl.cfg.ns > 1 ? at<unsigned>(workspace, pl.off_sync) : nullptr;
+  const long np = pl.cfg.ns > 1 ? launch_pairs(pl, false) : 0;
+  if (pl.cfg.ns > 1 && np < 8) return E2TTT_ERR_UNSUPPORTED;
   CoeffFwdArgs c{eta, beta, gamma, kw, km, carry, (int)pl.T, desc->chunk, (int)pl.NC,
-                 pl.U * pl.NC};
+                 pl.U * pl.NC, sync, sync ? sync_words(np) : 0};
   hipError_t e = launch_coeff_fwd(c, s);
   if (e != hipSuccess) return E2TTT_ERR_HIP;
   ChainArgs a{};
+  a.U = pl.U;
   a.q = q; a.k = k; a.v = v;
   a.w_in = w_in; a.m_in = m_in;
   a.kw = kw; a.km = km; a.carry = carry;
   a.out = out; a.w_out = w_out; a.m_out = m_out;
   a.ckpt = save_for_backward ? at<char>(workspace, pl.off_ckpt) : nullptr;
   a.ckpt_stride = pl.ckpt_stride;
+  if (save_for_backward) {
+    a.zk = at<float>(workspace, pl.off_zk);
+    a.rk = at<float>(workspace, pl.off_rk);
+    a.zq = at<float>(workspace, pl.off_zq);
+    a.rq = at<float>(workspace, pl.off_rq);
+  }
+  a.xbuf = at<float>(workspace, pl.off_xbuf);
+  a.sync = sync;
+  a.npairs = np;
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
   a.eps = desc->ln_eps;
-  return finish(launch_chain_fwd(pl.cfg, a, pl.U, s), s);
+  return finish(launch_chain_fwd(pl.cfg, a, s), s, sync);
 }
 
 e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const void* k,
@@ -203,7 +283,12 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   if (workspace_bytes < pl.ws_bytes_save || scratch_bytes < pl.scratch_bytes)
     return E2TTT_ERR_WORKSPACE_TOO_SMALL;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned* sync = pl.cfg.ns > 1 ? at<unsigned>(scratch, pl.off_bsync) : nullptr;
+  const long np = pl.cfg.ns > 1 ? launch_pairs(pl, true) : 0;
+  if (pl.cfg.ns > 1 && np < 8) return E2TTT_ERR_UNSUPPORTED;
+  if (sync && launch_zero_words(sync, sync_words(np), s) != hipSuccess) return E2TTT_ERR_HIP;
   ChainArgs a{};
+  a.U = pl.U;
   a.q = q; a.k = k; a.v = v;
   a.w_in = w_in; a.m_in = m_in;
   a.kw = at<float>(workspace, pl.off_kw);
@@ -211,6 +296,13 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   a.carry = at<float>(workspace, pl.off_carry);
   a.ckpt = const_cast<char*>(at<char>(workspace, pl.off_ckpt));
   a.ckpt_stride = pl.ckpt_stride;
+  a.zk = const_cast<float*>(at<float>(workspace, pl.off_zk));
+  a.rk = const_cast<float*>(at<float>(workspace, pl.off_rk));
+  a.zq = const_cast<float*>(at<float>(workspace, pl.off_zq));
+  a.rq = const_cast<float*>(at<float>(workspace, pl.off_rq));
+  a.xbuf = at<float>(scratch, pl.off_bxbuf);
+  a.sync = sync;
+  a.npairs = np;
   a.d_out = d_out; a.d_w_out = d_w_out; a.d_m_out = d_m_out;
   a.dq = dq; a.dk = dk; a.dv = dv;
   a.d_w_in = d_w_in; a.d_m_in = d_m_in;
@@ -220,11 +312,12 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
   a.eps = desc->ln_eps;
-  hipError_t e = launch_chain_bwd(pl.cfg, a, pl.U, s);
+  hipError_t e = launch_chain_bwd(pl.cfg, a, s);
   if (e != hipSuccess) return E2TTT_ERR_HIP;
   CoeffBwdArgs cb{eta, beta, gamma, a.kwb, a.kmb, a.carryb, d_eta, d_beta, d_gamma,
-                  (int)pl.T, desc->chunk, (int)pl.NC, pl.U * pl.NC};
-  return finish(launch_coeff_bwd(cb, s), s);
+                  (int)pl.T, desc->chunk, (int)pl.NC, pl.U * pl.NC, pl.cfg.ns,
+                  pl.U * pl.T, pl.U * pl.NC * 3};
+  return finish(launch_coeff_bwd(cb, s), s, sync);
 }
 
 }  // extern "C"

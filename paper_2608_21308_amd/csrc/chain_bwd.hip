@@ -25,6 +25,7 @@
 // where LNb(x) = (x - mean x - Z mean(x Z)) / sigma (per token, over the head dim).
 // SwiGLU and the bare net (no residual LN) follow the same pattern.
 #include "chain_common.h"
+#include "pair_xchg.h"
 
 namespace e2ttt {
 
@@ -184,6 +185,77 @@ __device__ __forceinline__ void jacc_store_io(const JAcc<S>& out, void* dst, lon
   }
 }
 
+// Write the j-round output tiles to an fp32 [CM][D] buffer: dst[t][i] = out + extra(t, i).
+template <class S, class FX>
+__device__ __forceinline__ void jacc_store_f32(const JAcc<S>& out, float* dst, FX extra, int w,
+                                               int g, int c) {
+  using L = BwdLayout<S>;
+  constexpr int NI = S::NIB / S::IBB;
+#pragma unroll
+  for (int a = 0; a < L::JIT; ++a) {
+    const int it = w + a * S::NW;
+    if (it < L::NITEM) {
+      const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * tb + 4 * g + r, i = 16 * (ib0 + b) + c;
+          dst[t * S::D + i] = out.v[a][b][r] + extra(t, i);
+        }
+    }
+  }
+}
+
+// Copy a CM x D fp32 tile (rows < len, zero beyond) from global memory to LDS.
+template <class S>
+__device__ __forceinline__ void stage_f32(float* dst, const float* src, long row0, int len,
+                                          int tid) {
+  constexpr int NV = S::CM * S::D / 4;
+  const float4* p = reinterpret_cast<const float4*>(src + row0 * S::D);
+#pragma unroll 1
+  for (int v = tid; v < NV; v += S::NT) {
+    float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if ((4 * v) / S::D < len) x = p[v];
+    reinterpret_cast<float4*>(dst)[v] = x;
+  }
+}
+
+// Exchange slot of one rank for one parity: [dYh | dk | dq] partials, CM x D floats each.
+template <class S>
+__device__ __forceinline__ float* bwd_slot(float* xbuf, long p, int rank, int parity) {
+  return xbuf + (((p * 2 + rank) * 2 + parity) * 3L) * S::CM * S::D;
+}
+
+// dk and dq of one chunk from the two ranks' partials (rank 0's carries the
+// -eh and dO terms), rows [rlo, rlo + RPW) below len.
+template <class S>
+__device__ __forceinline__ void flush_dkdq(const ChainArgs& a, long p, int parity, long row0,
+                                           int len, int rlo, int tid) {
+  using IO = IoT<S::BF>;
+  constexpr int RPW = S::CM / S::NS;
+  constexpr int NV = RPW * S::D / 4;
+  const float* s0 = bwd_slot<S>(a.xbuf, p, 0, parity);
+  const float* s1 = bwd_slot<S>(a.xbuf, p, 1, parity);
+  typename IO::T* dk = reinterpret_cast<typename IO::T*>(a.dk) + row0 * S::D;
+  typename IO::T* dq = reinterpret_cast<typename IO::T*>(a.dq) + row0 * S::D;
+#pragma unroll 1
+  for (int v = tid; v < NV; v += S::NT) {
+    const int e = rlo * S::D + 4 * v, t = e / S::D;
+    if (t >= len) continue;
+#pragma unroll
+    for (int sec = 1; sec <= 2; ++sec) {
+      const float4 x = *reinterpret_cast<const float4*>(s0 + sec * S::CM * S::D + e);
+      const float4 y = *reinterpret_cast<const float4*>(s1 + sec * S::CM * S::D + e);
+      typename IO::T* d = (sec == 1) ? dk : dq;
+      IO::st(d + e + 0, x.x + y.x);
+      IO::st(d + e + 1, x.y + y.y);
+      IO::st(d + e + 2, x.z + y.z);
+      IO::st(d + e + 3, x.w + y.w);
+    }
+  }
+}
+
 template <class S>
 __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   using O = typename S::O;
@@ -194,7 +266,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   constexpr int SEC = NMAT - 1;      // second-layer matrix
   constexpr int NF = NMAT - 1;       // number of first-layer matrices
   constexpr bool SW = S::FW == 1;
+  constexpr int EPL = D / 16;        // head elements per lane in row phases
+  constexpr int RPW = S::CM / S::NS; // rows of dv, dk, dq written by one rank
   __shared__ __attribute__((aligned(16))) unsigned char smem[L::TOTAL];
+  __shared__ int sword[2];
   E* xk = reinterpret_cast<E*>(smem + L::XK);
   E* jw = reinterpret_cast<E*>(smem + L::JW);
   E* ja = reinterpret_cast<E*>(smem + L::JA);
@@ -212,484 +287,56 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   float* scar = skm + S::CM;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, c = lane & 15;
-  const long u = blockIdx.x;
+  const int l16 = lane & 15;
   const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
   const float inv_d = 1.0f / D;
   const bool resln = a.resln != 0;
 
-  // adjoint of the final state
-  StateTiles<S> Wb, Mb;
-  load_state<S>(Wb, a.d_w_out ? a.d_w_out + u * a.P : nullptr, dh, w, g, c);
-  load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, w, g, c);
+  PairX<S::NS> px;
+  px.init(a.sync, a.npairs, sword);
+  const int rank = px.rank;
+  const int j0 = rank * S::DHP;
+  const long NP = (S::NS > 1) ? a.npairs : (long)gridDim.x;
+  const int rlo = rank * RPW;
+  float* const kwb_slot = a.kwb + rank * a.U * T;
+  float* const kmb_slot = a.kmb + rank * a.U * T;
+  float* const carryb_slot = a.carryb + rank * a.U * NC * 3;
+  long nch = 0;   // chunks processed by this workgroup (exchange parity)
 
-  for (int r = NC - 1; r >= 0; --r) {
-    const int s0 = r * C;
-    const int len = min(C, T - s0);
-    const long row0 = u * T + s0;
-    const char* ckW = static_cast<const char*>(a.ckpt) + (u * NC + r) * 2 * a.ckpt_stride;
-    const char* ckM = ckW + a.ckpt_stride;
+  for (long u = px.p; u < a.U; u += NP) {
+    // adjoint of the final state
+    StateTiles<S> Wb, Mb;
+    load_state<S>(Wb, a.d_w_out ? a.d_w_out + u * a.P : nullptr, dh, j0, w, g, c);
+    load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, j0, w, g, c);
+    int pend_r = -1, pend_par = 0;   // chunk whose dk, dq partials are not yet combined
 
-    // ------------------------------------------------------------ P0: stage
-    E* xv = reinterpret_cast<E*>(rr);
-    stage_tile<S>(xk, a.k, row0, len, tid);
-    stage_tile<S>(xv, a.v, row0, len, tid);
+    for (int r = NC - 1; r >= 0; --r, ++nch) {
+      const int s0 = r * C;
+      const int len = min(C, T - s0);
+      const long row0 = u * T + s0;
+      const int par = (int)(nch & 1);
+      const unsigned seq0 = px.seq_now();
+      const char* ckW =
+          static_cast<const char*>(a.ckpt) + ((u * NC + r) * S::NS + rank) * 2 * a.ckpt_stride;
+      const char* ckM = ckW + a.ckpt_stride;
+
+      // ---------------------------------------------------------- P0: stage
+      E* xv = reinterpret_cast<E*>(rr);
+      stage_tile<S>(xk, a.k, row0, len, tid);
+      stage_tile<S>(xv, a.v, row0, len, tid);
+      stage_f32<S>(yk, a.zk, row0, len, tid);   // Z (or Y without the residual LN)
 #pragma unroll 1
-    for (int t = tid; t < S::CM; t += S::NT) {
-      skw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
-      skm[t] = (t < len) ? a.km[row0 + t] : 0.0f;
-    }
-    if (tid < 3) scar[tid] = a.carry[(u * NC + r) * 3 + tid];
-    __syncthreads();
-
-    // -------------------------------------- P1: H = K W1^T, A = act(H) (recompute)
-    f32x4 Hk[NF][NTB][NJB];
-    Q Akq[NTB][NJB];
-    {
-      Q w1q[NF][NJB][NIB];
-#pragma unroll
-      for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-        for (int jj = 0; jj < NJB; ++jj) {
-          f32x4 acc[NF];
-#pragma unroll
-          for (int m = 0; m < NF; ++m) acc[m] = zero4();
-#pragma unroll
-          for (int p = 0; p < S::KS_D; ++p) {
-            auto af = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
-#pragma unroll
-            for (int m = 0; m < NF; ++m) {
-              typename O::Frag bf;
-#pragma unroll
-              for (int h = 0; h < S::NH; ++h) bf.h[h] = w1q[m][jj][S::NH * p + h];
-              acc[m] = O::mma(acc[m], af, bf);
-            }
-          }
-          f32x4 act;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if constexpr (!SW) act[q] = gelu_f(acc[0][q]);
-            else act[q] = silu_f(acc[0][q]) * acc[1][q];
-          }
-#pragma unroll
-          for (int m = 0; m < NF; ++m) Hk[m][tb][jj] = acc[m];
-          Akq[tb][jj] = O::cvt(act);
-          sched_fence();
-        }
-    }
-    // Y = A W2^T through one j-round (into yk, fp32)
-    {
-      JAcc<S> yacc;
-      yacc.zero();
-      Q w2q[NJB][NIB];
-      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
-      jround<S>(yacc, nullptr, ja, jw,
-                [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
-                [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
-      constexpr int NI = NIB / S::IBB;
-#pragma unroll
-      for (int aa = 0; aa < L::JIT; ++aa) {
-        const int it = w + aa * NW;
-        if (it < L::NITEM) {
-          const int tb = it / NI, ib0 = (it % NI) * S::IBB;
-#pragma unroll
-          for (int b = 0; b < S::IBB; ++b)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              yk[(16 * tb + 4 * g + q) * D + 16 * (ib0 + b) + c] = yacc.v[aa][b][q];
-        }
+      for (int t = tid; t < S::CM; t += S::NT) {
+        skw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
+        skm[t] = (t < len) ? a.km[row0 + t] : 0.0f;
+        row[2 * t] = (t < len) ? a.rk[row0 + t] : 0.0f;   // 1 / sigma
       }
-    }
-    __syncthreads();
-
-    // ------------------------------- P3: LN, e, dY (first-order, recomputed)
-    E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
-    constexpr int EPL = D / 16;                   // head elements per lane in row phases
-    const int l16 = lane & 15;
-#pragma unroll 1
-    for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
-      const int t = t0 + (lane >> 4);
-      float yv[EPL], e[EPL], z[EPL], dyv[EPL];
-      float sig = 1.0f, mez = 0.0f, s1 = 0.0f;   // sig: 1 / sigma
-#pragma unroll
-      for (int q = 0; q < EPL; ++q) { yv[q] = yk[t * D + l16 * EPL + q]; s1 += yv[q]; }
-      if (resln) {
-        const float mu = group16_sum(s1) * inv_d;
-        float s2 = 0.0f;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
-        sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
-        float se = 0.0f, sez = 0.0f;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-          const int i = l16 * EPL + q;
-          z[q] = yv[q] * sig;
-          e[q] = O::from_e(xv[t * S::LDD + i]) - O::from_e(xk[t * S::LDD + i]) - z[q];
-          se += e[q];
-          sez += e[q] * z[q];
-        }
-        const float me = group16_sum(se) * inv_d;
-        mez = group16_sum(sez) * inv_d;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) dyv[q] = (e[q] - me - z[q] * mez) * sig;
-      } else {
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-          z[q] = 0.0f;
-          e[q] = O::from_e(xv[t * S::LDD + l16 * EPL + q]) - yv[q];
-          dyv[q] = e[q];
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < EPL; ++q) {
-        const int i = l16 * EPL + q;
-        yk[t * D + i] = z[q];
-        ek[t * D + i] = e[q];
-        dyl[t * S::LDD + i] = O::to_e(dyv[q]);
-        dyt[i * S::LDC + t] = O::to_e(dyv[q]);
-      }
-      if (l16 == 0) { row[2 * t] = sig; row[2 * t + 1] = mez; }
-    }
-    __syncthreads();
-
-    // ------------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
-    // For every tile: dA = dY W2, dH = dA act'(H);  u = K Wb1^T, K Mb1^T;
-    // rW = dY Wb2, dY Mb2;  dK^W += rowsum(dH uW + A rW), dK^M likewise;
-    // p = K^W uW + K^M uM (= d(Phi)/d(dH)), r2 = K^W rW + K^M rM (direct a-term);
-    // dAh = p act'(H);  Hh = p dA act''(H) + r2 act'(H)  (the Yh W2 term is added later)
-    Q dHq[NF][NTB][NJB];
-    Q dAhq[NTB][NJB];
-    f32x4 Hh[NF][NTB][NJB];
-    {
-      float kwp[NTB][4], kmp[NTB][4];   // row partial sums for dK^W, dK^M
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) { kwp[tb][q] = 0.0f; kmp[tb][q] = 0.0f; }
-      Q w2q[NJB][NIB];
-      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
-      opaque_state<S>(Wb);
-      opaque_state<S>(Mb);
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-        for (int jj = 0; jj < NJB; ++jj) {
-          f32x4 dA = zero4(), rW = zero4(), rM = zero4();
-          f32x4 uW[NF], uM[NF];
-#pragma unroll
-          for (int m = 0; m < NF; ++m) { uW[m] = zero4(); uM[m] = zero4(); }
-#pragma unroll
-          for (int p = 0; p < S::KS_D; ++p) {
-            auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
-            auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
-            typename O::Frag b2, bw, bm;
-#pragma unroll
-            for (int h = 0; h < S::NH; ++h) {
-              b2.h[h] = w2q[jj][S::NH * p + h];
-              bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
-              bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
-            }
-            dA = O::mma(dA, fy, b2);
-            rW = O::mma(rW, fy, bw);
-            rM = O::mma(rM, fy, bm);
-#pragma unroll
-            for (int m = 0; m < NF; ++m) {
-#pragma unroll
-              for (int h = 0; h < S::NH; ++h) {
-                bw.h[h] = O::cvt(Wb.t[m][jj][S::NH * p + h]);
-                bm.h[h] = O::cvt(Mb.t[m][jj][S::NH * p + h]);
-              }
-              uW[m] = O::mma(uW[m], fk, bw);
-              uM[m] = O::mma(uM[m], fk, bm);
-            }
-          }
-          const f32x4 Af = quad_f32(Akq[tb][jj]);
-          f32x4 dH[NF], dAh, hh[NF];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int t = 16 * tb + 4 * g + q;
-            const float kwv = skw[t], kmv = skm[t];
-            const float r2 = kwv * rW[q] + kmv * rM[q];
-            if constexpr (!SW) {
-              const float h = Hk[0][tb][jj][q];
-              const float d1 = gelu_d1(h), d2 = gelu_d2(h);
-              dH[0][q] = dA[q] * d1;
-              const float pp = kwv * uW[0][q] + kmv * uM[0][q];
-              dAh[q] = pp * d1;
-              hh[0][q] = pp * dA[q] * d2 + r2 * d1;
-              kwp[tb][q] += dH[0][q] * uW[0][q] + Af[q] * rW[q];
-              kmp[tb][q] += dH[0][q] * uM[0][q] + Af[q] * rM[q];
-            } else {
-              const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
-              const float sg = silu_f(hg), s1 = silu_d1(hg), s2 = silu_d2(hg);
-              dH[0][q] = dA[q] * hu * s1;
-              dH[1][q] = dA[q] * sg;
-              const float pg = kwv * uW[0][q] + kmv * uM[0][q];
-              const float pu = kwv * uW[1][q] + kmv * uM[1][q];
-              dAh[q] = pg * hu * s1 + pu * sg;
-              hh[0][q] = pg * dA[q] * hu * s2 + pu * dA[q] * s1 + r2 * hu * s1;
-              hh[1][q] = pg * dA[q] * s1 + r2 * sg;
-              kwp[tb][q] += dH[0][q] * uW[0][q] + dH[1][q] * uW[1][q] + Af[q] * rW[q];
-              kmp[tb][q] += dH[0][q] * uM[0][q] + dH[1][q] * uM[1][q] + Af[q] * rM[q];
-            }
-          }
-#pragma unroll
-          for (int m = 0; m < NF; ++m) { dHq[m][tb][jj] = O::cvt(dH[m]); Hh[m][tb][jj] = hh[m]; }
-          dAhq[tb][jj] = O::cvt(dAh);
-          sched_fence();
-        }
-      // per-wave row partials of dK^W, dK^M
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float sw = group16_sum(kwp[tb][q]);
-          const float sm2 = group16_sum(kmp[tb][q]);
-          if (c == 0) {
-            kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sw;
-            kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sm2;
-          }
-        }
-      // carry adjoints: <Wb, W_0>, <Wb, M_0>, <Mb, M_0>
-      float pcw = 0.0f, pcm = 0.0f, pcb = 0.0f;
-#pragma unroll
-      for (int m = 0; m < NMAT; ++m) {
-        Q q0[NJB][NIB], qm[NJB][NIB];
-        load_ckpt_mat<S>(q0, ckW, m, w, lane);
-        load_ckpt_mat<S>(qm, ckM, m, w, lane);
-#pragma unroll
-        for (int jj = 0; jj < NJB; ++jj)
-#pragma unroll
-          for (int ib = 0; ib < NIB; ++ib) {
-            const f32x4 w0 = quad_f32(q0[jj][ib]), m0 = quad_f32(qm[jj][ib]);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              pcw += Wb.t[m][jj][ib][q] * w0[q];
-              pcm += Wb.t[m][jj][ib][q] * m0[q];
-              pcb += Mb.t[m][jj][ib][q] * m0[q];
-            }
-          }
-      }
-      pcw = wave_sum(pcw);
-      pcm = wave_sum(pcm);
-      pcb = wave_sum(pcb);
-      if (lane == 0) { cbp[w * 4 + 0] = pcw; cbp[w * 4 + 1] = pcm; cbp[w * 4 + 2] = pcb; }
-    }
-    // direct terms through the state adjoint, over the hidden index:
-    //   r1 = K^W (dH Wb1) + K^M (dH Mb1)  (into dK),  p2 = K^W (A Wb2^T) + K^M (A Mb2^T)  (into dYh)
-    JAcc<S> dkacc, dyhacc;
-    dkacc.zero();
-    dyhacc.zero();
-#pragma unroll
-    for (int m = 0; m < NF; ++m) {
-      jround<S>(dkacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
-                [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
-      jround<S>(dkacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
-                [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
-    }
-    jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
-              [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
-    jround<S>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
-              [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
-
-    // ------------------------------------ P5: adjoint state transition
-    {
-      const float cw = scar[0], cm = scar[1], cbv = scar[2];
-#pragma unroll
-      for (int m = 0; m < NMAT; ++m)
-#pragma unroll
-        for (int jj = 0; jj < NJB; ++jj)
-#pragma unroll
-          for (int ib = 0; ib < NIB; ++ib) {
-            const f32x4 wb = Wb.t[m][jj][ib];
-            Mb.t[m][jj][ib] = cm * wb + cbv * Mb.t[m][jj][ib];
-            Wb.t[m][jj][ib] = cw * wb;
-          }
-    }
-
-    // --------------------------- P6: dYh = p2 + dAh W2^T  (into RR, fp32)
-    {
-      Q w2q[NJB][NIB];
-      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
-      jround<S>(dyhacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(dAhq[tb][jj]); },
-                [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
-      float* dyh = reinterpret_cast<float*>(rr);
-      constexpr int NI = NIB / S::IBB;
-#pragma unroll
-      for (int aa = 0; aa < L::JIT; ++aa) {
-        const int it = w + aa * NW;
-        if (it < L::NITEM) {
-          const int tb = it / NI, ib0 = (it % NI) * S::IBB;
-#pragma unroll
-          for (int b = 0; b < S::IBB; ++b)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              dyh[(16 * tb + 4 * g + q) * D + 16 * (ib0 + b) + c] = dyhacc.v[aa][b][q];
-        }
-      }
-    }
-    __syncthreads();
-
-    // ------------------------------------- P7: LayerNorm second order
-    {
-      const float* dyh = reinterpret_cast<const float*>(rr);
-      using IOT = typename IoT<S::BF>::T;
-      IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
-#pragma unroll 1
-      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
-        const int t = t0 + (lane >> 4);
-        float dyhv[EPL], e[EPL], eh[EPL], yhv[EPL];
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-          dyhv[q] = dyh[t * D + l16 * EPL + q];
-          e[q] = ek[t * D + l16 * EPL + q];
-        }
-        if (resln) {
-          float z[EPL], dyv[EPL], zh[EPL];
-          const float sig = row[2 * t], mez = row[2 * t + 1];
-          float se = 0.0f, m1 = 0.0f, m2 = 0.0f;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            z[q] = yk[t * D + l16 * EPL + q];
-            se += e[q];
-            m1 += dyhv[q];
-            m2 += dyhv[q] * z[q];
-          }
-          const float me = group16_sum(se) * inv_d;
-          m1 = group16_sum(m1) * inv_d;
-          m2 = group16_sum(m2) * inv_d;
-          float sdd = 0.0f;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            dyv[q] = (e[q] - me - z[q] * mez) * sig;
-            eh[q] = (dyhv[q] - m1 - z[q] * m2) * sig;
-            sdd += dyhv[q] * dyv[q];
-          }
-          const float sh = -group16_sum(sdd) * sig;
-          float n1 = 0.0f, n2 = 0.0f;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            zh[q] = -(dyhv[q] * mez + e[q] * m2) * sig - eh[q];
-            n1 += zh[q];
-            n2 += zh[q] * z[q];
-          }
-          n1 = group16_sum(n1) * inv_d;
-          n2 = group16_sum(n2) * inv_d;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) yhv[q] = (zh[q] - n1 - z[q] * n2) * sig + sh * z[q] * inv_d;
-        } else {
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) { eh[q] = dyhv[q]; yhv[q] = -eh[q]; }
-        }
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-          const int i = l16 * EPL + q;
-          ek[t * D + i] = eh[q];
-          yh[t * S::LDD + i] = O::to_e(yhv[q]);
-          yht[i * S::LDC + t] = O::to_e(yhv[q]);
-          if (t < len) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
-        }
-      }
-    }
-    __syncthreads();
-
-    // ------------ P8: Hh += (Yh W2) act'(H); accumulate into Wb; dk = r1 - eh + Hh W1
-    {
-      // K^T into RR for the first-layer accumulation
-      E* xkt = reinterpret_cast<E*>(rr);
-#pragma unroll 1
-      for (int idx = tid; idx < D * S::CM; idx += S::NT) {
-        const int i = idx % D, t = idx / D;
-        xkt[i * S::LDC + t] = xk[t * S::LDD + i];
-      }
-      Q w2q[NJB][NIB];
-      load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-        for (int jj = 0; jj < NJB; ++jj) {
-          f32x4 ah = zero4();
-#pragma unroll
-          for (int p = 0; p < S::KS_D; ++p) {
-            auto af = lds_frag<S::BF>(yh, S::LDD, 16 * tb + c, p * S::KC, g);
-            typename O::Frag bf;
-#pragma unroll
-            for (int h = 0; h < S::NH; ++h) bf.h[h] = w2q[jj][S::NH * p + h];
-            ah = O::mma(ah, af, bf);
-          }
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if constexpr (!SW) {
-              Hh[0][tb][jj][q] += ah[q] * gelu_d1(Hk[0][tb][jj][q]);
-            } else {
-              const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
-              Hh[0][tb][jj][q] += ah[q] * hu * silu_d1(hg);
-              Hh[1][tb][jj][q] += ah[q] * silu_f(hg);
-            }
-          }
-          sched_fence();
-        }
-      __syncthreads();   // xkt complete
-      // Wb2 += dY^T dAh + Yh^T A ;  Wb1 += K^T Hh
-      opaque_state<S>(Wb);
-#pragma unroll
-      for (int jj = 0; jj < NJB; ++jj)
-#pragma unroll
-        for (int ib = 0; ib < NIB; ++ib) {
-#pragma unroll
-          for (int p = 0; p < S::KS_C; ++p) {
-            typename O::Frag bd, ba;
-#pragma unroll
-            for (int h = 0; h < S::NH; ++h) {
-              bd.h[h] = dAhq[S::NH * p + h][jj];
-              ba.h[h] = Akq[S::NH * p + h][jj];
-            }
-            const int rowi = 16 * ib + c, k0 = p * S::KC;
-            Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(dyt, S::LDC, rowi, k0, g), bd);
-            Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(yht, S::LDC, rowi, k0, g), ba);
-            auto fk = lds_frag<S::BF>(xkt, S::LDC, rowi, k0, g);
-#pragma unroll
-            for (int m = 0; m < NF; ++m) {
-              typename O::Frag bh;
-#pragma unroll
-              for (int h = 0; h < S::NH; ++h) bh.h[h] = O::cvt(Hh[m][S::NH * p + h][jj]);
-              Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fk, bh);
-            }
-          }
-          sched_fence();
-        }
-      // dk += Hh W1 (over the hidden index)
-#pragma unroll
-      for (int m = 0; m < NF; ++m) {
-        Q w1q[NJB][NIB];
-        load_ckpt_mat<S>(w1q, ckW, m, w, lane);
-        jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return Hh[m][tb][jj]; },
-                  [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
-      }
-      const float ksign = resln ? -1.0f : 0.0f;
-      jacc_store_io<S>(dkacc, a.dk, row0, len,
-                       [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
-    }
-    __syncthreads();
-
-    // -------------------------------------------- P9: output branch
-    {
-      E* xq = xk;                                      // Q [t][i]
-      E* xdo = reinterpret_cast<E*>(rr);               // dO [t][i]
-      E* ybq = yh;                                     // Yb_Q [t][i]
-      E* ybqt = dyt;                                   // Yb_Q^T [i][t]
-      E* xqt = yht;                                    // Q^T [i][t]
-      stage_tile<S>(xq, a.q, row0, len, tid);
-      stage_tile<S>(xdo, a.d_out, row0, len, tid);
+      if (tid < 3) scar[tid] = a.carry[(u * NC + r) * 3 + tid];
       __syncthreads();
-#pragma unroll 1
-      for (int idx = tid; idx < D * S::CM; idx += S::NT) {
-        const int i = idx % D, t = idx / D;
-        xqt[i * S::LDC + t] = xq[t * S::LDD + i];
-      }
-      f32x4 Hq[NF][NTB][NJB];
-      Q Aqq[NTB][NJB];
+
+      // ------------------------------------ P1: H = K W1^T, A = act(H) (recompute)
+      f32x4 Hk[NF][NTB][NJB];
+      Q Akq[NTB][NJB];
       {
         Q w1q[NF][NJB][NIB];
 #pragma unroll
@@ -703,7 +350,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             for (int m = 0; m < NF; ++m) acc[m] = zero4();
 #pragma unroll
             for (int p = 0; p < S::KS_D; ++p) {
-              auto af = lds_frag<S::BF>(xq, S::LDD, 16 * tb + c, p * S::KC, g);
+              auto af = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
 #pragma unroll
               for (int m = 0; m < NF; ++m) {
                 typename O::Frag bf;
@@ -719,185 +366,628 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               else act[q] = silu_f(acc[0][q]) * acc[1][q];
             }
 #pragma unroll
-            for (int m = 0; m < NF; ++m) Hq[m][tb][jj] = acc[m];
-            Aqq[tb][jj] = O::cvt(act);
+            for (int m = 0; m < NF; ++m) Hk[m][tb][jj] = acc[m];
+            Akq[tb][jj] = O::cvt(act);
             sched_fence();
           }
       }
-      {
-        JAcc<S> yacc;
-        yacc.zero();
-        Q w2q[NJB][NIB];
-        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
-        jround<S>(yacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(Aqq[tb][jj]); },
-                  [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
-        constexpr int NI = NIB / S::IBB;
-#pragma unroll
-        for (int aa = 0; aa < L::JIT; ++aa) {
-          const int it = w + aa * NW;
-          if (it < L::NITEM) {
-            const int tb = it / NI, ib0 = (it % NI) * S::IBB;
-#pragma unroll
-            for (int b = 0; b < S::IBB; ++b)
-#pragma unroll
-              for (int q = 0; q < 4; ++q)
-                yk[(16 * tb + 4 * g + q) * D + 16 * (ib0 + b) + c] = yacc.v[aa][b][q];
-          }
-        }
-      }
-      __syncthreads();
-      // Yb_Q = LN backward of dO at the Q rows (dO itself when there is no LN)
+
+      // --------------------- P3: e, dY (first order, from the saved LN output)
+      E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
 #pragma unroll 1
       for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
         const int t = t0 + (lane >> 4);
-        float dov[EPL], yb[EPL];
+        float z[EPL], e[EPL], dyv[EPL];
+        float mez = 0.0f;
 #pragma unroll
-        for (int q = 0; q < EPL; ++q) dov[q] = O::from_e(xdo[t * S::LDD + l16 * EPL + q]);
+        for (int q = 0; q < EPL; ++q) z[q] = yk[t * D + l16 * EPL + q];
         if (resln) {
-          float yv[EPL], s1 = 0.0f;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) { yv[q] = yk[t * D + l16 * EPL + q]; s1 += yv[q]; }
-          const float mu = group16_sum(s1) * inv_d;
-          float s2 = 0.0f;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
-          const float sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
-          float m1 = 0.0f, m2 = 0.0f;
+          const float sig = row[2 * t];
+          float se = 0.0f, sez = 0.0f;
 #pragma unroll
           for (int q = 0; q < EPL; ++q) {
-            yv[q] *= sig;              // z
-            m1 += dov[q];
-            m2 += dov[q] * yv[q];
+            const int i = l16 * EPL + q;
+            e[q] = O::from_e(xv[t * S::LDD + i]) - O::from_e(xk[t * S::LDD + i]) - z[q];
+            se += e[q];
+            sez += e[q] * z[q];
           }
-          m1 = group16_sum(m1) * inv_d;
-          m2 = group16_sum(m2) * inv_d;
+          const float me = group16_sum(se) * inv_d;
+          mez = group16_sum(sez) * inv_d;
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) yb[q] = (dov[q] - m1 - yv[q] * m2) * sig;
+          for (int q = 0; q < EPL; ++q) dyv[q] = (e[q] - me - z[q] * mez) * sig;
         } else {
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) yb[q] = dov[q];
+          for (int q = 0; q < EPL; ++q) {
+            e[q] = O::from_e(xv[t * S::LDD + l16 * EPL + q]) - z[q];
+            dyv[q] = e[q];
+            z[q] = 0.0f;
+          }
         }
 #pragma unroll
         for (int q = 0; q < EPL; ++q) {
           const int i = l16 * EPL + q;
-          ybq[t * S::LDD + i] = O::to_e(yb[q]);
-          ybqt[i * S::LDC + t] = O::to_e(yb[q]);
+          yk[t * D + i] = z[q];
+          ek[t * D + i] = e[q];
+          dyl[t * S::LDD + i] = O::to_e(dyv[q]);
+          dyt[i * S::LDC + t] = O::to_e(dyv[q]);
+        }
+        if (l16 == 0) row[2 * t + 1] = mez;
+      }
+      __syncthreads();
+
+      // ----------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
+      // For every tile: dA = dY W2, dH = dA act'(H);  u = K Wb1^T, K Mb1^T;
+      // rW = dY Wb2, dY Mb2;  dK^W += rowsum(dH uW + A rW), dK^M likewise;
+      // p = K^W uW + K^M uM (= d(Phi)/d(dH)), r2 = K^W rW + K^M rM (direct a-term);
+      // dAh = p act'(H);  Hh = p dA act''(H) + r2 act'(H)  (the Yh W2 term is added later)
+      Q dHq[NF][NTB][NJB];
+      Q dAhq[NTB][NJB];
+      f32x4 Hh[NF][NTB][NJB];
+      {
+        Q w2q[NJB][NIB];
+        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+        opaque_state<S>(Wb);
+        opaque_state<S>(Mb);
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb) {
+          float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            f32x4 dA = zero4(), rW = zero4(), rM = zero4();
+            f32x4 uW[NF], uM[NF];
+#pragma unroll
+            for (int m = 0; m < NF; ++m) { uW[m] = zero4(); uM[m] = zero4(); }
+#pragma unroll
+            for (int p = 0; p < S::KS_D; ++p) {
+              auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
+              auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
+              typename O::Frag b2, bw, bm;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) {
+                b2.h[h] = w2q[jj][S::NH * p + h];
+                bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
+                bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
+              }
+              dA = O::mma(dA, fy, b2);
+              rW = O::mma(rW, fy, bw);
+              rM = O::mma(rM, fy, bm);
+#pragma unroll
+              for (int m = 0; m < NF; ++m) {
+#pragma unroll
+                for (int h = 0; h < S::NH; ++h) {
+                  bw.h[h] = O::cvt(Wb.t[m][jj][S::NH * p + h]);
+                  bm.h[h] = O::cvt(Mb.t[m][jj][S::NH * p + h]);
+                }
+                uW[m] = O::mma(uW[m], fk, bw);
+                uM[m] = O::mma(uM[m], fk, bm);
+              }
+            }
+            const f32x4 Af = quad_f32(Akq[tb][jj]);
+            f32x4 dH[NF], dAh, hh[NF];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int t = 16 * tb + 4 * g + q;
+              const float kwv = skw[t], kmv = skm[t];
+              const float r2 = kwv * rW[q] + kmv * rM[q];
+              if constexpr (!SW) {
+                const float h = Hk[0][tb][jj][q];
+                const float d1 = gelu_d1(h), d2 = gelu_d2(h);
+                dH[0][q] = dA[q] * d1;
+                const float pp = kwv * uW[0][q] + kmv * uM[0][q];
+                dAh[q] = pp * d1;
+                hh[0][q] = pp * dA[q] * d2 + r2 * d1;
+                kwp[q] += dH[0][q] * uW[0][q] + Af[q] * rW[q];
+                kmp[q] += dH[0][q] * uM[0][q] + Af[q] * rM[q];
+              } else {
+                const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
+                const float sg = silu_f(hg), s1 = silu_d1(hg), s2 = silu_d2(hg);
+                dH[0][q] = dA[q] * hu * s1;
+                dH[1][q] = dA[q] * sg;
+                const float pg = kwv * uW[0][q] + kmv * uM[0][q];
+                const float pu = kwv * uW[1][q] + kmv * uM[1][q];
+                dAh[q] = pg * hu * s1 + pu * sg;
+                hh[0][q] = pg * dA[q] * hu * s2 + pu * dA[q] * s1 + r2 * hu * s1;
+                hh[1][q] = pg * dA[q] * s1 + r2 * sg;
+                kwp[q] += dH[0][q] * uW[0][q] + dH[1][q] * uW[1][q] + Af[q] * rW[q];
+                kmp[q] += dH[0][q] * uM[0][q] + dH[1][q] * uM[1][q] + Af[q] * rM[q];
+              }
+            }
+#pragma unroll
+            for (int m = 0; m < NF; ++m) { dHq[m][tb][jj] = O::cvt(dH[m]); Hh[m][tb][jj] = hh[m]; }
+            dAhq[tb][jj] = O::cvt(dAh);
+            sched_fence();
+          }
+          // per-wave row partials of dK^W, dK^M for this token block
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float sw = group16_sum(kwp[q]);
+            const float sm2 = group16_sum(kmp[q]);
+            if (c == 0) {
+              kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sw;
+              kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sm2;
+            }
+          }
+        }
+        // carry adjoints: <Wb, W_0>, <Wb, M_0>, <Mb, M_0>
+        float pcw = 0.0f, pcm = 0.0f, pcb = 0.0f;
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m) {
+          Q q0[NJB][NIB], qm[NJB][NIB];
+          load_ckpt_mat<S>(q0, ckW, m, w, lane);
+          load_ckpt_mat<S>(qm, ckM, m, w, lane);
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+              const f32x4 w0 = quad_f32(q0[jj][ib]), m0 = quad_f32(qm[jj][ib]);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                pcw += Wb.t[m][jj][ib][q] * w0[q];
+                pcm += Wb.t[m][jj][ib][q] * m0[q];
+                pcb += Mb.t[m][jj][ib][q] * m0[q];
+              }
+            }
+        }
+        pcw = wave_sum(pcw);
+        pcm = wave_sum(pcm);
+        pcb = wave_sum(pcb);
+        if (lane == 0) { cbp[w * 4 + 0] = pcw; cbp[w * 4 + 1] = pcm; cbp[w * 4 + 2] = pcb; }
+      }
+      // direct terms through the state adjoint, over the hidden index:
+      //   r1 = K^W (dH Wb1) + K^M (dH Mb1)  (into dK),  p2 = K^W (A Wb2^T) + K^M (A Mb2^T)  (into dYh)
+      JAcc<S> dkacc, dyhacc;
+      dkacc.zero();
+      dyhacc.zero();
+#pragma unroll
+      for (int m = 0; m < NF; ++m) {
+        jround<S>(dkacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
+                  [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
+        jround<S>(dkacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
+                  [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+      }
+      jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+                [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
+      jround<S>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+                [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+
+      // ------------------------------------ P5: adjoint state transition
+      {
+        const float cw = scar[0], cm = scar[1], cbv = scar[2];
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+              const f32x4 wb = Wb.t[m][jj][ib];
+              Mb.t[m][jj][ib] = cm * wb + cbv * Mb.t[m][jj][ib];
+              Wb.t[m][jj][ib] = cw * wb;
+            }
+      }
+
+      // --------------------------- P6: dYh = p2 + dAh W2^T  (into RR, fp32)
+      float* dyh = reinterpret_cast<float*>(rr);
+      {
+        Q w2q[NJB][NIB];
+        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+        jround<S>(dyhacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(dAhq[tb][jj]); },
+                  [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
+        jacc_store_f32<S>(dyhacc, dyh, [](int, int) { return 0.0f; }, w, g, c);
+      }
+      __syncthreads();
+      const float* dyh_peer = nullptr;
+      if constexpr (S::NS > 1) {
+        float* mine = bwd_slot<S>(a.xbuf, px.p, rank, par);
+#pragma unroll 1
+        for (int v = tid; v < S::CM * D / 4; v += S::NT)
+          reinterpret_cast<float4*>(mine)[v] = reinterpret_cast<const float4*>(dyh)[v];
+        px.post();                                  // seq0 + 1: dYh partial
+        px.wait_for(seq0 + 1, sword);               // the peer's
+        dyh_peer = bwd_slot<S>(a.xbuf, px.p, 1 - rank, par);
+        if (pend_r >= 0)
+          flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
+                        tid);
+      }
+
+      // ------------------------------------- P7: LayerNorm second order
+      {
+        using IOT = typename IoT<S::BF>::T;
+        IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
+#pragma unroll 1
+        for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+          const int t = t0 + (lane >> 4);
+          float dyhv[EPL], e[EPL], eh[EPL], yhv[EPL];
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            dyhv[q] = dyh[t * D + l16 * EPL + q];
+            e[q] = ek[t * D + l16 * EPL + q];
+          }
+          if constexpr (S::NS > 1) {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) dyhv[q] += dyh_peer[t * D + l16 * EPL + q];
+          }
+          if (resln) {
+            float z[EPL], dyv[EPL], zh[EPL];
+            const float sig = row[2 * t], mez = row[2 * t + 1];
+            float se = 0.0f, m1 = 0.0f, m2 = 0.0f;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) {
+              z[q] = yk[t * D + l16 * EPL + q];
+              se += e[q];
+              m1 += dyhv[q];
+              m2 += dyhv[q] * z[q];
+            }
+            const float me = group16_sum(se) * inv_d;
+            m1 = group16_sum(m1) * inv_d;
+            m2 = group16_sum(m2) * inv_d;
+            float sdd = 0.0f;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) {
+              dyv[q] = (e[q] - me - z[q] * mez) * sig;
+              eh[q] = (dyhv[q] - m1 - z[q] * m2) * sig;
+              sdd += dyhv[q] * dyv[q];
+            }
+            const float sh = -group16_sum(sdd) * sig;
+            float n1 = 0.0f, n2 = 0.0f;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) {
+              zh[q] = -(dyhv[q] * mez + e[q] * m2) * sig - eh[q];
+              n1 += zh[q];
+              n2 += zh[q] * z[q];
+            }
+            n1 = group16_sum(n1) * inv_d;
+            n2 = group16_sum(n2) * inv_d;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) yhv[q] = (zh[q] - n1 - z[q] * n2) * sig + sh * z[q] * inv_d;
+          } else {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) { eh[q] = dyhv[q]; yhv[q] = -eh[q]; }
+          }
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            const int i = l16 * EPL + q;
+            ek[t * D + i] = eh[q];
+            yh[t * S::LDD + i] = O::to_e(yhv[q]);
+            yht[i * S::LDC + t] = O::to_e(yhv[q]);
+            if (t < len && t >= rlo && t < rlo + RPW) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
+          }
         }
       }
       __syncthreads();
-      // Ab_Q = Yb_Q W2;  Hb_Q = Ab_Q act'(H_Q);  Wb2 += Yb_Q^T A_Q;  Wb1 += Q^T Hb_Q
-      Q Hbq[NF][NTB][NJB];
+
+      // ---------- P8: Hh += (Yh W2) act'(H); accumulate into Wb; dk = r1 - eh + Hh W1
       {
+        // K^T into RR for the first-layer accumulation
+        E* xkt = reinterpret_cast<E*>(rr);
+#pragma unroll 1
+        for (int idx = tid; idx < D * S::CM; idx += S::NT) {
+          const int i = idx % D, t = idx / D;
+          xkt[i * S::LDC + t] = xk[t * S::LDD + i];
+        }
         Q w2q[NJB][NIB];
         load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
 #pragma unroll
         for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
           for (int jj = 0; jj < NJB; ++jj) {
-            f32x4 ab = zero4();
+            f32x4 ah = zero4();
 #pragma unroll
             for (int p = 0; p < S::KS_D; ++p) {
-              auto af = lds_frag<S::BF>(ybq, S::LDD, 16 * tb + c, p * S::KC, g);
+              auto af = lds_frag<S::BF>(yh, S::LDD, 16 * tb + c, p * S::KC, g);
               typename O::Frag bf;
 #pragma unroll
               for (int h = 0; h < S::NH; ++h) bf.h[h] = w2q[jj][S::NH * p + h];
-              ab = O::mma(ab, af, bf);
+              ah = O::mma(ah, af, bf);
             }
-            f32x4 hb[NF];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               if constexpr (!SW) {
-                hb[0][q] = ab[q] * gelu_d1(Hq[0][tb][jj][q]);
+                Hh[0][tb][jj][q] += ah[q] * gelu_d1(Hk[0][tb][jj][q]);
               } else {
-                const float hg = Hq[0][tb][jj][q], hu = Hq[1][tb][jj][q];
-                hb[0][q] = ab[q] * hu * silu_d1(hg);
-                hb[1][q] = ab[q] * silu_f(hg);
+                const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
+                Hh[0][tb][jj][q] += ah[q] * hu * silu_d1(hg);
+                Hh[1][tb][jj][q] += ah[q] * silu_f(hg);
               }
             }
-#pragma unroll
-            for (int m = 0; m < NF; ++m) Hbq[m][tb][jj] = O::cvt(hb[m]);
             sched_fence();
           }
-      }
-      opaque_state<S>(Wb);
+        __syncthreads();   // xkt complete
+        // Wb2 += dY^T dAh + Yh^T A ;  Wb1 += K^T Hh
+        opaque_state<S>(Wb);
 #pragma unroll
-      for (int jj = 0; jj < NJB; ++jj)
+        for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-        for (int ib = 0; ib < NIB; ++ib) {
+          for (int ib = 0; ib < NIB; ++ib) {
 #pragma unroll
-          for (int p = 0; p < S::KS_C; ++p) {
-            typename O::Frag ba;
+            for (int p = 0; p < S::KS_C; ++p) {
+              typename O::Frag bd, ba;
 #pragma unroll
-            for (int h = 0; h < S::NH; ++h) ba.h[h] = Aqq[S::NH * p + h][jj];
-            const int rowi = 16 * ib + c, k0 = p * S::KC;
-            Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(ybqt, S::LDC, rowi, k0, g), ba);
-            auto fq = lds_frag<S::BF>(xqt, S::LDC, rowi, k0, g);
+              for (int h = 0; h < S::NH; ++h) {
+                bd.h[h] = dAhq[S::NH * p + h][jj];
+                ba.h[h] = Akq[S::NH * p + h][jj];
+              }
+              const int rowi = 16 * ib + c, k0 = p * S::KC;
+              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(dyt, S::LDC, rowi, k0, g), bd);
+              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(yht, S::LDC, rowi, k0, g), ba);
+              auto fk = lds_frag<S::BF>(xkt, S::LDC, rowi, k0, g);
 #pragma unroll
-            for (int m = 0; m < NF; ++m) {
-              typename O::Frag bh;
+              for (int m = 0; m < NF; ++m) {
+                typename O::Frag bh;
 #pragma unroll
-              for (int h = 0; h < S::NH; ++h) bh.h[h] = Hbq[m][S::NH * p + h][jj];
-              Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fq, bh);
+                for (int h = 0; h < S::NH; ++h) bh.h[h] = O::cvt(Hh[m][S::NH * p + h][jj]);
+                Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fk, bh);
+              }
             }
+            sched_fence();
           }
-          sched_fence();
-        }
-      // dq = dO (residual) + Hb_Q W1 (over the hidden index)
-      JAcc<S> dqacc;
-      dqacc.zero();
+        // dk += Hh W1 (over the hidden index)
 #pragma unroll
-      for (int m = 0; m < NF; ++m) {
-        Q w1q[NJB][NIB];
-        load_ckpt_mat<S>(w1q, ckW, m, w, lane);
-        jround<S>(dqacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(Hbq[m][tb][jj]); },
-                  [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
+        for (int m = 0; m < NF; ++m) {
+          Q w1q[NJB][NIB];
+          load_ckpt_mat<S>(w1q, ckW, m, w, lane);
+          jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return Hh[m][tb][jj]; },
+                    [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
+        }
+        const float ksign = (resln && rank == 0) ? -1.0f : 0.0f;
+        if constexpr (S::NS > 1) {
+          jacc_store_f32<S>(dkacc, bwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D,
+                            [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
+        } else {
+          jacc_store_io<S>(dkacc, a.dk, row0, len,
+                           [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
+        }
       }
-      const float qsign = resln ? 1.0f : 0.0f;
-      jacc_store_io<S>(dqacc, a.dq, row0, len,
-                       [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); }, w, g,
-                       c);
-    }
+      __syncthreads();
 
-    // ------------------------------ P10: scalar-kernel adjoints of this chunk
+      // -------------------------------------------- P9: output branch
+      {
+        E* xq = xk;                                      // Q [t][i]
+        E* xdo = reinterpret_cast<E*>(rr);               // dO [t][i]
+        E* ybq = yh;                                     // Yb_Q [t][i]
+        E* ybqt = dyt;                                   // Yb_Q^T [i][t]
+        E* xqt = yht;                                    // Q^T [i][t]
+        stage_tile<S>(xq, a.q, row0, len, tid);
+        stage_tile<S>(xdo, a.d_out, row0, len, tid);
+        stage_f32<S>(yk, a.zq, row0, len, tid);         // Z_Q (or Y_Q)
 #pragma unroll 1
-    for (int t = tid; t < len; t += S::NT) {
-      float sw = 0.0f, sm2 = 0.0f;
-      for (int ww = 0; ww < NW; ++ww) {
-        sw += kb[(0 * NW + ww) * S::CM + t];
-        sm2 += kb[(1 * NW + ww) * S::CM + t];
+        for (int t = tid; t < S::CM; t += S::NT) row[2 * t] = (t < len) ? a.rq[row0 + t] : 0.0f;
+        __syncthreads();
+#pragma unroll 1
+        for (int idx = tid; idx < D * S::CM; idx += S::NT) {
+          const int i = idx % D, t = idx / D;
+          xqt[i * S::LDC + t] = xq[t * S::LDD + i];
+        }
+        // Yb_Q = LN backward of dO at the Q rows (dO itself when there is no LN)
+#pragma unroll 1
+        for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+          const int t = t0 + (lane >> 4);
+          float dov[EPL], yb[EPL];
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) dov[q] = O::from_e(xdo[t * S::LDD + l16 * EPL + q]);
+          if (resln) {
+            const float sig = row[2 * t];
+            float z[EPL], m1 = 0.0f, m2 = 0.0f;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) {
+              z[q] = yk[t * D + l16 * EPL + q];
+              m1 += dov[q];
+              m2 += dov[q] * z[q];
+            }
+            m1 = group16_sum(m1) * inv_d;
+            m2 = group16_sum(m2) * inv_d;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) yb[q] = (dov[q] - m1 - z[q] * m2) * sig;
+          } else {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) yb[q] = dov[q];
+          }
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            const int i = l16 * EPL + q;
+            ybq[t * S::LDD + i] = O::to_e(yb[q]);
+            ybqt[i * S::LDC + t] = O::to_e(yb[q]);
+          }
+        }
+        f32x4 Hq[NF][NTB][NJB];
+        Q Aqq[NTB][NJB];
+        {
+          Q w1q[NF][NJB][NIB];
+#pragma unroll
+          for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
+#pragma unroll
+          for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj) {
+              f32x4 acc[NF];
+#pragma unroll
+              for (int m = 0; m < NF; ++m) acc[m] = zero4();
+#pragma unroll
+              for (int p = 0; p < S::KS_D; ++p) {
+                auto af = lds_frag<S::BF>(xq, S::LDD, 16 * tb + c, p * S::KC, g);
+#pragma unroll
+                for (int m = 0; m < NF; ++m) {
+                  typename O::Frag bf;
+#pragma unroll
+                  for (int h = 0; h < S::NH; ++h) bf.h[h] = w1q[m][jj][S::NH * p + h];
+                  acc[m] = O::mma(acc[m], af, bf);
+                }
+              }
+              f32x4 act;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                if constexpr (!SW) act[q] = gelu_f(acc[0][q]);
+                else act[q] = silu_f(acc[0][q]) * acc[1][q];
+              }
+#pragma unroll
+              for (int m = 0; m < NF; ++m) Hq[m][tb][jj] = acc[m];
+              Aqq[tb][jj] = O::cvt(act);
+              sched_fence();
+            }
+        }
+        __syncthreads();
+        // Ab_Q = Yb_Q W2;  Hb_Q = Ab_Q act'(H_Q);  Wb2 += Yb_Q^T A_Q;  Wb1 += Q^T Hb_Q
+        Q Hbq[NF][NTB][NJB];
+        {
+          Q w2q[NJB][NIB];
+          load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+#pragma unroll
+          for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj) {
+              f32x4 ab = zero4();
+#pragma unroll
+              for (int p = 0; p < S::KS_D; ++p) {
+                auto af = lds_frag<S::BF>(ybq, S::LDD, 16 * tb + c, p * S::KC, g);
+                typename O::Frag bf;
+#pragma unroll
+                for (int h = 0; h < S::NH; ++h) bf.h[h] = w2q[jj][S::NH * p + h];
+                ab = O::mma(ab, af, bf);
+              }
+              f32x4 hb[NF];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                if constexpr (!SW) {
+                  hb[0][q] = ab[q] * gelu_d1(Hq[0][tb][jj][q]);
+                } else {
+                  const float hg = Hq[0][tb][jj][q], hu = Hq[1][tb][jj][q];
+                  hb[0][q] = ab[q] * hu * silu_d1(hg);
+                  hb[1][q] = ab[q] * silu_f(hg);
+                }
+              }
+#pragma unroll
+              for (int m = 0; m < NF; ++m) Hbq[m][tb][jj] = O::cvt(hb[m]);
+              sched_fence();
+            }
+        }
+        opaque_state<S>(Wb);
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+          for (int ib = 0; ib < NIB; ++ib) {
+#pragma unroll
+            for (int p = 0; p < S::KS_C; ++p) {
+              typename O::Frag ba;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) ba.h[h] = Aqq[S::NH * p + h][jj];
+              const int rowi = 16 * ib + c, k0 = p * S::KC;
+              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(ybqt, S::LDC, rowi, k0, g), ba);
+              auto fq = lds_frag<S::BF>(xqt, S::LDC, rowi, k0, g);
+#pragma unroll
+              for (int m = 0; m < NF; ++m) {
+                typename O::Frag bh;
+#pragma unroll
+                for (int h = 0; h < S::NH; ++h) bh.h[h] = Hbq[m][S::NH * p + h][jj];
+                Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fq, bh);
+              }
+            }
+            sched_fence();
+          }
+        // dq = dO (residual) + Hb_Q W1 (over the hidden index)
+        JAcc<S> dqacc;
+        dqacc.zero();
+#pragma unroll
+        for (int m = 0; m < NF; ++m) {
+          Q w1q[NJB][NIB];
+          load_ckpt_mat<S>(w1q, ckW, m, w, lane);
+          jround<S>(dqacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(Hbq[m][tb][jj]); },
+                    [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
+        }
+        const float qsign = (resln && rank == 0) ? 1.0f : 0.0f;
+        if constexpr (S::NS > 1) {
+          jacc_store_f32<S>(dqacc, bwd_slot<S>(a.xbuf, px.p, rank, par) + 2 * S::CM * D,
+                            [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); },
+                            w, g, c);
+        } else {
+          jacc_store_io<S>(dqacc, a.dq, row0, len,
+                           [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); },
+                           w, g, c);
+        }
       }
-      a.kwb[row0 + t] = sw;
-      a.kmb[row0 + t] = sm2;
-    }
-    if (tid < 3) {
-      float s = 0.0f;
-      for (int ww = 0; ww < NW; ++ww) s += cbp[ww * 4 + tid];
-      a.carryb[(u * NC + r) * 3 + tid] = s;
-    }
-    __syncthreads();
-  }
 
-  store_state<S>(Wb, a.d_w_in + u * a.P, dh, w, g, c);
-  store_state<S>(Mb, a.d_m_in + u * a.P, dh, w, g, c);
+      // ------------------------------ P10: scalar-kernel adjoints of this chunk
+#pragma unroll 1
+      for (int t = tid; t < len; t += S::NT) {
+        float sw = 0.0f, sm2 = 0.0f;
+        for (int ww = 0; ww < NW; ++ww) {
+          sw += kb[(0 * NW + ww) * S::CM + t];
+          sm2 += kb[(1 * NW + ww) * S::CM + t];
+        }
+        kwb_slot[row0 + t] = sw;
+        kmb_slot[row0 + t] = sm2;
+      }
+      if (tid < 3) {
+        float sacc = 0.0f;
+        for (int ww = 0; ww < NW; ++ww) sacc += cbp[ww * 4 + tid];
+        carryb_slot[(u * NC + r) * 3 + tid] = sacc;
+      }
+      if constexpr (S::NS > 1) {
+        px.post();                                  // seq0 + 2: dk, dq partials
+        pend_r = r;
+        pend_par = par;
+      } else {
+        __syncthreads();
+      }
+    }
+
+    if constexpr (S::NS > 1) {
+      px.wait_for(px.seq_now(), sword);             // the peer's last post
+      if (pend_r >= 0)
+        flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
+                      tid);
+      __syncthreads();
+    }
+    store_state<S>(Wb, a.d_w_in + u * a.P, dh, j0, w, g, c);
+    store_state<S>(Mb, a.d_m_in + u * a.P, dh, j0, w, g, c);
+  }
 }
 
 template <class S>
-hipError_t launch(const ChainArgs& a, long units, hipStream_t stream) {
-  hipLaunchKernelGGL(chain_bwd_kernel<S>, dim3((unsigned)units), dim3(S::NT), 0, stream, a);
-  return hipGetLastError();
+int max_blocks_per_cu() {
+  static int nb = [] {
+    int v = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_bwd_kernel<S>, S::NT, 0) !=
+        hipSuccess)
+      v = 0;
+    return v;
+  }();
+  return nb;
+}
+
+template <class S>
+hipError_t launch(const ChainArgs& a, hipStream_t stream) {
+  if constexpr (S::NS == 1) {
+    hipLaunchKernelGGL(chain_bwd_kernel<S>, dim3((unsigned)a.U), dim3(S::NT), 0, stream, a);
+    return hipGetLastError();
+  } else {
+    ChainArgs b = a;
+    void* args[] = {&b};
+    return hipLaunchCooperativeKernel((const void*)chain_bwd_kernel<S>,
+                                      dim3((unsigned)(2 * a.npairs)), dim3(S::NT), args, 0,
+                                      stream);
+  }
 }
 
 }  // namespace
 
-#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF)                                              \
+#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF, NS)                                          \
   if (cfg.fw == FW && cfg.d == D && cfg.nw == NW && cfg.njb == NJB && cfg.ntb == NTB && \
-      cfg.bf == BF)                                                                     \
-    return launch<Shape<FW, D, NW, NJB, NTB, BF>>(a, units, stream);
+      cfg.bf == BF && cfg.ns == NS)                                                     \
+    return launch<Shape<FW, D, NW, NJB, NTB, BF, NS>>(a, stream);
 
-hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, long units,
-                            hipStream_t stream) {
+hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream) {
 #include "chain_variants.inc"
   return hipErrorInvalidValue;
+}
+#undef E2TTT_CASE
+
+#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF, NS)                                          \
+  if (cfg.fw == FW && cfg.d == D && cfg.nw == NW && cfg.njb == NJB && cfg.ntb == NTB && \
+      cfg.bf == BF && cfg.ns == NS)                                                     \
+    return max_blocks_per_cu<Shape<FW, D, NW, NJB, NTB, BF, NS>>();
+
+int chain_bwd_blocks_per_cu(const ChainConfig& cfg) {
+#include "chain_variants.inc"
+  return 0;
 }
 #undef E2TTT_CASE
 

@@ -1,9 +1,10 @@
 // Shape constants and register-resident state handling shared by the forward
 // and backward chain kernels.
 //
-// One workgroup owns one (batch, head) unit for the whole sequence.  Its NW
-// waves split the fast-weight hidden dimension: wave w owns the hidden columns
-// j in [16 w NJB, 16 (w+1) NJB).  Every fast-weight matrix is held as 16x16
+// NS workgroups (1 or 2) own one (batch, head) unit for the whole sequence;
+// rank r of them holds the hidden columns [r DHP, (r+1) DHP).  Its NW waves
+// split that range: wave w owns the local hidden columns j in
+// [16 w NJB, 16 (w+1) NJB).  Every fast-weight matrix is held as 16x16
 // MFMA accumulator tiles with the head index i as the tile ROW and the hidden
 // index j as the tile COLUMN:
 //   first-layer matrices (MLP W1, SwiGLU Wg and Wu, stored [dh][d]) as W^T,
@@ -18,7 +19,7 @@
 
 namespace e2ttt {
 
-template <int FW_, int D_, int NW_, int NJB_, int NTB_, bool BF_>
+template <int FW_, int D_, int NW_, int NJB_, int NTB_, bool BF_, int NS_>
 struct Shape {
   static constexpr int FW = FW_;
   static constexpr int D = D_;
@@ -26,13 +27,14 @@ struct Shape {
   static constexpr int NJB = NJB_;
   static constexpr int NTB = NTB_;
   static constexpr bool BF = BF_;
+  static constexpr int NS = NS_;              // workgroups per unit
   using O = OpT<BF>;
   using E = typename O::E;
   static constexpr int KC = O::KC;
   static constexpr int NH = O::NH;
   static constexpr int NIB = D / 16;          // 16-row blocks over the head dim
   static constexpr int CM = 16 * NTB;         // token rows per chunk tile
-  static constexpr int DHP = 16 * NW * NJB;   // padded hidden width
+  static constexpr int DHP = 16 * NW * NJB;   // padded hidden width of one workgroup
   static constexpr int DHK = ((DHP + KC - 1) / KC) * KC;  // hidden extent of LDS operands
   static constexpr int NMAT = (FW == 0) ? 2 : 3;
   static constexpr int NT = NW * 64;
@@ -49,7 +51,7 @@ struct Shape {
 };
 
 // State tiles of one wave: T[m][jj][ib] is the tile (rows i = 16 ib + 4 g + r,
-// column j = 16 (w NJB + jj) + c) of matrix m.
+// column j = j0 + 16 (w NJB + jj) + c, j0 = rank DHP) of matrix m.
 template <class S>
 struct StateTiles {
   f32x4 t[S::NMAT][S::NJB][S::NIB];
@@ -74,9 +76,9 @@ __device__ __forceinline__ void opaque_state(StateTiles<S>& st) {
 // compiler does not materialise one 64-bit address per element.
 template <class S, bool STORE>
 __device__ __forceinline__ void state_io(StateTiles<S>& st, const float* src, float* dst,
-                                         int dh, int w, int g, int c) {
+                                         int dh, int j0, int w, int g, int c) {
   constexpr int D = S::D;
-  const int jl = 16 * w * S::NJB + c;                      // this lane's first hidden column
+  const int jl = j0 + 16 * w * S::NJB + c;                 // this lane's first hidden column
   const int l1 = opaque_lane(jl * D + 4 * g);              // first-layer lane offset
   const int l2 = opaque_lane(4 * g * dh + jl);             // second-layer lane offset
 #pragma unroll
@@ -102,15 +104,15 @@ __device__ __forceinline__ void state_io(StateTiles<S>& st, const float* src, fl
 }
 
 template <class S>
-__device__ __forceinline__ void load_state(StateTiles<S>& st, const float* src, int dh, int w,
-                                           int g, int c) {
-  state_io<S, false>(st, src, nullptr, dh, w, g, c);
+__device__ __forceinline__ void load_state(StateTiles<S>& st, const float* src, int dh, int j0,
+                                           int w, int g, int c) {
+  state_io<S, false>(st, src, nullptr, dh, j0, w, g, c);
 }
 
 template <class S>
-__device__ __forceinline__ void store_state(StateTiles<S>& st, float* dst, int dh, int w, int g,
-                                            int c) {
-  state_io<S, true>(st, nullptr, dst, dh, w, g, c);
+__device__ __forceinline__ void store_state(StateTiles<S>& st, float* dst, int dh, int j0, int w,
+                                            int g, int c) {
+  state_io<S, true>(st, nullptr, dst, dh, j0, w, g, c);
 }
 
 // Checkpoint blocks hold the chunk-start state in the operand precision

@@ -11,7 +11,15 @@
 //        accumulate straight into the state tiles
 //   O  = Q + LN(act(Q W1^T) W2^T)     outputs from the chunk-start weights (a7)
 // The new state stays in registers for the next chunk (a8).
+//
+// With two workgroups per unit (pair_xchg.h) each holds half of the hidden
+// columns; the j-contractions Y_K and Y_Q then give partial sums that the two
+// ranks swap.  The Q-side first layer and Y_Q run between posting the Y_K
+// partial and waiting for the peer's, so the exchange overlaps that work; the
+// Y_Q swap is waited for only at the end of the chunk.  Both ranks form the
+// same sums (fp32 addition commutes), so they see bitwise identical Y_K and dY.
 #include "chain_common.h"
+#include "pair_xchg.h"
 
 namespace e2ttt {
 
@@ -25,35 +33,56 @@ struct FwdSmem {
   alignas(16) E xv[S::CM * S::LDD];
   alignas(16) E kwt[S::D * S::LDC];   // K^W_t k_t[i], layout [i][t]
   alignas(16) E kmt[S::D * S::LDC];   // K^M_t k_t[i]
-  alignas(16) E alds[S::CM * S::LDH]; // activations A[t][j]
+  alignas(16) E alds[S::CM * S::LDH]; // activations A[t][j] (this workgroup's columns)
   alignas(16) E w2[S::D * S::LDH];    // second-layer weights W2[i][j] (bf16/fp32 copy of W_0)
   alignas(16) E dy[S::CM * S::LDD];   // dY[t][i]
   alignas(16) E dytw[S::D * S::LDC];  // K^W_t dY[t][i], layout [i][t]
   alignas(16) E dytm[S::D * S::LDC];  // K^M_t dY[t][i]
-  alignas(16) float y[S::CM * S::D];
+  alignas(16) float y[S::CM * S::D];  // Y_K (partial over this workgroup's columns)
+  alignas(16) float yq[S::CM * S::D]; // Y_Q (partial)
   float kw[S::CM];
   float km[S::CM];
   float carry[4];
+  int word[2];
 };
+
+// Exchange slot of one rank for one parity: [Y_K | Y_Q], CM x D floats each.
+template <class S>
+__device__ __forceinline__ float* fwd_slot(float* xbuf, long p, int rank, int parity) {
+  return xbuf + (((p * 2 + rank) * 2 + parity) * 2L) * S::CM * S::D;
+}
+
+template <class S>
+__device__ __forceinline__ void copy_to_slot(float* dst, const float* src, int tid) {
+  constexpr int NV = S::CM * S::D / 4;
+#pragma unroll 1
+  for (int v = tid; v < NV; v += S::NT)
+    reinterpret_cast<float4*>(dst)[v] = reinterpret_cast<const float4*>(src)[v];
+}
 
 template <class S>
 __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   using O = typename S::O;
-  using E = typename S::E;
   using IO = IoT<S::BF>;
   constexpr int D = S::D, NJB = S::NJB, NTB = S::NTB, NIB = S::NIB, NMAT = S::NMAT;
   constexpr int SEC = NMAT - 1;  // index of the second-layer matrix
+  constexpr int EPL = D / 16;    // head elements per lane in the row phases
+  constexpr int RPW = S::CM / S::NS;   // output rows written by one rank
   __shared__ FwdSmem<S> sm;
   static_assert(sizeof(FwdSmem<S>) <= 160 * 1024, "LDS budget");
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, c = lane & 15;
-  const long u = blockIdx.x;
+  const int l16 = lane & 15;
   const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
   const float inv_d = 1.0f / D;
 
-  StateTiles<S> W, M;
-  load_state<S>(W, a.w_in + u * a.P, dh, w, g, c);
-  load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, w, g, c);
+  PairX<S::NS> px;
+  px.init(a.sync, a.npairs, sm.word);
+  const int rank = px.rank;
+  const int j0 = rank * S::DHP;
+  const long NP = (S::NS > 1) ? a.npairs : (long)gridDim.x;
+  const int rlo = rank * RPW;
+  long nch = 0;   // chunks processed by this workgroup (exchange parity)
 
   // hidden columns [DHP, DHK) of the j-operands stay zero for the whole run
   if constexpr (S::DHK > S::DHP) {
@@ -64,294 +93,364 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       sm.w2[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
   }
 
-  for (int r = 0; r < NC; ++r) {
-    const int s0 = r * C;
-    const int len = min(C, T - s0);
-    const long row0 = u * T + s0;
-    // ---------------------------------------------------------- stage (a1)
-    stage_tile<S>(sm.xk, a.k, row0, len, tid);
-    stage_tile<S>(sm.xq, a.q, row0, len, tid);
-    stage_tile<S>(sm.xv, a.v, row0, len, tid);
+  for (long u = px.p; u < a.U; u += NP) {
+    StateTiles<S> W, M;
+    load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
+    load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, j0, w, g, c);
+
+    for (int r = 0; r < NC; ++r, ++nch) {
+      const int s0 = r * C;
+      const int len = min(C, T - s0);
+      const long row0 = u * T + s0;
+      const int par = (int)(nch & 1);
+      const unsigned seq0 = px.seq_now();
+      // -------------------------------------------------------- stage (a1)
+      stage_tile<S>(sm.xk, a.k, row0, len, tid);
+      stage_tile<S>(sm.xq, a.q, row0, len, tid);
+      stage_tile<S>(sm.xv, a.v, row0, len, tid);
 #pragma unroll 1
-    for (int t = tid; t < S::CM; t += S::NT) {
-      sm.kw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
-      sm.km[t] = (t < len) ? a.km[row0 + t] : 0.0f;
-    }
-    if (tid < 3) sm.carry[tid] = a.carry[(u * NC + r) * 3 + tid];
-    if (a.ckpt) {
-      char* cb = static_cast<char*>(a.ckpt) + (u * NC + r) * 2 * a.ckpt_stride;
-      store_ckpt<S>(W, cb, w, lane);
-      store_ckpt<S>(M, cb + a.ckpt_stride, w, lane);
-    }
-    // second-layer weights of W_0 into LDS as the j-contraction operand
-#pragma unroll
-    for (int jj = 0; jj < NJB; ++jj)
-#pragma unroll
-      for (int ib = 0; ib < NIB; ++ib)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
-          sm.w2[(16 * ib + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] =
-              O::to_e(W.t[SEC][jj][ib][rr]);
-    opaque_state<S>(W);
-    opaque_state<S>(M);
-    __syncthreads();
-
-    // ------------------------------------------- K-side forward (a3)
-#pragma unroll 1
-    for (int idx = tid; idx < D * (S::CM / 4); idx += S::NT) {
-      const int i = idx % D, t0 = 4 * (idx / D);
-      typename O::Q qw, qm;
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const float kx = O::from_e(sm.xk[(t0 + q4) * S::LDD + i]);
-        qw[q4] = O::to_e(sm.kw[t0 + q4] * kx);
-        qm[q4] = O::to_e(sm.km[t0 + q4] * kx);
+      for (int t = tid; t < S::CM; t += S::NT) {
+        sm.kw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
+        sm.km[t] = (t < len) ? a.km[row0 + t] : 0.0f;
       }
-      *reinterpret_cast<typename O::Q*>(&sm.kwt[i * S::LDC + t0]) = qw;
-      *reinterpret_cast<typename O::Q*>(&sm.kmt[i * S::LDC + t0]) = qm;
-    }
-    f32x4 H[NTB][NJB];                   // MLP: H;  SwiGLU: Hg
-    f32x4 Hu[NTB][(S::FW == 1) ? NJB : 1];
-    typename O::Q AK[NTB][NJB];          // act(H) as operand quads (rows t)
-#pragma unroll
-    for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-      for (int jj = 0; jj < NJB; ++jj) {
-        f32x4 acc = zero4(), accu = zero4();
-#pragma unroll
-        for (int p = 0; p < S::KS_D; ++p) {
-          auto af = lds_frag<S::BF>(sm.xk, S::LDD, 16 * tb + c, p * S::KC, g);
-          acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
-          if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
-        }
-        f32x4 act;
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          if constexpr (S::FW == 0) act[rr] = gelu_f(acc[rr]);
-          else act[rr] = silu_f(acc[rr]) * accu[rr];
-        }
-        H[tb][jj] = acc;
-        if constexpr (S::FW == 1) Hu[tb][jj] = accu;
-        AK[tb][jj] = O::cvt(act);
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
-          sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act[rr]);
-        sched_fence();
+      if (tid < 3) sm.carry[tid] = a.carry[(u * NC + r) * 3 + tid];
+      if (a.ckpt) {
+        char* cb = static_cast<char*>(a.ckpt) + ((u * NC + r) * S::NS + rank) * 2 * a.ckpt_stride;
+        store_ckpt<S>(W, cb, w, lane);
+        store_ckpt<S>(M, cb + a.ckpt_stride, w, lane);
       }
-    __syncthreads();
-
-    jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y = A W2^T
-    __syncthreads();
-
-    // ------------------------------- LN and activation gradients (a4)
-    // Four token rows per wave step: lanes 16 r .. 16 r + 15 hold row t0 + r,
-    // EPL consecutive head elements each; row sums are 16-lane DPP reductions.
-    const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
-    {
-      constexpr int EPL = D / 16;
-      const int l16 = lane & 15;
-#pragma unroll 1
-      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * S::NW) {
-        const int t = t0 + (lane >> 4);
-        float yv[EPL], e[EPL], z[EPL], dyv[EPL];
-        float s1 = 0.0f;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) { yv[q] = sm.y[t * D + l16 * EPL + q]; s1 += yv[q]; }
-        if (a.resln) {
-          const float mu = group16_sum(s1) * inv_d;
-          float s2 = 0.0f;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
-          const float sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
-          float se = 0.0f, sez = 0.0f;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            const int i = l16 * EPL + q;
-            z[q] = yv[q] * sig;
-            e[q] = O::from_e(sm.xv[t * S::LDD + i]) - O::from_e(sm.xk[t * S::LDD + i]) - z[q];
-            se += e[q];
-            sez += e[q] * z[q];
-          }
-          const float me = group16_sum(se) * inv_d, mez = group16_sum(sez) * inv_d;
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) dyv[q] = (e[q] - me - z[q] * mez) * sig;
-        } else {
-#pragma unroll
-          for (int q = 0; q < EPL; ++q)
-            dyv[q] = O::from_e(sm.xv[t * S::LDD + l16 * EPL + q]) - yv[q];
-        }
-        const float kwt = sm.kw[t], kmt = sm.km[t];
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-          const int i = l16 * EPL + q;
-          sm.dy[t * S::LDD + i] = O::to_e(dyv[q]);
-          sm.dytw[i * S::LDC + t] = O::to_e(kwt * dyv[q]);
-          sm.dytm[i * S::LDC + t] = O::to_e(kmt * dyv[q]);
-        }
-      }
-    }
-    __syncthreads();
-
-    // ----------------------------- Q-side first layer (a7), into alds
-    opaque_state<S>(W);
-#pragma unroll
-    for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-      for (int jj = 0; jj < NJB; ++jj) {
-        f32x4 acc = zero4(), accu = zero4();
-#pragma unroll
-        for (int p = 0; p < S::KS_D; ++p) {
-          auto af = lds_frag<S::BF>(sm.xq, S::LDD, 16 * tb + c, p * S::KC, g);
-          acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
-          if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
-        }
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          float act;
-          if constexpr (S::FW == 0) act = gelu_f(acc[rr]);
-          else act = silu_f(acc[rr]) * accu[rr];
-          sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act);
-        }
-        sched_fence();
-      }
-
-    // ---------------------------------- dA = dY W2, first-layer deltas (a4)
-    opaque_state<S>(W);
-    typename O::Q DH[NTB][NJB];                         // MLP dH / SwiGLU dHg
-    typename O::Q DU[NTB][(S::FW == 1) ? NJB : 1];      // SwiGLU dHu
-#pragma unroll
-    for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-      for (int jj = 0; jj < NJB; ++jj) {
-        f32x4 da = zero4();
-#pragma unroll
-        for (int p = 0; p < S::KS_D; ++p) {
-          auto af = lds_frag<S::BF>(sm.dy, S::LDD, 16 * tb + c, p * S::KC, g);
-          da = O::mma(da, af, tile_frag<S>(&W.t[SEC][jj][0], p, 1));
-        }
-        f32x4 dh1, dh2;
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          if constexpr (S::FW == 0) {
-            dh1[rr] = da[rr] * gelu_d1(H[tb][jj][rr]);
-          } else {
-            const float hg = H[tb][jj][rr], hu = Hu[tb][jj][rr];
-            dh1[rr] = da[rr] * hu * silu_d1(hg);
-            dh2[rr] = da[rr] * silu_f(hg);
-          }
-        }
-        DH[tb][jj] = O::cvt(dh1);
-        if constexpr (S::FW == 1) DU[tb][jj] = O::cvt(dh2);
-        sched_fence();
-      }
-
-    // ------------------- closed-form transition (a5, a6): scale, then accumulate
-#pragma unroll
-    for (int m = 0; m < NMAT; ++m)
+      // second-layer weights of W_0 into LDS as the j-contraction operand
 #pragma unroll
       for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-        for (int ib = 0; ib < NIB; ++ib) {
-          W.t[m][jj][ib] = cw * W.t[m][jj][ib] + cm * M.t[m][jj][ib];
-          M.t[m][jj][ib] = cbv * M.t[m][jj][ib];
+        for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+            sm.w2[(16 * ib + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] =
+                O::to_e(W.t[SEC][jj][ib][rr]);
+      opaque_state<S>(W);
+      opaque_state<S>(M);
+      __syncthreads();
+
+      // ------------------------------------------- K-side forward (a3)
+#pragma unroll 1
+      for (int idx = tid; idx < D * (S::CM / 4); idx += S::NT) {
+        const int i = idx % D, t0 = 4 * (idx / D);
+        typename O::Q qw, qm;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float kx = O::from_e(sm.xk[(t0 + q4) * S::LDD + i]);
+          qw[q4] = O::to_e(sm.kw[t0 + q4] * kx);
+          qm[q4] = O::to_e(sm.km[t0 + q4] * kx);
         }
+        *reinterpret_cast<typename O::Q*>(&sm.kwt[i * S::LDC + t0]) = qw;
+        *reinterpret_cast<typename O::Q*>(&sm.kmt[i * S::LDC + t0]) = qm;
+      }
+      f32x4 H[NTB][NJB];                   // MLP: H;  SwiGLU: Hg
+      f32x4 Hu[NTB][(S::FW == 1) ? NJB : 1];
+      typename O::Q AK[NTB][NJB];          // act(H) as operand quads (rows t)
 #pragma unroll
-    for (int jj = 0; jj < NJB; ++jj)
+      for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
-      for (int ib = 0; ib < NIB; ++ib)
+        for (int jj = 0; jj < NJB; ++jj) {
+          f32x4 acc = zero4(), accu = zero4();
 #pragma unroll
-        for (int p = 0; p < S::KS_C; ++p) {
-          typename O::Frag bA, bH, bU;
-#pragma unroll
-          for (int h = 0; h < S::NH; ++h) {
-            bA.h[h] = AK[S::NH * p + h][jj];
-            bH.h[h] = DH[S::NH * p + h][jj];
-            if constexpr (S::FW == 1) bU.h[h] = DU[S::NH * p + h][jj];
+          for (int p = 0; p < S::KS_D; ++p) {
+            auto af = lds_frag<S::BF>(sm.xk, S::LDD, 16 * tb + c, p * S::KC, g);
+            acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
+            if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
           }
-          const int row = 16 * ib + c, k0 = p * S::KC;
-          // second layer: sum_t K_t dY[t][i] A[t][j]
-          W.t[SEC][jj][ib] = O::mma(W.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytw, S::LDC, row, k0, g), bA);
-          M.t[SEC][jj][ib] = O::mma(M.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytm, S::LDC, row, k0, g), bA);
-          // first layer(s): sum_t K_t k[t][i] dH[t][j]
-          auto kfw = lds_frag<S::BF>(sm.kwt, S::LDC, row, k0, g);
-          auto kfm = lds_frag<S::BF>(sm.kmt, S::LDC, row, k0, g);
-          W.t[0][jj][ib] = O::mma(W.t[0][jj][ib], kfw, bH);
-          M.t[0][jj][ib] = O::mma(M.t[0][jj][ib], kfm, bH);
-          if constexpr (S::FW == 1) {
-            W.t[1][jj][ib] = O::mma(W.t[1][jj][ib], kfw, bU);
-            M.t[1][jj][ib] = O::mma(M.t[1][jj][ib], kfm, bU);
+          f32x4 act;
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            if constexpr (S::FW == 0) act[rr] = gelu_f(acc[rr]);
+            else act[rr] = silu_f(acc[rr]) * accu[rr];
+          }
+          H[tb][jj] = acc;
+          if constexpr (S::FW == 1) Hu[tb][jj] = accu;
+          AK[tb][jj] = O::cvt(act);
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+            sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act[rr]);
+          sched_fence();
+        }
+      __syncthreads();
+
+      jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y_K (partial)
+      __syncthreads();
+      if constexpr (S::NS > 1) {
+        copy_to_slot<S>(fwd_slot<S>(a.xbuf, px.p, rank, par), sm.y, tid);
+        px.post();                                        // seq0 + 1: Y_K
+      }
+
+      // ------------------- Q-side first layer and Y_Q (a7), overlapping the swap
+      opaque_state<S>(W);
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj) {
+          f32x4 acc = zero4(), accu = zero4();
+#pragma unroll
+          for (int p = 0; p < S::KS_D; ++p) {
+            auto af = lds_frag<S::BF>(sm.xq, S::LDD, 16 * tb + c, p * S::KC, g);
+            acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
+            if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
+          }
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            float act;
+            if constexpr (S::FW == 0) act = gelu_f(acc[rr]);
+            else act = silu_f(acc[rr]) * accu[rr];
+            sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act);
           }
           sched_fence();
         }
-    __syncthreads();
+      __syncthreads();
+      jgemm_to_lds<S>(sm.alds, sm.w2, sm.yq, w, g, c);  // Y_Q (partial)
+      __syncthreads();
+      if constexpr (S::NS > 1) {
+        copy_to_slot<S>(fwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D, sm.yq, tid);
+        px.post();                                        // seq0 + 2: Y_Q
+        px.wait_for(seq0 + 1, sm.word);                   // peer's Y_K
+      }
 
-    jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y_Q = A_Q W2^T
-    __syncthreads();
-
-    // ------------------------------------------------- outputs (a7)
-    {
-      using IOT = typename IO::T;
-      constexpr int EPL = D / 16;
-      const int l16 = lane & 15;
-      IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
+      // ------------------------------- LN and activation gradients (a4)
+      // Four token rows per wave step: lanes 16 r .. 16 r + 15 hold row t0 + r,
+      // EPL consecutive head elements each; row sums are 16-lane DPP reductions.
+      const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
+      {
+        const float* peer = (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) : nullptr;
 #pragma unroll 1
-      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * S::NW) {
-        const int t = t0 + (lane >> 4);
-        float yv[EPL], f[EPL];
-        float s1 = 0.0f;
+        for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * S::NW) {
+          const int t = t0 + (lane >> 4);
+          float yv[EPL], e[EPL], z[EPL], dyv[EPL];
+          float s1 = 0.0f, sig = 1.0f;
 #pragma unroll
-        for (int q = 0; q < EPL; ++q) { yv[q] = sm.y[t * D + l16 * EPL + q]; s1 += yv[q]; }
-        if (a.resln) {
-          const float mu = group16_sum(s1) * inv_d;
-          float s2 = 0.0f;
+          for (int q = 0; q < EPL; ++q) yv[q] = sm.y[t * D + l16 * EPL + q];
+          if constexpr (S::NS > 1) {
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
-          const float sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+            for (int q = 0; q < EPL; ++q) yv[q] += peer[t * D + l16 * EPL + q];
+          }
 #pragma unroll
-          for (int q = 0; q < EPL; ++q)
-            f[q] = O::from_e(sm.xq[t * S::LDD + l16 * EPL + q]) + yv[q] * sig;
-        } else {
+          for (int q = 0; q < EPL; ++q) s1 += yv[q];
+          if (a.resln) {
+            const float mu = group16_sum(s1) * inv_d;
+            float s2 = 0.0f;
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) f[q] = yv[q];
-        }
-        if (t < len) {
+            for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
+            sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+            float se = 0.0f, sez = 0.0f;
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) IO::st(outp + (long)t * D + l16 * EPL + q, f[q]);
+            for (int q = 0; q < EPL; ++q) {
+              const int i = l16 * EPL + q;
+              z[q] = yv[q] * sig;
+              e[q] = O::from_e(sm.xv[t * S::LDD + i]) - O::from_e(sm.xk[t * S::LDD + i]) - z[q];
+              se += e[q];
+              sez += e[q] * z[q];
+            }
+            const float me = group16_sum(se) * inv_d, mez = group16_sum(sez) * inv_d;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) dyv[q] = (e[q] - me - z[q] * mez) * sig;
+          } else {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) {
+              z[q] = yv[q];
+              dyv[q] = O::from_e(sm.xv[t * S::LDD + l16 * EPL + q]) - yv[q];
+            }
+          }
+          if (a.zk && t >= rlo && t < rlo + RPW && t < len) {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) a.zk[(row0 + t) * D + l16 * EPL + q] = z[q];
+            if (l16 == 0) a.rk[row0 + t] = sig;
+          }
+          const float kwt = sm.kw[t], kmt = sm.km[t];
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) {
+            const int i = l16 * EPL + q;
+            sm.dy[t * S::LDD + i] = O::to_e(dyv[q]);
+            sm.dytw[i * S::LDC + t] = O::to_e(kwt * dyv[q]);
+            sm.dytm[i * S::LDC + t] = O::to_e(kmt * dyv[q]);
+          }
         }
       }
-    }
-    __syncthreads();
-  }
+      __syncthreads();
 
-  store_state<S>(W, a.w_out + u * a.P, dh, w, g, c);
-  store_state<S>(M, a.m_out + u * a.P, dh, w, g, c);
+      // ---------------------------------- dA = dY W2, first-layer deltas (a4)
+      opaque_state<S>(W);
+      typename O::Q DH[NTB][NJB];                         // MLP dH / SwiGLU dHg
+      typename O::Q DU[NTB][(S::FW == 1) ? NJB : 1];      // SwiGLU dHu
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj) {
+          f32x4 da = zero4();
+#pragma unroll
+          for (int p = 0; p < S::KS_D; ++p) {
+            auto af = lds_frag<S::BF>(sm.dy, S::LDD, 16 * tb + c, p * S::KC, g);
+            da = O::mma(da, af, tile_frag<S>(&W.t[SEC][jj][0], p, 1));
+          }
+          f32x4 dh1, dh2;
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            if constexpr (S::FW == 0) {
+              dh1[rr] = da[rr] * gelu_d1(H[tb][jj][rr]);
+            } else {
+              const float hg = H[tb][jj][rr], hu = Hu[tb][jj][rr];
+              dh1[rr] = da[rr] * hu * silu_d1(hg);
+              dh2[rr] = da[rr] * silu_f(hg);
+            }
+          }
+          DH[tb][jj] = O::cvt(dh1);
+          if constexpr (S::FW == 1) DU[tb][jj] = O::cvt(dh2);
+          sched_fence();
+        }
+
+      // ------------------- closed-form transition (a5, a6): scale, then accumulate
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+          for (int ib = 0; ib < NIB; ++ib) {
+            W.t[m][jj][ib] = cw * W.t[m][jj][ib] + cm * M.t[m][jj][ib];
+            M.t[m][jj][ib] = cbv * M.t[m][jj][ib];
+          }
+#pragma unroll
+      for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+          for (int p = 0; p < S::KS_C; ++p) {
+            typename O::Frag bA, bH, bU;
+#pragma unroll
+            for (int h = 0; h < S::NH; ++h) {
+              bA.h[h] = AK[S::NH * p + h][jj];
+              bH.h[h] = DH[S::NH * p + h][jj];
+              if constexpr (S::FW == 1) bU.h[h] = DU[S::NH * p + h][jj];
+            }
+            const int row = 16 * ib + c, k0 = p * S::KC;
+            // second layer: sum_t K_t dY[t][i] A[t][j]
+            W.t[SEC][jj][ib] = O::mma(W.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytw, S::LDC, row, k0, g), bA);
+            M.t[SEC][jj][ib] = O::mma(M.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytm, S::LDC, row, k0, g), bA);
+            // first layer(s): sum_t K_t k[t][i] dH[t][j]
+            auto kfw = lds_frag<S::BF>(sm.kwt, S::LDC, row, k0, g);
+            auto kfm = lds_frag<S::BF>(sm.kmt, S::LDC, row, k0, g);
+            W.t[0][jj][ib] = O::mma(W.t[0][jj][ib], kfw, bH);
+            M.t[0][jj][ib] = O::mma(M.t[0][jj][ib], kfm, bH);
+            if constexpr (S::FW == 1) {
+              W.t[1][jj][ib] = O::mma(W.t[1][jj][ib], kfw, bU);
+              M.t[1][jj][ib] = O::mma(M.t[1][jj][ib], kfm, bU);
+            }
+            sched_fence();
+          }
+
+      // ------------------------------------------------- outputs (a7)
+      if constexpr (S::NS > 1) px.wait_for(seq0 + 2, sm.word);   // peer's Y_Q
+      {
+        using IOT = typename IO::T;
+        IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
+        const float* peer =
+            (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) + S::CM * D : nullptr;
+#pragma unroll 1
+        for (int t0 = rlo + 4 * w; t0 < rlo + RPW; t0 += 4 * S::NW) {
+          const int t = t0 + (lane >> 4);
+          float yv[EPL], f[EPL];
+          float s1 = 0.0f, sig = 1.0f;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) yv[q] = sm.yq[t * D + l16 * EPL + q];
+          if constexpr (S::NS > 1) {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) yv[q] += peer[t * D + l16 * EPL + q];
+          }
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) s1 += yv[q];
+          if (a.resln) {
+            const float mu = group16_sum(s1) * inv_d;
+            float s2 = 0.0f;
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
+            sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) {
+              yv[q] *= sig;                                 // Z_Q
+              f[q] = O::from_e(sm.xq[t * S::LDD + l16 * EPL + q]) + yv[q];
+            }
+          } else {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) f[q] = yv[q];
+          }
+          if (t < len) {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) IO::st(outp + (long)t * D + l16 * EPL + q, f[q]);
+            if (a.zq) {
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) a.zq[(row0 + t) * D + l16 * EPL + q] = yv[q];
+              if (l16 == 0) a.rq[row0 + t] = sig;
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+
+    store_state<S>(W, a.w_out + u * a.P, dh, j0, w, g, c);
+    store_state<S>(M, a.m_out + u * a.P, dh, j0, w, g, c);
+  }
 }
 
 template <class S>
-hipError_t launch(const ChainArgs& a, long units, hipStream_t stream) {
-  hipLaunchKernelGGL(chain_fwd_kernel<S>, dim3((unsigned)units), dim3(S::NT), 0, stream, a);
-  return hipGetLastError();
+int max_blocks_per_cu() {
+  static int nb = [] {
+    int v = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_fwd_kernel<S>, S::NT, 0) !=
+        hipSuccess)
+      v = 0;
+    return v;
+  }();
+  return nb;
+}
+
+template <class S>
+hipError_t launch(const ChainArgs& a, hipStream_t stream) {
+  if constexpr (S::NS == 1) {
+    hipLaunchKernelGGL(chain_fwd_kernel<S>, dim3((unsigned)a.U), dim3(S::NT), 0, stream, a);
+    return hipGetLastError();
+  } else {
+    ChainArgs b = a;
+    void* args[] = {&b};
+    return hipLaunchCooperativeKernel((const void*)chain_fwd_kernel<S>,
+                                      dim3((unsigned)(2 * a.npairs)), dim3(S::NT), args, 0,
+                                      stream);
+  }
 }
 
 }  // namespace
 
-#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF)                                              \
+#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF, NS)                                          \
   if (cfg.fw == FW && cfg.d == D && cfg.nw == NW && cfg.njb == NJB && cfg.ntb == NTB && \
-      cfg.bf == BF)                                                                     \
-    return launch<Shape<FW, D, NW, NJB, NTB, BF>>(a, units, stream);
+      cfg.bf == BF && cfg.ns == NS)                                                     \
+    return launch<Shape<FW, D, NW, NJB, NTB, BF, NS>>(a, stream);
 
-hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, long units,
-                            hipStream_t stream) {
+hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream) {
 #include "chain_variants.inc"
   return hipErrorInvalidValue;
 }
 #undef E2TTT_CASE
 
-}  // namespace e2ttt
+#define E2TTT_CASE(FW, D, NW, NJB, NTB, BF, NS)                                          \
+  if (cfg.fw == FW && cfg.d == D && cfg.nw == NW && cfg.njb == NJB && cfg.ntb == NTB && \
+      cfg.bf == BF && cfg.ns == NS)                                                     \
+    return max_blocks_per_cu<Shape<FW, D, NW, NJB, NTB, BF, NS>>();
 
-namespace e2ttt {
+int chain_fwd_blocks_per_cu(const ChainConfig& cfg) {
+#include "chain_variants.inc"
+  return 0;
+}
+#undef E2TTT_CASE
+
 long chain_ckpt_bytes(const ChainConfig& cfg) {
   const long nmat = (cfg.fw == 0) ? 2 : 3;
   return nmat * 16L * cfg.nw * cfg.njb * cfg.d * (cfg.bf ? 2 : 4);
 }
+
 }  // namespace e2ttt

@@ -78,6 +78,9 @@ __device__ __forceinline__ float affine_scan_up(float a, float b, int lane) {
 }
 
 __global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
+  // the chain kernel that follows on this stream starts from cleared sync words
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < a.nzero; i += (long)gridDim.x * 256)
+    a.zero[i] = 0u;
   const long wid = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (wid >= a.nwork) return;
   const int lane = threadIdx.x & 63;
@@ -114,11 +117,17 @@ __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
   const long base = u * a.T + s0;
   const bool valid = lane < len;
   ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);
-  const float kwb = valid ? a.kwb[base + lane] : 0.0f;
-  const float kmb = valid ? a.kmb[base + lane] : 0.0f;
-  const float cwb = a.carryb[wid * 3 + 0];
-  const float cmb = a.carryb[wid * 3 + 1];
-  const float cbb = a.carryb[wid * 3 + 2];
+  // the chain kernel leaves one partial per workgroup of a unit; sum them
+  float kwb = 0.0f, kmb = 0.0f, cwb = 0.0f, cmb = 0.0f, cbb = 0.0f;
+  for (int sl = 0; sl < a.ns; ++sl) {
+    if (valid) {
+      kwb += a.kwb[sl * a.tok_slot + base + lane];
+      kmb += a.kmb[sl * a.tok_slot + base + lane];
+    }
+    cwb += a.carryb[sl * a.chk_slot + wid * 3 + 0];
+    cmb += a.carryb[sl * a.chk_slot + wid * 3 + 1];
+    cbb += a.carryb[sl * a.chk_slot + wid * 3 + 2];
+  }
 
   const float etab = kwb * s.S + kmb * s.bt;
   // S-bar and the direct beta_1 term of carry_m = beta_1 S_1
@@ -146,7 +155,18 @@ __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
   }
 }
 
+__global__ void __launch_bounds__(256) zero_words_kernel(unsigned* p, long n) {
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) p[i] = 0u;
+}
+
 }  // namespace
+
+hipError_t launch_zero_words(unsigned* p, long n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)min(64L, (n + 255) / 256);
+  hipLaunchKernelGGL(zero_words_kernel, dim3(blocks), dim3(256), 0, stream, p, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_coeff_fwd(const CoeffFwdArgs& a, hipStream_t stream) {
   const unsigned blocks = (unsigned)((a.nwork + 3) / 4);

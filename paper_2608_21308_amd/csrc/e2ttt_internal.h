@@ -16,24 +16,30 @@ struct CoeffFwdArgs {
   float* carry;         // [U][NC][3]
   int T, C, NC;
   long nwork;           // U * NC
+  unsigned* zero;       // nullable: words cleared by this kernel (pair sync words)
+  long nzero;
 };
 
 struct CoeffBwdArgs {
   const float* eta;
   const float* beta;
   const float* gamma;   // nullable
-  const float* kwb;     // [U][T]   adjoint of K^W
-  const float* kmb;     // [U][T]   adjoint of K^M
-  const float* carryb;  // [U][NC][3] adjoint of the carries
+  const float* kwb;     // [ns][U][T]   adjoint of K^W (summed over the slots)
+  const float* kmb;     // [ns][U][T]   adjoint of K^M
+  const float* carryb;  // [ns][U][NC][3] adjoint of the carries
   float* d_eta;
   float* d_beta;
   float* d_gamma;       // nullable iff gamma is
   int T, C, NC;
   long nwork;
+  int ns;               // partial slots of kwb, kmb, carryb (one per workgroup of a unit)
+  long tok_slot;        // elements between slots of kwb / kmb (U T)
+  long chk_slot;        // elements between slots of carryb (U NC 3)
 };
 
-// Chain kernels: one workgroup per (batch, head) unit, looping over chunks.
+// Chain kernels: one or two workgroups per (batch, head) unit, looping over chunks.
 struct ChainArgs {
+  long U;               // units
   const void* q;
   const void* k;
   const void* v;
@@ -55,13 +61,23 @@ struct ChainArgs {
   void* dv;
   float* d_w_in;
   float* d_m_in;
-  float* kwb;           // [U][T] adjoint of K^W (written by the backward chain)
+  float* kwb;           // [NS][U][T] adjoint of K^W, one partial per rank
   float* kmb;
-  float* carryb;        // [U][NC][3]
+  float* carryb;        // [NS][U][NC][3]
   // chunk-start checkpoints (operand precision, kernel register order),
   // nullable in the forward
   void* ckpt;
-  long ckpt_stride;     // bytes per (unit, chunk, W-or-M) block
+  long ckpt_stride;     // bytes per (unit, chunk, rank, W-or-M) block
+  // LN outputs saved by the forward for the backward (nullable in the forward):
+  // Z = LN(Y) (Y itself without the residual LN) [U][T][d], 1/sigma [U][T]
+  float* zk;
+  float* rk;
+  float* zq;
+  float* rq;
+  // two workgroups per unit: exchange slots and sync words (pair_xchg.h)
+  float* xbuf;
+  unsigned* sync;
+  long npairs;
   int T, C, NC, dh;
   long P;               // parameters per unit (unpadded)
   int resln;            // 1: f = x + LN(y); 0: f = y
@@ -76,16 +92,21 @@ struct ChainConfig {
   int njb;    // 16-wide hidden blocks per wave
   int ntb;    // 16-row token blocks per chunk
   int bf;     // 1: bf16 MFMA operands and io; 0: fp32
+  int ns;     // workgroups per unit (1, or 2 with a cooperative launch)
 };
 
 hipError_t launch_coeff_fwd(const CoeffFwdArgs& a, hipStream_t stream);
 hipError_t launch_coeff_bwd(const CoeffBwdArgs& a, hipStream_t stream);
 // Return hipErrorInvalidValue when no kernel exists for `cfg`.
-hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, long units,
-                            hipStream_t stream);
-hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, long units,
-                            hipStream_t stream);
-// Bytes of one checkpoint block (W or M of one unit at one chunk start).
+hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
+hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
+// Clears n words (a kernel, so that it may be captured in a graph).
+hipError_t launch_zero_words(unsigned* p, long n, hipStream_t stream);
+// Pairs a cooperative launch of the chain kernel can hold at once (multiple of 8).
+long chain_max_pairs(const ChainConfig& cfg, bool backward);
+// Bytes of one checkpoint block (W or M of one unit's workgroup at one chunk start).
 long chain_ckpt_bytes(const ChainConfig& cfg);
+// Floats of one rank's exchange slot set (both parities).
+long chain_xchg_floats(const ChainConfig& cfg, bool backward);
 
 }  // namespace e2ttt

@@ -1,0 +1,146 @@
+// Two workgroups per unit: exchange of partial sums through global memory.
+//
+// For the widest fast-weight nets one unit's hidden columns are split between
+// two workgroups (ranks 0 and 1 of a pair), each holding its half of the state
+// in registers.  Contractions over the hidden index then give each rank a
+// partial C x d sum that the other rank needs; the ranks swap these through a
+// small global buffer and a flag per rank.
+//
+// Placement.  Workgroups are dispatched to the eight XCDs round-robin by
+// workgroup id, so the pair p is given ids 16 (p / 8) + p % 8 and that + 8:
+// both land on XCD p % 8 and share its L2.  On a shared L2 a post is: plain
+// stores of the data, s_waitcnt vmcnt(0) (the stores have reached L2, the L1
+// being write-through), a workgroup barrier, then a device-scope store of the
+// flag; the wait is: a device-scope poll of the peer's flag, a barrier, then an
+// invalidation of this CU's L1 (buffer_inv sc0) before plain loads of the
+// peer's data.  At kernel start the ranks swap their hardware XCC ids with
+// device-scope accesses; if they differ (another dispatch order), every post
+// and wait of that pair uses agent-scope release / acquire fences instead,
+// which are coherent across XCDs but write back and invalidate the L2.
+//
+// Every wait is bounded (kTimeoutTicks of the 100 MHz real-time counter).  A
+// rank whose wait expires sets the status word, poisons its own flag so that
+// the peer stops waiting too, and skips all later waits, so the grid always
+// drains; the results of that launch are then undefined and the status word
+// reports it.  The kernels are launched cooperatively, so both ranks of a pair
+// are resident at the same time.
+//
+// Sync words (uint32, one 256-byte line each, zeroed by the kernel that runs
+// before the chain kernel on the same stream):
+//   line 0                    status (0 ok, 1 a wait expired)
+//   line 1 + 2 p + r          flag of rank r of pair p (last posted sequence number)
+//   line 1 + 2 NP + 2 p + r   hardware XCC id + 1 of rank r of pair p
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace e2ttt {
+
+constexpr int kSyncLine = 64;                       // uint32 words per line
+constexpr long long kTimeoutTicks = 200000000LL;    // 2 s of the 100 MHz counter
+constexpr unsigned kPoison = 0xFFFFFFFFu;
+
+__host__ __device__ constexpr long sync_words(long npairs) { return kSyncLine * (1 + 4 * npairs); }
+
+__device__ __forceinline__ unsigned ld_dev(const unsigned* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(unsigned* p, unsigned v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int hw_xcc_id() {
+  int v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 0xf;
+}
+
+// Pair index and rank of this workgroup for a launch of 2 NP workgroups.
+__device__ __forceinline__ void pair_of_block(int b, long& p, int& rank) {
+  rank = (b >> 3) & 1;
+  p = (long)(b >> 4) * 8 + (b & 7);
+}
+
+template <int NS> struct PairX;
+
+// One workgroup per unit: nothing to exchange.
+template <> struct PairX<1> {
+  int rank = 0;
+  long p = 0;
+  __device__ void init(unsigned*, long, int*) { p = blockIdx.x; }
+  __device__ void post() {}
+  __device__ void wait_for(unsigned, int*) {}
+  __device__ unsigned seq_now() const { return 0; }
+};
+
+template <> struct PairX<2> {
+  int rank = 0;
+  long p = 0;
+  unsigned* mine = nullptr;
+  const unsigned* peer = nullptr;
+  unsigned* status = nullptr;
+  unsigned seq = 0;
+  bool same_xcc = true;
+  bool dead = false;
+
+  // s_word: two ints of LDS for broadcasting thread 0's findings
+  __device__ void init(unsigned* sync, long npairs, int* s_word) {
+    pair_of_block(blockIdx.x, p, rank);
+    status = sync;
+    mine = sync + kSyncLine * (1 + 2 * p + rank);
+    peer = sync + kSyncLine * (1 + 2 * p + (1 - rank));
+    unsigned* xm = sync + kSyncLine * (1 + 2 * npairs + 2 * p + rank);
+    const unsigned* xp = sync + kSyncLine * (1 + 2 * npairs + 2 * p + (1 - rank));
+    if (threadIdx.x == 0) {
+      const unsigned id = (unsigned)hw_xcc_id() + 1u;
+      st_dev(xm, id);
+      const long long t0 = __builtin_amdgcn_s_memrealtime();
+      unsigned o = 0;
+      while ((o = ld_dev(xp)) == 0u) {
+        if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) break;
+      }
+      s_word[0] = (o == id) ? 1 : 0;
+      s_word[1] = (o != 0u) ? 1 : 0;
+      if (o == 0u) { st_dev(status, 1u); st_dev(mine, kPoison); }
+    }
+    __syncthreads();
+    same_xcc = s_word[0] != 0;
+    dead = s_word[1] == 0;
+    __syncthreads();
+  }
+
+  // Publish everything this workgroup stored before the call.  All threads call.
+  __device__ void post() {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    ++seq;
+    if (threadIdx.x == 0 && !dead) {
+      if (!same_xcc) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      st_dev(mine, seq);
+    }
+  }
+
+  __device__ unsigned seq_now() const { return seq; }
+
+  // Wait until the peer has posted at least `target`.  All threads call; the
+  // caller has passed a workgroup barrier since the previous call.
+  __device__ void wait_for(unsigned target, int* s_word) {
+    if (dead) return;
+    if (threadIdx.x == 0) {
+      const long long t0 = __builtin_amdgcn_s_memrealtime();
+      unsigned f;
+      int ok = 1;
+      while ((f = ld_dev(peer)) < target) {
+        if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) { ok = 0; break; }
+      }
+      if (f == kPoison) ok = 0;
+      if (!ok) { st_dev(status, 1u); st_dev(mine, kPoison); }
+      s_word[0] = ok;
+    }
+    __syncthreads();
+    if (s_word[0] == 0) dead = true;
+    if (same_xcc) asm volatile("buffer_inv sc0" ::: "memory");
+    else __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
+};
+
+}  // namespace e2ttt

@@ -23,7 +23,7 @@ DT_BF16 = 1
 FLAG_NO_RESIDUAL_LN = 1
 
 STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
-          4: "workspace too small", 5: "HIP error"}
+          4: "workspace too small", 5: "HIP error", 6: "device-side wait expired"}
 
 # Every entry point the header declares (checked by the CPU test-suite).
 EXPORTS = ("e2ttt_param_count", "e2ttt_workspace_bytes", "e2ttt_backward_scratch_bytes",

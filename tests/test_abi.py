@@ -103,5 +103,25 @@ def test_null_and_workspace_errors(lib):
 
 
 def test_status_strings(lib):
-    for s in range(6):
-        assert lib.e2ttt_status_str(s)
+    seen = set()
+    for s in range(7):
+        txt = lib.e2ttt_status_str(s)
+        assert txt and txt != b"unknown status"
+        seen.add(txt)
+    assert len(seen) == 7
+    assert lib.e2ttt_status_str(7) == b"unknown status"
+
+
+def test_split_workspace_sizes(lib):
+    # the dh = 256 MLP runs two workgroups per unit: the workspace grows by the
+    # exchange slots and sync words, the backward scratch by per-rank partials
+    d = desc(B=8, H=16, T=4096)
+    U, T, NC = 128, 4096, 64
+    ws = lib.e2ttt_workspace_bytes(ctypes.byref(d), 0)
+    ws_save = lib.e2ttt_workspace_bytes(ctypes.byref(d), 1)
+    sc = lib.e2ttt_backward_scratch_bytes(ctypes.byref(d))
+    tok = U * T * 4
+    assert ws >= 2 * tok + U * NC * 3 * 4 + 128 * 2 * 2 * 2 * 64 * 64 * 4
+    # checkpoints of W and M (bf16, both ranks) plus Z and 1/sigma of both passes
+    assert ws_save - ws >= U * NC * 2 * 2 * 64 * 256 * 2 + 2 * (tok * 64 + tok)
+    assert sc >= 2 * (2 * tok + U * NC * 3 * 4) + 128 * 2 * 2 * 3 * 64 * 64 * 4
