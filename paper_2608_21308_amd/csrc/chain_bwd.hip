@@ -286,8 +286,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   float* skm = skw + S::CM;
   float* scar = skm + S::CM;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, c = lane & 15;
-  const int l16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
   const float inv_d = 1.0f / D;
   const bool resln = a.resln != 0;
@@ -306,8 +305,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   for (long u = px.p; u < a.U; u += NP) {
     // adjoint of the final state
     StateTiles<S> Wb, Mb;
-    load_state<S>(Wb, a.d_w_out ? a.d_w_out + u * a.P : nullptr, dh, j0, w, g, c);
-    load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, j0, w, g, c);
+    {
+      E2TTT_LANE_IDS;
+      load_state<S>(Wb, a.d_w_out ? a.d_w_out + u * a.P : nullptr, dh, j0, w, g, c);
+      load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, j0, w, g, c);
+    }
     int pend_r = -1, pend_par = 0;   // chunk whose dk, dq partials are not yet combined
 
     for (int r = NC - 1; r >= 0; --r, ++nch) {
@@ -322,22 +324,26 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 
       // ---------------------------------------------------------- P0: stage
       E* xv = reinterpret_cast<E*>(rr);
-      stage_tile<S>(xk, a.k, row0, len, tid);
-      stage_tile<S>(xv, a.v, row0, len, tid);
-      stage_f32<S>(yk, a.zk, row0, len, tid);   // Z (or Y without the residual LN)
+      {
+        E2TTT_LANE_IDS;
+        stage_tile<S>(xk, a.k, row0, len, tid);
+        stage_tile<S>(xv, a.v, row0, len, tid);
+        stage_f32<S>(yk, a.zk, row0, len, tid);   // Z (or Y without the residual LN)
 #pragma unroll 1
-      for (int t = tid; t < S::CM; t += S::NT) {
-        skw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
-        skm[t] = (t < len) ? a.km[row0 + t] : 0.0f;
-        row[2 * t] = (t < len) ? a.rk[row0 + t] : 0.0f;   // 1 / sigma
+        for (int t = tid; t < S::CM; t += S::NT) {
+          skw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
+          skm[t] = (t < len) ? a.km[row0 + t] : 0.0f;
+          row[2 * t] = (t < len) ? a.rk[row0 + t] : 0.0f;   // 1 / sigma
+        }
+        if (tid < 3) scar[tid] = a.carry[(u * NC + r) * 3 + tid];
       }
-      if (tid < 3) scar[tid] = a.carry[(u * NC + r) * 3 + tid];
       __syncthreads();
 
       // ------------------------------------ P1: H = K W1^T, A = act(H) (recompute)
       f32x4 Hk[NF][NTB][NJB];
       Q Akq[NTB][NJB];
       {
+        E2TTT_LANE_IDS;
         Q w1q[NF][NJB][NIB];
 #pragma unroll
         for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
@@ -374,6 +380,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 
       // --------------------- P3: e, dY (first order, from the saved LN output)
       E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
+      {
+      E2TTT_LANE_IDS;
 #pragma unroll 1
       for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
         const int t = t0 + (lane >> 4);
@@ -413,6 +421,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         }
         if (l16 == 0) row[2 * t + 1] = mez;
       }
+      }
       __syncthreads();
 
       // ----------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
@@ -424,6 +433,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       Q dAhq[NTB][NJB];
       f32x4 Hh[NF][NTB][NJB];
       {
+        E2TTT_LANE_IDS;
         Q w2q[NJB][NIB];
         load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
         opaque_state<S>(Wb);
@@ -538,6 +548,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       JAcc<S> dkacc, dyhacc;
       dkacc.zero();
       dyhacc.zero();
+      {
+      E2TTT_LANE_IDS;
 #pragma unroll
       for (int m = 0; m < NF; ++m) {
         jround<S>(dkacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
@@ -549,6 +561,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
                 [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
       jround<S>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
                 [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+      }
 
       // ------------------------------------ P5: adjoint state transition
       {
@@ -568,6 +581,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       // --------------------------- P6: dYh = p2 + dAh W2^T  (into RR, fp32)
       float* dyh = reinterpret_cast<float*>(rr);
       {
+        E2TTT_LANE_IDS;
         Q w2q[NJB][NIB];
         load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
         jround<S>(dyhacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(dAhq[tb][jj]); },
@@ -577,6 +591,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       __syncthreads();
       const float* dyh_peer = nullptr;
       if constexpr (S::NS > 1) {
+        E2TTT_LANE_IDS;
         float* mine = bwd_slot<S>(a.xbuf, px.p, rank, par);
 #pragma unroll 1
         for (int v = tid; v < S::CM * D / 4; v += S::NT)
@@ -591,6 +606,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 
       // ------------------------------------- P7: LayerNorm second order
       {
+        E2TTT_LANE_IDS;
         using IOT = typename IoT<S::BF>::T;
         IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
 #pragma unroll 1
@@ -657,6 +673,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 
       // ---------- P8: Hh += (Yh W2) act'(H); accumulate into Wb; dk = r1 - eh + Hh W1
       {
+        E2TTT_LANE_IDS;
         // K^T into RR for the first-layer accumulation
         E* xkt = reinterpret_cast<E*>(rr);
 #pragma unroll 1
@@ -741,6 +758,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 
       // -------------------------------------------- P9: output branch
       {
+        E2TTT_LANE_IDS;
         E* xq = xk;                                      // Q [t][i]
         E* xdo = reinterpret_cast<E*>(rr);               // dO [t][i]
         E* ybq = yh;                                     // Yb_Q [t][i]
@@ -905,6 +923,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
 
       // ------------------------------ P10: scalar-kernel adjoints of this chunk
+      {
+      E2TTT_LANE_IDS;
 #pragma unroll 1
       for (int t = tid; t < len; t += S::NT) {
         float sw = 0.0f, sm2 = 0.0f;
@@ -920,6 +940,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         for (int ww = 0; ww < NW; ++ww) sacc += cbp[ww * 4 + tid];
         carryb_slot[(u * NC + r) * 3 + tid] = sacc;
       }
+      }
       if constexpr (S::NS > 1) {
         px.post();                                  // seq0 + 2: dk, dq partials
         pend_r = r;
@@ -930,14 +951,18 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     }
 
     if constexpr (S::NS > 1) {
+      E2TTT_LANE_IDS;
       px.wait_for(px.seq_now(), sword);             // the peer's last post
       if (pend_r >= 0)
         flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
                       tid);
       __syncthreads();
     }
-    store_state<S>(Wb, a.d_w_in + u * a.P, dh, j0, w, g, c);
-    store_state<S>(Mb, a.d_m_in + u * a.P, dh, j0, w, g, c);
+    {
+      E2TTT_LANE_IDS;
+      store_state<S>(Wb, a.d_w_in + u * a.P, dh, j0, w, g, c);
+      store_state<S>(Mb, a.d_m_in + u * a.P, dh, j0, w, g, c);
+    }
   }
 }
 

@@ -71,8 +71,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   __shared__ FwdSmem<S> sm;
   static_assert(sizeof(FwdSmem<S>) <= 160 * 1024, "LDS budget");
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, c = lane & 15;
-  const int l16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
   const float inv_d = 1.0f / D;
 
@@ -86,6 +85,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
   // hidden columns [DHP, DHK) of the j-operands stay zero for the whole run
   if constexpr (S::DHK > S::DHP) {
+    E2TTT_LANE_IDS;
     constexpr int NZ = S::DHK - S::DHP;
     for (int idx = tid; idx < S::CM * NZ; idx += S::NT)
       sm.alds[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
@@ -95,8 +95,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
   for (long u = px.p; u < a.U; u += NP) {
     StateTiles<S> W, M;
-    load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
-    load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, j0, w, g, c);
+    {
+      E2TTT_LANE_IDS;
+      load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
+      load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, j0, w, g, c);
+    }
 
     for (int r = 0; r < NC; ++r, ++nch) {
       const int s0 = r * C;
@@ -105,6 +108,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       const int par = (int)(nch & 1);
       const unsigned seq0 = px.seq_now();
       // -------------------------------------------------------- stage (a1)
+      {
+      E2TTT_LANE_IDS;
       stage_tile<S>(sm.xk, a.k, row0, len, tid);
       stage_tile<S>(sm.xq, a.q, row0, len, tid);
       stage_tile<S>(sm.xv, a.v, row0, len, tid);
@@ -130,9 +135,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
                 O::to_e(W.t[SEC][jj][ib][rr]);
       opaque_state<S>(W);
       opaque_state<S>(M);
+      }
       __syncthreads();
 
       // ------------------------------------------- K-side forward (a3)
+      f32x4 H[NTB][NJB];                   // MLP: H;  SwiGLU: Hg
+      f32x4 Hu[NTB][(S::FW == 1) ? NJB : 1];
+      typename O::Q AK[NTB][NJB];          // act(H) as operand quads (rows t)
+      {
+      E2TTT_LANE_IDS;
 #pragma unroll 1
       for (int idx = tid; idx < D * (S::CM / 4); idx += S::NT) {
         const int i = idx % D, t0 = 4 * (idx / D);
@@ -146,9 +157,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         *reinterpret_cast<typename O::Q*>(&sm.kwt[i * S::LDC + t0]) = qw;
         *reinterpret_cast<typename O::Q*>(&sm.kmt[i * S::LDC + t0]) = qm;
       }
-      f32x4 H[NTB][NJB];                   // MLP: H;  SwiGLU: Hg
-      f32x4 Hu[NTB][(S::FW == 1) ? NJB : 1];
-      typename O::Q AK[NTB][NJB];          // act(H) as operand quads (rows t)
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -174,16 +182,23 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act[rr]);
           sched_fence();
         }
+      }
       __syncthreads();
 
-      jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y_K (partial)
+      {
+        E2TTT_LANE_IDS;
+        jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y_K (partial)
+      }
       __syncthreads();
       if constexpr (S::NS > 1) {
+        E2TTT_LANE_IDS;
         copy_to_slot<S>(fwd_slot<S>(a.xbuf, px.p, rank, par), sm.y, tid);
         px.post();                                        // seq0 + 1: Y_K
       }
 
       // ------------------- Q-side first layer and Y_Q (a7), overlapping the swap
+      {
+      E2TTT_LANE_IDS;
       opaque_state<S>(W);
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb)
@@ -205,10 +220,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           }
           sched_fence();
         }
+      }
       __syncthreads();
-      jgemm_to_lds<S>(sm.alds, sm.w2, sm.yq, w, g, c);  // Y_Q (partial)
+      {
+        E2TTT_LANE_IDS;
+        jgemm_to_lds<S>(sm.alds, sm.w2, sm.yq, w, g, c);  // Y_Q (partial)
+      }
       __syncthreads();
       if constexpr (S::NS > 1) {
+        E2TTT_LANE_IDS;
         copy_to_slot<S>(fwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D, sm.yq, tid);
         px.post();                                        // seq0 + 2: Y_Q
         px.wait_for(seq0 + 1, sm.word);                   // peer's Y_K
@@ -219,6 +239,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // EPL consecutive head elements each; row sums are 16-lane DPP reductions.
       const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
       {
+        E2TTT_LANE_IDS;
         const float* peer = (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) : nullptr;
 #pragma unroll 1
         for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * S::NW) {
@@ -279,6 +300,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       opaque_state<S>(W);
       typename O::Q DH[NTB][NJB];                         // MLP dH / SwiGLU dHg
       typename O::Q DU[NTB][(S::FW == 1) ? NJB : 1];      // SwiGLU dHu
+      {
+      E2TTT_LANE_IDS;
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -304,6 +327,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           if constexpr (S::FW == 1) DU[tb][jj] = O::cvt(dh2);
           sched_fence();
         }
+      }
 
       // ------------------- closed-form transition (a5, a6): scale, then accumulate
 #pragma unroll
@@ -315,6 +339,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             W.t[m][jj][ib] = cw * W.t[m][jj][ib] + cm * M.t[m][jj][ib];
             M.t[m][jj][ib] = cbv * M.t[m][jj][ib];
           }
+      {
+      E2TTT_LANE_IDS;
 #pragma unroll
       for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
@@ -343,10 +369,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             }
             sched_fence();
           }
+      }
 
       // ------------------------------------------------- outputs (a7)
       if constexpr (S::NS > 1) px.wait_for(seq0 + 2, sm.word);   // peer's Y_Q
       {
+        E2TTT_LANE_IDS;
         using IOT = typename IO::T;
         IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
         const float* peer =
@@ -393,8 +421,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       __syncthreads();
     }
 
-    store_state<S>(W, a.w_out + u * a.P, dh, j0, w, g, c);
-    store_state<S>(M, a.m_out + u * a.P, dh, j0, w, g, c);
+    {
+      E2TTT_LANE_IDS;
+      store_state<S>(W, a.w_out + u * a.P, dh, j0, w, g, c);
+      store_state<S>(M, a.m_out + u * a.P, dh, j0, w, g, c);
+    }
   }
 }
 

@@ -44,6 +44,15 @@ __device__ __forceinline__ int opaque_lane(int x) {
   return x;
 }
 
+// Thread indices re-derived behind an opaque copy of threadIdx.x.  A kernel
+// phase that starts with E2TTT_LANE_IDS forms its per-lane address arithmetic
+// inside the phase; without it the compiler hoists every such address to the
+// kernel entry and keeps dozens of them live (or spilled) across the chunk loop.
+#define E2TTT_LANE_IDS                                                \
+  const int tid = ::e2ttt::opaque_lane((int)threadIdx.x);             \
+  const int lane = tid & 63, g = lane >> 4, c = lane & 15, l16 = c;   \
+  (void)tid; (void)lane; (void)g; (void)c; (void)l16
+
 template <bool BF> struct OpT;
 
 template <> struct OpT<true> {
