@@ -61,7 +61,13 @@ struct BwdLayout {
   static constexpr int KB = A16(ROW + S::CM * 8);          // dK^W, dK^M partials [2][NW][CM]
   static constexpr int CB = A16(KB + 2 * S::NW * S::CM * 4);  // carry adjoint partials [NW][4]
   static constexpr int SC = A16(CB + S::NW * 16);          // kw[CM], km[CM], carry[4]
-  static constexpr int TOTAL = A16(SC + (2 * S::CM + 4) * 4);
+  static constexpr int BASE = A16(SC + (2 * S::CM + 4) * 4);
+  // Hh of P4 (completed in P8) kept in LDS when it fits: one float4 per lane
+  // per token block and first-layer matrix (lane-private, conflict-free)
+  static constexpr int HHB = (S::FW == 0 ? 1 : 2) * S::NTB * S::NW * 64 * 16;
+  static constexpr bool HH_LDS = BASE + HHB <= 160 * 1024;
+  static constexpr int HHR = BASE;
+  static constexpr int TOTAL = HH_LDS ? BASE + HHB : BASE;
   static_assert(TOTAL <= 160 * 1024, "LDS budget of the backward chain kernel");
   // j-round output items per wave: (token block, head block pair) items
   static constexpr int NITEM = S::NTB * (S::NIB / S::IBB);
@@ -82,8 +88,10 @@ struct JAcc {
 // j-round: out[t][i] (+)= rowscale[t] * sum_j Act[t][j] Wt[i][j] over the full
 // hidden range.  Act and Wt are register tiles of every wave: act(tb, jj) is
 // the tile (rows t, column j) and wt(ib, jj) the tile (rows i, column j).
-// Both are written to the half-width LDS buffers one half at a time.
-template <class S, class FA, class FWT>
+// Both are written to the half-width LDS buffers one half at a time.  With a
+// single half (JH == 1) and WRITE_ACT false, ja already holds Act (written by
+// the caller or by the previous j-round) and only Wt is written.
+template <class S, bool WRITE_ACT = true, class FA, class FWT>
 __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, typename S::E* ja,
                                        typename S::E* jw, FA act, FWT wt, int w, int g, int c) {
   using L = BwdLayout<S>;
@@ -111,11 +119,13 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
 #pragma unroll
       for (int jj = 0; jj < S::NJB; ++jj) {
         const int col = col0 + 16 * jj + c;
+        if (WRITE_ACT || L::JH > 1) {
 #pragma unroll
-        for (int tb = 0; tb < S::NTB; ++tb) {
-          const f32x4 v = act(tb, jj);
+          for (int tb = 0; tb < S::NTB; ++tb) {
+            const f32x4 v = act(tb, jj);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = O::to_e(v[r]);
+            for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = O::to_e(v[r]);
+          }
         }
 #pragma unroll
         for (int ib = 0; ib < S::NIB; ++ib) {
@@ -339,45 +349,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
       __syncthreads();
 
-      // ------------------------------------ P1: H = K W1^T, A = act(H) (recompute)
-      f32x4 Hk[NF][NTB][NJB];
-      Q Akq[NTB][NJB];
-      {
-        E2TTT_LANE_IDS;
-        Q w1q[NF][NJB][NIB];
-#pragma unroll
-        for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
-#pragma unroll
-        for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-          for (int jj = 0; jj < NJB; ++jj) {
-            f32x4 acc[NF];
-#pragma unroll
-            for (int m = 0; m < NF; ++m) acc[m] = zero4();
-#pragma unroll
-            for (int p = 0; p < S::KS_D; ++p) {
-              auto af = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
-#pragma unroll
-              for (int m = 0; m < NF; ++m) {
-                typename O::Frag bf;
-#pragma unroll
-                for (int h = 0; h < S::NH; ++h) bf.h[h] = w1q[m][jj][S::NH * p + h];
-                acc[m] = O::mma(acc[m], af, bf);
-              }
-            }
-            f32x4 act;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              if constexpr (!SW) act[q] = gelu_f(acc[0][q]);
-              else act[q] = silu_f(acc[0][q]) * acc[1][q];
-            }
-#pragma unroll
-            for (int m = 0; m < NF; ++m) Hk[m][tb][jj] = acc[m];
-            Akq[tb][jj] = O::cvt(act);
-            sched_fence();
-          }
-      }
-
       // --------------------- P3: e, dY (first order, from the saved LN output)
       E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
       {
@@ -424,101 +395,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
       __syncthreads();
 
-      // ----------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
-      // For every tile: dA = dY W2, dH = dA act'(H);  u = K Wb1^T, K Mb1^T;
-      // rW = dY Wb2, dY Mb2;  dK^W += rowsum(dH uW + A rW), dK^M likewise;
-      // p = K^W uW + K^M uM (= d(Phi)/d(dH)), r2 = K^W rW + K^M rM (direct a-term);
-      // dAh = p act'(H);  Hh = p dA act''(H) + r2 act'(H)  (the Yh W2 term is added later)
-      Q dHq[NF][NTB][NJB];
-      Q dAhq[NTB][NJB];
-      f32x4 Hh[NF][NTB][NJB];
+      // ------------- carry adjoints: <Wb, W_0>, <Wb, M_0>, <Mb, M_0> (per wave)
       {
         E2TTT_LANE_IDS;
-        Q w2q[NJB][NIB];
-        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
-        opaque_state<S>(Wb);
-        opaque_state<S>(Mb);
-#pragma unroll
-        for (int tb = 0; tb < NTB; ++tb) {
-          float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-          for (int jj = 0; jj < NJB; ++jj) {
-            f32x4 dA = zero4(), rW = zero4(), rM = zero4();
-            f32x4 uW[NF], uM[NF];
-#pragma unroll
-            for (int m = 0; m < NF; ++m) { uW[m] = zero4(); uM[m] = zero4(); }
-#pragma unroll
-            for (int p = 0; p < S::KS_D; ++p) {
-              auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
-              auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
-              typename O::Frag b2, bw, bm;
-#pragma unroll
-              for (int h = 0; h < S::NH; ++h) {
-                b2.h[h] = w2q[jj][S::NH * p + h];
-                bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
-                bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
-              }
-              dA = O::mma(dA, fy, b2);
-              rW = O::mma(rW, fy, bw);
-              rM = O::mma(rM, fy, bm);
-#pragma unroll
-              for (int m = 0; m < NF; ++m) {
-#pragma unroll
-                for (int h = 0; h < S::NH; ++h) {
-                  bw.h[h] = O::cvt(Wb.t[m][jj][S::NH * p + h]);
-                  bm.h[h] = O::cvt(Mb.t[m][jj][S::NH * p + h]);
-                }
-                uW[m] = O::mma(uW[m], fk, bw);
-                uM[m] = O::mma(uM[m], fk, bm);
-              }
-            }
-            const f32x4 Af = quad_f32(Akq[tb][jj]);
-            f32x4 dH[NF], dAh, hh[NF];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int t = 16 * tb + 4 * g + q;
-              const float kwv = skw[t], kmv = skm[t];
-              const float r2 = kwv * rW[q] + kmv * rM[q];
-              if constexpr (!SW) {
-                const float h = Hk[0][tb][jj][q];
-                const float d1 = gelu_d1(h), d2 = gelu_d2(h);
-                dH[0][q] = dA[q] * d1;
-                const float pp = kwv * uW[0][q] + kmv * uM[0][q];
-                dAh[q] = pp * d1;
-                hh[0][q] = pp * dA[q] * d2 + r2 * d1;
-                kwp[q] += dH[0][q] * uW[0][q] + Af[q] * rW[q];
-                kmp[q] += dH[0][q] * uM[0][q] + Af[q] * rM[q];
-              } else {
-                const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
-                const float sg = silu_f(hg), s1 = silu_d1(hg), s2 = silu_d2(hg);
-                dH[0][q] = dA[q] * hu * s1;
-                dH[1][q] = dA[q] * sg;
-                const float pg = kwv * uW[0][q] + kmv * uM[0][q];
-                const float pu = kwv * uW[1][q] + kmv * uM[1][q];
-                dAh[q] = pg * hu * s1 + pu * sg;
-                hh[0][q] = pg * dA[q] * hu * s2 + pu * dA[q] * s1 + r2 * hu * s1;
-                hh[1][q] = pg * dA[q] * s1 + r2 * sg;
-                kwp[q] += dH[0][q] * uW[0][q] + dH[1][q] * uW[1][q] + Af[q] * rW[q];
-                kmp[q] += dH[0][q] * uM[0][q] + dH[1][q] * uM[1][q] + Af[q] * rM[q];
-              }
-            }
-#pragma unroll
-            for (int m = 0; m < NF; ++m) { dHq[m][tb][jj] = O::cvt(dH[m]); Hh[m][tb][jj] = hh[m]; }
-            dAhq[tb][jj] = O::cvt(dAh);
-            sched_fence();
-          }
-          // per-wave row partials of dK^W, dK^M for this token block
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float sw = group16_sum(kwp[q]);
-            const float sm2 = group16_sum(kmp[q]);
-            if (c == 0) {
-              kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sw;
-              kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sm2;
-            }
-          }
-        }
-        // carry adjoints: <Wb, W_0>, <Wb, M_0>, <Mb, M_0>
         float pcw = 0.0f, pcm = 0.0f, pcb = 0.0f;
 #pragma unroll
         for (int m = 0; m < NMAT; ++m) {
@@ -543,6 +422,188 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         pcb = wave_sum(pcb);
         if (lane == 0) { cbp[w * 4 + 0] = pcw; cbp[w * 4 + 1] = pcm; cbp[w * 4 + 2] = pcb; }
       }
+
+      // ----------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
+      // Two passes over the token blocks keep fewer operands live at once.
+      // Pass 1, per tile: H = K W1^T and A = act(H) (recomputed from the
+      // checkpoint), dA = dY W2, dH = dA act'(H), u = K Wb1^T and K Mb1^T,
+      // p = K^W uW + K^M uM (= d(Phi)/d(dH)), dAh = p act'(H),
+      // Hh = p dA act''(H), dK^W += rowsum(dH uW), dK^M likewise.
+      // Pass 2, per tile: rW = dY Wb2, rM = dY Mb2, r2 = K^W rW + K^M rM (the
+      // direct a-term), Hh += r2 act'(H), dK^W += rowsum(A rW), dK^M likewise.
+      // (The Yh W2 term of Hh is added in P8.)
+      // MLP with one j-round half: dH goes straight into the j-round act buffer
+      constexpr bool DH_LDS = (NF == 1) && (L::JH == 1);
+      Q Akq[NTB][NJB];
+      // act'(H) factors: MLP GELU'(H); SwiGLU Hu SiLU'(Hg), SiLU(Hg)
+      f32x4 D1[NF][NTB][NJB];
+      Q dHq[DH_LDS ? 1 : NF][NTB][NJB];
+      Q dAhq[NTB][NJB];
+      // Hh, in LDS when it fits (hh_at), else in registers
+      f32x4 HhR[L::HH_LDS ? 1 : NF][L::HH_LDS ? 1 : NTB][L::HH_LDS ? 1 : NJB];
+      f32x4* const hhlds = reinterpret_cast<f32x4*>(smem + L::HHR);
+      auto hh_at = [&](int m, int tb, int jj, int ln) -> f32x4& {
+        if constexpr (L::HH_LDS)
+          return hhlds[((m * NTB + tb) * NW + w) * 64 + ln];
+        else
+          return HhR[m][tb][jj];
+      };
+      {
+        E2TTT_LANE_IDS;
+        Q w1q[NF][NJB][NIB];
+#pragma unroll
+        for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
+        Q w2q[NJB][NIB];
+        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb) {
+          // bf16 operand copies of the adjoint state are re-formed per token
+          // block (a few conversions) instead of being held across the loop
+          opaque_state<S>(Wb);
+          opaque_state<S>(Mb);
+          E2TTT_LANE_IDS;
+          float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            f32x4 dA = zero4();
+            f32x4 uW[NF], uM[NF], hk[NF];
+#pragma unroll
+            for (int m = 0; m < NF; ++m) { uW[m] = zero4(); uM[m] = zero4(); hk[m] = zero4(); }
+#pragma unroll
+            for (int p = 0; p < S::KS_D; ++p) {
+              auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
+              auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
+              typename O::Frag b2, bw, bm;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) b2.h[h] = w2q[jj][S::NH * p + h];
+              dA = O::mma(dA, fy, b2);
+#pragma unroll
+              for (int m = 0; m < NF; ++m) {
+#pragma unroll
+                for (int h = 0; h < S::NH; ++h) {
+                  b2.h[h] = w1q[m][jj][S::NH * p + h];
+                  bw.h[h] = O::cvt(Wb.t[m][jj][S::NH * p + h]);
+                  bm.h[h] = O::cvt(Mb.t[m][jj][S::NH * p + h]);
+                }
+                hk[m] = O::mma(hk[m], fk, b2);
+                uW[m] = O::mma(uW[m], fk, bw);
+                uM[m] = O::mma(uM[m], fk, bm);
+              }
+              sched_fence();   // one K-step's operands live at a time
+            }
+            f32x4 dH[NF], dAh, hh[NF], Af, d1v[NF];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int t = 16 * tb + 4 * g + q;
+              const float kwv = skw[t], kmv = skm[t];
+              if constexpr (!SW) {
+                const Act3 ga = gelu3(hk[0][q]);
+                Af[q] = ga.f;
+                d1v[0][q] = ga.d1;
+                dH[0][q] = dA[q] * ga.d1;
+                const float pp = kwv * uW[0][q] + kmv * uM[0][q];
+                dAh[q] = pp * ga.d1;
+                hh[0][q] = pp * dA[q] * ga.d2;
+                kwp[q] += dH[0][q] * uW[0][q];
+                kmp[q] += dH[0][q] * uM[0][q];
+              } else {
+                const float hg = hk[0][q], hu = hk[1][q];
+                const Act3 sa = silu3(hg);
+                const float sg = sa.f, s1 = sa.d1, s2 = sa.d2;
+                Af[q] = sg * hu;
+                d1v[0][q] = hu * s1;
+                d1v[1][q] = sg;
+                dH[0][q] = dA[q] * hu * s1;
+                dH[1][q] = dA[q] * sg;
+                const float pg = kwv * uW[0][q] + kmv * uM[0][q];
+                const float pu = kwv * uW[1][q] + kmv * uM[1][q];
+                dAh[q] = pg * hu * s1 + pu * sg;
+                hh[0][q] = pg * dA[q] * hu * s2 + pu * dA[q] * s1;
+                hh[1][q] = pg * dA[q] * s1;
+                kwp[q] += dH[0][q] * uW[0][q] + dH[1][q] * uW[1][q];
+                kmp[q] += dH[0][q] * uM[0][q] + dH[1][q] * uM[1][q];
+              }
+            }
+#pragma unroll
+            for (int m = 0; m < NF; ++m) {
+              hh_at(m, tb, jj, lane) = hh[m];
+              D1[m][tb][jj] = d1v[m];
+            }
+            if constexpr (DH_LDS) {
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                ja[(16 * tb + 4 * g + q) * L::LDJ + 16 * (w * NJB + jj) + c] = O::to_e(dH[0][q]);
+            } else {
+#pragma unroll
+              for (int m = 0; m < NF; ++m) dHq[m][tb][jj] = O::cvt(dH[m]);
+            }
+            dAhq[tb][jj] = O::cvt(dAh);
+            Akq[tb][jj] = O::cvt(Af);
+            sched_fence();
+          }
+          // per-wave row partials of dK^W, dK^M for this token block
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float sw = group16_sum(kwp[q]);
+            const float sm2 = group16_sum(kmp[q]);
+            if (c == 0) {
+              kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sw;
+              kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sm2;
+            }
+          }
+        }
+      }
+      {
+        E2TTT_LANE_IDS;
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb) {
+          opaque_state<S>(Wb);
+          opaque_state<S>(Mb);
+          E2TTT_LANE_IDS;
+          float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            f32x4 rW = zero4(), rM = zero4();
+#pragma unroll
+            for (int p = 0; p < S::KS_D; ++p) {
+              auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
+              typename O::Frag bw, bm;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) {
+                bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
+                bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
+              }
+              rW = O::mma(rW, fy, bw);
+              rM = O::mma(rM, fy, bm);
+            }
+            const f32x4 Af = quad_f32(Akq[tb][jj]);
+            f32x4 hv[NF];
+#pragma unroll
+            for (int m = 0; m < NF; ++m) hv[m] = hh_at(m, tb, jj, lane);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int t = 16 * tb + 4 * g + q;
+              const float r2 = skw[t] * rW[q] + skm[t] * rM[q];
+#pragma unroll
+              for (int m = 0; m < NF; ++m) hv[m][q] += r2 * D1[m][tb][jj][q];
+              kwp[q] += Af[q] * rW[q];
+              kmp[q] += Af[q] * rM[q];
+            }
+#pragma unroll
+            for (int m = 0; m < NF; ++m) hh_at(m, tb, jj, lane) = hv[m];
+            sched_fence();
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float sw = group16_sum(kwp[q]);
+            const float sm2 = group16_sum(kmp[q]);
+            if (c == 0) {
+              kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] += sw;
+              kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] += sm2;
+            }
+          }
+        }
+      }
       // direct terms through the state adjoint, over the hidden index:
       //   r1 = K^W (dH Wb1) + K^M (dH Mb1)  (into dK),  p2 = K^W (A Wb2^T) + K^M (A Mb2^T)  (into dYh)
       JAcc<S> dkacc, dyhacc;
@@ -550,17 +611,21 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       dyhacc.zero();
       {
       E2TTT_LANE_IDS;
+      // (with a single j-round half the two rounds of a pair share the act buffer)
 #pragma unroll
       for (int m = 0; m < NF; ++m) {
-        jround<S>(dkacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
-                  [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
-        jround<S>(dkacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(dHq[m][tb][jj]); },
-                  [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+        const int mq = DH_LDS ? 0 : m;
+        jround<S, !DH_LDS>(dkacc, skw, ja, jw,
+                           [&](int tb, int jj) { return quad_f32(dHq[mq][tb][jj]); },
+                           [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
+        jround<S, false>(dkacc, skm, ja, jw,
+                         [&](int tb, int jj) { return quad_f32(dHq[mq][tb][jj]); },
+                         [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
       }
       jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
                 [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
-      jround<S>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
-                [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+      jround<S, false>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+                       [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
       }
 
       // ------------------------------------ P5: adjoint state transition
@@ -697,14 +762,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               ah = O::mma(ah, af, bf);
             }
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              if constexpr (!SW) {
-                Hh[0][tb][jj][q] += ah[q] * gelu_d1(Hk[0][tb][jj][q]);
-              } else {
-                const float hg = Hk[0][tb][jj][q], hu = Hk[1][tb][jj][q];
-                Hh[0][tb][jj][q] += ah[q] * hu * silu_d1(hg);
-                Hh[1][tb][jj][q] += ah[q] * silu_f(hg);
-              }
+            for (int m = 0; m < NF; ++m) {
+              f32x4 hv = hh_at(m, tb, jj, lane);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) hv[q] += ah[q] * D1[m][tb][jj][q];
+              hh_at(m, tb, jj, lane) = hv;
             }
             sched_fence();
           }
@@ -731,7 +793,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               for (int m = 0; m < NF; ++m) {
                 typename O::Frag bh;
 #pragma unroll
-                for (int h = 0; h < S::NH; ++h) bh.h[h] = O::cvt(Hh[m][S::NH * p + h][jj]);
+                for (int h = 0; h < S::NH; ++h) bh.h[h] = O::cvt(hh_at(m, S::NH * p + h, jj, lane));
                 Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fk, bh);
               }
             }
@@ -742,7 +804,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         for (int m = 0; m < NF; ++m) {
           Q w1q[NJB][NIB];
           load_ckpt_mat<S>(w1q, ckW, m, w, lane);
-          jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return Hh[m][tb][jj]; },
+          jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return hh_at(m, tb, jj, lane); },
                     [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
         }
         const float ksign = (resln && rank == 0) ? -1.0f : 0.0f;
@@ -806,7 +868,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             ybqt[i * S::LDC + t] = O::to_e(yb[q]);
           }
         }
-        f32x4 Hq[NF][NTB][NJB];
+        f32x4 D1q[NF][NTB][NJB];   // act'(H_Q) factors, as D1 above
         Q Aqq[NTB][NJB];
         {
           Q w1q[NF][NJB][NIB];
@@ -833,11 +895,17 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               f32x4 act;
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                if constexpr (!SW) act[q] = gelu_f(acc[0][q]);
-                else act[q] = silu_f(acc[0][q]) * acc[1][q];
+                if constexpr (!SW) {
+                  const NormalCdf n = normal_cdf(acc[0][q]);
+                  act[q] = acc[0][q] * n.cdf;
+                  D1q[0][tb][jj][q] = n.cdf + acc[0][q] * n.pdf;
+                } else {
+                  const float hg = acc[0][q], hu = acc[1][q], sg = sigm_f(hg);
+                  D1q[1][tb][jj][q] = hg * sg;
+                  D1q[0][tb][jj][q] = hu * sg * (1.0f + hg * (1.0f - sg));
+                  act[q] = hg * sg * hu;
+                }
               }
-#pragma unroll
-              for (int m = 0; m < NF; ++m) Hq[m][tb][jj] = acc[m];
               Aqq[tb][jj] = O::cvt(act);
               sched_fence();
             }
@@ -864,13 +932,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               f32x4 hb[NF];
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                if constexpr (!SW) {
-                  hb[0][q] = ab[q] * gelu_d1(Hq[0][tb][jj][q]);
-                } else {
-                  const float hg = Hq[0][tb][jj][q], hu = Hq[1][tb][jj][q];
-                  hb[0][q] = ab[q] * hu * silu_d1(hg);
-                  hb[1][q] = ab[q] * silu_f(hg);
-                }
+#pragma unroll
+                for (int m = 0; m < NF; ++m) hb[m][q] = ab[q] * D1q[m][tb][jj][q];
               }
 #pragma unroll
               for (int m = 0; m < NF; ++m) Hbq[m][tb][jj] = O::cvt(hb[m]);

@@ -179,6 +179,37 @@ __device__ __forceinline__ void stage_tile(typename S::E* dst, const void* src, 
   }
 }
 
+// A CM x D token tile held in registers (16-byte vectors, rows < len, zero
+// beyond): the next chunk's inputs are loaded while the current chunk runs and
+// written to LDS when it starts, so their global-memory latency is hidden.
+template <class S>
+struct TileRegs {
+  static constexpr int VE = 16 / (int)sizeof(typename S::E);   // elements per vector
+  static constexpr int NV = S::CM * S::D / VE;
+  static constexpr int PER = (NV + S::NT - 1) / S::NT;
+  uint4 v[PER];
+
+  __device__ __forceinline__ void load(const void* src, long row0, int len, int tid) {
+    using IOT = typename IoT<S::BF>::T;
+    static_assert(sizeof(IOT) == sizeof(typename S::E), "io and operand types differ");
+    const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const IOT*>(src) + row0 * S::D);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = (tid + k * S::NT) * VE;
+      v[k] = make_uint4(0u, 0u, 0u, 0u);
+      if (e < S::CM * S::D && e / S::D < len) v[k] = p[tid + k * S::NT];
+    }
+  }
+  __device__ __forceinline__ void store(typename S::E* dst, int tid) const {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = (tid + k * S::NT) * VE;
+      if (e < S::CM * S::D)
+        *reinterpret_cast<uint4*>(dst + (e / S::D) * S::LDD + e % S::D) = v[k];
+    }
+  }
+};
+
 // Y[t][i] = sum_j A[t][j] Wt[i][j]  (j-contraction, both operands in LDS),
 // written to y (fp32 [CM][D]).  Work is split into (token block, head block
 // pair) items over the waves.

@@ -93,6 +93,23 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       sm.w2[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
   }
 
+  // inputs of the next chunk, loaded one chunk ahead
+  TileRegs<S> pk, pq, pv;
+  float pkw = 0.0f, pkm = 0.0f, pcar = 0.0f;
+  auto prefetch = [&](long uu, int rc) {
+    E2TTT_LANE_IDS;
+    const long r0 = uu * T + (long)rc * C;
+    const int ln = min(C, T - rc * C);
+    pk.load(a.k, r0, ln, tid);
+    pq.load(a.q, r0, ln, tid);
+    pv.load(a.v, r0, ln, tid);
+    if (tid < S::CM) {
+      pkw = (tid < ln) ? a.kw[r0 + tid] : 0.0f;
+      pkm = (tid < ln) ? a.km[r0 + tid] : 0.0f;
+    }
+    if (tid < 3) pcar = a.carry[(uu * NC + rc) * 3 + tid];
+  };
+
   for (long u = px.p; u < a.U; u += NP) {
     StateTiles<S> W, M;
     {
@@ -100,6 +117,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
       load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, j0, w, g, c);
     }
+    prefetch(u, 0);
 
     for (int r = 0; r < NC; ++r, ++nch) {
       const int s0 = r * C;
@@ -110,15 +128,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // -------------------------------------------------------- stage (a1)
       {
       E2TTT_LANE_IDS;
-      stage_tile<S>(sm.xk, a.k, row0, len, tid);
-      stage_tile<S>(sm.xq, a.q, row0, len, tid);
-      stage_tile<S>(sm.xv, a.v, row0, len, tid);
-#pragma unroll 1
-      for (int t = tid; t < S::CM; t += S::NT) {
-        sm.kw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
-        sm.km[t] = (t < len) ? a.km[row0 + t] : 0.0f;
+      pk.store(sm.xk, tid);
+      pq.store(sm.xq, tid);
+      pv.store(sm.xv, tid);
+      if (tid < S::CM) {
+        sm.kw[tid] = pkw;
+        sm.km[tid] = pkm;
       }
-      if (tid < 3) sm.carry[tid] = a.carry[(u * NC + r) * 3 + tid];
+      if (tid < 3) sm.carry[tid] = pcar;
       if (a.ckpt) {
         char* cb = static_cast<char*>(a.ckpt) + ((u * NC + r) * S::NS + rank) * 2 * a.ckpt_stride;
         store_ckpt<S>(W, cb, w, lane);
@@ -137,9 +154,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       opaque_state<S>(M);
       }
       __syncthreads();
+      if (r + 1 < NC) prefetch(u, r + 1);
 
       // ------------------------------------------- K-side forward (a3)
-      f32x4 H[NTB][NJB];                   // MLP: H;  SwiGLU: Hg
+      // act'(H) kept for dH: MLP GELU'(H); SwiGLU (Hu SiLU'(Hg), SiLU(Hg))
+      f32x4 H[NTB][NJB];
       f32x4 Hu[NTB][(S::FW == 1) ? NJB : 1];
       typename O::Q AK[NTB][NJB];          // act(H) as operand quads (rows t)
       {
@@ -168,14 +187,22 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
             if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
           }
-          f32x4 act;
+          f32x4 act, d1, d2;
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
-            if constexpr (S::FW == 0) act[rr] = gelu_f(acc[rr]);
-            else act[rr] = silu_f(acc[rr]) * accu[rr];
+            if constexpr (S::FW == 0) {
+              const NormalCdf n = normal_cdf(acc[rr]);
+              act[rr] = acc[rr] * n.cdf;
+              d1[rr] = n.cdf + acc[rr] * n.pdf;
+            } else {
+              const float hg = acc[rr], hu = accu[rr], sg = sigm_f(hg);
+              d2[rr] = hg * sg;                              // SiLU(Hg)
+              d1[rr] = hu * sg * (1.0f + hg * (1.0f - sg));  // Hu SiLU'(Hg)
+              act[rr] = d2[rr] * hu;
+            }
           }
-          H[tb][jj] = acc;
-          if constexpr (S::FW == 1) Hu[tb][jj] = accu;
+          H[tb][jj] = d1;
+          if constexpr (S::FW == 1) Hu[tb][jj] = d2;
           AK[tb][jj] = O::cvt(act);
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr)
@@ -315,13 +342,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           f32x4 dh1, dh2;
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
-            if constexpr (S::FW == 0) {
-              dh1[rr] = da[rr] * gelu_d1(H[tb][jj][rr]);
-            } else {
-              const float hg = H[tb][jj][rr], hu = Hu[tb][jj][rr];
-              dh1[rr] = da[rr] * hu * silu_d1(hg);
-              dh2[rr] = da[rr] * silu_f(hg);
-            }
+            dh1[rr] = da[rr] * H[tb][jj][rr];
+            if constexpr (S::FW == 1) dh2[rr] = da[rr] * Hu[tb][jj][rr];
           }
           DH[tb][jj] = O::cvt(dh1);
           if constexpr (S::FW == 1) DU[tb][jj] = O::cvt(dh2);

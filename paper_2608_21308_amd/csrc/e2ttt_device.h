@@ -159,6 +159,20 @@ __device__ __forceinline__ float silu_d2(float x) {
   return s * (1.0f - s) * (2.0f + x * (1.0f - 2.0f * s));
 }
 
+// An activation with its first two derivatives from one evaluation of the
+// transcendental part (one erfc for GELU, one sigmoid for SiLU).
+struct Act3 {
+  float f, d1, d2;
+};
+__device__ __forceinline__ Act3 gelu3(float x) {
+  const NormalCdf n = normal_cdf(x);
+  return Act3{x * n.cdf, n.cdf + x * n.pdf, n.pdf * (2.0f - x * x)};
+}
+__device__ __forceinline__ Act3 silu3(float x) {
+  const float s = sigm_f(x);
+  return Act3{x * s, s * (1.0f + x * (1.0f - s)), s * (1.0f - s) * (2.0f + x * (1.0f - 2.0f * s))};
+}
+
 // ------------------------------------------------------------- reductions
 // DPP lane permutations within a row of 16 lanes (no LDS round trip).
 template <int CTRL>
