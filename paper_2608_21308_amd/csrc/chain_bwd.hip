@@ -217,20 +217,6 @@ __device__ __forceinline__ void jacc_store_f32(const JAcc<S>& out, float* dst, F
   }
 }
 
-// Copy a CM x D fp32 tile (rows < len, zero beyond) from global memory to LDS.
-template <class S>
-__device__ __forceinline__ void stage_f32(float* dst, const float* src, long row0, int len,
-                                          int tid) {
-  constexpr int NV = S::CM * S::D / 4;
-  const float4* p = reinterpret_cast<const float4*>(src + row0 * S::D);
-#pragma unroll 1
-  for (int v = tid; v < NV; v += S::NT) {
-    float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if ((4 * v) / S::D < len) x = p[v];
-    reinterpret_cast<float4*>(dst)[v] = x;
-  }
-}
-
 // Exchange slot of one rank for one parity: [dYh | dk | dq] partials, CM x D floats each.
 template <class S>
 __device__ __forceinline__ float* bwd_slot(float* xbuf, long p, int rank, int parity) {
@@ -312,6 +298,35 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   float* const carryb_slot = a.carryb + rank * a.U * NC * 3;
   long nch = 0;   // chunks processed by this workgroup (exchange parity)
 
+  // inputs loaded ahead of use: the K side of the next chunk during the output
+  // branch, the Q side of this chunk during P7
+  TileRegs<S> pK, pV, pQ, pD;
+  F32TileRegs<S> pZ, pZq;
+  float pkw = 0.0f, pkm = 0.0f, prk = 0.0f, prq = 0.0f, pcar = 0.0f;
+  auto prefetch_k = [&](long uu, int rc) {
+    E2TTT_LANE_IDS;
+    const long r0 = uu * T + (long)rc * C;
+    const int ln = min(C, T - rc * C);
+    pK.load(a.k, r0, ln, tid);
+    pV.load(a.v, r0, ln, tid);
+    pZ.load(a.zk, r0, ln, tid);
+    if (tid < S::CM) {
+      pkw = (tid < ln) ? a.kw[r0 + tid] : 0.0f;
+      pkm = (tid < ln) ? a.km[r0 + tid] : 0.0f;
+      prk = (tid < ln) ? a.rk[r0 + tid] : 0.0f;
+    }
+    if (tid < 3) pcar = a.carry[(uu * NC + rc) * 3 + tid];
+  };
+  auto prefetch_q = [&](long uu, int rc) {
+    E2TTT_LANE_IDS;
+    const long r0 = uu * T + (long)rc * C;
+    const int ln = min(C, T - rc * C);
+    pQ.load(a.q, r0, ln, tid);
+    pD.load(a.d_out, r0, ln, tid);
+    pZq.load(a.zq, r0, ln, tid);
+    if (tid < S::CM) prq = (tid < ln) ? a.rq[r0 + tid] : 0.0f;
+  };
+
   for (long u = px.p; u < a.U; u += NP) {
     // adjoint of the final state
     StateTiles<S> Wb, Mb;
@@ -321,6 +336,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, j0, w, g, c);
     }
     int pend_r = -1, pend_par = 0;   // chunk whose dk, dq partials are not yet combined
+    prefetch_k(u, NC - 1);
 
     for (int r = NC - 1; r >= 0; --r, ++nch) {
       const int s0 = r * C;
@@ -332,20 +348,31 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           static_cast<const char*>(a.ckpt) + ((u * NC + r) * S::NS + rank) * 2 * a.ckpt_stride;
       const char* ckM = ckW + a.ckpt_stride;
 
+      // chunk-start weights W_0 (kept for the whole chunk) and momentum M_0
+      // (for the carry adjoints), issued first so that P0 and P3 hide them
+      Q w0q[NMAT][NJB][NIB], m0q[NMAT][NJB][NIB];
+      {
+        E2TTT_LANE_IDS;
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m) {
+          load_ckpt_mat<S>(w0q[m], ckW, m, w, lane);
+          load_ckpt_mat<S>(m0q[m], ckM, m, w, lane);
+        }
+      }
+
       // ---------------------------------------------------------- P0: stage
       E* xv = reinterpret_cast<E*>(rr);
       {
         E2TTT_LANE_IDS;
-        stage_tile<S>(xk, a.k, row0, len, tid);
-        stage_tile<S>(xv, a.v, row0, len, tid);
-        stage_f32<S>(yk, a.zk, row0, len, tid);   // Z (or Y without the residual LN)
-#pragma unroll 1
-        for (int t = tid; t < S::CM; t += S::NT) {
-          skw[t] = (t < len) ? a.kw[row0 + t] : 0.0f;
-          skm[t] = (t < len) ? a.km[row0 + t] : 0.0f;
-          row[2 * t] = (t < len) ? a.rk[row0 + t] : 0.0f;   // 1 / sigma
+        pK.store(xk, tid);
+        pV.store(xv, tid);
+        pZ.store(yk, tid);                       // Z (or Y without the residual LN)
+        if (tid < S::CM) {
+          skw[tid] = pkw;
+          skm[tid] = pkm;
+          row[2 * tid] = prk;                    // 1 / sigma
         }
-        if (tid < 3) scar[tid] = a.carry[(u * NC + r) * 3 + tid];
+        if (tid < 3) scar[tid] = pcar;
       }
       __syncthreads();
 
@@ -401,14 +428,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         float pcw = 0.0f, pcm = 0.0f, pcb = 0.0f;
 #pragma unroll
         for (int m = 0; m < NMAT; ++m) {
-          Q q0[NJB][NIB], qm[NJB][NIB];
-          load_ckpt_mat<S>(q0, ckW, m, w, lane);
-          load_ckpt_mat<S>(qm, ckM, m, w, lane);
 #pragma unroll
           for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
             for (int ib = 0; ib < NIB; ++ib) {
-              const f32x4 w0 = quad_f32(q0[jj][ib]), m0 = quad_f32(qm[jj][ib]);
+              const f32x4 w0 = quad_f32(w0q[m][jj][ib]), m0 = quad_f32(m0q[m][jj][ib]);
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
                 pcw += Wb.t[m][jj][ib][q] * w0[q];
@@ -450,11 +474,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       };
       {
         E2TTT_LANE_IDS;
-        Q w1q[NF][NJB][NIB];
-#pragma unroll
-        for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
-        Q w2q[NJB][NIB];
-        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+        const auto& w1q = w0q;            // first-layer matrices m < NF
+        const auto& w2q = w0q[SEC];
 #pragma unroll
         for (int tb = 0; tb < NTB; ++tb) {
           // bf16 operand copies of the adjoint state are re-formed per token
@@ -647,8 +668,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       float* dyh = reinterpret_cast<float*>(rr);
       {
         E2TTT_LANE_IDS;
-        Q w2q[NJB][NIB];
-        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+        const auto& w2q = w0q[SEC];
         jround<S>(dyhacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(dAhq[tb][jj]); },
                   [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
         jacc_store_f32<S>(dyhacc, dyh, [](int, int) { return 0.0f; }, w, g, c);
@@ -670,6 +690,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
 
       // ------------------------------------- P7: LayerNorm second order
+      prefetch_q(u, r);
       {
         E2TTT_LANE_IDS;
         using IOT = typename IoT<S::BF>::T;
@@ -746,8 +767,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           const int i = idx % D, t = idx / D;
           xkt[i * S::LDC + t] = xk[t * S::LDD + i];
         }
-        Q w2q[NJB][NIB];
-        load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+        const auto& w2q = w0q[SEC];
 #pragma unroll
         for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -802,8 +822,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         // dk += Hh W1 (over the hidden index)
 #pragma unroll
         for (int m = 0; m < NF; ++m) {
-          Q w1q[NJB][NIB];
-          load_ckpt_mat<S>(w1q, ckW, m, w, lane);
+          const auto& w1q = w0q[m];
           jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return hh_at(m, tb, jj, lane); },
                     [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
         }
@@ -826,12 +845,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         E* ybq = yh;                                     // Yb_Q [t][i]
         E* ybqt = dyt;                                   // Yb_Q^T [i][t]
         E* xqt = yht;                                    // Q^T [i][t]
-        stage_tile<S>(xq, a.q, row0, len, tid);
-        stage_tile<S>(xdo, a.d_out, row0, len, tid);
-        stage_f32<S>(yk, a.zq, row0, len, tid);         // Z_Q (or Y_Q)
-#pragma unroll 1
-        for (int t = tid; t < S::CM; t += S::NT) row[2 * t] = (t < len) ? a.rq[row0 + t] : 0.0f;
+        pQ.store(xq, tid);
+        pD.store(xdo, tid);
+        pZq.store(yk, tid);                             // Z_Q (or Y_Q)
+        if (tid < S::CM) row[2 * tid] = prq;
         __syncthreads();
+        if (r > 0) prefetch_k(u, r - 1);
 #pragma unroll 1
         for (int idx = tid; idx < D * S::CM; idx += S::NT) {
           const int i = idx % D, t = idx / D;
@@ -871,9 +890,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         f32x4 D1q[NF][NTB][NJB];   // act'(H_Q) factors, as D1 above
         Q Aqq[NTB][NJB];
         {
-          Q w1q[NF][NJB][NIB];
-#pragma unroll
-          for (int m = 0; m < NF; ++m) load_ckpt_mat<S>(w1q[m], ckW, m, w, lane);
+          const auto& w1q = w0q;
 #pragma unroll
           for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -914,8 +931,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         // Ab_Q = Yb_Q W2;  Hb_Q = Ab_Q act'(H_Q);  Wb2 += Yb_Q^T A_Q;  Wb1 += Q^T Hb_Q
         Q Hbq[NF][NTB][NJB];
         {
-          Q w2q[NJB][NIB];
-          load_ckpt_mat<S>(w2q, ckW, SEC, w, lane);
+          const auto& w2q = w0q[SEC];
 #pragma unroll
           for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -968,8 +984,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         dqacc.zero();
 #pragma unroll
         for (int m = 0; m < NF; ++m) {
-          Q w1q[NJB][NIB];
-          load_ckpt_mat<S>(w1q, ckW, m, w, lane);
+          const auto& w1q = w0q[m];
           jround<S>(dqacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(Hbq[m][tb][jj]); },
                     [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
         }

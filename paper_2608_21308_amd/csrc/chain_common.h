@@ -210,6 +210,30 @@ struct TileRegs {
   }
 };
 
+// The same for an fp32 CM x D tile (saved LayerNorm outputs), stored to a
+// dense [CM][D] fp32 LDS array.
+template <class S>
+struct F32TileRegs {
+  static constexpr int NV = S::CM * S::D / 4;
+  static constexpr int PER = (NV + S::NT - 1) / S::NT;
+  float4 v[PER];
+
+  __device__ __forceinline__ void load(const float* src, long row0, int len, int tid) {
+    const float4* p = reinterpret_cast<const float4*>(src + row0 * S::D);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = (tid + k * S::NT) * 4;
+      v[k] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (e < S::CM * S::D && e / S::D < len) v[k] = p[tid + k * S::NT];
+    }
+  }
+  __device__ __forceinline__ void store(float* dst, int tid) const {
+#pragma unroll
+    for (int k = 0; k < PER; ++k)
+      if (tid + k * S::NT < NV) reinterpret_cast<float4*>(dst)[tid + k * S::NT] = v[k];
+  }
+};
+
 // Y[t][i] = sum_j A[t][j] Wt[i][j]  (j-contraction, both operands in LDS),
 // written to y (fp32 [CM][D]).  Work is split into (token block, head block
 // pair) items over the waves.
