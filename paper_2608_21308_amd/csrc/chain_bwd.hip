@@ -448,14 +448,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
 
       // ----------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
-      // Two passes over the token blocks keep fewer operands live at once.
-      // Pass 1, per tile: H = K W1^T and A = act(H) (recomputed from the
-      // checkpoint), dA = dY W2, dH = dA act'(H), u = K Wb1^T and K Mb1^T,
-      // p = K^W uW + K^M uM (= d(Phi)/d(dH)), dAh = p act'(H),
-      // Hh = p dA act''(H), dK^W += rowsum(dH uW), dK^M likewise.
-      // Pass 2, per tile: rW = dY Wb2, rM = dY Mb2, r2 = K^W rW + K^M rM (the
-      // direct a-term), Hh += r2 act'(H), dK^W += rowsum(A rW), dK^M likewise.
-      // (The Yh W2 term of Hh is added in P8.)
+      // For every tile: H = K W1^T and A = act(H) (recomputed from the checkpoint),
+      // dA = dY W2, dH = dA act'(H);  u = K Wb1^T, K Mb1^T;
+      // rW = dY Wb2, dY Mb2;  dK^W += rowsum(dH uW + A rW), dK^M likewise;
+      // p = K^W uW + K^M uM (= d(Phi)/d(dH)), r2 = K^W rW + K^M rM (direct a-term);
+      // dAh = p act'(H);  Hh = p dA act''(H) + r2 act'(H)  (the Yh W2 term is added in P8)
       // MLP with one j-round half: dH goes straight into the j-round act buffer
       constexpr bool DH_LDS = (NF == 1) && (L::JH == 1);
       Q Akq[NTB][NJB];
@@ -473,7 +470,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           return HhR[m][tb][jj];
       };
       {
-        E2TTT_LANE_IDS;
         const auto& w1q = w0q;            // first-layer matrices m < NF
         const auto& w2q = w0q[SEC];
 #pragma unroll
@@ -486,7 +482,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
           for (int jj = 0; jj < NJB; ++jj) {
-            f32x4 dA = zero4();
+            f32x4 dA = zero4(), rW = zero4(), rM = zero4();
             f32x4 uW[NF], uM[NF], hk[NF];
 #pragma unroll
             for (int m = 0; m < NF; ++m) { uW[m] = zero4(); uM[m] = zero4(); hk[m] = zero4(); }
@@ -496,8 +492,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
               typename O::Frag b2, bw, bm;
 #pragma unroll
-              for (int h = 0; h < S::NH; ++h) b2.h[h] = w2q[jj][S::NH * p + h];
+              for (int h = 0; h < S::NH; ++h) {
+                b2.h[h] = w2q[jj][S::NH * p + h];
+                bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
+                bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
+              }
               dA = O::mma(dA, fy, b2);
+              rW = O::mma(rW, fy, bw);
+              rM = O::mma(rM, fy, bm);
 #pragma unroll
               for (int m = 0; m < NF; ++m) {
 #pragma unroll
@@ -512,44 +514,42 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               }
               sched_fence();   // one K-step's operands live at a time
             }
-            f32x4 dH[NF], dAh, hh[NF], Af, d1v[NF];
+            f32x4 dH[NF], dAh, hh[NF], Af;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int t = 16 * tb + 4 * g + q;
               const float kwv = skw[t], kmv = skm[t];
+              const float r2 = kwv * rW[q] + kmv * rM[q];
               if constexpr (!SW) {
                 const Act3 ga = gelu3(hk[0][q]);
                 Af[q] = ga.f;
-                d1v[0][q] = ga.d1;
+                D1[0][tb][jj][q] = ga.d1;
                 dH[0][q] = dA[q] * ga.d1;
                 const float pp = kwv * uW[0][q] + kmv * uM[0][q];
                 dAh[q] = pp * ga.d1;
-                hh[0][q] = pp * dA[q] * ga.d2;
-                kwp[q] += dH[0][q] * uW[0][q];
-                kmp[q] += dH[0][q] * uM[0][q];
+                hh[0][q] = pp * dA[q] * ga.d2 + r2 * ga.d1;
+                kwp[q] += dH[0][q] * uW[0][q] + Af[q] * rW[q];
+                kmp[q] += dH[0][q] * uM[0][q] + Af[q] * rM[q];
               } else {
                 const float hg = hk[0][q], hu = hk[1][q];
                 const Act3 sa = silu3(hg);
                 const float sg = sa.f, s1 = sa.d1, s2 = sa.d2;
                 Af[q] = sg * hu;
-                d1v[0][q] = hu * s1;
-                d1v[1][q] = sg;
+                D1[0][tb][jj][q] = hu * s1;
+                D1[1][tb][jj][q] = sg;
                 dH[0][q] = dA[q] * hu * s1;
                 dH[1][q] = dA[q] * sg;
                 const float pg = kwv * uW[0][q] + kmv * uM[0][q];
                 const float pu = kwv * uW[1][q] + kmv * uM[1][q];
                 dAh[q] = pg * hu * s1 + pu * sg;
-                hh[0][q] = pg * dA[q] * hu * s2 + pu * dA[q] * s1;
-                hh[1][q] = pg * dA[q] * s1;
-                kwp[q] += dH[0][q] * uW[0][q] + dH[1][q] * uW[1][q];
-                kmp[q] += dH[0][q] * uM[0][q] + dH[1][q] * uM[1][q];
+                hh[0][q] = pg * dA[q] * hu * s2 + pu * dA[q] * s1 + r2 * hu * s1;
+                hh[1][q] = pg * dA[q] * s1 + r2 * sg;
+                kwp[q] += dH[0][q] * uW[0][q] + dH[1][q] * uW[1][q] + Af[q] * rW[q];
+                kmp[q] += dH[0][q] * uM[0][q] + dH[1][q] * uM[1][q] + Af[q] * rM[q];
               }
             }
 #pragma unroll
-            for (int m = 0; m < NF; ++m) {
-              hh_at(m, tb, jj, lane) = hh[m];
-              D1[m][tb][jj] = d1v[m];
-            }
+            for (int m = 0; m < NF; ++m) hh_at(m, tb, jj, lane) = hh[m];
             if constexpr (DH_LDS) {
 #pragma unroll
               for (int q = 0; q < 4; ++q)
@@ -570,57 +570,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             if (c == 0) {
               kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sw;
               kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sm2;
-            }
-          }
-        }
-      }
-      {
-        E2TTT_LANE_IDS;
-#pragma unroll
-        for (int tb = 0; tb < NTB; ++tb) {
-          opaque_state<S>(Wb);
-          opaque_state<S>(Mb);
-          E2TTT_LANE_IDS;
-          float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-          for (int jj = 0; jj < NJB; ++jj) {
-            f32x4 rW = zero4(), rM = zero4();
-#pragma unroll
-            for (int p = 0; p < S::KS_D; ++p) {
-              auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
-              typename O::Frag bw, bm;
-#pragma unroll
-              for (int h = 0; h < S::NH; ++h) {
-                bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
-                bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
-              }
-              rW = O::mma(rW, fy, bw);
-              rM = O::mma(rM, fy, bm);
-            }
-            const f32x4 Af = quad_f32(Akq[tb][jj]);
-            f32x4 hv[NF];
-#pragma unroll
-            for (int m = 0; m < NF; ++m) hv[m] = hh_at(m, tb, jj, lane);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int t = 16 * tb + 4 * g + q;
-              const float r2 = skw[t] * rW[q] + skm[t] * rM[q];
-#pragma unroll
-              for (int m = 0; m < NF; ++m) hv[m][q] += r2 * D1[m][tb][jj][q];
-              kwp[q] += Af[q] * rW[q];
-              kmp[q] += Af[q] * rM[q];
-            }
-#pragma unroll
-            for (int m = 0; m < NF; ++m) hh_at(m, tb, jj, lane) = hv[m];
-            sched_fence();
-          }
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float sw = group16_sum(kwp[q]);
-            const float sm2 = group16_sum(kmp[q]);
-            if (c == 0) {
-              kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] += sw;
-              kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] += sm2;
             }
           }
         }

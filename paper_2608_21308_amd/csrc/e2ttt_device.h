@@ -111,29 +111,25 @@ __device__ __forceinline__ typename OpT<BF>::Frag lds_frag(const typename OpT<BF
 __device__ __forceinline__ float rcp_f(float x) { return __builtin_amdgcn_rcpf(x); }
 __device__ __forceinline__ float rsq_f(float x) { return __builtin_amdgcn_rsqf(x); }
 
-// Standard normal CDF Phi(x) and density phi(x) from the Chebyshev-fitted
-// complementary error function of Press et al., Numerical Recipes (2nd ed.,
-// section 6.2, "erfcc"): erfc(z) = t exp(-z^2 + P(t)), t = 1 / (1 + z / 2),
-// z >= 0, with fractional error below 1.2e-7 for every z.  Using erfc keeps
-// Phi accurate in relative terms in its lower tail, where 1 + erf cancels.
+// Standard normal CDF Phi(x) and density phi(x).  Phi(-|x|) = erfc(z) / 2 with
+// z = |x| / sqrt(2), and erfc from Abramowitz & Stegun, Handbook of
+// Mathematical Functions, eq. 7.1.26: erfc(z) = t (a1 + a2 t + ... + a5 t^4)
+// exp(-z^2), t = 1 / (1 + p z), z >= 0, absolute error at most 1.5e-7.  The
+// factor exp(-z^2) = exp(-x^2 / 2) is shared with phi, so the pair costs one
+// reciprocal and one exponential.
 struct NormalCdf {
   float cdf, pdf;
 };
 __device__ __forceinline__ NormalCdf normal_cdf(float x) {
   const float z = fabsf(x) * 0.70710678118654752f;
-  const float t = rcp_f(1.0f + 0.5f * z);
-  float p = 0.17087277f;
-  p = fmaf(p, t, -0.82215223f);
-  p = fmaf(p, t, 1.48851587f);
-  p = fmaf(p, t, -1.13520398f);
-  p = fmaf(p, t, 0.27886807f);
-  p = fmaf(p, t, -0.18628806f);
-  p = fmaf(p, t, 0.09678418f);
-  p = fmaf(p, t, 0.37409196f);
-  p = fmaf(p, t, 1.00002368f);
-  p = fmaf(p, t, -1.26551223f);
+  const float t = rcp_f(fmaf(0.3275911f, z, 1.0f));
+  float p = 1.061405429f;
+  p = fmaf(p, t, -1.453152027f);
+  p = fmaf(p, t, 1.421413741f);
+  p = fmaf(p, t, -0.284496736f);
+  p = fmaf(p, t, 0.254829592f);
   const float ez2 = __expf(-z * z);                 // exp(-x^2 / 2)
-  const float half_erfc = 0.5f * t * ez2 * __expf(p);  // Phi(-|x|)
+  const float half_erfc = 0.5f * t * p * ez2;       // Phi(-|x|)
   NormalCdf r;
   r.cdf = (x >= 0.0f) ? 1.0f - half_erfc : half_erfc;
   r.pdf = 0.39894228040143268f * ez2;
