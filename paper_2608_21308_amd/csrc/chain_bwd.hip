@@ -141,7 +141,7 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
       const int it = w + a * S::NW;
       if (it < L::NITEM) {
         const int tb = it / NI, ib0 = (it % NI) * S::IBB;
-#pragma unroll 2
+#pragma unroll
         for (int p = 0; p < L::JWD / S::KC; ++p) {
           auto af = lds_frag<S::BF>(ja, L::LDJ, 16 * tb + c, p * S::KC, g);
 #pragma unroll
@@ -149,7 +149,6 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
             auto bf = lds_frag<S::BF>(jw, L::LDJ, 16 * (ib0 + b) + c, p * S::KC, g);
             tmp.v[a][b] = O::mma(tmp.v[a][b], af, bf);
           }
-          sched_fence();
         }
       }
     }
@@ -380,8 +379,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
       {
       E2TTT_LANE_IDS;
-#pragma unroll 1
-      for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+#pragma unroll
+      for (int it_ = 0; it_ < (S::CM + 4 * NW - 1) / (4 * NW); ++it_) {
+        const int t0 = 4 * w + it_ * 4 * NW;
+        if (t0 < S::CM) {
         const int t = t0 + (lane >> 4);
         float z[EPL], e[EPL], dyv[EPL];
         float mez = 0.0f;
@@ -418,6 +419,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           dyt[i * S::LDC + t] = O::to_e(dyv[q]);
         }
         if (l16 == 0) row[2 * t + 1] = mez;
+              }
       }
       }
       __syncthreads();
@@ -644,8 +646,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
         using IOT = typename IoT<S::BF>::T;
         IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
-#pragma unroll 1
-        for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+#pragma unroll
+        for (int it_ = 0; it_ < (S::CM + 4 * NW - 1) / (4 * NW); ++it_) {
+          const int t0 = 4 * w + it_ * 4 * NW;
+          if (t0 < S::CM) {
           const int t = t0 + (lane >> 4);
           float dyhv[EPL], e[EPL], eh[EPL], yhv[EPL];
 #pragma unroll
@@ -702,6 +706,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             yht[i * S::LDC + t] = O::to_e(yhv[q]);
             if (t < len && t >= rlo && t < rlo + RPW) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
           }
+                  }
         }
       }
       __syncthreads();
@@ -806,8 +811,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           xqt[i * S::LDC + t] = xq[t * S::LDD + i];
         }
         // Yb_Q = LN backward of dO at the Q rows (dO itself when there is no LN)
-#pragma unroll 1
-        for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * NW) {
+#pragma unroll
+        for (int it_ = 0; it_ < (S::CM + 4 * NW - 1) / (4 * NW); ++it_) {
+          const int t0 = 4 * w + it_ * 4 * NW;
+          if (t0 < S::CM) {
           const int t = t0 + (lane >> 4);
           float dov[EPL], yb[EPL];
 #pragma unroll
@@ -835,6 +842,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             ybq[t * S::LDD + i] = O::to_e(yb[q]);
             ybqt[i * S::LDC + t] = O::to_e(yb[q]);
           }
+                  }
         }
         f32x4 D1q[NF][NTB][NJB];   // act'(H_Q) factors, as D1 above
         Q Aqq[NTB][NJB];

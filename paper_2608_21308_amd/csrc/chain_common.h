@@ -246,7 +246,7 @@ __device__ __forceinline__ void jgemm_to_lds(const typename S::E* A, const typen
     f32x4 acc[S::IBB];
 #pragma unroll
     for (int b = 0; b < S::IBB; ++b) acc[b] = zero4();
-#pragma unroll 2
+#pragma unroll
     for (int p = 0; p < S::KS_H; ++p) {
       auto af = lds_frag<S::BF>(A, S::LDH, 16 * tb + c, p * S::KC, g);
 #pragma unroll
@@ -254,7 +254,6 @@ __device__ __forceinline__ void jgemm_to_lds(const typename S::E* A, const typen
         auto bf = lds_frag<S::BF>(Wt, S::LDH, 16 * (ib0 + b) + c, p * S::KC, g);
         acc[b] = S::O::mma(acc[b], af, bf);
       }
-      sched_fence();
     }
 #pragma unroll
     for (int b = 0; b < S::IBB; ++b)

@@ -268,8 +268,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         const float* peer = (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) : nullptr;
-#pragma unroll 1
-        for (int t0 = 4 * w; t0 < S::CM; t0 += 4 * S::NW) {
+#pragma unroll
+        for (int it_ = 0; it_ < (S::CM + 4 * S::NW - 1) / (4 * S::NW); ++it_) {
+          const int t0 = 4 * w + it_ * 4 * S::NW;
+          if (t0 < S::CM) {
           const int t = t0 + (lane >> 4);
           float yv[EPL], e[EPL], z[EPL], dyv[EPL];
           float s1 = 0.0f, sig = 1.0f;
@@ -319,6 +321,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             sm.dytw[i * S::LDC + t] = O::to_e(kwt * dyv[q]);
             sm.dytm[i * S::LDC + t] = O::to_e(kmt * dyv[q]);
           }
+                  }
         }
       }
       __syncthreads();
@@ -389,7 +392,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
               W.t[1][jj][ib] = O::mma(W.t[1][jj][ib], kfw, bU);
               M.t[1][jj][ib] = O::mma(M.t[1][jj][ib], kfm, bU);
             }
-            sched_fence();
           }
       }
 
@@ -401,8 +403,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
         const float* peer =
             (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) + S::CM * D : nullptr;
-#pragma unroll 1
-        for (int t0 = rlo + 4 * w; t0 < rlo + RPW; t0 += 4 * S::NW) {
+#pragma unroll
+        for (int it_ = 0; it_ < (RPW + 4 * S::NW - 1) / (4 * S::NW); ++it_) {
+          const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
+          if (t0 < rlo + RPW) {
           const int t = t0 + (lane >> 4);
           float yv[EPL], f[EPL];
           float s1 = 0.0f, sig = 1.0f;
@@ -438,6 +442,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
               if (l16 == 0) a.rq[row0 + t] = sig;
             }
           }
+                  }
         }
       }
       __syncthreads();
