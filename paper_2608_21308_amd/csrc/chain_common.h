@@ -160,6 +160,30 @@ __device__ __forceinline__ typename S::O::Frag tile_frag(const f32x4* tiles, int
   return f;
 }
 
+// acc += af * (fragment of fp32 state tiles, as operand).  On the bf16 path
+// the state operand is split into bf16 high and low parts (x = hi + lo to
+// about 16 significant bits) and both are multiplied: one more MFMA and a few
+// conversions buy an operand as precise as the fp32 state for the products
+// whose rounding drives the drift of the chunk chain.
+template <class S>
+__device__ __forceinline__ f32x4 mma_state(f32x4 acc, const typename S::O::Frag& af,
+                                           const f32x4* tiles, int p, int stride) {
+  using O = typename S::O;
+  if constexpr (S::BF) {
+    typename O::Frag hi, lo;
+#pragma unroll
+    for (int h = 0; h < S::NH; ++h) {
+      const f32x4 v = tiles[(S::NH * p + h) * stride];
+      hi.h[h] = O::cvt(v);
+      lo.h[h] = O::cvt(v - quad_f32(hi.h[h]));
+    }
+    acc = O::mma(acc, af, hi);
+    return O::mma(acc, af, lo);
+  } else {
+    return O::mma(acc, af, tile_frag<S>(tiles, p, stride));
+  }
+}
+
 // Copy a CM x D token tile (rows < len, zero beyond) from global io memory to
 // LDS in 16-byte vectors (the io element type equals the LDS element type).
 template <class S>

@@ -31,8 +31,7 @@ struct FwdSmem {
   alignas(16) E xk[S::CM * S::LDD];
   alignas(16) E xq[S::CM * S::LDD];
   alignas(16) E xv[S::CM * S::LDD];
-  alignas(16) E kwt[S::D * S::LDC];   // K^W_t k_t[i], layout [i][t]
-  alignas(16) E kmt[S::D * S::LDC];   // K^M_t k_t[i]
+  alignas(16) E kt[S::D * S::LDC];    // K^T, layout [i][t]
   alignas(16) E alds[S::CM * S::LDH]; // activations A[t][j] (this workgroup's columns)
   alignas(16) E w2[S::D * S::LDH];    // second-layer weights W2[i][j] (bf16/fp32 copy of W_0)
   alignas(16) E dy[S::CM * S::LDD];   // dY[t][i]
@@ -40,8 +39,8 @@ struct FwdSmem {
   alignas(16) E dytm[S::D * S::LDC];  // K^M_t dY[t][i]
   alignas(16) float y[S::CM * S::D];  // Y_K (partial over this workgroup's columns)
   alignas(16) float yq[S::CM * S::D]; // Y_Q (partial)
-  float kw[S::CM];
-  float km[S::CM];
+  alignas(16) float kw[S::CM];
+  alignas(16) float km[S::CM];
   float carry[4];
   int word[2];
 };
@@ -166,15 +165,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll 1
       for (int idx = tid; idx < D * (S::CM / 4); idx += S::NT) {
         const int i = idx % D, t0 = 4 * (idx / D);
-        typename O::Q qw, qm;
+        typename O::Q qk;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float kx = O::from_e(sm.xk[(t0 + q4) * S::LDD + i]);
-          qw[q4] = O::to_e(sm.kw[t0 + q4] * kx);
-          qm[q4] = O::to_e(sm.km[t0 + q4] * kx);
-        }
-        *reinterpret_cast<typename O::Q*>(&sm.kwt[i * S::LDC + t0]) = qw;
-        *reinterpret_cast<typename O::Q*>(&sm.kmt[i * S::LDC + t0]) = qm;
+        for (int q4 = 0; q4 < 4; ++q4) qk[q4] = sm.xk[(t0 + q4) * S::LDD + i];
+        *reinterpret_cast<typename O::Q*>(&sm.kt[i * S::LDC + t0]) = qk;
       }
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb)
@@ -184,8 +178,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.xk, S::LDD, 16 * tb + c, p * S::KC, g);
-            acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
-            if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
+            acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
+            if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
           }
           f32x4 act, d1, d2;
 #pragma unroll
@@ -235,8 +229,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.xq, S::LDD, 16 * tb + c, p * S::KC, g);
-            acc = O::mma(acc, af, tile_frag<S>(&W.t[0][jj][0], p, 1));
-            if constexpr (S::FW == 1) accu = O::mma(accu, af, tile_frag<S>(&W.t[1][jj][0], p, 1));
+            acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
+            if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
           }
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
@@ -328,8 +322,13 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
       // ---------------------------------- dA = dY W2, first-layer deltas (a4)
       opaque_state<S>(W);
-      typename O::Q DH[NTB][NJB];                         // MLP dH / SwiGLU dHg
-      typename O::Q DU[NTB][(S::FW == 1) ? NJB : 1];      // SwiGLU dHu
+      // first-layer update operands K^W_t dH[t][j] and K^M_t dH[t][j] (the scalar
+      // kernels go on dH, so that the other operand is K^T, exact in bf16); for
+      // the MLP on the bf16 path they are split into bf16 high and low parts
+      constexpr bool SPLIT_UPD = S::BF && S::FW == 0;
+      constexpr int NU = (S::FW == 1) ? 2 : 1;            // first-layer matrices
+      typename O::Q DW[NU][NTB][NJB], DM[NU][NTB][NJB];
+      typename O::Q DWl[SPLIT_UPD ? NU : 1][NTB][NJB], DMl[SPLIT_UPD ? NU : 1][NTB][NJB];
       {
       E2TTT_LANE_IDS;
 #pragma unroll
@@ -340,16 +339,26 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.dy, S::LDD, 16 * tb + c, p * S::KC, g);
-            da = O::mma(da, af, tile_frag<S>(&W.t[SEC][jj][0], p, 1));
+            da = mma_state<S>(da, af, &W.t[SEC][jj][0], p, 1);
           }
-          f32x4 dh1, dh2;
+          f32x4 dh[NU];
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
-            dh1[rr] = da[rr] * H[tb][jj][rr];
-            if constexpr (S::FW == 1) dh2[rr] = da[rr] * Hu[tb][jj][rr];
+            dh[0][rr] = da[rr] * H[tb][jj][rr];
+            if constexpr (S::FW == 1) dh[1][rr] = da[rr] * Hu[tb][jj][rr];
           }
-          DH[tb][jj] = O::cvt(dh1);
-          if constexpr (S::FW == 1) DU[tb][jj] = O::cvt(dh2);
+          const f32x4 kwv = *reinterpret_cast<const f32x4*>(&sm.kw[16 * tb + 4 * g]);
+          const f32x4 kmv = *reinterpret_cast<const f32x4*>(&sm.km[16 * tb + 4 * g]);
+#pragma unroll
+          for (int m = 0; m < NU; ++m) {
+            const f32x4 vw = kwv * dh[m], vm = kmv * dh[m];
+            DW[m][tb][jj] = O::cvt(vw);
+            DM[m][tb][jj] = O::cvt(vm);
+            if constexpr (SPLIT_UPD) {
+              DWl[m][tb][jj] = O::cvt(vw - quad_f32(DW[m][tb][jj]));
+              DMl[m][tb][jj] = O::cvt(vm - quad_f32(DM[m][tb][jj]));
+            }
+          }
           sched_fence();
         }
       }
@@ -372,25 +381,34 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         for (int ib = 0; ib < NIB; ++ib)
 #pragma unroll
           for (int p = 0; p < S::KS_C; ++p) {
-            typename O::Frag bA, bH, bU;
+            typename O::Frag bA;
 #pragma unroll
-            for (int h = 0; h < S::NH; ++h) {
-              bA.h[h] = AK[S::NH * p + h][jj];
-              bH.h[h] = DH[S::NH * p + h][jj];
-              if constexpr (S::FW == 1) bU.h[h] = DU[S::NH * p + h][jj];
-            }
+            for (int h = 0; h < S::NH; ++h) bA.h[h] = AK[S::NH * p + h][jj];
             const int row = 16 * ib + c, k0 = p * S::KC;
             // second layer: sum_t K_t dY[t][i] A[t][j]
             W.t[SEC][jj][ib] = O::mma(W.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytw, S::LDC, row, k0, g), bA);
             M.t[SEC][jj][ib] = O::mma(M.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytm, S::LDC, row, k0, g), bA);
-            // first layer(s): sum_t K_t k[t][i] dH[t][j]
-            auto kfw = lds_frag<S::BF>(sm.kwt, S::LDC, row, k0, g);
-            auto kfm = lds_frag<S::BF>(sm.kmt, S::LDC, row, k0, g);
-            W.t[0][jj][ib] = O::mma(W.t[0][jj][ib], kfw, bH);
-            M.t[0][jj][ib] = O::mma(M.t[0][jj][ib], kfm, bH);
-            if constexpr (S::FW == 1) {
-              W.t[1][jj][ib] = O::mma(W.t[1][jj][ib], kfw, bU);
-              M.t[1][jj][ib] = O::mma(M.t[1][jj][ib], kfm, bU);
+            // first layer(s): sum_t k[t][i] (K_t dH[t][j])
+            auto kf = lds_frag<S::BF>(sm.kt, S::LDC, row, k0, g);
+#pragma unroll
+            for (int m = 0; m < NU; ++m) {
+              typename O::Frag bw, bm;
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) {
+                bw.h[h] = DW[m][S::NH * p + h][jj];
+                bm.h[h] = DM[m][S::NH * p + h][jj];
+              }
+              W.t[m][jj][ib] = O::mma(W.t[m][jj][ib], kf, bw);
+              M.t[m][jj][ib] = O::mma(M.t[m][jj][ib], kf, bm);
+              if constexpr (SPLIT_UPD) {
+#pragma unroll
+                for (int h = 0; h < S::NH; ++h) {
+                  bw.h[h] = DWl[m][S::NH * p + h][jj];
+                  bm.h[h] = DMl[m][S::NH * p + h][jj];
+                }
+                W.t[m][jj][ib] = O::mma(W.t[m][jj][ib], kf, bw);
+                M.t[m][jj][ib] = O::mma(M.t[m][jj][ib], kf, bm);
+              }
             }
           }
       }
