@@ -259,11 +259,13 @@ struct F32TileRegs {
 };
 
 // Y[t][i] = sum_j A[t][j] Wt[i][j]  (j-contraction, both operands in LDS),
-// written to y (fp32 [CM][D]).  Work is split into (token block, head block
-// pair) items over the waves.
+// written to y (fp32 [CM][D]) and, when given, in the same layout to `slot`
+// in global memory.  Work is split into (token block, head block pair) items
+// over the waves.
 template <class S>
 __device__ __forceinline__ void jgemm_to_lds(const typename S::E* A, const typename S::E* Wt,
-                                             float* y, int w, int g, int c) {
+                                             float* y, int w, int g, int c,
+                                             float* slot = nullptr) {
   constexpr int NI = S::NIB / S::IBB;
   for (int it = w; it < S::NTB * NI; it += S::NW) {
     const int tb = it / NI, ib0 = (it % NI) * S::IBB;
@@ -282,7 +284,11 @@ __device__ __forceinline__ void jgemm_to_lds(const typename S::E* A, const typen
 #pragma unroll
     for (int b = 0; b < S::IBB; ++b)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) y[(16 * tb + 4 * g + r) * S::D + 16 * (ib0 + b) + c] = acc[b][r];
+      for (int r = 0; r < 4; ++r) {
+        const int e = (16 * tb + 4 * g + r) * S::D + 16 * (ib0 + b) + c;
+        y[e] = acc[b][r];
+        if (slot) slot[e] = acc[b][r];
+      }
   }
 }
 

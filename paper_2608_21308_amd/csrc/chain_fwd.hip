@@ -26,13 +26,25 @@ namespace e2ttt {
 namespace {
 
 template <class S>
+struct FwdSmemBase {
+  using E = typename S::E;
+  static constexpr int BYTES =
+      (3 * S::CM * S::LDD + S::D * S::LDC + S::CM * S::LDH + S::D * S::LDH + S::CM * S::LDD +
+       2 * S::D * S::LDC) * (int)sizeof(E) + 2 * S::CM * S::D * 4 + 2 * S::CM * 4 + 64;
+  // a separate Q-side activation buffer when it fits in LDS
+  static constexpr bool Q2 = BYTES + S::CM * S::LDH * (int)sizeof(E) <= 160 * 1024;
+};
+
+template <class S>
 struct FwdSmem {
   using E = typename S::E;
+  static constexpr bool Q2 = FwdSmemBase<S>::Q2;
   alignas(16) E xk[S::CM * S::LDD];
   alignas(16) E xq[S::CM * S::LDD];
   alignas(16) E xv[S::CM * S::LDD];
   alignas(16) E kt[S::D * S::LDC];    // K^T, layout [i][t]
   alignas(16) E alds[S::CM * S::LDH]; // activations A[t][j] (this workgroup's columns)
+  alignas(16) E alds2[Q2 ? S::CM * S::LDH : 8]; // Q-side activations (else alds)
   alignas(16) E w2[S::D * S::LDH];    // second-layer weights W2[i][j] (bf16/fp32 copy of W_0)
   alignas(16) E dy[S::CM * S::LDD];   // dY[t][i]
   alignas(16) E dytw[S::D * S::LDC];  // K^W_t dY[t][i], layout [i][t]
@@ -49,14 +61,6 @@ struct FwdSmem {
 template <class S>
 __device__ __forceinline__ float* fwd_slot(float* xbuf, long p, int rank, int parity) {
   return xbuf + (((p * 2 + rank) * 2 + parity) * 2L) * S::CM * S::D;
-}
-
-template <class S>
-__device__ __forceinline__ void copy_to_slot(float* dst, const float* src, int tid) {
-  constexpr int NV = S::CM * S::D / 4;
-#pragma unroll 1
-  for (int v = tid; v < NV; v += S::NT)
-    reinterpret_cast<float4*>(dst)[v] = reinterpret_cast<const float4*>(src)[v];
 }
 
 template <class S>
@@ -86,8 +90,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   if constexpr (S::DHK > S::DHP) {
     E2TTT_LANE_IDS;
     constexpr int NZ = S::DHK - S::DHP;
-    for (int idx = tid; idx < S::CM * NZ; idx += S::NT)
+    for (int idx = tid; idx < S::CM * NZ; idx += S::NT) {
       sm.alds[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
+      if constexpr (FwdSmem<S>::Q2)
+        sm.alds2[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
+    }
     for (int idx = tid; idx < D * NZ; idx += S::NT)
       sm.w2[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
   }
@@ -208,14 +215,13 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
       {
         E2TTT_LANE_IDS;
-        jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c);   // Y_K (partial)
+        jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c,   // Y_K (partial)
+                        (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, rank, par) : nullptr);
       }
-      __syncthreads();
-      if constexpr (S::NS > 1) {
-        E2TTT_LANE_IDS;
-        copy_to_slot<S>(fwd_slot<S>(a.xbuf, px.p, rank, par), sm.y, tid);
-        px.post();                                        // seq0 + 1: Y_K
-      }
+      px.post();                                          // seq0 + 1: Y_K
+      // without a separate Q-side buffer, alds is rewritten below
+      if constexpr (!FwdSmem<S>::Q2 && S::NS == 1) __syncthreads();
+      typename S::E* const aq = FwdSmem<S>::Q2 ? sm.alds2 : sm.alds;
 
       // ------------------- Q-side first layer and Y_Q (a7), overlapping the swap
       {
@@ -237,7 +243,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             float act;
             if constexpr (S::FW == 0) act = gelu_f(acc[rr]);
             else act = silu_f(acc[rr]) * accu[rr];
-            sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act);
+            aq[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act);
           }
           sched_fence();
         }
@@ -245,15 +251,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       __syncthreads();
       {
         E2TTT_LANE_IDS;
-        jgemm_to_lds<S>(sm.alds, sm.w2, sm.yq, w, g, c);  // Y_Q (partial)
+        jgemm_to_lds<S>(aq, sm.w2, sm.yq, w, g, c,        // Y_Q (partial)
+                        (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D : nullptr);
       }
-      __syncthreads();
-      if constexpr (S::NS > 1) {
-        E2TTT_LANE_IDS;
-        copy_to_slot<S>(fwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D, sm.yq, tid);
-        px.post();                                        // seq0 + 2: Y_Q
-        px.wait_for(seq0 + 1, sm.word);                   // peer's Y_K
-      }
+      px.post();                                          // seq0 + 2: Y_Q
+      px.wait_for(seq0 + 1, sm.word);                     // peer's Y_K
 
       // ------------------------------- LN and activation gradients (a4)
       // Four token rows per wave step: lanes 16 r .. 16 r + 15 hold row t0 + r,
