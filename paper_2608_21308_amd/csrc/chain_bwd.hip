@@ -40,7 +40,7 @@ struct BwdLayout {
   static_assert(JWD % S::KC == 0, "half width must be a multiple of the K-step");
   static_assert(JWD % (16 * S::NJB) == 0, "a wave's hidden slice must lie in one half");
   static constexpr int TD = S::CM * S::LDD * (int)sizeof(E);   // [t][i]
-  static constexpr int DT = S::D * S::LDC * (int)sizeof(E);    // [i][t]
+  static constexpr int DT = S::D * S::LDC * (int)sizeof(E);    // [i][t] (it_idx)
   static constexpr int TDX = (TD > DT) ? TD : DT;
   static constexpr int TJ = S::CM * LDJ * (int)sizeof(E);      // [t][j] half
   static constexpr int IJ = S::D * LDJ * (int)sizeof(E);       // [i][j] half
@@ -416,7 +416,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           yk[t * D + i] = z[q];
           ek[t * D + i] = e[q];
           dyl[t * S::LDD + i] = O::to_e(dyv[q]);
-          dyt[i * S::LDC + t] = O::to_e(dyv[q]);
+          dyt[it_idx<S>(i, t)] = O::to_e(dyv[q]);
         }
         if (l16 == 0) row[2 * t + 1] = mez;
               }
@@ -703,7 +703,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             const int i = l16 * EPL + q;
             ek[t * D + i] = eh[q];
             yh[t * S::LDD + i] = O::to_e(yhv[q]);
-            yht[i * S::LDC + t] = O::to_e(yhv[q]);
+            yht[it_idx<S>(i, t)] = O::to_e(yhv[q]);
             if (t < len && t >= rlo && t < rlo + RPW) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
           }
                   }
@@ -719,7 +719,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll 1
         for (int idx = tid; idx < D * S::CM; idx += S::NT) {
           const int i = idx % D, t = idx / D;
-          xkt[i * S::LDC + t] = xk[t * S::LDD + i];
+          xkt[it_idx<S>(i, t)] = xk[t * S::LDD + i];
         }
         const auto& w2q = w0q[SEC];
 #pragma unroll
@@ -760,9 +760,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
                 ba.h[h] = Akq[S::NH * p + h][jj];
               }
               const int rowi = 16 * ib + c, k0 = p * S::KC;
-              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(dyt, S::LDC, rowi, k0, g), bd);
-              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(yht, S::LDC, rowi, k0, g), ba);
-              auto fk = lds_frag<S::BF>(xkt, S::LDC, rowi, k0, g);
+              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], it_frag<S>(dyt, rowi, k0, g), bd);
+              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], it_frag<S>(yht, rowi, k0, g), ba);
+              auto fk = it_frag<S>(xkt, rowi, k0, g);
 #pragma unroll
               for (int m = 0; m < NF; ++m) {
                 typename O::Frag bh;
@@ -808,7 +808,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll 1
         for (int idx = tid; idx < D * S::CM; idx += S::NT) {
           const int i = idx % D, t = idx / D;
-          xqt[i * S::LDC + t] = xq[t * S::LDD + i];
+          xqt[it_idx<S>(i, t)] = xq[t * S::LDD + i];
         }
         // Yb_Q = LN backward of dO at the Q rows (dO itself when there is no LN)
 #pragma unroll
@@ -840,7 +840,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) {
             const int i = l16 * EPL + q;
             ybq[t * S::LDD + i] = O::to_e(yb[q]);
-            ybqt[i * S::LDC + t] = O::to_e(yb[q]);
+            ybqt[it_idx<S>(i, t)] = O::to_e(yb[q]);
           }
                   }
         }
@@ -924,8 +924,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
               for (int h = 0; h < S::NH; ++h) ba.h[h] = Aqq[S::NH * p + h][jj];
               const int rowi = 16 * ib + c, k0 = p * S::KC;
-              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], lds_frag<S::BF>(ybqt, S::LDC, rowi, k0, g), ba);
-              auto fq = lds_frag<S::BF>(xqt, S::LDC, rowi, k0, g);
+              Wb.t[SEC][jj][ib] = O::mma(Wb.t[SEC][jj][ib], it_frag<S>(ybqt, rowi, k0, g), ba);
+              auto fq = it_frag<S>(xqt, rowi, k0, g);
 #pragma unroll
               for (int m = 0; m < NF; ++m) {
                 typename O::Frag bh;

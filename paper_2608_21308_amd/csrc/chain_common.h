@@ -184,6 +184,36 @@ __device__ __forceinline__ f32x4 mma_state(f32x4 acc, const typename S::O::Frag&
   }
 }
 
+// 16 bytes into a padded [t][i] row.  Rows of the bf16 path are only 8-byte
+// aligned (the row padding is 8 bytes), so the vector goes out as two 8-byte
+// stores there.
+template <class S>
+__device__ __forceinline__ void store_row16(typename S::E* dst, const uint4& x) {
+  if constexpr ((S::LDD * sizeof(typename S::E)) % 16 == 0) {
+    *reinterpret_cast<uint4*>(dst) = x;
+  } else {
+    reinterpret_cast<uint2*>(dst)[0] = make_uint2(x.x, x.y);
+    reinterpret_cast<uint2*>(dst)[1] = make_uint2(x.z, x.w);
+  }
+}
+
+// [i][t] operands (rows i = head index, columns t = token, the contraction
+// index of the state updates) keep each row's 4-element quads permuted:
+// element (i, t) sits at quad (t / 4) ^ ((i / 16) mod 4) of row i.  The row
+// phases write these arrays one element per lane with 16 lanes on rows 4
+// apart; unpermuted, those rows fall on 4 LDS banks (a 4-way conflict on every
+// such store), permuted on 16.  Fragment reads stay single paired loads: the
+// permutation only moves the lane's quad within its K-step.
+template <class S>
+__device__ __forceinline__ int it_idx(int i, int t) {
+  return i * S::LDC + ((((t >> 2) ^ (i >> 4)) & 3) | ((t >> 2) & ~3)) * 4 + (t & 3);
+}
+template <class S>
+__device__ __forceinline__ typename S::O::Frag it_frag(const typename S::E* base, int row, int k0,
+                                                       int g) {
+  return lds_frag<S::BF>(base, S::LDC, row, k0, g ^ ((row >> 4) & 3));
+}
+
 // Copy a CM x D token tile (rows < len, zero beyond) from global io memory to
 // LDS in 16-byte vectors (the io element type equals the LDS element type).
 template <class S>
@@ -199,7 +229,7 @@ __device__ __forceinline__ void stage_tile(typename S::E* dst, const void* src, 
     const int e = v * VE, t = e / S::D, i = e % S::D;
     uint4 x = make_uint4(0u, 0u, 0u, 0u);
     if (t < len) x = p[v];
-    *reinterpret_cast<uint4*>(dst + t * S::LDD + i) = x;
+    store_row16<S>(dst + t * S::LDD + i, x);
   }
 }
 
@@ -228,8 +258,7 @@ struct TileRegs {
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int e = (tid + k * S::NT) * VE;
-      if (e < S::CM * S::D)
-        *reinterpret_cast<uint4*>(dst + (e / S::D) * S::LDD + e % S::D) = v[k];
+      if (e < S::CM * S::D) store_row16<S>(dst + (e / S::D) * S::LDD + e % S::D, v[k]);
     }
   }
 };

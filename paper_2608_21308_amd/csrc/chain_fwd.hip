@@ -42,12 +42,12 @@ struct FwdSmem {
   alignas(16) E xk[S::CM * S::LDD];
   alignas(16) E xq[S::CM * S::LDD];
   alignas(16) E xv[S::CM * S::LDD];
-  alignas(16) E kt[S::D * S::LDC];    // K^T, layout [i][t]
+  alignas(16) E kt[S::D * S::LDC];    // K^T, layout [i][t] (it_idx)
   alignas(16) E alds[S::CM * S::LDH]; // activations A[t][j] (this workgroup's columns)
   alignas(16) E alds2[Q2 ? S::CM * S::LDH : 8]; // Q-side activations (else alds)
   alignas(16) E w2[S::D * S::LDH];    // second-layer weights W2[i][j] (bf16/fp32 copy of W_0)
   alignas(16) E dy[S::CM * S::LDD];   // dY[t][i]
-  alignas(16) E dytw[S::D * S::LDC];  // K^W_t dY[t][i], layout [i][t]
+  alignas(16) E dytw[S::D * S::LDC];  // K^W_t dY[t][i], layout [i][t] (it_idx)
   alignas(16) E dytm[S::D * S::LDC];  // K^M_t dY[t][i]
   alignas(16) float y[S::CM * S::D];  // Y_K (partial over this workgroup's columns)
   alignas(16) float yq[S::CM * S::D]; // Y_Q (partial)
@@ -175,7 +175,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         typename O::Q qk;
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) qk[q4] = sm.xk[(t0 + q4) * S::LDD + i];
-        *reinterpret_cast<typename O::Q*>(&sm.kt[i * S::LDC + t0]) = qk;
+        *reinterpret_cast<typename O::Q*>(&sm.kt[it_idx<S>(i, t0)]) = qk;
       }
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb)
@@ -314,8 +314,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) {
             const int i = l16 * EPL + q;
             sm.dy[t * S::LDD + i] = O::to_e(dyv[q]);
-            sm.dytw[i * S::LDC + t] = O::to_e(kwt * dyv[q]);
-            sm.dytm[i * S::LDC + t] = O::to_e(kmt * dyv[q]);
+            sm.dytw[it_idx<S>(i, t)] = O::to_e(kwt * dyv[q]);
+            sm.dytm[it_idx<S>(i, t)] = O::to_e(kmt * dyv[q]);
           }
                   }
         }
@@ -388,10 +388,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             for (int h = 0; h < S::NH; ++h) bA.h[h] = AK[S::NH * p + h][jj];
             const int row = 16 * ib + c, k0 = p * S::KC;
             // second layer: sum_t K_t dY[t][i] A[t][j]
-            W.t[SEC][jj][ib] = O::mma(W.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytw, S::LDC, row, k0, g), bA);
-            M.t[SEC][jj][ib] = O::mma(M.t[SEC][jj][ib], lds_frag<S::BF>(sm.dytm, S::LDC, row, k0, g), bA);
+            W.t[SEC][jj][ib] = O::mma(W.t[SEC][jj][ib], it_frag<S>(sm.dytw, row, k0, g), bA);
+            M.t[SEC][jj][ib] = O::mma(M.t[SEC][jj][ib], it_frag<S>(sm.dytm, row, k0, g), bA);
             // first layer(s): sum_t k[t][i] (K_t dH[t][j])
-            auto kf = lds_frag<S::BF>(sm.kt, S::LDC, row, k0, g);
+            auto kf = it_frag<S>(sm.kt, row, k0, g);
 #pragma unroll
             for (int m = 0; m < NU; ++m) {
               typename O::Frag bw, bm;

@@ -60,7 +60,11 @@ template <> struct OpT<true> {
   using Q = bf16x4;                 // four consecutive contraction indices
   static constexpr int KC = 32;     // contraction indices per K-step
   static constexpr int NH = 2;      // quads per fragment
-  static constexpr int PAD = 8;     // row padding of LDS operands (16 bytes)
+  // Row padding of LDS operands: 4 elements (8 bytes), so that row strides
+  // are 2 (mod 4) dwords.  Fragment reads (paired 8-byte loads, 16 lanes on
+  // 16 consecutive rows per LDS cycle) then touch 32 distinct banks; with a
+  // 16-byte pad (stride 0 mod 4) pairs of rows 8 apart share banks.
+  static constexpr int PAD = 4;
   struct Frag { Q h[2]; };
   static __device__ __forceinline__ Q cvt(f32x4 x) {
     return Q{(__bf16)x[0], (__bf16)x[1], (__bf16)x[2], (__bf16)x[3]};
