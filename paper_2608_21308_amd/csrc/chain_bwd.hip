@@ -122,16 +122,16 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
         if (WRITE_ACT || L::JH > 1) {
 #pragma unroll
           for (int tb = 0; tb < S::NTB; ++tb) {
-            const f32x4 v = act(tb, jj);
+            const auto v = as_quad<S>(act(tb, jj));
 #pragma unroll
-            for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = O::to_e(v[r]);
+            for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = v[r];
           }
         }
 #pragma unroll
         for (int ib = 0; ib < S::NIB; ++ib) {
-          const f32x4 v = wt(ib, jj);
+          const auto v = as_quad<S>(wt(ib, jj));
 #pragma unroll
-          for (int r = 0; r < 4; ++r) jw[(16 * ib + 4 * g + r) * L::LDJ + col] = O::to_e(v[r]);
+          for (int r = 0; r < 4; ++r) jw[(16 * ib + 4 * g + r) * L::LDJ + col] = v[r];
         }
       }
     }
@@ -588,15 +588,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       for (int m = 0; m < NF; ++m) {
         const int mq = DH_LDS ? 0 : m;
         jround<S, !DH_LDS>(dkacc, skw, ja, jw,
-                           [&](int tb, int jj) { return quad_f32(dHq[mq][tb][jj]); },
+                           [&](int tb, int jj) { return dHq[mq][tb][jj]; },
                            [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
         jround<S, false>(dkacc, skm, ja, jw,
-                         [&](int tb, int jj) { return quad_f32(dHq[mq][tb][jj]); },
+                         [&](int tb, int jj) { return dHq[mq][tb][jj]; },
                          [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
       }
-      jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+      jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
                 [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
-      jround<S, false>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return quad_f32(Akq[tb][jj]); },
+      jround<S, false>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
                        [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
       }
 
@@ -620,8 +620,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         const auto& w2q = w0q[SEC];
-        jround<S>(dyhacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(dAhq[tb][jj]); },
-                  [&](int ib, int jj) { return quad_f32(w2q[jj][ib]); }, w, g, c);
+        jround<S>(dyhacc, nullptr, ja, jw, [&](int tb, int jj) { return dAhq[tb][jj]; },
+                  [&](int ib, int jj) { return w2q[jj][ib]; }, w, g, c);
         jacc_store_f32<S>(dyhacc, dyh, [](int, int) { return 0.0f; }, w, g, c);
       }
       __syncthreads();
@@ -778,7 +778,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         for (int m = 0; m < NF; ++m) {
           const auto& w1q = w0q[m];
           jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return hh_at(m, tb, jj, lane); },
-                    [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
+                    [&](int ib, int jj) { return w1q[jj][ib]; }, w, g, c);
         }
         const float ksign = (resln && rank == 0) ? -1.0f : 0.0f;
         if constexpr (S::NS > 1) {
@@ -870,9 +870,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
                 if constexpr (!SW) {
-                  const NormalCdf n = normal_cdf(acc[0][q]);
-                  act[q] = acc[0][q] * n.cdf;
-                  D1q[0][tb][jj][q] = n.cdf + acc[0][q] * n.pdf;
+                  const Act2 ga = gelu2(acc[0][q]);
+                  act[q] = ga.f;
+                  D1q[0][tb][jj][q] = ga.d1;
                 } else {
                   const float hg = acc[0][q], hu = acc[1][q], sg = sigm_f(hg);
                   D1q[1][tb][jj][q] = hg * sg;
@@ -942,8 +942,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
         for (int m = 0; m < NF; ++m) {
           const auto& w1q = w0q[m];
-          jround<S>(dqacc, nullptr, ja, jw, [&](int tb, int jj) { return quad_f32(Hbq[m][tb][jj]); },
-                    [&](int ib, int jj) { return quad_f32(w1q[jj][ib]); }, w, g, c);
+          jround<S>(dqacc, nullptr, ja, jw, [&](int tb, int jj) { return Hbq[m][tb][jj]; },
+                    [&](int ib, int jj) { return w1q[jj][ib]; }, w, g, c);
         }
         const float qsign = (resln && rank == 0) ? 1.0f : 0.0f;
         if constexpr (S::NS > 1) {

@@ -148,6 +148,26 @@ template <class Q>
 __device__ __forceinline__ f32x4 quad_f32(const Q& q) {
   return f32x4{(float)q[0], (float)q[1], (float)q[2], (float)q[3]};
 }
+// bf16 quads widen by moving each half-word into the high half of a word: one
+// shift or mask per element, read straight from the packed pair.
+__device__ __forceinline__ f32x4 quad_f32(const bf16x4& q) {
+  typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+  const u32x2 u = __builtin_bit_cast(u32x2, q);
+  return f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+               __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+}
+
+// An operand quad from fp32 values (converted) or from a quad already in the
+// operand precision (passed through).
+template <class S>
+__device__ __forceinline__ typename S::O::Q as_quad(const f32x4& x) {
+  return S::O::cvt(x);
+}
+template <class S, class Q,
+          typename std::enable_if<!std::is_same<Q, f32x4>::value, int>::type = 0>
+__device__ __forceinline__ Q as_quad(const Q& q) {
+  return q;
+}
 
 // Operand fragment whose contraction index is the tile ROW of `tiles`
 // (tiles[k-block]) for K-step p.

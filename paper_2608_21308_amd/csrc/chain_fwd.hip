@@ -192,9 +192,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
             if constexpr (S::FW == 0) {
-              const NormalCdf n = normal_cdf(acc[rr]);
-              act[rr] = acc[rr] * n.cdf;
-              d1[rr] = n.cdf + acc[rr] * n.pdf;
+              const Act2 ga = gelu2(acc[rr]);
+              act[rr] = ga.f;
+              d1[rr] = ga.d1;
             } else {
               const float hg = acc[rr], hu = accu[rr], sg = sigm_f(hg);
               d2[rr] = hg * sg;                              // SiLU(Hg)

@@ -115,38 +115,48 @@ __device__ __forceinline__ typename OpT<BF>::Frag lds_frag(const typename OpT<BF
 __device__ __forceinline__ float rcp_f(float x) { return __builtin_amdgcn_rcpf(x); }
 __device__ __forceinline__ float rsq_f(float x) { return __builtin_amdgcn_rsqf(x); }
 
-// Standard normal CDF Phi(x) and density phi(x).  Phi(-|x|) = erfc(z) / 2 with
-// z = |x| / sqrt(2), and erfc from Abramowitz & Stegun, Handbook of
-// Mathematical Functions, eq. 7.1.26: erfc(z) = t (a1 + a2 t + ... + a5 t^4)
-// exp(-z^2), t = 1 / (1 + p z), z >= 0, absolute error at most 1.5e-7.  The
-// factor exp(-z^2) = exp(-x^2 / 2) is shared with phi, so the pair costs one
-// reciprocal and one exponential.
-struct NormalCdf {
-  float cdf, pdf;
+// GELU(x) = x Phi(x) with Phi the standard normal CDF, evaluated through
+// h = Phi(-|x|) = erfc(|x| / sqrt(2)) / 2 and e = exp(-x^2 / 2).  erfc comes
+// from Abramowitz & Stegun, Handbook of Mathematical Functions, eq. 7.1.26:
+// erfc(z) = t (a1 + a2 t + ... + a5 t^4) exp(-z^2), t = 1 / (1 + p z), z >= 0,
+// absolute error at most 1.5e-7.  Here p is pre-multiplied by 1/sqrt(2) and
+// the a_k by 1/2, so h = t poly(t) e.  One reciprocal and one exponential
+// serve GELU and both of its derivatives:
+//   GELU(x)   = max(x, 0) - |x| h
+//   GELU'(x)  = Phi(x) + x phi(x),   Phi(x) = 1 - h for x >= 0, h otherwise
+//   GELU''(x) = phi(x) (2 - x^2),    phi(x) = e / sqrt(2 pi).
+struct GeluParts {
+  float h, e, x2;
 };
-__device__ __forceinline__ NormalCdf normal_cdf(float x) {
-  const float z = fabsf(x) * 0.70710678118654752f;
-  const float t = rcp_f(fmaf(0.3275911f, z, 1.0f));
-  float p = 1.061405429f;
-  p = fmaf(p, t, -1.453152027f);
-  p = fmaf(p, t, 1.421413741f);
-  p = fmaf(p, t, -0.284496736f);
-  p = fmaf(p, t, 0.254829592f);
-  const float ez2 = __expf(-z * z);                 // exp(-x^2 / 2)
-  const float half_erfc = 0.5f * t * p * ez2;       // Phi(-|x|)
-  NormalCdf r;
-  r.cdf = (x >= 0.0f) ? 1.0f - half_erfc : half_erfc;
-  r.pdf = 0.39894228040143268f * ez2;
+__device__ __forceinline__ GeluParts gelu_parts(float x) {
+  GeluParts r;
+  r.x2 = x * x;
+  r.e = __builtin_amdgcn_exp2f(r.x2 * -0.7213475204444817f);   // 2^(-x^2 log2(e) / 2)
+  const float t = rcp_f(fmaf(fabsf(x), 0.23164189f, 1.0f));
+  float p = 0.5307027f;
+  p = fmaf(p, t, -0.72657603f);
+  p = fmaf(p, t, 0.7107069f);
+  p = fmaf(p, t, -0.14224836f);
+  p = fmaf(p, t, 0.1274148f);
+  r.h = (p * t) * r.e;
   return r;
 }
-// GELU (exact, x Phi(x)) and its first two derivatives.
-__device__ __forceinline__ float gelu_f(float x) { return x * normal_cdf(x).cdf; }
-__device__ __forceinline__ float gelu_d1(float x) {
-  const NormalCdf n = normal_cdf(x);
-  return n.cdf + x * n.pdf;
+__device__ __forceinline__ float gelu_from(float x, const GeluParts& g) {
+  return fmaf(-fabsf(x), g.h, fmaxf(x, 0.0f));
 }
-__device__ __forceinline__ float gelu_d2(float x) {
-  return 0.39894228040143268f * __expf(-0.5f * x * x) * (2.0f - x * x);
+__device__ __forceinline__ float gelu_f(float x) { return gelu_from(x, gelu_parts(x)); }
+// Phi(x) = 1/2 + sign(x) (1/2 - h), branch- and compare-free (a compare per
+// element would hold a scalar register pair per element in flight).
+__device__ __forceinline__ float gelu_cdf(float x, const GeluParts& g) {
+  return 0.5f + copysignf(0.5f - g.h, x);
+}
+// GELU and GELU'.
+struct Act2 {
+  float f, d1;
+};
+__device__ __forceinline__ Act2 gelu2(float x) {
+  const GeluParts g = gelu_parts(x);
+  return Act2{gelu_from(x, g), fmaf(x * 0.3989423f, g.e, gelu_cdf(x, g))};
 }
 __device__ __forceinline__ float sigm_f(float x) { return rcp_f(1.0f + __expf(-x)); }
 __device__ __forceinline__ float silu_f(float x) { return x * sigm_f(x); }
@@ -165,8 +175,9 @@ struct Act3 {
   float f, d1, d2;
 };
 __device__ __forceinline__ Act3 gelu3(float x) {
-  const NormalCdf n = normal_cdf(x);
-  return Act3{x * n.cdf, n.cdf + x * n.pdf, n.pdf * (2.0f - x * x)};
+  const GeluParts g = gelu_parts(x);
+  const float pdf = 0.3989423f * g.e;
+  return Act3{gelu_from(x, g), fmaf(x, pdf, gelu_cdf(x, g)), pdf * (2.0f - g.x2)};
 }
 __device__ __forceinline__ Act3 silu3(float x) {
   const float s = sigm_f(x);
