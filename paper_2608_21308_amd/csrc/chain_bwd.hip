@@ -626,6 +626,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
       __syncthreads();
       const float* dyh_peer = nullptr;
+      constexpr int P7IT = (S::CM + 4 * NW - 1) / (4 * NW);
+      float pdyh[S::NS > 1 ? P7IT : 1][EPL];
       if constexpr (S::NS > 1) {
         E2TTT_LANE_IDS;
         float* mine = bwd_slot<S>(a.xbuf, px.p, rank, par);
@@ -635,6 +637,13 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         px.post();                                  // seq0 + 1: dYh partial
         px.wait_for(seq0 + 1, sword);               // the peer's
         dyh_peer = bwd_slot<S>(a.xbuf, px.p, 1 - rank, par);
+        // the peer's rows of every P7 step, loaded before the global stores
+        // below (which would otherwise order each step's loads after them)
+#pragma unroll
+        for (int it_ = 0; it_ < P7IT; ++it_) {
+          const int t0 = 4 * w + it_ * 4 * NW;
+          if (t0 < S::CM) load_row_part<EPL>(pdyh[it_], dyh_peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+        }
         if (pend_r >= 0)
           flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
                         tid);
@@ -647,7 +656,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         using IOT = typename IoT<S::BF>::T;
         IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
 #pragma unroll
-        for (int it_ = 0; it_ < (S::CM + 4 * NW - 1) / (4 * NW); ++it_) {
+        for (int it_ = 0; it_ < P7IT; ++it_) {
           const int t0 = 4 * w + it_ * 4 * NW;
           if (t0 < S::CM) {
           const int t = t0 + (lane >> 4);
@@ -659,7 +668,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           }
           if constexpr (S::NS > 1) {
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) dyhv[q] += dyh_peer[t * D + l16 * EPL + q];
+            for (int q = 0; q < EPL; ++q) dyhv[q] += pdyh[it_][q];
           }
           if (resln) {
             float z[EPL], dyv[EPL], zh[EPL];

@@ -204,6 +204,69 @@ __device__ __forceinline__ f32x4 mma_state(f32x4 acc, const typename S::O::Frag&
   }
 }
 
+// bf16 high and low parts (x = hi + lo to about 16 significant bits) of
+// every state tile, formed once per chunk when the same state is an MFMA
+// operand several times; the high part is also the operand-precision copy
+// (checkpoint, LDS operand).
+template <class S>
+struct SplitTiles {
+  typename S::O::Q hi[S::NMAT][S::NJB][S::NIB];
+  typename S::O::Q lo[S::NMAT][S::NJB][S::NIB];
+};
+template <class S>
+__device__ __forceinline__ void split_state(SplitTiles<S>& sp, const StateTiles<S>& st) {
+#pragma unroll
+  for (int m = 0; m < S::NMAT; ++m)
+#pragma unroll
+    for (int jj = 0; jj < S::NJB; ++jj)
+#pragma unroll
+      for (int ib = 0; ib < S::NIB; ++ib) {
+        const f32x4 v = st.t[m][jj][ib];
+        sp.hi[m][jj][ib] = S::O::cvt(v);
+        sp.lo[m][jj][ib] = S::O::cvt(v - quad_f32(sp.hi[m][jj][ib]));
+      }
+}
+// acc += af * (hi + lo) for K-step p of the pre-split tiles of one (m, jj).
+template <class S>
+__device__ __forceinline__ f32x4 mma_split(f32x4 acc, const typename S::O::Frag& af,
+                                           const typename S::O::Q* hi,
+                                           const typename S::O::Q* lo, int p) {
+  typename S::O::Frag fh, fl;
+#pragma unroll
+  for (int h = 0; h < S::NH; ++h) {
+    fh.h[h] = hi[S::NH * p + h];
+    fl.h[h] = lo[S::NH * p + h];
+  }
+  acc = S::O::mma(acc, af, fh);
+  return S::O::mma(acc, af, fl);
+}
+// Checkpoint block from pre-converted quads (same layout as store_ckpt).
+template <class S>
+__device__ __forceinline__ void store_ckpt_q(const typename S::O::Q (&q)[S::NMAT][S::NJB][S::NIB],
+                                             void* dst, int w, int lane) {
+  using Q = typename S::O::Q;
+  Q* lp = reinterpret_cast<Q*>(dst) + opaque_lane(w * 64 + lane);
+#pragma unroll
+  for (int m = 0; m < S::NMAT; ++m)
+#pragma unroll
+    for (int jj = 0; jj < S::NJB; ++jj)
+#pragma unroll
+      for (int ib = 0; ib < S::NIB; ++ib)
+        lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64] = q[m][jj][ib];
+}
+
+// EPL consecutive fp32 values from global memory (one vector load when EPL = 4).
+template <int EPL>
+__device__ __forceinline__ void load_row_part(float (&dst)[EPL], const float* src) {
+  if constexpr (EPL == 4) {
+    const float4 v = *reinterpret_cast<const float4*>(src);
+    dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) dst[q] = src[q];
+  }
+}
+
 // 16 bytes into a padded [t][i] row.  Rows of the bf16 path are only 8-byte
 // aligned (the row padding is 8 bytes), so the vector goes out as two 8-byte
 // stores there.

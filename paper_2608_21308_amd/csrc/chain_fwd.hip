@@ -69,6 +69,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   using IO = IoT<S::BF>;
   constexpr int D = S::D, NJB = S::NJB, NTB = S::NTB, NIB = S::NIB, NMAT = S::NMAT;
   constexpr int SEC = NMAT - 1;  // index of the second-layer matrix
+  // MLP on the bf16 path: the bf16 high / low parts of W_0 are formed once per
+  // chunk (checkpoint, LDS copy of W2, and the K-side, Q-side and dA products
+  // share them); the wider SwiGLU state re-forms them per use instead
+  constexpr bool PRESPLIT = S::BF && S::FW == 0;
   constexpr int EPL = D / 16;    // head elements per lane in the row phases
   constexpr int RPW = S::CM / S::NS;   // output rows written by one rank
   __shared__ FwdSmem<S> sm;
@@ -118,6 +122,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
   for (long u = px.p; u < a.U; u += NP) {
     StateTiles<S> W, M;
+    SplitTiles<S> WS;   // bf16 hi / lo parts of W_0 (PRESPLIT)
     {
       E2TTT_LANE_IDS;
       load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
@@ -142,20 +147,23 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         sm.km[tid] = pkm;
       }
       if (tid < 3) sm.carry[tid] = pcar;
+      if constexpr (PRESPLIT) split_state<S>(WS, W);
       if (a.ckpt) {
         char* cb = static_cast<char*>(a.ckpt) + ((u * NC + r) * S::NS + rank) * 2 * a.ckpt_stride;
-        store_ckpt<S>(W, cb, w, lane);
+        if constexpr (PRESPLIT) store_ckpt_q<S>(WS.hi, cb, w, lane);
+        else store_ckpt<S>(W, cb, w, lane);
         store_ckpt<S>(M, cb + a.ckpt_stride, w, lane);
       }
       // second-layer weights of W_0 into LDS as the j-contraction operand
 #pragma unroll
       for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-        for (int ib = 0; ib < NIB; ++ib)
+        for (int ib = 0; ib < NIB; ++ib) {
+          const auto q = as_quad<S>(PRESPLIT ? WS.hi[SEC][jj][ib] : O::cvt(W.t[SEC][jj][ib]));
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr)
-            sm.w2[(16 * ib + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] =
-                O::to_e(W.t[SEC][jj][ib][rr]);
+            sm.w2[(16 * ib + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = q[rr];
+        }
       opaque_state<S>(W);
       opaque_state<S>(M);
       }
@@ -185,7 +193,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.xk, S::LDD, 16 * tb + c, p * S::KC, g);
-            acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
+            if constexpr (PRESPLIT) acc = mma_split<S>(acc, af, WS.hi[0][jj], WS.lo[0][jj], p);
+            else acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
             if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
           }
           f32x4 act, d1, d2;
@@ -235,7 +244,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.xq, S::LDD, 16 * tb + c, p * S::KC, g);
-            acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
+            if constexpr (PRESPLIT) acc = mma_split<S>(acc, af, WS.hi[0][jj], WS.lo[0][jj], p);
+            else acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
             if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
           }
 #pragma unroll
@@ -263,9 +273,25 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
       {
         E2TTT_LANE_IDS;
-        const float* peer = (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) : nullptr;
+        constexpr int NIT = (S::CM + 4 * S::NW - 1) / (4 * S::NW);
+        // this lane's row of the rows [rlo, rlo + RPW) kept for the backward;
+        // written after the loop, so that no global store sits between the
+        // peer loads and their use
+        float zsave[EPL], rsave = 0.0f;
+        int tsave = -1;
+        // the peer's rows of every step are loaded first: the global stores
+        // below would otherwise keep each step's loads behind the previous step
+        float pyv[S::NS > 1 ? NIT : 1][EPL];
+        if constexpr (S::NS > 1) {
+          const float* peer = fwd_slot<S>(a.xbuf, px.p, 1 - rank, par);
 #pragma unroll
-        for (int it_ = 0; it_ < (S::CM + 4 * S::NW - 1) / (4 * S::NW); ++it_) {
+          for (int it_ = 0; it_ < NIT; ++it_) {
+            const int t0 = 4 * w + it_ * 4 * S::NW;
+            if (t0 < S::CM) load_row_part<EPL>(pyv[it_], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+          }
+        }
+#pragma unroll
+        for (int it_ = 0; it_ < NIT; ++it_) {
           const int t0 = 4 * w + it_ * 4 * S::NW;
           if (t0 < S::CM) {
           const int t = t0 + (lane >> 4);
@@ -275,7 +301,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) yv[q] = sm.y[t * D + l16 * EPL + q];
           if constexpr (S::NS > 1) {
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) yv[q] += peer[t * D + l16 * EPL + q];
+            for (int q = 0; q < EPL; ++q) yv[q] += pyv[it_][q];
           }
 #pragma unroll
           for (int q = 0; q < EPL; ++q) s1 += yv[q];
@@ -304,10 +330,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
               dyv[q] = O::from_e(sm.xv[t * S::LDD + l16 * EPL + q]) - yv[q];
             }
           }
-          if (a.zk && t >= rlo && t < rlo + RPW && t < len) {
+          if (t >= rlo && t < rlo + RPW && t < len) {   // saved after the loop
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) a.zk[(row0 + t) * D + l16 * EPL + q] = z[q];
-            if (l16 == 0) a.rk[row0 + t] = sig;
+            for (int q = 0; q < EPL; ++q) zsave[q] = z[q];
+            rsave = sig;
+            tsave = t;
           }
           const float kwt = sm.kw[t], kmt = sm.km[t];
 #pragma unroll
@@ -318,6 +345,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             sm.dytm[it_idx<S>(i, t)] = O::to_e(kmt * dyv[q]);
           }
                   }
+        }
+        if (a.zk && tsave >= 0) {
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) a.zk[(row0 + tsave) * D + l16 * EPL + q] = zsave[q];
+          if (l16 == 0) a.rk[row0 + tsave] = rsave;
         }
       }
       __syncthreads();
@@ -341,7 +373,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.dy, S::LDD, 16 * tb + c, p * S::KC, g);
-            da = mma_state<S>(da, af, &W.t[SEC][jj][0], p, 1);
+            if constexpr (PRESPLIT) da = mma_split<S>(da, af, WS.hi[SEC][jj], WS.lo[SEC][jj], p);
+            else da = mma_state<S>(da, af, &W.t[SEC][jj][0], p, 1);
           }
           f32x4 dh[NU];
 #pragma unroll
