@@ -258,14 +258,29 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           sched_fence();
         }
       }
-      __syncthreads();
+      // The peer's Y_K was posted before its Q-side; waiting here (a barrier,
+      // which also completes the Q-side activations) lets the loads of its
+      // rows for every LN step run under the Y_Q contraction.
+      constexpr int NIT = (S::CM + 4 * S::NW - 1) / (4 * S::NW);
+      float pyv[S::NS > 1 ? NIT : 1][EPL];
+      if constexpr (S::NS > 1) {
+        px.wait_for(seq0 + 1, sm.word);                   // peer's Y_K
+        E2TTT_LANE_IDS;
+        const float* peer = fwd_slot<S>(a.xbuf, px.p, 1 - rank, par);
+#pragma unroll
+        for (int it_ = 0; it_ < NIT; ++it_) {
+          const int t0 = 4 * w + it_ * 4 * S::NW;
+          if (t0 < S::CM) load_row_part<EPL>(pyv[it_], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+        }
+      } else {
+        __syncthreads();
+      }
       {
         E2TTT_LANE_IDS;
         jgemm_to_lds<S>(aq, sm.w2, sm.yq, w, g, c,        // Y_Q (partial)
                         (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D : nullptr);
       }
       px.post();                                          // seq0 + 2: Y_Q
-      px.wait_for(seq0 + 1, sm.word);                     // peer's Y_K
 
       // ------------------------------- LN and activation gradients (a4)
       // Four token rows per wave step: lanes 16 r .. 16 r + 15 hold row t0 + r,
@@ -273,23 +288,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
       {
         E2TTT_LANE_IDS;
-        constexpr int NIT = (S::CM + 4 * S::NW - 1) / (4 * S::NW);
-        // this lane's row of the rows [rlo, rlo + RPW) kept for the backward;
-        // written after the loop, so that no global store sits between the
-        // peer loads and their use
-        float zsave[EPL], rsave = 0.0f;
-        int tsave = -1;
-        // the peer's rows of every step are loaded first: the global stores
-        // below would otherwise keep each step's loads behind the previous step
-        float pyv[S::NS > 1 ? NIT : 1][EPL];
-        if constexpr (S::NS > 1) {
-          const float* peer = fwd_slot<S>(a.xbuf, px.p, 1 - rank, par);
-#pragma unroll
-          for (int it_ = 0; it_ < NIT; ++it_) {
-            const int t0 = 4 * w + it_ * 4 * S::NW;
-            if (t0 < S::CM) load_row_part<EPL>(pyv[it_], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
-          }
-        }
+        // this lane's rows of the rows [rlo, rlo + RPW), kept for the backward,
+        // are written after the loop, so that no global store sits between
+        // the peer's rows and their use
+        float zsave[NIT][EPL], rsave[NIT];
+        bool keep[NIT];
 #pragma unroll
         for (int it_ = 0; it_ < NIT; ++it_) {
           const int t0 = 4 * w + it_ * 4 * S::NW;
@@ -330,12 +333,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
               dyv[q] = O::from_e(sm.xv[t * S::LDD + l16 * EPL + q]) - yv[q];
             }
           }
-          if (t >= rlo && t < rlo + RPW && t < len) {   // saved after the loop
+          keep[it_] = t >= rlo && t < rlo + RPW && t < len;
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) zsave[q] = z[q];
-            rsave = sig;
-            tsave = t;
-          }
+          for (int q = 0; q < EPL; ++q) zsave[it_][q] = z[q];
+          rsave[it_] = sig;
           const float kwt = sm.kw[t], kmt = sm.km[t];
 #pragma unroll
           for (int q = 0; q < EPL; ++q) {
@@ -346,13 +347,35 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           }
                   }
         }
-        if (a.zk && tsave >= 0) {
+        if (a.zk) {
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) a.zk[(row0 + tsave) * D + l16 * EPL + q] = zsave[q];
-          if (l16 == 0) a.rk[row0 + tsave] = rsave;
+          for (int it_ = 0; it_ < NIT; ++it_) {
+            const int t = 4 * w + it_ * 4 * S::NW + (lane >> 4);
+            if (t < S::CM && keep[it_]) {
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) a.zk[(row0 + t) * D + l16 * EPL + q] = zsave[it_][q];
+              if (l16 == 0) a.rk[row0 + t] = rsave[it_];
+            }
+          }
         }
       }
-      __syncthreads();
+      // The peer's Y_Q was posted before its LN phase: wait for it here (the
+      // barrier that ends the LN phase) and load its rows of the outputs, so
+      // that they arrive under dA and the state update.
+      constexpr int NITO = (RPW + 4 * S::NW - 1) / (4 * S::NW);
+      float pyq[S::NS > 1 ? NITO : 1][EPL];
+      if constexpr (S::NS > 1) {
+        px.wait_for(seq0 + 2, sm.word);                   // peer's Y_Q
+        E2TTT_LANE_IDS;
+        const float* peer = fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) + S::CM * D;
+#pragma unroll
+        for (int it_ = 0; it_ < NITO; ++it_) {
+          const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
+          if (t0 < rlo + RPW) load_row_part<EPL>(pyq[it_], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+        }
+      } else {
+        __syncthreads();
+      }
 
       // ---------------------------------- dA = dY W2, first-layer deltas (a4)
       opaque_state<S>(W);
@@ -449,15 +472,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       }
 
       // ------------------------------------------------- outputs (a7)
-      if constexpr (S::NS > 1) px.wait_for(seq0 + 2, sm.word);   // peer's Y_Q
       {
         E2TTT_LANE_IDS;
         using IOT = typename IO::T;
         IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
-        const float* peer =
-            (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) + S::CM * D : nullptr;
 #pragma unroll
-        for (int it_ = 0; it_ < (RPW + 4 * S::NW - 1) / (4 * S::NW); ++it_) {
+        for (int it_ = 0; it_ < NITO; ++it_) {
           const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
           if (t0 < rlo + RPW) {
           const int t = t0 + (lane >> 4);
@@ -467,7 +487,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) yv[q] = sm.yq[t * D + l16 * EPL + q];
           if constexpr (S::NS > 1) {
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) yv[q] += peer[t * D + l16 * EPL + q];
+            for (int q = 0; q < EPL; ++q) yv[q] += pyq[it_][q];
           }
 #pragma unroll
           for (int q = 0; q < EPL; ++q) s1 += yv[q];

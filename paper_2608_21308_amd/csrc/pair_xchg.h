@@ -122,10 +122,11 @@ template <> struct PairX<2> {
   __device__ unsigned seq_now() const { return seq; }
 
   // Wait until the peer has posted at least `target`.  All threads call; the
-  // caller has passed a workgroup barrier since the previous call.
+  // caller has passed a workgroup barrier since the previous call.  The call
+  // is always a workgroup barrier (also once the pair is dead).
   __device__ void wait_for(unsigned target, int* s_word) {
-    if (dead) return;
-    if (threadIdx.x == 0) {
+    const bool was_dead = dead;   // uniform over the workgroup
+    if (threadIdx.x == 0 && !was_dead) {
       const long long t0 = __builtin_amdgcn_s_memrealtime();
       unsigned f;
       int ok = 1;
@@ -137,6 +138,7 @@ template <> struct PairX<2> {
       s_word[0] = ok;
     }
     __syncthreads();
+    if (was_dead) return;
     if (s_word[0] == 0) dead = true;
     if (same_xcc) asm volatile("buffer_inv sc0" ::: "memory");
     else __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
