@@ -57,7 +57,12 @@ struct BwdLayout {
   static constexpr int DYT = A16(RR + R1);       // dY^T [i][t]          | out branch: Yb_Q^T
   static constexpr int YH = A16(DYT + DT);       // Yh [t][i]            | out branch: Yb_Q
   static constexpr int YHT = A16(YH + TD);       // Yh^T [i][t]          | out branch: Q^T
-  static constexpr int ROW = A16(YHT + DT);      // per token: 1/sigma, mean(e Z)
+  static constexpr int ROW = A16(YHT + DT);       // per token: 1/sigma, mean(e Z)
+  // Until P7 writes Yh, the Yh / Yh^T regions are free: a second j-round
+  // weight buffer there lets two j-rounds over the same activations share
+  // one pass (jround2)
+  static constexpr int JW2 = YH;
+  static constexpr bool J2 = (JH == 1) && (ROW - YH >= IJ);
   static constexpr int KB = A16(ROW + S::CM * 8);          // dK^W, dK^M partials [2][NW][CM]
   static constexpr int CB = A16(KB + 2 * S::NW * S::CM * 4);  // carry adjoint partials [NW][4]
   static constexpr int SC = A16(CB + S::NW * 16);          // kw[CM], km[CM], carry[4]
@@ -165,6 +170,89 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
         for (int r = 0; r < 4; ++r) {
           const float s = rowscale ? rowscale[16 * tb + 4 * g + r] : 1.0f;
           out.v[a][b][r] += s * tmp.v[a][b][r];
+        }
+    }
+  }
+}
+
+// Two j-rounds over the same activations in one pass (single hidden half):
+// out[t][i] += rs1[t] sum_j Act[t][j] Wt1[i][j] + rs2[t] sum_j Act[t][j] Wt2[i][j].
+// jw2 is a second weight buffer; WRITE_ACT as for jround.
+template <class S, bool WRITE_ACT, class FA, class FW1, class FW2>
+__device__ __forceinline__ void jround2(JAcc<S>& out, const float* rs1, const float* rs2,
+                                        typename S::E* ja, typename S::E* jw, typename S::E* jw2,
+                                        FA act, FW1 wt1, FW2 wt2, int w, int g, int c) {
+  using L = BwdLayout<S>;
+  using O = typename S::O;
+  static_assert(L::JH == 1, "jround2 needs a single hidden half");
+  constexpr int NI = S::NIB / S::IBB;
+  JAcc<S> t1, t2;
+  t1.zero();
+  t2.zero();
+  // padding columns beyond the hidden width read as zero
+  constexpr int NZ = L::JWD - S::DHP;
+  if constexpr (NZ > 0) {
+#pragma unroll 1
+    for (int idx = threadIdx.x; idx < (S::CM + 2 * S::D) * NZ; idx += S::NT) {
+      const int rw = idx / NZ, col = S::DHP + idx % NZ;
+      if (rw < S::CM) ja[rw * L::LDJ + col] = O::to_e(0.0f);
+      else if (rw < S::CM + S::D) jw[(rw - S::CM) * L::LDJ + col] = O::to_e(0.0f);
+      else jw2[(rw - S::CM - S::D) * L::LDJ + col] = O::to_e(0.0f);
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < S::NJB; ++jj) {
+    const int col = 16 * (w * S::NJB + jj) + c;
+    if constexpr (WRITE_ACT) {
+#pragma unroll
+      for (int tb = 0; tb < S::NTB; ++tb) {
+        const auto v = as_quad<S>(act(tb, jj));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = v[r];
+      }
+    }
+#pragma unroll
+    for (int ib = 0; ib < S::NIB; ++ib) {
+      const auto v1 = as_quad<S>(wt1(ib, jj));
+      const auto v2 = as_quad<S>(wt2(ib, jj));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        jw[(16 * ib + 4 * g + r) * L::LDJ + col] = v1[r];
+        jw2[(16 * ib + 4 * g + r) * L::LDJ + col] = v2[r];
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < L::JIT; ++a) {
+    const int it = w + a * S::NW;
+    if (it < L::NITEM) {
+      const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll
+      for (int p = 0; p < L::JWD / S::KC; ++p) {
+        auto af = lds_frag<S::BF>(ja, L::LDJ, 16 * tb + c, p * S::KC, g);
+#pragma unroll
+        for (int b = 0; b < S::IBB; ++b) {
+          auto b1 = lds_frag<S::BF>(jw, L::LDJ, 16 * (ib0 + b) + c, p * S::KC, g);
+          auto b2 = lds_frag<S::BF>(jw2, L::LDJ, 16 * (ib0 + b) + c, p * S::KC, g);
+          t1.v[a][b] = O::mma(t1.v[a][b], af, b1);
+          t2.v[a][b] = O::mma(t2.v[a][b], af, b2);
+        }
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < L::JIT; ++a) {
+    const int it = w + a * S::NW;
+    if (it < L::NITEM) {
+      const int tb = it / NI;
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * tb + 4 * g + r;
+          out.v[a][b][r] += rs1[t] * t1.v[a][b][r] + rs2[t] * t2.v[a][b][r];
         }
     }
   }
@@ -584,20 +672,34 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       {
       E2TTT_LANE_IDS;
       // (with a single j-round half the two rounds of a pair share the act buffer)
+      E* const jw2 = reinterpret_cast<E*>(smem + L::JW2);
 #pragma unroll
       for (int m = 0; m < NF; ++m) {
         const int mq = DH_LDS ? 0 : m;
-        jround<S, !DH_LDS>(dkacc, skw, ja, jw,
+        if constexpr (L::J2) {
+          jround2<S, !DH_LDS>(dkacc, skw, skm, ja, jw, jw2,
+                              [&](int tb, int jj) { return dHq[mq][tb][jj]; },
+                              [&](int ib, int jj) { return Wb.t[m][jj][ib]; },
+                              [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+        } else {
+          jround<S, !DH_LDS>(dkacc, skw, ja, jw,
+                             [&](int tb, int jj) { return dHq[mq][tb][jj]; },
+                             [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
+          jround<S, false>(dkacc, skm, ja, jw,
                            [&](int tb, int jj) { return dHq[mq][tb][jj]; },
-                           [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
-        jround<S, false>(dkacc, skm, ja, jw,
-                         [&](int tb, int jj) { return dHq[mq][tb][jj]; },
-                         [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+                           [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+        }
       }
-      jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
-                [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
-      jround<S, false>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
-                       [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+      if constexpr (L::J2) {
+        jround2<S, true>(dyhacc, skw, skm, ja, jw, jw2, [&](int tb, int jj) { return Akq[tb][jj]; },
+                         [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; },
+                         [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+      } else {
+        jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
+                  [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
+        jround<S, false>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
+                         [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+      }
       }
 
       // ------------------------------------ P5: adjoint state transition
