@@ -652,15 +652,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             Akq[tb][jj] = O::cvt(Af);
             sched_fence();
           }
-          // per-wave row partials of dK^W, dK^M for this token block
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float sw = group16_sum(kwp[q]);
-            const float sm2 = group16_sum(kmp[q]);
-            if (c == 0) {
-              kb[(0 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sw;
-              kb[(1 * NW + w) * S::CM + 16 * tb + 4 * g + q] = sm2;
-            }
+          // per-wave row partials of dK^W, dK^M for this token block: after the
+          // reduce-scatter, lane c (even) holds the row sum of dK^W (c < 8) or
+          // dK^M (c >= 8) for row 4 g + (c / 2) mod 4
+          {
+            const float vals[8] = {kwp[0], kwp[1], kwp[2], kwp[3], kmp[0], kmp[1], kmp[2], kmp[3]};
+            const float sred = row16_reduce_scatter8(vals, c);
+            if ((c & 1) == 0)
+              kb[(((c >> 3) & 1) * NW + w) * S::CM + 16 * tb + 4 * g + ((c >> 1) & 3)] = sred;
           }
         }
       }

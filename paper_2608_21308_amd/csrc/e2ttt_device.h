@@ -199,6 +199,29 @@ __device__ __forceinline__ float group16_sum(float v) {
   v += dpp_f<0x140>(v);   // row_mirror
   return v;
 }
+// Reduce-scatter of eight values over the 16 lanes of a DPP row: with l16 the
+// lane's index in its row and b3 b2 b1 b0 its bits, the lane returns the row
+// sum of v[4 b3 + 2 b2 + b1].  Each step pairs lanes that differ in one bit
+// (row_mirror: bit 3, row_half_mirror: bit 2, quad perms: bits 1 and 0); a
+// lane keeps the half of its values its bit selects and adds the partner's
+// copy of that half: 22 VALU operations instead of the 32 of eight group16_sum.
+__device__ __forceinline__ float row16_reduce_scatter8(const float (&v)[8], int l16) {
+  const bool b3 = (l16 & 8) != 0, b2 = (l16 & 4) != 0, b1 = (l16 & 2) != 0;
+  float u[4], h[2];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float keep = b3 ? v[4 + k] : v[k], send = b3 ? v[k] : v[4 + k];
+    u[k] = keep + dpp_f<0x140>(send);   // row_mirror
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float keep = b2 ? u[2 + k] : u[k], send = b2 ? u[k] : u[2 + k];
+    h[k] = keep + dpp_f<0x141>(send);   // row_half_mirror
+  }
+  const float keep = b1 ? h[1] : h[0], send = b1 ? h[0] : h[1];
+  const float x = keep + dpp_f<0x4E>(send);   // quad_perm [2,3,0,1]
+  return x + dpp_f<0xB1>(x);                  // quad_perm [1,0,3,2]
+}
 // Sum over all 64 lanes, returned to every lane (all lanes must be active).
 __device__ __forceinline__ float wave_sum(float v) {
   const int b = __float_as_int(group16_sum(v));
