@@ -100,9 +100,10 @@ size_t e2ttt_param_count(const e2ttt_desc* desc);
 /* Bytes of `workspace` that e2ttt_chunk_forward needs.  With
  * save_for_backward != 0 the workspace also keeps what the backward reuses
  * (per-token scalar kernels, chunk-start checkpoints of W and M in the
- * operand precision, and the LayerNorm outputs and inverse deviations of the
- * key and query passes), and the same buffer, untouched, must then be passed
- * to e2ttt_chunk_backward.  Returns 0 for a bad descriptor. */
+ * operand precision, the LayerNorm outputs and inverse deviations of the key
+ * and query passes, and for the GELU MLP the query-side activations and GELU
+ * derivatives), and the same buffer, untouched, must then be passed to
+ * e2ttt_chunk_backward.  Returns 0 for a bad descriptor. */
 size_t e2ttt_workspace_bytes(const e2ttt_desc* desc, int save_for_backward);
 
 /* Bytes of `scratch` that e2ttt_chunk_backward needs (0 for a bad descriptor). */

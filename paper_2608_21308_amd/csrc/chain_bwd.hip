@@ -909,6 +909,28 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         E* ybq = yh;                                     // Yb_Q [t][i]
         E* ybqt = dyt;                                   // Yb_Q^T [i][t]
         E* xqt = yht;                                    // Q^T [i][t]
+        f32x4 D1q[NF][NTB][NJB];   // act'(H_Q) factors, as D1 above
+        Q Aqq[NTB][NJB];
+        if constexpr (!SW) {
+          // A_Q and GELU'(H_Q) as the forward formed them (its query side at
+          // W_0), loaded now so that they arrive under the staging and the
+          // Yb_Q row phase below
+          constexpr int NQ = NTB * NJB * NW * 64;
+          const char* qb = static_cast<const char*>(a.qsave) + ((u * NC + r) * S::NS + rank) * a.qs_stride;
+          const Q* qa = reinterpret_cast<const Q*>(qb);
+#pragma unroll
+          for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj) {
+              const int qi = ((tb * NJB + jj) * NW + w) * 64 + lane;
+              Aqq[tb][jj] = qa[qi];
+              if constexpr (S::BF)
+                D1q[0][tb][jj] = __builtin_convertvector(
+                    reinterpret_cast<const f16x4*>(qb + NQ * sizeof(Q))[qi], f32x4);
+              else
+                D1q[0][tb][jj] = reinterpret_cast<const f32x4*>(qb + NQ * sizeof(Q))[qi];
+            }
+        }
         pQ.store(xq, tid);
         pD.store(xdo, tid);
         pZq.store(yk, tid);                             // Z_Q (or Y_Q)
@@ -954,9 +976,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           }
                   }
         }
-        f32x4 D1q[NF][NTB][NJB];   // act'(H_Q) factors, as D1 above
-        Q Aqq[NTB][NJB];
-        {
+        if constexpr (SW) {   // the SwiGLU query side is recomputed from W_0
           const auto& w1q = w0q;
 #pragma unroll
           for (int tb = 0; tb < NTB; ++tb)
@@ -979,16 +999,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               f32x4 act;
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                if constexpr (!SW) {
-                  const Act2 ga = gelu2(acc[0][q]);
-                  act[q] = ga.f;
-                  D1q[0][tb][jj][q] = ga.d1;
-                } else {
-                  const float hg = acc[0][q], hu = acc[1][q], sg = sigm_f(hg);
-                  D1q[1][tb][jj][q] = hg * sg;
-                  D1q[0][tb][jj][q] = hu * sg * (1.0f + hg * (1.0f - sg));
-                  act[q] = hg * sg * hu;
-                }
+                const float hg = acc[0][q], hu = acc[1][q], sg = sigm_f(hg);
+                D1q[1][tb][jj][q] = hg * sg;
+                D1q[0][tb][jj][q] = hu * sg * (1.0f + hg * (1.0f - sg));
+                act[q] = hg * sg * hu;
               }
               Aqq[tb][jj] = O::cvt(act);
               sched_fence();

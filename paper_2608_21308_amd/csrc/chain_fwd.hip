@@ -233,6 +233,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       typename S::E* const aq = FwdSmem<S>::Q2 ? sm.alds2 : sm.alds;
 
       // ------------------- Q-side first layer and Y_Q (a7), overlapping the swap
+      // (MLP, saving for the backward: A_Q and GELU'(H_Q) of every tile)
+      typename O::Q qsa[S::FW == 0 ? NTB : 1][NJB];
+      f32x4 qsd[S::FW == 0 ? NTB : 1][NJB];
       {
       E2TTT_LANE_IDS;
       opaque_state<S>(W);
@@ -248,12 +251,28 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             else acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
             if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
           }
+          f32x4 act, d1;
+          if (S::FW == 0 && a.qsave) {   // GELU and GELU', saved for the backward
 #pragma unroll
-          for (int rr = 0; rr < 4; ++rr) {
-            float act;
-            if constexpr (S::FW == 0) act = gelu_f(acc[rr]);
-            else act = silu_f(acc[rr]) * accu[rr];
-            aq[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act);
+            for (int rr = 0; rr < 4; ++rr) {
+              const Act2 ga = gelu2(acc[rr]);
+              act[rr] = ga.f;
+              d1[rr] = ga.d1;
+            }
+          } else {
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+              if constexpr (S::FW == 0) act[rr] = gelu_f(acc[rr]);
+              else act[rr] = silu_f(acc[rr]) * accu[rr];
+            }
+          }
+          const auto aquad = O::cvt(act);
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+            aq[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = aquad[rr];
+          if constexpr (S::FW == 0) {   // stored after the Y_Q post below
+            qsa[tb][jj] = aquad;
+            qsd[tb][jj] = d1;
           }
           sched_fence();
         }
@@ -281,6 +300,25 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
                         (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D : nullptr);
       }
       px.post();                                          // seq0 + 2: Y_Q
+      // the saved query side goes out after the post, so that the post's wait
+      // for this chunk's stores does not include it
+      if (S::FW == 0 && a.qsave) {
+        E2TTT_LANE_IDS;
+        constexpr int NQ = S::NTB * S::NJB * S::NW * 64;   // quads per block
+        char* qb = static_cast<char*>(a.qsave) + ((u * NC + r) * S::NS + rank) * a.qs_stride;
+#pragma unroll
+        for (int tb = 0; tb < (S::FW == 0 ? NTB : 0); ++tb)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            const int qi = ((tb * NJB + jj) * S::NW + w) * 64 + lane;
+            reinterpret_cast<typename O::Q*>(qb)[qi] = qsa[tb][jj];
+            if constexpr (S::BF)   // fp16: 2^-11 relative, below the bf16 rounding of Hb_Q
+              reinterpret_cast<f16x4*>(qb + NQ * sizeof(typename O::Q))[qi] =
+                  __builtin_convertvector(qsd[tb][jj], f16x4);
+            else
+              reinterpret_cast<f32x4*>(qb + NQ * sizeof(typename O::Q))[qi] = qsd[tb][jj];
+          }
+      }
 
       // ------------------------------- LN and activation gradients (a4)
       // Four token rows per wave step: lanes 16 r .. 16 r + 15 hold row t0 + r,
@@ -582,6 +620,13 @@ int chain_fwd_blocks_per_cu(const ChainConfig& cfg) {
 long chain_ckpt_bytes(const ChainConfig& cfg) {
   const long nmat = (cfg.fw == 0) ? 2 : 3;
   return nmat * 16L * cfg.nw * cfg.njb * cfg.d * (cfg.bf ? 2 : 4);
+}
+
+long chain_qside_bytes(const ChainConfig& cfg) {
+  if (cfg.fw != 0) return 0;
+  // one operand quad (A_Q) and one GELU'(H_Q) quad per lane and tile: bf16 and
+  // fp16 on the bf16 path, fp32 and fp32 on the fp32 path
+  return (long)cfg.ntb * cfg.njb * cfg.nw * 64 * (cfg.bf ? 8 + 8 : 16 + 16);
 }
 
 }  // namespace e2ttt
