@@ -29,8 +29,8 @@ struct Plan {
   size_t off_kw = 0, off_km = 0, off_carry = 0, off_sync = 0, off_xbuf = 0, ws_bytes = 0;
   size_t off_ckpt = 0, off_zk = 0, off_rk = 0, off_zq = 0, off_rq = 0, ws_bytes_save = 0;
   long ckpt_stride = 0;
-  size_t off_qs = 0;
-  long qs_stride = 0;
+  size_t off_as = 0;
+  long as_stride = 0;
   // backward scratch
   size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, off_bsync = 0, off_bxbuf = 0;
   size_t scratch_bytes = 0;
@@ -97,9 +97,9 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_rk = pl.off_zk + align_up(tokd);
   pl.off_zq = pl.off_rk + align_up(tok);
   pl.off_rq = pl.off_zq + align_up(tokd);
-  pl.qs_stride = chain_qside_bytes(pl.cfg);
-  pl.off_qs = pl.off_rq + align_up(tok);
-  pl.ws_bytes_save = pl.off_qs + align_up((size_t)U * pl.NC * ns * pl.qs_stride);
+  pl.as_stride = chain_saved_act_bytes(pl.cfg);
+  pl.off_as = pl.off_rq + align_up(tok);
+  pl.ws_bytes_save = pl.off_as + align_up((size_t)U * pl.NC * ns * pl.as_stride);
   pl.off_kwb = 0;
   pl.off_kmb = align_up(ns * tok);
   pl.off_carryb = pl.off_kmb + align_up(ns * tok);
@@ -255,8 +255,8 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   a.ckpt = save_for_backward ? at<char>(workspace, pl.off_ckpt) : nullptr;
   a.ckpt_stride = pl.ckpt_stride;
   if (save_for_backward) {
-    a.qsave = pl.qs_stride ? at<char>(workspace, pl.off_qs) : nullptr;
-    a.qs_stride = pl.qs_stride;
+    a.asave = pl.as_stride ? at<char>(workspace, pl.off_as) : nullptr;
+    a.as_stride = pl.as_stride;
     a.zk = at<float>(workspace, pl.off_zk);
     a.rk = at<float>(workspace, pl.off_rk);
     a.zq = at<float>(workspace, pl.off_zq);
@@ -302,8 +302,8 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   a.carry = at<float>(workspace, pl.off_carry);
   a.ckpt = const_cast<char*>(at<char>(workspace, pl.off_ckpt));
   a.ckpt_stride = pl.ckpt_stride;
-  a.qsave = pl.qs_stride ? const_cast<char*>(at<char>(workspace, pl.off_qs)) : nullptr;
-  a.qs_stride = pl.qs_stride;
+  a.asave = pl.as_stride ? const_cast<char*>(at<char>(workspace, pl.off_as)) : nullptr;
+  a.as_stride = pl.as_stride;
   a.zk = const_cast<float*>(at<float>(workspace, pl.off_zk));
   a.rk = const_cast<float*>(at<float>(workspace, pl.off_rk));
   a.zq = const_cast<float*>(at<float>(workspace, pl.off_zq));

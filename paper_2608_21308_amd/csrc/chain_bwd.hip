@@ -915,20 +915,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           // A_Q and GELU'(H_Q) as the forward formed them (its query side at
           // W_0), loaded now so that they arrive under the staging and the
           // Yb_Q row phase below
-          constexpr int NQ = NTB * NJB * NW * 64;
-          const char* qb = static_cast<const char*>(a.qsave) + ((u * NC + r) * S::NS + rank) * a.qs_stride;
-          const Q* qa = reinterpret_cast<const Q*>(qb);
+          const SavedAct<S> sv(static_cast<char*>(a.asave) + ((u * NC + r) * S::NS + rank) * a.as_stride);
 #pragma unroll
           for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
             for (int jj = 0; jj < NJB; ++jj) {
-              const int qi = ((tb * NJB + jj) * NW + w) * 64 + lane;
-              Aqq[tb][jj] = qa[qi];
-              if constexpr (S::BF)
-                D1q[0][tb][jj] = __builtin_convertvector(
-                    reinterpret_cast<const f16x4*>(qb + NQ * sizeof(Q))[qi], f32x4);
-              else
-                D1q[0][tb][jj] = reinterpret_cast<const f32x4*>(qb + NQ * sizeof(Q))[qi];
+              const int qi = SavedAct<S>::idx(tb, jj, w, lane);
+              Aqq[tb][jj] = sv.aq()[qi];
+              D1q[0][tb][jj] = DerivQ<S::BF>::unpack(sv.d1q()[qi]);
             }
         }
         pQ.store(xq, tid);

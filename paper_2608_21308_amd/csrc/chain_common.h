@@ -267,6 +267,36 @@ __device__ __forceinline__ void load_row_part(float (&dst)[EPL], const float* sr
   }
 }
 
+// Saved activation derivatives: fp16 quads on the bf16 path (2^-11 relative,
+// below the bf16 rounding of the MFMA operands they scale), fp32 on the fp32 path.
+template <bool BF> struct DerivQ {
+  using T = f16x4;
+  static __device__ __forceinline__ T pack(f32x4 v) { return __builtin_convertvector(v, f16x4); }
+  static __device__ __forceinline__ f32x4 unpack(T v) { return __builtin_convertvector(v, f32x4); }
+};
+template <> struct DerivQ<false> {
+  using T = f32x4;
+  static __device__ __forceinline__ T pack(f32x4 v) { return v; }
+  static __device__ __forceinline__ f32x4 unpack(T v) { return v; }
+};
+
+// Layout of one saved-activation block (one unit's workgroup, one chunk; GELU
+// MLP): two sections of NQ entries in register order, entry
+// ((tb NJB + jj) NW + w) 64 + lane: A_Q (operand quads), then GELU'(H_Q).
+template <class S>
+struct SavedAct {
+  using Q = typename S::O::Q;
+  using DQ = typename DerivQ<S::BF>::T;
+  static constexpr int NQ = S::NTB * S::NJB * S::NW * 64;
+  char* base;
+  __device__ SavedAct(void* block) : base(static_cast<char*>(block)) {}
+  static __device__ __forceinline__ int idx(int tb, int jj, int w, int lane) {
+    return ((tb * S::NJB + jj) * S::NW + w) * 64 + lane;
+  }
+  __device__ Q* aq() const { return reinterpret_cast<Q*>(base); }
+  __device__ DQ* d1q() const { return reinterpret_cast<DQ*>(base + (long)NQ * sizeof(Q)); }
+};
+
 // 16 bytes into a padded [t][i] row.  Rows of the bf16 path are only 8-byte
 // aligned (the row padding is 8 bytes), so the vector goes out as two 8-byte
 // stores there.

@@ -252,7 +252,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
           }
           f32x4 act, d1;
-          if (S::FW == 0 && a.qsave) {   // GELU and GELU', saved for the backward
+          if (S::FW == 0 && a.asave) {   // GELU and GELU', saved for the backward
 #pragma unroll
             for (int rr = 0; rr < 4; ++rr) {
               const Act2 ga = gelu2(acc[rr]);
@@ -302,21 +302,16 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       px.post();                                          // seq0 + 2: Y_Q
       // the saved query side goes out after the post, so that the post's wait
       // for this chunk's stores does not include it
-      if (S::FW == 0 && a.qsave) {
+      if (S::FW == 0 && a.asave) {
         E2TTT_LANE_IDS;
-        constexpr int NQ = S::NTB * S::NJB * S::NW * 64;   // quads per block
-        char* qb = static_cast<char*>(a.qsave) + ((u * NC + r) * S::NS + rank) * a.qs_stride;
+        const SavedAct<S> sv(static_cast<char*>(a.asave) + ((u * NC + r) * S::NS + rank) * a.as_stride);
 #pragma unroll
         for (int tb = 0; tb < (S::FW == 0 ? NTB : 0); ++tb)
 #pragma unroll
           for (int jj = 0; jj < NJB; ++jj) {
-            const int qi = ((tb * NJB + jj) * S::NW + w) * 64 + lane;
-            reinterpret_cast<typename O::Q*>(qb)[qi] = qsa[tb][jj];
-            if constexpr (S::BF)   // fp16: 2^-11 relative, below the bf16 rounding of Hb_Q
-              reinterpret_cast<f16x4*>(qb + NQ * sizeof(typename O::Q))[qi] =
-                  __builtin_convertvector(qsd[tb][jj], f16x4);
-            else
-              reinterpret_cast<f32x4*>(qb + NQ * sizeof(typename O::Q))[qi] = qsd[tb][jj];
+            const int qi = SavedAct<S>::idx(tb, jj, w, lane);
+            sv.aq()[qi] = qsa[tb][jj];
+            sv.d1q()[qi] = DerivQ<S::BF>::pack(qsd[tb][jj]);
           }
       }
 
@@ -622,11 +617,11 @@ long chain_ckpt_bytes(const ChainConfig& cfg) {
   return nmat * 16L * cfg.nw * cfg.njb * cfg.d * (cfg.bf ? 2 : 4);
 }
 
-long chain_qside_bytes(const ChainConfig& cfg) {
+long chain_saved_act_bytes(const ChainConfig& cfg) {
   if (cfg.fw != 0) return 0;
-  // one operand quad (A_Q) and one GELU'(H_Q) quad per lane and tile: bf16 and
-  // fp16 on the bf16 path, fp32 and fp32 on the fp32 path
-  return (long)cfg.ntb * cfg.njb * cfg.nw * 64 * (cfg.bf ? 8 + 8 : 16 + 16);
+  // SavedAct: an operand quad (A_Q) and a derivative quad per lane and tile,
+  // 8 bytes each on the bf16 path (bf16, fp16), 16 on the fp32 path
+  return (long)cfg.ntb * cfg.njb * cfg.nw * 64 * (cfg.bf ? 2 * 8 : 2 * 16);
 }
 
 }  // namespace e2ttt

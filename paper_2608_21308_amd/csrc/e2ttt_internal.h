@@ -68,10 +68,11 @@ struct ChainArgs {
   // nullable in the forward
   void* ckpt;
   long ckpt_stride;     // bytes per (unit, chunk, rank, W-or-M) block
-  // query-side activations A_Q and act'(H_Q) of every chunk (GELU MLP), saved by
-  // the forward for the backward's output branch (nullable in the forward)
-  void* qsave;
-  long qs_stride;       // bytes per (unit, chunk, rank) block
+  // query-side activations A_Q and GELU'(H_Q) of every chunk (GELU MLP), saved
+  // by the forward for the backward's output branch (nullable in the forward;
+  // layout: SavedAct in chain_common.h)
+  void* asave;
+  long as_stride;       // bytes per (unit, chunk, rank) block
   // LN outputs saved by the forward for the backward (nullable in the forward):
   // Z = LN(Y) (Y itself without the residual LN) [U][T][d], 1/sigma [U][T]
   float* zk;
@@ -110,9 +111,9 @@ hipError_t launch_zero_words(unsigned* p, long n, hipStream_t stream);
 long chain_max_pairs(const ChainConfig& cfg, bool backward);
 // Bytes of one checkpoint block (W or M of one unit's workgroup at one chunk start).
 long chain_ckpt_bytes(const ChainConfig& cfg);
-// Bytes of one saved query-side block (one unit's workgroup, one chunk); 0 when
-// the backward recomputes the query side instead (SwiGLU).
-long chain_qside_bytes(const ChainConfig& cfg);
+// Bytes of one saved-activation block (one unit's workgroup, one chunk); 0 when
+// the backward recomputes the activations instead (SwiGLU).
+long chain_saved_act_bytes(const ChainConfig& cfg);
 // Floats of one rank's exchange slot set (both parities).
 long chain_xchg_floats(const ChainConfig& cfg, bool backward);
 
