@@ -163,6 +163,43 @@ e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const 
                                 const float* gamma, float* kw, float* km, float* carry,
                                 void* stream);
 
+/*
+ * Gate parameterization of Sec. 4 ("Input-Dependent Dynamics", eqs. (12)-(14)):
+ * per token, from the outputs l_eta, l_beta, l_alpha of the three linear heads,
+ *   eta   = eta_base * sigmoid(l_eta)                       (12)
+ *   beta  = sigmoid(l_beta)^(1 / tau)                       (13)
+ *   alpha = alpha_base * sigmoid(l_alpha),  gamma = 1 - eta * alpha   (14)
+ * (the paper trains with eta_base = 0.01, tau = 32, alpha_base = 0.1, App. B.1).
+ * The outputs are the gate arrays e2ttt_chunk_forward takes, and the backward
+ * maps the gate gradients e2ttt_chunk_backward returns to the logits.
+ *   n                       number of tokens (B H T); 0 is a no-op
+ *   l_eta, l_beta, l_alpha  [n] f32 device arrays; l_alpha NULL means no decay
+ *                           gate (gamma = 1): gamma, d_gamma and d_l_alpha must
+ *                           then be NULL too
+ *   eta, beta, gamma        [n] f32 outputs
+ * Errors: a required pointer NULL (or one of the alpha-side pointers given
+ * without l_alpha) -> E2TTT_ERR_NULL_ARG; n < 0, tau <= 0 or a negative or
+ * non-finite base -> E2TTT_ERR_BAD_SHAPE.  Caller-owned buffers, no workspace.
+ */
+typedef struct {
+  float eta_base;    /* >= 0 */
+  float alpha_base;  /* >= 0 */
+  float tau;         /* > 0 */
+} e2ttt_gate_params;
+
+e2ttt_status e2ttt_gates_forward(const e2ttt_gate_params* params, int64_t n, const float* l_eta,
+                                 const float* l_beta, const float* l_alpha, float* eta,
+                                 float* beta, float* gamma, void* stream);
+
+/* Backward of e2ttt_gates_forward: given d_eta, d_beta, d_gamma [n] f32 (for
+ * example from e2ttt_chunk_backward), the gradients d_l_eta, d_l_beta,
+ * d_l_alpha [n] f32 of the logits.  Same pointer rules as the forward. */
+e2ttt_status e2ttt_gates_backward(const e2ttt_gate_params* params, int64_t n,
+                                  const float* l_eta, const float* l_beta, const float* l_alpha,
+                                  const float* d_eta, const float* d_beta, const float* d_gamma,
+                                  float* d_l_eta, float* d_l_beta, float* d_l_alpha,
+                                  void* stream);
+
 /* Static description of a status code. */
 const char* e2ttt_status_str(e2ttt_status status);
 

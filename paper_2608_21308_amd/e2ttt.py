@@ -28,7 +28,7 @@ STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
 # Every entry point the header declares (checked by the CPU test-suite).
 EXPORTS = ("e2ttt_param_count", "e2ttt_workspace_bytes", "e2ttt_backward_scratch_bytes",
            "e2ttt_chunk_forward", "e2ttt_chunk_backward", "e2ttt_chunk_coeffs",
-           "e2ttt_status_str")
+           "e2ttt_gates_forward", "e2ttt_gates_backward", "e2ttt_status_str")
 
 
 class E2TTTError(RuntimeError):
@@ -42,6 +42,15 @@ class Desc(ctypes.Structure):
                 ("d", ctypes.c_int32), ("dh", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("fw", ctypes.c_int32), ("io", ctypes.c_int32), ("flags", ctypes.c_uint32),
                 ("ln_eps", ctypes.c_float)]
+
+
+class GateParams(ctypes.Structure):
+    """e2ttt_gate_params (the paper's defaults, App. B.1)."""
+    _fields_ = [("eta_base", ctypes.c_float), ("alpha_base", ctypes.c_float),
+                ("tau", ctypes.c_float)]
+
+    def __init__(self, eta_base=0.01, alpha_base=0.1, tau=32.0):
+        super().__init__(eta_base, alpha_base, tau)
 
 
 _lib = None
@@ -70,6 +79,11 @@ def load():
     lib.e2ttt_chunk_backward.restype = i
     lib.e2ttt_chunk_coeffs.argtypes = [dp] + [vp] * 7
     lib.e2ttt_chunk_coeffs.restype = i
+    gp = ctypes.POINTER(GateParams)
+    lib.e2ttt_gates_forward.argtypes = [gp, ctypes.c_int64] + [vp] * 7
+    lib.e2ttt_gates_forward.restype = i
+    lib.e2ttt_gates_backward.argtypes = [gp, ctypes.c_int64] + [vp] * 10
+    lib.e2ttt_gates_backward.restype = i
     lib.e2ttt_status_str.argtypes = [i]
     lib.e2ttt_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -194,6 +208,43 @@ def chunk_coeffs(cfg: Config, eta, beta, gamma):
                                 _ptr(km), _ptr(carry), _stream())
     _check(st, "e2ttt_chunk_coeffs")
     return kw, km, carry
+
+
+def _check_gate_tensors(*ts):
+    n = ts[0].numel()
+    for t in ts:
+        if t is None:
+            continue
+        if t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != n:
+            raise ValueError("gate arrays must be contiguous float32 tensors of one size")
+
+
+def gates_forward(params: GateParams, l_eta, l_beta, l_alpha=None):
+    """Gate parameterization, eqs. (12)-(14): (eta, beta, gamma) from the logits
+    (gamma None when l_alpha is None)."""
+    _check_gate_tensors(l_eta, l_beta, l_alpha)
+    lib = load()
+    eta = torch.empty_like(l_eta)
+    beta = torch.empty_like(l_beta)
+    gamma = None if l_alpha is None else torch.empty_like(l_alpha)
+    st = lib.e2ttt_gates_forward(ctypes.byref(params), l_eta.numel(), _ptr(l_eta), _ptr(l_beta),
+                                 _ptr(l_alpha), _ptr(eta), _ptr(beta), _ptr(gamma), _stream())
+    _check(st, "e2ttt_gates_forward")
+    return eta, beta, gamma
+
+
+def gates_backward(params: GateParams, l_eta, l_beta, l_alpha, d_eta, d_beta, d_gamma):
+    """Gradients of the logits from the gate gradients: (d_l_eta, d_l_beta, d_l_alpha)."""
+    _check_gate_tensors(l_eta, l_beta, l_alpha, d_eta, d_beta, d_gamma)
+    lib = load()
+    g_eta = torch.empty_like(l_eta)
+    g_beta = torch.empty_like(l_beta)
+    g_alpha = None if l_alpha is None else torch.empty_like(l_alpha)
+    st = lib.e2ttt_gates_backward(ctypes.byref(params), l_eta.numel(), _ptr(l_eta), _ptr(l_beta),
+                                  _ptr(l_alpha), _ptr(d_eta), _ptr(d_beta), _ptr(d_gamma),
+                                  _ptr(g_eta), _ptr(g_beta), _ptr(g_alpha), _stream())
+    _check(st, "e2ttt_gates_backward")
+    return g_eta, g_beta, g_alpha
 
 
 class E2TTTFunction(torch.autograd.Function):

@@ -125,3 +125,33 @@ def test_split_workspace_sizes(lib):
     # checkpoints of W and M (bf16, both ranks) plus Z and 1/sigma of both passes
     assert ws_save - ws >= U * NC * 2 * 2 * 64 * 256 * 2 + 2 * (tok * 64 + tok)
     assert sc >= 2 * (2 * tok + U * NC * 3 * 4) + 128 * 2 * 2 * 3 * 64 * 64 * 4
+
+
+def test_gate_argument_errors(lib):
+    """e2ttt_gates_forward / _backward validate everything before launching."""
+    p = e2ttt.GateParams()
+    f = ctypes.c_void_p(16)   # never dereferenced
+    fwd, bwd = lib.e2ttt_gates_forward, lib.e2ttt_gates_backward
+    assert fwd(None, 8, f, f, f, f, f, f, None) == 1
+    assert fwd(ctypes.byref(p), -1, f, f, f, f, f, f, None) == 2
+    assert fwd(ctypes.byref(p), 0, None, None, None, None, None, None, None) == 0   # no-op
+    for i in range(4):                               # l_eta, l_beta, eta, beta
+        a = [f, f, f, f, f, f]
+        a[[0, 1, 3, 4][i]] = None
+        assert fwd(ctypes.byref(p), 8, *a, None) == 1, i
+    assert fwd(ctypes.byref(p), 8, f, f, None, f, f, f, None) == 1       # gamma without l_alpha
+    assert fwd(ctypes.byref(p), 8, f, f, f, f, f, None, None) == 1       # l_alpha without gamma
+    for bad in (e2ttt.GateParams(tau=0.0), e2ttt.GateParams(eta_base=-1.0),
+                e2ttt.GateParams(alpha_base=float("nan")), e2ttt.GateParams(tau=float("inf"))):
+        assert fwd(ctypes.byref(bad), 8, f, f, f, f, f, f, None) == 2
+    b = [f] * 9
+    assert bwd(None, 8, *b, None) == 1
+    assert bwd(ctypes.byref(p), -3, *b, None) == 2
+    for i in (0, 1, 3, 4, 6, 7):                     # l_eta l_beta d_eta d_beta d_l_eta d_l_beta
+        a = list(b)
+        a[i] = None
+        assert bwd(ctypes.byref(p), 8, *a, None) == 1, i
+    for i in (2, 5, 8):                              # the alpha side is all or nothing
+        a = list(b)
+        a[i] = None
+        assert bwd(ctypes.byref(p), 8, *a, None) == 1, i
