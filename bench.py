@@ -67,6 +67,103 @@ def cpu_baseline(w, seconds_hint: float = 20.0) -> dict:
                       "scaled by %d/%d" % (n_units, w.B * w.H, w.T, dt, w.B * w.H, n_units)}
 
 
+def time_gates(e2ttt, w, dev, reps: int = 50) -> dict:
+    """Gate parameterization kernels (eqs. (12)-(14)) over the same B*H*T
+    tokens, outside the timed step: average time of back-to-back calls through
+    the C ABI from HIP events, and the HBM rate of their algorithmic bytes (forward reads 3 logits and writes
+    3 gates per token, backward reads 6 values and writes 3; fp32)."""
+    import ctypes
+    import torch
+    lib = e2ttt.load()
+    n = w.B * w.H * w.T
+    g = torch.Generator(device=dev).manual_seed(11)
+    le, lb, la, de, db, dg = (torch.randn(n, device=dev, generator=g) for _ in range(6))
+    p = ctypes.byref(e2ttt.GateParams())
+    o = [torch.empty(n, device=dev) for _ in range(6)]
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    res = {}
+    for name, nbytes, call in (
+            ("fwd", 24 * n, lambda: lib.e2ttt_gates_forward(p, n, P(le), P(lb), P(la), P(o[0]),
+                                                            P(o[1]), P(o[2]), st)),
+            ("bwd", 36 * n, lambda: lib.e2ttt_gates_backward(p, n, P(le), P(lb), P(la), P(de),
+                                                             P(db), P(dg), P(o[3]), P(o[4]),
+                                                             P(o[5]), st))):
+        if call() != 0:
+            raise RuntimeError("gate %s call failed" % name)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(reps):
+            call()
+        ev[1].record()
+        torch.cuda.synchronize()
+        us = ev[0].elapsed_time(ev[1]) * 1e3 / reps
+        res[name + "_us"] = us
+        res[name + "_GBs"] = nbytes / (us * 1e-6) / 1e9
+        res[name + "_hbm_frac"] = res[name + "_GBs"] / PEAK_HBM_GBS
+    res["tokens"] = n
+    return res
+
+
+def time_decode(e2ttt, w, x, dev, reps: int = 200) -> dict:
+    """Streaming decode over the same units (eq. (6), Table 1): per step every
+    unit answers one token with e2ttt_apply at its chunk-start state, and every
+    C steps e2ttt_chunk_forward over the C buffered tokens advances the state.
+    Both are timed back to back on the stream through the C ABI (HIP events);
+    a step's cost is apply + update / C, and a step yields one token for each
+    of the B sequences.  The apply kernel is bound by reading the fp32 state
+    (P floats per unit) once."""
+    import ctypes
+    import torch
+    lib = e2ttt.load()
+    U = w.B * w.H
+    cfg1 = e2ttt.Config(w.B, w.H, 1, w.d, w.dh, w.C, w.fw, e2ttt.DT_BF16)
+    cfgc = e2ttt.Config(w.B, w.H, w.C, w.d, w.dh, w.C, w.fw, e2ttt.DT_BF16)
+    state = torch.from_numpy(x["w_in"]).to(dev)
+    q1 = torch.from_numpy(x["q"][:, :, :1].copy()).to(dev).to(torch.bfloat16)
+    o1 = torch.empty_like(q1)
+    chunk = {n: torch.from_numpy(x[n][:, :, :w.C].copy()).to(dev)
+             for n in ("q", "k", "v", "eta", "beta", "gamma")}
+    for n in ("q", "k", "v"):
+        chunk[n] = chunk[n].to(torch.bfloat16)
+    w_next, m_next = torch.empty_like(state), torch.empty_like(state)
+    ws = e2ttt.alloc_workspace(cfgc, False, dev)
+    oc = torch.empty_like(chunk["q"])
+    d1, dc = cfg1.desc(), cfgc.desc()
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+
+    def apply():
+        return lib.e2ttt_apply(ctypes.byref(d1), P(q1), P(state), P(o1), st)
+
+    def update():
+        return lib.e2ttt_chunk_forward(ctypes.byref(dc), P(chunk["q"]), P(chunk["k"]),
+                                       P(chunk["v"]), P(chunk["eta"]), P(chunk["beta"]),
+                                       P(chunk["gamma"]), P(state), None, P(oc), P(w_next),
+                                       P(m_next), P(ws), ws.numel(), 0, st)
+
+    res = {}
+    for name, call, n in (("apply", apply, reps), ("update", update, max(1, reps // 10))):
+        if call() != 0:
+            raise RuntimeError("decode %s call failed" % name)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(n):
+            call()
+        ev[1].record()
+        torch.cuda.synchronize()
+        res[name + "_us"] = ev[0].elapsed_time(ev[1]) * 1e3 / n
+    state_bytes = U * e2ttt.Config(w.B, w.H, 1, w.d, w.dh, w.C, w.fw).P * 4
+    step_us = res["apply_us"] + res["update_us"] / w.C
+    res.update(step_us=step_us, tokens_per_s=w.B / (step_us * 1e-6),
+               apply_state_GBs=state_bytes / (res["apply_us"] * 1e-6) / 1e9,
+               apply_hbm_frac=state_bytes / (res["apply_us"] * 1e-6) / 1e9 / PEAK_HBM_GBS,
+               batch=w.B, units=U, chunk=w.C)
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -183,6 +280,8 @@ def main():
                      "flop_per_launch": dom_flop, "avg_launch_ms": dom_ms},
         "detail": {"fwd_ms": avg_fwd, "bwd_ms": avg_bwd, "source_hash": source_hash()},
     }
+    res["gates"] = time_gates(e2ttt, w, dev)
+    res["decode"] = time_decode(e2ttt, w, x, dev)
     if args.no_cpu_baseline:
         res["cpu_baseline"] = None
     else:

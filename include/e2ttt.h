@@ -164,6 +164,25 @@ e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const 
                                 void* stream);
 
 /*
+ * Net evaluation at a given state: out_t = f_W(q_t) for T tokens per unit, all
+ * at the unit's one state W.  This is how a token's output is formed (eq. (6):
+ * the net at the start state of the token's chunk, Table 1), exposed for
+ * streaming decode: while a chunk fills, each arriving token is answered from
+ * the current chunk-start state with this call (T = 1), and once C tokens have
+ * arrived e2ttt_chunk_forward over those C tokens (w_in, m_in = the current
+ * state) gives the next chunk-start state.  Outputs and states then equal
+ * those of one e2ttt_chunk_forward over the whole sequence.
+ *   desc   as for the chunk calls (same supported set); desc.T is the number
+ *          of tokens per unit to evaluate; desc.chunk is checked but unused
+ *   q      [B][H][T][d] io
+ *   w      [B][H][P]   f32, 16-byte aligned (else E2TTT_ERR_BAD_SHAPE)
+ *   out    [B][H][T][d] io; may not overlap q or w
+ * fp32 arithmetic on the fp32 state (exact-erf GELU); no workspace.
+ */
+e2ttt_status e2ttt_apply(const e2ttt_desc* desc, const void* q, const float* w, void* out,
+                         void* stream);
+
+/*
  * Gate parameterization of Sec. 4 ("Input-Dependent Dynamics", eqs. (12)-(14)):
  * per token, from the outputs l_eta, l_beta, l_alpha of the three linear heads,
  *   eta   = eta_base * sigmoid(l_eta)                       (12)

@@ -222,6 +222,27 @@ e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const 
   return finish(launch_coeff_fwd(c, s), s);
 }
 
+e2ttt_status e2ttt_apply(const e2ttt_desc* desc, const void* q, const float* w, void* out,
+                         void* stream) {
+  Plan pl;
+  e2ttt_status st = make_plan(desc, pl);
+  if (st != E2TTT_OK) return st;
+  if (!q || !w || !out) return E2TTT_ERR_NULL_ARG;
+  if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return E2TTT_ERR_BAD_SHAPE;
+  if (desc->dh > kApplyMaxDh) return E2TTT_ERR_UNSUPPORTED;
+  if (pl.U * ((pl.T + 7) / 8) > INT_MAX) return E2TTT_ERR_UNSUPPORTED;
+  ApplyArgs a{};
+  a.q = q; a.w = w; a.out = out;
+  a.U = pl.U;
+  a.T = (int)pl.T;
+  a.dh = desc->dh;
+  a.P = pl.P;
+  a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
+  a.eps = desc->ln_eps;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return finish(launch_apply(pl.cfg, desc->fw, a, s), s);
+}
+
 e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const void* k,
                                  const void* v, const float* eta, const float* beta,
                                  const float* gamma, const float* w_in, const float* m_in,

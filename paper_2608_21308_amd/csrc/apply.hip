@@ -1,0 +1,163 @@
+// Evaluation of the fast-weight net at a given state, o = f_W(q) (eq. (6):
+// the output of a token is the net at its chunk's start state).  Streaming
+// decode answers each new token this way from the current chunk-start state
+// and advances the state with the chunk update once C tokens have arrived.
+//
+// One workgroup per (unit, group of up to TT tokens).  The work is a pair of
+// matrix-vector products per token over a state that is read once per
+// workgroup, so it is bound by HBM reads of W (fp32, P floats per unit):
+//   1. hidden: for every hidden row j, h_j = W1[j,:] . q (SwiGLU: the gate and
+//      up rows together).  D/4 lanes hold one row as float4 pieces (a wave
+//      reads 64/(D/4) whole rows per load, fully coalesced) and sum their
+//      partial dots over a DPP row; the activation goes to LDS.
+//   2. output: for every row i of W2 (Wd), y_i = W2[i,:] . a, one wave per row,
+//      lanes striding the hidden index (coalesced), summed over the wave.
+//   3. LayerNorm over the D outputs of each token and the residual, one wave
+//      per token; written in the io type.
+#include <math.h>
+
+#include "e2ttt.h"
+#include "e2ttt_device.h"
+#include "e2ttt_internal.h"
+
+namespace e2ttt {
+namespace {
+
+constexpr int kApplyWaves = 8;
+
+// Sum over groups of L consecutive lanes (L = 4 or 16), returned to every lane of the group.
+template <int L>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(L == 4 || L == 16, "row group of 4 or 16 lanes");
+  if constexpr (L == 16) {
+    return group16_sum(v);
+  } else {
+    v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+    v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+    return v;
+  }
+}
+
+__device__ __forceinline__ float gelu_exact(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+__device__ __forceinline__ float silu_exact(float x) { return x / (1.0f + expf(-x)); }
+
+template <int D, bool BF, int FW, int TT>
+__global__ void __launch_bounds__(64 * kApplyWaves) apply_kernel(ApplyArgs a) {
+  using Io = IoT<BF>;
+  using E = typename Io::T;
+  constexpr int L = D / 4;            // lanes per row of W1
+  constexpr int RPI = 64 / L;         // rows of W1 per wave per load
+  __shared__ float qs[TT][D];
+  __shared__ float hs[TT][kApplyMaxDh];
+  __shared__ float ys[TT][D];
+
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const long u = blockIdx.x / a.groups;
+  const int t0 = (int)(blockIdx.x % a.groups) * TT;
+  const int nt = min(TT, a.T - t0);
+  const E* q = static_cast<const E*>(a.q) + (u * a.T + t0) * D;
+  E* out = static_cast<E*>(a.out) + (u * a.T + t0) * D;
+  const float* w = a.w + u * a.P;
+
+  for (int x = threadIdx.x; x < TT * D; x += 64 * kApplyWaves) {
+    const int t = x / D, i = x % D;
+    qs[t][i] = (t < nt) ? Io::ld(q + (long)t * D + i) : 0.0f;
+  }
+  __syncthreads();
+
+  // 1. hidden rows
+  const int c4 = lane % L, rsub = lane / L;
+  f32x4 qv[TT];
+#pragma unroll
+  for (int t = 0; t < TT; ++t)
+    qv[t] = f32x4{qs[t][4 * c4], qs[t][4 * c4 + 1], qs[t][4 * c4 + 2], qs[t][4 * c4 + 3]};
+  const int dh = a.dh;
+  for (int r0 = wv * RPI; r0 < dh; r0 += kApplyWaves * RPI) {
+    const int r = r0 + rsub;
+    const bool ok = r < dh;
+    const f32x4 w1 = ok ? *reinterpret_cast<const f32x4*>(w + (long)r * D + 4 * c4) : zero4();
+    f32x4 w3 = zero4();
+    if constexpr (FW == 1)
+      w3 = ok ? *reinterpret_cast<const f32x4*>(w + (long)(dh + r) * D + 4 * c4) : zero4();
+#pragma unroll
+    for (int t = 0; t < TT; ++t) {
+      float h = group_sum<L>(w1[0] * qv[t][0] + w1[1] * qv[t][1] + w1[2] * qv[t][2] +
+                             w1[3] * qv[t][3]);
+      if constexpr (FW == 0) {
+        if (ok && c4 == 0) hs[t][r] = gelu_exact(h);
+      } else {
+        const float g = h;
+        const float up = group_sum<L>(w3[0] * qv[t][0] + w3[1] * qv[t][1] +
+                                      w3[2] * qv[t][2] + w3[3] * qv[t][3]);
+        if (ok && c4 == 0) hs[t][r] = silu_exact(g) * up;
+      }
+    }
+  }
+  __syncthreads();
+
+  // 2. output rows: W2 (MLP) or Wd (SwiGLU) starts after the input-side matrices
+  const float* w2 = w + (long)(FW == 0 ? 1 : 2) * dh * D;
+  for (int i = wv; i < D; i += kApplyWaves) {
+    float acc[TT];
+#pragma unroll
+    for (int t = 0; t < TT; ++t) acc[t] = 0.0f;
+    for (int j = lane; j < dh; j += 64) {
+      const float wij = w2[(long)i * dh + j];
+#pragma unroll
+      for (int t = 0; t < TT; ++t) acc[t] = fmaf(wij, hs[t][j], acc[t]);
+    }
+#pragma unroll
+    for (int t = 0; t < TT; ++t) {
+      const float y = wave_sum(acc[t]);
+      if (lane == 0) ys[t][i] = y;
+    }
+  }
+  __syncthreads();
+
+  // 3. LayerNorm (biased variance) and residual, one wave per token
+  for (int t = wv; t < nt; t += kApplyWaves) {
+    const bool act = lane < D;
+    const float y = act ? ys[t][lane] : 0.0f;
+    float o = y;
+    if (a.resln) {
+      const float mean = wave_sum(y) * (1.0f / D);
+      const float dv = act ? y - mean : 0.0f;
+      const float var = wave_sum(dv * dv) * (1.0f / D);
+      o = qs[t][lane < D ? lane : 0] + dv / sqrtf(var + a.eps);
+    }
+    if (act) Io::st(out + (long)t * D + lane, o);
+  }
+}
+
+template <int D, bool BF, int FW, int TT>
+hipError_t launch(const ApplyArgs& a, hipStream_t s) {
+  const long blocks = a.U * a.groups;
+  hipLaunchKernelGGL((apply_kernel<D, BF, FW, TT>), dim3((unsigned)blocks),
+                     dim3(64 * kApplyWaves), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int D, bool BF, int FW>
+hipError_t launch_tt(ApplyArgs a, hipStream_t s) {
+  if (a.T == 1) {
+    a.groups = 1;
+    return launch<D, BF, FW, 1>(a, s);
+  }
+  a.groups = (a.T + 7) / 8;
+  return launch<D, BF, FW, 8>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_apply(const ChainConfig& cfg, int fw, ApplyArgs a, hipStream_t s) {
+  if (a.dh > kApplyMaxDh || a.T < 1) return hipErrorInvalidValue;
+  if (cfg.bf && cfg.d == 64)
+    return fw == 0 ? launch_tt<64, true, 0>(a, s) : launch_tt<64, true, 1>(a, s);
+  if (!cfg.bf && cfg.d == 16)
+    return fw == 0 ? launch_tt<16, false, 0>(a, s) : launch_tt<16, false, 1>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace e2ttt

@@ -100,11 +100,28 @@ struct ChainConfig {
   int ns;     // workgroups per unit (1, or 2 with a cooperative launch)
 };
 
+// Net evaluation at a given state (e2ttt_apply): per unit, T tokens of q at
+// one state w of P floats.
+struct ApplyArgs {
+  const void* q;        // [U][T][d] io
+  const float* w;       // [U][P]
+  void* out;            // [U][T][d] io
+  long U;
+  int T, dh;
+  int groups;           // token groups per unit (set by the launcher)
+  long P;
+  int resln;
+  float eps;
+};
+constexpr int kApplyMaxDh = 256;
+
 hipError_t launch_coeff_fwd(const CoeffFwdArgs& a, hipStream_t stream);
 hipError_t launch_coeff_bwd(const CoeffBwdArgs& a, hipStream_t stream);
 // Return hipErrorInvalidValue when no kernel exists for `cfg`.
 hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
 hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
+// Returns hipErrorInvalidValue for a head dim / io type / width without a kernel.
+hipError_t launch_apply(const ChainConfig& cfg, int fw, ApplyArgs a, hipStream_t stream);
 // Clears n words (a kernel, so that it may be captured in a graph).
 hipError_t launch_zero_words(unsigned* p, long n, hipStream_t stream);
 // Pairs a cooperative launch of the chain kernel can hold at once (multiple of 8).

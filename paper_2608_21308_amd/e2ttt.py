@@ -28,7 +28,7 @@ STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
 # Every entry point the header declares (checked by the CPU test-suite).
 EXPORTS = ("e2ttt_param_count", "e2ttt_workspace_bytes", "e2ttt_backward_scratch_bytes",
            "e2ttt_chunk_forward", "e2ttt_chunk_backward", "e2ttt_chunk_coeffs",
-           "e2ttt_gates_forward", "e2ttt_gates_backward", "e2ttt_status_str")
+           "e2ttt_apply", "e2ttt_gates_forward", "e2ttt_gates_backward", "e2ttt_status_str")
 
 
 class E2TTTError(RuntimeError):
@@ -79,6 +79,8 @@ def load():
     lib.e2ttt_chunk_backward.restype = i
     lib.e2ttt_chunk_coeffs.argtypes = [dp] + [vp] * 7
     lib.e2ttt_chunk_coeffs.restype = i
+    lib.e2ttt_apply.argtypes = [dp] + [vp] * 4
+    lib.e2ttt_apply.restype = i
     gp = ctypes.POINTER(GateParams)
     lib.e2ttt_gates_forward.argtypes = [gp, ctypes.c_int64] + [vp] * 7
     lib.e2ttt_gates_forward.restype = i
@@ -133,6 +135,42 @@ def _check(st: int, where: str):
         raise E2TTTError(st, where)
 
 
+_IO = ("q", "k", "v", "out", "d_out", "dq", "dk", "dv")
+_GATE = ("eta", "beta", "gamma", "d_eta", "d_beta", "d_gamma", "kw", "km")
+_STATE = ("w_in", "m_in", "w_out", "m_out", "d_w_in", "d_m_in", "d_w_out", "d_m_out")
+
+
+def _check_tensors(cfg: Config, **ts):
+    """Host-side guard before any launch: every tensor the library will read or
+    write is a contiguous device tensor on the device of the first one, with
+    the element type and element count the header gives for its role.  The
+    library itself checks only sizes it is handed (workspace, scratch)."""
+    dev = None
+    n_tok = cfg.B * cfg.H * cfg.T
+    for name, t in ts.items():
+        if t is None:
+            continue
+        if not isinstance(t, torch.Tensor) or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous tensor" % name)
+        if name in _IO:
+            want = (cfg.torch_io, n_tok * cfg.d)
+        elif name in _GATE:
+            want = (torch.float32, n_tok)
+        elif name in _STATE:
+            want = (torch.float32, cfg.B * cfg.H * cfg.P)
+        else:                       # workspace, scratch: byte buffers
+            want = (torch.uint8, t.numel())
+        if t.dtype != want[0] or t.numel() != want[1]:
+            raise ValueError("%s: expected %d elements of %s, got %d of %s"
+                             % (name, want[1], want[0], t.numel(), t.dtype))
+        if t.device.type != "cuda":
+            raise ValueError("%s must be a device tensor" % name)
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError("%s is on %s, expected %s" % (name, t.device, dev))
+
+
 def workspace_bytes(cfg: Config, save_for_backward: bool) -> int:
     d = cfg.desc()
     return int(load().e2ttt_workspace_bytes(ctypes.byref(d), int(bool(save_for_backward))))
@@ -153,6 +191,8 @@ def alloc_workspace(cfg: Config, save_for_backward: bool, device="cuda"):
 def forward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in=None, *, out=None, w_out=None,
             m_out=None, workspace=None, save_for_backward=False):
     """Runs e2ttt_chunk_forward on the current stream; returns (out, w_out, m_out, workspace)."""
+    _check_tensors(cfg, q=q, k=k, v=v, eta=eta, beta=beta, gamma=gamma, w_in=w_in, m_in=m_in,
+                   out=out, w_out=w_out, m_out=m_out, workspace=workspace)
     lib = load()
     dev = q.device
     if out is None:
@@ -176,6 +216,9 @@ def backward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, workspace, d_ou
              d_m_out=None, *, grads=None, scratch=None):
     """Runs e2ttt_chunk_backward; returns a dict of gradients (dq, dk, dv, d_eta, d_beta,
     d_gamma, d_w_in, d_m_in)."""
+    _check_tensors(cfg, q=q, k=k, v=v, eta=eta, beta=beta, gamma=gamma, w_in=w_in, m_in=m_in,
+                   workspace=workspace, d_out=d_out, d_w_out=d_w_out, d_m_out=d_m_out,
+                   scratch=scratch, **(grads or {}))
     lib = load()
     dev = q.device
     if grads is None:
@@ -197,8 +240,22 @@ def backward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, workspace, d_ou
     return grads
 
 
+def apply(cfg: Config, q, w, out=None):
+    """Runs e2ttt_apply: out = f_W(q) for the cfg.T tokens of q per unit, all at
+    the state w [B,H,P]."""
+    _check_tensors(cfg, q=q, w_in=w, out=out)
+    lib = load()
+    if out is None:
+        out = torch.empty_like(q)
+    d = cfg.desc()
+    st = lib.e2ttt_apply(ctypes.byref(d), _ptr(q), _ptr(w), _ptr(out), _stream())
+    _check(st, "e2ttt_apply")
+    return out
+
+
 def chunk_coeffs(cfg: Config, eta, beta, gamma):
     """Scalar kernels: (kw [B,H,T], km [B,H,T], carry [B,H,NC,3])."""
+    _check_tensors(cfg, eta=eta, beta=beta, gamma=gamma)
     lib = load()
     kw = torch.empty_like(eta)
     km = torch.empty_like(eta)
@@ -217,29 +274,46 @@ def _check_gate_tensors(*ts):
             continue
         if t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != n:
             raise ValueError("gate arrays must be contiguous float32 tensors of one size")
+        if t.device.type != "cuda" or t.device != ts[0].device:
+            raise ValueError("gate arrays must be device tensors on one GPU")
 
 
-def gates_forward(params: GateParams, l_eta, l_beta, l_alpha=None):
+def gates_forward(params: GateParams, l_eta, l_beta, l_alpha=None, out=None):
     """Gate parameterization, eqs. (12)-(14): (eta, beta, gamma) from the logits
-    (gamma None when l_alpha is None)."""
+    (gamma None when l_alpha is None).  `out`: optional (eta, beta, gamma)
+    tensors to write into."""
     _check_gate_tensors(l_eta, l_beta, l_alpha)
     lib = load()
-    eta = torch.empty_like(l_eta)
-    beta = torch.empty_like(l_beta)
-    gamma = None if l_alpha is None else torch.empty_like(l_alpha)
+    if out is None:
+        eta = torch.empty_like(l_eta)
+        beta = torch.empty_like(l_beta)
+        gamma = None if l_alpha is None else torch.empty_like(l_alpha)
+    else:
+        eta, beta, gamma = out
+        _check_gate_tensors(eta, beta, gamma)
+        if eta.numel() != l_eta.numel() or (gamma is None) != (l_alpha is None):
+            raise ValueError("gate outputs must match the logits")
     st = lib.e2ttt_gates_forward(ctypes.byref(params), l_eta.numel(), _ptr(l_eta), _ptr(l_beta),
                                  _ptr(l_alpha), _ptr(eta), _ptr(beta), _ptr(gamma), _stream())
     _check(st, "e2ttt_gates_forward")
     return eta, beta, gamma
 
 
-def gates_backward(params: GateParams, l_eta, l_beta, l_alpha, d_eta, d_beta, d_gamma):
-    """Gradients of the logits from the gate gradients: (d_l_eta, d_l_beta, d_l_alpha)."""
+def gates_backward(params: GateParams, l_eta, l_beta, l_alpha, d_eta, d_beta, d_gamma,
+                   out=None):
+    """Gradients of the logits from the gate gradients: (d_l_eta, d_l_beta,
+    d_l_alpha).  `out`: optional tensors of those three to write into."""
     _check_gate_tensors(l_eta, l_beta, l_alpha, d_eta, d_beta, d_gamma)
     lib = load()
-    g_eta = torch.empty_like(l_eta)
-    g_beta = torch.empty_like(l_beta)
-    g_alpha = None if l_alpha is None else torch.empty_like(l_alpha)
+    if out is None:
+        g_eta = torch.empty_like(l_eta)
+        g_beta = torch.empty_like(l_beta)
+        g_alpha = None if l_alpha is None else torch.empty_like(l_alpha)
+    else:
+        g_eta, g_beta, g_alpha = out
+        _check_gate_tensors(g_eta, g_beta, g_alpha)
+        if g_eta.numel() != l_eta.numel() or (g_alpha is None) != (l_alpha is None):
+            raise ValueError("gate gradient outputs must match the logits")
     st = lib.e2ttt_gates_backward(ctypes.byref(params), l_eta.numel(), _ptr(l_eta), _ptr(l_beta),
                                   _ptr(l_alpha), _ptr(d_eta), _ptr(d_beta), _ptr(d_gamma),
                                   _ptr(g_eta), _ptr(g_beta), _ptr(g_alpha), _stream())

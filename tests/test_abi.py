@@ -63,6 +63,7 @@ def test_bad_descriptors(lib, kw, status):
     st = lib.e2ttt_chunk_backward(ctypes.byref(d), *([fake] * 9), 1 << 40, *([fake] * 12),
                                   1 << 40, None)
     assert st == status
+    assert lib.e2ttt_apply(ctypes.byref(d), fake, fake, fake, None) == status
 
 
 def test_null_and_workspace_errors(lib):
@@ -155,3 +156,46 @@ def test_gate_argument_errors(lib):
         a = list(b)
         a[i] = None
         assert bwd(ctypes.byref(p), 8, *a, None) == 1, i
+
+
+def test_binding_rejects_host_and_misshaped_tensors():
+    """The Python binding refuses host tensors, wrong dtypes and wrong element
+    counts before it reaches the library (a host pointer handed to a kernel
+    would fault the GPU)."""
+    import torch
+    cfg = e2ttt.Config(1, 2, 32, 16, 64, 16, e2ttt.FW_MLP, e2ttt.DT_F32)
+    io = torch.zeros(1, 2, 32, 16)
+    g = torch.zeros(1, 2, 32)
+    st = torch.zeros(1, 2, cfg.P)
+    with pytest.raises(ValueError, match="device tensor"):
+        e2ttt.forward(cfg, io, io, io, g, g, g, st, None)
+    with pytest.raises(ValueError, match="device tensor"):
+        e2ttt.backward(cfg, io, io, io, g, g, g, st, None, torch.zeros(8, dtype=torch.uint8), io)
+    with pytest.raises(ValueError, match="device tensor"):
+        e2ttt.chunk_coeffs(cfg, g, g, g)
+    with pytest.raises(ValueError, match="device tensor"):
+        e2ttt.gates_forward(e2ttt.GateParams(), g, g, g)
+    with pytest.raises(ValueError, match="device tensor"):
+        e2ttt.gates_backward(e2ttt.GateParams(), g, g, g, g, g, g)
+    # element type and count by role, checked before the device
+    for kw in (dict(q=io.to(torch.bfloat16)), dict(k=io[..., :8].contiguous()),
+               dict(eta=io), dict(w_in=g), dict(d_w_in=st.double()),
+               dict(workspace=torch.zeros(4))):
+        with pytest.raises(ValueError, match="expected"):
+            e2ttt._check_tensors(cfg, **kw)
+    with pytest.raises(ValueError, match="contiguous"):
+        e2ttt._check_tensors(cfg, q=torch.zeros(1, 2, 16, 32).transpose(2, 3))
+    with pytest.raises(ValueError, match="device tensor"):
+        e2ttt._check_tensors(cfg, q=io, eta=g, w_in=st, workspace=torch.zeros(4, dtype=torch.uint8))
+
+
+def test_apply_argument_errors(lib):
+    d = desc()
+    f = ctypes.c_void_p(256)   # never dereferenced
+    assert lib.e2ttt_apply(None, f, f, f, None) == 1
+    for i in range(3):
+        a = [f, f, f]
+        a[i] = None
+        assert lib.e2ttt_apply(ctypes.byref(d), *a, None) == 1, i
+    # the state is read as float4: a pointer that is not 16-byte aligned is refused
+    assert lib.e2ttt_apply(ctypes.byref(d), f, ctypes.c_void_p(260), f, None) == 2

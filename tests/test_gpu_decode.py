@@ -1,0 +1,133 @@
+"""GPU parity of the net evaluation at a given state (e2ttt_apply) and of
+streaming decode built from it.
+
+Eq. (6) and Table 1: a token's output is the fast-weight net at the start
+state of its chunk.  e2ttt_apply evaluates f_W(q) at one state; a decoder
+answers each token with it and advances the state with e2ttt_chunk_forward
+once a chunk is full.  The oracle is oracle.net (f_W of one unit) for the
+first and oracle.forward over the whole sequence for the second.
+
+Bars: fp32 io, rel-L2 1e-5 (fp32 arithmetic on both matrix-vector products);
+bf16 io, every element within one bf16 ulp of the exact value (the kernel
+computes in fp32 and rounds once) plus the fp32 evaluation error; the streaming decode, the chunk
+update's own bars (rel-L2 1e-5 fp32, 2e-2 bf16).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2608_21308_amd import e2ttt, workloads as WL
+from tests.gpu_util import TOL, config_of, rel_l2, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    e2ttt.load()
+
+
+CASES = {
+    "mlp_f32_d16": WL.WORKLOADS[0].with_(B=2, H=3, T=16, C=16),
+    "swiglu_f32_d16": WL.WORKLOADS[0].with_(fw=e2ttt.FW_SWIGLU, dh=48, B=2, H=3, T=16, C=16),
+    "mlp_bf16_d64": WL.WORKLOADS[1].with_(B=2, H=3, T=16, C=16),
+    "swiglu_bf16_d64": WL.WORKLOADS[2].with_(B=2, H=3, T=16, C=16),
+}
+
+
+def perturbed_state(x, seed):
+    """A state away from the initial draw: w_in times (1 + 0.3 N(0, 1))."""
+    rng = np.random.default_rng(seed)
+    w = x["w_in"]
+    return (w * (1.0 + 0.3 * rng.standard_normal(w.shape))).astype(np.float32)
+
+
+def bf16_ulp(x):
+    """Spacing of bf16 values at |x| (8 significand bits)."""
+    e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -126)))
+    return 2.0 ** (e - 7)
+
+
+def check_apply(w, T, flags=0, seed=0):
+    wl = w.with_(T=T)
+    x = WL.make_inputs(wl, with_grads=False)
+    W = perturbed_state(x, seed)
+    cfg = config_of(wl, flags=flags)
+    t = to_dev(dict(q=x["q"], w=W), wl.io)
+    got = e2ttt.apply(cfg, t["q"], t["w"]).float().cpu().numpy()
+    ref = np.empty_like(got, dtype=np.float64)
+    for b in range(wl.B):
+        for h in range(wl.H):
+            ref[b, h] = oracle.net(W[b, h], x["q"][b, h], fw=wl.fw, dh=wl.dh, flags=flags)
+    print("apply %s T=%d flags=%d" % (wl.name, T, flags), flush=True)
+    if wl.io == "f32":
+        assert rel_l2(got, ref) <= TOL["f32"]
+    else:
+        err = np.abs(got - ref)
+        # one bf16 rounding plus the fp32 evaluation error (a few 2^-24 of the terms)
+        bound = bf16_ulp(ref) + 1e-6 * (np.abs(x["q"]) + np.abs(ref) + 1.0)
+        assert np.all(err <= bound), float(np.max(err / bound))
+    return got
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+@pytest.mark.parametrize("T", [1, 7, 8, 13, 64])
+def test_apply_matches_the_net(case, T):
+    check_apply(CASES[case], T, seed=T)
+
+
+@pytest.mark.parametrize("case", ["mlp_f32_d16", "mlp_bf16_d64"])
+def test_apply_bare_net(case):
+    check_apply(CASES[case], 5, flags=e2ttt.FLAG_NO_RESIDUAL_LN, seed=3)
+
+
+def test_apply_is_the_chunk_forward_output():
+    """Within one chunk every output is f_{W_0}(q_t): e2ttt_apply at w_in and
+    e2ttt_chunk_forward agree (fp32 path, both at their fp32 bar)."""
+    w = CASES["mlp_f32_d16"].with_(T=16)
+    x = WL.make_inputs(w, with_grads=False)
+    cfg = config_of(w)
+    t = to_dev(x, w.io)
+    out, _, _, _ = e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                                 t["w_in"], None)
+    got = e2ttt.apply(cfg, t["q"], t["w_in"])
+    assert rel_l2(got, out.float().cpu().numpy()) <= 2 * TOL["f32"]
+
+
+def stream(w, x, dev="cuda"):
+    """Token-by-token decode: e2ttt_apply for each token's output, then
+    e2ttt_chunk_forward over each full (or final partial) chunk to advance the
+    state.  Returns (outputs [B,H,T,d], w, m) on the host."""
+    t = to_dev(x, w.io, dev)
+    state, mom = t["w_in"].clone(), None
+    cfg1 = config_of(w, T=1)
+    outs = []
+    for c0 in range(0, w.T, w.C):
+        c1 = min(c0 + w.C, w.T)
+        for s in range(c0, c1):
+            outs.append(e2ttt.apply(cfg1, t["q"][:, :, s:s + 1].contiguous(), state))
+        sl = {n: None if t[n] is None else t[n][:, :, c0:c1].contiguous()
+              for n in ("q", "k", "v", "eta", "beta", "gamma")}
+        cfgc = config_of(w, T=c1 - c0)
+        _, state, mom, _ = e2ttt.forward(cfgc, sl["q"], sl["k"], sl["v"], sl["eta"], sl["beta"],
+                                         sl["gamma"], state, mom)
+    out = torch.cat(outs, dim=2)
+    return out.float().cpu().numpy(), state.cpu().numpy(), mom.cpu().numpy()
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_streaming_decode_matches_the_sequence_forward(case):
+    """Decode one token at a time over 3 full chunks and a ragged one; outputs
+    and final state equal the oracle's forward over the whole sequence."""
+    w = CASES[case].with_(T=3 * 16 + 5)
+    x = WL.make_inputs(w, with_grads=False)
+    out, wo, mo = stream(w, x)
+    r_out, r_w, r_m = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"],
+                                     x["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
+    errs = dict(out=rel_l2(out, r_out), w=rel_l2(wo - x["w_in"], r_w - x["w_in"]),
+                m=rel_l2(mo, r_m))
+    print("decode %s" % case, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    for k, e in errs.items():
+        assert e <= TOL[w.io], k
