@@ -6,12 +6,16 @@
 // One workgroup per (unit, group of up to TT tokens).  The work is a pair of
 // matrix-vector products per token over a state that is read once per
 // workgroup, so it is bound by HBM reads of W (fp32, P floats per unit):
+//   0. every lane issues all of its loads of the state at once (the whole
+//      P floats of the unit are in flight together; a workgroup is otherwise
+//      latency-bound on a single unit's 2 d dh floats).
 //   1. hidden: for every hidden row j, h_j = W1[j,:] . q (SwiGLU: the gate and
 //      up rows together).  D/4 lanes hold one row as float4 pieces (a wave
 //      reads 64/(D/4) whole rows per load, fully coalesced) and sum their
 //      partial dots over a DPP row; the activation goes to LDS.
-//   2. output: for every row i of W2 (Wd), y_i = W2[i,:] . a, one wave per row,
-//      lanes striding the hidden index (coalesced), summed over the wave.
+//   2. output: for every row i of W2 (Wd), y_i = W2[i,:] . a, one wave per
+//      row, each lane holding four consecutive hidden indices (one float4
+//      load), summed over the wave.
 //   3. LayerNorm over the D outputs of each token and the residual, one wave
 //      per token; written in the io type.
 #include <math.h>
@@ -47,8 +51,12 @@ template <int D, bool BF, int FW, int TT>
 __global__ void __launch_bounds__(64 * kApplyWaves) apply_kernel(ApplyArgs a) {
   using Io = IoT<BF>;
   using E = typename Io::T;
-  constexpr int L = D / 4;            // lanes per row of W1
-  constexpr int RPI = 64 / L;         // rows of W1 per wave per load
+  constexpr int NWV = kApplyWaves;
+  constexpr int L = D / 4;                                   // lanes per row of W1
+  constexpr int RPI = 64 / L;                                // W1 rows per wave per load
+  constexpr int NR1 = (kApplyMaxDh + NWV * RPI - 1) / (NWV * RPI);  // W1 loads per lane
+  constexpr int NR2 = D / NWV;                               // W2 rows per wave
+  static_assert(D % NWV == 0 && 4 * 64 >= kApplyMaxDh, "one float4 of W2 per lane and row");
   __shared__ float qs[TT][D];
   __shared__ float hs[TT][kApplyMaxDh];
   __shared__ float ys[TT][D];
@@ -60,64 +68,90 @@ __global__ void __launch_bounds__(64 * kApplyWaves) apply_kernel(ApplyArgs a) {
   const E* q = static_cast<const E*>(a.q) + (u * a.T + t0) * D;
   E* out = static_cast<E*>(a.out) + (u * a.T + t0) * D;
   const float* w = a.w + u * a.P;
+  const int dh = a.dh;
+  const float* w2 = w + (long)(FW == 0 ? 1 : 2) * dh * D;   // W2 (MLP) or Wd (SwiGLU)
 
-  for (int x = threadIdx.x; x < TT * D; x += 64 * kApplyWaves) {
+  // Every load of this workgroup's share of the state is issued up front, so
+  // the whole state (P floats) is in flight at once.
+  const int c4 = lane % L, rsub = lane / L;
+  f32x4 w1r[NR1], w3r[NR1], w2r[NR2];
+#pragma unroll
+  for (int k = 0; k < NR1; ++k) {
+    const int r = (k * NWV + wv) * RPI + rsub;
+    w1r[k] = zero4();
+    w3r[k] = zero4();
+    if (r < dh) {
+      w1r[k] = *reinterpret_cast<const f32x4*>(w + (long)r * D + 4 * c4);
+      if constexpr (FW == 1)
+        w3r[k] = *reinterpret_cast<const f32x4*>(w + (long)(dh + r) * D + 4 * c4);
+    }
+  }
+  const int j4 = 4 * lane;
+  if ((dh & 3) == 0) {   // rows of W2 start 16-byte aligned
+#pragma unroll
+    for (int k = 0; k < NR2; ++k) {
+      const int i = k * NWV + wv;
+      w2r[k] = (j4 < dh) ? *reinterpret_cast<const f32x4*>(w2 + (long)i * dh + j4) : zero4();
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < NR2; ++k) {
+      const int i = k * NWV + wv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w2r[k][e] = (j4 + e < dh) ? w2[(long)i * dh + j4 + e] : 0.0f;
+    }
+  }
+
+  for (int x = threadIdx.x; x < TT * D; x += 64 * NWV) {
     const int t = x / D, i = x % D;
     qs[t][i] = (t < nt) ? Io::ld(q + (long)t * D + i) : 0.0f;
   }
   __syncthreads();
 
-  // 1. hidden rows
-  const int c4 = lane % L, rsub = lane / L;
+  // 1. hidden rows: h = W1 q (SwiGLU: g = Wg q, up = Wu q), activation to LDS
   f32x4 qv[TT];
 #pragma unroll
   for (int t = 0; t < TT; ++t)
     qv[t] = f32x4{qs[t][4 * c4], qs[t][4 * c4 + 1], qs[t][4 * c4 + 2], qs[t][4 * c4 + 3]};
-  const int dh = a.dh;
-  for (int r0 = wv * RPI; r0 < dh; r0 += kApplyWaves * RPI) {
+#pragma unroll
+  for (int k = 0; k < NR1; ++k) {
+    const int r0 = (k * NWV + wv) * RPI;
+    if (r0 >= dh) break;   // uniform over the wave
     const int r = r0 + rsub;
-    const bool ok = r < dh;
-    const f32x4 w1 = ok ? *reinterpret_cast<const f32x4*>(w + (long)r * D + 4 * c4) : zero4();
-    f32x4 w3 = zero4();
-    if constexpr (FW == 1)
-      w3 = ok ? *reinterpret_cast<const f32x4*>(w + (long)(dh + r) * D + 4 * c4) : zero4();
 #pragma unroll
     for (int t = 0; t < TT; ++t) {
-      float h = group_sum<L>(w1[0] * qv[t][0] + w1[1] * qv[t][1] + w1[2] * qv[t][2] +
-                             w1[3] * qv[t][3]);
+      const float h = group_sum<L>(w1r[k][0] * qv[t][0] + w1r[k][1] * qv[t][1] +
+                                   w1r[k][2] * qv[t][2] + w1r[k][3] * qv[t][3]);
       if constexpr (FW == 0) {
-        if (ok && c4 == 0) hs[t][r] = gelu_exact(h);
+        if (r < dh && c4 == 0) hs[t][r] = gelu_exact(h);
       } else {
-        const float g = h;
-        const float up = group_sum<L>(w3[0] * qv[t][0] + w3[1] * qv[t][1] +
-                                      w3[2] * qv[t][2] + w3[3] * qv[t][3]);
-        if (ok && c4 == 0) hs[t][r] = silu_exact(g) * up;
+        const float up = group_sum<L>(w3r[k][0] * qv[t][0] + w3r[k][1] * qv[t][1] +
+                                      w3r[k][2] * qv[t][2] + w3r[k][3] * qv[t][3]);
+        if (r < dh && c4 == 0) hs[t][r] = silu_exact(h) * up;
       }
     }
   }
   __syncthreads();
 
-  // 2. output rows: W2 (MLP) or Wd (SwiGLU) starts after the input-side matrices
-  const float* w2 = w + (long)(FW == 0 ? 1 : 2) * dh * D;
-  for (int i = wv; i < D; i += kApplyWaves) {
-    float acc[TT];
+  // 2. output rows: y_i = W2[i,:] . a, lane holding hidden indices 4 lane .. 4 lane + 3
 #pragma unroll
-    for (int t = 0; t < TT; ++t) acc[t] = 0.0f;
-    for (int j = lane; j < dh; j += 64) {
-      const float wij = w2[(long)i * dh + j];
+  for (int t = 0; t < TT; ++t) {
+    f32x4 av = zero4();
+    if (j4 < dh) {
 #pragma unroll
-      for (int t = 0; t < TT; ++t) acc[t] = fmaf(wij, hs[t][j], acc[t]);
+      for (int e = 0; e < 4; ++e) av[e] = (j4 + e < dh) ? hs[t][j4 + e] : 0.0f;
     }
 #pragma unroll
-    for (int t = 0; t < TT; ++t) {
-      const float y = wave_sum(acc[t]);
-      if (lane == 0) ys[t][i] = y;
+    for (int k = 0; k < NR2; ++k) {
+      const float y = wave_sum(w2r[k][0] * av[0] + w2r[k][1] * av[1] + w2r[k][2] * av[2] +
+                               w2r[k][3] * av[3]);
+      if (lane == 0) ys[t][k * NWV + wv] = y;
     }
   }
   __syncthreads();
 
   // 3. LayerNorm (biased variance) and residual, one wave per token
-  for (int t = wv; t < nt; t += kApplyWaves) {
+  for (int t = wv; t < nt; t += NWV) {
     const bool act = lane < D;
     const float y = act ? ys[t][lane] : 0.0f;
     float o = y;
