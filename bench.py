@@ -280,6 +280,20 @@ def main():
                      "flop_per_launch": dom_flop, "avg_launch_ms": dom_ms},
         "detail": {"fwd_ms": avg_fwd, "bwd_ms": avg_bwd, "source_hash": source_hash()},
     }
+    # the same step under the chunk-averaged rule (ablation baseline): only the
+    # scalar kernels differ, so this isolates what the closed form costs
+    cfg_avg = e2ttt.Config(w.B, w.H, w.T, w.d, w.dh, w.C, w.fw, e2ttt.DT_BF16,
+                           e2ttt.FLAG_CHUNK_AVERAGED)
+    cfg_main = cfg
+    cfg = cfg_avg
+    step()
+    torch.cuda.synchronize()
+    ta = time.perf_counter()
+    for _ in range(max(1, args.steps // 2)):
+        step()
+    torch.cuda.synchronize()
+    res["averaged_rule_ms_per_step"] = (time.perf_counter() - ta) * 1e3 / max(1, args.steps // 2)
+    cfg = cfg_main
     res["gates"] = time_gates(e2ttt, w, dev)
     res["decode"] = time_decode(e2ttt, w, x, dev)
     if args.no_cpu_baseline:

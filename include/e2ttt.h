@@ -83,6 +83,17 @@ typedef enum { E2TTT_DT_F32 = 0, E2TTT_DT_BF16 = 1 } e2ttt_dtype;
 
 /* f(x) = y (the bare matrix net) instead of f(x) = x + LN(y). */
 #define E2TTT_FLAG_NO_RESIDUAL_LN 0x1u
+/* Chunk-averaged update rule instead of the closed form of Prop. 1: the
+ * ablation baseline of Sec. 5 (Tables 4 and 5) that collapses the per-token
+ * momentum and decay factors of a chunk to their means, after the chunk-level
+ * momentum of eqs. (4)-(5).  Per chunk of L tokens, with beta_bar and
+ * gamma_bar the means of beta_t and gamma_t over the chunk (gamma NULL:
+ * gamma_bar = 1, which is eqs. (4)-(5) exactly):
+ *   M_C = beta_bar M_0 + sum_t eta_t G_t,   W_C = gamma_bar W_0 + M_C,
+ * that is K^W_t = K^M_t = eta_t and carry (gamma_bar, beta_bar, beta_bar).
+ * Outputs, gradients and every other convention are unchanged (all entry
+ * points that take a descriptor honour the flag). */
+#define E2TTT_FLAG_CHUNK_AVERAGED 0x2u
 
 typedef struct {
   int32_t B, H, T;      /* batch, heads, tokens                        */

@@ -67,7 +67,8 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
     return E2TTT_ERR_BAD_SHAPE;
   if (d.fw != E2TTT_FW_GELU_MLP && d.fw != E2TTT_FW_SWIGLU) return E2TTT_ERR_UNSUPPORTED;
   if (d.io != E2TTT_DT_F32 && d.io != E2TTT_DT_BF16) return E2TTT_ERR_UNSUPPORTED;
-  if (d.flags & ~E2TTT_FLAG_NO_RESIDUAL_LN) return E2TTT_ERR_UNSUPPORTED;
+  if (d.flags & ~(E2TTT_FLAG_NO_RESIDUAL_LN | E2TTT_FLAG_CHUNK_AVERAGED))
+    return E2TTT_ERR_UNSUPPORTED;
   if (!(d.flags & E2TTT_FLAG_NO_RESIDUAL_LN) && !(d.ln_eps > 0.0f)) return E2TTT_ERR_BAD_SHAPE;
   if (d.chunk > 64) return E2TTT_ERR_UNSUPPORTED;
   const long U = (long)d.B * d.H;
@@ -110,6 +111,8 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
       align_up((size_t)pl.npairs * 2 * chain_xchg_floats(pl.cfg, true) * sizeof(float));
   return E2TTT_OK;
 }
+
+int averaged(const e2ttt_desc* d) { return (d->flags & E2TTT_FLAG_CHUNK_AVERAGED) ? 1 : 0; }
 
 e2ttt_status hip_status(hipError_t e) { return e == hipSuccess ? E2TTT_OK : E2TTT_ERR_HIP; }
 
@@ -217,7 +220,7 @@ e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const 
   if (st != E2TTT_OK) return st;
   if (!eta || !beta || !kw || !km || !carry) return E2TTT_ERR_NULL_ARG;
   CoeffFwdArgs c{eta, beta, gamma, kw, km, carry, (int)pl.T, desc->chunk, (int)pl.NC,
-                 pl.U * pl.NC, nullptr, 0};
+                 pl.U * pl.NC, nullptr, 0, averaged(desc)};
   hipStream_t s = static_cast<hipStream_t>(stream);
   return finish(launch_coeff_fwd(c, s), s);
 }
@@ -264,7 +267,7 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   const long np = pl.cfg.ns > 1 ? launch_pairs(pl, false) : 0;
   if (pl.cfg.ns > 1 && np < 8) return E2TTT_ERR_UNSUPPORTED;
   CoeffFwdArgs c{eta, beta, gamma, kw, km, carry, (int)pl.T, desc->chunk, (int)pl.NC,
-                 pl.U * pl.NC, sync, sync ? sync_words(np) : 0};
+                 pl.U * pl.NC, sync, sync ? sync_words(np) : 0, averaged(desc)};
   hipError_t e = launch_coeff_fwd(c, s);
   if (e != hipSuccess) return E2TTT_ERR_HIP;
   ChainArgs a{};
@@ -345,7 +348,7 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   if (e != hipSuccess) return E2TTT_ERR_HIP;
   CoeffBwdArgs cb{eta, beta, gamma, a.kwb, a.kmb, a.carryb, d_eta, d_beta, d_gamma,
                   (int)pl.T, desc->chunk, (int)pl.NC, pl.U * pl.NC, pl.cfg.ns,
-                  pl.U * pl.T, pl.U * pl.NC * 3};
+                  pl.U * pl.T, pl.U * pl.NC * 3, averaged(desc)};
   return finish(launch_coeff_bwd(cb, s), s, sync);
 }
 

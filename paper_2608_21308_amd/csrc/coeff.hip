@@ -12,6 +12,11 @@
 // to zero is the exact limit) and S_t by an affine wave scan, which never
 // divides and stays finite for beta -> 0 where the ratio form is 0/0.
 //
+// Chunk-averaged rule (the ablation baseline, eqs. (4)-(5) with mean factors):
+//   K^W_t = K^M_t = eta_t,  carry = (mean gamma, mean beta, mean beta),
+// with the backward  d eta_t = dK^W_t + dK^M_t,  d beta_t = (dcm + dcb) / L,
+// d gamma_t = dcw / L.
+//
 // One wave64 handles one (unit, chunk); lane tau holds token t = tau + 1.
 #include <hip/hip_runtime.h>
 
@@ -77,6 +82,13 @@ __device__ __forceinline__ float affine_scan_up(float a, float b, int lane) {
   return a;
 }
 
+// Sum over the wave (butterfly, the same order on every lane).
+__device__ __forceinline__ float wave_total(float v) {
+#pragma unroll
+  for (int k = 32; k >= 1; k >>= 1) v += __shfl_xor(v, k, 64);
+  return v;
+}
+
 __global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
   // the chain kernel that follows on this stream starts from cleared sync words
   for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < a.nzero; i += (long)gridDim.x * 256)
@@ -89,6 +101,23 @@ __global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
   const int s0 = r * a.C;
   const int len = min(a.C, a.T - s0);
   const long base = u * a.T + s0;
+  if (a.averaged) {
+    const bool valid = lane < len;
+    const float e = valid ? a.eta[base + lane] : 0.0f;
+    const float bsum = wave_total(valid ? a.beta[base + lane] : 0.0f);
+    const float gsum = wave_total(valid ? (a.gamma ? a.gamma[base + lane] : 1.0f) : 0.0f);
+    const float inv = 1.0f / (float)len;
+    if (valid) {
+      a.kw[base + lane] = e;
+      a.km[base + lane] = e;
+    }
+    if (lane == 0) {
+      a.carry[wid * 3 + 0] = gsum * inv;
+      a.carry[wid * 3 + 1] = bsum * inv;
+      a.carry[wid * 3 + 2] = bsum * inv;
+    }
+    return;
+  }
   ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);
   if (lane < len) {
     a.kw[base + lane] = s.e * s.S;
@@ -116,7 +145,6 @@ __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
   const int len = min(a.C, a.T - s0);
   const long base = u * a.T + s0;
   const bool valid = lane < len;
-  ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);
   // the chain kernel leaves one partial per workgroup of a unit; sum them
   float kwb = 0.0f, kmb = 0.0f, cwb = 0.0f, cmb = 0.0f, cbb = 0.0f;
   for (int sl = 0; sl < a.ns; ++sl) {
@@ -128,6 +156,16 @@ __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
     cmb += a.carryb[sl * a.chk_slot + wid * 3 + 1];
     cbb += a.carryb[sl * a.chk_slot + wid * 3 + 2];
   }
+  if (a.averaged) {
+    const float inv = 1.0f / (float)len;
+    if (valid) {
+      a.d_eta[base + lane] = kwb + kmb;
+      a.d_beta[base + lane] = (cmb + cbb) * inv;
+      if (a.d_gamma) a.d_gamma[base + lane] = cwb * inv;
+    }
+    return;
+  }
+  ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);
 
   const float etab = kwb * s.S + kmb * s.bt;
   // S-bar and the direct beta_1 term of carry_m = beta_1 S_1

@@ -18,6 +18,7 @@ struct CoeffFwdArgs {
   long nwork;           // U * NC
   unsigned* zero;       // nullable: words cleared by this kernel (pair sync words)
   long nzero;
+  int averaged;         // 1: chunk-averaged rule (K^W = K^M = eta, mean beta / gamma carries)
 };
 
 struct CoeffBwdArgs {
@@ -35,6 +36,7 @@ struct CoeffBwdArgs {
   int ns;               // partial slots of kwb, kmb, carryb (one per workgroup of a unit)
   long tok_slot;        // elements between slots of kwb / kmb (U T)
   long chk_slot;        // elements between slots of carryb (U NC 3)
+  int averaged;         // as CoeffFwdArgs::averaged
 };
 
 // Chain kernels: one or two workgroups per (batch, head) unit, looping over chunks.

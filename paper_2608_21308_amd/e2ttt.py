@@ -21,6 +21,7 @@ FW_SWIGLU = 1
 DT_F32 = 0
 DT_BF16 = 1
 FLAG_NO_RESIDUAL_LN = 1
+FLAG_CHUNK_AVERAGED = 2
 
 STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
           4: "workspace too small", 5: "HIP error", 6: "device-side wait expired"}
