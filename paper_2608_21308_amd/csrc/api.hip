@@ -15,8 +15,8 @@ namespace {
 using namespace e2ttt;
 
 constexpr size_t kAlign = 256;
-// Upper bound on workgroup pairs of one cooperative launch (256 CUs, one
-// chain workgroup per CU); more units are taken in turn by the same pairs.
+// Upper bound on workgroup groups (two or three workgroups sharing a unit) of
+// one cooperative launch; more units are taken in turn by the same groups.
 constexpr long kMaxPairs = 128;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -24,7 +24,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Plan {
   long U = 0, T = 0, NC = 0, P = 0;
   ChainConfig cfg{};
-  long npairs = 0;        // pairs the exchange buffers are sized for (two workgroups per unit)
+  long npairs = 0;        // groups the exchange buffers are sized for (ns workgroups per unit)
   // forward workspace
   size_t off_kw = 0, off_km = 0, off_carry = 0, off_sync = 0, off_xbuf = 0, ws_bytes = 0;
   size_t off_ckpt = 0, off_zk = 0, off_rk = 0, off_zq = 0, off_rq = 0, ws_bytes_save = 0;
@@ -46,9 +46,13 @@ e2ttt_status select_config(const e2ttt_desc& d, ChainConfig& cfg) {
     if (d.d != 64) return E2TTT_ERR_UNSUPPORTED;
     cfg.ntb = 4;
     if (nblk <= 4) { cfg.nw = 4; cfg.njb = 1; }
-    else if (nblk <= 8) { cfg.nw = 8; cfg.njb = 1; }
+    else if (d.fw == E2TTT_FW_GELU_MLP && nblk <= 8) { cfg.nw = 8; cfg.njb = 1; }
     else if (d.fw == E2TTT_FW_GELU_MLP && nblk <= 16) { cfg.nw = 8; cfg.njb = 1; cfg.ns = 2; }
-    else if (d.fw == E2TTT_FW_SWIGLU && nblk <= 11) { cfg.nw = 11; cfg.njb = 1; }
+    // SwiGLU keeps three matrices of state per wave: one wave per SIMD (four
+    // waves per workgroup) holds them without spilling, so wider nets spread
+    // over two or three workgroups of 64 hidden columns each
+    else if (d.fw == E2TTT_FW_SWIGLU && nblk <= 8) { cfg.nw = 4; cfg.njb = 1; cfg.ns = 2; }
+    else if (d.fw == E2TTT_FW_SWIGLU && nblk <= 12) { cfg.nw = 4; cfg.njb = 1; cfg.ns = 3; }
     else return E2TTT_ERR_UNSUPPORTED;
   } else {
     if (d.d != 16) return E2TTT_ERR_UNSUPPORTED;
@@ -83,14 +87,14 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   const size_t chk = (size_t)U * pl.NC * 3 * sizeof(float);
   const long ns = pl.cfg.ns;
   pl.npairs = (ns > 1) ? std::min((U + 7) / 8 * 8, kMaxPairs) : 0;
-  const size_t sync_b = (ns > 1) ? (size_t)sync_words(pl.npairs) * sizeof(unsigned) : 0;
+  const size_t sync_b = (ns > 1) ? (size_t)sync_words(pl.npairs, (int)ns) * sizeof(unsigned) : 0;
   pl.off_kw = 0;
   pl.off_km = align_up(tok);
   pl.off_carry = pl.off_km + align_up(tok);
   pl.off_sync = pl.off_carry + align_up(chk);
   pl.off_xbuf = pl.off_sync + align_up(sync_b);
   pl.off_ckpt = pl.off_xbuf +
-                align_up((size_t)pl.npairs * 2 * chain_xchg_floats(pl.cfg, false) * sizeof(float));
+                align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, false) * sizeof(float));
   pl.ws_bytes = pl.off_ckpt;
   pl.ckpt_stride = chain_ckpt_bytes(pl.cfg);
   const size_t tokd = tok * d.d;
@@ -108,7 +112,7 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_bxbuf = pl.off_bsync + align_up(sync_b);
   pl.scratch_bytes =
       pl.off_bxbuf +
-      align_up((size_t)pl.npairs * 2 * chain_xchg_floats(pl.cfg, true) * sizeof(float));
+      align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, true) * sizeof(float));
   return E2TTT_OK;
 }
 
@@ -160,7 +164,7 @@ long chain_max_pairs(const ChainConfig& cfg, bool backward) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return 0;
   const int nb = backward ? chain_bwd_blocks_per_cu(cfg) : chain_fwd_blocks_per_cu(cfg);
-  return ((long)nb * cus / 2) / 8 * 8;
+  return ((long)nb * cus / (cfg.ns > 1 ? cfg.ns : 1)) / 8 * 8;
 }
 
 long chain_xchg_floats(const ChainConfig& cfg, bool backward) {
@@ -267,7 +271,7 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   const long np = pl.cfg.ns > 1 ? launch_pairs(pl, false) : 0;
   if (pl.cfg.ns > 1 && np < 8) return E2TTT_ERR_UNSUPPORTED;
   CoeffFwdArgs c{eta, beta, gamma, kw, km, carry, (int)pl.T, desc->chunk, (int)pl.NC,
-                 pl.U * pl.NC, sync, sync ? sync_words(np) : 0, averaged(desc)};
+                 pl.U * pl.NC, sync, sync ? sync_words(np, pl.cfg.ns) : 0, averaged(desc)};
   hipError_t e = launch_coeff_fwd(c, s);
   if (e != hipSuccess) return E2TTT_ERR_HIP;
   ChainArgs a{};
@@ -316,7 +320,8 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   unsigned* sync = pl.cfg.ns > 1 ? at<unsigned>(scratch, pl.off_bsync) : nullptr;
   const long np = pl.cfg.ns > 1 ? launch_pairs(pl, true) : 0;
   if (pl.cfg.ns > 1 && np < 8) return E2TTT_ERR_UNSUPPORTED;
-  if (sync && launch_zero_words(sync, sync_words(np), s) != hipSuccess) return E2TTT_ERR_HIP;
+  if (sync && launch_zero_words(sync, sync_words(np, pl.cfg.ns), s) != hipSuccess)
+    return E2TTT_ERR_HIP;
   ChainArgs a{};
   a.U = pl.U;
   a.q = q; a.k = k; a.v = v;

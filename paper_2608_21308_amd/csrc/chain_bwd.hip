@@ -307,34 +307,39 @@ __device__ __forceinline__ void jacc_store_f32(const JAcc<S>& out, float* dst, F
 // Exchange slot of one rank for one parity: [dYh | dk | dq] partials, CM x D floats each.
 template <class S>
 __device__ __forceinline__ float* bwd_slot(float* xbuf, long p, int rank, int parity) {
-  return xbuf + (((p * 2 + rank) * 2 + parity) * 3L) * S::CM * S::D;
+  return xbuf + (((p * S::NS + rank) * 2 + parity) * 3L) * S::CM * S::D;
 }
 
-// dk and dq of one chunk from the two ranks' partials (rank 0's carries the
-// -eh and dO terms), rows [rlo, rlo + RPW) below len.
+// dk and dq of one chunk from the ranks' partials, added in rank order (rank
+// 0's carries the -eh and dO terms), rows [rlo, min(CM, rlo + RPW)) below len.
 template <class S>
 __device__ __forceinline__ void flush_dkdq(const ChainArgs& a, long p, int parity, long row0,
                                            int len, int rlo, int tid) {
   using IO = IoT<S::BF>;
-  constexpr int RPW = S::CM / S::NS;
+  constexpr int RPW = row_share<S>();
   constexpr int NV = RPW * S::D / 4;
-  const float* s0 = bwd_slot<S>(a.xbuf, p, 0, parity);
-  const float* s1 = bwd_slot<S>(a.xbuf, p, 1, parity);
+  const int tend = min(len, min(S::CM, rlo + RPW));
   typename IO::T* dk = reinterpret_cast<typename IO::T*>(a.dk) + row0 * S::D;
   typename IO::T* dq = reinterpret_cast<typename IO::T*>(a.dq) + row0 * S::D;
 #pragma unroll 1
   for (int v = tid; v < NV; v += S::NT) {
     const int e = rlo * S::D + 4 * v, t = e / S::D;
-    if (t >= len) continue;
+    if (t >= tend) continue;
 #pragma unroll
     for (int sec = 1; sec <= 2; ++sec) {
-      const float4 x = *reinterpret_cast<const float4*>(s0 + sec * S::CM * S::D + e);
-      const float4 y = *reinterpret_cast<const float4*>(s1 + sec * S::CM * S::D + e);
+      float4 x = *reinterpret_cast<const float4*>(bwd_slot<S>(a.xbuf, p, 0, parity) +
+                                                  sec * S::CM * S::D + e);
+#pragma unroll
+      for (int rk = 1; rk < S::NS; ++rk) {
+        const float4 y = *reinterpret_cast<const float4*>(bwd_slot<S>(a.xbuf, p, rk, parity) +
+                                                          sec * S::CM * S::D + e);
+        x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+      }
       typename IO::T* d = (sec == 1) ? dk : dq;
-      IO::st(d + e + 0, x.x + y.x);
-      IO::st(d + e + 1, x.y + y.y);
-      IO::st(d + e + 2, x.z + y.z);
-      IO::st(d + e + 3, x.w + y.w);
+      IO::st(d + e + 0, x.x);
+      IO::st(d + e + 1, x.y);
+      IO::st(d + e + 2, x.z);
+      IO::st(d + e + 3, x.w);
     }
   }
 }
@@ -350,7 +355,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   constexpr int NF = NMAT - 1;       // number of first-layer matrices
   constexpr bool SW = S::FW == 1;
   constexpr int EPL = D / 16;        // head elements per lane in row phases
-  constexpr int RPW = S::CM / S::NS; // rows of dv, dk, dq written by one rank
+  constexpr int RPW = row_share<S>(); // rows of dv, dk, dq written by one rank (last: fewer)
+  constexpr int NPEER = S::NS - 1;
   __shared__ __attribute__((aligned(16))) unsigned char smem[L::TOTAL];
   __shared__ int sword[2];
   E* xk = reinterpret_cast<E*>(smem + L::XK);
@@ -380,6 +386,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   const int j0 = rank * S::DHP;
   const long NP = (S::NS > 1) ? a.npairs : (long)gridDim.x;
   const int rlo = rank * RPW;
+  const int rhi = min(S::CM, rlo + RPW);
   float* const kwb_slot = a.kwb + rank * a.U * T;
   float* const kmb_slot = a.kmb + rank * a.U * T;
   float* const carryb_slot = a.carryb + rank * a.U * NC * 3;
@@ -726,9 +733,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         jacc_store_f32<S>(dyhacc, dyh, [](int, int) { return 0.0f; }, w, g, c);
       }
       __syncthreads();
-      const float* dyh_peer = nullptr;
       constexpr int P7IT = (S::CM + 4 * NW - 1) / (4 * NW);
-      float pdyh[S::NS > 1 ? P7IT : 1][EPL];
+      float pdyh[S::NS > 1 ? P7IT : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
         E2TTT_LANE_IDS;
         float* mine = bwd_slot<S>(a.xbuf, px.p, rank, par);
@@ -736,14 +742,18 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         for (int v = tid; v < S::CM * D / 4; v += S::NT)
           reinterpret_cast<float4*>(mine)[v] = reinterpret_cast<const float4*>(dyh)[v];
         px.post();                                  // seq0 + 1: dYh partial
-        px.wait_for(seq0 + 1, sword);               // the peer's
-        dyh_peer = bwd_slot<S>(a.xbuf, px.p, 1 - rank, par);
-        // the peer's rows of every P7 step, loaded before the global stores
+        px.wait_for(seq0 + 1, sword);               // the peers'
+        // the peers' rows of every P7 step, loaded before the global stores
         // below (which would otherwise order each step's loads after them)
 #pragma unroll
-        for (int it_ = 0; it_ < P7IT; ++it_) {
-          const int t0 = 4 * w + it_ * 4 * NW;
-          if (t0 < S::CM) load_row_part<EPL>(pdyh[it_], dyh_peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+        for (int k = 0; k < NPEER; ++k) {
+          const float* dyh_peer = bwd_slot<S>(a.xbuf, px.p, other_rank(k, rank), par);
+#pragma unroll
+          for (int it_ = 0; it_ < P7IT; ++it_) {
+            const int t0 = 4 * w + it_ * 4 * NW;
+            if (t0 < S::CM)
+              load_row_part<EPL>(pdyh[it_][k], dyh_peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+          }
         }
         if (pend_r >= 0)
           flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
@@ -769,7 +779,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           }
           if constexpr (S::NS > 1) {
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) dyhv[q] += pdyh[it_][q];
+            for (int q = 0; q < EPL; ++q) {
+              float pv[NPEER];
+#pragma unroll
+              for (int k = 0; k < NPEER; ++k) pv[k] = pdyh[it_][k][q];
+              dyhv[q] = sum_ranks<S::NS>(dyhv[q], pv, rank);
+            }
           }
           if (resln) {
             float z[EPL], dyv[EPL], zh[EPL];
@@ -814,7 +829,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             ek[t * D + i] = eh[q];
             yh[t * S::LDD + i] = O::to_e(yhv[q]);
             yht[it_idx<S>(i, t)] = O::to_e(yhv[q]);
-            if (t < len && t >= rlo && t < rlo + RPW) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
+            if (t < len && t >= rlo && t < rhi) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
           }
                   }
         }
@@ -1105,7 +1120,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 
     if constexpr (S::NS > 1) {
       E2TTT_LANE_IDS;
-      px.wait_for(px.seq_now(), sword);             // the peer's last post
+      px.wait_for(px.seq_now(), sword);             // the peers' last post
       if (pend_r >= 0)
         flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
                       tid);
@@ -1140,7 +1155,7 @@ hipError_t launch(const ChainArgs& a, hipStream_t stream) {
     ChainArgs b = a;
     void* args[] = {&b};
     return hipLaunchCooperativeKernel((const void*)chain_bwd_kernel<S>,
-                                      dim3((unsigned)(2 * a.npairs)), dim3(S::NT), args, 0,
+                                      dim3((unsigned)(S::NS * a.npairs)), dim3(S::NT), args, 0,
                                       stream);
   }
 }

@@ -50,6 +50,14 @@ struct Shape {
   static_assert(CM % KC == 0, "chunk tile must be a multiple of the K-step");
 };
 
+// Token rows of a chunk tile whose outputs one of the NS ranks of a unit
+// writes: rows [rank R, min(CM, (rank + 1) R)), R a multiple of four so that
+// the four-row steps of the row phases never straddle two ranks.
+template <class S>
+__host__ __device__ constexpr int row_share() {
+  return ((S::CM + S::NS - 1) / S::NS + 3) / 4 * 4;
+}
+
 // State tiles of one wave: T[m][jj][ib] is the tile (rows i = 16 ib + 4 g + r,
 // column j = j0 + 16 (w NJB + jj) + c, j0 = rank DHP) of matrix m.
 template <class S>

@@ -12,12 +12,12 @@
 //   O  = Q + LN(act(Q W1^T) W2^T)     outputs from the chunk-start weights (a7)
 // The new state stays in registers for the next chunk (a8).
 //
-// With two workgroups per unit (pair_xchg.h) each holds half of the hidden
-// columns; the j-contractions Y_K and Y_Q then give partial sums that the two
+// With NS workgroups per unit (pair_xchg.h) each holds a share of the hidden
+// columns; the j-contractions Y_K and Y_Q then give partial sums that the
 // ranks swap.  The Q-side first layer and Y_Q run between posting the Y_K
-// partial and waiting for the peer's, so the exchange overlaps that work; the
-// Y_Q swap is waited for only at the end of the chunk.  Both ranks form the
-// same sums (fp32 addition commutes), so they see bitwise identical Y_K and dY.
+// partial and waiting for the peers', so the exchange overlaps that work; the
+// Y_Q swap is waited for only at the end of the chunk.  Every rank adds the
+// partials in rank order, so all see bitwise identical Y_K and dY.
 #include "chain_common.h"
 #include "pair_xchg.h"
 
@@ -60,7 +60,7 @@ struct FwdSmem {
 // Exchange slot of one rank for one parity: [Y_K | Y_Q], CM x D floats each.
 template <class S>
 __device__ __forceinline__ float* fwd_slot(float* xbuf, long p, int rank, int parity) {
-  return xbuf + (((p * 2 + rank) * 2 + parity) * 2L) * S::CM * S::D;
+  return xbuf + (((p * S::NS + rank) * 2 + parity) * 2L) * S::CM * S::D;
 }
 
 template <class S>
@@ -74,7 +74,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // share them); the wider SwiGLU state re-forms them per use instead
   constexpr bool PRESPLIT = S::BF && S::FW == 0;
   constexpr int EPL = D / 16;    // head elements per lane in the row phases
-  constexpr int RPW = S::CM / S::NS;   // output rows written by one rank
+  constexpr int RPW = row_share<S>();  // output rows written by one rank (last: fewer)
+  constexpr int NPEER = S::NS - 1;
   __shared__ FwdSmem<S> sm;
   static_assert(sizeof(FwdSmem<S>) <= 160 * 1024, "LDS budget");
 
@@ -88,6 +89,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   const int j0 = rank * S::DHP;
   const long NP = (S::NS > 1) ? a.npairs : (long)gridDim.x;
   const int rlo = rank * RPW;
+  const int rhi = min(S::CM, rlo + RPW);
   long nch = 0;   // chunks processed by this workgroup (exchange parity)
 
   // hidden columns [DHP, DHK) of the j-operands stay zero for the whole run
@@ -281,15 +283,19 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // which also completes the Q-side activations) lets the loads of its
       // rows for every LN step run under the Y_Q contraction.
       constexpr int NIT = (S::CM + 4 * S::NW - 1) / (4 * S::NW);
-      float pyv[S::NS > 1 ? NIT : 1][EPL];
+      float pyv[S::NS > 1 ? NIT : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
-        px.wait_for(seq0 + 1, sm.word);                   // peer's Y_K
+        px.wait_for(seq0 + 1, sm.word);                   // peers' Y_K
         E2TTT_LANE_IDS;
-        const float* peer = fwd_slot<S>(a.xbuf, px.p, 1 - rank, par);
 #pragma unroll
-        for (int it_ = 0; it_ < NIT; ++it_) {
-          const int t0 = 4 * w + it_ * 4 * S::NW;
-          if (t0 < S::CM) load_row_part<EPL>(pyv[it_], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+        for (int k = 0; k < NPEER; ++k) {
+          const float* peer = fwd_slot<S>(a.xbuf, px.p, other_rank(k, rank), par);
+#pragma unroll
+          for (int it_ = 0; it_ < NIT; ++it_) {
+            const int t0 = 4 * w + it_ * 4 * S::NW;
+            if (t0 < S::CM)
+              load_row_part<EPL>(pyv[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+          }
         }
       } else {
         __syncthreads();
@@ -321,7 +327,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       const float cw = sm.carry[0], cm = sm.carry[1], cbv = sm.carry[2];
       {
         E2TTT_LANE_IDS;
-        // this lane's rows of the rows [rlo, rlo + RPW), kept for the backward,
+        // this lane's rows of the rows [rlo, rhi), kept for the backward,
         // are written after the loop, so that no global store sits between
         // the peer's rows and their use
         float zsave[NIT][EPL], rsave[NIT];
@@ -337,7 +343,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) yv[q] = sm.y[t * D + l16 * EPL + q];
           if constexpr (S::NS > 1) {
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) yv[q] += pyv[it_][q];
+            for (int q = 0; q < EPL; ++q) {
+              float pv[NPEER];
+#pragma unroll
+              for (int k = 0; k < NPEER; ++k) pv[k] = pyv[it_][k][q];
+              yv[q] = sum_ranks<S::NS>(yv[q], pv, rank);
+            }
           }
 #pragma unroll
           for (int q = 0; q < EPL; ++q) s1 += yv[q];
@@ -366,7 +377,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
               dyv[q] = O::from_e(sm.xv[t * S::LDD + l16 * EPL + q]) - yv[q];
             }
           }
-          keep[it_] = t >= rlo && t < rlo + RPW && t < len;
+          keep[it_] = t >= rlo && t < rhi && t < len;
 #pragma unroll
           for (int q = 0; q < EPL; ++q) zsave[it_][q] = z[q];
           rsave[it_] = sig;
@@ -396,15 +407,19 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // barrier that ends the LN phase) and load its rows of the outputs, so
       // that they arrive under dA and the state update.
       constexpr int NITO = (RPW + 4 * S::NW - 1) / (4 * S::NW);
-      float pyq[S::NS > 1 ? NITO : 1][EPL];
+      float pyq[S::NS > 1 ? NITO : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
-        px.wait_for(seq0 + 2, sm.word);                   // peer's Y_Q
+        px.wait_for(seq0 + 2, sm.word);                   // peers' Y_Q
         E2TTT_LANE_IDS;
-        const float* peer = fwd_slot<S>(a.xbuf, px.p, 1 - rank, par) + S::CM * D;
 #pragma unroll
-        for (int it_ = 0; it_ < NITO; ++it_) {
-          const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
-          if (t0 < rlo + RPW) load_row_part<EPL>(pyq[it_], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+        for (int k = 0; k < NPEER; ++k) {
+          const float* peer = fwd_slot<S>(a.xbuf, px.p, other_rank(k, rank), par) + S::CM * D;
+#pragma unroll
+          for (int it_ = 0; it_ < NITO; ++it_) {
+            const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
+            if (t0 < rhi)
+              load_row_part<EPL>(pyq[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+          }
         }
       } else {
         __syncthreads();
@@ -512,7 +527,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
         for (int it_ = 0; it_ < NITO; ++it_) {
           const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
-          if (t0 < rlo + RPW) {
+          if (t0 < rhi) {
           const int t = t0 + (lane >> 4);
           float yv[EPL], f[EPL];
           float s1 = 0.0f, sig = 1.0f;
@@ -520,7 +535,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) yv[q] = sm.yq[t * D + l16 * EPL + q];
           if constexpr (S::NS > 1) {
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) yv[q] += pyq[it_][q];
+            for (int q = 0; q < EPL; ++q) {
+              float pv[NPEER];
+#pragma unroll
+              for (int k = 0; k < NPEER; ++k) pv[k] = pyq[it_][k][q];
+              yv[q] = sum_ranks<S::NS>(yv[q], pv, rank);
+            }
           }
 #pragma unroll
           for (int q = 0; q < EPL; ++q) s1 += yv[q];
@@ -583,7 +603,7 @@ hipError_t launch(const ChainArgs& a, hipStream_t stream) {
     ChainArgs b = a;
     void* args[] = {&b};
     return hipLaunchCooperativeKernel((const void*)chain_fwd_kernel<S>,
-                                      dim3((unsigned)(2 * a.npairs)), dim3(S::NT), args, 0,
+                                      dim3((unsigned)(S::NS * a.npairs)), dim3(S::NT), args, 0,
                                       stream);
   }
 }

@@ -1,35 +1,36 @@
-// Two workgroups per unit: exchange of partial sums through global memory.
+// Several workgroups per unit: exchange of partial sums through global memory.
 //
 // For the widest fast-weight nets one unit's hidden columns are split between
-// two workgroups (ranks 0 and 1 of a pair), each holding its half of the state
-// in registers.  Contractions over the hidden index then give each rank a
-// partial C x d sum that the other rank needs; the ranks swap these through a
-// small global buffer and a flag per rank.
+// NS workgroups (NS = 2 or 3; ranks 0 .. NS-1 of a group), each holding its
+// share of the state in registers.  Contractions over the hidden index then
+// give each rank a partial C x d sum that the others need; the ranks swap
+// these through a small global buffer and a flag per rank.  Every rank adds
+// the NS partials in rank order, so all ranks see bitwise identical sums.
 //
 // Placement.  Workgroups are dispatched to the eight XCDs round-robin by
-// workgroup id, so the pair p is given ids 16 (p / 8) + p % 8 and that + 8:
-// both land on XCD p % 8 and share its L2.  On a shared L2 a post is: plain
-// stores of the data, s_waitcnt vmcnt(0) (the stores have reached L2, the L1
-// being write-through), a workgroup barrier, then a device-scope store of the
-// flag; the wait is: a device-scope poll of the peer's flag, a barrier, then an
-// invalidation of this CU's L1 (buffer_inv sc0) before plain loads of the
-// peer's data.  At kernel start the ranks swap their hardware XCC ids with
-// device-scope accesses; if they differ (another dispatch order), every post
-// and wait of that pair uses agent-scope release / acquire fences instead,
-// which are coherent across XCDs but write back and invalidate the L2.
+// workgroup id, so rank r of group p is given id 8 NS (p / 8) + p % 8 + 8 r:
+// all ranks land on XCD p % 8 and share its L2.  On a shared L2 a post is:
+// plain stores of the data, s_waitcnt vmcnt(0) (the stores have reached L2,
+// the L1 being write-through), a workgroup barrier, then a device-scope store
+// of the flag; the wait is: a device-scope poll of the peers' flags, a
+// barrier, then an invalidation of this CU's L1 (buffer_inv sc0) before plain
+// loads of the peers' data.  At kernel start the ranks swap their hardware XCC
+// ids with device-scope accesses; if they differ (another dispatch order),
+// every post and wait of that group uses agent-scope release / acquire fences
+// instead, which are coherent across XCDs but write back and invalidate the L2.
 //
 // Every wait is bounded (kTimeoutTicks of the 100 MHz real-time counter).  A
 // rank whose wait expires sets the status word, poisons its own flag so that
-// the peer stops waiting too, and skips all later waits, so the grid always
+// the others stop waiting too, and skips all later waits, so the grid always
 // drains; the results of that launch are then undefined and the status word
-// reports it.  The kernels are launched cooperatively, so both ranks of a pair
+// reports it.  The kernels are launched cooperatively, so all ranks of a group
 // are resident at the same time.
 //
 // Sync words (uint32, one 256-byte line each, zeroed by the kernel that runs
-// before the chain kernel on the same stream):
-//   line 0                    status (0 ok, 1 a wait expired)
-//   line 1 + 2 p + r          flag of rank r of pair p (last posted sequence number)
-//   line 1 + 2 NP + 2 p + r   hardware XCC id + 1 of rank r of pair p
+// before the chain kernel on the same stream), for NG groups:
+//   line 0                        status (0 ok, 1 a wait expired)
+//   line 1 + NS p + r             flag of rank r of group p (last posted sequence number)
+//   line 1 + NS NG + NS p + r     hardware XCC id + 1 of rank r of group p
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -40,7 +41,9 @@ constexpr int kSyncLine = 64;                       // uint32 words per line
 constexpr long long kTimeoutTicks = 200000000LL;    // 2 s of the 100 MHz counter
 constexpr unsigned kPoison = 0xFFFFFFFFu;
 
-__host__ __device__ constexpr long sync_words(long npairs) { return kSyncLine * (1 + 4 * npairs); }
+__host__ __device__ constexpr long sync_words(long ngroups, int ns) {
+  return kSyncLine * (1 + 2L * ns * ngroups);
+}
 
 __device__ __forceinline__ unsigned ld_dev(const unsigned* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -54,10 +57,30 @@ __device__ __forceinline__ int hw_xcc_id() {
   return v & 0xf;
 }
 
-// Pair index and rank of this workgroup for a launch of 2 NP workgroups.
-__device__ __forceinline__ void pair_of_block(int b, long& p, int& rank) {
-  rank = (b >> 3) & 1;
-  p = (long)(b >> 4) * 8 + (b & 7);
+// Group index and rank of workgroup b in a launch of NS NG workgroups.
+template <int NS>
+__device__ __forceinline__ void group_of_block(int b, long& p, int& rank) {
+  rank = (b >> 3) % NS;
+  p = (long)(b / (8 * NS)) * 8 + (b & 7);
+}
+
+// The k-th rank other than `rank`, in increasing order (k < NS - 1).
+__device__ __forceinline__ int other_rank(int k, int rank) { return k < rank ? k : k + 1; }
+
+// Sum of the NS partials of one value in rank order: `own` is this rank's,
+// peer[k] that of other_rank(k, rank).  Every array index is a compile-time
+// constant (the rank only selects), so the partials stay in registers.
+template <int NS>
+__device__ __forceinline__ float sum_ranks(float own, const float (&peer)[NS - 1], int rank) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int r = 0; r < NS; ++r) {
+    const float below = peer[r > 0 ? r - 1 : 0];       // rank r when r > rank
+    const float above = peer[r < NS - 1 ? r : 0];      // rank r when r < rank
+    const float v = (r == rank) ? own : ((r < rank) ? above : below);
+    acc = (r == 0) ? v : acc + v;
+  }
+  return acc;
 }
 
 template <int NS> struct PairX;
@@ -72,35 +95,44 @@ template <> struct PairX<1> {
   __device__ unsigned seq_now() const { return 0; }
 };
 
-template <> struct PairX<2> {
+template <int NS> struct PairX {
+  static_assert(NS >= 2 && NS <= 4, "two to four workgroups per unit");
   int rank = 0;
   long p = 0;
   unsigned* mine = nullptr;
-  const unsigned* peer = nullptr;
+  const unsigned* peer[NS - 1] = {};
   unsigned* status = nullptr;
   unsigned seq = 0;
   bool same_xcc = true;
   bool dead = false;
 
   // s_word: two ints of LDS for broadcasting thread 0's findings
-  __device__ void init(unsigned* sync, long npairs, int* s_word) {
-    pair_of_block(blockIdx.x, p, rank);
+  __device__ void init(unsigned* sync, long ngroups, int* s_word) {
+    group_of_block<NS>(blockIdx.x, p, rank);
     status = sync;
-    mine = sync + kSyncLine * (1 + 2 * p + rank);
-    peer = sync + kSyncLine * (1 + 2 * p + (1 - rank));
-    unsigned* xm = sync + kSyncLine * (1 + 2 * npairs + 2 * p + rank);
-    const unsigned* xp = sync + kSyncLine * (1 + 2 * npairs + 2 * p + (1 - rank));
+    mine = sync + kSyncLine * (1 + NS * p + rank);
+#pragma unroll
+    for (int k = 0; k < NS - 1; ++k)
+      peer[k] = sync + kSyncLine * (1 + NS * p + other_rank(k, rank));
     if (threadIdx.x == 0) {
+      unsigned* xm = sync + kSyncLine * (1 + NS * ngroups + NS * p + rank);
       const unsigned id = (unsigned)hw_xcc_id() + 1u;
       st_dev(xm, id);
       const long long t0 = __builtin_amdgcn_s_memrealtime();
-      unsigned o = 0;
-      while ((o = ld_dev(xp)) == 0u) {
-        if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) break;
+      int same = 1, alive = 1;
+#pragma unroll
+      for (int k = 0; k < NS - 1; ++k) {
+        const unsigned* xp = sync + kSyncLine * (1 + NS * ngroups + NS * p + other_rank(k, rank));
+        unsigned o = 0;
+        while ((o = ld_dev(xp)) == 0u) {
+          if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) break;
+        }
+        if (o != id) same = 0;
+        if (o == 0u) alive = 0;
       }
-      s_word[0] = (o == id) ? 1 : 0;
-      s_word[1] = (o != 0u) ? 1 : 0;
-      if (o == 0u) { st_dev(status, 1u); st_dev(mine, kPoison); }
+      s_word[0] = same;
+      s_word[1] = alive;
+      if (!alive) { st_dev(status, 1u); st_dev(mine, kPoison); }
     }
     __syncthreads();
     same_xcc = s_word[0] != 0;
@@ -121,19 +153,24 @@ template <> struct PairX<2> {
 
   __device__ unsigned seq_now() const { return seq; }
 
-  // Wait until the peer has posted at least `target`.  All threads call; the
-  // caller has passed a workgroup barrier since the previous call.  The call
-  // is always a workgroup barrier (also once the pair is dead).
+  // Wait until every other rank has posted at least `target`.  All threads
+  // call; the caller has passed a workgroup barrier since the previous call.
+  // The call is always a workgroup barrier (also once the group is dead).
   __device__ void wait_for(unsigned target, int* s_word) {
     const bool was_dead = dead;   // uniform over the workgroup
     if (threadIdx.x == 0 && !was_dead) {
       const long long t0 = __builtin_amdgcn_s_memrealtime();
-      unsigned f;
       int ok = 1;
-      while ((f = ld_dev(peer)) < target) {
-        if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) { ok = 0; break; }
+#pragma unroll
+      for (int k = 0; k < NS - 1; ++k) {
+        if (ok) {
+          unsigned f;
+          while ((f = ld_dev(peer[k])) < target) {
+            if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) { ok = 0; break; }
+          }
+          if (f == kPoison) ok = 0;
+        }
       }
-      if (f == kPoison) ok = 0;
       if (!ok) { st_dev(status, 1u); st_dev(mine, kPoison); }
       s_word[0] = ok;
     }
