@@ -28,11 +28,12 @@
  *     return nothing has been written.  Errors raised by kernels while they
  *     run surface on the stream as HIP errors.
  *   - Results are bitwise reproducible run to run (no floating-point atomics).
- *   - For the widest nets (GELU MLP with dh > 128 at d = 64) each unit is
- *     split over two workgroups that swap partial sums through the workspace
- *     (or the backward scratch); those kernels are launched cooperatively, so
- *     a call may wait for the whole device.  Calls that share a workspace or
- *     scratch buffer must not run concurrently.
+ *   - For the wider nets at d = 64 (GELU MLP with dh > 128, SwiGLU with
+ *     dh > 64) each unit is split over two or three workgroups that swap
+ *     partial sums through the workspace (or the backward scratch); those
+ *     kernels are launched cooperatively, so a call may wait for the whole
+ *     device.  Calls that share a workspace or scratch buffer must not run
+ *     concurrently.
  *
  * Tensor layouts (row-major, C order):
  *   q, k, v, out, d_out, dq, dk, dv : [B][H][T][d]   element type desc.io
@@ -43,7 +44,7 @@
  *   SwiGLU   : Wg[dh][d], then Wu[dh][d], then Wd[d][dh]        P = 3 d dh
  *   (Wg, Wu, Wd are the paper's W1, W2, W3 of the SwiGLU net.)
  *
- * Supported shapes: io = BF16 with d = 64 (dh <= 256 for the MLP, <= 176 for
+ * Supported shapes: io = BF16 with d = 64 (dh <= 256 for the MLP, <= 192 for
  * SwiGLU), or io = F32 with d = 16 (dh <= 128); dh is padded inside the
  * library to a multiple of 16; 1 <= chunk <= 64; T >= 1 with a ragged last
  * chunk of T mod chunk tokens allowed (Prop. 1 holds for any chunk length).
