@@ -139,7 +139,8 @@ def test_forward_mlp_bf16_config():
 @pytest.mark.parametrize("T,C,dh,fw,flags", [(200, 64, 256, 0, 0), (130, 32, 256, 0, 0),
                                              (96, 16, 64, 0, 0), (256, 64, 120, 0, 0),
                                              (300, 64, 172, 1, 1), (64, 64, 172, 1, 0),
-                                             (192, 48, 100, 1, 1)])
+                                             (192, 48, 100, 1, 1), (130, 64, 192, 1, 0),
+                                             (70, 16, 130, 1, 1), (96, 32, 100, 1, 0)])
 def test_forward_bf16_shapes(T, C, dh, fw, flags):
     w = WL.WORKLOADS[1].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, seed=900 + T + dh)
     errs, _, _ = run_both(w, WL.make_inputs(w, with_grads=False), flags=flags)
@@ -163,6 +164,27 @@ def test_forward_1p3b_layer_sampled_units():
     errs = {"out": rel_l2(flat(out), ro[0]), "w_out": rel_l2(flat(wo), rw[0]),
             "m_out": rel_l2(flat(mo), rm[0])}
     assert_tol(errs, "bf16", w.name)
+    assert torch.isfinite(out.float()).all()
+
+
+@pytest.mark.parametrize("dh", [172, 100])
+def test_forward_swiglu_more_units_than_resident_groups(dh):
+    # B8 H16: 128 units on three (or two) workgroups each is more groups than
+    # the device holds at once; the resident groups take the units in turn
+    w = WL.WORKLOADS[2].with_(B=8, H=16, T=130, C=64, dh=dh)
+    x = WL.make_inputs(w, with_grads=False)
+    cfg = config_of(w)
+    t = to_dev(x, "bf16")
+    out, wo, mo, _ = gpu_forward(cfg, t)
+    torch.cuda.synchronize()
+    units = [0, 41, 86, 127]
+    xs = WL.make_inputs(w, with_grads=False, units=units)
+    ro, rw, rm = oracle.forward(xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"], xs["gamma"],
+                                xs["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
+    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units]
+    errs = {"out": rel_l2(flat(out), ro[0]), "w_out": rel_l2(flat(wo), rw[0]),
+            "m_out": rel_l2(flat(mo), rm[0])}
+    assert_tol(errs, "bf16", "swiglu B8 H16 dh=%d" % dh)
     assert torch.isfinite(out.float()).all()
 
 
