@@ -168,8 +168,10 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the headline step (no averaged-rule, gate or decode timings)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this size (for counter calibration)")
     args = ap.parse_args()
@@ -280,22 +282,23 @@ def main():
                      "flop_per_launch": dom_flop, "avg_launch_ms": dom_ms},
         "detail": {"fwd_ms": avg_fwd, "bwd_ms": avg_bwd, "source_hash": source_hash()},
     }
-    # the same step under the chunk-averaged rule (ablation baseline): only the
-    # scalar kernels differ, so this isolates what the closed form costs
-    cfg_avg = e2ttt.Config(w.B, w.H, w.T, w.d, w.dh, w.C, w.fw, e2ttt.DT_BF16,
+    if not args.no_extras:
+        # the same step under the chunk-averaged rule (ablation baseline): only
+        # the scalar kernels differ, so this isolates what the closed form costs
+        cfg_main = cfg
+        cfg = e2ttt.Config(w.B, w.H, w.T, w.d, w.dh, w.C, w.fw, e2ttt.DT_BF16,
                            e2ttt.FLAG_CHUNK_AVERAGED)
-    cfg_main = cfg
-    cfg = cfg_avg
-    step()
-    torch.cuda.synchronize()
-    ta = time.perf_counter()
-    for _ in range(max(1, args.steps // 2)):
         step()
-    torch.cuda.synchronize()
-    res["averaged_rule_ms_per_step"] = (time.perf_counter() - ta) * 1e3 / max(1, args.steps // 2)
-    cfg = cfg_main
-    res["gates"] = time_gates(e2ttt, w, dev)
-    res["decode"] = time_decode(e2ttt, w, x, dev)
+        torch.cuda.synchronize()
+        na = max(1, args.steps // 2)
+        ta = time.perf_counter()
+        for _ in range(na):
+            step()
+        torch.cuda.synchronize()
+        res["averaged_rule_ms_per_step"] = (time.perf_counter() - ta) * 1e3 / na
+        cfg = cfg_main
+        res["gates"] = time_gates(e2ttt, w, dev)
+        res["decode"] = time_decode(e2ttt, w, x, dev)
     if args.no_cpu_baseline:
         res["cpu_baseline"] = None
     else:
