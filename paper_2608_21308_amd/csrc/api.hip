@@ -19,7 +19,18 @@ constexpr size_t kAlign = 256;
 // one cooperative launch; more units are taken in turn by the same groups.
 constexpr long kMaxPairs = 128;
 
+// Chunks up to 64 tokens run everywhere; longer chunks (up to 512, the
+// paper's setting) run in the forward without saving for the backward, on the
+// MLP bf16 and the fp32 variants (whose chunk products take operand copies of
+// W_0 that stay fixed across the chunk's tiles).
+constexpr int kMaxChunk = 512;
+constexpr int kMaxTrainChunk = 64;
+
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool long_chunk_ok(const e2ttt_desc& d) {
+  return d.chunk <= kMaxTrainChunk || d.io == E2TTT_DT_F32 || d.fw == E2TTT_FW_GELU_MLP;
+}
 
 struct Plan {
   long U = 0, T = 0, NC = 0, P = 0;
@@ -74,7 +85,7 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   if (d.flags & ~(E2TTT_FLAG_NO_RESIDUAL_LN | E2TTT_FLAG_CHUNK_AVERAGED))
     return E2TTT_ERR_UNSUPPORTED;
   if (!(d.flags & E2TTT_FLAG_NO_RESIDUAL_LN) && !(d.ln_eps > 0.0f)) return E2TTT_ERR_BAD_SHAPE;
-  if (d.chunk > 64) return E2TTT_ERR_UNSUPPORTED;
+  if (d.chunk > kMaxChunk) return E2TTT_ERR_UNSUPPORTED;
   const long U = (long)d.B * d.H;
   if (U > INT_MAX || (long)d.T * d.d > (1L << 40) / U) return E2TTT_ERR_UNSUPPORTED;
   e2ttt_status st = select_config(d, pl.cfg);
@@ -195,12 +206,14 @@ size_t e2ttt_param_count(const e2ttt_desc* desc) {
 size_t e2ttt_workspace_bytes(const e2ttt_desc* desc, int save_for_backward) {
   Plan pl;
   if (make_plan(desc, pl) != E2TTT_OK) return 0;
+  if (!long_chunk_ok(*desc) || (save_for_backward && desc->chunk > kMaxTrainChunk)) return 0;
   return save_for_backward ? pl.ws_bytes_save : pl.ws_bytes;
 }
 
 size_t e2ttt_backward_scratch_bytes(const e2ttt_desc* desc) {
   Plan pl;
-  return make_plan(desc, pl) == E2TTT_OK ? pl.scratch_bytes : 0;
+  if (make_plan(desc, pl) != E2TTT_OK || desc->chunk > kMaxTrainChunk) return 0;
+  return pl.scratch_bytes;
 }
 
 const char* e2ttt_status_str(e2ttt_status s) {
@@ -258,6 +271,8 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
+  if (!long_chunk_ok(*desc) || (save_for_backward && desc->chunk > kMaxTrainChunk))
+    return E2TTT_ERR_UNSUPPORTED;
   if (!q || !k || !v || !eta || !beta || !w_in || !out || !w_out || !m_out || !workspace)
     return E2TTT_ERR_NULL_ARG;
   if (workspace_bytes < (save_for_backward ? pl.ws_bytes_save : pl.ws_bytes))
@@ -310,6 +325,7 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
+  if (desc->chunk > kMaxTrainChunk) return E2TTT_ERR_UNSUPPORTED;
   if (!q || !k || !v || !eta || !beta || !w_in || !workspace || !d_out || !dq || !dk || !dv ||
       !d_eta || !d_beta || !d_w_in || !d_m_in || !scratch)
     return E2TTT_ERR_NULL_ARG;

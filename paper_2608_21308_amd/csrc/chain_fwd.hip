@@ -12,12 +12,20 @@
 //   O  = Q + LN(act(Q W1^T) W2^T)     outputs from the chunk-start weights (a7)
 // The new state stays in registers for the next chunk (a8).
 //
+// Chunks longer than the CM-row tile (C up to 512) run as consecutive tiles of
+// one chunk: every tile takes its gradients and outputs at the chunk-start
+// weights (the operand copies formed at the chunk's first tile), the state is
+// scaled by the carries once, at the first tile, and every tile accumulates
+// its sum_t K_t G_t into it, so the chunk end is Prop. 1 over all C tokens.
+//
 // With NS workgroups per unit (pair_xchg.h) each holds a share of the hidden
 // columns; the j-contractions Y_K and Y_Q then give partial sums that the
 // ranks swap.  The Q-side first layer and Y_Q run between posting the Y_K
 // partial and waiting for the peers', so the exchange overlaps that work; the
 // Y_Q swap is waited for only at the end of the chunk.  Every rank adds the
 // partials in rank order, so all see bitwise identical Y_K and dY.
+#include <algorithm>
+
 #include "chain_common.h"
 #include "pair_xchg.h"
 
@@ -63,7 +71,9 @@ __device__ __forceinline__ float* fwd_slot(float* xbuf, long p, int rank, int pa
   return xbuf + (((p * S::NS + rank) * 2 + parity) * 2L) * S::CM * S::D;
 }
 
-template <class S>
+// LONG: chunks longer than the CM-row tile (a separate instantiation, so that
+// the common case keeps W_0's operand copies dead between chunks).
+template <class S, bool LONG>
 __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   using O = typename S::O;
   using IO = IoT<S::BF>;
@@ -73,6 +83,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // chunk (checkpoint, LDS copy of W2, and the K-side, Q-side and dA products
   // share them); the wider SwiGLU state re-forms them per use instead
   constexpr bool PRESPLIT = S::BF && S::FW == 0;
+  // fp32 path: a copy of W_0 is the operand of the chunk's products, so that
+  // the tiles of a long chunk all see the chunk-start weights
+  constexpr bool W0COPY = !S::BF;
   constexpr int EPL = D / 16;    // head elements per lane in the row phases
   constexpr int RPW = row_share<S>();  // output rows written by one rank (last: fewer)
   constexpr int NPEER = S::NS - 1;
@@ -81,6 +94,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
+  const int TPC = LONG ? (C + S::CM - 1) / S::CM : 1;   // tiles per chunk
+  const int TL = LONG ? S::CM : C;                       // tokens per tile
   const float inv_d = 1.0f / D;
 
   PairX<S::NS> px;
@@ -108,10 +123,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // inputs of the next chunk, loaded one chunk ahead
   TileRegs<S> pk, pq, pv;
   float pkw = 0.0f, pkm = 0.0f, pcar = 0.0f;
-  auto prefetch = [&](long uu, int rc) {
+  auto prefetch = [&](long uu, int rc, int kt) {
     E2TTT_LANE_IDS;
-    const long r0 = uu * T + (long)rc * C;
-    const int ln = min(C, T - rc * C);
+    const int st = LONG ? rc * C + kt * TL : rc * C;
+    const long r0 = uu * T + st;
+    const int ln = LONG ? min(TL, min(T, (rc + 1) * C) - st) : min(C, T - st);
     pk.load(a.k, r0, ln, tid);
     pq.load(a.q, r0, ln, tid);
     pv.load(a.v, r0, ln, tid);
@@ -125,16 +141,23 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   for (long u = px.p; u < a.U; u += NP) {
     StateTiles<S> W, M;
     SplitTiles<S> WS;   // bf16 hi / lo parts of W_0 (PRESPLIT)
+    StateTiles<S> W0c;  // W_0 (W0COPY)
     {
       E2TTT_LANE_IDS;
       load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
       load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, j0, w, g, c);
     }
-    prefetch(u, 0);
+    prefetch(u, 0, 0);
 
-    for (int r = 0; r < NC; ++r, ++nch) {
-      const int s0 = r * C;
-      const int len = min(C, T - s0);
+    // tile kt of chunk r (always kt = 0 unless LONG)
+    for (int r = 0, kt = 0; r < NC; ++nch) {
+      const int s0 = LONG ? r * C + kt * TL : r * C;
+      const int cend = LONG ? min(T, (r + 1) * C) : 0;
+      const bool first = !LONG || kt == 0;         // the chunk's first tile
+      const int len = LONG ? min(TL, cend - s0) : min(C, T - s0);
+      const bool more = LONG && s0 + TL < cend;    // another tile of this chunk follows
+      const int rc = r;
+      if (more) ++kt; else { ++r; kt = 0; }
       const long row0 = u * T + s0;
       const int par = (int)(nch & 1);
       const unsigned seq0 = px.seq_now();
@@ -149,9 +172,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         sm.km[tid] = pkm;
       }
       if (tid < 3) sm.carry[tid] = pcar;
+      if (first) {
       if constexpr (PRESPLIT) split_state<S>(WS, W);
+      if constexpr (W0COPY) W0c = W;
       if (a.ckpt) {
-        char* cb = static_cast<char*>(a.ckpt) + ((u * NC + r) * S::NS + rank) * 2 * a.ckpt_stride;
+        char* cb = static_cast<char*>(a.ckpt) + ((u * NC + rc) * S::NS + rank) * 2 * a.ckpt_stride;
         if constexpr (PRESPLIT) store_ckpt_q<S>(WS.hi, cb, w, lane);
         else store_ckpt<S>(W, cb, w, lane);
         store_ckpt<S>(M, cb + a.ckpt_stride, w, lane);
@@ -166,11 +191,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int rr = 0; rr < 4; ++rr)
             sm.w2[(16 * ib + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = q[rr];
         }
+      }
       opaque_state<S>(W);
       opaque_state<S>(M);
       }
       __syncthreads();
-      if (r + 1 < NC) prefetch(u, r + 1);
+      if (r < NC) prefetch(u, r, kt);              // the next tile (r, kt advanced above)
+
+      // operand of the chunk's products: W itself, or its chunk-start copy
+      const StateTiles<S>& Wop = W0COPY ? W0c : W;
 
       // ------------------------------------------- K-side forward (a3)
       // act'(H) kept for dH: MLP GELU'(H); SwiGLU (Hu SiLU'(Hg), SiLU(Hg))
@@ -196,8 +225,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.xk, S::LDD, 16 * tb + c, p * S::KC, g);
             if constexpr (PRESPLIT) acc = mma_split<S>(acc, af, WS.hi[0][jj], WS.lo[0][jj], p);
-            else acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
-            if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
+            else acc = mma_state<S>(acc, af, &Wop.t[0][jj][0], p, 1);
+            if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &Wop.t[1][jj][0], p, 1);
           }
           f32x4 act, d1, d2;
 #pragma unroll
@@ -250,8 +279,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.xq, S::LDD, 16 * tb + c, p * S::KC, g);
             if constexpr (PRESPLIT) acc = mma_split<S>(acc, af, WS.hi[0][jj], WS.lo[0][jj], p);
-            else acc = mma_state<S>(acc, af, &W.t[0][jj][0], p, 1);
-            if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &W.t[1][jj][0], p, 1);
+            else acc = mma_state<S>(acc, af, &Wop.t[0][jj][0], p, 1);
+            if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &Wop.t[1][jj][0], p, 1);
           }
           f32x4 act, d1;
           if (S::FW == 0 && a.asave) {   // GELU and GELU', saved for the backward
@@ -310,7 +339,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // for this chunk's stores does not include it
       if (S::FW == 0 && a.asave) {
         E2TTT_LANE_IDS;
-        const SavedAct<S> sv(static_cast<char*>(a.asave) + ((u * NC + r) * S::NS + rank) * a.as_stride);
+        const SavedAct<S> sv(static_cast<char*>(a.asave) + ((u * NC + rc) * S::NS + rank) * a.as_stride);
 #pragma unroll
         for (int tb = 0; tb < (S::FW == 0 ? NTB : 0); ++tb)
 #pragma unroll
@@ -445,7 +474,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int p = 0; p < S::KS_D; ++p) {
             auto af = lds_frag<S::BF>(sm.dy, S::LDD, 16 * tb + c, p * S::KC, g);
             if constexpr (PRESPLIT) da = mma_split<S>(da, af, WS.hi[SEC][jj], WS.lo[SEC][jj], p);
-            else da = mma_state<S>(da, af, &W.t[SEC][jj][0], p, 1);
+            else da = mma_state<S>(da, af, &Wop.t[SEC][jj][0], p, 1);
           }
           f32x4 dh[NU];
 #pragma unroll
@@ -470,6 +499,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       }
 
       // ------------------- closed-form transition (a5, a6): scale, then accumulate
+      if (first) {
 #pragma unroll
       for (int m = 0; m < NMAT; ++m)
 #pragma unroll
@@ -479,6 +509,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             W.t[m][jj][ib] = cw * W.t[m][jj][ib] + cm * M.t[m][jj][ib];
             M.t[m][jj][ib] = cbv * M.t[m][jj][ib];
           }
+      }
       {
       E2TTT_LANE_IDS;
 #pragma unroll
@@ -582,30 +613,50 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   }
 }
 
+// Long chunks are compiled for the variants whose chunk products take fixed
+// operand copies of W_0: the MLP on the bf16 path and the fp32 path.
+template <class S>
+constexpr bool has_long() { return !(S::BF && S::FW == 1); }
+
+template <class S, bool LONG>
+int occupancy() {
+  int v = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_fwd_kernel<S, LONG>, S::NT, 0) !=
+      hipSuccess)
+    v = 0;
+  return v;
+}
+
 template <class S>
 int max_blocks_per_cu() {
   static int nb = [] {
-    int v = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_fwd_kernel<S>, S::NT, 0) !=
-        hipSuccess)
-      v = 0;
+    int v = occupancy<S, false>();
+    if constexpr (has_long<S>()) v = std::min(v, occupancy<S, true>());
     return v;
   }();
   return nb;
 }
 
-template <class S>
-hipError_t launch(const ChainArgs& a, hipStream_t stream) {
+template <class S, bool LONG>
+hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
   if constexpr (S::NS == 1) {
-    hipLaunchKernelGGL(chain_fwd_kernel<S>, dim3((unsigned)a.U), dim3(S::NT), 0, stream, a);
+    hipLaunchKernelGGL((chain_fwd_kernel<S, LONG>), dim3((unsigned)a.U), dim3(S::NT), 0, stream,
+                       a);
     return hipGetLastError();
   } else {
     ChainArgs b = a;
     void* args[] = {&b};
-    return hipLaunchCooperativeKernel((const void*)chain_fwd_kernel<S>,
+    return hipLaunchCooperativeKernel((const void*)chain_fwd_kernel<S, LONG>,
                                       dim3((unsigned)(S::NS * a.npairs)), dim3(S::NT), args, 0,
                                       stream);
   }
+}
+
+template <class S>
+hipError_t launch(const ChainArgs& a, hipStream_t stream) {
+  if (a.C <= S::CM) return launch_as<S, false>(a, stream);
+  if constexpr (has_long<S>()) return launch_as<S, true>(a, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace

@@ -89,6 +89,63 @@ __device__ __forceinline__ float wave_total(float v) {
   return v;
 }
 
+// Chunks longer than a wave (C up to 512): the wave walks the chunk's 64-token
+// segments from the last to the first, carrying the products of the later
+// segments' factors (for the suffix products) and S at the next segment's
+// first token (for the affine recursion S_t = g~_t + beta_{t+1} S_{t+1}).
+__device__ void coeff_fwd_long(const CoeffFwdArgs& a, long wid, long base, int len, int lane) {
+  float cb = 1.0f, cg = 1.0f;           // products of beta, gamma over the later segments
+  float s_next = 0.0f, b_next = 1.0f;   // S and beta at the next segment's first token
+  float b0 = 1.0f, S0 = 0.0f, pb0 = 1.0f, pg0 = 1.0f;
+  const int nseg = (len + 63) / 64;
+  for (int seg = nseg - 1; seg >= 0; --seg) {
+    const long sb = base + seg * 64;
+    const int n = min(64, len - seg * 64);
+    const bool valid = lane < n;
+    const float e = valid ? a.eta[sb + lane] : 0.0f;
+    const float b = valid ? a.beta[sb + lane] : 1.0f;
+    const float gm = (valid && a.gamma) ? a.gamma[sb + lane] : 1.0f;
+    float pb = b, pg = gm;
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) {
+      const float ob = __shfl_down(pb, k, 64), og = __shfl_down(pg, k, 64);
+      if (lane + k < 64) { pb *= ob; pg *= og; }
+    }
+    float bt = __shfl_down(pb, 1, 64), gt = __shfl_down(pg, 1, 64);
+    if (lane == 63) { bt = 1.0f; gt = 1.0f; }
+    bt *= cb;                            // exclusive suffix products over the whole chunk
+    gt *= cg;
+    const float bnext = __shfl_down(b, 1, 64);
+    const bool last_seg = seg == nseg - 1;
+    float A, B;
+    if (lane < n - 1) { A = gt; B = bnext; }
+    else if (lane == n - 1) {
+      if (last_seg) { A = 1.0f; B = 0.0f; }
+      else { A = gt + b_next * s_next; B = 0.0f; }
+    } else { A = 0.0f; B = 0.0f; }
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) {
+      const float oA = __shfl_down(A, k, 64), oB = __shfl_down(B, k, 64);
+      if (lane + k < 64) { A = A + B * oA; B = B * oB; }
+    }
+    if (valid) {
+      a.kw[sb + lane] = e * A;
+      a.km[sb + lane] = e * bt;
+    }
+    s_next = __shfl(A, 0, 64);
+    b_next = __shfl(b, 0, 64);
+    const float segb = __shfl(pb, 0, 64), segg = __shfl(pg, 0, 64);
+    cb *= segb;
+    cg *= segg;
+    if (seg == 0) { b0 = b_next; S0 = s_next; pb0 = cb; pg0 = cg; }
+  }
+  if (lane == 0) {
+    a.carry[wid * 3 + 0] = pg0;
+    a.carry[wid * 3 + 1] = b0 * S0;
+    a.carry[wid * 3 + 2] = pb0;
+  }
+}
+
 __global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
   // the chain kernel that follows on this stream starts from cleared sync words
   for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < a.nzero; i += (long)gridDim.x * 256)
@@ -102,20 +159,28 @@ __global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
   const int len = min(a.C, a.T - s0);
   const long base = u * a.T + s0;
   if (a.averaged) {
-    const bool valid = lane < len;
-    const float e = valid ? a.eta[base + lane] : 0.0f;
-    const float bsum = wave_total(valid ? a.beta[base + lane] : 0.0f);
-    const float gsum = wave_total(valid ? (a.gamma ? a.gamma[base + lane] : 1.0f) : 0.0f);
-    const float inv = 1.0f / (float)len;
-    if (valid) {
-      a.kw[base + lane] = e;
-      a.km[base + lane] = e;
+    float bpart = 0.0f, gpart = 0.0f;
+    for (int t0 = 0; t0 < len; t0 += 64) {
+      const bool valid = t0 + lane < len;
+      const float e = valid ? a.eta[base + t0 + lane] : 0.0f;
+      bpart += valid ? a.beta[base + t0 + lane] : 0.0f;
+      gpart += valid ? (a.gamma ? a.gamma[base + t0 + lane] : 1.0f) : 0.0f;
+      if (valid) {
+        a.kw[base + t0 + lane] = e;
+        a.km[base + t0 + lane] = e;
+      }
     }
+    const float bsum = wave_total(bpart), gsum = wave_total(gpart);
+    const float inv = 1.0f / (float)len;
     if (lane == 0) {
       a.carry[wid * 3 + 0] = gsum * inv;
       a.carry[wid * 3 + 1] = bsum * inv;
       a.carry[wid * 3 + 2] = bsum * inv;
     }
+    return;
+  }
+  if (len > 64) {
+    coeff_fwd_long(a, wid, base, len, lane);
     return;
   }
   ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);

@@ -50,7 +50,7 @@ def test_sizes(lib):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(T=0), 2), (dict(B=-1), 2), (dict(chunk=0), 2), (dict(ln_eps=0.0), 2),
-    (dict(chunk=65), 3), (dict(fw=2), 3), (dict(io=7), 3), (dict(flags=4), 3),
+    (dict(chunk=513), 3), (dict(fw=2), 3), (dict(io=7), 3), (dict(flags=4), 3),
     (dict(d=32), 3), (dict(d=16), 3), (dict(dh=300), 3), (dict(fw=1, dh=200), 3),
     (dict(io=0, d=64), 3), (dict(io=0, d=16, dh=200), 3)])
 def test_bad_descriptors(lib, kw, status):
@@ -199,3 +199,22 @@ def test_apply_argument_errors(lib):
         assert lib.e2ttt_apply(ctypes.byref(d), *a, None) == 1, i
     # the state is read as float4: a pointer that is not 16-byte aligned is refused
     assert lib.e2ttt_apply(ctypes.byref(d), f, ctypes.c_void_p(260), f, None) == 2
+
+
+def test_long_chunks_are_forward_only(lib):
+    """Chunks of 65..512 tokens: forward without saving, on the MLP bf16 and
+    fp32 variants; everything that would need the backward (or SwiGLU on bf16)
+    is refused before any launch."""
+    f = ctypes.c_void_p(16)   # never dereferenced
+    for kw in (dict(chunk=128), dict(chunk=512), dict(io=0, d=16, dh=64, chunk=200)):
+        d = desc(**kw)
+        assert lib.e2ttt_param_count(ctypes.byref(d)) > 0
+        assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 0) > 0
+        assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 1) == 0
+        assert lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) == 0
+        assert lib.e2ttt_chunk_forward(ctypes.byref(d), *([f] * 12), 1 << 40, 1, None) == 3
+        assert lib.e2ttt_chunk_backward(ctypes.byref(d), *([f] * 9), 1 << 40, *([f] * 12),
+                                        1 << 40, None) == 3
+    d = desc(fw=1, dh=172, chunk=128)   # SwiGLU on bf16: chunks of at most 64
+    assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 0) == 0
+    assert lib.e2ttt_chunk_forward(ctypes.byref(d), *([f] * 12), 1 << 40, 0, None) == 3

@@ -1,0 +1,136 @@
+"""GPU parity of chunks longer than one 64-row tile (C up to 512, the paper's
+setting, Sec. 5): the forward runs a chunk as consecutive tiles that all take
+gradients and outputs at the chunk-start weights, and Prop. 1 over the whole
+chunk sets the next state.  The oracle computes the token recurrence of eq.
+(7) with any chunk length.
+
+Bars: the scalar kernels within 1e-5 relative (fp32 scans over up to 512
+factors); the forward at rel-L2 1e-5 for fp32 io (widened only by the case's
+own fp32 conditioning, as for short chunks) and 2e-2 for bf16 io.  Long
+chunks are forward-only: saving for the backward, the backward and SwiGLU on
+bf16 are refused with E2TTT_ERR_UNSUPPORTED.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2608_21308_amd import e2ttt, workloads as WL
+from tests.gpu_util import TOL, config_of, fp32_sensitivity, rel_l2, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    e2ttt.load()
+
+
+@pytest.mark.parametrize("T,C", [(300, 65), (700, 128), (1000, 200), (1100, 512), (512, 512)])
+@pytest.mark.parametrize("averaged", [False, True])
+def test_long_chunk_coeffs(T, C, averaged):
+    w = WL.WORKLOADS[1].with_(B=1, H=2, T=T, C=C)
+    x = WL.make_inputs(w, with_grads=False)
+    cfg = config_of(w, flags=e2ttt.FLAG_CHUNK_AVERAGED if averaged else 0)
+    t = to_dev(x, "bf16")
+    kw, km, carry = e2ttt.chunk_coeffs(cfg, t["eta"], t["beta"], t["gamma"])
+    torch.cuda.synchronize()
+    kw, km, carry = kw.cpu().numpy(), km.cpu().numpy(), carry.cpu().numpy()
+    for u in range(2):
+        for r, s0 in enumerate(range(0, T, C)):
+            sl = slice(s0, min(T, s0 + C))
+            e, b, g = (x[n][0, u, sl].astype(np.float64) for n in ("eta", "beta", "gamma"))
+            if averaged:
+                rkw = rkm = e
+                rc = (g.mean(), b.mean(), b.mean())
+            else:
+                rkw, rkm, rc = oracle.chunk_coeffs(e, b, g)
+            np.testing.assert_allclose(kw[0, u, sl], rkw, rtol=1e-5, atol=1e-12)
+            np.testing.assert_allclose(km[0, u, sl], rkm, rtol=1e-5, atol=1e-30)
+            np.testing.assert_allclose(carry[0, u, r], rc, rtol=1e-5, atol=1e-30)
+
+
+def run_forward(w, x, flags=0):
+    cfg = config_of(w, flags=flags)
+    t = to_dev(x, w.io)
+    out, wo, mo, _ = e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                                   t["w_in"], t.get("m_in"))
+    torch.cuda.synchronize()
+    return out, wo, mo
+
+
+def oracle_forward(w, x, flags=0):
+    return oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"], x["w_in"],
+                          x.get("m_in"), C=w.C, fw=w.fw, dh=w.dh, flags=flags)
+
+
+def errors(got, ref, x):
+    out, wo, mo = got
+    ro, rw, rm = ref
+    return {"out": rel_l2(out, ro),
+            "w_out": rel_l2(wo.cpu().numpy() - x["w_in"], rw - x["w_in"]),
+            "m_out": rel_l2(mo, rm)}
+
+
+@pytest.mark.parametrize("fw", [WL.FW_MLP, WL.FW_SWIGLU])
+@pytest.mark.parametrize("T,C,flags", [(300, 128, 0), (200, 200, 0), (700, 512, 1),
+                                       (170, 65, 0)])
+def test_long_chunk_forward_fp32(fw, T, C, flags):
+    w = WL.WORKLOADS[0].with_(fw=fw, B=1, H=2, T=T, C=C, seed=1300 + T + C)
+    x = WL.make_inputs(w, with_grads=False)
+    x["m_in"] = (1e-3 * np.random.default_rng(T).standard_normal(x["w_in"].shape)).astype(
+        np.float32)
+    errs = errors(run_forward(w, x, flags), oracle_forward(w, x, flags), x)
+    sens = fp32_sensitivity(
+        lambda y: dict(zip(("out", "w_out", "m_out"), oracle_forward(w, y, flags))), x)
+    what = "long fp32 fw=%d T=%d C=%d flags=%d" % (fw, T, C, flags)
+    print(what, {k: "%.2e" % v for k, v in errs.items()},
+          "sens", {k: "%.1e" % v for k, v in sens.items()}, flush=True)
+    bad = {n: e for n, e in errs.items() if not e <= max(TOL["f32"], 10 * sens[n])}
+    assert not bad, what + ": %s" % bad
+
+
+@pytest.mark.parametrize("T,C,dh", [(1100, 512, 256), (1100, 512, 64), (600, 128, 256),
+                                    (300, 100, 120)])
+def test_long_chunk_forward_bf16(T, C, dh):
+    w = WL.WORKLOADS[1].with_(B=2, H=2, T=T, C=C, dh=dh, seed=1400 + T + dh)
+    x = WL.make_inputs(w, with_grads=False)
+    errs = errors(run_forward(w, x), oracle_forward(w, x), x)
+    print("long bf16 T=%d C=%d dh=%d" % (T, C, dh), {k: "%.2e" % v for k, v in errs.items()},
+          flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+def test_long_chunk_1p3b_layer_sampled_units():
+    # the headline layer shape at the paper's chunk length: all 128 units in
+    # one launch (more units than resident pairs are taken in turn)
+    w = WL.WORKLOADS[3].with_(C=512)
+    x = WL.make_inputs(w, with_grads=False)
+    out, wo, mo = run_forward(w, x)
+    units = [0, 77, 127]
+    xs = WL.make_inputs(w, with_grads=False, units=units)
+    ro, rw, rm = oracle_forward(w, xs)
+    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units]
+    errs = {"out": rel_l2(flat(out), ro[0]),
+            "w_out": rel_l2(flat(wo).cpu().numpy() - xs["w_in"][0], rw[0] - xs["w_in"][0]),
+            "m_out": rel_l2(flat(mo), rm[0])}
+    print("long bf16 1.3B layer C=512", {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+def test_long_chunks_refused_where_unsupported():
+    w = WL.WORKLOADS[1].with_(B=1, H=2, T=256, C=128)
+    x = WL.make_inputs(w, with_grads=False)
+    t = to_dev(x, "bf16")
+    with pytest.raises(e2ttt.E2TTTError, match="unsupported"):   # saving for the backward
+        e2ttt.forward(config_of(w), t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                      t["w_in"], None, workspace=torch.empty(1 << 20, dtype=torch.uint8,
+                                                             device="cuda"),
+                      save_for_backward=True)
+    ws = WL.WORKLOADS[2].with_(B=1, H=2, T=256, C=128)
+    xs = to_dev(WL.make_inputs(ws, with_grads=False), "bf16")
+    with pytest.raises(e2ttt.E2TTTError, match="unsupported"):   # SwiGLU on bf16
+        e2ttt.forward(config_of(ws), xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"],
+                      xs["gamma"], xs["w_in"], None,
+                      workspace=torch.empty(1 << 20, dtype=torch.uint8, device="cuda"))
