@@ -67,6 +67,37 @@ def cpu_baseline(w, seconds_hint: float = 20.0) -> dict:
                       "scaled by %d/%d" % (n_units, w.B * w.H, w.T, dt, w.B * w.H, n_units)}
 
 
+def time_long_chunk(e2ttt, w, t, dev, reps: int = 10) -> dict:
+    """Forward (no saving) of the same layer at chunk 64 and at the paper's
+    chunk 512 (64-token tiles at the chunk-start weights): HIP events around
+    back-to-back calls."""
+    import torch
+    res = {}
+    for C in (w.C, 512):
+        cfg = e2ttt.Config(w.B, w.H, w.T, w.d, w.dh, C, w.fw, e2ttt.DT_BF16)
+        ws = e2ttt.alloc_workspace(cfg, False, dev)
+        out = torch.empty_like(t["q"])
+        wo, mo = torch.empty_like(t["w_in"]), torch.empty_like(t["w_in"])
+
+        def call():
+            e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                          t["w_in"], None, out=out, w_out=wo, m_out=mo, workspace=ws)
+
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(reps):
+            call()
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / reps
+        res["C%d_fwd_ms" % C] = ms
+        res["C%d_tokens_per_s" % C] = w.B * w.T / (ms * 1e-3)
+    return res
+
+
 def time_gates(e2ttt, w, dev, reps: int = 50) -> dict:
     """Gate parameterization kernels (eqs. (12)-(14)) over the same B*H*T
     tokens, outside the timed step: average time of back-to-back calls through
@@ -297,6 +328,7 @@ def main():
         torch.cuda.synchronize()
         res["averaged_rule_ms_per_step"] = (time.perf_counter() - ta) * 1e3 / na
         cfg = cfg_main
+        res["long_chunk_forward"] = time_long_chunk(e2ttt, w, t, dev)
         res["gates"] = time_gates(e2ttt, w, dev)
         res["decode"] = time_decode(e2ttt, w, x, dev)
     if args.no_cpu_baseline:
