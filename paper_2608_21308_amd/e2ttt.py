@@ -341,3 +341,30 @@ class E2TTTFunction(torch.autograd.Function):
                      None if d_m_out is None else d_m_out.contiguous())
         return (None, g["dq"], g["dk"], g["dv"], g["d_eta"], g["d_beta"], g["d_gamma"],
                 g["d_w_in"], None if m_in is None else g["d_m_in"])
+
+
+class GatesFunction(torch.autograd.Function):
+    """Autograd wrapper of the gate parameterization (eqs. (12)-(14)): logits
+    in, (eta, beta, gamma) out; the backward calls e2ttt_gates_backward.
+    gamma is None when l_alpha is None."""
+
+    @staticmethod
+    def forward(ctx, params, l_eta, l_beta, l_alpha):
+        eta, beta, gamma = gates_forward(params, l_eta, l_beta, l_alpha)
+        ctx.params = params
+        ctx.save_for_backward(l_eta, l_beta, l_alpha)
+        return eta, beta, gamma
+
+    @staticmethod
+    def backward(ctx, d_eta, d_beta, d_gamma):
+        l_eta, l_beta, l_alpha = ctx.saved_tensors
+        zero = lambda ref: torch.zeros_like(ref)
+        d_eta = zero(l_eta) if d_eta is None else d_eta.contiguous()
+        d_beta = zero(l_beta) if d_beta is None else d_beta.contiguous()
+        if l_alpha is not None:
+            d_gamma = zero(l_alpha) if d_gamma is None else d_gamma.contiguous()
+        else:
+            d_gamma = None
+        g_eta, g_beta, g_alpha = gates_backward(ctx.params, l_eta, l_beta, l_alpha, d_eta,
+                                                d_beta, d_gamma)
+        return None, g_eta, g_beta, g_alpha

@@ -116,3 +116,30 @@ def test_gates_feed_the_chunk_update():
           "sens", {k: "%.1e" % v for k, v in sens.items()}, flush=True)
     for n in errs:
         assert errs[n] <= max(1e-5, 10 * sens[n]), n
+
+
+def test_gates_and_chunk_update_through_autograd():
+    """Logits -> GatesFunction -> E2TTTFunction -> loss, differentiated by
+    torch autograd: the logit gradients equal the oracle's chain backward
+    (d_eta, d_beta, d_gamma) mapped through the gate oracle's backward (fp32
+    path, within the chain's 1e-5 bar)."""
+    from oracle import oracle
+    from paper_2608_21308_amd import workloads as WL
+    from tests.gpu_util import config_of, rel_l2, to_dev
+    w = WL.WORKLOADS[0].with_(B=1, H=2, T=40, C=16, backward=True)
+    x = WL.make_inputs(w)
+    le, lb, la = (a.reshape(w.B, w.H, w.T) for a in logits(w.B * w.H * w.T, 9, scale=1.5))
+    r_eta, r_beta, r_gamma = gref.forward(*(a.astype(np.float64) for a in (le, lb, la)))
+    rg = oracle.backward(x["q"], x["k"], x["v"], r_eta, r_beta, r_gamma, x["w_in"], None,
+                         x["d_out"], C=w.C, fw=w.fw, dh=w.dh)
+    want = gref.backward(*(a.astype(np.float64) for a in (le, lb, la)), rg["d_eta"],
+                         rg["d_beta"], rg["d_gamma"])
+    t = to_dev(x, w.io)
+    L = [torch.from_numpy(a).cuda().requires_grad_(True) for a in (le, lb, la)]
+    eta, beta, gamma = e2ttt.GatesFunction.apply(e2ttt.GateParams(), *L)
+    out, wo, mo = e2ttt.E2TTTFunction.apply(config_of(w), t["q"], t["k"], t["v"], eta, beta,
+                                            gamma, t["w_in"], None)
+    (out * t["d_out"]).sum().backward()
+    errs = [rel_l2(l.grad, r) for l, r in zip(L, want)]
+    print("autograd logits", ["%.2e" % e for e in errs], flush=True)
+    assert all(e <= 1e-5 for e in errs), errs
