@@ -83,9 +83,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // chunk (checkpoint, LDS copy of W2, and the K-side, Q-side and dA products
   // share them); the wider SwiGLU state re-forms them per use instead
   constexpr bool PRESPLIT = S::BF && S::FW == 0;
-  // fp32 path: a copy of W_0 is the operand of the chunk's products, so that
-  // the tiles of a long chunk all see the chunk-start weights
-  constexpr bool W0COPY = !S::BF;
+  // fp32 path: the chunk's sum_t K_t G_t accumulates apart from the state and
+  // joins it in one addition at the chunk end (one rounding of W and M per
+  // chunk instead of one per contraction step); W itself stays W_0 for the
+  // whole chunk and is the products' operand, also across a long chunk's tiles
+  constexpr bool SEPDELTA = !S::BF;
   constexpr int EPL = D / 16;    // head elements per lane in the row phases
   constexpr int RPW = row_share<S>();  // output rows written by one rank (last: fewer)
   constexpr int NPEER = S::NS - 1;
@@ -141,7 +143,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   for (long u = px.p; u < a.U; u += NP) {
     StateTiles<S> W, M;
     SplitTiles<S> WS;   // bf16 hi / lo parts of W_0 (PRESPLIT)
-    StateTiles<S> W0c;  // W_0 (W0COPY)
+    StateTiles<S> XW, XM;   // the chunk's sum_t K_t G_t (SEPDELTA)
     {
       E2TTT_LANE_IDS;
       load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
@@ -174,7 +176,17 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       if (tid < 3) sm.carry[tid] = pcar;
       if (first) {
       if constexpr (PRESPLIT) split_state<S>(WS, W);
-      if constexpr (W0COPY) W0c = W;
+      if constexpr (SEPDELTA) {
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+              XW.t[m][jj][ib] = zero4();
+              XM.t[m][jj][ib] = zero4();
+            }
+      }
       if (a.ckpt) {
         char* cb = static_cast<char*>(a.ckpt) + ((u * NC + rc) * S::NS + rank) * 2 * a.ckpt_stride;
         if constexpr (PRESPLIT) store_ckpt_q<S>(WS.hi, cb, w, lane);
@@ -198,8 +210,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       __syncthreads();
       if (r < NC) prefetch(u, r, kt);              // the next tile (r, kt advanced above)
 
-      // operand of the chunk's products: W itself, or its chunk-start copy
-      const StateTiles<S>& Wop = W0COPY ? W0c : W;
+      // operand of the chunk's products (W_0: W is not updated before the chunk end
+      // on the fp32 path, nor before the transition below on the others)
+      const StateTiles<S>& Wop = W;
 
       // ------------------------------------------- K-side forward (a3)
       // act'(H) kept for dH: MLP GELU'(H); SwiGLU (Hu SiLU'(Hg), SiLU(Hg))
@@ -499,7 +512,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       }
 
       // ------------------- closed-form transition (a5, a6): scale, then accumulate
-      if (first) {
+      StateTiles<S>& AW = SEPDELTA ? XW : W;   // accumulation targets
+      StateTiles<S>& AM = SEPDELTA ? XM : M;
+      if (!SEPDELTA && first) {
 #pragma unroll
       for (int m = 0; m < NMAT; ++m)
 #pragma unroll
@@ -523,8 +538,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             for (int h = 0; h < S::NH; ++h) bA.h[h] = AK[S::NH * p + h][jj];
             const int row = 16 * ib + c, k0 = p * S::KC;
             // second layer: sum_t K_t dY[t][i] A[t][j]
-            W.t[SEC][jj][ib] = O::mma(W.t[SEC][jj][ib], it_frag<S>(sm.dytw, row, k0, g), bA);
-            M.t[SEC][jj][ib] = O::mma(M.t[SEC][jj][ib], it_frag<S>(sm.dytm, row, k0, g), bA);
+            AW.t[SEC][jj][ib] = O::mma(AW.t[SEC][jj][ib], it_frag<S>(sm.dytw, row, k0, g), bA);
+            AM.t[SEC][jj][ib] = O::mma(AM.t[SEC][jj][ib], it_frag<S>(sm.dytm, row, k0, g), bA);
             // first layer(s): sum_t k[t][i] (K_t dH[t][j])
             auto kf = it_frag<S>(sm.kt, row, k0, g);
 #pragma unroll
@@ -535,19 +550,30 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
                 bw.h[h] = DW[m][S::NH * p + h][jj];
                 bm.h[h] = DM[m][S::NH * p + h][jj];
               }
-              W.t[m][jj][ib] = O::mma(W.t[m][jj][ib], kf, bw);
-              M.t[m][jj][ib] = O::mma(M.t[m][jj][ib], kf, bm);
+              AW.t[m][jj][ib] = O::mma(AW.t[m][jj][ib], kf, bw);
+              AM.t[m][jj][ib] = O::mma(AM.t[m][jj][ib], kf, bm);
               if constexpr (SPLIT_UPD) {
 #pragma unroll
                 for (int h = 0; h < S::NH; ++h) {
                   bw.h[h] = DWl[m][S::NH * p + h][jj];
                   bm.h[h] = DMl[m][S::NH * p + h][jj];
                 }
-                W.t[m][jj][ib] = O::mma(W.t[m][jj][ib], kf, bw);
-                M.t[m][jj][ib] = O::mma(M.t[m][jj][ib], kf, bm);
+                AW.t[m][jj][ib] = O::mma(AW.t[m][jj][ib], kf, bw);
+                AM.t[m][jj][ib] = O::mma(AM.t[m][jj][ib], kf, bm);
               }
             }
           }
+      }
+      if (SEPDELTA && !more) {   // chunk end: W_C = cw W_0 + cm M_0 + dW, M_C = cb M_0 + dM
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+              W.t[m][jj][ib] = (cw * W.t[m][jj][ib] + cm * M.t[m][jj][ib]) + XW.t[m][jj][ib];
+              M.t[m][jj][ib] = cbv * M.t[m][jj][ib] + XM.t[m][jj][ib];
+            }
       }
 
       // ------------------------------------------------- outputs (a7)

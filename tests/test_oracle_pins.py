@@ -43,7 +43,7 @@ def test_coeffs_golden(oracle, name):
 
 @pytest.mark.parametrize("C", [1, 2, 5, 16, 64])
 def test_coeffs_unit_retention(oracle, C):
-    # App. A.2: beta = gamma = 1  =>  R_t = C - t + 1, K^W_t = eta_t (C - t + 1),
+    # App. A.3: beta = gamma = 1  =>  R_t = C - t + 1, K^W_t = eta_t (C - t + 1),
     # K^M_t = eta_t, carries (1, C, 1).
     rng = np.random.default_rng(C)
     eta = rng.uniform(0.01, 0.1, C)
@@ -96,7 +96,7 @@ def test_coeffs_vs_recurrence_and_ratio_form(oracle, C):
 
 
 def test_coeffs_bounds(oracle):
-    # App. A.2: for beta, gamma in (0, 1], 0 <= beta-tilde_t R_t <= C - t + 1
+    # App. A.3: for beta, gamma in (0, 1], 0 <= beta-tilde_t R_t <= C - t + 1
     # and K^M_t <= eta_t.
     rng = np.random.default_rng(7)
     for C in (4, 64):
