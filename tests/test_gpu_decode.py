@@ -117,17 +117,19 @@ def stream(w, x, dev="cuda"):
     return out.float().cpu().numpy(), state.cpu().numpy(), mom.cpu().numpy()
 
 
-@pytest.mark.parametrize("case", sorted(CASES))
-def test_streaming_decode_matches_the_sequence_forward(case):
+@pytest.mark.parametrize("case,C", [(c, 16) for c in sorted(CASES)] +
+                         [("mlp_f32_d16", 128), ("mlp_bf16_d64", 128)])
+def test_streaming_decode_matches_the_sequence_forward(case, C):
     """Decode one token at a time over 3 full chunks and a ragged one; outputs
-    and final state equal the oracle's forward over the whole sequence."""
-    w = CASES[case].with_(T=3 * 16 + 5)
+    and final state equal the oracle's forward over the whole sequence (also
+    with chunks longer than one 64-token tile)."""
+    w = CASES[case].with_(T=3 * C + 5, C=C)
     x = WL.make_inputs(w, with_grads=False)
     out, wo, mo = stream(w, x)
     r_out, r_w, r_m = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"],
                                      x["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
     errs = dict(out=rel_l2(out, r_out), w=rel_l2(wo - x["w_in"], r_w - x["w_in"]),
                 m=rel_l2(mo, r_m))
-    print("decode %s" % case, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    print("decode %s C=%d" % (case, C), {k: "%.2e" % v for k, v in errs.items()}, flush=True)
     for k, e in errs.items():
         assert e <= TOL[w.io], k
