@@ -20,11 +20,11 @@ constexpr size_t kAlign = 256;
 constexpr long kMaxPairs = 128;
 
 // Chunks up to 64 tokens run everywhere; longer chunks (up to 512, the
-// paper's setting) run in the forward without saving for the backward, on the
-// MLP bf16 and the fp32 variants (whose chunk products take operand copies of
-// W_0 that stay fixed across the chunk's tiles).
+// paper's setting) run as 64-row tiles on the MLP bf16 and the fp32 variants
+// (whose chunk products take operands of W_0 that stay fixed across the
+// chunk's tiles), forward and backward.
 constexpr int kMaxChunk = 512;
-constexpr int kMaxTrainChunk = 64;
+constexpr int kMaxTrainChunk = 64;   // SwiGLU on bf16
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -42,8 +42,9 @@ struct Plan {
   long ckpt_stride = 0;
   size_t off_as = 0;
   long as_stride = 0;
+  long tpc = 1;           // 64-row tiles per chunk (chunks longer than one tile)
   // backward scratch
-  size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, off_bsync = 0, off_bxbuf = 0;
+  size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, off_bsync = 0, off_bxbuf = 0, off_frz = 0;
   size_t scratch_bytes = 0;
 };
 
@@ -113,17 +114,23 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_rk = pl.off_zk + align_up(tokd);
   pl.off_zq = pl.off_rk + align_up(tok);
   pl.off_rq = pl.off_zq + align_up(tokd);
+  const int cm_rows = 16 * pl.cfg.ntb;
+  pl.tpc = (d.chunk > cm_rows) ? (d.chunk + cm_rows - 1) / cm_rows : 1;
   pl.as_stride = chain_saved_act_bytes(pl.cfg);
   pl.off_as = pl.off_rq + align_up(tok);
-  pl.ws_bytes_save = pl.off_as + align_up((size_t)U * pl.NC * ns * pl.as_stride);
+  pl.ws_bytes_save = pl.off_as + align_up((size_t)U * pl.NC * pl.tpc * ns * pl.as_stride);
   pl.off_kwb = 0;
   pl.off_kmb = align_up(ns * tok);
   pl.off_carryb = pl.off_kmb + align_up(ns * tok);
   pl.off_bsync = pl.off_carryb + align_up(ns * chk);
   pl.off_bxbuf = pl.off_bsync + align_up(sync_b);
-  pl.scratch_bytes =
+  pl.off_frz =
       pl.off_bxbuf +
       align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, true) * sizeof(float));
+  const long nwg = (ns > 1) ? pl.npairs * ns : U;   // workgroups of the backward launch
+  pl.scratch_bytes =
+      pl.off_frz +
+      (pl.tpc > 1 ? align_up((size_t)nwg * 2 * chain_frz_floats(pl.cfg) * sizeof(float)) : 0);
   return E2TTT_OK;
 }
 
@@ -183,6 +190,11 @@ long chain_xchg_floats(const ChainConfig& cfg, bool backward) {
   return 2L * (backward ? 3 : 2) * 16 * cfg.ntb * cfg.d;
 }
 
+long chain_frz_floats(const ChainConfig& cfg) {
+  // one workgroup's share of the state: nmat matrices of 16 nw njb hidden columns x d
+  return (cfg.fw == 0 ? 2L : 3L) * 16 * cfg.nw * cfg.njb * cfg.d;
+}
+
 }  // namespace e2ttt
 
 namespace {
@@ -206,13 +218,13 @@ size_t e2ttt_param_count(const e2ttt_desc* desc) {
 size_t e2ttt_workspace_bytes(const e2ttt_desc* desc, int save_for_backward) {
   Plan pl;
   if (make_plan(desc, pl) != E2TTT_OK) return 0;
-  if (!long_chunk_ok(*desc) || (save_for_backward && desc->chunk > kMaxTrainChunk)) return 0;
+  if (!long_chunk_ok(*desc)) return 0;
   return save_for_backward ? pl.ws_bytes_save : pl.ws_bytes;
 }
 
 size_t e2ttt_backward_scratch_bytes(const e2ttt_desc* desc) {
   Plan pl;
-  if (make_plan(desc, pl) != E2TTT_OK || desc->chunk > kMaxTrainChunk) return 0;
+  if (make_plan(desc, pl) != E2TTT_OK || !long_chunk_ok(*desc)) return 0;
   return pl.scratch_bytes;
 }
 
@@ -271,8 +283,7 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
-  if (!long_chunk_ok(*desc) || (save_for_backward && desc->chunk > kMaxTrainChunk))
-    return E2TTT_ERR_UNSUPPORTED;
+  if (!long_chunk_ok(*desc)) return E2TTT_ERR_UNSUPPORTED;
   if (!q || !k || !v || !eta || !beta || !w_in || !out || !w_out || !m_out || !workspace)
     return E2TTT_ERR_NULL_ARG;
   if (workspace_bytes < (save_for_backward ? pl.ws_bytes_save : pl.ws_bytes))
@@ -325,7 +336,7 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
-  if (desc->chunk > kMaxTrainChunk) return E2TTT_ERR_UNSUPPORTED;
+  if (!long_chunk_ok(*desc)) return E2TTT_ERR_UNSUPPORTED;
   if (!q || !k || !v || !eta || !beta || !w_in || !workspace || !d_out || !dq || !dk || !dv ||
       !d_eta || !d_beta || !d_w_in || !d_m_in || !scratch)
     return E2TTT_ERR_NULL_ARG;
@@ -362,6 +373,7 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   a.kwb = at<float>(scratch, pl.off_kwb);
   a.kmb = at<float>(scratch, pl.off_kmb);
   a.carryb = at<float>(scratch, pl.off_carryb);
+  a.bfrz = pl.tpc > 1 ? at<float>(scratch, pl.off_frz) : nullptr;
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
   a.eps = desc->ln_eps;

@@ -24,6 +24,8 @@
 //   zh = -(dYh mean(eZ) + e mean(dYh Z))/sigma - eh,  sigh = -sum(dYh dY)/sigma,
 // where LNb(x) = (x - mean x - Z mean(x Z)) / sigma (per token, over the head dim).
 // SwiGLU and the bare net (no residual LN) follow the same pattern.
+#include <algorithm>
+
 #include "chain_common.h"
 #include "pair_xchg.h"
 
@@ -344,7 +346,15 @@ __device__ __forceinline__ void flush_dkdq(const ChainArgs& a, long p, int parit
   }
 }
 
-template <class S>
+// LONG: chunks longer than the CM-row tile.  Their tiles are processed last
+// to first; every tile's P4 needs the adjoint state at the chunk end (Wb_C,
+// Mb_C) while P8 and P9 add the tile's contributions to Wb.  So Wb_C is kept
+// in a per-workgroup fp32 buffer from the chunk's first processed tile on; at
+// the end of each tile the contribution Wb - Wb_C moves to a second buffer and
+// Wb is reset to Wb_C; after the chunk's last processed tile (its first) the
+// transition Wb_0 = cw Wb_C + sum of contributions, Mb_0 = cm Wb_C + cb Mb_C
+// is applied once.
+template <class S, bool LONG>
 __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   using O = typename S::O;
   using E = typename S::E;
@@ -379,6 +389,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
   const float inv_d = 1.0f / D;
   const bool resln = a.resln != 0;
+  const int TPC = LONG ? (C + S::CM - 1) / S::CM : 1;   // tiles per chunk
+  const int TL = LONG ? S::CM : C;                       // tokens per tile
+  auto ntiles = [&](int rc) { return LONG ? (min(T, (rc + 1) * C) - rc * C + TL - 1) / TL : 1; };
+  constexpr int NB = NMAT * NJB * NIB * S::NT;            // float4 per frozen block
+  f32x4* const frz = LONG ? reinterpret_cast<f32x4*>(a.bfrz) + (long)blockIdx.x * 2 * NB : nullptr;
 
   PairX<S::NS> px;
   px.init(a.sync, a.npairs, sword);
@@ -397,10 +412,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   TileRegs<S> pK, pV, pQ, pD;
   F32TileRegs<S> pZ, pZq;
   float pkw = 0.0f, pkm = 0.0f, prk = 0.0f, prq = 0.0f, pcar = 0.0f;
-  auto prefetch_k = [&](long uu, int rc) {
+  auto prefetch_k = [&](long uu, int rc, int kt) {
     E2TTT_LANE_IDS;
-    const long r0 = uu * T + (long)rc * C;
-    const int ln = min(C, T - rc * C);
+    const int st = LONG ? rc * C + kt * TL : rc * C;
+    const long r0 = uu * T + st;
+    const int ln = LONG ? min(TL, min(T, (rc + 1) * C) - st) : min(C, T - st);
     pK.load(a.k, r0, ln, tid);
     pV.load(a.v, r0, ln, tid);
     pZ.load(a.zk, r0, ln, tid);
@@ -411,10 +427,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     }
     if (tid < 3) pcar = a.carry[(uu * NC + rc) * 3 + tid];
   };
-  auto prefetch_q = [&](long uu, int rc) {
+  auto prefetch_q = [&](long uu, int rc, int kt) {
     E2TTT_LANE_IDS;
-    const long r0 = uu * T + (long)rc * C;
-    const int ln = min(C, T - rc * C);
+    const int st = LONG ? rc * C + kt * TL : rc * C;
+    const long r0 = uu * T + st;
+    const int ln = LONG ? min(TL, min(T, (rc + 1) * C) - st) : min(C, T - st);
     pQ.load(a.q, r0, ln, tid);
     pD.load(a.d_out, r0, ln, tid);
     pZq.load(a.zq, r0, ln, tid);
@@ -429,17 +446,25 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       load_state<S>(Wb, a.d_w_out ? a.d_w_out + u * a.P : nullptr, dh, j0, w, g, c);
       load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, j0, w, g, c);
     }
-    int pend_r = -1, pend_par = 0;   // chunk whose dk, dq partials are not yet combined
-    prefetch_k(u, NC - 1);
+    // the tile whose dk, dq partials are not yet combined (first token, length)
+    int pend_s0 = -1, pend_len = 0, pend_par = 0;
+    prefetch_k(u, NC - 1, ntiles(NC - 1) - 1);
 
-    for (int r = NC - 1; r >= 0; --r, ++nch) {
-      const int s0 = r * C;
-      const int len = min(C, T - s0);
+    // tile kt of chunk r, last to first (always kt = 0 unless LONG)
+    for (int r = NC - 1, kt = ntiles(NC - 1) - 1; r >= 0; ++nch) {
+      const int s0 = LONG ? r * C + kt * TL : r * C;
+      const int cend = LONG ? min(T, (r + 1) * C) : 0;
+      const int len = LONG ? min(TL, cend - s0) : min(C, T - s0);
+      const bool firstp = !LONG || s0 + TL >= cend;   // the chunk's first tile processed (its last)
+      const bool lastp = !LONG || kt == 0;            // the chunk's last tile processed (its first)
+      const int rc = r, kc = kt;                      // this tile
+      if (kt > 0) --kt;
+      else if (--r >= 0) kt = ntiles(r) - 1;
       const long row0 = u * T + s0;
       const int par = (int)(nch & 1);
       const unsigned seq0 = px.seq_now();
       const char* ckW =
-          static_cast<const char*>(a.ckpt) + ((u * NC + r) * S::NS + rank) * 2 * a.ckpt_stride;
+          static_cast<const char*>(a.ckpt) + ((u * NC + rc) * S::NS + rank) * 2 * a.ckpt_stride;
       const char* ckM = ckW + a.ckpt_stride;
 
       // chunk-start weights W_0 (kept for the whole chunk) and momentum M_0
@@ -520,7 +545,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       __syncthreads();
 
       // ------------- carry adjoints: <Wb, W_0>, <Wb, M_0>, <Mb, M_0> (per wave)
-      {
+      if (firstp) {
         E2TTT_LANE_IDS;
         float pcw = 0.0f, pcm = 0.0f, pcb = 0.0f;
 #pragma unroll
@@ -542,6 +567,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         pcm = wave_sum(pcm);
         pcb = wave_sum(pcb);
         if (lane == 0) { cbp[w * 4 + 0] = pcw; cbp[w * 4 + 1] = pcm; cbp[w * 4 + 2] = pcb; }
+        if constexpr (LONG) {   // keep Wb_C for the chunk's other tiles
+#pragma unroll
+          for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+              for (int ib = 0; ib < NIB; ++ib)
+                frz[((m * NJB + jj) * NIB + ib) * S::NT + tid] = Wb.t[m][jj][ib];
+        }
       }
 
       // ----------- P4: first-order deltas, scalar-kernel adjoints, Hessian terms
@@ -709,7 +743,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
 
       // ------------------------------------ P5: adjoint state transition
-      {
+      // (LONG: once per chunk, after its last tile processed)
+      if constexpr (!LONG) {
         const float cw = scar[0], cm = scar[1], cbv = scar[2];
 #pragma unroll
         for (int m = 0; m < NMAT; ++m)
@@ -755,13 +790,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               load_row_part<EPL>(pdyh[it_][k], dyh_peer + (t0 + (lane >> 4)) * D + l16 * EPL);
           }
         }
-        if (pend_r >= 0)
-          flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
-                        tid);
+        if (pend_s0 >= 0)
+          flush_dkdq<S>(a, px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       }
 
       // ------------------------------------- P7: LayerNorm second order
-      prefetch_q(u, r);
+      prefetch_q(u, rc, kc);
       {
         E2TTT_LANE_IDS;
         using IOT = typename IoT<S::BF>::T;
@@ -930,7 +964,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           // A_Q and GELU'(H_Q) as the forward formed them (its query side at
           // W_0), loaded now so that they arrive under the staging and the
           // Yb_Q row phase below
-          const SavedAct<S> sv(static_cast<char*>(a.asave) + ((u * NC + r) * S::NS + rank) * a.as_stride);
+          const SavedAct<S> sv(static_cast<char*>(a.asave) +
+                               (((u * NC + rc) * TPC + kc) * S::NS + rank) * a.as_stride);
 #pragma unroll
           for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -945,7 +980,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         pZq.store(yk, tid);                             // Z_Q (or Y_Q)
         if (tid < S::CM) row[2 * tid] = prq;
         __syncthreads();
-        if (r > 0) prefetch_k(u, r - 1);
+        if (r >= 0) prefetch_k(u, r, kt);              // the next tile (r, kt advanced above)
 #pragma unroll 1
         for (int idx = tid; idx < D * S::CM; idx += S::NT) {
           const int i = idx % D, t = idx / D;
@@ -1103,15 +1138,40 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         kwb_slot[row0 + t] = sw;
         kmb_slot[row0 + t] = sm2;
       }
-      if (tid < 3) {
+      if (firstp && tid < 3) {
         float sacc = 0.0f;
         for (int ww = 0; ww < NW; ++ww) sacc += cbp[ww * 4 + tid];
-        carryb_slot[(u * NC + r) * 3 + tid] = sacc;
+        carryb_slot[(u * NC + rc) * 3 + tid] = sacc;
+      }
+      if constexpr (LONG) {
+        // Wb = Wb_C + this tile's contributions: move them to the second block
+        // and restore Wb_C, or (the chunk's last tile processed) apply the
+        // transition with all of them
+        const float cw = scar[0], cm = scar[1], cbv = scar[2];
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+              const long idx = ((m * NJB + jj) * NIB + ib) * S::NT + tid;
+              const f32x4 f = frz[idx];
+              const f32x4 dacc = firstp ? Wb.t[m][jj][ib] - f : frz[NB + idx] + (Wb.t[m][jj][ib] - f);
+              if (lastp) {
+                Wb.t[m][jj][ib] = cw * f + dacc;
+                Mb.t[m][jj][ib] = cm * f + cbv * Mb.t[m][jj][ib];
+              } else {
+                frz[NB + idx] = dacc;
+                Wb.t[m][jj][ib] = f;
+              }
+              sched_fence();
+            }
       }
       }
       if constexpr (S::NS > 1) {
         px.post();                                  // seq0 + 2: dk, dq partials
-        pend_r = r;
+        pend_s0 = s0;
+        pend_len = len;
         pend_par = par;
       } else {
         __syncthreads();
@@ -1121,9 +1181,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     if constexpr (S::NS > 1) {
       E2TTT_LANE_IDS;
       px.wait_for(px.seq_now(), sword);             // the peers' last post
-      if (pend_r >= 0)
-        flush_dkdq<S>(a, px.p, pend_par, u * T + (long)pend_r * C, min(C, T - pend_r * C), rlo,
-                      tid);
+      if (pend_s0 >= 0)
+        flush_dkdq<S>(a, px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       __syncthreads();
     }
     {
@@ -1134,30 +1193,52 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   }
 }
 
+// Long chunks are compiled where the forward has them (MLP on bf16, fp32).
+template <class S>
+constexpr bool has_long() { return !(S::BF && S::FW == 1); }
+
+template <class S, bool LONG>
+int occupancy() {
+  int v = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_bwd_kernel<S, LONG>, S::NT, 0) !=
+      hipSuccess)
+    v = 0;
+  return v;
+}
+
 template <class S>
 int max_blocks_per_cu() {
   static int nb = [] {
-    int v = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_bwd_kernel<S>, S::NT, 0) !=
-        hipSuccess)
-      v = 0;
+    int v = occupancy<S, false>();
+    if constexpr (has_long<S>()) v = std::min(v, occupancy<S, true>());
     return v;
   }();
   return nb;
 }
 
-template <class S>
-hipError_t launch(const ChainArgs& a, hipStream_t stream) {
+template <class S, bool LONG>
+hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
   if constexpr (S::NS == 1) {
-    hipLaunchKernelGGL(chain_bwd_kernel<S>, dim3((unsigned)a.U), dim3(S::NT), 0, stream, a);
+    hipLaunchKernelGGL((chain_bwd_kernel<S, LONG>), dim3((unsigned)a.U), dim3(S::NT), 0, stream,
+                       a);
     return hipGetLastError();
   } else {
     ChainArgs b = a;
     void* args[] = {&b};
-    return hipLaunchCooperativeKernel((const void*)chain_bwd_kernel<S>,
+    return hipLaunchCooperativeKernel((const void*)chain_bwd_kernel<S, LONG>,
                                       dim3((unsigned)(S::NS * a.npairs)), dim3(S::NT), args, 0,
                                       stream);
   }
+}
+
+template <class S>
+hipError_t launch(const ChainArgs& a, hipStream_t stream) {
+  if (a.C <= S::CM) return launch_as<S, false>(a, stream);
+  if constexpr (has_long<S>()) {
+    if (!a.bfrz) return hipErrorInvalidValue;
+    return launch_as<S, true>(a, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace

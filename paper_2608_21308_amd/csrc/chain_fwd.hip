@@ -158,7 +158,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       const bool first = !LONG || kt == 0;         // the chunk's first tile
       const int len = LONG ? min(TL, cend - s0) : min(C, T - s0);
       const bool more = LONG && s0 + TL < cend;    // another tile of this chunk follows
-      const int rc = r;
+      const int rc = r, kc = kt;                   // this tile
       if (more) ++kt; else { ++r; kt = 0; }
       const long row0 = u * T + s0;
       const int par = (int)(nch & 1);
@@ -352,7 +352,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // for this chunk's stores does not include it
       if (S::FW == 0 && a.asave) {
         E2TTT_LANE_IDS;
-        const SavedAct<S> sv(static_cast<char*>(a.asave) + ((u * NC + rc) * S::NS + rank) * a.as_stride);
+        const SavedAct<S> sv(static_cast<char*>(a.asave) +
+                             (((u * NC + rc) * TPC + kc) * S::NS + rank) * a.as_stride);
 #pragma unroll
         for (int tb = 0; tb < (S::FW == 0 ? NTB : 0); ++tb)
 #pragma unroll

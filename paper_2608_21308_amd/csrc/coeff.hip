@@ -93,18 +93,27 @@ __device__ __forceinline__ float wave_total(float v) {
 // segments from the last to the first, carrying the products of the later
 // segments' factors (for the suffix products) and S at the next segment's
 // first token (for the affine recursion S_t = g~_t + beta_{t+1} S_{t+1}).
-__device__ void coeff_fwd_long(const CoeffFwdArgs& a, long wid, long base, int len, int lane) {
+constexpr int kMaxSeg = 8;   // 512 / 64
+
+struct LongScalars {
+  float S[kMaxSeg], bt[kMaxSeg], gt[kMaxSeg];   // per segment, this lane's token
+  float carry[3];                                // (g~_0, beta_1 S_1, b~_0)
+};
+
+__device__ __forceinline__ void long_scalars(const float* eta, const float* beta,
+                                             const float* gamma, long base, int len, int lane,
+                                             LongScalars& o) {
   float cb = 1.0f, cg = 1.0f;           // products of beta, gamma over the later segments
   float s_next = 0.0f, b_next = 1.0f;   // S and beta at the next segment's first token
-  float b0 = 1.0f, S0 = 0.0f, pb0 = 1.0f, pg0 = 1.0f;
   const int nseg = (len + 63) / 64;
-  for (int seg = nseg - 1; seg >= 0; --seg) {
+#pragma unroll
+  for (int seg = kMaxSeg - 1; seg >= 0; --seg) {
+    if (seg >= nseg) continue;          // uniform
     const long sb = base + seg * 64;
     const int n = min(64, len - seg * 64);
     const bool valid = lane < n;
-    const float e = valid ? a.eta[sb + lane] : 0.0f;
-    const float b = valid ? a.beta[sb + lane] : 1.0f;
-    const float gm = (valid && a.gamma) ? a.gamma[sb + lane] : 1.0f;
+    const float b = valid ? beta[sb + lane] : 1.0f;
+    const float gm = (valid && gamma) ? gamma[sb + lane] : 1.0f;
     float pb = b, pg = gm;
 #pragma unroll
     for (int k = 1; k < 64; k <<= 1) {
@@ -116,11 +125,10 @@ __device__ void coeff_fwd_long(const CoeffFwdArgs& a, long wid, long base, int l
     bt *= cb;                            // exclusive suffix products over the whole chunk
     gt *= cg;
     const float bnext = __shfl_down(b, 1, 64);
-    const bool last_seg = seg == nseg - 1;
     float A, B;
     if (lane < n - 1) { A = gt; B = bnext; }
     else if (lane == n - 1) {
-      if (last_seg) { A = 1.0f; B = 0.0f; }
+      if (seg == nseg - 1) { A = 1.0f; B = 0.0f; }
       else { A = gt + b_next * s_next; B = 0.0f; }
     } else { A = 0.0f; B = 0.0f; }
 #pragma unroll
@@ -128,21 +136,37 @@ __device__ void coeff_fwd_long(const CoeffFwdArgs& a, long wid, long base, int l
       const float oA = __shfl_down(A, k, 64), oB = __shfl_down(B, k, 64);
       if (lane + k < 64) { A = A + B * oA; B = B * oB; }
     }
-    if (valid) {
-      a.kw[sb + lane] = e * A;
-      a.km[sb + lane] = e * bt;
-    }
+    o.S[seg] = A;
+    o.bt[seg] = bt;
+    o.gt[seg] = gt;
     s_next = __shfl(A, 0, 64);
     b_next = __shfl(b, 0, 64);
-    const float segb = __shfl(pb, 0, 64), segg = __shfl(pg, 0, 64);
-    cb *= segb;
-    cg *= segg;
-    if (seg == 0) { b0 = b_next; S0 = s_next; pb0 = cb; pg0 = cg; }
+    cb *= __shfl(pb, 0, 64);
+    cg *= __shfl(pg, 0, 64);
+  }
+  o.carry[0] = cg;
+  o.carry[1] = b_next * s_next;
+  o.carry[2] = cb;
+}
+
+__device__ void coeff_fwd_long(const CoeffFwdArgs& a, long wid, long base, int len, int lane) {
+  LongScalars o;
+  long_scalars(a.eta, a.beta, a.gamma, base, len, lane, o);
+  const int nseg = (len + 63) / 64;
+#pragma unroll
+  for (int seg = 0; seg < kMaxSeg; ++seg) {
+    if (seg >= nseg) break;
+    const long sb = base + seg * 64;
+    if (lane < min(64, len - seg * 64)) {
+      const float e = a.eta[sb + lane];
+      a.kw[sb + lane] = e * o.S[seg];
+      a.km[sb + lane] = e * o.bt[seg];
+    }
   }
   if (lane == 0) {
-    a.carry[wid * 3 + 0] = pg0;
-    a.carry[wid * 3 + 1] = b0 * S0;
-    a.carry[wid * 3 + 2] = pb0;
+    a.carry[wid * 3 + 0] = o.carry[0];
+    a.carry[wid * 3 + 1] = o.carry[1];
+    a.carry[wid * 3 + 2] = o.carry[2];
   }
 }
 
@@ -200,6 +224,68 @@ __global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
 // the same scans:  S-bar accumulates through an ascending affine scan, and the
 // suffix-product adjoints are pushed to the factors with ascending affine
 // scans as well (no division by beta or gamma).
+// Backward of a long chunk: the same adjoint recursions as the single-wave
+// kernel below, walked over the chunk's segments from the first to the last
+// (every scan is ascending); each segment's scans start from the previous
+// segment's last values (S-hat, Y, Z, and the previous token's beta, gamma and
+// K^M eta), which enter lane 0 as x_0 = a_0 + b_0 x_{-1}.
+__device__ void coeff_bwd_long(const CoeffBwdArgs& a, long wid, long base, int len, int lane,
+                               float cwb, float cmb, float cbb) {
+  LongScalars o;
+  long_scalars(a.eta, a.beta, a.gamma, base, len, lane, o);
+  const int nseg = (len + 63) / 64;
+  float sh_last = 0.0f, kme_last = 0.0f, b_last = 1.0f, g_last = 1.0f, y_last = 0.0f,
+        z_last = 0.0f;
+#pragma unroll
+  for (int seg = 0; seg < kMaxSeg; ++seg) {
+    if (seg >= nseg) break;
+    const long sb = base + seg * 64;
+    const int n = min(64, len - seg * 64);
+    const bool valid = lane < n;
+    const float e = valid ? a.eta[sb + lane] : 0.0f;
+    const float b = valid ? a.beta[sb + lane] : 1.0f;
+    const float gm = (valid && a.gamma) ? a.gamma[sb + lane] : 1.0f;
+    float kwb = 0.0f, kmb = 0.0f;
+    for (int sl = 0; sl < a.ns; ++sl) {
+      if (valid) {
+        kwb += a.kwb[sl * a.tok_slot + sb + lane];
+        kmb += a.kmb[sl * a.tok_slot + sb + lane];
+      }
+    }
+    const float S = o.S[seg], bt = o.bt[seg], gt = o.gt[seg];
+    const bool t0 = seg == 0 && lane == 0;            // the chunk's first token
+    const float etab = kwb * S + kmb * bt;
+    float Sb = kwb * e;
+    float betab = 0.0f;
+    if (t0) { Sb += cmb * b; betab = cmb * S; }
+    if (seg > 0 && lane == 0) Sb += b * sh_last;
+    const float Sh = affine_scan_up(Sb, b, lane);
+    float Sh_prev = __shfl_up(Sh, 1, 64);
+    float kme_prev = __shfl_up(kmb * e, 1, 64);
+    float b_prev = __shfl_up(b, 1, 64);
+    float g_prev = __shfl_up(gm, 1, 64);
+    if (lane == 0) { Sh_prev = sh_last; kme_prev = kme_last; b_prev = b_last; g_prev = g_last; }
+    if (!t0) betab += Sh_prev * S;
+    float btb = t0 ? cbb : kme_prev;
+    float gtb = t0 ? cwb : Sh_prev;
+    if (seg > 0 && lane == 0) { btb += b_prev * y_last; gtb += g_prev * z_last; }
+    const float Y = affine_scan_up(btb, b_prev, lane);
+    const float Z = affine_scan_up(gtb, g_prev, lane);
+    betab += bt * Y;
+    if (valid) {
+      a.d_eta[sb + lane] = etab;
+      a.d_beta[sb + lane] = betab;
+      if (a.d_gamma) a.d_gamma[sb + lane] = gt * Z;
+    }
+    sh_last = __shfl(Sh, 63, 64);
+    kme_last = __shfl(kmb * e, 63, 64);
+    b_last = __shfl(b, 63, 64);
+    g_last = __shfl(gm, 63, 64);
+    y_last = __shfl(Y, 63, 64);
+    z_last = __shfl(Z, 63, 64);
+  }
+}
+
 __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
   const long wid = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (wid >= a.nwork) return;
@@ -223,11 +309,22 @@ __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
   }
   if (a.averaged) {
     const float inv = 1.0f / (float)len;
-    if (valid) {
-      a.d_eta[base + lane] = kwb + kmb;
-      a.d_beta[base + lane] = (cmb + cbb) * inv;
-      if (a.d_gamma) a.d_gamma[base + lane] = cwb * inv;
+    for (int t0 = 0; t0 < len; t0 += 64) {
+      const int t = t0 + lane;
+      if (t >= len) continue;
+      float kw2 = 0.0f, km2 = 0.0f;
+      for (int sl = 0; sl < a.ns; ++sl) {
+        kw2 += a.kwb[sl * a.tok_slot + base + t];
+        km2 += a.kmb[sl * a.tok_slot + base + t];
+      }
+      a.d_eta[base + t] = kw2 + km2;
+      a.d_beta[base + t] = (cmb + cbb) * inv;
+      if (a.d_gamma) a.d_gamma[base + t] = cwb * inv;
     }
+    return;
+  }
+  if (len > 64) {
+    coeff_bwd_long(a, wid, base, len, lane, cwb, cmb, cbb);
     return;
   }
   ChunkScalars s = chunk_scalars(a.eta, a.beta, a.gamma, base, len, lane);

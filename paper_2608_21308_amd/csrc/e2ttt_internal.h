@@ -74,7 +74,12 @@ struct ChainArgs {
   // by the forward for the backward's output branch (nullable in the forward;
   // layout: SavedAct in chain_common.h)
   void* asave;
-  long as_stride;       // bytes per (unit, chunk, rank) block
+  long as_stride;       // bytes per (unit, chunk tile, rank) block
+  // backward of chunks longer than one tile: per workgroup, the adjoint state
+  // at the chunk end and the sum of the tiles' contributions to its update
+  // (fp32, in the register-tile order of the state), two blocks of
+  // chain_frz_floats(cfg) floats each
+  float* bfrz;
   // LN outputs saved by the forward for the backward (nullable in the forward):
   // Z = LN(Y) (Y itself without the residual LN) [U][T][d], 1/sigma [U][T]
   float* zk;
@@ -130,6 +135,8 @@ hipError_t launch_zero_words(unsigned* p, long n, hipStream_t stream);
 long chain_max_pairs(const ChainConfig& cfg, bool backward);
 // Bytes of one checkpoint block (W or M of one unit's workgroup at one chunk start).
 long chain_ckpt_bytes(const ChainConfig& cfg);
+// floats of one workgroup's frozen adjoint-state block (long-chunk backward)
+long chain_frz_floats(const ChainConfig& cfg);
 // Bytes of one saved-activation block (one unit's workgroup, one chunk); 0 when
 // the backward recomputes the activations instead (SwiGLU).
 long chain_saved_act_bytes(const ChainConfig& cfg);

@@ -201,20 +201,24 @@ def test_apply_argument_errors(lib):
     assert lib.e2ttt_apply(ctypes.byref(d), f, ctypes.c_void_p(260), f, None) == 2
 
 
-def test_long_chunks_are_forward_only(lib):
-    """Chunks of 65..512 tokens: forward without saving, on the MLP bf16 and
-    fp32 variants; everything that would need the backward (or SwiGLU on bf16)
-    is refused before any launch."""
+def test_long_chunks(lib):
+    """Chunks of 65..512 tokens run on the MLP bf16 and fp32 variants (forward
+    and backward); SwiGLU on bf16 is refused before any launch."""
     f = ctypes.c_void_p(16)   # never dereferenced
     for kw in (dict(chunk=128), dict(chunk=512), dict(io=0, d=16, dh=64, chunk=200)):
         d = desc(**kw)
         assert lib.e2ttt_param_count(ctypes.byref(d)) > 0
-        assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 0) > 0
-        assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 1) == 0
-        assert lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) == 0
-        assert lib.e2ttt_chunk_forward(ctypes.byref(d), *([f] * 12), 1 << 40, 1, None) == 3
-        assert lib.e2ttt_chunk_backward(ctypes.byref(d), *([f] * 9), 1 << 40, *([f] * 12),
-                                        1 << 40, None) == 3
+        ws0 = lib.e2ttt_workspace_bytes(ctypes.byref(d), 0)
+        ws1 = lib.e2ttt_workspace_bytes(ctypes.byref(d), 1)
+        assert 0 < ws0 < ws1
+        short = desc(**dict(kw, chunk=64))
+        # the backward scratch adds two fp32 copies of each workgroup's state share
+        assert (lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) >
+                lib.e2ttt_backward_scratch_bytes(ctypes.byref(short)))
     d = desc(fw=1, dh=172, chunk=128)   # SwiGLU on bf16: chunks of at most 64
     assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 0) == 0
+    assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 1) == 0
+    assert lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) == 0
     assert lib.e2ttt_chunk_forward(ctypes.byref(d), *([f] * 12), 1 << 40, 0, None) == 3
+    assert lib.e2ttt_chunk_backward(ctypes.byref(d), *([f] * 9), 1 << 40, *([f] * 12),
+                                    1 << 40, None) == 3

@@ -1,14 +1,14 @@
 """GPU parity of chunks longer than one 64-row tile (C up to 512, the paper's
 setting, Sec. 5): the forward runs a chunk as consecutive tiles that all take
 gradients and outputs at the chunk-start weights, and Prop. 1 over the whole
-chunk sets the next state.  The oracle computes the token recurrence of eq.
+chunk sets the next state; the backward runs the tiles last to first against
+the adjoint state at the chunk end and applies the transition once.  The oracle computes the token recurrence of eq.
 (7) with any chunk length.
 
 Bars: the scalar kernels within 1e-5 relative (fp32 scans over up to 512
-factors); the forward at rel-L2 1e-5 for fp32 io (widened only by the case's
-own fp32 conditioning, as for short chunks) and 2e-2 for bf16 io.  Long
-chunks are forward-only: saving for the backward, the backward and SwiGLU on
-bf16 are refused with E2TTT_ERR_UNSUPPORTED.
+factors); forward and backward at rel-L2 1e-5 for fp32 io (widened only by
+the case's own fp32 conditioning, as for short chunks) and 2e-2 for bf16 io.
+SwiGLU on bf16 keeps chunks of at most 64 tokens (E2TTT_ERR_UNSUPPORTED).
 """
 import numpy as np
 import pytest
@@ -119,21 +119,51 @@ def test_long_chunk_1p3b_layer_sampled_units():
     assert all(e <= TOL["bf16"] for e in errs.values()), errs
 
 
-def test_long_chunks_refused_where_unsupported():
-    w = WL.WORKLOADS[1].with_(B=1, H=2, T=256, C=128)
-    x = WL.make_inputs(w, with_grads=False)
-    t = to_dev(x, "bf16")
-    with pytest.raises(e2ttt.E2TTTError, match="unsupported"):   # saving for the backward
-        e2ttt.forward(config_of(w), t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
-                      t["w_in"], None, workspace=torch.empty(1 << 20, dtype=torch.uint8,
-                                                             device="cuda"),
-                      save_for_backward=True)
+def test_long_chunks_refused_for_swiglu_bf16():
     ws = WL.WORKLOADS[2].with_(B=1, H=2, T=256, C=128)
     xs = to_dev(WL.make_inputs(ws, with_grads=False), "bf16")
-    with pytest.raises(e2ttt.E2TTTError, match="unsupported"):   # SwiGLU on bf16
+    with pytest.raises(e2ttt.E2TTTError, match="unsupported"):
         e2ttt.forward(config_of(ws), xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"],
                       xs["gamma"], xs["w_in"], None,
                       workspace=torch.empty(1 << 20, dtype=torch.uint8, device="cuda"))
+
+
+# ---------------------------------------------------------------- backward
+@pytest.mark.parametrize("fw", [WL.FW_MLP, WL.FW_SWIGLU])
+@pytest.mark.parametrize("T,C,flags", [(300, 128, 0), (230, 200, 0), (600, 512, 1),
+                                       (150, 65, 0)])
+def test_long_chunk_backward_fp32(fw, T, C, flags):
+    from tests.test_gpu_backward import errors as berrors, gpu_fwd_bwd, oracle_bwd, \
+        with_state_inputs
+    w = WL.WORKLOADS[0].with_(fw=fw, B=2, H=2, T=T, C=C, backward=True, seed=1600 + T + C)
+    x = with_state_inputs(WL.make_inputs(w), 13 + T)
+    errs = berrors(gpu_fwd_bwd(w, x, flags), oracle_bwd(w, x, flags))
+    sens = fp32_sensitivity(lambda y: oracle_bwd(w, y, flags), x)
+    what = "long bwd fp32 fw=%d T=%d C=%d flags=%d" % (fw, T, C, flags)
+    print(what, {k: "%.2e" % v for k, v in errs.items()},
+          "sens", {k: "%.1e" % v for k, v in sens.items()}, flush=True)
+    bad = {n: e for n, e in errs.items() if not e <= max(TOL["f32"], 10 * sens[n])}
+    assert not bad, what + ": %s" % bad
+
+
+@pytest.mark.parametrize("T,C,dh", [(1100, 512, 256), (700, 512, 64), (600, 128, 256),
+                                    (300, 100, 120)])
+def test_long_chunk_backward_bf16(T, C, dh):
+    from tests.test_gpu_backward import errors as berrors, gpu_fwd_bwd, oracle_bwd, \
+        with_state_inputs
+    w = WL.WORKLOADS[1].with_(B=2, H=2, T=T, C=C, dh=dh, backward=True, seed=1700 + T + dh)
+    x = with_state_inputs(WL.make_inputs(w), T, m_scale=1e-2)
+    errs = berrors(gpu_fwd_bwd(w, x), oracle_bwd(w, x))
+    print("long bwd bf16 T=%d C=%d dh=%d" % (T, C, dh), {k: "%.2e" % v for k, v in errs.items()},
+          flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+def test_long_chunk_averaged_rule_backward():
+    # the chunk-averaged rule over 512-token chunks (its paper setting)
+    from tests.test_gpu_averaged import compare, with_state
+    w = WL.WORKLOADS[1].with_(B=1, H=2, T=600, C=512, dh=256, backward=True, seed=1800)
+    compare(w, with_state(WL.make_inputs(w), 3, 1e-2), 0, "avg bf16 C=512")
 
 
 def state_rounding_sensitivity(w, x, flags, seed=0):
