@@ -47,12 +47,11 @@
  * Supported shapes: io = BF16 with d = 64 (dh <= 256 for the MLP, <= 192 for
  * SwiGLU), or io = F32 with d = 16 (dh <= 128); dh is padded inside the
  * library to a multiple of 16; 1 <= chunk <= 64 everywhere, and chunks of
- * 65..512 tokens (the paper's C = 512) in e2ttt_chunk_forward without
- * save_for_backward for the GELU MLP on bf16 and both nets on fp32 (the
- * chunk runs as 64-token tiles that all take gradients and outputs at the
- * chunk-start weights; the backward and e2ttt_workspace_bytes(.., 1) refuse
- * them); T >= 1 with a ragged last chunk of T mod chunk tokens allowed
- * (Prop. 1 holds for any chunk length).
+ * 65..512 tokens (the paper's C = 512) for the GELU MLP on bf16 and both
+ * nets on fp32, forward and backward (the chunk runs as 64-token tiles that
+ * all take gradients and outputs at the chunk-start weights; SwiGLU on bf16
+ * refuses chunks above 64); T >= 1 with a ragged last chunk of T mod chunk
+ * tokens allowed (Prop. 1 holds for any chunk length).
  * bf16 tensors use MFMA bf16 operands with fp32 accumulation and fp32 state;
  * f32 tensors use fp32 MFMA throughout.  Anything else returns
  * E2TTT_ERR_UNSUPPORTED.
