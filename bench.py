@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+PEAK_F32_TFLOPS = 157.3          # MI355X dense fp32 MFMA
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chain_bwd_mlp_1p3b_traffic.json")
 METRIC = "E²-TTT layer fwd+bwd tokens/s (H=16,d=64,T=4096) + MFMA util %"
 
@@ -52,7 +53,8 @@ def cpu_baseline(w, seconds_hint: float = 20.0) -> dict:
     from paper_2608_21308_amd import workloads as WL
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
     threads = max(1, min(threads, os.cpu_count() or 1))
-    n_units = min(threads, w.B * w.H)
+    # three units per thread: about 10 s of wall time on 16 cores
+    n_units = min(3 * threads, w.B * w.H)
     x = WL.make_inputs(w, units=list(range(n_units)))
     t0 = time.perf_counter()
     oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"], x["w_in"], None, C=w.C,
@@ -195,6 +197,107 @@ def time_decode(e2ttt, w, x, dev, reps: int = 200) -> dict:
     return res
 
 
+def measure_peaks(dev) -> dict:
+    """What this MI355X reaches on the two roofline resources: a dense bf16 GEMM
+    (torch.matmul, 8192^3, hipBLASLt) and a device-to-device copy of 1 GiB
+    (read + write bytes), each timed with HIP events over back-to-back calls.
+    Reported beside the published peaks the roofline fractions use."""
+    import torch
+    res = {}
+    n = 8192
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    c = torch.empty(n, n, device=dev, dtype=torch.bfloat16)
+    for _ in range(3):
+        torch.matmul(a, b, out=c)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    reps = 20
+    ev[0].record()
+    for _ in range(reps):
+        torch.matmul(a, b, out=c)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    res["bf16_gemm_TFLOPs"] = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    res["bf16_gemm_frac_of_published"] = res["bf16_gemm_TFLOPs"] / PEAK_BF16_TFLOPS
+    del a, b, c
+    nb = 1 << 30
+    src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        dst.copy_(src)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    res["copy_GBs"] = 2.0 * nb / (ms * 1e-3) / 1e9
+    res["copy_frac_of_published"] = res["copy_GBs"] / PEAK_HBM_GBS
+    res["shapes"] = "gemm %dx%dx%d bf16 (torch.matmul); copy 1 GiB device to device" % (n, n, n)
+    return res
+
+
+def time_workloads(e2ttt, WL, dev, reps: int = 10) -> dict:
+    """The other synthetic workloads at their own shapes (parity-test cases,
+    timed here as context): every pass they include, back to back, HIP events
+    around each call; tokens/s counts B*T per forward (+ backward) pass."""
+    import torch
+    res = {}
+    for w in (WL.WORKLOADS[0], WL.WORKLOADS[1], WL.WORKLOADS[2], WL.WORKLOADS[4]):
+        x = WL.make_inputs(w)
+        bf = w.io == "bf16"
+        t = {}
+        for n, a in x.items():
+            if a is None:
+                t[n] = None
+                continue
+            ten = torch.from_numpy(a).to(dev)
+            t[n] = ten.to(torch.bfloat16) if (bf and n in ("q", "k", "v", "d_out")) else ten
+        cfg = e2ttt.Config(w.B, w.H, w.T, w.d, w.dh, w.C, w.fw,
+                           e2ttt.DT_BF16 if bf else e2ttt.DT_F32)
+        ws = e2ttt.alloc_workspace(cfg, w.backward, dev)
+        out = torch.empty_like(t["q"])
+        wo, mo = torch.empty_like(t["w_in"]), torch.empty_like(t["w_in"])
+        scratch = (torch.empty(e2ttt.backward_scratch_bytes(cfg), dtype=torch.uint8, device=dev)
+                   if w.backward else None)
+        grads = None
+        if w.backward:
+            grads = dict(dq=torch.empty_like(t["q"]), dk=torch.empty_like(t["k"]),
+                         dv=torch.empty_like(t["v"]), d_eta=torch.empty_like(t["eta"]),
+                         d_beta=torch.empty_like(t["beta"]), d_gamma=torch.empty_like(t["gamma"]),
+                         d_w_in=torch.empty_like(t["w_in"]), d_m_in=torch.empty_like(t["w_in"]))
+
+        def step():
+            e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                          t["w_in"], None, out=out, w_out=wo, m_out=mo, workspace=ws,
+                          save_for_backward=w.backward)
+            if w.backward:
+                e2ttt.backward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                               t["w_in"], None, ws, t["d_out"], grads=grads, scratch=scratch)
+
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(reps):
+            step()
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / reps
+        units = (9 + 18 * w.backward) if w.fw == WL.FW_MLP else (13 + 26 * w.backward)
+        flop = float(units) * 2.0 * w.d * w.dh * w.T * w.B * w.H
+        peak = PEAK_BF16_TFLOPS if bf else PEAK_F32_TFLOPS
+        res[w.name] = {"pass": "fwd+bwd" if w.backward else "fwd", "ms": ms,
+                       "tokens_per_s": w.B * w.T / (ms * 1e-3),
+                       "mfma_frac": flop / (ms * 1e-3) / 1e12 / peak,
+                       "peak_TFLOPs": peak, "units_x_chunks": "%d x %d" % (w.units, w.n_chunks)}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -331,6 +434,8 @@ def main():
         res["long_chunk_forward"] = time_long_chunk(e2ttt, w, t, dev)
         res["gates"] = time_gates(e2ttt, w, dev)
         res["decode"] = time_decode(e2ttt, w, x, dev)
+        res["other_workloads"] = time_workloads(e2ttt, WL, dev)
+        res["peaks_measured"] = measure_peaks(dev)
     if args.no_cpu_baseline:
         res["cpu_baseline"] = None
     else:
