@@ -388,12 +388,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int T = a.T, C = a.C, NC = a.NC, dh = a.dh;
   const float inv_d = 1.0f / D;
-  const bool resln = a.resln != 0;
+  const bool resln = E2TTT_ARG(resln) != 0;
   const int TPC = LONG ? (C + S::CM - 1) / S::CM : 1;   // tiles per chunk
   const int TL = LONG ? S::CM : C;                       // tokens per tile
   auto ntiles = [&](int rc) { return LONG ? (min(T, (rc + 1) * C) - rc * C + TL - 1) / TL : 1; };
   constexpr int NB = NMAT * NJB * NIB * S::NT;            // float4 per frozen block
-  f32x4* const frz = LONG ? reinterpret_cast<f32x4*>(a.bfrz) + (long)blockIdx.x * 2 * NB : nullptr;
+  f32x4* const frz = LONG ? reinterpret_cast<f32x4*>(E2TTT_ARG(bfrz)) + (long)blockIdx.x * 2 * NB : nullptr;
 
   PairX<S::NS> px;
   px.init(a.sync, a.npairs, sword);
@@ -402,9 +402,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   const long NP = (S::NS > 1) ? a.npairs : (long)gridDim.x;
   const int rlo = rank * RPW;
   const int rhi = min(S::CM, rlo + RPW);
-  float* const kwb_slot = a.kwb + rank * a.U * T;
-  float* const kmb_slot = a.kmb + rank * a.U * T;
-  float* const carryb_slot = a.carryb + rank * a.U * NC * 3;
+  float* const kwb_slot = E2TTT_ARG(kwb) + rank * a.U * T;
+  float* const kmb_slot = E2TTT_ARG(kmb) + rank * a.U * T;
+  float* const carryb_slot = E2TTT_ARG(carryb) + rank * a.U * NC * 3;
   long nch = 0;   // chunks processed by this workgroup (exchange parity)
 
   // inputs loaded ahead of use: the K side of the next chunk during the output
@@ -417,25 +417,25 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     const int st = LONG ? rc * C + kt * TL : rc * C;
     const long r0 = uu * T + st;
     const int ln = LONG ? min(TL, min(T, (rc + 1) * C) - st) : min(C, T - st);
-    pK.load(a.k, r0, ln, tid);
-    pV.load(a.v, r0, ln, tid);
-    pZ.load(a.zk, r0, ln, tid);
+    pK.load(E2TTT_ARG(k), r0, ln, tid);
+    pV.load(E2TTT_ARG(v), r0, ln, tid);
+    pZ.load(E2TTT_ARG(zk), r0, ln, tid);
     if (tid < S::CM) {
-      pkw = (tid < ln) ? a.kw[r0 + tid] : 0.0f;
-      pkm = (tid < ln) ? a.km[r0 + tid] : 0.0f;
-      prk = (tid < ln) ? a.rk[r0 + tid] : 0.0f;
+      pkw = (tid < ln) ? E2TTT_ARG(kw)[r0 + tid] : 0.0f;
+      pkm = (tid < ln) ? E2TTT_ARG(km)[r0 + tid] : 0.0f;
+      prk = (tid < ln) ? E2TTT_ARG(rk)[r0 + tid] : 0.0f;
     }
-    if (tid < 3) pcar = a.carry[(uu * NC + rc) * 3 + tid];
+    if (tid < 3) pcar = E2TTT_ARG(carry)[(uu * NC + rc) * 3 + tid];
   };
   auto prefetch_q = [&](long uu, int rc, int kt) {
     E2TTT_LANE_IDS;
     const int st = LONG ? rc * C + kt * TL : rc * C;
     const long r0 = uu * T + st;
     const int ln = LONG ? min(TL, min(T, (rc + 1) * C) - st) : min(C, T - st);
-    pQ.load(a.q, r0, ln, tid);
-    pD.load(a.d_out, r0, ln, tid);
-    pZq.load(a.zq, r0, ln, tid);
-    if (tid < S::CM) prq = (tid < ln) ? a.rq[r0 + tid] : 0.0f;
+    pQ.load(E2TTT_ARG(q), r0, ln, tid);
+    pD.load(E2TTT_ARG(d_out), r0, ln, tid);
+    pZq.load(E2TTT_ARG(zq), r0, ln, tid);
+    if (tid < S::CM) prq = (tid < ln) ? E2TTT_ARG(rq)[r0 + tid] : 0.0f;
   };
 
   for (long u = px.p; u < a.U; u += NP) {
@@ -443,8 +443,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     StateTiles<S> Wb, Mb;
     {
       E2TTT_LANE_IDS;
-      load_state<S>(Wb, a.d_w_out ? a.d_w_out + u * a.P : nullptr, dh, j0, w, g, c);
-      load_state<S>(Mb, a.d_m_out ? a.d_m_out + u * a.P : nullptr, dh, j0, w, g, c);
+      load_state<S>(Wb, E2TTT_ARG(d_w_out) ? E2TTT_ARG(d_w_out) + u * a.P : nullptr, dh, j0, w, g, c);
+      load_state<S>(Mb, E2TTT_ARG(d_m_out) ? E2TTT_ARG(d_m_out) + u * a.P : nullptr, dh, j0, w, g, c);
     }
     // the tile whose dk, dq partials are not yet combined (first token, length)
     int pend_s0 = -1, pend_len = 0, pend_par = 0;
@@ -463,9 +463,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       const long row0 = u * T + s0;
       const int par = (int)(nch & 1);
       const unsigned seq0 = px.seq_now();
-      const char* ckW =
-          static_cast<const char*>(a.ckpt) + ((u * NC + rc) * S::NS + rank) * 2 * a.ckpt_stride;
-      const char* ckM = ckW + a.ckpt_stride;
+      const char* ckW = static_cast<const char*>(E2TTT_ARG(ckpt)) +
+                        ((u * NC + rc) * S::NS + rank) * 2 * E2TTT_ARG(ckpt_stride);
+      const char* ckM = ckW + E2TTT_ARG(ckpt_stride);
 
       // chunk-start weights W_0 (kept for the whole chunk) and momentum M_0
       // (for the carry adjoints), issued first so that P0 and P3 hide them
@@ -772,7 +772,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       float pdyh[S::NS > 1 ? P7IT : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
         E2TTT_LANE_IDS;
-        float* mine = bwd_slot<S>(a.xbuf, px.p, rank, par);
+        float* mine = bwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par);
 #pragma unroll 1
         for (int v = tid; v < S::CM * D / 4; v += S::NT)
           reinterpret_cast<float4*>(mine)[v] = reinterpret_cast<const float4*>(dyh)[v];
@@ -782,7 +782,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         // below (which would otherwise order each step's loads after them)
 #pragma unroll
         for (int k = 0; k < NPEER; ++k) {
-          const float* dyh_peer = bwd_slot<S>(a.xbuf, px.p, other_rank(k, rank), par);
+          const float* dyh_peer = bwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par);
 #pragma unroll
           for (int it_ = 0; it_ < P7IT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * NW;
@@ -799,7 +799,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         using IOT = typename IoT<S::BF>::T;
-        IOT* dvp = reinterpret_cast<IOT*>(a.dv) + row0 * D;
+        IOT* dvp = reinterpret_cast<IOT*>(E2TTT_ARG(dv)) + row0 * D;
 #pragma unroll
         for (int it_ = 0; it_ < P7IT; ++it_) {
           const int t0 = 4 * w + it_ * 4 * NW;
@@ -941,10 +941,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         }
         const float ksign = (resln && rank == 0) ? -1.0f : 0.0f;
         if constexpr (S::NS > 1) {
-          jacc_store_f32<S>(dkacc, bwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D,
+          jacc_store_f32<S>(dkacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) + S::CM * D,
                             [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
         } else {
-          jacc_store_io<S>(dkacc, a.dk, row0, len,
+          jacc_store_io<S>(dkacc, E2TTT_ARG(dk), row0, len,
                            [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
         }
       }
@@ -964,8 +964,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           // A_Q and GELU'(H_Q) as the forward formed them (its query side at
           // W_0), loaded now so that they arrive under the staging and the
           // Yb_Q row phase below
-          const SavedAct<S> sv(static_cast<char*>(a.asave) +
-                               (((u * NC + rc) * TPC + kc) * S::NS + rank) * a.as_stride);
+          const SavedAct<S> sv(static_cast<char*>(E2TTT_ARG(asave)) +
+                               (((u * NC + rc) * TPC + kc) * S::NS + rank) * E2TTT_ARG(as_stride));
 #pragma unroll
           for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -1115,11 +1115,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         }
         const float qsign = (resln && rank == 0) ? 1.0f : 0.0f;
         if constexpr (S::NS > 1) {
-          jacc_store_f32<S>(dqacc, bwd_slot<S>(a.xbuf, px.p, rank, par) + 2 * S::CM * D,
+          jacc_store_f32<S>(dqacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) + 2 * S::CM * D,
                             [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); },
                             w, g, c);
         } else {
-          jacc_store_io<S>(dqacc, a.dq, row0, len,
+          jacc_store_io<S>(dqacc, E2TTT_ARG(dq), row0, len,
                            [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); },
                            w, g, c);
         }
@@ -1187,8 +1187,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     }
     {
       E2TTT_LANE_IDS;
-      store_state<S>(Wb, a.d_w_in + u * a.P, dh, j0, w, g, c);
-      store_state<S>(Mb, a.d_m_in + u * a.P, dh, j0, w, g, c);
+      store_state<S>(Wb, E2TTT_ARG(d_w_in) + u * a.P, dh, j0, w, g, c);
+      store_state<S>(Mb, E2TTT_ARG(d_m_in) + u * a.P, dh, j0, w, g, c);
     }
   }
 }

@@ -77,6 +77,24 @@ __device__ __forceinline__ void opaque_state(StateTiles<S>& st) {
       for (int ib = 0; ib < S::NIB; ++ib) asm volatile("" : "+v"(st.t[m][jj][ib]));
 }
 
+// A field of the chain kernels' argument block (their only parameter, at
+// offset 0 of the kernel-argument segment), read from that segment where it
+// is used.  Read as `a.field`, every pointer of the block stays in scalar
+// registers for the whole kernel; with the chunk loop's own scalar values that
+// overflows the scalar register file, and the compiler parks the block in
+// vector-register lanes and reads whole register tuples back at every use.
+// A scalar load at the use (one instruction, served from the scalar cache)
+// keeps each value live only where it is needed.
+template <class T>
+__device__ __forceinline__ T chain_arg(int off) {
+  typedef __attribute__((address_space(4))) const char KChar;
+  KChar* kp = (KChar*)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(kp));
+  return *reinterpret_cast<__attribute__((address_space(4))) const T*>(kp + off);
+}
+#define E2TTT_ARG(f) \
+  ::e2ttt::chain_arg<decltype(::e2ttt::ChainArgs::f)>((int)offsetof(::e2ttt::ChainArgs, f))
+
 // Element (i, j) of matrix m of one unit's P parameters lives at
 //   first layer  [dh][d]: m dh d + j d + i
 //   second layer [d][dh]: (NMAT-1) dh d + i dh + j.

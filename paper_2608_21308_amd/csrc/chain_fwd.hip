@@ -130,14 +130,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
     const int st = LONG ? rc * C + kt * TL : rc * C;
     const long r0 = uu * T + st;
     const int ln = LONG ? min(TL, min(T, (rc + 1) * C) - st) : min(C, T - st);
-    pk.load(a.k, r0, ln, tid);
-    pq.load(a.q, r0, ln, tid);
-    pv.load(a.v, r0, ln, tid);
+    pk.load(E2TTT_ARG(k), r0, ln, tid);
+    pq.load(E2TTT_ARG(q), r0, ln, tid);
+    pv.load(E2TTT_ARG(v), r0, ln, tid);
     if (tid < S::CM) {
-      pkw = (tid < ln) ? a.kw[r0 + tid] : 0.0f;
-      pkm = (tid < ln) ? a.km[r0 + tid] : 0.0f;
+      pkw = (tid < ln) ? E2TTT_ARG(kw)[r0 + tid] : 0.0f;
+      pkm = (tid < ln) ? E2TTT_ARG(km)[r0 + tid] : 0.0f;
     }
-    if (tid < 3) pcar = a.carry[(uu * NC + rc) * 3 + tid];
+    if (tid < 3) pcar = E2TTT_ARG(carry)[(uu * NC + rc) * 3 + tid];
   };
 
   for (long u = px.p; u < a.U; u += NP) {
@@ -146,8 +146,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
     StateTiles<S> XW, XM;   // the chunk's sum_t K_t G_t (SEPDELTA)
     {
       E2TTT_LANE_IDS;
-      load_state<S>(W, a.w_in + u * a.P, dh, j0, w, g, c);
-      load_state<S>(M, a.m_in ? a.m_in + u * a.P : nullptr, dh, j0, w, g, c);
+      load_state<S>(W, E2TTT_ARG(w_in) + u * a.P, dh, j0, w, g, c);
+      load_state<S>(M, E2TTT_ARG(m_in) ? E2TTT_ARG(m_in) + u * a.P : nullptr, dh, j0, w, g, c);
     }
     prefetch(u, 0, 0);
 
@@ -187,11 +187,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
               XM.t[m][jj][ib] = zero4();
             }
       }
-      if (a.ckpt) {
-        char* cb = static_cast<char*>(a.ckpt) + ((u * NC + rc) * S::NS + rank) * 2 * a.ckpt_stride;
+      if (E2TTT_ARG(ckpt)) {
+        char* cb = static_cast<char*>(E2TTT_ARG(ckpt)) +
+                   ((u * NC + rc) * S::NS + rank) * 2 * E2TTT_ARG(ckpt_stride);
         if constexpr (PRESPLIT) store_ckpt_q<S>(WS.hi, cb, w, lane);
         else store_ckpt<S>(W, cb, w, lane);
-        store_ckpt<S>(M, cb + a.ckpt_stride, w, lane);
+        store_ckpt<S>(M, cb + E2TTT_ARG(ckpt_stride), w, lane);
       }
       // second-layer weights of W_0 into LDS as the j-contraction operand
 #pragma unroll
@@ -269,7 +270,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c,   // Y_K (partial)
-                        (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, rank, par) : nullptr);
+                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) : nullptr);
       }
       px.post();                                          // seq0 + 1: Y_K
       // without a separate Q-side buffer, alds is rewritten below
@@ -296,7 +297,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             if constexpr (S::FW == 1) accu = mma_state<S>(accu, af, &Wop.t[1][jj][0], p, 1);
           }
           f32x4 act, d1;
-          if (S::FW == 0 && a.asave) {   // GELU and GELU', saved for the backward
+          if (S::FW == 0 && E2TTT_ARG(asave)) {   // GELU and GELU', saved for the backward
 #pragma unroll
             for (int rr = 0; rr < 4; ++rr) {
               const Act2 ga = gelu2(acc[rr]);
@@ -331,7 +332,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
 #pragma unroll
         for (int k = 0; k < NPEER; ++k) {
-          const float* peer = fwd_slot<S>(a.xbuf, px.p, other_rank(k, rank), par);
+          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par);
 #pragma unroll
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * S::NW;
@@ -345,15 +346,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         jgemm_to_lds<S>(aq, sm.w2, sm.yq, w, g, c,        // Y_Q (partial)
-                        (S::NS > 1) ? fwd_slot<S>(a.xbuf, px.p, rank, par) + S::CM * D : nullptr);
+                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) + S::CM * D : nullptr);
       }
       px.post();                                          // seq0 + 2: Y_Q
       // the saved query side goes out after the post, so that the post's wait
       // for this chunk's stores does not include it
-      if (S::FW == 0 && a.asave) {
+      if (S::FW == 0 && E2TTT_ARG(asave)) {
         E2TTT_LANE_IDS;
-        const SavedAct<S> sv(static_cast<char*>(a.asave) +
-                             (((u * NC + rc) * TPC + kc) * S::NS + rank) * a.as_stride);
+        const SavedAct<S> sv(static_cast<char*>(E2TTT_ARG(asave)) +
+                             (((u * NC + rc) * TPC + kc) * S::NS + rank) * E2TTT_ARG(as_stride));
 #pragma unroll
         for (int tb = 0; tb < (S::FW == 0 ? NTB : 0); ++tb)
 #pragma unroll
@@ -395,12 +396,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           }
 #pragma unroll
           for (int q = 0; q < EPL; ++q) s1 += yv[q];
-          if (a.resln) {
+          if (E2TTT_ARG(resln)) {
             const float mu = group16_sum(s1) * inv_d;
             float s2 = 0.0f;
 #pragma unroll
             for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
-            sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+            sig = rsq_f(group16_sum(s2) * inv_d + E2TTT_ARG(eps));   // 1 / sigma
             float se = 0.0f, sez = 0.0f;
 #pragma unroll
             for (int q = 0; q < EPL; ++q) {
@@ -434,14 +435,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           }
                   }
         }
-        if (a.zk) {
+        if (E2TTT_ARG(zk)) {
 #pragma unroll
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t = 4 * w + it_ * 4 * S::NW + (lane >> 4);
             if (t < S::CM && keep[it_]) {
 #pragma unroll
-              for (int q = 0; q < EPL; ++q) a.zk[(row0 + t) * D + l16 * EPL + q] = zsave[it_][q];
-              if (l16 == 0) a.rk[row0 + t] = rsave[it_];
+              for (int q = 0; q < EPL; ++q) E2TTT_ARG(zk)[(row0 + t) * D + l16 * EPL + q] = zsave[it_][q];
+              if (l16 == 0) E2TTT_ARG(rk)[row0 + t] = rsave[it_];
             }
           }
         }
@@ -456,7 +457,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
 #pragma unroll
         for (int k = 0; k < NPEER; ++k) {
-          const float* peer = fwd_slot<S>(a.xbuf, px.p, other_rank(k, rank), par) + S::CM * D;
+          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par) + S::CM * D;
 #pragma unroll
           for (int it_ = 0; it_ < NITO; ++it_) {
             const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
@@ -581,7 +582,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         using IOT = typename IO::T;
-        IOT* outp = reinterpret_cast<IOT*>(a.out) + row0 * D;
+        IOT* outp = reinterpret_cast<IOT*>(E2TTT_ARG(out)) + row0 * D;
 #pragma unroll
         for (int it_ = 0; it_ < NITO; ++it_) {
           const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
@@ -602,12 +603,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           }
 #pragma unroll
           for (int q = 0; q < EPL; ++q) s1 += yv[q];
-          if (a.resln) {
+          if (E2TTT_ARG(resln)) {
             const float mu = group16_sum(s1) * inv_d;
             float s2 = 0.0f;
 #pragma unroll
             for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
-            sig = rsq_f(group16_sum(s2) * inv_d + a.eps);   // 1 / sigma
+            sig = rsq_f(group16_sum(s2) * inv_d + E2TTT_ARG(eps));   // 1 / sigma
 #pragma unroll
             for (int q = 0; q < EPL; ++q) {
               yv[q] *= sig;                                 // Z_Q
@@ -620,10 +621,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           if (t < len) {
 #pragma unroll
             for (int q = 0; q < EPL; ++q) IO::st(outp + (long)t * D + l16 * EPL + q, f[q]);
-            if (a.zq) {
+            if (E2TTT_ARG(zq)) {
 #pragma unroll
-              for (int q = 0; q < EPL; ++q) a.zq[(row0 + t) * D + l16 * EPL + q] = yv[q];
-              if (l16 == 0) a.rq[row0 + t] = sig;
+              for (int q = 0; q < EPL; ++q) E2TTT_ARG(zq)[(row0 + t) * D + l16 * EPL + q] = yv[q];
+              if (l16 == 0) E2TTT_ARG(rq)[row0 + t] = sig;
             }
           }
                   }
@@ -634,8 +635,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
     {
       E2TTT_LANE_IDS;
-      store_state<S>(W, a.w_out + u * a.P, dh, j0, w, g, c);
-      store_state<S>(M, a.m_out + u * a.P, dh, j0, w, g, c);
+      store_state<S>(W, E2TTT_ARG(w_out) + u * a.P, dh, j0, w, g, c);
+      store_state<S>(M, E2TTT_ARG(m_out) + u * a.P, dh, j0, w, g, c);
     }
   }
 }
