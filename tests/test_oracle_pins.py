@@ -181,6 +181,35 @@ def test_chunk_size_one_is_online_gd_with_momentum(oracle, fw, flags):
     np.testing.assert_allclose(mo[0, 0], M.numpy(), rtol=1e-10, atol=1e-12)
 
 
+
+@pytest.mark.parametrize("fw,flags", NETS)
+def test_mse_as_mean_is_a_rescaled_eta(oracle, fw, flags):
+    # The paper names the inner loss "MSE" without a constant (Sec. 2); the
+    # oracle takes L_t = 1/2 ||f(k_t) - v_t||^2.  With the mean over d instead,
+    # L'_t = (1/d) ||f(k_t) - v_t||^2 = (2/d) L_t, every gradient is (2/d) G_t,
+    # and G_t only enters as eta_t G_t, so the oracle at eta (2/d) must equal a
+    # token loop that differentiates torch's mean-reduced mse_loss.
+    T, C, d, dh = 11, 4, 6, 9
+    x = rand_problem(T, d, dh, fw, 77 + fw + 2 * flags)
+    resln = flags == 0
+    x2 = dict(x)
+    x2["eta"] = x["eta"] * (2.0 / d)
+    out, wo, mo = oracle.forward(**x2, C=C, fw=fw, dh=dh, flags=flags)
+    W = torch.tensor(x["w_in"][0, 0])
+    M = torch.tensor(x["m_in"][0, 0])
+    for s0 in range(0, T, C):
+        W0 = W.clone().requires_grad_(True)
+        for t in range(s0, min(T, s0 + C)):
+            o = torchref.net(W0, torch.tensor(x["q"][0, 0, t]), d, dh, fw, resln)
+            np.testing.assert_allclose(out[0, 0, t], o.detach().numpy(), rtol=1e-10, atol=1e-12)
+            f = torchref.net(W0, torch.tensor(x["k"][0, 0, t]), d, dh, fw, resln)
+            L = torch.nn.functional.mse_loss(f, torch.tensor(x["v"][0, 0, t]))
+            (g,) = torch.autograd.grad(L, W0)
+            M = x["beta"][0, 0, t] * M - x["eta"][0, 0, t] * g
+            W = x["gamma"][0, 0, t] * W + M
+    np.testing.assert_allclose(wo[0, 0], W.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(mo[0, 0], M.numpy(), rtol=1e-10, atol=1e-12)
+
 @pytest.mark.parametrize("fw", [FW_MLP, FW_SWIGLU])
 @pytest.mark.parametrize("C,T", [(1, 5), (2, 8), (4, 11), (8, 8), (16, 37)])
 def test_chunk_end_states_match_closed_form(oracle, fw, C, T):
