@@ -46,12 +46,11 @@
  *
  * Supported shapes: io = BF16 with d = 64 (dh <= 256 for the MLP, <= 192 for
  * SwiGLU), or io = F32 with d = 16 (dh <= 128); dh is padded inside the
- * library to a multiple of 16; 1 <= chunk <= 64 everywhere, and chunks of
- * 65..512 tokens (the paper's C = 512) for the GELU MLP on bf16 and both
- * nets on fp32, forward and backward (the chunk runs as 64-token tiles that
- * all take gradients and outputs at the chunk-start weights; SwiGLU on bf16
- * refuses chunks above 64); T >= 1 with a ragged last chunk of T mod chunk
- * tokens allowed (Prop. 1 holds for any chunk length).
+ * library to a multiple of 16; 1 <= chunk <= 512 (the paper's C = 512),
+ * forward and backward; a chunk longer than 64 tokens runs as 64-token tiles
+ * that all take gradients and outputs at the chunk-start weights; T >= 1 with
+ * a ragged last chunk of T mod chunk tokens allowed (Prop. 1 holds for any
+ * chunk length).
  * bf16 tensors use MFMA bf16 operands with fp32 accumulation and fp32 state;
  * f32 tensors use fp32 MFMA throughout.  Anything else returns
  * E2TTT_ERR_UNSUPPORTED.

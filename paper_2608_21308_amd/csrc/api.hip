@@ -19,25 +19,20 @@ constexpr size_t kAlign = 256;
 // one cooperative launch; more units are taken in turn by the same groups.
 constexpr long kMaxPairs = 128;
 
-// Chunks up to 64 tokens run everywhere; longer chunks (up to 512, the
-// paper's setting) run as 64-row tiles on the MLP bf16 and the fp32 variants
-// (whose chunk products take operands of W_0 that stay fixed across the
-// chunk's tiles), forward and backward.
+// Chunks of up to 512 tokens (the paper's setting); a chunk longer than the
+// kernels' 64-row tile runs as consecutive tiles at the chunk-start weights,
+// forward and backward.
 constexpr int kMaxChunk = 512;
-constexpr int kMaxTrainChunk = 64;   // SwiGLU on bf16
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-
-bool long_chunk_ok(const e2ttt_desc& d) {
-  return d.chunk <= kMaxTrainChunk || d.io == E2TTT_DT_F32 || d.fw == E2TTT_FW_GELU_MLP;
-}
 
 struct Plan {
   long U = 0, T = 0, NC = 0, P = 0;
   ChainConfig cfg{};
   long npairs = 0;        // groups the exchange buffers are sized for (ns workgroups per unit)
   // forward workspace
-  size_t off_kw = 0, off_km = 0, off_carry = 0, off_sync = 0, off_xbuf = 0, ws_bytes = 0;
+  size_t off_kw = 0, off_km = 0, off_carry = 0, off_sync = 0, off_xbuf = 0, off_w0 = 0;
+  size_t ws_bytes = 0;
   size_t off_ckpt = 0, off_zk = 0, off_rk = 0, off_zq = 0, off_rq = 0, ws_bytes_save = 0;
   long ckpt_stride = 0;
   size_t off_as = 0;
@@ -105,8 +100,15 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_carry = pl.off_km + align_up(tok);
   pl.off_sync = pl.off_carry + align_up(chk);
   pl.off_xbuf = pl.off_sync + align_up(sync_b);
-  pl.off_ckpt = pl.off_xbuf +
-                align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, false) * sizeof(float));
+  const int cm_rows = 16 * pl.cfg.ntb;
+  pl.tpc = (d.chunk > cm_rows) ? (d.chunk + cm_rows - 1) / cm_rows : 1;
+  const long nwg = (ns > 1) ? pl.npairs * ns : U;   // workgroups of a chain launch
+  pl.off_w0 = pl.off_xbuf +
+              align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, false) * sizeof(float));
+  // long chunks of SwiGLU on bf16: the forward's per-workgroup copy of W_0
+  const bool w0b = pl.tpc > 1 && pl.cfg.bf && pl.cfg.fw == E2TTT_FW_SWIGLU;
+  pl.off_ckpt =
+      pl.off_w0 + (w0b ? align_up((size_t)nwg * chain_frz_floats(pl.cfg) * sizeof(float)) : 0);
   pl.ws_bytes = pl.off_ckpt;
   pl.ckpt_stride = chain_ckpt_bytes(pl.cfg);
   const size_t tokd = tok * d.d;
@@ -114,8 +116,6 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_rk = pl.off_zk + align_up(tokd);
   pl.off_zq = pl.off_rk + align_up(tok);
   pl.off_rq = pl.off_zq + align_up(tokd);
-  const int cm_rows = 16 * pl.cfg.ntb;
-  pl.tpc = (d.chunk > cm_rows) ? (d.chunk + cm_rows - 1) / cm_rows : 1;
   pl.as_stride = chain_saved_act_bytes(pl.cfg);
   pl.off_as = pl.off_rq + align_up(tok);
   pl.ws_bytes_save = pl.off_as + align_up((size_t)U * pl.NC * pl.tpc * ns * pl.as_stride);
@@ -127,7 +127,6 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_frz =
       pl.off_bxbuf +
       align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, true) * sizeof(float));
-  const long nwg = (ns > 1) ? pl.npairs * ns : U;   // workgroups of the backward launch
   pl.scratch_bytes =
       pl.off_frz +
       (pl.tpc > 1 ? align_up((size_t)nwg * 2 * chain_frz_floats(pl.cfg) * sizeof(float)) : 0);
@@ -218,13 +217,12 @@ size_t e2ttt_param_count(const e2ttt_desc* desc) {
 size_t e2ttt_workspace_bytes(const e2ttt_desc* desc, int save_for_backward) {
   Plan pl;
   if (make_plan(desc, pl) != E2TTT_OK) return 0;
-  if (!long_chunk_ok(*desc)) return 0;
   return save_for_backward ? pl.ws_bytes_save : pl.ws_bytes;
 }
 
 size_t e2ttt_backward_scratch_bytes(const e2ttt_desc* desc) {
   Plan pl;
-  if (make_plan(desc, pl) != E2TTT_OK || !long_chunk_ok(*desc)) return 0;
+  if (make_plan(desc, pl) != E2TTT_OK) return 0;
   return pl.scratch_bytes;
 }
 
@@ -283,7 +281,6 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
-  if (!long_chunk_ok(*desc)) return E2TTT_ERR_UNSUPPORTED;
   if (!q || !k || !v || !eta || !beta || !w_in || !out || !w_out || !m_out || !workspace)
     return E2TTT_ERR_NULL_ARG;
   if (workspace_bytes < (save_for_backward ? pl.ws_bytes_save : pl.ws_bytes))
@@ -317,6 +314,7 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
     a.rq = at<float>(workspace, pl.off_rq);
   }
   a.xbuf = at<float>(workspace, pl.off_xbuf);
+  a.w0blk = pl.off_ckpt > pl.off_w0 ? at<float>(workspace, pl.off_w0) : nullptr;
   a.sync = sync;
   a.npairs = np;
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
@@ -336,7 +334,6 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
-  if (!long_chunk_ok(*desc)) return E2TTT_ERR_UNSUPPORTED;
   if (!q || !k || !v || !eta || !beta || !w_in || !workspace || !d_out || !dq || !dk || !dv ||
       !d_eta || !d_beta || !d_w_in || !d_m_in || !scratch)
     return E2TTT_ERR_NULL_ARG;

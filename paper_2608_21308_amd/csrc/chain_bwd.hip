@@ -1193,10 +1193,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   }
 }
 
-// Long chunks are compiled where the forward has them (MLP on bf16, fp32).
-template <class S>
-constexpr bool has_long() { return !(S::BF && S::FW == 1); }
-
 template <class S, bool LONG>
 int occupancy() {
   int v = 0;
@@ -1209,9 +1205,8 @@ int occupancy() {
 template <class S>
 int max_blocks_per_cu() {
   static int nb = [] {
-    int v = occupancy<S, false>();
-    if constexpr (has_long<S>()) v = std::min(v, occupancy<S, true>());
-    return v;
+    // one launch geometry serves both instantiations
+    return std::min(occupancy<S, false>(), occupancy<S, true>());
   }();
   return nb;
 }
@@ -1234,11 +1229,8 @@ hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
 template <class S>
 hipError_t launch(const ChainArgs& a, hipStream_t stream) {
   if (a.C <= S::CM) return launch_as<S, false>(a, stream);
-  if constexpr (has_long<S>()) {
-    if (!a.bfrz) return hipErrorInvalidValue;
-    return launch_as<S, true>(a, stream);
-  }
-  return hipErrorInvalidValue;
+  if (!a.bfrz) return hipErrorInvalidValue;
+  return launch_as<S, true>(a, stream);
 }
 
 }  // namespace

@@ -88,6 +88,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // chunk instead of one per contraction step); W itself stays W_0 for the
   // whole chunk and is the products' operand, also across a long chunk's tiles
   constexpr bool SEPDELTA = !S::BF;
+  // SwiGLU on the bf16 path re-forms W_0's operands at every product.  In a
+  // long chunk's later tiles the state has already taken the chunk's first
+  // updates, so those products read W_0 back from the fp32 copy (register-tile
+  // order, lane-private) that the chunk's first tile leaves in this
+  // workgroup's block.
+  constexpr bool RELOAD = LONG && S::BF && S::FW == 1;
+  constexpr long NB0 = (long)NMAT * NJB * NIB * S::NT;   // f32x4 per block
+  f32x4* const w0blk =
+      RELOAD ? reinterpret_cast<f32x4*>(E2TTT_ARG(w0blk)) + (long)blockIdx.x * NB0 : nullptr;
   constexpr int EPL = D / 16;    // head elements per lane in the row phases
   constexpr int RPW = row_share<S>();  // output rows written by one rank (last: fewer)
   constexpr int NPEER = S::NS - 1;
@@ -176,6 +185,17 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       if (tid < 3) sm.carry[tid] = pcar;
       if (first) {
       if constexpr (PRESPLIT) split_state<S>(WS, W);
+      if constexpr (RELOAD) {
+        if (more) {
+#pragma unroll
+          for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+              for (int ib = 0; ib < NIB; ++ib)
+                w0blk[((m * NJB + jj) * NIB + ib) * S::NT + tid] = W.t[m][jj][ib];
+        }
+      }
       if constexpr (SEPDELTA) {
 #pragma unroll
         for (int m = 0; m < NMAT; ++m)
@@ -213,13 +233,28 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
       // operand of the chunk's products (W_0: W is not updated before the chunk end
       // on the fp32 path, nor before the transition below on the others)
-      const StateTiles<S>& Wop = W;
+      StateTiles<S> W0r;   // RELOAD: W_0 tiles of the matrices the next product takes
+      auto w0_mats = [&](int m0, int m1) {
+        E2TTT_LANE_IDS;
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m) {
+          if (m < m0 || m > m1) continue;
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib)
+              W0r.t[m][jj][ib] = first ? W.t[m][jj][ib]
+                                       : w0blk[((m * NJB + jj) * NIB + ib) * S::NT + tid];
+        }
+      };
+      const StateTiles<S>& Wop = RELOAD ? W0r : W;
 
       // ------------------------------------------- K-side forward (a3)
       // act'(H) kept for dH: MLP GELU'(H); SwiGLU (Hu SiLU'(Hg), SiLU(Hg))
       f32x4 H[NTB][NJB];
       f32x4 Hu[NTB][(S::FW == 1) ? NJB : 1];
       typename O::Q AK[NTB][NJB];          // act(H) as operand quads (rows t)
+      if constexpr (RELOAD) w0_mats(0, 1);
       {
       E2TTT_LANE_IDS;
 #pragma unroll 1
@@ -281,6 +316,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // (MLP, saving for the backward: A_Q and GELU'(H_Q) of every tile)
       typename O::Q qsa[S::FW == 0 ? NTB : 1][NJB];
       f32x4 qsd[S::FW == 0 ? NTB : 1][NJB];
+      if constexpr (RELOAD) w0_mats(0, 1);
       {
       E2TTT_LANE_IDS;
       opaque_state<S>(W);
@@ -471,6 +507,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
       // ---------------------------------- dA = dY W2, first-layer deltas (a4)
       opaque_state<S>(W);
+      if constexpr (RELOAD) w0_mats(SEC, SEC);
       // first-layer update operands K^W_t dH[t][j] and K^M_t dH[t][j] (the scalar
       // kernels go on dH, so that the other operand is K^T, exact in bf16); for
       // the MLP on the bf16 path they are split into bf16 high and low parts
@@ -641,11 +678,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   }
 }
 
-// Long chunks are compiled for the variants whose chunk products take fixed
-// operand copies of W_0: the MLP on the bf16 path and the fp32 path.
-template <class S>
-constexpr bool has_long() { return !(S::BF && S::FW == 1); }
-
 template <class S, bool LONG>
 int occupancy() {
   int v = 0;
@@ -658,9 +690,8 @@ int occupancy() {
 template <class S>
 int max_blocks_per_cu() {
   static int nb = [] {
-    int v = occupancy<S, false>();
-    if constexpr (has_long<S>()) v = std::min(v, occupancy<S, true>());
-    return v;
+    // one launch geometry serves both instantiations
+    return std::min(occupancy<S, false>(), occupancy<S, true>());
   }();
   return nb;
 }
@@ -683,8 +714,9 @@ hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
 template <class S>
 hipError_t launch(const ChainArgs& a, hipStream_t stream) {
   if (a.C <= S::CM) return launch_as<S, false>(a, stream);
-  if constexpr (has_long<S>()) return launch_as<S, true>(a, stream);
-  return hipErrorInvalidValue;
+  // a long chunk whose products re-form W_0 from the state needs the W_0 blocks
+  if (S::BF && S::FW == 1 && !a.w0blk) return hipErrorInvalidValue;
+  return launch_as<S, true>(a, stream);
 }
 
 }  // namespace

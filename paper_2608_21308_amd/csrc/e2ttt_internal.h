@@ -80,6 +80,10 @@ struct ChainArgs {
   // (fp32, in the register-tile order of the state), two blocks of
   // chain_frz_floats(cfg) floats each
   float* bfrz;
+  // forward of chunks longer than one tile with operands re-formed from the
+  // state (SwiGLU on bf16): per workgroup, the chunk-start weights W_0 (fp32,
+  // register-tile order), chain_frz_floats(cfg) floats each
+  float* w0blk;
   // LN outputs saved by the forward for the backward (nullable in the forward):
   // Z = LN(Y) (Y itself without the residual LN) [U][T][d], 1/sigma [U][T]
   float* zk;

@@ -202,8 +202,8 @@ def test_apply_argument_errors(lib):
 
 
 def test_long_chunks(lib):
-    """Chunks of 65..512 tokens run on the MLP bf16 and fp32 variants (forward
-    and backward); SwiGLU on bf16 is refused before any launch."""
+    """Chunks of 65..512 tokens run on every variant, forward and backward;
+    above 512 the call is refused before any launch."""
     f = ctypes.c_void_p(16)   # never dereferenced
     for kw in (dict(chunk=128), dict(chunk=512), dict(io=0, d=16, dh=64, chunk=200)):
         d = desc(**kw)
@@ -215,9 +215,15 @@ def test_long_chunks(lib):
         # the backward scratch adds two fp32 copies of each workgroup's state share
         assert (lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) >
                 lib.e2ttt_backward_scratch_bytes(ctypes.byref(short)))
-    d = desc(fw=1, dh=172, chunk=128)   # SwiGLU on bf16: chunks of at most 64
+    # SwiGLU on bf16: the forward workspace also holds every workgroup's copy
+    # of W_0 (fp32) for the chunk's later tiles
+    d = desc(fw=1, dh=172, chunk=512)
+    short = desc(fw=1, dh=172, chunk=64)
+    assert (lib.e2ttt_workspace_bytes(ctypes.byref(d), 0) >
+            lib.e2ttt_workspace_bytes(ctypes.byref(short), 0) + 3 * 64 * 64 * 4)
+    assert lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) > 0
+    d = desc(fw=1, dh=172, chunk=513)
     assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 0) == 0
-    assert lib.e2ttt_workspace_bytes(ctypes.byref(d), 1) == 0
     assert lib.e2ttt_backward_scratch_bytes(ctypes.byref(d)) == 0
     assert lib.e2ttt_chunk_forward(ctypes.byref(d), *([f] * 12), 1 << 40, 0, None) == 3
     assert lib.e2ttt_chunk_backward(ctypes.byref(d), *([f] * 9), 1 << 40, *([f] * 12),
