@@ -242,11 +242,13 @@ def measure_peaks(dev) -> dict:
 
 def time_workloads(e2ttt, WL, dev, reps: int = 10) -> dict:
     """The other synthetic workloads at their own shapes (parity-test cases,
-    timed here as context): every pass they include, back to back, HIP events
+    timed here as context), and the paper's own 1.3B throughput shape (head
+    dim 128, chunk 512): every pass they include, back to back, HIP events
     around each call; tokens/s counts B*T per forward (+ backward) pass."""
     import torch
     res = {}
-    for w in (WL.WORKLOADS[0], WL.WORKLOADS[1], WL.WORKLOADS[2], WL.WORKLOADS[4]):
+    for w in (WL.WORKLOADS[0], WL.WORKLOADS[1], WL.WORKLOADS[2], WL.WORKLOADS[4],
+              WL.PAPER_1P3B):
         x = WL.make_inputs(w)
         bf = w.io == "bf16"
         t = {}

@@ -28,9 +28,10 @@
  *     return nothing has been written.  Errors raised by kernels while they
  *     run surface on the stream as HIP errors.
  *   - Results are bitwise reproducible run to run (no floating-point atomics).
- *   - For the wider nets at d = 64 (GELU MLP with dh > 128, SwiGLU with
- *     dh > 64) each unit is split over two or three workgroups that swap
- *     partial sums through the workspace (or the backward scratch); those
+ *   - For the wider nets (d = 64: GELU MLP with dh > 128, SwiGLU with
+ *     dh > 64; d = 128: dh > 64) each unit is split over two to eight
+ *     workgroups that swap partial sums through the workspace (or the
+ *     backward scratch); those
  *     kernels are launched cooperatively, so a call may wait for the whole
  *     device.  Calls that share a workspace or scratch buffer must not run
  *     concurrently.
@@ -45,10 +46,12 @@
  *   (Wg, Wu, Wd are the paper's W1, W2, W3 of the SwiGLU net.)
  *
  * Supported shapes: io = BF16 with d = 64 (dh <= 256 for the MLP, <= 192 for
- * SwiGLU), or io = F32 with d = 16 (dh <= 128); dh is padded inside the
- * library to a multiple of 16; 1 <= chunk <= 512 (the paper's C = 512),
- * forward and backward; a chunk longer than 64 tokens runs as 64-token tiles
- * that all take gradients and outputs at the chunk-start weights; T >= 1 with
+ * SwiGLU) or d = 128 (the GELU MLP, dh <= 512), or io = F32 with d = 16
+ * (dh <= 128); dh is padded inside the library to a multiple of 16;
+ * 1 <= chunk <= 512 (the paper's C = 512), forward and backward; a chunk
+ * longer than the kernels' token tile (64 rows, 32 at d = 128) runs as
+ * consecutive tiles that all take gradients and outputs at the chunk-start
+ * weights; e2ttt_apply takes d <= 64; T >= 1 with
  * a ragged last chunk of T mod chunk tokens allowed (Prop. 1 holds for any
  * chunk length).
  * bf16 tensors use MFMA bf16 operands with fp32 accumulation and fp32 state;

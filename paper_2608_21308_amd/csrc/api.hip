@@ -15,7 +15,7 @@ namespace {
 using namespace e2ttt;
 
 constexpr size_t kAlign = 256;
-// Upper bound on workgroup groups (two or three workgroups sharing a unit) of
+// Upper bound on workgroup groups (two to eight workgroups sharing a unit) of
 // one cooperative launch; more units are taken in turn by the same groups.
 constexpr long kMaxPairs = 128;
 
@@ -49,7 +49,21 @@ e2ttt_status select_config(const e2ttt_desc& d, ChainConfig& cfg) {
   cfg.bf = (d.io == E2TTT_DT_BF16) ? 1 : 0;
   const int nblk = (d.dh + 15) / 16;
   cfg.ns = 1;
-  if (cfg.bf) {
+  if (cfg.bf && d.d == 128) {
+    // head dim 128 (the paper's 1.3B model, 2048 / 16 heads), GELU MLP: the
+    // state of 64 hidden columns per workgroup (four waves, one per SIMD) and
+    // 32-row token tiles (longer chunks run as consecutive tiles) fit the
+    // register file and LDS; wider nets spread over 2, 4 or 8 workgroups
+    if (d.fw != E2TTT_FW_GELU_MLP) return E2TTT_ERR_UNSUPPORTED;
+    cfg.ntb = 2;
+    cfg.nw = 4;
+    cfg.njb = 1;
+    if (nblk <= 4) cfg.ns = 1;
+    else if (nblk <= 8) cfg.ns = 2;
+    else if (nblk <= 16) cfg.ns = 4;
+    else if (nblk <= 32) cfg.ns = 8;
+    else return E2TTT_ERR_UNSUPPORTED;
+  } else if (cfg.bf) {
     if (d.d != 64) return E2TTT_ERR_UNSUPPORTED;
     cfg.ntb = 4;
     if (nblk <= 4) { cfg.nw = 4; cfg.njb = 1; }
@@ -105,8 +119,9 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   const long nwg = (ns > 1) ? pl.npairs * ns : U;   // workgroups of a chain launch
   pl.off_w0 = pl.off_xbuf +
               align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, false) * sizeof(float));
-  // long chunks of SwiGLU on bf16: the forward's per-workgroup copy of W_0
-  const bool w0b = pl.tpc > 1 && pl.cfg.bf && pl.cfg.fw == E2TTT_FW_SWIGLU;
+  // long chunks on bf16 whose products re-form W_0's operands from the state
+  // (SwiGLU, and the MLP at head dim 128): the forward's per-workgroup copy of W_0
+  const bool w0b = pl.tpc > 1 && pl.cfg.bf && (pl.cfg.fw == E2TTT_FW_SWIGLU || d.d > 64);
   pl.off_ckpt =
       pl.off_w0 + (w0b ? align_up((size_t)nwg * chain_frz_floats(pl.cfg) * sizeof(float)) : 0);
   pl.ws_bytes = pl.off_ckpt;
@@ -259,7 +274,7 @@ e2ttt_status e2ttt_apply(const e2ttt_desc* desc, const void* q, const float* w, 
   if (st != E2TTT_OK) return st;
   if (!q || !w || !out) return E2TTT_ERR_NULL_ARG;
   if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return E2TTT_ERR_BAD_SHAPE;
-  if (desc->dh > kApplyMaxDh) return E2TTT_ERR_UNSUPPORTED;
+  if (desc->dh > kApplyMaxDh || desc->d > 64) return E2TTT_ERR_UNSUPPORTED;
   if (pl.U * ((pl.T + 7) / 8) > INT_MAX) return E2TTT_ERR_UNSUPPORTED;
   ApplyArgs a{};
   a.q = q; a.w = w; a.out = out;

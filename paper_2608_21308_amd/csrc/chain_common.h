@@ -1,7 +1,7 @@
 // Shape constants and register-resident state handling shared by the forward
 // and backward chain kernels.
 //
-// NS workgroups (1 or 2) own one (batch, head) unit for the whole sequence;
+// NS workgroups (1 to 8) own one (batch, head) unit for the whole sequence;
 // rank r of them holds the hidden columns [r DHP, (r+1) DHP).  Its NW waves
 // split that range: wave w owns the local hidden columns j in
 // [16 w NJB, 16 (w+1) NJB).  Every fast-weight matrix is held as 16x16

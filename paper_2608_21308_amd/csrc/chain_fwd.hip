@@ -82,7 +82,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // MLP on the bf16 path: the bf16 high / low parts of W_0 are formed once per
   // chunk (checkpoint, LDS copy of W2, and the K-side, Q-side and dA products
   // share them); the wider SwiGLU state re-forms them per use instead
-  constexpr bool PRESPLIT = S::BF && S::FW == 0;
+  constexpr bool PRESPLIT = S::BF && S::FW == 0 && S::D <= 64;
   // fp32 path: the chunk's sum_t K_t G_t accumulates apart from the state and
   // joins it in one addition at the chunk end (one rounding of W and M per
   // chunk instead of one per contraction step); W itself stays W_0 for the
@@ -93,13 +93,18 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // updates, so those products read W_0 back from the fp32 copy (register-tile
   // order, lane-private) that the chunk's first tile leaves in this
   // workgroup's block.
-  constexpr bool RELOAD = LONG && S::BF && S::FW == 1;
+  constexpr bool RELOAD = LONG && S::BF && !PRESPLIT;
   constexpr long NB0 = (long)NMAT * NJB * NIB * S::NT;   // f32x4 per block
   f32x4* const w0blk =
       RELOAD ? reinterpret_cast<f32x4*>(E2TTT_ARG(w0blk)) + (long)blockIdx.x * NB0 : nullptr;
   constexpr int EPL = D / 16;    // head elements per lane in the row phases
   constexpr int RPW = row_share<S>();  // output rows written by one rank (last: fewer)
   constexpr int NPEER = S::NS - 1;
+  // the peers' rows of Y_K and Y_Q are loaded right after the waits (so that
+  // they arrive under the next contraction) while they are few; with many
+  // peers or wide rows that would hold too many registers, and each row
+  // phase loads them where it adds them
+  constexpr bool PEER_EARLY = NPEER * EPL <= 8 && S::D <= 64;
   __shared__ FwdSmem<S> sm;
   static_assert(sizeof(FwdSmem<S>) <= 160 * 1024, "LDS budget");
 
@@ -362,12 +367,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // which also completes the Q-side activations) lets the loads of its
       // rows for every LN step run under the Y_Q contraction.
       constexpr int NIT = (S::CM + 4 * S::NW - 1) / (4 * S::NW);
-      float pyv[S::NS > 1 ? NIT : 1][S::NS > 1 ? NPEER : 1][EPL];
+      float pyv[S::NS > 1 && PEER_EARLY ? NIT : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
         px.wait_for(seq0 + 1, sm.word);                   // peers' Y_K
         E2TTT_LANE_IDS;
 #pragma unroll
-        for (int k = 0; k < NPEER; ++k) {
+        for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
           const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par);
 #pragma unroll
           for (int it_ = 0; it_ < NIT; ++it_) {
@@ -421,13 +426,24 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           float s1 = 0.0f, sig = 1.0f;
 #pragma unroll
           for (int q = 0; q < EPL; ++q) yv[q] = sm.y[t * D + l16 * EPL + q];
-          if constexpr (S::NS > 1) {
+          if constexpr (S::NS > 1 && PEER_EARLY) {
 #pragma unroll
             for (int q = 0; q < EPL; ++q) {
               float pv[NPEER];
 #pragma unroll
               for (int k = 0; k < NPEER; ++k) pv[k] = pyv[it_][k][q];
               yv[q] = sum_ranks<S::NS>(yv[q], pv, rank);
+            }
+          } else if constexpr (S::NS > 1) {
+            // every rank's partial from its slot (this rank's too), added in
+            // rank order as sum_ranks does: the same sum on every rank
+#pragma unroll
+            for (int r = 0; r < S::NS; ++r) {
+              float pr[EPL];
+              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.p, r, par) + t * D +
+                                         l16 * EPL);
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
             }
           }
 #pragma unroll
@@ -487,12 +503,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       // barrier that ends the LN phase) and load its rows of the outputs, so
       // that they arrive under dA and the state update.
       constexpr int NITO = (RPW + 4 * S::NW - 1) / (4 * S::NW);
-      float pyq[S::NS > 1 ? NITO : 1][S::NS > 1 ? NPEER : 1][EPL];
+      float pyq[S::NS > 1 && PEER_EARLY ? NITO : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
         px.wait_for(seq0 + 2, sm.word);                   // peers' Y_Q
         E2TTT_LANE_IDS;
 #pragma unroll
-        for (int k = 0; k < NPEER; ++k) {
+        for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
           const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par) + S::CM * D;
 #pragma unroll
           for (int it_ = 0; it_ < NITO; ++it_) {
@@ -629,13 +645,24 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           float s1 = 0.0f, sig = 1.0f;
 #pragma unroll
           for (int q = 0; q < EPL; ++q) yv[q] = sm.yq[t * D + l16 * EPL + q];
-          if constexpr (S::NS > 1) {
+          if constexpr (S::NS > 1 && PEER_EARLY) {
 #pragma unroll
             for (int q = 0; q < EPL; ++q) {
               float pv[NPEER];
 #pragma unroll
               for (int k = 0; k < NPEER; ++k) pv[k] = pyq[it_][k][q];
               yv[q] = sum_ranks<S::NS>(yv[q], pv, rank);
+            }
+          } else if constexpr (S::NS > 1) {
+            // every rank's partial from its slot (this rank's too), added in
+            // rank order as sum_ranks does: the same sum on every rank
+#pragma unroll
+            for (int r = 0; r < S::NS; ++r) {
+              float pr[EPL];
+              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.p, r, par) + S::CM * D + t * D +
+                                         l16 * EPL);
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
             }
           }
 #pragma unroll
@@ -715,7 +742,7 @@ template <class S>
 hipError_t launch(const ChainArgs& a, hipStream_t stream) {
   if (a.C <= S::CM) return launch_as<S, false>(a, stream);
   // a long chunk whose products re-form W_0 from the state needs the W_0 blocks
-  if (S::BF && S::FW == 1 && !a.w0blk) return hipErrorInvalidValue;
+  if (S::BF && (S::FW == 1 || S::D > 64) && !a.w0blk) return hipErrorInvalidValue;
   return launch_as<S, true>(a, stream);
 }
 

@@ -1,7 +1,7 @@
 // Several workgroups per unit: exchange of partial sums through global memory.
 //
 // For the widest fast-weight nets one unit's hidden columns are split between
-// NS workgroups (NS = 2 or 3; ranks 0 .. NS-1 of a group), each holding its
+// NS workgroups (NS = 2 to 8; ranks 0 .. NS-1 of a group), each holding its
 // share of the state in registers.  Contractions over the hidden index then
 // give each rank a partial C x d sum that the others need; the ranks swap
 // these through a small global buffer and a flag per rank.  Every rank adds
@@ -96,7 +96,7 @@ template <> struct PairX<1> {
 };
 
 template <int NS> struct PairX {
-  static_assert(NS >= 2 && NS <= 4, "two to four workgroups per unit");
+  static_assert(NS >= 2 && NS <= 8, "two to eight workgroups per unit");
   int rank = 0;
   long p = 0;
   unsigned* mine = nullptr;

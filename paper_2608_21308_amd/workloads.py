@@ -76,6 +76,13 @@ WORKLOADS = [
 ]
 
 
+# The paper's own throughput shape for its 1.3B model (Sec. 5: hidden 2048 over
+# 16 heads, so head dim 128; sequences of 2K tokens, batch 2, chunk 512), with
+# an MLP fast weight of hidden 4 d = 512 per head; the same recipe as above.
+PAPER_1P3B = Workload("paper_1p3b_d128_c512_bf16", FW_MLP, 2, 16, 2048, 128, 512, 512, "bf16",
+                      True, 20270, "paper-scale 1.3B layer: head dim 128, chunk 512, fwd + bwd")
+
+
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bf16 (ties to even); returns float32."""
     x = np.ascontiguousarray(x, dtype=np.float32)

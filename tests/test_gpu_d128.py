@@ -1,0 +1,116 @@
+"""GPU parity at head dim 128 (the paper's 1.3B model: hidden 2048 over 16
+heads, Sec. 5), GELU MLP on bf16.  The kernels hold 64 hidden columns per
+workgroup and work on 32-row token tiles, so dh 64 / 128 / 256 / 512 run on
+one, two, four and eight workgroups per unit, and chunks longer than 32
+tokens run as consecutive tiles at the chunk-start weights.  The oracle is
+the fp64 token recurrence (eq. (7)) at any head dim; bar 2e-2 rel-L2.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2608_21308_amd import e2ttt, workloads as WL
+from tests.gpu_util import TOL, config_of, rel_l2, to_dev
+from tests.test_gpu_backward import GRADS, errors as berrors, gpu_fwd_bwd, oracle_bwd, \
+    with_state_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    e2ttt.load()
+
+
+def d128(**kw):
+    base = dict(B=2, H=2, T=256, d=128, dh=512, C=64, backward=False)
+    base.update(kw)
+    return WL.PAPER_1P3B.with_(**base)
+
+
+def run_forward(w, x):
+    t = to_dev(x, "bf16")
+    out, wo, mo, _ = e2ttt.forward(config_of(w), t["q"], t["k"], t["v"], t["eta"], t["beta"],
+                                   t["gamma"], t["w_in"], t.get("m_in"))
+    torch.cuda.synchronize()
+    return out, wo, mo
+
+
+def fwd_errors(got, x, w, units=None):
+    ro, rw, rm = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"],
+                                x["w_in"], x.get("m_in"), C=w.C, fw=w.fw, dh=w.dh)
+    out, wo, mo = (g.float().cpu().numpy() for g in got)
+    if units is not None:
+        pick = lambda a: a.reshape((-1,) + a.shape[2:])[units][None]
+        out, wo, mo = pick(out), pick(wo), pick(mo)
+    return {"out": rel_l2(out, ro), "w_out": rel_l2(wo - x["w_in"], rw - x["w_in"]),
+            "m_out": rel_l2(mo, rm)}
+
+
+@pytest.mark.parametrize("T,C,dh", [(200, 32, 64), (300, 64, 128), (260, 100, 256),
+                                    (700, 512, 512), (130, 16, 512), (90, 90, 200)])
+def test_forward_d128(T, C, dh):
+    w = d128(T=T, C=C, dh=dh, seed=2100 + T + dh)
+    x = WL.make_inputs(w, with_grads=False)
+    x["m_in"] = (1e-2 * np.random.default_rng(T).standard_normal(x["w_in"].shape)).astype(
+        np.float32)
+    errs = fwd_errors(run_forward(w, x), x, w)
+    print("d128 fwd T=%d C=%d dh=%d" % (T, C, dh), {k: "%.2e" % v for k, v in errs.items()},
+          flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+@pytest.mark.parametrize("T,C,dh", [(200, 32, 64), (300, 64, 128), (260, 100, 256),
+                                    (600, 512, 512), (130, 16, 512)])
+def test_backward_d128(T, C, dh):
+    w = d128(T=T, C=C, dh=dh, backward=True, seed=2200 + T + dh)
+    x = with_state_inputs(WL.make_inputs(w), T, m_scale=1e-2)
+    errs = berrors(gpu_fwd_bwd(w, x), oracle_bwd(w, x))
+    print("d128 bwd T=%d C=%d dh=%d" % (T, C, dh), {k: "%.2e" % v for k, v in errs.items()},
+          flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+def test_d128_more_units_than_resident_groups():
+    # dh 512 on eight workgroups per unit: 40 units are more groups than the
+    # device holds at once (256 CUs / 8 = 32), so groups take units in turn;
+    # every unit is checked, forward and backward
+    w = d128(B=5, H=8, T=96, C=64, backward=True, seed=2300)
+    x = WL.make_inputs(w)
+    t = to_dev(x, "bf16")
+    cfg = config_of(w)
+    out, wo, mo, ws = e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"],
+                                    t["gamma"], t["w_in"], None, save_for_backward=True)
+    g = e2ttt.backward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"], t["w_in"],
+                       None, ws, t["d_out"])
+    torch.cuda.synchronize()
+    errs = fwd_errors((out, wo, mo), x, w)
+    errs.update(berrors(g, oracle_bwd(w, x)))
+    print("d128 40 units", {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+def test_paper_1p3b_layer_sampled_units():
+    # the paper's throughput shape (B2 H16 T2048, d 128, dh 512, C 512): the
+    # full launch, the oracle on two units, forward and backward
+    w = WL.PAPER_1P3B
+    x = WL.make_inputs(w)
+    g = gpu_fwd_bwd(w, x)
+    units = [0, 29]
+    xs = WL.make_inputs(w, units=units)
+    ref = oracle_bwd(w, xs)
+    errs = berrors(g, ref, units)
+    print("paper 1.3B d128 C512 bwd", {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+    for n in GRADS:
+        assert torch.isfinite(g[n].float()).all(), n
+
+
+def test_apply_refuses_d128():
+    w = d128(T=1)
+    x = WL.make_inputs(w, with_grads=False)
+    t = to_dev(x, "bf16")
+    with pytest.raises(e2ttt.E2TTTError, match="unsupported"):
+        e2ttt.apply(config_of(w), t["q"], t["w_in"])
