@@ -64,9 +64,29 @@ def cpu_baseline(w, seconds_hint: float = 20.0) -> dict:
     dt = time.perf_counter() - t0
     # the full workload has B*H units; with units spread over the same threads
     full = dt * (w.B * w.H) / n_units
+    # one unit on one thread: the oracle's single-core rate, scaled the same way
+    x1 = WL.make_inputs(w, units=[0])
+    t1 = time.perf_counter()
+    oracle.forward(x1["q"], x1["k"], x1["v"], x1["eta"], x1["beta"], x1["gamma"], x1["w_in"], None,
+                   C=w.C, fw=w.fw, dh=w.dh, nthreads=1)
+    oracle.backward(x1["q"], x1["k"], x1["v"], x1["eta"], x1["beta"], x1["gamma"], x1["w_in"], None,
+                    x1["d_out"], C=w.C, fw=w.fw, dh=w.dh, nthreads=1)
+    dt1 = time.perf_counter() - t1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": (w.B * w.T) / full, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": "%d of %d (batch, head) units, full T=%d, fwd+bwd, fp64, %.1f s wall; "
-                      "scaled by %d/%d" % (n_units, w.B * w.H, w.T, dt, w.B * w.H, n_units)}
+                      "scaled by %d/%d" % (n_units, w.B * w.H, w.T, dt, w.B * w.H, n_units),
+            "single_thread_value": (w.B * w.T) / (dt1 * w.B * w.H),
+            "single_thread_sample": "1 unit on 1 thread, %.1f s, scaled by %d" % (dt1, w.B * w.H),
+            "cpu_model": model}
 
 
 def time_long_chunk(e2ttt, w, t, dev, reps: int = 10) -> dict:
