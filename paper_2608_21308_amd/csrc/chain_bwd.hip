@@ -535,9 +535,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           const int i = l16 * EPL + q;
           yk[t * D + i] = z[q];
           ek[t * D + i] = e[q];
-          dyl[t * S::LDD + i] = O::to_e(dyv[q]);
-          dyt[it_idx<S>(i, t)] = O::to_e(dyv[q]);
         }
+        store_row_ti<S, EPL>(dyl, S::LDD, t, l16 * EPL, dyv);
+        store_row_it<S, EPL>(dyt, t, l16 * EPL, dyv);
         if (l16 == 0) row[2 * t + 1] = mez;
               }
       }
@@ -861,10 +861,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) {
             const int i = l16 * EPL + q;
             ek[t * D + i] = eh[q];
-            yh[t * S::LDD + i] = O::to_e(yhv[q]);
-            yht[it_idx<S>(i, t)] = O::to_e(yhv[q]);
             if (t < len && t >= rlo && t < rhi) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
           }
+          store_row_ti<S, EPL>(yh, S::LDD, t, l16 * EPL, yhv);
+          store_row_it<S, EPL>(yht, t, l16 * EPL, yhv);
                   }
         }
       }
@@ -875,11 +875,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
         // K^T into RR for the first-layer accumulation
         E* xkt = reinterpret_cast<E*>(rr);
-#pragma unroll 1
-        for (int idx = tid; idx < D * S::CM; idx += S::NT) {
-          const int i = idx % D, t = idx / D;
-          xkt[it_idx<S>(i, t)] = xk[t * S::LDD + i];
-        }
+        transpose_to_it<S>(xkt, xk, tid);
         const auto& w2q = w0q[SEC];
 #pragma unroll
         for (int tb = 0; tb < NTB; ++tb)
@@ -981,11 +977,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         if (tid < S::CM) row[2 * tid] = prq;
         __syncthreads();
         if (r >= 0) prefetch_k(u, r, kt);              // the next tile (r, kt advanced above)
-#pragma unroll 1
-        for (int idx = tid; idx < D * S::CM; idx += S::NT) {
-          const int i = idx % D, t = idx / D;
-          xqt[it_idx<S>(i, t)] = xq[t * S::LDD + i];
-        }
+        transpose_to_it<S>(xqt, xq, tid);
         // Yb_Q = LN backward of dO at the Q rows (dO itself when there is no LN)
 #pragma unroll
         for (int it_ = 0; it_ < (S::CM + 4 * NW - 1) / (4 * NW); ++it_) {
@@ -1012,12 +1004,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int q = 0; q < EPL; ++q) yb[q] = dov[q];
           }
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            const int i = l16 * EPL + q;
-            ybq[t * S::LDD + i] = O::to_e(yb[q]);
-            ybqt[it_idx<S>(i, t)] = O::to_e(yb[q]);
-          }
+          store_row_ti<S, EPL>(ybq, S::LDD, t, l16 * EPL, yb);
+          store_row_it<S, EPL>(ybqt, t, l16 * EPL, yb);
                   }
         }
         if constexpr (SW) {   // the SwiGLU query side is recomputed from W_0

@@ -353,6 +353,60 @@ __device__ __forceinline__ typename S::O::Frag it_frag(const typename S::E* base
   return lds_frag<S::BF>(base, S::LDC, row, k0, g ^ ((row >> 4) & 3));
 }
 
+// Row-phase stores: a lane holds EPL consecutive head indices i0 .. i0+EPL-1
+// (i0 a multiple of EPL) of token row t.
+// Into a [t][i] operand array (leading dimension ld): one 8-byte store per
+// four bf16 values (the rows are 8-byte aligned), element stores otherwise.
+template <class S, int EPL>
+__device__ __forceinline__ void store_row_ti(typename S::E* dst, int ld, int t, int i0,
+                                             const float (&v)[EPL]) {
+  if constexpr (S::BF && EPL % 4 == 0) {
+#pragma unroll
+    for (int k = 0; k < EPL / 4; ++k)
+      *reinterpret_cast<typename S::O::Q*>(dst + t * ld + i0 + 4 * k) =
+          S::O::cvt(f32x4{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]});
+  } else {
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) dst[t * ld + i0 + q] = S::O::to_e(v[q]);
+  }
+}
+// Into an [i][t] operand array (it_idx layout), each value scaled by `sc`:
+// the EPL rows lie in one 16-row block, so they share the quad permutation and
+// sit at one base address plus multiples of the row stride; on the bf16 path
+// two values are converted per instruction.
+template <class S, int EPL>
+__device__ __forceinline__ void store_row_it(typename S::E* dst, int t, int i0,
+                                             const float (&v)[EPL], float sc = 1.0f) {
+  static_assert(16 % EPL == 0, "a lane's head indices must lie in one 16-row block");
+  const int b = it_idx<S>(i0, t);
+  if constexpr (S::BF && EPL % 2 == 0) {
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+#pragma unroll
+    for (int q = 0; q < EPL; q += 2) {
+      const bf16x2 pr = {(__bf16)(sc * v[q]), (__bf16)(sc * v[q + 1])};
+      dst[b + q * S::LDC] = pr[0];
+      dst[b + (q + 1) * S::LDC] = pr[1];
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) dst[b + q * S::LDC] = S::O::to_e(sc * v[q]);
+  }
+}
+// [t][i] -> [i][t] (it_idx layout) copy of a CM x D operand tile, four tokens
+// of one head index per item (one quad store).
+template <class S>
+__device__ __forceinline__ void transpose_to_it(typename S::E* dst, const typename S::E* src,
+                                                int tid) {
+#pragma unroll 1
+  for (int idx = tid; idx < S::D * (S::CM / 4); idx += S::NT) {
+    const int i = idx % S::D, t0 = 4 * (idx / S::D);
+    typename S::O::Q qv;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) qv[q4] = src[(t0 + q4) * S::LDD + i];
+    *reinterpret_cast<typename S::O::Q*>(&dst[it_idx<S>(i, t0)]) = qv;
+  }
+}
+
 // Copy a CM x D token tile (rows < len, zero beyond) from global io memory to
 // LDS in 16-byte vectors (the io element type equals the LDS element type).
 template <class S>

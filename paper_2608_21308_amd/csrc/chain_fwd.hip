@@ -262,14 +262,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       if constexpr (RELOAD) w0_mats(0, 1);
       {
       E2TTT_LANE_IDS;
-#pragma unroll 1
-      for (int idx = tid; idx < D * (S::CM / 4); idx += S::NT) {
-        const int i = idx % D, t0 = 4 * (idx / D);
-        typename O::Q qk;
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) qk[q4] = sm.xk[(t0 + q4) * S::LDD + i];
-        *reinterpret_cast<typename O::Q*>(&sm.kt[it_idx<S>(i, t0)]) = qk;
-      }
+      transpose_to_it<S>(sm.kt, sm.xk, tid);
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
@@ -478,13 +471,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int q = 0; q < EPL; ++q) zsave[it_][q] = z[q];
           rsave[it_] = sig;
           const float kwt = sm.kw[t], kmt = sm.km[t];
-#pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            const int i = l16 * EPL + q;
-            sm.dy[t * S::LDD + i] = O::to_e(dyv[q]);
-            sm.dytw[it_idx<S>(i, t)] = O::to_e(kwt * dyv[q]);
-            sm.dytm[it_idx<S>(i, t)] = O::to_e(kmt * dyv[q]);
-          }
+          store_row_ti<S, EPL>(sm.dy, S::LDD, t, l16 * EPL, dyv);
+          store_row_it<S, EPL>(sm.dytw, t, l16 * EPL, dyv, kwt);
+          store_row_it<S, EPL>(sm.dytm, t, l16 * EPL, dyv, kmt);
                   }
         }
         if (E2TTT_ARG(zk)) {
