@@ -140,6 +140,7 @@ size_t e2ttt_backward_scratch_bytes(const e2ttt_desc* desc);
  *   workspace, workspace_bytes    caller-owned device memory, at least
  *                                 e2ttt_workspace_bytes(desc, save_for_backward)
  * w_out / m_out may alias w_in / m_in only when save_for_backward == 0.
+ * q, k, v, out and workspace must be 16-byte aligned (else E2TTT_ERR_BAD_SHAPE).
  */
 e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const void* k,
                                  const void* v, const float* eta, const float* beta,
@@ -160,6 +161,8 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
  *   d_gamma           [B][H][T] f32; must be NULL iff gamma is NULL
  *   d_w_in, d_m_in    [B][H][P] f32     gradient of the initial state
  *   scratch           at least e2ttt_backward_scratch_bytes(desc) bytes
+ * q, k, v, workspace, d_out, dq, dk, dv and scratch must be 16-byte aligned
+ * (else E2TTT_ERR_BAD_SHAPE).
  */
 e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const void* k,
                                   const void* v, const float* eta, const float* beta,

@@ -26,6 +26,9 @@ constexpr int kMaxChunk = 512;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// The kernels move token rows, checkpoints and partial sums as 16-byte vectors.
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 struct Plan {
   long U = 0, T = 0, NC = 0, P = 0;
   ChainConfig cfg{};
@@ -298,6 +301,8 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   if (st != E2TTT_OK) return st;
   if (!q || !k || !v || !eta || !beta || !w_in || !out || !w_out || !m_out || !workspace)
     return E2TTT_ERR_NULL_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(workspace))
+    return E2TTT_ERR_BAD_SHAPE;
   if (workspace_bytes < (save_for_backward ? pl.ws_bytes_save : pl.ws_bytes))
     return E2TTT_ERR_WORKSPACE_TOO_SMALL;
   if (save_for_backward && (w_out == w_in || (m_in && m_out == m_in))) return E2TTT_ERR_BAD_SHAPE;
@@ -353,6 +358,9 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
       !d_eta || !d_beta || !d_w_in || !d_m_in || !scratch)
     return E2TTT_ERR_NULL_ARG;
   if ((gamma == nullptr) != (d_gamma == nullptr)) return E2TTT_ERR_BAD_SHAPE;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(workspace) ||
+      !aligned16(d_out) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned16(scratch))
+    return E2TTT_ERR_BAD_SHAPE;
   if (workspace_bytes < pl.ws_bytes_save || scratch_bytes < pl.scratch_bytes)
     return E2TTT_ERR_WORKSPACE_TOO_SMALL;
   hipStream_t s = static_cast<hipStream_t>(stream);

@@ -338,10 +338,7 @@ __device__ __forceinline__ void flush_dkdq(const ChainArgs& a, long p, int parit
         x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
       }
       typename IO::T* d = (sec == 1) ? dk : dq;
-      IO::st(d + e + 0, x.x);
-      IO::st(d + e + 1, x.y);
-      IO::st(d + e + 2, x.z);
-      IO::st(d + e + 3, x.w);
+      IO::st4(d + e, f32x4{x.x, x.y, x.z, x.w});
     }
   }
 }
@@ -858,11 +855,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             for (int q = 0; q < EPL; ++q) { eh[q] = dyhv[q]; yhv[q] = -eh[q]; }
           }
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            const int i = l16 * EPL + q;
-            ek[t * D + i] = eh[q];
-            if (t < len && t >= rlo && t < rhi) IoT<S::BF>::st(dvp + (long)t * D + i, eh[q]);
-          }
+          for (int q = 0; q < EPL; ++q) ek[t * D + l16 * EPL + q] = eh[q];
+          if (t < len && t >= rlo && t < rhi)
+            store_row_io<IoT<S::BF>, EPL>(dvp + (long)t * D + l16 * EPL, eh);
           store_row_ti<S, EPL>(yh, S::LDD, t, l16 * EPL, yhv);
           store_row_it<S, EPL>(yht, t, l16 * EPL, yhv);
                   }

@@ -392,6 +392,20 @@ __device__ __forceinline__ void store_row_it(typename S::E* dst, int t, int i0,
     for (int q = 0; q < EPL; ++q) dst[b + q * S::LDC] = S::O::to_e(sc * v[q]);
   }
 }
+// EPL consecutive values of a row to global memory (io element type T, or
+// fp32): four values per vector store when EPL allows (dst 8- or 16-byte aligned).
+template <class IO, int EPL>
+__device__ __forceinline__ void store_row_io(typename IO::T* dst, const float (&v)[EPL]) {
+  if constexpr (EPL % 4 == 0) {
+#pragma unroll
+    for (int k = 0; k < EPL / 4; ++k)
+      IO::st4(dst + 4 * k, f32x4{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]});
+  } else {
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) IO::st(dst + q, v[q]);
+  }
+}
+
 // [t][i] -> [i][t] (it_idx layout) copy of a CM x D operand tile, four tokens
 // of one head index per item (one quad store).
 template <class S>

@@ -481,8 +481,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t = 4 * w + it_ * 4 * S::NW + (lane >> 4);
             if (t < S::CM && keep[it_]) {
-#pragma unroll
-              for (int q = 0; q < EPL; ++q) E2TTT_ARG(zk)[(row0 + t) * D + l16 * EPL + q] = zsave[it_][q];
+              store_row_io<IoT<false>, EPL>(E2TTT_ARG(zk) + (row0 + t) * D + l16 * EPL, zsave[it_]);
               if (l16 == 0) E2TTT_ARG(rk)[row0 + t] = rsave[it_];
             }
           }
@@ -672,11 +671,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             for (int q = 0; q < EPL; ++q) f[q] = yv[q];
           }
           if (t < len) {
-#pragma unroll
-            for (int q = 0; q < EPL; ++q) IO::st(outp + (long)t * D + l16 * EPL + q, f[q]);
+            store_row_io<IO, EPL>(outp + (long)t * D + l16 * EPL, f);
             if (E2TTT_ARG(zq)) {
-#pragma unroll
-              for (int q = 0; q < EPL; ++q) E2TTT_ARG(zq)[(row0 + t) * D + l16 * EPL + q] = yv[q];
+              store_row_io<IoT<false>, EPL>(E2TTT_ARG(zq) + (row0 + t) * D + l16 * EPL, yv);
               if (l16 == 0) E2TTT_ARG(rq)[row0 + t] = sig;
             }
           }

@@ -238,11 +238,17 @@ template <> struct IoT<true> {
   using T = __bf16;
   static __device__ __forceinline__ float ld(const T* p) { return (float)*p; }
   static __device__ __forceinline__ void st(T* p, float x) { *p = (__bf16)x; }
+  // four consecutive values, one 8-byte store (p 8-byte aligned)
+  static __device__ __forceinline__ void st4(T* p, f32x4 x) {
+    *reinterpret_cast<bf16x4*>(p) = bf16x4{(__bf16)x[0], (__bf16)x[1], (__bf16)x[2], (__bf16)x[3]};
+  }
 };
 template <> struct IoT<false> {
   using T = float;
   static __device__ __forceinline__ float ld(const T* p) { return *p; }
   static __device__ __forceinline__ void st(T* p, float x) { *p = x; }
+  // four consecutive values, one 16-byte store (p 16-byte aligned)
+  static __device__ __forceinline__ void st4(T* p, f32x4 x) { *reinterpret_cast<f32x4*>(p) = x; }
 };
 
 }  // namespace e2ttt

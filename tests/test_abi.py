@@ -89,8 +89,17 @@ def test_null_and_workspace_errors(lib):
     a = list(args)
     a[9] = a[6] = ctypes.c_void_p(32)
     assert lib.e2ttt_chunk_forward(ctypes.byref(d), *a, 1 << 40, 1, None) == 2
+    # token tensors and buffers are moved as 16-byte vectors: misaligned ones are refused
+    for i in (0, 1, 2, 8, 11):    # q k v out workspace
+        a = list(args)
+        a[i] = ctypes.c_void_p(18)
+        assert lib.e2ttt_chunk_forward(ctypes.byref(d), *a, 1 << 40, 0, None) == 2, i
     # backward: d_gamma must be given iff gamma is
     bargs = [fake] * 9 + [1 << 40] + [fake] * 12 + [1 << 40, None]
+    for i in (0, 1, 2, 8, 10, 13, 14, 15, 21):   # q k v workspace d_out dq dk dv scratch
+        b = list(bargs)
+        b[i] = ctypes.c_void_p(24)
+        assert lib.e2ttt_chunk_backward(ctypes.byref(d), *b) == 2, i
     b = list(bargs)
     b[5] = None
     assert lib.e2ttt_chunk_backward(ctypes.byref(d), *b) == 2
