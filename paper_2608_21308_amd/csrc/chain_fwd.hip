@@ -481,7 +481,16 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t = 4 * w + it_ * 4 * S::NW + (lane >> 4);
             if (t < S::CM && keep[it_]) {
-              store_row_io<IoT<false>, EPL>(E2TTT_ARG(zk) + (row0 + t) * D + l16 * EPL, zsave[it_]);
+              // (SwiGLU, at the register limit, keeps element stores: with the
+              // vector store the three-workgroup variant spilled 57 VGPRs)
+              if constexpr (S::FW == 0) {
+                store_row_io<IoT<false>, EPL>(E2TTT_ARG(zk) + (row0 + t) * D + l16 * EPL,
+                                              zsave[it_]);
+              } else {
+#pragma unroll
+                for (int q = 0; q < EPL; ++q)
+                  E2TTT_ARG(zk)[(row0 + t) * D + l16 * EPL + q] = zsave[it_][q];
+              }
               if (l16 == 0) E2TTT_ARG(rk)[row0 + t] = rsave[it_];
             }
           }
