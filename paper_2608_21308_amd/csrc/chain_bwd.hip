@@ -600,12 +600,21 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       {
         const auto& w1q = w0q;            // first-layer matrices m < NF
         const auto& w2q = w0q[SEC];
+        // operand copies of the adjoint state, formed once for all token blocks
+        opaque_state<S>(Wb);
+        opaque_state<S>(Mb);
+        Q wbq[NMAT][NJB][NIB], mbq[NMAT][NJB][NIB];
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+              wbq[m][jj][ib] = O::cvt(Wb.t[m][jj][ib]);
+              mbq[m][jj][ib] = O::cvt(Mb.t[m][jj][ib]);
+            }
 #pragma unroll
         for (int tb = 0; tb < NTB; ++tb) {
-          // bf16 operand copies of the adjoint state are re-formed per token
-          // block (a few conversions) instead of being held across the loop
-          opaque_state<S>(Wb);
-          opaque_state<S>(Mb);
           E2TTT_LANE_IDS;
           float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -622,8 +631,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
               for (int h = 0; h < S::NH; ++h) {
                 b2.h[h] = w2q[jj][S::NH * p + h];
-                bw.h[h] = O::cvt(Wb.t[SEC][jj][S::NH * p + h]);
-                bm.h[h] = O::cvt(Mb.t[SEC][jj][S::NH * p + h]);
+                bw.h[h] = wbq[SEC][jj][S::NH * p + h];
+                bm.h[h] = mbq[SEC][jj][S::NH * p + h];
               }
               dA = O::mma(dA, fy, b2);
               rW = O::mma(rW, fy, bw);
@@ -633,8 +642,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
                 for (int h = 0; h < S::NH; ++h) {
                   b2.h[h] = w1q[m][jj][S::NH * p + h];
-                  bw.h[h] = O::cvt(Wb.t[m][jj][S::NH * p + h]);
-                  bm.h[h] = O::cvt(Mb.t[m][jj][S::NH * p + h]);
+                  bw.h[h] = wbq[m][jj][S::NH * p + h];
+                  bm.h[h] = mbq[m][jj][S::NH * p + h];
                 }
                 hk[m] = O::mma(hk[m], fk, b2);
                 uW[m] = O::mma(uW[m], fk, bw);
