@@ -597,13 +597,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         else
           return HhR[m][tb][jj];
       };
+      // operand copies of the adjoint state, formed once for all token blocks
+      // of P4 and the j-rounds after it
+      Q wbq[NMAT][NJB][NIB], mbq[NMAT][NJB][NIB];
       {
         const auto& w1q = w0q;            // first-layer matrices m < NF
         const auto& w2q = w0q[SEC];
-        // operand copies of the adjoint state, formed once for all token blocks
         opaque_state<S>(Wb);
         opaque_state<S>(Mb);
-        Q wbq[NMAT][NJB][NIB], mbq[NMAT][NJB][NIB];
 #pragma unroll
         for (int m = 0; m < NMAT; ++m)
 #pragma unroll
@@ -725,26 +726,26 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         if constexpr (L::J2) {
           jround2<S, !DH_LDS>(dkacc, skw, skm, ja, jw, jw2,
                               [&](int tb, int jj) { return dHq[mq][tb][jj]; },
-                              [&](int ib, int jj) { return Wb.t[m][jj][ib]; },
-                              [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+                              [&](int ib, int jj) { return wbq[m][jj][ib]; },
+                              [&](int ib, int jj) { return mbq[m][jj][ib]; }, w, g, c);
         } else {
           jround<S, !DH_LDS>(dkacc, skw, ja, jw,
                              [&](int tb, int jj) { return dHq[mq][tb][jj]; },
-                             [&](int ib, int jj) { return Wb.t[m][jj][ib]; }, w, g, c);
+                             [&](int ib, int jj) { return wbq[m][jj][ib]; }, w, g, c);
           jround<S, false>(dkacc, skm, ja, jw,
                            [&](int tb, int jj) { return dHq[mq][tb][jj]; },
-                           [&](int ib, int jj) { return Mb.t[m][jj][ib]; }, w, g, c);
+                           [&](int ib, int jj) { return mbq[m][jj][ib]; }, w, g, c);
         }
       }
       if constexpr (L::J2) {
         jround2<S, true>(dyhacc, skw, skm, ja, jw, jw2, [&](int tb, int jj) { return Akq[tb][jj]; },
-                         [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; },
-                         [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+                         [&](int ib, int jj) { return wbq[SEC][jj][ib]; },
+                         [&](int ib, int jj) { return mbq[SEC][jj][ib]; }, w, g, c);
       } else {
         jround<S>(dyhacc, skw, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
-                  [&](int ib, int jj) { return Wb.t[SEC][jj][ib]; }, w, g, c);
+                  [&](int ib, int jj) { return wbq[SEC][jj][ib]; }, w, g, c);
         jround<S, false>(dyhacc, skm, ja, jw, [&](int tb, int jj) { return Akq[tb][jj]; },
-                         [&](int ib, int jj) { return Mb.t[SEC][jj][ib]; }, w, g, c);
+                         [&](int ib, int jj) { return mbq[SEC][jj][ib]; }, w, g, c);
       }
       }
 
@@ -906,6 +907,13 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         __syncthreads();   // xkt complete
         // Wb2 += dY^T dAh + Yh^T A ;  Wb1 += K^T Hh
         opaque_state<S>(Wb);
+        Q hhq[NF][NTB][NJB];   // Hh as operand quads, for every head block and the dk round
+#pragma unroll
+        for (int m = 0; m < NF; ++m)
+#pragma unroll
+          for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj) hhq[m][tb][jj] = O::cvt(hh_at(m, tb, jj, lane));
 #pragma unroll
         for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
@@ -926,7 +934,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               for (int m = 0; m < NF; ++m) {
                 typename O::Frag bh;
 #pragma unroll
-                for (int h = 0; h < S::NH; ++h) bh.h[h] = O::cvt(hh_at(m, S::NH * p + h, jj, lane));
+                for (int h = 0; h < S::NH; ++h) bh.h[h] = hhq[m][S::NH * p + h][jj];
                 Wb.t[m][jj][ib] = O::mma(Wb.t[m][jj][ib], fk, bh);
               }
             }
@@ -936,7 +944,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
         for (int m = 0; m < NF; ++m) {
           const auto& w1q = w0q[m];
-          jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return hh_at(m, tb, jj, lane); },
+          jround<S>(dkacc, nullptr, ja, jw, [&](int tb, int jj) { return hhq[m][tb][jj]; },
                     [&](int ib, int jj) { return w1q[jj][ib]; }, w, g, c);
         }
         const float ksign = (resln && rank == 0) ? -1.0f : 0.0f;
