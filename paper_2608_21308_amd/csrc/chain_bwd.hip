@@ -364,6 +364,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   constexpr int EPL = D / 16;        // head elements per lane in row phases
   constexpr int RPW = row_share<S>(); // rows of dv, dk, dq written by one rank (last: fewer)
   constexpr int NPEER = S::NS - 1;
+  // the peers' dYh rows are loaded right after the swap while they are few;
+  // with many peers or wide rows (head dim 128) that would hold too many
+  // registers, and P7 loads every rank's partial where it adds them
+  constexpr bool PEER_EARLY = NPEER * EPL <= 8 && S::D <= 64;
   __shared__ __attribute__((aligned(16))) unsigned char smem[L::TOTAL];
   __shared__ int sword[2];
   E* xk = reinterpret_cast<E*>(smem + L::XK);
@@ -776,7 +780,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
       __syncthreads();
       constexpr int P7IT = (S::CM + 4 * NW - 1) / (4 * NW);
-      float pdyh[S::NS > 1 ? P7IT : 1][S::NS > 1 ? NPEER : 1][EPL];
+      float pdyh[S::NS > 1 && PEER_EARLY ? P7IT : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
         E2TTT_LANE_IDS;
         float* mine = bwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par);
@@ -788,7 +792,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         // the peers' rows of every P7 step, loaded before the global stores
         // below (which would otherwise order each step's loads after them)
 #pragma unroll
-        for (int k = 0; k < NPEER; ++k) {
+        for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
           const float* dyh_peer = bwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par);
 #pragma unroll
           for (int it_ = 0; it_ < P7IT; ++it_) {
@@ -818,13 +822,24 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             dyhv[q] = dyh[t * D + l16 * EPL + q];
             e[q] = ek[t * D + l16 * EPL + q];
           }
-          if constexpr (S::NS > 1) {
+          if constexpr (S::NS > 1 && PEER_EARLY) {
 #pragma unroll
             for (int q = 0; q < EPL; ++q) {
               float pv[NPEER];
 #pragma unroll
               for (int k = 0; k < NPEER; ++k) pv[k] = pdyh[it_][k][q];
               dyhv[q] = sum_ranks<S::NS>(dyhv[q], pv, rank);
+            }
+          } else if constexpr (S::NS > 1) {
+            // every rank's partial from its slot (this rank's too), added in
+            // rank order as sum_ranks does: the same sum on every rank
+#pragma unroll
+            for (int r = 0; r < S::NS; ++r) {
+              float pr[EPL];
+              load_row_part<EPL>(pr, bwd_slot<S>(E2TTT_ARG(xbuf), px.p, r, par) + t * D +
+                                         l16 * EPL);
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) dyhv[q] = (r == 0) ? pr[q] : dyhv[q] + pr[q];
             }
           }
           if (resln) {
