@@ -381,9 +381,10 @@ __device__ __forceinline__ void store_row_it(typename S::E* dst, int t, int i0,
   const int b = it_idx<S>(i0, t);
   if constexpr (S::BF && EPL % 2 == 0) {
     typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+    typedef __attribute__((ext_vector_type(2))) float f32x2;
 #pragma unroll
     for (int q = 0; q < EPL; q += 2) {
-      const bf16x2 pr = {(__bf16)(sc * v[q]), (__bf16)(sc * v[q + 1])};
+      const bf16x2 pr = __builtin_convertvector(f32x2{sc * v[q], sc * v[q + 1]}, bf16x2);
       dst[b + q * S::LDC] = pr[0];
       dst[b + (q + 1) * S::LDC] = pr[1];
     }
