@@ -46,7 +46,7 @@
  *   (Wg, Wu, Wd are the paper's W1, W2, W3 of the SwiGLU net.)
  *
  * Supported shapes: io = BF16 with d = 64 (dh <= 256 for the MLP, <= 192 for
- * SwiGLU) or d = 128 (the GELU MLP, dh <= 512), or io = F32 with d = 16
+ * SwiGLU) or d = 128 (dh <= 512), or io = F32 with d = 16
  * (dh <= 128); dh is padded inside the library to a multiple of 16;
  * 1 <= chunk <= 512 (the paper's C = 512), forward and backward; a chunk
  * longer than the kernels' token tile (64 rows, 32 at d = 128) runs as

@@ -53,17 +53,17 @@ e2ttt_status select_config(const e2ttt_desc& d, ChainConfig& cfg) {
   const int nblk = (d.dh + 15) / 16;
   cfg.ns = 1;
   if (cfg.bf && d.d == 128) {
-    // head dim 128 (the paper's 1.3B model, 2048 / 16 heads), GELU MLP: the
-    // state of 64 hidden columns per workgroup (four waves, one per SIMD) and
-    // 32-row token tiles (longer chunks run as consecutive tiles) fit the
-    // register file and LDS; wider nets spread over 2, 4 or 8 workgroups
-    if (d.fw != E2TTT_FW_GELU_MLP) return E2TTT_ERR_UNSUPPORTED;
+    // head dim 128 (the paper's 1.3B model, 2048 / 16 heads): the state of 64
+    // hidden columns per workgroup (four waves, one per SIMD) and 32-row token
+    // tiles (longer chunks run as consecutive tiles) fit LDS; wider nets spread
+    // over 2, 4, 6 (SwiGLU) or 8 workgroups
     cfg.ntb = 2;
     cfg.nw = 4;
     cfg.njb = 1;
     if (nblk <= 4) cfg.ns = 1;
     else if (nblk <= 8) cfg.ns = 2;
     else if (nblk <= 16) cfg.ns = 4;
+    else if (d.fw == E2TTT_FW_SWIGLU && nblk <= 24) cfg.ns = 6;
     else if (nblk <= 32) cfg.ns = 8;
     else return E2TTT_ERR_UNSUPPORTED;
   } else if (cfg.bf) {

@@ -1,5 +1,5 @@
 """GPU parity at head dim 128 (the paper's 1.3B model: hidden 2048 over 16
-heads, Sec. 5), GELU MLP on bf16.  The kernels hold 64 hidden columns per
+heads, Sec. 5), GELU MLP and SwiGLU on bf16.  The kernels hold 64 hidden columns per
 workgroup and work on 32-row token tiles, so dh 64 / 128 / 256 / 512 run on
 one, two, four and eight workgroups per unit, and chunks longer than 32
 tokens run as consecutive tiles at the chunk-start weights.  The oracle is
@@ -30,17 +30,17 @@ def d128(**kw):
     return WL.PAPER_1P3B.with_(**base)
 
 
-def run_forward(w, x):
+def run_forward(w, x, flags=0):
     t = to_dev(x, "bf16")
-    out, wo, mo, _ = e2ttt.forward(config_of(w), t["q"], t["k"], t["v"], t["eta"], t["beta"],
-                                   t["gamma"], t["w_in"], t.get("m_in"))
+    out, wo, mo, _ = e2ttt.forward(config_of(w, flags=flags), t["q"], t["k"], t["v"], t["eta"],
+                                   t["beta"], t["gamma"], t["w_in"], t.get("m_in"))
     torch.cuda.synchronize()
     return out, wo, mo
 
 
-def fwd_errors(got, x, w, units=None):
+def fwd_errors(got, x, w, units=None, flags=0):
     ro, rw, rm = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"],
-                                x["w_in"], x.get("m_in"), C=w.C, fw=w.fw, dh=w.dh)
+                                x["w_in"], x.get("m_in"), C=w.C, fw=w.fw, dh=w.dh, flags=flags)
     out, wo, mo = (g.float().cpu().numpy() for g in got)
     if units is not None:
         pick = lambda a: a.reshape((-1,) + a.shape[2:])[units][None]
@@ -106,6 +106,35 @@ def test_paper_1p3b_layer_sampled_units():
     assert all(e <= TOL["bf16"] for e in errs.values()), errs
     for n in GRADS:
         assert torch.isfinite(g[n].float()).all(), n
+
+
+# SwiGLU at d = 128: dh 64 / 128 / 256 / 344 (the 8/3 width) / 512 on 1 / 2 / 4 / 6 / 8
+# workgroups per unit.  The residual-LayerNorm SwiGLU trajectories of these inputs
+# are chaotic over many chunks, so that form is checked over one or two chunks and
+# the bare net (flags 1) over longer runs.
+@pytest.mark.parametrize("T,C,dh,flags", [(200, 32, 64, 1), (300, 64, 128, 1), (260, 100, 256, 1),
+                                          (500, 200, 344, 1), (130, 64, 512, 1),
+                                          (200, 200, 344, 0), (96, 64, 128, 0)])
+def test_forward_d128_swiglu(T, C, dh, flags):
+    w = d128(fw=WL.FW_SWIGLU, T=T, C=C, dh=dh, seed=2400 + T + dh)
+    x = WL.make_inputs(w, with_grads=False)
+    x["m_in"] = (1e-2 * np.random.default_rng(T).standard_normal(x["w_in"].shape)).astype(
+        np.float32)
+    errs = fwd_errors(run_forward(w, x, flags), x, w, flags=flags)
+    print("d128 swiglu fwd T=%d C=%d dh=%d flags=%d" % (T, C, dh, flags),
+          {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
+
+
+@pytest.mark.parametrize("T,C,dh,flags", [(200, 32, 64, 1), (300, 64, 128, 1), (400, 200, 344, 1),
+                                          (130, 64, 512, 1), (200, 100, 344, 0)])
+def test_backward_d128_swiglu(T, C, dh, flags):
+    w = d128(fw=WL.FW_SWIGLU, T=T, C=C, dh=dh, backward=True, seed=2500 + T + dh)
+    x = with_state_inputs(WL.make_inputs(w), T, m_scale=1e-2)
+    errs = berrors(gpu_fwd_bwd(w, x, flags), oracle_bwd(w, x, flags))
+    print("d128 swiglu bwd T=%d C=%d dh=%d flags=%d" % (T, C, dh, flags),
+          {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs
 
 
 def test_apply_refuses_d128():
