@@ -315,25 +315,25 @@ __device__ __forceinline__ float* bwd_slot(float* xbuf, long p, int rank, int pa
 // dk and dq of one chunk from the ranks' partials, added in rank order (rank
 // 0's carries the -eh and dO terms), rows [rlo, min(CM, rlo + RPW)) below len.
 template <class S>
-__device__ __forceinline__ void flush_dkdq(const ChainArgs& a, long p, int parity, long row0,
-                                           int len, int rlo, int tid) {
+__device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int len, int rlo,
+                                           int tid) {
   using IO = IoT<S::BF>;
   constexpr int RPW = row_share<S>();
   constexpr int NV = RPW * S::D / 4;
   const int tend = min(len, min(S::CM, rlo + RPW));
-  typename IO::T* dk = reinterpret_cast<typename IO::T*>(a.dk) + row0 * S::D;
-  typename IO::T* dq = reinterpret_cast<typename IO::T*>(a.dq) + row0 * S::D;
+  typename IO::T* dk = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dk)) + row0 * S::D;
+  typename IO::T* dq = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dq)) + row0 * S::D;
 #pragma unroll 1
   for (int v = tid; v < NV; v += S::NT) {
     const int e = rlo * S::D + 4 * v, t = e / S::D;
     if (t >= tend) continue;
 #pragma unroll
     for (int sec = 1; sec <= 2; ++sec) {
-      float4 x = *reinterpret_cast<const float4*>(bwd_slot<S>(a.xbuf, p, 0, parity) +
+      float4 x = *reinterpret_cast<const float4*>(bwd_slot<S>(E2TTT_ARG(xbuf), p, 0, parity) +
                                                   sec * S::CM * S::D + e);
 #pragma unroll
       for (int rk = 1; rk < S::NS; ++rk) {
-        const float4 y = *reinterpret_cast<const float4*>(bwd_slot<S>(a.xbuf, p, rk, parity) +
+        const float4 y = *reinterpret_cast<const float4*>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity) +
                                                           sec * S::CM * S::D + e);
         x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
       }
@@ -802,7 +802,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           }
         }
         if (pend_s0 >= 0)
-          flush_dkdq<S>(a, px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
+          flush_dkdq<S>(px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       }
 
       // ------------------------------------- P7: LayerNorm second order
@@ -1197,7 +1197,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       E2TTT_LANE_IDS;
       px.wait_for(px.seq_now(), sword);             // the peers' last post
       if (pend_s0 >= 0)
-        flush_dkdq<S>(a, px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
+        flush_dkdq<S>(px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       __syncthreads();
     }
     {
