@@ -14,7 +14,7 @@ import torch
 
 from oracle import averaged as A
 from paper_2608_21308_amd import e2ttt, workloads as WL
-from tests.gpu_util import TOL, config_of, rel_l2, to_dev
+from tests.gpu_util import TOL, config_of, parity_errors, tile_of, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -73,16 +73,19 @@ def run_oracle(w, x, flags):
 def compare(w, x, flags, what):
     got = run_gpu(w, x, flags | AVG)
     ref = run_oracle(w, x, flags)
-    errs = {}
+    pairs = {}
     for n, r in ref.items():
         if r is None:
             assert got[n] is None, n
             continue
         a = got[n].float().cpu().numpy()
         if n == "w_out":      # the state moves little: compare its change
-            errs[n] = rel_l2(a - x["w_in"], r - x["w_in"])
+            pairs[n] = (a - x["w_in"], r - x["w_in"], "state")
+        elif n in ("m_out", "d_w_in", "d_m_in"):
+            pairs[n] = (a, r, "state")
         else:
-            errs[n] = rel_l2(a, r)
+            pairs[n] = (a, r)
+    errs = parity_errors(pairs, tile_of(w.C))
     tol = TOL[w.io]
     print(what, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
     bad = {k: v for k, v in errs.items() if not v <= tol}

@@ -3,7 +3,8 @@ oracle's reverse-mode token loop, on identical seeded inputs.
 
 The loss is sum<d_out, out> + <d_w_out, w_out> + <d_m_out, m_out>; every
 gradient (q, k, v, eta, beta, gamma, w_in, m_in) is compared by rel-L2:
-1e-5 for fp32 io, 2e-2 for bf16 io.  Long fp32 runs and the chaotic SwiGLU +
+1e-5 for fp32 io, 2e-2 for bf16 io, and every block (a unit's tile of up to
+64 tokens, or a unit's state) within twice that.  Long fp32 runs and the chaotic SwiGLU +
 residual-LN workloads are handled as in the forward tests (short fp32 runs;
 chunk windows from the oracle's own state with a condition-aware bound).
 """
@@ -13,7 +14,8 @@ import torch
 
 from oracle import oracle
 from paper_2608_21308_amd import e2ttt, workloads as WL
-from tests.gpu_util import TOL, config_of, fp32_sensitivity, rel_l2, slice_tokens, to_dev
+from tests import fp32ref
+from tests.gpu_util import TOL, config_of, parity_errors, rel_l2, slice_tokens, tile_of, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -43,8 +45,10 @@ def oracle_bwd(w, x, flags=0):
                            fw=w.fw, dh=w.dh, flags=flags)
 
 
-def errors(g, ref, units=None):
-    errs = {}
+def errors(g, ref, units=None, C=64):
+    """Whole-tensor rel-L2 and largest block error (gpu_util.parity_errors) of
+    every gradient; units: the flat unit indices the reference covers."""
+    pairs = {}
     for n in GRADS:
         if ref.get(n) is None:
             assert g.get(n) is None
@@ -52,8 +56,9 @@ def errors(g, ref, units=None):
         a = g[n]
         if units is not None:
             a = a.reshape((-1,) + tuple(a.shape[2:]))[units][None]
-        errs[n] = rel_l2(a, ref[n])
-    return errs
+        pairs[n] = (a, ref[n], "state") if n in ("d_w_in", "d_m_in") else (a, ref[n])
+    # (g may hold torch tensors or numpy arrays)
+    return parity_errors(pairs, tile_of(C))
 
 
 def assert_tol(errs, io, what):
@@ -84,13 +89,16 @@ def test_backward_fp32_shapes(fw, T, C, dh, flags):
                               seed=700 + T + C + dh)
     x = with_state_inputs(WL.make_inputs(w), 11 + T)
     g = gpu_fwd_bwd(w, x, flags)
-    errs = errors(g, oracle_bwd(w, x, flags))
-    # 1e-5, widened only by the case's own fp32 conditioning (see the forward test)
-    sens = fp32_sensitivity(lambda y: oracle_bwd(w, y, flags), x)
-    bound = {n: max(TOL["f32"], 10 * sens[n]) for n in errs}
+    ref = oracle_bwd(w, x, flags)
+    errs = errors(g, ref, C=C)
+    # 1e-5, widened only where a plain float32 evaluation (tests/fp32ref.py)
+    # is itself farther than 1e-5 / FP32_FACTOR from the oracle
+    e32 = errors(fp32ref.backward(x, C=C, fw=fw, dh=dh, flags=flags), ref, C=C)
+    bound = fp32ref.fp32_bar(e32)
     what = "bwd fp32 fw=%d T=%d C=%d dh=%d flags=%d" % (fw, T, C, dh, flags)
-    print(what, {k: "%.2e" % v for k, v in errs.items()},
-          "sens", {k: "%.1e" % v for k, v in sens.items()}, flush=True)
+    print(what, "gpu", {k: "%.2e" % v for k, v in errs.items()},
+          "fp32 reference", {k: "%.1e" % v for k, v in e32.items()},
+          "above 1e-5:", sorted(n for n in errs if errs[n] > TOL["f32"]), flush=True)
     bad = {n: (errs[n], bound[n]) for n in errs if not errs[n] <= bound[n]}
     assert not bad, what + ": %s" % bad
 
@@ -99,7 +107,7 @@ def test_backward_tiny_fp32_workload():
     w = WL.WORKLOADS[0].with_(backward=True)
     x = WL.make_inputs(w)
     g = gpu_fwd_bwd(w, x)
-    assert_tol(errors(g, oracle_bwd(w, x)), "f32", "bwd " + w.name)
+    assert_tol(errors(g, oracle_bwd(w, x), C=w.C), "f32", "bwd " + w.name)
 
 
 def test_backward_without_gamma():
@@ -108,7 +116,7 @@ def test_backward_without_gamma():
     x["gamma"] = None
     g = gpu_fwd_bwd(w, x)
     assert g["d_gamma"] is None
-    assert_tol(errors(g, oracle_bwd(w, x)), "f32", "bwd gamma=None")
+    assert_tol(errors(g, oracle_bwd(w, x), C=w.C), "f32", "bwd gamma=None")
 
 
 # ------------------------------------------------------------ bf16 path
@@ -121,7 +129,7 @@ def test_backward_bf16_shapes(T, C, dh, fw, flags):
     w = WL.WORKLOADS[1].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, backward=True, seed=300 + T + dh)
     x = with_state_inputs(WL.make_inputs(w), T, m_scale=1e-2)
     g = gpu_fwd_bwd(w, x, flags)
-    assert_tol(errors(g, oracle_bwd(w, x, flags)), "bf16",
+    assert_tol(errors(g, oracle_bwd(w, x, flags), C=C), "bf16",
                "bwd bf16 T=%d C=%d dh=%d fw=%d flags=%d" % (T, C, dh, fw, flags))
 
 
@@ -133,7 +141,7 @@ def test_backward_1p3b_layer_sampled_units():
     units = [0, 93]
     xs = WL.make_inputs(w, units=units)
     ref = oracle_bwd(w, xs)
-    assert_tol(errors(g, ref, units), "bf16", "bwd " + w.name)
+    assert_tol(errors(g, ref, units, C=w.C), "bf16", "bwd " + w.name)
     for n in GRADS:
         assert torch.isfinite(g[n].float()).all(), n
 
@@ -152,14 +160,14 @@ def test_backward_swiglu_more_units_than_resident_groups():
     ref = oracle_bwd(w, WL.make_inputs(w, units=units), e2ttt.FLAG_NO_RESIDUAL_LN)
     for i, u in enumerate(units):
         sub = {n: None if r is None else r[:, i:i + 1] for n, r in ref.items()}
-        assert_tol(errors(g, sub, [u]), "bf16", "bwd swiglu B8 H16 bare unit %d" % u)
+        assert_tol(errors(g, sub, [u], C=w.C), "bf16", "bwd swiglu B8 H16 bare unit %d" % u)
 
 
 def test_backward_swiglu_literal_net_workload():
     w = WL.WORKLOADS[2]
     x = WL.make_inputs(w)
     g = gpu_fwd_bwd(w, x, flags=e2ttt.FLAG_NO_RESIDUAL_LN)
-    assert_tol(errors(g, oracle_bwd(w, x, flags=e2ttt.FLAG_NO_RESIDUAL_LN)), "bf16",
+    assert_tol(errors(g, oracle_bwd(w, x, flags=e2ttt.FLAG_NO_RESIDUAL_LN), C=w.C), "bf16",
                "bwd %s (bare net)" % w.name)
 
 
@@ -186,13 +194,13 @@ def test_backward_swiglu_ln_chunk_windows(starts):
         wu = w.with_(T=w.C)
         g = gpu_fwd_bwd(wu, y)
         ref = oracle_bwd(wu, y)
-        errs = errors(g, ref)
+        errs = errors(g, ref, C=w.C)
         yb = dict(y)
         yb["w_in"] = WL.round_bf16(y["w_in"])
         yb["m_in"] = None if y["m_in"] is None else WL.round_bf16(y["m_in"])
         refb = oracle_bwd(wu, yb)
-        sens = {n: rel_l2(refb[n], ref[n]) for n in errs}
-        bound = {n: max(TOL["bf16"], 2 * sens[n]) for n in errs}
+        sens = {n: rel_l2(refb[n], ref[n]) for n in GRADS if ref.get(n) is not None}
+        bound = {n: max(TOL["bf16"], 2 * sens[n.split("/")[0]]) for n in errs}
         strict += all(v <= TOL["bf16"] / 4 for v in sens.values())
         print("bwd %s chunk %d gpu %s sens %s" % (w.name, r,
               {k: "%.1e" % v for k, v in errs.items()}, {k: "%.1e" % v for k, v in sens.items()}),

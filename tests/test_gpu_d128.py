@@ -11,7 +11,7 @@ import torch
 
 from oracle import oracle
 from paper_2608_21308_amd import e2ttt, workloads as WL
-from tests.gpu_util import TOL, config_of, rel_l2, to_dev
+from tests.gpu_util import TOL, config_of, parity_errors, tile_of, to_dev
 from tests.test_gpu_backward import GRADS, errors as berrors, gpu_fwd_bwd, oracle_bwd, \
     with_state_inputs
 
@@ -45,8 +45,8 @@ def fwd_errors(got, x, w, units=None, flags=0):
     if units is not None:
         pick = lambda a: a.reshape((-1,) + a.shape[2:])[units][None]
         out, wo, mo = pick(out), pick(wo), pick(mo)
-    return {"out": rel_l2(out, ro), "w_out": rel_l2(wo - x["w_in"], rw - x["w_in"]),
-            "m_out": rel_l2(mo, rm)}
+    return parity_errors({"out": (out, ro), "w_out": (wo - x["w_in"], rw - x["w_in"], "state"),
+                          "m_out": (mo, rm, "state")}, tile_of(w.C))
 
 
 @pytest.mark.parametrize("T,C,dh", [(200, 32, 64), (300, 64, 128), (260, 100, 256),
@@ -67,7 +67,7 @@ def test_forward_d128(T, C, dh):
 def test_backward_d128(T, C, dh):
     w = d128(T=T, C=C, dh=dh, backward=True, seed=2200 + T + dh)
     x = with_state_inputs(WL.make_inputs(w), T, m_scale=1e-2)
-    errs = berrors(gpu_fwd_bwd(w, x), oracle_bwd(w, x))
+    errs = berrors(gpu_fwd_bwd(w, x), oracle_bwd(w, x), C=C)
     print("d128 bwd T=%d C=%d dh=%d" % (T, C, dh), {k: "%.2e" % v for k, v in errs.items()},
           flush=True)
     assert all(e <= TOL["bf16"] for e in errs.values()), errs
@@ -87,7 +87,7 @@ def test_d128_more_units_than_resident_groups():
                        None, ws, t["d_out"])
     torch.cuda.synchronize()
     errs = fwd_errors((out, wo, mo), x, w)
-    errs.update(berrors(g, oracle_bwd(w, x)))
+    errs.update(berrors(g, oracle_bwd(w, x), C=w.C))
     print("d128 40 units", {k: "%.2e" % v for k, v in errs.items()}, flush=True)
     assert all(e <= TOL["bf16"] for e in errs.values()), errs
 
@@ -101,7 +101,7 @@ def test_paper_1p3b_layer_sampled_units():
     units = [0, 29]
     xs = WL.make_inputs(w, units=units)
     ref = oracle_bwd(w, xs)
-    errs = berrors(g, ref, units)
+    errs = berrors(g, ref, units, C=w.C)
     print("paper 1.3B d128 C512 bwd", {k: "%.2e" % v for k, v in errs.items()}, flush=True)
     assert all(e <= TOL["bf16"] for e in errs.values()), errs
     for n in GRADS:
@@ -131,7 +131,7 @@ def test_forward_d128_swiglu(T, C, dh, flags):
 def test_backward_d128_swiglu(T, C, dh, flags):
     w = d128(fw=WL.FW_SWIGLU, T=T, C=C, dh=dh, backward=True, seed=2500 + T + dh)
     x = with_state_inputs(WL.make_inputs(w), T, m_scale=1e-2)
-    errs = berrors(gpu_fwd_bwd(w, x, flags), oracle_bwd(w, x, flags))
+    errs = berrors(gpu_fwd_bwd(w, x, flags), oracle_bwd(w, x, flags), C=C)
     print("d128 swiglu bwd T=%d C=%d dh=%d flags=%d" % (T, C, dh, flags),
           {k: "%.2e" % v for k, v in errs.items()}, flush=True)
     assert all(e <= TOL["bf16"] for e in errs.values()), errs

@@ -18,7 +18,7 @@ import torch
 
 from oracle import oracle
 from paper_2608_21308_amd import e2ttt, workloads as WL
-from tests.gpu_util import TOL, config_of, rel_l2, to_dev
+from tests.gpu_util import TOL, config_of, parity_errors, rel_l2, tile_of, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -128,8 +128,8 @@ def test_streaming_decode_matches_the_sequence_forward(case, C):
     out, wo, mo = stream(w, x)
     r_out, r_w, r_m = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"],
                                      x["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
-    errs = dict(out=rel_l2(out, r_out), w=rel_l2(wo - x["w_in"], r_w - x["w_in"]),
-                m=rel_l2(mo, r_m))
+    errs = parity_errors({"out": (out, r_out), "w": (wo - x["w_in"], r_w - x["w_in"], "state"),
+                          "m": (mo, r_m, "state")}, tile_of(w.C))
     print("decode %s C=%d" % (case, C), {k: "%.2e" % v for k, v in errs.items()}, flush=True)
     for k, e in errs.items():
         assert e <= TOL[w.io], k

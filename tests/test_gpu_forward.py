@@ -1,7 +1,9 @@
 """GPU parity of the forward path (e2ttt_chunk_forward, e2ttt_chunk_coeffs)
 against the fp64 oracle on identical seeded inputs.
 
-Tolerances: rel-L2 1e-5 for fp32 io, 2e-2 for bf16 io (per output tensor).
+Tolerances: rel-L2 1e-5 for fp32 io, 2e-2 for bf16 io (per output tensor),
+and every block (a unit's tile of up to 64 tokens, or a unit's state) within
+twice that (gpu_util.parity_errors).
 The SwiGLU + residual-LayerNorm workloads are chaotic under the synthetic
 gates: a 1e-7 perturbation of the initial weights grows to O(1) within about
 eight chunks even in fp64 (test_swiglu_ln_trajectory_is_chaotic pins this on
@@ -15,7 +17,8 @@ import torch
 
 from oracle import oracle
 from paper_2608_21308_amd import e2ttt, workloads as WL
-from tests.gpu_util import (TOL, config_of, fp32_sensitivity, gpu_forward, rel_l2, slice_tokens,
+from tests import fp32ref
+from tests.gpu_util import (TOL, config_of, gpu_forward, parity_errors, rel_l2, slice_tokens, tile_of,
                             to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -37,11 +40,11 @@ def run_both(w, x, flags=0, m_in=None, check_state=True):
     torch.cuda.synchronize()
     ro, rw, rm = oracle.forward(x["q"], x["k"], x["v"], x["eta"], x["beta"], x["gamma"],
                                 x["w_in"], m_in, C=w.C, fw=w.fw, dh=w.dh, flags=flags)
-    errs = {"out": rel_l2(out, ro)}
+    pairs = {"out": (out, ro)}
     if check_state:
-        errs["w_out"] = rel_l2(wo, rw)
-        errs["m_out"] = rel_l2(mo, rm)
-    return errs, (out, wo, mo), (ro, rw, rm)
+        pairs["w_out"] = (wo, rw, "state")
+        pairs["m_out"] = (mo, rm, "state")
+    return parity_errors(pairs, tile_of(w.C)), (out, wo, mo), (ro, rw, rm)
 
 
 def assert_tol(errs, io, what=""):
@@ -102,29 +105,22 @@ def test_forward_tiny_fp32_config():
                                           (12, 7, 50, 0), (3, 1, 64, 0), (32, 16, 128, 0),
                                           (50, 32, 100, 0), (128, 16, 64, 1), (75, 7, 50, 1)])
 def test_forward_fp32_shapes(fw, T, C, dh, flags):
-    # one or two chunks (plus ragged tails) per run: over long trajectories the
-    # residual-LN dynamics amplify fp32 rounding itself past 1e-5 (a float32
-    # numpy implementation of the same closed form drifts by 4e-6 .. 1e-4 on
-    # 11 chunks of these shapes), so long-run fp32 parity is pinned on the
-    # tiny workload above and on the bare net (flags = 1) here.
-    # The bound is 1e-5, widened only for cases whose own fp32 conditioning is
-    # worse: the oracle's output change under one-ulp perturbations of its inputs,
-    # times 10 (the kernel rounds at every chunk, the probe only once).
+    # The bar is 1e-5, widened only where a plain float32 evaluation of the
+    # same closed form (tests/fp32ref.py, correctly rounded PyTorch operations
+    # on the CPU) is itself farther than 1e-5 / FP32_FACTOR from the oracle.
     w = WL.WORKLOADS[0].with_(fw=fw, B=2, H=2, T=T, C=C, dh=dh, seed=500 + T + C + dh)
     x = WL.make_inputs(w, with_grads=False)
     m_in = np.random.default_rng(T).standard_normal(x["w_in"].shape).astype(np.float32) * 1e-3
-    errs, _, _ = run_both(w, x, flags=flags, m_in=m_in)
-
-    def fn(y):
-        o, wo, mo = oracle.forward(y["q"], y["k"], y["v"], y["eta"], y["beta"], y["gamma"],
-                                   y["w_in"], m_in, C=C, fw=fw, dh=dh, flags=flags)
-        return {"out": o, "w_out": wo, "m_out": mo}
-
-    sens = fp32_sensitivity(fn, x)
-    what = "fp32 fw=%d T=%d C=%d dh=%d flags=%d (sens %s)" % (
-        fw, T, C, dh, flags, {k: "%.1e" % v for k, v in sens.items()})
-    bound = {n: max(TOL["f32"], 10 * sens[n]) for n in errs}
-    print(what, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    errs, _, ref = run_both(w, x, flags=flags, m_in=m_in)
+    x32 = dict(x, m_in=m_in)
+    o32, w32, m32 = fp32ref.forward(x32, C=C, fw=fw, dh=dh, flags=flags)
+    e32 = parity_errors({"out": (o32, ref[0]), "w_out": (w32, ref[1], "state"),
+                         "m_out": (m32, ref[2], "state")}, tile_of(C))
+    bound = fp32ref.fp32_bar(e32)
+    what = "fp32 fw=%d T=%d C=%d dh=%d flags=%d" % (fw, T, C, dh, flags)
+    print(what, "gpu", {k: "%.2e" % v for k, v in errs.items()},
+          "fp32 reference", {k: "%.1e" % v for k, v in e32.items()},
+          "above 1e-5:", sorted(n for n in errs if errs[n] > TOL["f32"]), flush=True)
     bad = {n: (errs[n], bound[n]) for n in errs if not errs[n] <= bound[n]}
     assert not bad, what + ": %s" % bad
 
@@ -160,9 +156,9 @@ def test_forward_1p3b_layer_sampled_units():
     xs = WL.make_inputs(w, with_grads=False, units=units)
     ro, rw, rm = oracle.forward(xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"], xs["gamma"],
                                 xs["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
-    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units]
-    errs = {"out": rel_l2(flat(out), ro[0]), "w_out": rel_l2(flat(wo), rw[0]),
-            "m_out": rel_l2(flat(mo), rm[0])}
+    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units][None]
+    errs = parity_errors({"out": (flat(out), ro), "w_out": (flat(wo), rw, "state"),
+                          "m_out": (flat(mo), rm, "state")}, tile_of(w.C))
     assert_tol(errs, "bf16", w.name)
     assert torch.isfinite(out.float()).all()
 
@@ -181,9 +177,9 @@ def test_forward_swiglu_more_units_than_resident_groups(dh):
     xs = WL.make_inputs(w, with_grads=False, units=units)
     ro, rw, rm = oracle.forward(xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"], xs["gamma"],
                                 xs["w_in"], None, C=w.C, fw=w.fw, dh=w.dh)
-    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units]
-    errs = {"out": rel_l2(flat(out), ro[0]), "w_out": rel_l2(flat(wo), rw[0]),
-            "m_out": rel_l2(flat(mo), rm[0])}
+    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units][None]
+    errs = parity_errors({"out": (flat(out), ro), "w_out": (flat(wo), rw, "state"),
+                          "m_out": (flat(mo), rm, "state")}, tile_of(w.C))
     assert_tol(errs, "bf16", "swiglu B8 H16 dh=%d" % dh)
     assert torch.isfinite(out.float()).all()
 
@@ -195,21 +191,45 @@ def test_swiglu_literal_net_end_to_end():
     assert_tol(errs, "bf16", w.name + " (bare net)")
 
 
-def test_swiglu_prefill_literal_net_sampled_units():
+@pytest.mark.parametrize("decay", [True, False])
+def test_swiglu_prefill_literal_net_sampled_units(decay):
+    # The 512-chunk prefill with the bare net: outputs and the state carried
+    # over all 512 chunks of four units (first, last, two middle) against the
+    # oracle's token recurrence over all 32,768 tokens.  With the workload's
+    # decay gate the bare net's state fades: after 32,768 tokens the oracle's
+    # W is ~1e-35 of w_in and its M ~1e-75, below the float32 range, so the
+    # momentum is checked only to be below float32's smallest normal number
+    # (0 or subnormal) there; the same draws with the decay gate off
+    # (gamma = 1) keep the state O(1) and check W - w_in, W and M after 512
+    # chunks at the bar.
     w = WL.WORKLOADS[4]
     x = WL.make_inputs(w)
+    if not decay:
+        x["gamma"] = None
     cfg = config_of(w, flags=e2ttt.FLAG_NO_RESIDUAL_LN)
     t = to_dev(x, "bf16")
     out, wo, mo, _ = gpu_forward(cfg, t)
     torch.cuda.synchronize()
-    units = [3, 12]
+    units = [0, 6, 11, 15]
     xs = WL.make_inputs(w, units=units)
+    if not decay:
+        xs["gamma"] = None
     ro, rw, rm = oracle.forward(xs["q"], xs["k"], xs["v"], xs["eta"], xs["beta"], xs["gamma"],
                                 xs["w_in"], None, C=w.C, fw=w.fw, dh=w.dh,
                                 flags=e2ttt.FLAG_NO_RESIDUAL_LN)
-    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units]
-    errs = {"out": rel_l2(flat(out), ro[0])}
-    assert_tol(errs, "bf16", w.name + " (bare net)")
+    flat = lambda a: a.reshape((w.B * w.H,) + a.shape[2:])[units][None]
+    gw, gm = flat(wo).cpu().numpy(), flat(mo).cpu().numpy()
+    pairs = {"out": (flat(out), ro), "w_out": (gw, rw, "state")}
+    tiny = float(np.finfo(np.float32).tiny)
+    if decay:
+        assert np.abs(rm).max() < tiny and np.abs(gm).max() < tiny, (np.abs(rm).max(),
+                                                                     np.abs(gm).max())
+    else:
+        pairs["w_out-w_in"] = (gw - xs["w_in"], rw - xs["w_in"], "state")
+        pairs["m_out"] = (gm, rm, "state")
+    errs = parity_errors(pairs, tile_of(w.C))
+    assert_tol(errs, "bf16", w.name + " (bare net, %s, units %s)" % (
+        "decay gate" if decay else "gamma = 1", units))
     assert torch.isfinite(out.float()).all()
 
 
@@ -248,7 +268,7 @@ def test_swiglu_ln_chunk_windows(cfg_idx, units, starts):
         pb = oracle.forward(yb["q"], yb["k"], yb["v"], yb["eta"], yb["beta"], yb["gamma"],
                             yb["w_in"], mb, C=w.C, fw=w.fw, dh=w.dh)
         sens = {n: rel_l2(a, b) for n, a, b in zip(("out", "w_out", "m_out"), pb, ref)}
-        bound = {n: max(TOL["bf16"], 2 * sens[n]) for n in errs}
+        bound = {n: max(TOL["bf16"], 2 * sens[n.split("/")[0]]) for n in errs}
         strict += all(v <= TOL["bf16"] / 4 for v in sens.values())
         print("%s chunk %d gpu %s  bf16-state sensitivity %s" % (
             w.name, r, {k: "%.2e" % v for k, v in errs.items()},
