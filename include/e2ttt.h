@@ -15,7 +15,10 @@
  * and the state (W, M) is carried from chunk to chunk.  The fast-weight net f
  * is the GELU MLP f(x) = x + LN(W2 GELU(W1 x)) or the SwiGLU net
  * f(x) = x + LN(Wd (SiLU(Wg x) * (Wu x))) of Sec. 4 (LayerNorm without affine,
- * biased variance, eps = ln_eps; GELU uses the exact erf form).
+ * biased variance, eps = ln_eps).  GELU is x Phi(x) with the normal CDF; the
+ * chunk kernels evaluate Phi through the rational erfc of Abramowitz & Stegun
+ * eq. 7.1.26 (absolute error at most 1.5e-7, so a relative error of Phi that
+ * grows for x << 0 where Phi itself is tiny), e2ttt_apply through erff.
  *
  * Conventions shared by every entry point:
  *   - Every tensor pointer is a DEVICE pointer (hipMalloc'd or equivalent) on
@@ -77,11 +80,12 @@ typedef enum {
   E2TTT_ERR_HIP = 5,                   /* a HIP launch failed                     */
   E2TTT_ERR_DEVICE = 6                 /* a bounded device-side wait expired      */
 } e2ttt_status;
-/* E2TTT_ERR_DEVICE is reported only when the environment variable
- * E2TTT_DEBUG_SYNC=1 makes every call wait for its kernels: a wait between the
- * two workgroups of a unit expired (after 2 s), the grid was drained and the
- * results of that call are undefined.  Without E2TTT_DEBUG_SYNC the word that
- * records it sits in the workspace / scratch and no error is returned. */
+/* E2TTT_ERR_DEVICE: a bounded wait between the workgroups of a unit expired
+ * (after 2 s, or the limit set by E2TTT_WAIT_LIMIT_US), the grid was drained
+ * and the results of that call are undefined.  The kernels record it in a
+ * status word of the workspace (forward) or scratch (backward) buffer;
+ * e2ttt_wait_status reads it.  With the environment variable
+ * E2TTT_DEBUG_SYNC=1 every call also waits for its kernels and returns it. */
 
 typedef enum { E2TTT_FW_GELU_MLP = 0, E2TTT_FW_SWIGLU = 1 } e2ttt_fw;
 
@@ -191,14 +195,15 @@ e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const 
  * streaming decode: while a chunk fills, each arriving token is answered from
  * the current chunk-start state with this call (T = 1), and once C tokens have
  * arrived e2ttt_chunk_forward over those C tokens (w_in, m_in = the current
- * state) gives the next chunk-start state.  Outputs and states then equal
- * those of one e2ttt_chunk_forward over the whole sequence.
+ * state) gives the next chunk-start state.  Outputs and states then agree
+ * with those of one e2ttt_chunk_forward over the whole sequence within the
+ * bf16 / fp32 tolerances (the two evaluate GELU's Phi differently, above).
  *   desc   as for the chunk calls (same supported set); desc.T is the number
  *          of tokens per unit to evaluate; desc.chunk is checked but unused
  *   q      [B][H][T][d] io
  *   w      [B][H][P]   f32, 16-byte aligned (else E2TTT_ERR_BAD_SHAPE)
  *   out    [B][H][T][d] io; may not overlap q or w
- * fp32 arithmetic on the fp32 state (exact-erf GELU); no workspace.
+ * fp32 arithmetic on the fp32 state (GELU through erff); no workspace.
  */
 e2ttt_status e2ttt_apply(const e2ttt_desc* desc, const void* q, const float* w, void* out,
                          void* stream);
@@ -239,6 +244,21 @@ e2ttt_status e2ttt_gates_backward(const e2ttt_gate_params* params, int64_t n,
                                   const float* d_eta, const float* d_beta, const float* d_gamma,
                                   float* d_l_eta, float* d_l_beta, float* d_l_alpha,
                                   void* stream);
+
+/*
+ * Status of the bounded waits between the workgroups of a unit in the last
+ * e2ttt_chunk_forward that used `workspace` and the last e2ttt_chunk_backward
+ * that used `scratch` (either may be NULL, not both).  Waits for `stream`
+ * first (the calls must have been enqueued there or be complete), then reads
+ * the status words: E2TTT_ERR_DEVICE when a wait of either call expired (its
+ * results are undefined), E2TTT_OK otherwise (always for descriptors that run
+ * one workgroup per unit).  Each call clears its buffer's word when it starts.
+ * The wait limit is 2 s; the environment variable E2TTT_WAIT_LIMIT_US (a
+ * decimal count of microseconds, read at every call) sets another, which lets
+ * a test make waits give up without any kernel failing.
+ */
+e2ttt_status e2ttt_wait_status(const e2ttt_desc* desc, const void* workspace,
+                               const void* scratch, void* stream);
 
 /* Static description of a status code. */
 const char* e2ttt_status_str(e2ttt_status status);

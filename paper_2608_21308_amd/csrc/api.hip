@@ -155,6 +155,18 @@ int averaged(const e2ttt_desc* d) { return (d->flags & E2TTT_FLAG_CHUNK_AVERAGED
 
 e2ttt_status hip_status(hipError_t e) { return e == hipSuccess ? E2TTT_OK : E2TTT_ERR_HIP; }
 
+// Bound of every wait between the workgroups of a unit, in ticks of the
+// 100 MHz real-time counter: 2 s, or E2TTT_WAIT_LIMIT_US microseconds when
+// that variable holds a decimal count (read at every call).
+long long wait_ticks() {
+  const char* s = std::getenv("E2TTT_WAIT_LIMIT_US");
+  if (!s || !*s) return kTimeoutTicks;
+  char* end = nullptr;
+  const long long us = std::strtoll(s, &end, 10);
+  if (*end != '\0' || us < 0) return kTimeoutTicks;
+  return std::min(us, 600000000LL) * 100;
+}
+
 bool debug_sync() {
   static const bool on = [] {
     const char* s = std::getenv("E2TTT_DEBUG_SYNC");
@@ -337,6 +349,7 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   a.w0blk = pl.off_ckpt > pl.off_w0 ? at<float>(workspace, pl.off_w0) : nullptr;
   a.sync = sync;
   a.npairs = np;
+  a.wait_ticks = wait_ticks();
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
   a.eps = desc->ln_eps;
@@ -387,6 +400,7 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   a.xbuf = at<float>(scratch, pl.off_bxbuf);
   a.sync = sync;
   a.npairs = np;
+  a.wait_ticks = wait_ticks();
   a.d_out = d_out; a.d_w_out = d_w_out; a.d_m_out = d_m_out;
   a.dq = dq; a.dk = dk; a.dv = dv;
   a.d_w_in = d_w_in; a.d_m_in = d_m_in;
@@ -403,6 +417,25 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
                   (int)pl.T, desc->chunk, (int)pl.NC, pl.U * pl.NC, pl.cfg.ns,
                   pl.U * pl.T, pl.U * pl.NC * 3, averaged(desc)};
   return finish(launch_coeff_bwd(cb, s), s, sync);
+}
+
+e2ttt_status e2ttt_wait_status(const e2ttt_desc* desc, const void* workspace,
+                               const void* scratch, void* stream) {
+  Plan pl;
+  e2ttt_status st = make_plan(desc, pl);
+  if (st != E2TTT_OK) return st;
+  if (!workspace && !scratch) return E2TTT_ERR_NULL_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (hipStreamSynchronize(s) != hipSuccess) return E2TTT_ERR_HIP;
+  if (pl.cfg.ns == 1) return E2TTT_OK;   // one workgroup per unit: no waits
+  unsigned word[2] = {0u, 0u};
+  if (workspace && hipMemcpy(&word[0], at<unsigned>(workspace, pl.off_sync), sizeof(unsigned),
+                             hipMemcpyDeviceToHost) != hipSuccess)
+    return E2TTT_ERR_HIP;
+  if (scratch && hipMemcpy(&word[1], at<unsigned>(scratch, pl.off_bsync), sizeof(unsigned),
+                           hipMemcpyDeviceToHost) != hipSuccess)
+    return E2TTT_ERR_HIP;
+  return (word[0] != 0u || word[1] != 0u) ? E2TTT_ERR_DEVICE : E2TTT_OK;
 }
 
 }  // extern "C"

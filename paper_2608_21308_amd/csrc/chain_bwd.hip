@@ -397,7 +397,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   f32x4* const frz = LONG ? reinterpret_cast<f32x4*>(E2TTT_ARG(bfrz)) + (long)blockIdx.x * 2 * NB : nullptr;
 
   PairX<S::NS> px;
-  px.init(a.sync, a.npairs, sword);
+  px.init(a.sync, a.npairs, sword, a.wait_ticks);
   const int rank = px.rank;
   const int j0 = rank * S::DHP;
   const long NP = (S::NS > 1) ? a.npairs : (long)gridDim.x;
@@ -424,7 +424,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     if (tid < S::CM) {
       pkw = (tid < ln) ? E2TTT_ARG(kw)[r0 + tid] : 0.0f;
       pkm = (tid < ln) ? E2TTT_ARG(km)[r0 + tid] : 0.0f;
-      prk = (tid < ln) ? E2TTT_ARG(rk)[r0 + tid] : 0.0f;
+      prk = (tid < ln) ? ld_stream(E2TTT_ARG(rk) + r0 + tid) : 0.0f;
     }
     if (tid < 3) pcar = E2TTT_ARG(carry)[(uu * NC + rc) * 3 + tid];
   };
@@ -436,7 +436,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
     pQ.load(E2TTT_ARG(q), r0, ln, tid);
     pD.load(E2TTT_ARG(d_out), r0, ln, tid);
     pZq.load(E2TTT_ARG(zq), r0, ln, tid);
-    if (tid < S::CM) prq = (tid < ln) ? E2TTT_ARG(rq)[r0 + tid] : 0.0f;
+    if (tid < S::CM) prq = (tid < ln) ? ld_stream(E2TTT_ARG(rq) + r0 + tid) : 0.0f;
   };
 
   for (long u = px.p; u < a.U; u += NP) {
@@ -994,8 +994,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int jj = 0; jj < NJB; ++jj) {
               const int qi = SavedAct<S>::idx(tb, jj, w, lane);
-              Aqq[tb][jj] = sv.aq()[qi];
-              D1q[0][tb][jj] = DerivQ<S::BF>::unpack(sv.d1q()[qi]);
+              Aqq[tb][jj] = ld_stream(sv.aq() + qi);
+              D1q[0][tb][jj] = DerivQ<S::BF>::unpack(ld_stream(sv.d1q() + qi));
             }
         }
         pQ.store(xq, tid);

@@ -155,7 +155,7 @@ __device__ __forceinline__ void store_ckpt(const StateTiles<S>& st, void* dst, i
     for (int jj = 0; jj < S::NJB; ++jj)
 #pragma unroll
       for (int ib = 0; ib < S::NIB; ++ib)
-        lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64] = S::O::cvt(st.t[m][jj][ib]);
+        st_stream(lp + ((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64, S::O::cvt(st.t[m][jj][ib]));
 }
 
 // Quads of matrix m of a checkpoint block, for this lane.
@@ -167,7 +167,8 @@ __device__ __forceinline__ void load_ckpt_mat(typename S::O::Q (&q)[S::NJB][S::N
 #pragma unroll
   for (int jj = 0; jj < S::NJB; ++jj)
 #pragma unroll
-    for (int ib = 0; ib < S::NIB; ++ib) q[jj][ib] = lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64];
+    for (int ib = 0; ib < S::NIB; ++ib)
+      q[jj][ib] = ld_stream(lp + ((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64);
 }
 
 template <class Q>
@@ -278,7 +279,7 @@ __device__ __forceinline__ void store_ckpt_q(const typename S::O::Q (&q)[S::NMAT
     for (int jj = 0; jj < S::NJB; ++jj)
 #pragma unroll
       for (int ib = 0; ib < S::NIB; ++ib)
-        lp[((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64] = q[m][jj][ib];
+        st_stream(lp + ((m * S::NJB + jj) * S::NIB + ib) * S::NW * 64, q[m][jj][ib]);
 }
 
 // EPL consecutive fp32 values from global memory (one vector load when EPL = 4).
@@ -459,7 +460,7 @@ struct TileRegs {
     for (int k = 0; k < PER; ++k) {
       const int e = (tid + k * S::NT) * VE;
       v[k] = make_uint4(0u, 0u, 0u, 0u);
-      if (e < S::CM * S::D && e / S::D < len) v[k] = p[tid + k * S::NT];
+      if (e < S::CM * S::D && e / S::D < len) v[k] = ld_stream16(p + tid + k * S::NT);
     }
   }
   __device__ __forceinline__ void store(typename S::E* dst, int tid) const {
@@ -480,12 +481,11 @@ struct F32TileRegs {
   float4 v[PER];
 
   __device__ __forceinline__ void load(const float* src, long row0, int len, int tid) {
-    const float4* p = reinterpret_cast<const float4*>(src + row0 * S::D);
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int e = (tid + k * S::NT) * 4;
       v[k] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      if (e < S::CM * S::D && e / S::D < len) v[k] = p[tid + k * S::NT];
+      if (e < S::CM * S::D && e / S::D < len) v[k] = ld_stream16f(src + row0 * S::D + 4 * (tid + k * S::NT));
     }
   }
   __device__ __forceinline__ void store(float* dst, int tid) const {

@@ -115,7 +115,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   const float inv_d = 1.0f / D;
 
   PairX<S::NS> px;
-  px.init(a.sync, a.npairs, sm.word);
+  px.init(a.sync, a.npairs, sm.word, a.wait_ticks);
   const int rank = px.rank;
   const int j0 = rank * S::DHP;
   const long NP = (S::NS > 1) ? a.npairs : (long)gridDim.x;
@@ -394,8 +394,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
           for (int jj = 0; jj < NJB; ++jj) {
             const int qi = SavedAct<S>::idx(tb, jj, w, lane);
-            sv.aq()[qi] = qsa[tb][jj];
-            sv.d1q()[qi] = DerivQ<S::BF>::pack(qsd[tb][jj]);
+            st_stream(sv.aq() + qi, qsa[tb][jj]);
+            st_stream(sv.d1q() + qi, DerivQ<S::BF>::pack(qsd[tb][jj]));
           }
       }
 
@@ -489,9 +489,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
               } else {
 #pragma unroll
                 for (int q = 0; q < EPL; ++q)
-                  E2TTT_ARG(zk)[(row0 + t) * D + l16 * EPL + q] = zsave[it_][q];
+                  st_stream(E2TTT_ARG(zk) + (row0 + t) * D + l16 * EPL + q, zsave[it_][q]);
               }
-              if (l16 == 0) E2TTT_ARG(rk)[row0 + t] = rsave[it_];
+              if (l16 == 0) st_stream(E2TTT_ARG(rk) + row0 + t, rsave[it_]);
             }
           }
         }
@@ -683,7 +683,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             store_row_io<IO, EPL>(outp + (long)t * D + l16 * EPL, f);
             if (E2TTT_ARG(zq)) {
               store_row_io<IoT<false>, EPL>(E2TTT_ARG(zq) + (row0 + t) * D + l16 * EPL, yv);
-              if (l16 == 0) E2TTT_ARG(rq)[row0 + t] = sig;
+              if (l16 == 0) st_stream(E2TTT_ARG(rq) + row0 + t, sig);
             }
           }
                   }

@@ -232,23 +232,51 @@ __device__ __forceinline__ float wave_sum(float v) {
           __int_as_float(__builtin_amdgcn_readlane(b, 48)));
 }
 
+// --------------------------------------------------------- streaming access
+// Global loads and stores of data a launch touches once (token rows, outputs,
+// chunk-start checkpoints, saved activations and LayerNorm rows) are marked
+// non-temporal: the L2 evicts those lines first, so that they do not push out
+// the exchange slots through which the workgroups of a unit swap partial sums
+// every chunk (those stay L2-resident and never need to reach HBM).
+typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
+template <class T>
+__device__ __forceinline__ void st_stream(T* p, const T& v) {
+  __builtin_nontemporal_store(v, p);
+}
+template <class T>
+__device__ __forceinline__ T ld_stream(const T* p) {
+  return __builtin_nontemporal_load(p);
+}
+__device__ __forceinline__ uint4 ld_stream16(const void* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float4 ld_stream16f(const float* p) {
+  const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
 // ----------------------------------------------------------- io element load
 template <bool BF> struct IoT;
+// (stores are streaming: outputs and gradients are written once per launch)
 template <> struct IoT<true> {
   using T = __bf16;
   static __device__ __forceinline__ float ld(const T* p) { return (float)*p; }
-  static __device__ __forceinline__ void st(T* p, float x) { *p = (__bf16)x; }
+  static __device__ __forceinline__ void st(T* p, float x) { st_stream(p, (__bf16)x); }
   // four consecutive values, one 8-byte store (p 8-byte aligned)
   static __device__ __forceinline__ void st4(T* p, f32x4 x) {
-    *reinterpret_cast<bf16x4*>(p) = bf16x4{(__bf16)x[0], (__bf16)x[1], (__bf16)x[2], (__bf16)x[3]};
+    st_stream(reinterpret_cast<bf16x4*>(p),
+              bf16x4{(__bf16)x[0], (__bf16)x[1], (__bf16)x[2], (__bf16)x[3]});
   }
 };
 template <> struct IoT<false> {
   using T = float;
   static __device__ __forceinline__ float ld(const T* p) { return *p; }
-  static __device__ __forceinline__ void st(T* p, float x) { *p = x; }
+  static __device__ __forceinline__ void st(T* p, float x) { st_stream(p, x); }
   // four consecutive values, one 16-byte store (p 16-byte aligned)
-  static __device__ __forceinline__ void st4(T* p, f32x4 x) { *reinterpret_cast<f32x4*>(p) = x; }
+  static __device__ __forceinline__ void st4(T* p, f32x4 x) {
+    st_stream(reinterpret_cast<f32x4*>(p), x);
+  }
 };
 
 }  // namespace e2ttt

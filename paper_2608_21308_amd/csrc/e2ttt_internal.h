@@ -94,6 +94,7 @@ struct ChainArgs {
   float* xbuf;
   unsigned* sync;
   long npairs;
+  long long wait_ticks;  // limit of every bounded wait between ranks (100 MHz counter ticks)
   int T, C, NC, dh;
   long P;               // parameters per unit (unpadded)
   int resln;            // 1: f = x + LN(y); 0: f = y

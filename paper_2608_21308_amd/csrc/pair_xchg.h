@@ -19,7 +19,8 @@
 // every post and wait of that group uses agent-scope release / acquire fences
 // instead, which are coherent across XCDs but write back and invalidate the L2.
 //
-// Every wait is bounded (kTimeoutTicks of the 100 MHz real-time counter).  A
+// Every wait is bounded (by default kTimeoutTicks of the 100 MHz real-time
+// counter; the host passes the limit with the launch).  A
 // rank whose wait expires sets the status word, poisons its own flag so that
 // the others stop waiting too, and skips all later waits, so the grid always
 // drains; the results of that launch are then undefined and the status word
@@ -89,7 +90,7 @@ template <int NS> struct PairX;
 template <> struct PairX<1> {
   int rank = 0;
   long p = 0;
-  __device__ void init(unsigned*, long, int*) { p = blockIdx.x; }
+  __device__ void init(unsigned*, long, int*, long long) { p = blockIdx.x; }
   __device__ void post() {}
   __device__ void wait_for(unsigned, int*) {}
   __device__ unsigned seq_now() const { return 0; }
@@ -105,10 +106,13 @@ template <int NS> struct PairX {
   unsigned seq = 0;
   bool same_xcc = true;
   bool dead = false;
+  long long limit = kTimeoutTicks;
 
-  // s_word: two ints of LDS for broadcasting thread 0's findings
-  __device__ void init(unsigned* sync, long ngroups, int* s_word) {
+  // s_word: two ints of LDS for broadcasting thread 0's findings; limit: the
+  // bound of every wait, in ticks of the 100 MHz real-time counter
+  __device__ void init(unsigned* sync, long ngroups, int* s_word, long long limit_ticks) {
     group_of_block<NS>(blockIdx.x, p, rank);
+    limit = limit_ticks;
     status = sync;
     mine = sync + kSyncLine * (1 + NS * p + rank);
 #pragma unroll
@@ -125,7 +129,7 @@ template <int NS> struct PairX {
         const unsigned* xp = sync + kSyncLine * (1 + NS * ngroups + NS * p + other_rank(k, rank));
         unsigned o = 0;
         while ((o = ld_dev(xp)) == 0u) {
-          if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) break;
+          if (__builtin_amdgcn_s_memrealtime() - t0 > limit) break;
         }
         if (o != id) same = 0;
         if (o == 0u) alive = 0;
@@ -166,7 +170,7 @@ template <int NS> struct PairX {
         if (ok) {
           unsigned f;
           while ((f = ld_dev(peer[k])) < target) {
-            if (__builtin_amdgcn_s_memrealtime() - t0 > kTimeoutTicks) { ok = 0; break; }
+            if (__builtin_amdgcn_s_memrealtime() - t0 > limit) { ok = 0; break; }
           }
           if (f == kPoison) ok = 0;
         }

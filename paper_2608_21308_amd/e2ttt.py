@@ -29,7 +29,8 @@ STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
 # Every entry point the header declares (checked by the CPU test-suite).
 EXPORTS = ("e2ttt_param_count", "e2ttt_workspace_bytes", "e2ttt_backward_scratch_bytes",
            "e2ttt_chunk_forward", "e2ttt_chunk_backward", "e2ttt_chunk_coeffs",
-           "e2ttt_apply", "e2ttt_gates_forward", "e2ttt_gates_backward", "e2ttt_status_str")
+           "e2ttt_apply", "e2ttt_gates_forward", "e2ttt_gates_backward", "e2ttt_wait_status",
+           "e2ttt_status_str")
 
 
 class E2TTTError(RuntimeError):
@@ -87,6 +88,8 @@ def load():
     lib.e2ttt_gates_forward.restype = i
     lib.e2ttt_gates_backward.argtypes = [gp, ctypes.c_int64] + [vp] * 10
     lib.e2ttt_gates_backward.restype = i
+    lib.e2ttt_wait_status.argtypes = [dp, vp, vp, vp]
+    lib.e2ttt_wait_status.restype = i
     lib.e2ttt_status_str.argtypes = [i]
     lib.e2ttt_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -252,6 +255,18 @@ def apply(cfg: Config, q, w, out=None):
     st = lib.e2ttt_apply(ctypes.byref(d), _ptr(q), _ptr(w), _ptr(out), _stream())
     _check(st, "e2ttt_apply")
     return out
+
+
+def wait_status(cfg: Config, workspace=None, scratch=None) -> int:
+    """e2ttt_wait_status: waits for the current stream, then returns the status
+    code of the bounded waits of the last forward that used `workspace` and the
+    last backward that used `scratch` (0, or 6 when a wait expired)."""
+    if workspace is None and scratch is None:
+        raise ValueError("give a workspace, a scratch buffer or both")
+    _check_tensors(cfg, workspace=workspace, scratch=scratch)
+    d = cfg.desc()
+    return int(load().e2ttt_wait_status(ctypes.byref(d), _ptr(workspace), _ptr(scratch),
+                                        _stream()))
 
 
 def chunk_coeffs(cfg: Config, eta, beta, gamma):
