@@ -260,6 +260,26 @@ e2ttt_status e2ttt_gates_backward(const e2ttt_gate_params* params, int64_t n,
 e2ttt_status e2ttt_wait_status(const e2ttt_desc* desc, const void* workspace,
                                const void* scratch, void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * e2ttt_chunk_forward with save_for_backward = 0 on a workspace the library
+ * owns, a device array of E2TTT_STATIC_WORKSPACE_BYTES on each GPU it runs
+ * on, held until the process ends.  Inputs, outputs and their rules are those
+ * of e2ttt_chunk_forward.  A descriptor whose workspace
+ * (e2ttt_workspace_bytes(desc, 0)) exceeds E2TTT_STATIC_WORKSPACE_BYTES
+ * returns E2TTT_ERR_WORKSPACE_TOO_SMALL before anything is launched.  The call
+ * allocates nothing.  Every call on a GPU shares that GPU's array: calls that
+ * overlap on one GPU race (enqueue them on one stream, or wait between them).
+ * e2ttt_wait_status cannot read its status word (the array is the library's);
+ * E2TTT_DEBUG_SYNC=1 reports an expired wait from the call itself.
+ */
+#define E2TTT_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+e2ttt_status e2ttt_chunk_forward_static(const e2ttt_desc* desc, const void* q, const void* k,
+                                        const void* v, const float* eta, const float* beta,
+                                        const float* gamma, const float* w_in, const float* m_in,
+                                        void* out, float* w_out, float* m_out, void* stream);
+
 /* Static description of a status code. */
 const char* e2ttt_status_str(e2ttt_status status);
 

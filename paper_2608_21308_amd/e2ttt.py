@@ -30,7 +30,7 @@ STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
 EXPORTS = ("e2ttt_param_count", "e2ttt_workspace_bytes", "e2ttt_backward_scratch_bytes",
            "e2ttt_chunk_forward", "e2ttt_chunk_backward", "e2ttt_chunk_coeffs",
            "e2ttt_apply", "e2ttt_gates_forward", "e2ttt_gates_backward", "e2ttt_wait_status",
-           "e2ttt_status_str")
+           "e2ttt_chunk_forward_static", "e2ttt_status_str")
 
 
 class E2TTTError(RuntimeError):
@@ -90,6 +90,8 @@ def load():
     lib.e2ttt_gates_backward.restype = i
     lib.e2ttt_wait_status.argtypes = [dp, vp, vp, vp]
     lib.e2ttt_wait_status.restype = i
+    lib.e2ttt_chunk_forward_static.argtypes = [dp] + [vp] * 12
+    lib.e2ttt_chunk_forward_static.restype = i
     lib.e2ttt_status_str.argtypes = [i]
     lib.e2ttt_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -214,6 +216,26 @@ def forward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in=None, *, out=None
                                  workspace.numel(), int(bool(save_for_backward)), _stream())
     _check(st, "e2ttt_chunk_forward")
     return out, w_out, m_out, workspace
+
+
+# Bytes of the library-owned workspace of e2ttt_chunk_forward_static.
+STATIC_WORKSPACE_BYTES = 64 << 20
+
+
+def forward_static(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, out, w_out, m_out):
+    """Runs e2ttt_chunk_forward_static (no save for the backward) on the current
+    stream into the caller's out, w_out, m_out; allocates nothing."""
+    for name, t in (("out", out), ("w_out", w_out), ("m_out", m_out)):
+        if t is None:
+            raise ValueError("%s must be given: this entry point allocates nothing" % name)
+    _check_tensors(cfg, q=q, k=k, v=v, eta=eta, beta=beta, gamma=gamma, w_in=w_in, m_in=m_in,
+                   out=out, w_out=w_out, m_out=m_out)
+    d = cfg.desc()
+    st = load().e2ttt_chunk_forward_static(ctypes.byref(d), _ptr(q), _ptr(k), _ptr(v), _ptr(eta),
+                                           _ptr(beta), _ptr(gamma), _ptr(w_in), _ptr(m_in),
+                                           _ptr(out), _ptr(w_out), _ptr(m_out), _stream())
+    _check(st, "e2ttt_chunk_forward_static")
+    return out, w_out, m_out
 
 
 def backward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, workspace, d_out, d_w_out=None,
