@@ -289,7 +289,7 @@ e2ttt_status e2ttt_apply(const e2ttt_desc* desc, const void* q, const float* w, 
   if (st != E2TTT_OK) return st;
   if (!q || !w || !out) return E2TTT_ERR_NULL_ARG;
   if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return E2TTT_ERR_BAD_SHAPE;
-  if (desc->dh > kApplyMaxDh || desc->d > 64) return E2TTT_ERR_UNSUPPORTED;
+  if (desc->dh > (desc->d == 128 ? 512 : kApplyMaxDh)) return E2TTT_ERR_UNSUPPORTED;
   if (pl.U * ((pl.T + 7) / 8) > INT_MAX) return E2TTT_ERR_UNSUPPORTED;
   ApplyArgs a{};
   a.q = q; a.w = w; a.out = out;

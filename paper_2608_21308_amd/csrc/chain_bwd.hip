@@ -783,7 +783,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       float pdyh[S::NS > 1 && PEER_EARLY ? P7IT : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
         E2TTT_LANE_IDS;
-        float* mine = bwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par);
+        float* mine = bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par);
 #pragma unroll 1
         for (int v = tid; v < S::CM * D / 4; v += S::NT)
           reinterpret_cast<float4*>(mine)[v] = reinterpret_cast<const float4*>(dyh)[v];
@@ -793,7 +793,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         // below (which would otherwise order each step's loads after them)
 #pragma unroll
         for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
-          const float* dyh_peer = bwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par);
+          const float* dyh_peer = bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, other_rank(k, rank), par);
 #pragma unroll
           for (int it_ = 0; it_ < P7IT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * NW;
@@ -802,7 +802,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           }
         }
         if (pend_s0 >= 0)
-          flush_dkdq<S>(px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
+          flush_dkdq<S>(px.xs, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       }
 
       // ------------------------------------- P7: LayerNorm second order
@@ -836,7 +836,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_part<EPL>(pr, bwd_slot<S>(E2TTT_ARG(xbuf), px.p, r, par) + t * D +
+              load_row_part<EPL>(pr, bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
                                          l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) dyhv[q] = (r == 0) ? pr[q] : dyhv[q] + pr[q];
@@ -964,7 +964,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         }
         const float ksign = (resln && rank == 0) ? -1.0f : 0.0f;
         if constexpr (S::NS > 1) {
-          jacc_store_f32<S>(dkacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) + S::CM * D,
+          jacc_store_f32<S>(dkacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) + S::CM * D,
                             [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
         } else {
           jacc_store_io<S>(dkacc, E2TTT_ARG(dk), row0, len,
@@ -1130,7 +1130,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         }
         const float qsign = (resln && rank == 0) ? 1.0f : 0.0f;
         if constexpr (S::NS > 1) {
-          jacc_store_f32<S>(dqacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) + 2 * S::CM * D,
+          jacc_store_f32<S>(dqacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) + 2 * S::CM * D,
                             [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); },
                             w, g, c);
         } else {
@@ -1197,7 +1197,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       E2TTT_LANE_IDS;
       px.wait_for(px.seq_now(), sword);             // the peers' last post
       if (pend_s0 >= 0)
-        flush_dkdq<S>(px.p, pend_par, u * T + pend_s0, pend_len, rlo, tid);
+        flush_dkdq<S>(px.xs, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       __syncthreads();
     }
     {

@@ -303,7 +303,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c,   // Y_K (partial)
-                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) : nullptr);
+                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) : nullptr);
       }
       px.post();                                          // seq0 + 1: Y_K
       // without a separate Q-side buffer, alds is rewritten below
@@ -366,7 +366,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
 #pragma unroll
         for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
-          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par);
+          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, other_rank(k, rank), par);
 #pragma unroll
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * S::NW;
@@ -380,7 +380,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         jgemm_to_lds<S>(aq, sm.w2, sm.yq, w, g, c,        // Y_Q (partial)
-                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.p, rank, par) + S::CM * D : nullptr);
+                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) + S::CM * D : nullptr);
       }
       px.post();                                          // seq0 + 2: Y_Q
       // the saved query side goes out after the post, so that the post's wait
@@ -433,7 +433,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.p, r, par) + t * D +
+              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
                                          l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
@@ -506,7 +506,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
 #pragma unroll
         for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
-          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.p, other_rank(k, rank), par) + S::CM * D;
+          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, other_rank(k, rank), par) + S::CM * D;
 #pragma unroll
           for (int it_ = 0; it_ < NITO; ++it_) {
             const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
@@ -656,7 +656,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.p, r, par) + S::CM * D + t * D +
+              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par) + S::CM * D + t * D +
                                          l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];

@@ -65,6 +65,16 @@ __device__ __forceinline__ void group_of_block(int b, long& p, int& rank) {
   p = (long)(b / (8 * NS)) * 8 + (b & 7);
 }
 
+// Exchange-slot index of group p among ngroups (a multiple of 8): the groups
+// that share an XCD (p mod 8) get consecutive slot blocks, so that each XCD's
+// slots form one contiguous range spread over all sets of its L2.  Indexed by
+// p itself, the blocks of one XCD's groups would lie 8 blocks (a power-of-two
+// multiple of the set span) apart, all on the same L2 sets, and evict each
+// other between a post and the peer's read.
+__device__ __forceinline__ long slots_of_group(long p, long ngroups) {
+  return (p & 7) * (ngroups >> 3) + (p >> 3);
+}
+
 // The k-th rank other than `rank`, in increasing order (k < NS - 1).
 __device__ __forceinline__ int other_rank(int k, int rank) { return k < rank ? k : k + 1; }
 
@@ -90,6 +100,7 @@ template <int NS> struct PairX;
 template <> struct PairX<1> {
   int rank = 0;
   long p = 0;
+  long xs = 0;
   __device__ void init(unsigned*, long, int*, long long) { p = blockIdx.x; }
   __device__ void post() {}
   __device__ void wait_for(unsigned, int*) {}
@@ -100,6 +111,7 @@ template <int NS> struct PairX {
   static_assert(NS >= 2 && NS <= 8, "two to eight workgroups per unit");
   int rank = 0;
   long p = 0;
+  long xs = 0;   // the group's exchange-slot index (slots_of_group)
   unsigned* mine = nullptr;
   const unsigned* peer[NS - 1] = {};
   unsigned* status = nullptr;
@@ -112,6 +124,7 @@ template <int NS> struct PairX {
   // bound of every wait, in ticks of the 100 MHz real-time counter
   __device__ void init(unsigned* sync, long ngroups, int* s_word, long long limit_ticks) {
     group_of_block<NS>(blockIdx.x, p, rank);
+    xs = slots_of_group(p, ngroups);
     limit = limit_ticks;
     status = sync;
     mine = sync + kSyncLine * (1 + NS * p + rank);

@@ -137,9 +137,17 @@ def test_backward_d128_swiglu(T, C, dh, flags):
     assert all(e <= TOL["bf16"] for e in errs.values()), errs
 
 
-def test_apply_refuses_d128():
-    w = d128(T=1)
+def test_apply_d128_decode_step_all_units():
+    """One decode step of the paper's 1.3B layer (Table 13: batch 8, 16 heads of
+    128, MLP hidden 512): e2ttt_apply at a moved state for all 128 units, every
+    unit against the oracle's net (one bf16 rounding plus the fp32 evaluation)."""
+    from tests.test_gpu_decode import bf16_ulp, perturbed_state
+    w = d128(B=8, H=16, T=1)
     x = WL.make_inputs(w, with_grads=False)
-    t = to_dev(x, "bf16")
-    with pytest.raises(e2ttt.E2TTTError, match="unsupported"):
-        e2ttt.apply(config_of(w), t["q"], t["w_in"])
+    W = perturbed_state(x, 11)
+    t = to_dev(dict(q=x["q"], w=W), "bf16")
+    got = e2ttt.apply(config_of(w), t["q"], t["w"]).float().cpu().numpy()
+    ref = np.stack([np.stack([oracle.net(W[b, h], x["q"][b, h], fw=w.fw, dh=w.dh)
+                              for h in range(w.H)]) for b in range(w.B)])
+    bound = bf16_ulp(ref) + 1e-6 * (np.abs(x["q"]) + np.abs(ref) + 1.0)
+    assert np.all(np.abs(got - ref) <= bound), float(np.max(np.abs(got - ref) / bound))

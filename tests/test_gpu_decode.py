@@ -34,6 +34,12 @@ CASES = {
     "swiglu_f32_d16": WL.WORKLOADS[0].with_(fw=e2ttt.FW_SWIGLU, dh=48, B=2, H=3, T=16, C=16),
     "mlp_bf16_d64": WL.WORKLOADS[1].with_(B=2, H=3, T=16, C=16),
     "swiglu_bf16_d64": WL.WORKLOADS[2].with_(B=2, H=3, T=16, C=16),
+    # head dim 128 (the paper's 1.3B model, Table 13's decode setting): MLP
+    # hidden 512, SwiGLU hidden 344 (8/3 of 128, rounded to a multiple of 8)
+    # and a hidden width that is not a multiple of four
+    "mlp_bf16_d128": WL.PAPER_1P3B.with_(B=2, H=3, T=16, C=16),
+    "swiglu_bf16_d128": WL.PAPER_1P3B.with_(fw=e2ttt.FW_SWIGLU, dh=344, B=2, H=3, T=16, C=16),
+    "mlp_bf16_d128_dh202": WL.PAPER_1P3B.with_(dh=202, B=1, H=2, T=16, C=16),
 }
 
 
@@ -78,7 +84,8 @@ def test_apply_matches_the_net(case, T):
     check_apply(CASES[case], T, seed=T)
 
 
-@pytest.mark.parametrize("case", ["mlp_f32_d16", "mlp_bf16_d64"])
+@pytest.mark.parametrize("case", ["mlp_f32_d16", "mlp_bf16_d64", "mlp_bf16_d128",
+                                  "swiglu_bf16_d128"])
 def test_apply_bare_net(case):
     check_apply(CASES[case], 5, flags=e2ttt.FLAG_NO_RESIDUAL_LN, seed=3)
 
@@ -118,7 +125,8 @@ def stream(w, x, dev="cuda"):
 
 
 @pytest.mark.parametrize("case,C", [(c, 16) for c in sorted(CASES)] +
-                         [("mlp_f32_d16", 128), ("mlp_bf16_d64", 128)])
+                         [("mlp_f32_d16", 128), ("mlp_bf16_d64", 128), ("mlp_bf16_d128", 64),
+                          ("swiglu_bf16_d128", 64)])
 def test_streaming_decode_matches_the_sequence_forward(case, C):
     """Decode one token at a time over 3 full chunks and a ragged one; outputs
     and final state equal the oracle's forward over the whole sequence (also
