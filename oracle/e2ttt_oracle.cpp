@@ -9,8 +9,10 @@
 // What it computes (arxiv 2608.21308):
 //   * Fast-weight net f_W (Sec. 4, "Fast-weight Network"): GELU MLP
 //     f(x) = x + LN(W2 GELU(W1 x)) or SwiGLU f(x) = x + LN(Wd (SiLU(Wg x) * (Wu x))),
-//     LayerNorm without affine, biased variance, explicit eps, exact erf GELU.
+//     LayerNorm with biased variance, explicit eps, exact erf GELU.
 //     Flag bit 0 drops "x + LN(.)" so that f(x) is the bare matrix net.
+//     Optionally a learnable per-head LayerNorm affine (flag bit 2):
+//     f(x) = x + a * LN(y) + b with a, b in R^d, slow weights of the head.
 //   * Inner loss L_t = 1/2 ||f_W(k_t) - v_t||^2 (Sec. 2, eq. (1); the paper
 //     names MSE without a constant, see the readings list in the design notes).
 //   * Per-token recurrence with gradients frozen at the chunk-start weights
@@ -81,16 +83,23 @@ template <class T> T silu_grad(T x) { T s = sigmoid(x); return s * (1.0 + x * (1
 
 struct Net {
   int d, dh, fw;     // fw: 0 = GELU MLP, 1 = SwiGLU
-  bool resln;        // true: f(x) = x + LN(y); false: f(x) = y
+  bool resln;        // true: f(x) = x + a * LN(y) + b; false: f(x) = y
   double eps;
+  const double* lna = nullptr;   // LayerNorm affine a[d] of the unit's head (nullptr: a = 1)
+  const double* lnb = nullptr;   // and b[d] (nullptr: b = 0)
   long P() const { return (fw == 0 ? 2L : 3L) * d * dh; }
+  double a(int i) const { return lna ? lna[i] : 1.0; }
+  double b(int i) const { return lnb ? lnb[i] : 0.0; }
 };
 
 // f_W(x) and, when fbar != nullptr, its vector-Jacobian product:
-//   Wbar += (df/dW)^T fbar,  xbar = (df/dx)^T fbar.
+//   Wbar += (df/dW)^T fbar,  xbar = (df/dx)^T fbar,
+//   and, when given, lnabar += (df/da)^T fbar, lnbbar += (df/db)^T fbar for
+//   the LayerNorm affine.
 // Every intermediate is recomputed here; the code is the definition written out.
 template <class T>
-void net_eval(const Net& n, const T* W, const T* x, T* f, const T* fbar, T* Wbar, T* xbar) {
+void net_eval(const Net& n, const T* W, const T* x, T* f, const T* fbar, T* Wbar, T* xbar,
+              T* lnabar = nullptr, T* lnbbar = nullptr) {
   const int d = n.d, dh = n.dh;
   std::vector<T> h(dh), hu(dh), a(dh), y(d), z(d);
   const T* W1 = W;                       // MLP W1 / SwiGLU Wg   [dh][d]
@@ -123,7 +132,10 @@ void net_eval(const Net& n, const T* W, const T* x, T* f, const T* fbar, T* Wbar
     for (int i = 0; i < d; ++i) var += (y[i] - mu) * (y[i] - mu);
     var = var * (1.0 / d);
     sigma = sqrt_(var + n.eps);
-    for (int i = 0; i < d; ++i) { z[i] = (y[i] - mu) / sigma; f[i] = x[i] + z[i]; }
+    for (int i = 0; i < d; ++i) {
+      z[i] = (y[i] - mu) / sigma;
+      f[i] = x[i] + n.a(i) * z[i] + n.b(i);
+    }
   } else {
     for (int i = 0; i < d; ++i) f[i] = y[i];
   }
@@ -133,15 +145,22 @@ void net_eval(const Net& n, const T* W, const T* x, T* f, const T* fbar, T* Wbar
   std::vector<T> ybar(d), abar(dh), hbar(dh), hubar(dh);
   for (int i = 0; i < d; ++i) xbar[i] = 0.0;
   if (n.resln) {
-    // f = x + z  ->  xbar = fbar, zbar = fbar;
+    // f = x + a z + b  ->  xbar = fbar, zbar = a fbar, abar += fbar z, bbar += fbar;
     // z = (y - mean y)/sigma  ->  ybar = (zbar - mean zbar - z mean(zbar z)) / sigma.
+    std::vector<T> zbar(d);
     T m1 = 0.0, m2 = 0.0;
-    for (int i = 0; i < d; ++i) { m1 += fbar[i]; m2 += fbar[i] * z[i]; }
+    for (int i = 0; i < d; ++i) {
+      zbar[i] = n.a(i) * fbar[i];
+      m1 += zbar[i];
+      m2 += zbar[i] * z[i];
+      if (lnabar) lnabar[i] += fbar[i] * z[i];
+      if (lnbbar) lnbbar[i] += fbar[i];
+    }
     m1 = m1 * (1.0 / d);
     m2 = m2 * (1.0 / d);
     for (int i = 0; i < d; ++i) {
       xbar[i] = fbar[i];
-      ybar[i] = (fbar[i] - m1 - z[i] * m2) / sigma;
+      ybar[i] = (zbar[i] - m1 - z[i] * m2) / sigma;
     }
   } else {
     for (int i = 0; i < d; ++i) ybar[i] = fbar[i];
@@ -175,16 +194,19 @@ void net_eval(const Net& n, const T* W, const T* x, T* f, const T* fbar, T* Wbar
   }
 }
 
-// Gradients of the inner loss L = 1/2 ||f_W(k) - v||^2 with respect to W, k, v.
+// Gradients of the inner loss L = 1/2 ||f_W(k) - v||^2 with respect to W, k, v
+// and, when ga / gb are given, the LayerNorm affine a, b.
 template <class T>
-void loss_grad(const Net& n, const T* W, const T* k, const T* v, T* gW, T* gk, T* gv) {
+void loss_grad(const Net& n, const T* W, const T* k, const T* v, T* gW, T* gk, T* gv,
+               T* ga = nullptr, T* gb = nullptr) {
   const int d = n.d;
   std::vector<T> f(d), r(d);
   net_eval<T>(n, W, k, f.data(), nullptr, nullptr, nullptr);
   for (int i = 0; i < d; ++i) { r[i] = f[i] - v[i]; gv[i] = -r[i]; }
   const long P = n.P();
   for (long p = 0; p < P; ++p) gW[p] = 0.0;
-  net_eval<T>(n, W, k, f.data(), r.data(), gW, gk);
+  if (ga) for (int i = 0; i < d; ++i) { ga[i] = 0.0; gb[i] = 0.0; }
+  net_eval<T>(n, W, k, f.data(), r.data(), gW, gk, ga, gb);
 }
 
 struct Problem {
@@ -234,7 +256,7 @@ void unit_backward(const Problem& pb, const double* q, const double* k, const do
                    const double* w_in, const double* m_in, const double* d_out,
                    const double* d_w_out, const double* d_m_out, double* dq, double* dk,
                    double* dv, double* d_eta, double* d_beta, double* d_gamma,
-                   double* d_w_in, double* d_m_in) {
+                   double* d_w_in, double* d_m_in, double* d_lna, double* d_lnb) {
   const Net& n = pb.net;
   const int d = n.d, T = pb.T, C = pb.C;
   const long P = n.P();
@@ -250,7 +272,7 @@ void unit_backward(const Problem& pb, const double* q, const double* k, const do
 
   std::vector<double> Ws, Ms, Gs;        // token states W_t, M_t (t = 0..len) and G_t
   std::vector<double> gk(d), gv(d), fb(d), xb(d);
-  std::vector<Dual> Wd(P), gWd(P), kd(d), vd(d), gkd(d), gvd(d);
+  std::vector<Dual> Wd(P), gWd(P), kd(d), vd(d), gkd(d), gvd(d), gad(d), gbd(d);
   std::vector<double> Gbar;
   for (int c = NC - 1; c >= 0; --c) {
     const int s0 = c * C;
@@ -308,12 +330,15 @@ void unit_backward(const Problem& pb, const double* q, const double* k, const do
       const double* Gb = Gbar.data() + (size_t)i * P;
       for (long p = 0; p < P; ++p) Wd[p] = Dual(W0[p], Gb[p]);
       for (int j = 0; j < d; ++j) { kd[j] = Dual(k[(long)t * d + j]); vd[j] = Dual(v[(long)t * d + j]); }
-      loss_grad<Dual>(n, Wd.data(), kd.data(), vd.data(), gWd.data(), gkd.data(), gvd.data());
-      // G = -grad_W L, so d<Gbar, G>/dW0 = -(tangent of grad_W L), likewise for k, v.
+      loss_grad<Dual>(n, Wd.data(), kd.data(), vd.data(), gWd.data(), gkd.data(), gvd.data(),
+                      gad.data(), gbd.data());
+      // G = -grad_W L, so d<Gbar, G>/dW0 = -(tangent of grad_W L), likewise for k, v
+      // and the affine a, b.
       for (long p = 0; p < P; ++p) Wbar[p] -= gWd[p].d;
       for (int j = 0; j < d; ++j) {
         dk[(long)t * d + j] = -gkd[j].d;
         dv[(long)t * d + j] = -gvd[j].d;
+        if (d_lna) { d_lna[j] -= gad[j].d; d_lnb[j] -= gbd[j].d; }
       }
     }
     // o_t = f_{W_0}(q_t)
@@ -321,7 +346,7 @@ void unit_backward(const Problem& pb, const double* q, const double* k, const do
     for (int i = 0; i < len; ++i) {
       const int t = s0 + i;
       net_eval<double>(n, W0, q + (long)t * d, fb.data(), d_out + (long)t * d, Wob.data(),
-                       dq + (long)t * d);
+                       dq + (long)t * d, d_lna, d_lnb);
     }
     for (long p = 0; p < P; ++p) Wbar[p] += Wob[p];
   }
@@ -339,6 +364,16 @@ bool make_problem(Problem& pb, int B, int H, int T, int d, int dh, int C, int fw
   return true;
 }
 
+// The problem of unit u: the affine of its head h = u mod H (ln_a, ln_b are
+// [H][d]; either may be NULL: a = 1, b = 0).
+Problem unit_problem(const Problem& pb, long u, const double* ln_a, const double* ln_b) {
+  Problem q = pb;
+  const long h = u % pb.H;
+  q.net.lna = ln_a ? ln_a + h * pb.net.d : nullptr;
+  q.net.lnb = ln_b ? ln_b + h * pb.net.d : nullptr;
+  return q;
+}
+
 }  // namespace
 
 extern "C" {
@@ -351,21 +386,24 @@ long e2ttt_oracle_param_count(int d, int dh, int fw) {
 }
 
 // Forward over all B*H units.  Returns 0, or -1 on a bad argument.
+// ln_a, ln_b: the LayerNorm affine per head, [H][d], each NULL for a = 1 / b = 0.
 int e2ttt_oracle_forward(int B, int H, int T, int d, int dh, int C, int fw, int flags, double eps,
                          const double* q, const double* k, const double* v, const double* eta,
                          const double* beta, const double* gamma, const double* w_in,
-                         const double* m_in, double* out, double* w_out, double* m_out,
-                         int nthreads) {
+                         const double* m_in, const double* ln_a, const double* ln_b, double* out,
+                         double* w_out, double* m_out, int nthreads) {
   Problem pb;
   if (!make_problem(pb, B, H, T, d, dh, C, fw, flags, eps)) return -1;
   if (!q || !k || !v || !eta || !beta || !w_in || !out || !w_out || !m_out) return -1;
+  if ((ln_a || ln_b) && !pb.net.resln) return -1;   // the affine belongs to the LayerNorm
   const long P = pb.net.P();
   const long U = pb.units();
   if (nthreads < 1) nthreads = 1;
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
   for (long u = 0; u < U; ++u) {
     const long tok = u * T;
-    unit_forward(pb, q + tok * d, k + tok * d, v + tok * d, eta + tok, beta + tok,
+    unit_forward(unit_problem(pb, u, ln_a, ln_b), q + tok * d, k + tok * d, v + tok * d,
+                 eta + tok, beta + tok,
                  gamma ? gamma + tok : nullptr, w_in + u * P, m_in ? m_in + u * P : nullptr,
                  out + tok * d, w_out + u * P, m_out + u * P, nullptr);
   }
@@ -373,32 +411,49 @@ int e2ttt_oracle_forward(int B, int H, int T, int d, int dh, int C, int fw, int 
 }
 
 // Backward over all B*H units (see unit_backward for the loss).  d_w_out,
-// d_m_out and m_in may be NULL (zero); d_gamma must be NULL iff gamma is NULL.
+// d_m_out and m_in may be NULL (zero); d_gamma must be NULL iff gamma is NULL;
+// d_ln_a, d_ln_b ([H][d], summed over the batch) must be given iff ln_a and
+// ln_b are (both or neither).
 int e2ttt_oracle_backward(int B, int H, int T, int d, int dh, int C, int fw, int flags, double eps,
                           const double* q, const double* k, const double* v, const double* eta,
                           const double* beta, const double* gamma, const double* w_in,
-                          const double* m_in, const double* d_out, const double* d_w_out,
-                          const double* d_m_out, double* dq, double* dk, double* dv,
-                          double* d_eta, double* d_beta, double* d_gamma, double* d_w_in,
-                          double* d_m_in, int nthreads) {
+                          const double* m_in, const double* ln_a, const double* ln_b,
+                          const double* d_out, const double* d_w_out, const double* d_m_out,
+                          double* dq, double* dk, double* dv, double* d_eta, double* d_beta,
+                          double* d_gamma, double* d_w_in, double* d_m_in, double* d_ln_a,
+                          double* d_ln_b, int nthreads) {
   Problem pb;
   if (!make_problem(pb, B, H, T, d, dh, C, fw, flags, eps)) return -1;
   if (!q || !k || !v || !eta || !beta || !w_in || !d_out || !dq || !dk || !dv || !d_eta ||
       !d_beta || !d_w_in || !d_m_in)
     return -1;
   if ((gamma == nullptr) != (d_gamma == nullptr)) return -1;
+  const bool aff = ln_a || ln_b;
+  if (aff && (!ln_a || !ln_b || !d_ln_a || !d_ln_b || !pb.net.resln)) return -1;
   const long P = pb.net.P();
   const long U = pb.units();
+  // the affine gradients of every unit, summed over the batch afterwards in order
+  std::vector<double> ga(aff ? U * d : 0, 0.0), gb(aff ? U * d : 0, 0.0);
   if (nthreads < 1) nthreads = 1;
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
   for (long u = 0; u < U; ++u) {
     const long tok = u * T;
-    unit_backward(pb, q + tok * d, k + tok * d, v + tok * d, eta + tok, beta + tok,
+    unit_backward(unit_problem(pb, u, ln_a, ln_b), q + tok * d, k + tok * d, v + tok * d,
+                  eta + tok, beta + tok,
                   gamma ? gamma + tok : nullptr, w_in + u * P, m_in ? m_in + u * P : nullptr,
                   d_out + tok * d, d_w_out ? d_w_out + u * P : nullptr,
                   d_m_out ? d_m_out + u * P : nullptr, dq + tok * d, dk + tok * d, dv + tok * d,
                   d_eta + tok, d_beta + tok, d_gamma ? d_gamma + tok : nullptr, d_w_in + u * P,
-                  d_m_in + u * P);
+                  d_m_in + u * P, aff ? ga.data() + u * d : nullptr,
+                  aff ? gb.data() + u * d : nullptr);
+  }
+  if (aff) {
+    for (long i = 0; i < (long)H * d; ++i) { d_ln_a[i] = 0.0; d_ln_b[i] = 0.0; }
+    for (long u = 0; u < U; ++u)
+      for (int i = 0; i < d; ++i) {
+        d_ln_a[(u % H) * d + i] += ga[u * d + i];
+        d_ln_b[(u % H) * d + i] += gb[u * d + i];
+      }
   }
   return 0;
 }
@@ -434,10 +489,12 @@ int e2ttt_oracle_chunk_coeffs(int C, const double* eta, const double* beta, cons
 
 // f_W(x) for one unit and a batch of n rows x[n][d] (used by the tests to pin
 // special cases such as "eta = 0 leaves every output at f_{W_in}(q_t)").
-int e2ttt_oracle_net(int d, int dh, int fw, int flags, double eps, const double* W, int n,
-                     const double* x, double* f) {
+// ln_a, ln_b: the LayerNorm affine a[d], b[d] (NULL: a = 1, b = 0).
+int e2ttt_oracle_net(int d, int dh, int fw, int flags, double eps, const double* W,
+                     const double* ln_a, const double* ln_b, int n, const double* x, double* f) {
   Net net;
   net.d = d; net.dh = dh; net.fw = fw; net.resln = (flags & 1) == 0; net.eps = eps;
+  net.lna = ln_a; net.lnb = ln_b;
   if (d < 1 || dh < 1 || (fw != 0 && fw != 1) || n < 0 || !W || !x || !f) return -1;
   for (int r = 0; r < n; ++r)
     net_eval<double>(net, W, x + (long)r * d, f + (long)r * d, nullptr, nullptr, nullptr);
@@ -446,10 +503,12 @@ int e2ttt_oracle_net(int d, int dh, int fw, int flags, double eps, const double*
 
 // Negative inner-loss gradients G = -grad_W L at W for rows (k, v), one per row
 // (G is [n][P]); used by the tests to pin the closed form of Prop. 1.
-int e2ttt_oracle_neg_grad(int d, int dh, int fw, int flags, double eps, const double* W, int n,
-                          const double* k, const double* v, double* G) {
+int e2ttt_oracle_neg_grad(int d, int dh, int fw, int flags, double eps, const double* W,
+                          const double* ln_a, const double* ln_b, int n, const double* k,
+                          const double* v, double* G) {
   Net net;
   net.d = d; net.dh = dh; net.fw = fw; net.resln = (flags & 1) == 0; net.eps = eps;
+  net.lna = ln_a; net.lnb = ln_b;
   if (d < 1 || dh < 1 || (fw != 0 && fw != 1) || n < 0 || !W || !k || !v || !G) return -1;
   const long P = net.P();
   std::vector<double> gk(d), gv(d);

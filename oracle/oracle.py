@@ -50,15 +50,15 @@ def _load():
         dp = ctypes.c_void_p
         i = ctypes.c_int
         d = ctypes.c_double
-        lib.e2ttt_oracle_forward.argtypes = [i, i, i, i, i, i, i, i, d] + [dp] * 11 + [i]
+        lib.e2ttt_oracle_forward.argtypes = [i, i, i, i, i, i, i, i, d] + [dp] * 13 + [i]
         lib.e2ttt_oracle_forward.restype = i
-        lib.e2ttt_oracle_backward.argtypes = [i, i, i, i, i, i, i, i, d] + [dp] * 19 + [i]
+        lib.e2ttt_oracle_backward.argtypes = [i, i, i, i, i, i, i, i, d] + [dp] * 23 + [i]
         lib.e2ttt_oracle_backward.restype = i
         lib.e2ttt_oracle_chunk_coeffs.argtypes = [i] + [dp] * 6
         lib.e2ttt_oracle_chunk_coeffs.restype = i
-        lib.e2ttt_oracle_net.argtypes = [i, i, i, i, d, dp, i, dp, dp]
+        lib.e2ttt_oracle_net.argtypes = [i, i, i, i, d, dp, dp, dp, i, dp, dp]
         lib.e2ttt_oracle_net.restype = i
-        lib.e2ttt_oracle_neg_grad.argtypes = [i, i, i, i, d, dp, i, dp, dp, dp]
+        lib.e2ttt_oracle_neg_grad.argtypes = [i, i, i, i, d, dp, dp, dp, i, dp, dp, dp]
         lib.e2ttt_oracle_neg_grad.restype = i
         lib.e2ttt_oracle_param_count.argtypes = [i, i, i]
         lib.e2ttt_oracle_param_count.restype = ctypes.c_long
@@ -84,9 +84,13 @@ def default_threads() -> int:
     return max(1, min(os.cpu_count() or 1, int(os.environ.get("E2TTT_ORACLE_THREADS", "64"))))
 
 
-def forward(q, k, v, eta, beta, gamma, w_in, m_in, *, C, fw, dh, flags=0, eps=1e-5, nthreads=None):
-    """Returns (out [B,H,T,d], w_out [B,H,P], m_out [B,H,P]) in float64."""
+def forward(q, k, v, eta, beta, gamma, w_in, m_in, *, C, fw, dh, flags=0, eps=1e-5, nthreads=None,
+            ln_a=None, ln_b=None):
+    """Returns (out [B,H,T,d], w_out [B,H,P], m_out [B,H,P]) in float64.
+
+    ln_a, ln_b: the learnable LayerNorm affine per head, [H, d] (None: a = 1, b = 0)."""
     q, k, v, eta, beta, gamma, w_in, m_in = map(_f64, (q, k, v, eta, beta, gamma, w_in, m_in))
+    ln_a, ln_b = _f64(ln_a), _f64(ln_b)
     B, H, T, d = q.shape
     P = param_count(d, dh, fw)
     assert w_in.shape == (B, H, P), (w_in.shape, (B, H, P))
@@ -94,22 +98,25 @@ def forward(q, k, v, eta, beta, gamma, w_in, m_in, *, C, fw, dh, flags=0, eps=1e
     w_out = np.zeros((B, H, P))
     m_out = np.zeros((B, H, P))
     rc = _load().e2ttt_oracle_forward(B, H, T, d, dh, C, fw, flags, eps, _p(q), _p(k), _p(v),
-                                      _p(eta), _p(beta), _p(gamma), _p(w_in), _p(m_in), _p(out),
-                                      _p(w_out), _p(m_out), nthreads or default_threads())
+                                      _p(eta), _p(beta), _p(gamma), _p(w_in), _p(m_in), _p(ln_a),
+                                      _p(ln_b), _p(out), _p(w_out), _p(m_out),
+                                      nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle forward rejected its arguments")
     return out, w_out, m_out
 
 
 def backward(q, k, v, eta, beta, gamma, w_in, m_in, d_out, d_w_out=None, d_m_out=None, *, C, fw,
-             dh, flags=0, eps=1e-5, nthreads=None):
+             dh, flags=0, eps=1e-5, nthreads=None, ln_a=None, ln_b=None):
     """Gradients of sum<d_out,out> + <d_w_out,w_out> + <d_m_out,m_out>.
 
     Returns a dict with dq, dk, dv, d_eta, d_beta, d_gamma (None if gamma is
-    None), d_w_in, d_m_in, all float64.
+    None), d_w_in, d_m_in, and with the LayerNorm affine (ln_a and ln_b [H, d],
+    both or neither) d_ln_a, d_ln_b [H, d] summed over the batch, all float64.
     """
     q, k, v, eta, beta, gamma, w_in, m_in, d_out, d_w_out, d_m_out = map(
         _f64, (q, k, v, eta, beta, gamma, w_in, m_in, d_out, d_w_out, d_m_out))
+    ln_a, ln_b = _f64(ln_a), _f64(ln_b)
     B, H, T, d = q.shape
     P = param_count(d, dh, fw)
     res = {n: np.zeros((B, H, T, d)) for n in ("dq", "dk", "dv")}
@@ -118,11 +125,16 @@ def backward(q, k, v, eta, beta, gamma, w_in, m_in, d_out, d_w_out=None, d_m_out
     res["d_gamma"] = None if gamma is None else np.zeros((B, H, T))
     res["d_w_in"] = np.zeros((B, H, P))
     res["d_m_in"] = np.zeros((B, H, P))
+    aff = ln_a is not None or ln_b is not None
+    if aff:
+        res["d_ln_a"] = np.zeros((H, d))
+        res["d_ln_b"] = np.zeros((H, d))
     rc = _load().e2ttt_oracle_backward(
         B, H, T, d, dh, C, fw, flags, eps, _p(q), _p(k), _p(v), _p(eta), _p(beta), _p(gamma),
-        _p(w_in), _p(m_in), _p(d_out), _p(d_w_out), _p(d_m_out), _p(res["dq"]), _p(res["dk"]),
-        _p(res["dv"]), _p(res["d_eta"]), _p(res["d_beta"]), _p(res["d_gamma"]), _p(res["d_w_in"]),
-        _p(res["d_m_in"]), nthreads or default_threads())
+        _p(w_in), _p(m_in), _p(ln_a), _p(ln_b), _p(d_out), _p(d_w_out), _p(d_m_out), _p(res["dq"]),
+        _p(res["dk"]), _p(res["dv"]), _p(res["d_eta"]), _p(res["d_beta"]), _p(res["d_gamma"]),
+        _p(res["d_w_in"]), _p(res["d_m_in"]), _p(res.get("d_ln_a")), _p(res.get("d_ln_b")),
+        nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle backward rejected its arguments")
     return res
@@ -142,24 +154,26 @@ def chunk_coeffs(eta, beta, gamma=None):
     return kw, km, tuple(carry)
 
 
-def net(W, x, *, fw, dh, flags=0, eps=1e-5):
-    """f_W(x) for rows x[n, d] of one unit."""
-    W, x = _f64(W), _f64(x)
+def net(W, x, *, fw, dh, flags=0, eps=1e-5, ln_a=None, ln_b=None):
+    """f_W(x) for rows x[n, d] of one unit (ln_a, ln_b: its head's affine [d], or None)."""
+    W, x, ln_a, ln_b = _f64(W), _f64(x), _f64(ln_a), _f64(ln_b)
     n, d = x.shape
     f = np.zeros((n, d))
-    rc = _load().e2ttt_oracle_net(d, dh, fw, flags, eps, _p(W), n, _p(x), _p(f))
+    rc = _load().e2ttt_oracle_net(d, dh, fw, flags, eps, _p(W), _p(ln_a), _p(ln_b), n, _p(x),
+                                  _p(f))
     if rc != 0:
         raise ValueError("bad net arguments")
     return f
 
 
-def neg_grad(W, k, v, *, fw, dh, flags=0, eps=1e-5):
+def neg_grad(W, k, v, *, fw, dh, flags=0, eps=1e-5, ln_a=None, ln_b=None):
     """G[n, P] = -grad_W 1/2||f_W(k_r) - v_r||^2 for each row r."""
-    W, k, v = _f64(W), _f64(k), _f64(v)
+    W, k, v, ln_a, ln_b = _f64(W), _f64(k), _f64(v), _f64(ln_a), _f64(ln_b)
     n, d = k.shape
     P = param_count(d, dh, fw)
     G = np.zeros((n, P))
-    rc = _load().e2ttt_oracle_neg_grad(d, dh, fw, flags, eps, _p(W), n, _p(k), _p(v), _p(G))
+    rc = _load().e2ttt_oracle_neg_grad(d, dh, fw, flags, eps, _p(W), _p(ln_a), _p(ln_b), n, _p(k),
+                                       _p(v), _p(G))
     if rc != 0:
         raise ValueError("bad grad arguments")
     return G

@@ -16,8 +16,9 @@ def split(W, d, dh, fw):
             W[2 * dh * d:].reshape(d, dh))
 
 
-def net(W, x, d, dh, fw, resln=True, eps=1e-5):
-    """f_W(x) for x [..., d] (paper Sec. 4, fast-weight network)."""
+def net(W, x, d, dh, fw, resln=True, eps=1e-5, ln_a=None, ln_b=None):
+    """f_W(x) for x [..., d] (paper Sec. 4, fast-weight network); ln_a, ln_b:
+    the LayerNorm's elementwise affine (weight, bias), or None."""
     if fw == 0:
         W1, W2 = split(W, d, dh, fw)
         y = F.gelu(x @ W1.T) @ W2.T
@@ -26,7 +27,7 @@ def net(W, x, d, dh, fw, resln=True, eps=1e-5):
         y = (F.silu(x @ Wg.T) * (x @ Wu.T)) @ Wd.T
     if not resln:
         return y
-    return x + F.layer_norm(y, (d,), eps=eps)
+    return x + F.layer_norm(y, (d,), weight=ln_a, bias=ln_b, eps=eps)
 
 
 def neg_grad(W, k, v, d, dh, fw, resln=True, eps=1e-5, create_graph=False):
@@ -38,7 +39,8 @@ def neg_grad(W, k, v, d, dh, fw, resln=True, eps=1e-5, create_graph=False):
     return -g
 
 
-def chunked_forward(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=True, eps=1e-5):
+def chunked_forward(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=True, eps=1e-5,
+                    ln_a=None, ln_b=None):
     """One unit: token recurrence with gradients at chunk-start weights
     (paper eq. (7)), outputs f_{W_0}(q_t); differentiable end to end."""
     T = q.shape[0]
@@ -49,9 +51,9 @@ def chunked_forward(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=T
         W0 = W
         idx = range(s0, min(T, s0 + C))
         for t in idx:
-            outs.append(net(W0, q[t], d, dh, fw, resln, eps))
+            outs.append(net(W0, q[t], d, dh, fw, resln, eps, ln_a, ln_b))
         for t in idx:
-            L = 0.5 * ((net(W0, k[t], d, dh, fw, resln, eps) - v[t]) ** 2).sum()
+            L = 0.5 * ((net(W0, k[t], d, dh, fw, resln, eps, ln_a, ln_b) - v[t]) ** 2).sum()
             (g,) = torch.autograd.grad(L, W0, create_graph=True)
             M = beta[t] * M + eta[t] * (-g)
             g_t = gamma[t] if gamma is not None else 1.0
