@@ -14,8 +14,9 @@
  *     W_t = gamma_t W_{t-1} + M_t (eq. (7)) at every chunk end,
  * and the state (W, M) is carried from chunk to chunk.  The fast-weight net f
  * is the GELU MLP f(x) = x + LN(W2 GELU(W1 x)) or the SwiGLU net
- * f(x) = x + LN(Wd (SiLU(Wg x) * (Wu x))) of Sec. 4 (LayerNorm without affine,
- * biased variance, eps = ln_eps).  GELU is x Phi(x) with the normal CDF; the
+ * f(x) = x + LN(Wd (SiLU(Wg x) * (Wu x))) of Sec. 4 (LayerNorm with biased
+ * variance, eps = ln_eps, and optionally a learnable affine per head,
+ * E2TTT_FLAG_LN_AFFINE).  GELU is x Phi(x) with the normal CDF; the
  * chunk kernels evaluate Phi through the rational erfc of Abramowitz & Stegun
  * eq. 7.1.26 (absolute error at most 1.5e-7, so a relative error of Phi that
  * grows for x << 0 where Phi itself is tiny), e2ttt_apply through erff.
@@ -105,6 +106,13 @@ typedef enum { E2TTT_DT_F32 = 0, E2TTT_DT_BF16 = 1 } e2ttt_dtype;
  * Outputs, gradients and every other convention are unchanged (all entry
  * points that take a descriptor honour the flag). */
 #define E2TTT_FLAG_CHUNK_AVERAGED 0x2u
+/* Learnable LayerNorm affine of the fast-weight net (Sec. 4's LayerNorm with
+ * an elementwise weight and bias per head, slow weights shared by the batch):
+ *   f(x) = x + a * LN(y) + b,   a, b in R^d per head.
+ * Calls with this flag take a and b (and return their gradients) through the
+ * *_ln entry points below; the plain entry points return E2TTT_ERR_NULL_ARG
+ * for it.  Not combinable with E2TTT_FLAG_NO_RESIDUAL_LN (E2TTT_ERR_BAD_SHAPE). */
+#define E2TTT_FLAG_LN_AFFINE 0x4u
 
 typedef struct {
   int32_t B, H, T;      /* batch, heads, tokens                        */
@@ -279,6 +287,39 @@ e2ttt_status e2ttt_chunk_forward_static(const e2ttt_desc* desc, const void* q, c
                                         const void* v, const float* eta, const float* beta,
                                         const float* gamma, const float* w_in, const float* m_in,
                                         void* out, float* w_out, float* m_out, void* stream);
+
+/*
+ * The chunk calls and the net evaluation with the learnable LayerNorm affine
+ * (E2TTT_FLAG_LN_AFFINE in desc.flags): the same arguments as e2ttt_chunk_forward,
+ * e2ttt_chunk_backward and e2ttt_apply, plus
+ *   ln_weight, ln_bias    [H][d] f32 device arrays: a and b of each head (unit
+ *                         (b, h) uses row h); required with the flag
+ *   d_ln_weight, d_ln_bias [H][d] f32 (backward only): the gradients of a and b,
+ *                         summed over the batch and all tokens (overwritten)
+ * Without the flag every one of these pointers must be NULL, and the calls
+ * equal the plain ones.  The backward's scratch (e2ttt_backward_scratch_bytes,
+ * which reads the flag) then also holds, per token row, the adjoint the
+ * affine's gradients are summed from, and one partial sum per block of 256
+ * tokens; ln_weight and ln_bias must be 16-byte aligned (else E2TTT_ERR_BAD_SHAPE).
+ */
+e2ttt_status e2ttt_chunk_forward_ln(const e2ttt_desc* desc, const float* ln_weight,
+                                    const float* ln_bias, const void* q, const void* k,
+                                    const void* v, const float* eta, const float* beta,
+                                    const float* gamma, const float* w_in, const float* m_in,
+                                    void* out, float* w_out, float* m_out, void* workspace,
+                                    size_t workspace_bytes, int save_for_backward, void* stream);
+e2ttt_status e2ttt_chunk_backward_ln(const e2ttt_desc* desc, const float* ln_weight,
+                                     const float* ln_bias, const void* q, const void* k,
+                                     const void* v, const float* eta, const float* beta,
+                                     const float* gamma, const float* w_in, const float* m_in,
+                                     const void* workspace, size_t workspace_bytes,
+                                     const void* d_out, const float* d_w_out,
+                                     const float* d_m_out, void* dq, void* dk, void* dv,
+                                     float* d_eta, float* d_beta, float* d_gamma, float* d_w_in,
+                                     float* d_m_in, float* d_ln_weight, float* d_ln_bias,
+                                     void* scratch, size_t scratch_bytes, void* stream);
+e2ttt_status e2ttt_apply_ln(const e2ttt_desc* desc, const float* ln_weight, const float* ln_bias,
+                            const void* q, const float* w, void* out, void* stream);
 
 /* Static description of a status code. */
 const char* e2ttt_status_str(e2ttt_status status);

@@ -43,7 +43,9 @@ struct Plan {
   long tpc = 1;           // 64-row tiles per chunk (chunks longer than one tile)
   // backward scratch
   size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, off_bsync = 0, off_bxbuf = 0, off_frz = 0;
+  size_t off_zbar = 0, off_apart = 0;   // LayerNorm affine: written rows and partial sums
   size_t scratch_bytes = 0;
+  bool affine = false;
 };
 
 e2ttt_status select_config(const e2ttt_desc& d, ChainConfig& cfg) {
@@ -95,9 +97,12 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
     return E2TTT_ERR_BAD_SHAPE;
   if (d.fw != E2TTT_FW_GELU_MLP && d.fw != E2TTT_FW_SWIGLU) return E2TTT_ERR_UNSUPPORTED;
   if (d.io != E2TTT_DT_F32 && d.io != E2TTT_DT_BF16) return E2TTT_ERR_UNSUPPORTED;
-  if (d.flags & ~(E2TTT_FLAG_NO_RESIDUAL_LN | E2TTT_FLAG_CHUNK_AVERAGED))
+  if (d.flags & ~(E2TTT_FLAG_NO_RESIDUAL_LN | E2TTT_FLAG_CHUNK_AVERAGED | E2TTT_FLAG_LN_AFFINE))
     return E2TTT_ERR_UNSUPPORTED;
   if (!(d.flags & E2TTT_FLAG_NO_RESIDUAL_LN) && !(d.ln_eps > 0.0f)) return E2TTT_ERR_BAD_SHAPE;
+  // the affine belongs to the LayerNorm of the residual form
+  if ((d.flags & E2TTT_FLAG_LN_AFFINE) && (d.flags & E2TTT_FLAG_NO_RESIDUAL_LN))
+    return E2TTT_ERR_BAD_SHAPE;
   if (d.chunk > kMaxChunk) return E2TTT_ERR_UNSUPPORTED;
   const long U = (long)d.B * d.H;
   if (U > INT_MAX || (long)d.T * d.d > (1L << 40) / U) return E2TTT_ERR_UNSUPPORTED;
@@ -145,9 +150,27 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.off_frz =
       pl.off_bxbuf +
       align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, true) * sizeof(float));
-  pl.scratch_bytes =
+  pl.off_zbar =
       pl.off_frz +
       (pl.tpc > 1 ? align_up((size_t)nwg * 2 * chain_frz_floats(pl.cfg) * sizeof(float)) : 0);
+  pl.affine = (d.flags & E2TTT_FLAG_LN_AFFINE) != 0;
+  pl.off_apart = pl.off_zbar + (pl.affine ? align_up(tokd) : 0);
+  const long nb = (d.T + kAffineTokBlock - 1) / kAffineTokBlock;
+  pl.scratch_bytes =
+      pl.off_apart + (pl.affine ? align_up((size_t)U * nb * 2 * d.d * sizeof(float)) : 0);
+  return E2TTT_OK;
+}
+
+// The affine pointers agree with the descriptor: all given with the flag
+// (gradients only in the backward), none without it.
+e2ttt_status check_affine(const Plan& pl, const float* a, const float* b, bool backward,
+                          const float* ga, const float* gb) {
+  if (pl.affine) {
+    if (!a || !b || (backward && (!ga || !gb))) return E2TTT_ERR_NULL_ARG;
+    if (!aligned16(a) || !aligned16(b)) return E2TTT_ERR_BAD_SHAPE;
+  } else if (a || b || ga || gb) {
+    return E2TTT_ERR_BAD_SHAPE;
+  }
   return E2TTT_OK;
 }
 
@@ -284,10 +307,17 @@ e2ttt_status e2ttt_chunk_coeffs(const e2ttt_desc* desc, const float* eta, const 
 
 e2ttt_status e2ttt_apply(const e2ttt_desc* desc, const void* q, const float* w, void* out,
                          void* stream) {
+  return e2ttt_apply_ln(desc, nullptr, nullptr, q, w, out, stream);
+}
+
+e2ttt_status e2ttt_apply_ln(const e2ttt_desc* desc, const float* ln_weight, const float* ln_bias,
+                            const void* q, const float* w, void* out, void* stream) {
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
   if (!q || !w || !out) return E2TTT_ERR_NULL_ARG;
+  st = check_affine(pl, ln_weight, ln_bias, false, nullptr, nullptr);
+  if (st != E2TTT_OK) return st;
   if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return E2TTT_ERR_BAD_SHAPE;
   if (desc->dh > (desc->d == 128 ? 512 : kApplyMaxDh)) return E2TTT_ERR_UNSUPPORTED;
   if (pl.U * ((pl.T + 7) / 8) > INT_MAX) return E2TTT_ERR_UNSUPPORTED;
@@ -299,6 +329,9 @@ e2ttt_status e2ttt_apply(const e2ttt_desc* desc, const void* q, const float* w, 
   a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
   a.eps = desc->ln_eps;
+  a.ln_a = ln_weight;
+  a.ln_b = ln_bias;
+  a.H = desc->H;
   hipStream_t s = static_cast<hipStream_t>(stream);
   return finish(launch_apply(pl.cfg, desc->fw, a, s), s);
 }
@@ -308,11 +341,24 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
                                  const float* gamma, const float* w_in, const float* m_in,
                                  void* out, float* w_out, float* m_out, void* workspace,
                                  size_t workspace_bytes, int save_for_backward, void* stream) {
+  return e2ttt_chunk_forward_ln(desc, nullptr, nullptr, q, k, v, eta, beta, gamma, w_in, m_in,
+                                out, w_out, m_out, workspace, workspace_bytes, save_for_backward,
+                                stream);
+}
+
+e2ttt_status e2ttt_chunk_forward_ln(const e2ttt_desc* desc, const float* ln_weight,
+                                    const float* ln_bias, const void* q, const void* k,
+                                    const void* v, const float* eta, const float* beta,
+                                    const float* gamma, const float* w_in, const float* m_in,
+                                    void* out, float* w_out, float* m_out, void* workspace,
+                                    size_t workspace_bytes, int save_for_backward, void* stream) {
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
   if (st != E2TTT_OK) return st;
   if (!q || !k || !v || !eta || !beta || !w_in || !out || !w_out || !m_out || !workspace)
     return E2TTT_ERR_NULL_ARG;
+  st = check_affine(pl, ln_weight, ln_bias, false, nullptr, nullptr);
+  if (st != E2TTT_OK) return st;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(workspace))
     return E2TTT_ERR_BAD_SHAPE;
   if (workspace_bytes < (save_for_backward ? pl.ws_bytes_save : pl.ws_bytes))
@@ -353,6 +399,9 @@ e2ttt_status e2ttt_chunk_forward(const e2ttt_desc* desc, const void* q, const vo
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
   a.eps = desc->ln_eps;
+  a.ln_a = ln_weight;
+  a.ln_b = ln_bias;
+  a.H = desc->H;
   return finish(launch_chain_fwd(pl.cfg, a, s), s, sync);
 }
 
@@ -364,8 +413,26 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
                                   void* dq, void* dk, void* dv, float* d_eta, float* d_beta,
                                   float* d_gamma, float* d_w_in, float* d_m_in, void* scratch,
                                   size_t scratch_bytes, void* stream) {
+  return e2ttt_chunk_backward_ln(desc, nullptr, nullptr, q, k, v, eta, beta, gamma, w_in, m_in,
+                                 workspace, workspace_bytes, d_out, d_w_out, d_m_out, dq, dk, dv,
+                                 d_eta, d_beta, d_gamma, d_w_in, d_m_in, nullptr, nullptr,
+                                 scratch, scratch_bytes, stream);
+}
+
+e2ttt_status e2ttt_chunk_backward_ln(const e2ttt_desc* desc, const float* ln_weight,
+                                     const float* ln_bias, const void* q, const void* k,
+                                     const void* v, const float* eta, const float* beta,
+                                     const float* gamma, const float* w_in, const float* m_in,
+                                     const void* workspace, size_t workspace_bytes,
+                                     const void* d_out, const float* d_w_out,
+                                     const float* d_m_out, void* dq, void* dk, void* dv,
+                                     float* d_eta, float* d_beta, float* d_gamma, float* d_w_in,
+                                     float* d_m_in, float* d_ln_weight, float* d_ln_bias,
+                                     void* scratch, size_t scratch_bytes, void* stream) {
   Plan pl;
   e2ttt_status st = make_plan(desc, pl);
+  if (st != E2TTT_OK) return st;
+  st = check_affine(pl, ln_weight, ln_bias, true, d_ln_weight, d_ln_bias);
   if (st != E2TTT_OK) return st;
   if (!q || !k || !v || !eta || !beta || !w_in || !workspace || !d_out || !dq || !dk || !dv ||
       !d_eta || !d_beta || !d_w_in || !d_m_in || !scratch)
@@ -411,12 +478,23 @@ e2ttt_status e2ttt_chunk_backward(const e2ttt_desc* desc, const void* q, const v
   a.T = (int)pl.T; a.C = desc->chunk; a.NC = (int)pl.NC; a.dh = desc->dh; a.P = pl.P;
   a.resln = (desc->flags & E2TTT_FLAG_NO_RESIDUAL_LN) ? 0 : 1;
   a.eps = desc->ln_eps;
+  a.ln_a = ln_weight;
+  a.ln_b = ln_bias;
+  a.H = desc->H;
+  a.ln_zbar = pl.affine ? at<float>(scratch, pl.off_zbar) : nullptr;
   hipError_t e = launch_chain_bwd(pl.cfg, a, s);
   if (e != hipSuccess) return E2TTT_ERR_HIP;
   CoeffBwdArgs cb{eta, beta, gamma, a.kwb, a.kmb, a.carryb, d_eta, d_beta, d_gamma,
                   (int)pl.T, desc->chunk, (int)pl.NC, pl.U * pl.NC, pl.cfg.ns,
                   pl.U * pl.T, pl.U * pl.NC * 3, averaged(desc)};
-  return finish(launch_coeff_bwd(cb, s), s, sync);
+  e = launch_coeff_bwd(cb, s);
+  if (e == hipSuccess && pl.affine) {
+    AffineGradArgs g{d_out, k, v, a.zk, a.zq, a.ln_zbar, ln_weight, ln_bias,
+                     at<float>(scratch, pl.off_apart), d_ln_weight, d_ln_bias, pl.U, desc->H,
+                     (int)pl.T, desc->d, pl.cfg.bf};
+    e = launch_affine_grad(g, s);
+  }
+  return finish(e, s, sync);
 }
 
 e2ttt_status e2ttt_wait_status(const e2ttt_desc* desc, const void* workspace,

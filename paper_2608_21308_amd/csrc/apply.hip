@@ -159,7 +159,9 @@ __global__ void __launch_bounds__(64 * kApplyWaves) apply_kernel(ApplyArgs a) {
       const float mean = wave_sum(y) * (1.0f / D);
       const float dv = act ? y - mean : 0.0f;
       const float var = wave_sum(dv * dv) * (1.0f / D);
-      o = qs[t][lane < D ? lane : 0] + dv / sqrtf(var + a.eps);
+      const float z = dv / sqrtf(var + a.eps);
+      const int ic = lane < D ? lane : 0;
+      o = qs[t][ic] + (a.ln_a ? fmaf(a.ln_a[(u % a.H) * D + ic], z, a.ln_b[(u % a.H) * D + ic]) : z);
     }
     if (act) Io::st(out + (long)t * D + lane, o);
   }
@@ -299,8 +301,14 @@ __global__ void __launch_bounds__(64 * kApplyWaves) apply128_kernel(ApplyArgs a)
       const float d0 = y0 - mean, d1 = y1 - mean;
       const float var = wave_sum(d0 * d0 + d1 * d1) * (1.0f / D);
       const float inv = 1.0f / sqrtf(var + a.eps);
-      o0 = qs[t][lane] + d0 * inv;
-      o1 = qs[t][lane + 64] + d1 * inv;
+      float z0 = d0 * inv, z1 = d1 * inv;
+      if (a.ln_a) {
+        const long ho = (u % a.H) * D;
+        z0 = fmaf(a.ln_a[ho + lane], z0, a.ln_b[ho + lane]);
+        z1 = fmaf(a.ln_a[ho + lane + 64], z1, a.ln_b[ho + lane + 64]);
+      }
+      o0 = qs[t][lane] + z0;
+      o1 = qs[t][lane + 64] + z1;
     }
     Io::st(out + (long)t * D + lane, o0);
     Io::st(out + (long)t * D + lane + 64, o1);

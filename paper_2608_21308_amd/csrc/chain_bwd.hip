@@ -512,12 +512,28 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         if (resln) {
           const float sig = row[2 * t];
           float se = 0.0f, sez = 0.0f;
+          if (E2TTT_ARG(ln_a)) {
+            // f = k + a z + b: e below is a (v - f), what the LayerNorm backward takes
+            float la[EPL], lb[EPL];
+            const long ho = (u % E2TTT_ARG(H)) * D + l16 * EPL;
+            load_row_part<EPL>(la, E2TTT_ARG(ln_a) + ho);
+            load_row_part<EPL>(lb, E2TTT_ARG(ln_b) + ho);
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) {
-            const int i = l16 * EPL + q;
-            e[q] = O::from_e(xv[t * S::LDD + i]) - O::from_e(xk[t * S::LDD + i]) - z[q];
-            se += e[q];
-            sez += e[q] * z[q];
+            for (int q = 0; q < EPL; ++q) {
+              const int i = l16 * EPL + q;
+              const float r = O::from_e(xv[t * S::LDD + i]) - O::from_e(xk[t * S::LDD + i]);
+              e[q] = la[q] * (r - fmaf(la[q], z[q], lb[q]));
+              se += e[q];
+              sez += e[q] * z[q];
+            }
+          } else {
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) {
+              const int i = l16 * EPL + q;
+              e[q] = O::from_e(xv[t * S::LDD + i]) - O::from_e(xk[t * S::LDD + i]) - z[q];
+              se += e[q];
+              sez += e[q] * z[q];
+            }
           }
           const float me = group16_sum(se) * inv_d;
           mez = group16_sum(sez) * inv_d;
@@ -866,8 +882,26 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             const float sh = -group16_sum(sdd) * sig;
             float n1 = 0.0f, n2 = 0.0f;
 #pragma unroll
+            for (int q = 0; q < EPL; ++q) zh[q] = -(dyhv[q] * mez + e[q] * m2) * sig;
+            if (E2TTT_ARG(ln_a)) {
+              // with f = k + a z + b: e's adjoint is a eh (dv, and -a eh into dk), and z
+              // takes -a^2 eh; eh itself (the adjoint of a e) is kept for the
+              // affine's gradients
+              float la[EPL];
+              load_row_part<EPL>(la, E2TTT_ARG(ln_a) + (u % E2TTT_ARG(H)) * D + l16 * EPL);
+              if (t < len && t >= rlo && t < rhi)
+                store_row_io<IoT<false>, EPL>(E2TTT_ARG(ln_zbar) + (row0 + t) * D + l16 * EPL, eh);
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) {
+                zh[q] -= la[q] * la[q] * eh[q];
+                eh[q] *= la[q];
+              }
+            } else {
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) zh[q] -= eh[q];
+            }
+#pragma unroll
             for (int q = 0; q < EPL; ++q) {
-              zh[q] = -(dyhv[q] * mez + e[q] * m2) * sig - eh[q];
               n1 += zh[q];
               n2 += zh[q] * z[q];
             }
@@ -1017,6 +1051,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           if (resln) {
             const float sig = row[2 * t];
             float z[EPL], m1 = 0.0f, m2 = 0.0f;
+            if (E2TTT_ARG(ln_a)) {   // o = q + a z_q + b: the LayerNorm backward takes a dO
+              float la[EPL];
+              load_row_part<EPL>(la, E2TTT_ARG(ln_a) + (u % E2TTT_ARG(H)) * D + l16 * EPL);
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) dov[q] *= la[q];
+            }
 #pragma unroll
             for (int q = 0; q < EPL; ++q) {
               z[q] = yk[t * D + l16 * EPL + q];

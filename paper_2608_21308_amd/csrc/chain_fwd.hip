@@ -448,13 +448,30 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             for (int q = 0; q < EPL; ++q) { yv[q] -= mu; s2 += yv[q] * yv[q]; }
             sig = rsq_f(group16_sum(s2) * inv_d + E2TTT_ARG(eps));   // 1 / sigma
             float se = 0.0f, sez = 0.0f;
+            if (E2TTT_ARG(ln_a)) {
+              // f = k + a z + b: the LayerNorm backward takes a (v - f)
+              float la[EPL], lb[EPL];
+              const long ho = (u % E2TTT_ARG(H)) * D + l16 * EPL;
+              load_row_part<EPL>(la, E2TTT_ARG(ln_a) + ho);
+              load_row_part<EPL>(lb, E2TTT_ARG(ln_b) + ho);
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) {
-              const int i = l16 * EPL + q;
-              z[q] = yv[q] * sig;
-              e[q] = O::from_e(sm.xv[t * S::LDD + i]) - O::from_e(sm.xk[t * S::LDD + i]) - z[q];
-              se += e[q];
-              sez += e[q] * z[q];
+              for (int q = 0; q < EPL; ++q) {
+                const int i = l16 * EPL + q;
+                z[q] = yv[q] * sig;
+                const float r = O::from_e(sm.xv[t * S::LDD + i]) - O::from_e(sm.xk[t * S::LDD + i]);
+                e[q] = la[q] * (r - fmaf(la[q], z[q], lb[q]));
+                se += e[q];
+                sez += e[q] * z[q];
+              }
+            } else {
+#pragma unroll
+              for (int q = 0; q < EPL; ++q) {
+                const int i = l16 * EPL + q;
+                z[q] = yv[q] * sig;
+                e[q] = O::from_e(sm.xv[t * S::LDD + i]) - O::from_e(sm.xk[t * S::LDD + i]) - z[q];
+                se += e[q];
+                sez += e[q] * z[q];
+              }
             }
             const float me = group16_sum(se) * inv_d, mez = group16_sum(sez) * inv_d;
 #pragma unroll
@@ -674,6 +691,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             for (int q = 0; q < EPL; ++q) {
               yv[q] *= sig;                                 // Z_Q
               f[q] = O::from_e(sm.xq[t * S::LDD + l16 * EPL + q]) + yv[q];
+            }
+            if (E2TTT_ARG(ln_a)) {                          // f = q + a Z_Q + b
+              float la[EPL], lb[EPL];
+              const long ho = (u % E2TTT_ARG(H)) * D + l16 * EPL;
+              load_row_part<EPL>(la, E2TTT_ARG(ln_a) + ho);
+              load_row_part<EPL>(lb, E2TTT_ARG(ln_b) + ho);
+#pragma unroll
+              for (int q = 0; q < EPL; ++q)
+                f[q] = O::from_e(sm.xq[t * S::LDD + l16 * EPL + q]) + fmaf(la[q], yv[q], lb[q]);
             }
           } else {
 #pragma unroll

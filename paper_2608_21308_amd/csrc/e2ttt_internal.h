@@ -99,7 +99,37 @@ struct ChainArgs {
   long P;               // parameters per unit (unpadded)
   int resln;            // 1: f = x + LN(y); 0: f = y
   float eps;
+  // learnable LayerNorm affine, f = x + a LN(y) + b, per head [H][d] fp32
+  // (nullable together: no affine); unit u belongs to head u mod H
+  const float* ln_a;
+  const float* ln_b;
+  int H;
+  // backward with the affine: the adjoint of a * e for every token row
+  // [U][T][d] fp32, rows [rank share] written by each rank
+  float* ln_zbar;
 };
+
+// The affine's gradients from the saved and written rows (ln_affine.hip):
+// per head h and column i, over the batch and all tokens,
+//   d_a = sum dO z_q + zbar (e - a z_k),  d_b = sum dO - a zbar,
+//   e = v - k - a z_k - b.
+struct AffineGradArgs {
+  const void* d_out;    // [U][T][d] io
+  const void* k;
+  const void* v;
+  const float* zk;      // [U][T][d] fp32 (saved by the forward)
+  const float* zq;
+  const float* zbar;    // [U][T][d] fp32 (written by the backward chain)
+  const float* ln_a;    // [H][d]
+  const float* ln_b;
+  float* part;          // [U][NB][2][d] partial sums per token block
+  float* d_ln_a;        // [H][d]
+  float* d_ln_b;
+  long U;
+  int H, T, d, bf;
+};
+constexpr int kAffineTokBlock = 256;
+hipError_t launch_affine_grad(const AffineGradArgs& a, hipStream_t stream);
 
 // Kernel configuration chosen by the host for a descriptor.
 struct ChainConfig {
@@ -124,6 +154,9 @@ struct ApplyArgs {
   long P;
   int resln;
   float eps;
+  const float* ln_a;    // LayerNorm affine per head [H][d], nullable together
+  const float* ln_b;
+  int H;
 };
 constexpr int kApplyMaxDh = 256;
 

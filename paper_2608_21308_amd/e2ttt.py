@@ -22,6 +22,7 @@ DT_F32 = 0
 DT_BF16 = 1
 FLAG_NO_RESIDUAL_LN = 1
 FLAG_CHUNK_AVERAGED = 2
+FLAG_LN_AFFINE = 4
 
 STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
           4: "workspace too small", 5: "HIP error", 6: "device-side wait expired"}
@@ -30,7 +31,8 @@ STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
 EXPORTS = ("e2ttt_param_count", "e2ttt_workspace_bytes", "e2ttt_backward_scratch_bytes",
            "e2ttt_chunk_forward", "e2ttt_chunk_backward", "e2ttt_chunk_coeffs",
            "e2ttt_apply", "e2ttt_gates_forward", "e2ttt_gates_backward", "e2ttt_wait_status",
-           "e2ttt_chunk_forward_static", "e2ttt_status_str")
+           "e2ttt_chunk_forward_static", "e2ttt_chunk_forward_ln", "e2ttt_chunk_backward_ln",
+           "e2ttt_apply_ln", "e2ttt_status_str")
 
 
 class E2TTTError(RuntimeError):
@@ -92,6 +94,12 @@ def load():
     lib.e2ttt_wait_status.restype = i
     lib.e2ttt_chunk_forward_static.argtypes = [dp] + [vp] * 12
     lib.e2ttt_chunk_forward_static.restype = i
+    lib.e2ttt_chunk_forward_ln.argtypes = [dp] + [vp] * 14 + [sz, i, vp]
+    lib.e2ttt_chunk_forward_ln.restype = i
+    lib.e2ttt_chunk_backward_ln.argtypes = [dp] + [vp] * 11 + [sz] + [vp] * 14 + [sz, vp]
+    lib.e2ttt_chunk_backward_ln.restype = i
+    lib.e2ttt_apply_ln.argtypes = [dp] + [vp] * 6
+    lib.e2ttt_apply_ln.restype = i
     lib.e2ttt_status_str.argtypes = [i]
     lib.e2ttt_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -144,6 +152,7 @@ def _check(st: int, where: str):
 _IO = ("q", "k", "v", "out", "d_out", "dq", "dk", "dv")
 _GATE = ("eta", "beta", "gamma", "d_eta", "d_beta", "d_gamma", "kw", "km")
 _STATE = ("w_in", "m_in", "w_out", "m_out", "d_w_in", "d_m_in", "d_w_out", "d_m_out")
+_HEAD = ("ln_weight", "ln_bias", "d_ln_weight", "d_ln_bias")
 
 
 def _check_tensors(cfg: Config, **ts):
@@ -164,6 +173,8 @@ def _check_tensors(cfg: Config, **ts):
             want = (torch.float32, n_tok)
         elif name in _STATE:
             want = (torch.float32, cfg.B * cfg.H * cfg.P)
+        elif name in _HEAD:
+            want = (torch.float32, cfg.H * cfg.d)
         else:                       # workspace, scratch: byte buffers
             want = (torch.uint8, t.numel())
         if t.dtype != want[0] or t.numel() != want[1]:
@@ -195,10 +206,12 @@ def alloc_workspace(cfg: Config, save_for_backward: bool, device="cuda"):
 
 
 def forward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in=None, *, out=None, w_out=None,
-            m_out=None, workspace=None, save_for_backward=False):
-    """Runs e2ttt_chunk_forward on the current stream; returns (out, w_out, m_out, workspace)."""
+            m_out=None, workspace=None, save_for_backward=False, ln_weight=None, ln_bias=None):
+    """Runs e2ttt_chunk_forward (e2ttt_chunk_forward_ln with the LayerNorm affine
+    ln_weight, ln_bias [H, d]) on the current stream; returns (out, w_out, m_out, workspace)."""
     _check_tensors(cfg, q=q, k=k, v=v, eta=eta, beta=beta, gamma=gamma, w_in=w_in, m_in=m_in,
-                   out=out, w_out=w_out, m_out=m_out, workspace=workspace)
+                   out=out, w_out=w_out, m_out=m_out, workspace=workspace, ln_weight=ln_weight,
+                   ln_bias=ln_bias)
     lib = load()
     dev = q.device
     if out is None:
@@ -210,10 +223,11 @@ def forward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in=None, *, out=None
     if workspace is None:
         workspace = alloc_workspace(cfg, save_for_backward, dev)
     d = cfg.desc()
-    st = lib.e2ttt_chunk_forward(ctypes.byref(d), _ptr(q), _ptr(k), _ptr(v), _ptr(eta),
-                                 _ptr(beta), _ptr(gamma), _ptr(w_in), _ptr(m_in), _ptr(out),
-                                 _ptr(w_out), _ptr(m_out), _ptr(workspace),
-                                 workspace.numel(), int(bool(save_for_backward)), _stream())
+    st = lib.e2ttt_chunk_forward_ln(ctypes.byref(d), _ptr(ln_weight), _ptr(ln_bias), _ptr(q),
+                                    _ptr(k), _ptr(v), _ptr(eta), _ptr(beta), _ptr(gamma),
+                                    _ptr(w_in), _ptr(m_in), _ptr(out), _ptr(w_out), _ptr(m_out),
+                                    _ptr(workspace), workspace.numel(),
+                                    int(bool(save_for_backward)), _stream())
     _check(st, "e2ttt_chunk_forward")
     return out, w_out, m_out, workspace
 
@@ -239,12 +253,13 @@ def forward_static(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, out, w_ou
 
 
 def backward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, workspace, d_out, d_w_out=None,
-             d_m_out=None, *, grads=None, scratch=None):
-    """Runs e2ttt_chunk_backward; returns a dict of gradients (dq, dk, dv, d_eta, d_beta,
-    d_gamma, d_w_in, d_m_in)."""
+             d_m_out=None, *, grads=None, scratch=None, ln_weight=None, ln_bias=None):
+    """Runs e2ttt_chunk_backward (e2ttt_chunk_backward_ln with the LayerNorm affine);
+    returns a dict of gradients (dq, dk, dv, d_eta, d_beta, d_gamma, d_w_in, d_m_in, and
+    d_ln_weight, d_ln_bias [H, d] with the affine)."""
     _check_tensors(cfg, q=q, k=k, v=v, eta=eta, beta=beta, gamma=gamma, w_in=w_in, m_in=m_in,
                    workspace=workspace, d_out=d_out, d_w_out=d_w_out, d_m_out=d_m_out,
-                   scratch=scratch, **(grads or {}))
+                   scratch=scratch, ln_weight=ln_weight, ln_bias=ln_bias, **(grads or {}))
     lib = load()
     dev = q.device
     if grads is None:
@@ -252,29 +267,34 @@ def backward(cfg: Config, q, k, v, eta, beta, gamma, w_in, m_in, workspace, d_ou
                      d_eta=torch.empty_like(eta), d_beta=torch.empty_like(beta),
                      d_gamma=None if gamma is None else torch.empty_like(gamma),
                      d_w_in=torch.empty_like(w_in), d_m_in=torch.empty_like(w_in))
+        if ln_weight is not None:
+            grads["d_ln_weight"] = torch.empty_like(ln_weight)
+            grads["d_ln_bias"] = torch.empty_like(ln_weight)
     if scratch is None:
         scratch = torch.empty(backward_scratch_bytes(cfg), dtype=torch.uint8, device=dev)
     d = cfg.desc()
     g = grads
-    st = lib.e2ttt_chunk_backward(
-        ctypes.byref(d), _ptr(q), _ptr(k), _ptr(v), _ptr(eta), _ptr(beta), _ptr(gamma),
-        _ptr(w_in), _ptr(m_in), _ptr(workspace), workspace.numel(), _ptr(d_out), _ptr(d_w_out),
-        _ptr(d_m_out), _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["d_eta"]),
-        _ptr(g["d_beta"]), _ptr(g["d_gamma"]), _ptr(g["d_w_in"]), _ptr(g["d_m_in"]),
-        _ptr(scratch), scratch.numel(), _stream())
+    st = lib.e2ttt_chunk_backward_ln(
+        ctypes.byref(d), _ptr(ln_weight), _ptr(ln_bias), _ptr(q), _ptr(k), _ptr(v), _ptr(eta),
+        _ptr(beta), _ptr(gamma), _ptr(w_in), _ptr(m_in), _ptr(workspace), workspace.numel(),
+        _ptr(d_out), _ptr(d_w_out), _ptr(d_m_out), _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]),
+        _ptr(g["d_eta"]), _ptr(g["d_beta"]), _ptr(g["d_gamma"]), _ptr(g["d_w_in"]),
+        _ptr(g["d_m_in"]), _ptr(g.get("d_ln_weight")), _ptr(g.get("d_ln_bias")), _ptr(scratch),
+        scratch.numel(), _stream())
     _check(st, "e2ttt_chunk_backward")
     return grads
 
 
-def apply(cfg: Config, q, w, out=None):
-    """Runs e2ttt_apply: out = f_W(q) for the cfg.T tokens of q per unit, all at
-    the state w [B,H,P]."""
-    _check_tensors(cfg, q=q, w_in=w, out=out)
+def apply(cfg: Config, q, w, out=None, ln_weight=None, ln_bias=None):
+    """Runs e2ttt_apply (e2ttt_apply_ln with the LayerNorm affine): out = f_W(q)
+    for the cfg.T tokens of q per unit, all at the state w [B,H,P]."""
+    _check_tensors(cfg, q=q, w_in=w, out=out, ln_weight=ln_weight, ln_bias=ln_bias)
     lib = load()
     if out is None:
         out = torch.empty_like(q)
     d = cfg.desc()
-    st = lib.e2ttt_apply(ctypes.byref(d), _ptr(q), _ptr(w), _ptr(out), _stream())
+    st = lib.e2ttt_apply_ln(ctypes.byref(d), _ptr(ln_weight), _ptr(ln_bias), _ptr(q), _ptr(w),
+                            _ptr(out), _stream())
     _check(st, "e2ttt_apply")
     return out
 

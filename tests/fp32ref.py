@@ -58,8 +58,10 @@ def scalar_kernels(eta, beta, gamma):
     return eta * S, eta * bt, (cw, beta[0] * S[0], beta[0] * bt[0])
 
 
-def closed_form_unit(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=True, eps=1e-5):
-    """One unit over all chunks: (outputs [T, d], W_T, M_T), differentiable."""
+def closed_form_unit(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=True, eps=1e-5,
+                     ln_a=None, ln_b=None):
+    """One unit over all chunks: (outputs [T, d], W_T, M_T), differentiable;
+    ln_a, ln_b: the unit's LayerNorm affine [d], or None."""
     T = q.shape[0]
     W = w_in
     M = m_in if m_in is not None else torch.zeros_like(w_in)
@@ -71,8 +73,9 @@ def closed_form_unit(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=
             W0 = W0.detach().requires_grad_(True)
         g = None if gamma is None else gamma[sl]
         kw, km, (cw, cm, cb) = scalar_kernels(eta[sl], beta[sl], g)
-        outs.append(torchref.net(W0, q[sl], d, dh, fw, resln, eps))
-        per_tok = 0.5 * ((torchref.net(W0, k[sl], d, dh, fw, resln, eps) - v[sl]) ** 2).sum(-1)
+        outs.append(torchref.net(W0, q[sl], d, dh, fw, resln, eps, ln_a, ln_b))
+        per_tok = 0.5 * ((torchref.net(W0, k[sl], d, dh, fw, resln, eps, ln_a, ln_b) - v[sl]) ** 2
+                         ).sum(-1)
         (gw,) = torch.autograd.grad((kw * per_tok).sum(), W0, create_graph=True)
         (gm,) = torch.autograd.grad((km * per_tok).sum(), W0, create_graph=True)
         W = cw * W0 + cm * M0 - gw
@@ -87,16 +90,18 @@ def _t(a, dtype, grad=False):
     return t.requires_grad_(True) if grad else t
 
 
-def forward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32):
-    """(out [B,H,T,d], w_out, m_out) as float64 numpy, evaluated in `dtype`."""
+def forward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32, ln=None):
+    """(out [B,H,T,d], w_out, m_out) as float64 numpy, evaluated in `dtype`;
+    ln: the LayerNorm affine per head, a pair of [H, d] arrays, or None."""
     B, H, T, d = np.asarray(x["q"]).shape
     resln = not (flags & 1)
     outs, ws, ms = [], [], []
     for b in range(B):
         for h in range(H):
             g = lambda n: None if x.get(n) is None else _t(x[n][b, h], dtype)
+            la, lb = (None, None) if ln is None else (_t(ln[0][h], dtype), _t(ln[1][h], dtype))
             o, W, M = closed_form_unit(g("q"), g("k"), g("v"), g("eta"), g("beta"), g("gamma"),
-                                       g("w_in"), g("m_in"), C, d, dh, fw, resln, eps)
+                                       g("w_in"), g("m_in"), C, d, dh, fw, resln, eps, la, lb)
             outs.append(o.detach().double().numpy())
             ws.append(W.detach().double().numpy())
             ms.append(M.detach().double().numpy())
@@ -105,11 +110,16 @@ def forward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32):
             np.stack(ms).reshape(B, H, P))
 
 
-def backward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32):
+def backward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32, ln=None):
     """Gradients of sum<d_out,out> + <d_w_out,w_out> + <d_m_out,m_out>, named as
-    the oracle's (dq, dk, dv, d_eta, d_beta, d_gamma, d_w_in, d_m_in), float64 numpy."""
+    the oracle's (dq, dk, dv, d_eta, d_beta, d_gamma, d_w_in, d_m_in, and with
+    the affine ln = (a, b) [H, d] also d_ln_a, d_ln_b summed over the batch),
+    float64 numpy."""
     B, H, T, d = np.asarray(x["q"]).shape
     resln = not (flags & 1)
+    if ln is not None:
+        ta = _t(ln[0], dtype, grad=True)
+        tb = _t(ln[1], dtype, grad=True)
     names = ("q", "k", "v", "eta", "beta", "gamma", "w_in", "m_in")
     gname = {"q": "dq", "k": "dk", "v": "dv", "eta": "d_eta", "beta": "d_beta",
              "gamma": "d_gamma", "w_in": "d_w_in", "m_in": "d_m_in"}
@@ -127,13 +137,17 @@ def backward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32):
                     leaf[n] = _t(x[n][b, h], dtype, grad=True)
             o, W, M = closed_form_unit(leaf["q"], leaf["k"], leaf["v"], leaf["eta"],
                                        leaf["beta"], leaf["gamma"], leaf["w_in"], leaf["m_in"],
-                                       C, d, dh, fw, resln, eps)
+                                       C, d, dh, fw, resln, eps,
+                                       None if ln is None else ta[h],
+                                       None if ln is None else tb[h])
             loss = (o * _t(x["d_out"][b, h], dtype)).sum()
             if x.get("d_w_out") is not None:
                 loss = loss + (W * _t(x["d_w_out"][b, h], dtype)).sum()
             if x.get("d_m_out") is not None:
                 loss = loss + (M * _t(x["d_m_out"][b, h], dtype)).sum()
             live = [n for n in names if leaf[n] is not None]
+            if ln is not None:
+                loss.backward(inputs=[ta, tb], retain_graph=True)
             grads = torch.autograd.grad(loss, [leaf[n] for n in live], allow_unused=True)
             for n, gr in zip(live, grads):
                 val = np.zeros(leaf[n].shape) if gr is None else gr.detach().double().numpy()
@@ -145,6 +159,9 @@ def backward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32):
             continue
         a = np.stack(res[n])
         out[n] = a.reshape((B, H) + a.shape[1:])
+    if ln is not None:
+        out["d_ln_a"] = ta.grad.double().numpy()
+        out["d_ln_b"] = tb.grad.double().numpy()
     return out
 
 

@@ -50,7 +50,8 @@ def test_sizes(lib):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(T=0), 2), (dict(B=-1), 2), (dict(chunk=0), 2), (dict(ln_eps=0.0), 2),
-    (dict(chunk=513), 3), (dict(fw=2), 3), (dict(io=7), 3), (dict(flags=4), 3),
+    (dict(chunk=513), 3), (dict(fw=2), 3), (dict(io=7), 3), (dict(flags=8), 3),
+    (dict(flags=5), 2),
     (dict(d=32), 3), (dict(d=16), 3), (dict(dh=300), 3), (dict(fw=1, dh=200), 3),
     (dict(io=0, d=64), 3), (dict(io=0, d=16, dh=200), 3)])
 def test_bad_descriptors(lib, kw, status):
@@ -110,6 +111,31 @@ def test_null_and_workspace_errors(lib):
     b = list(bargs)
     b[-2] = sc - 1
     assert lib.e2ttt_chunk_backward(ctypes.byref(d), *b) == 4
+
+
+def test_ln_affine_pointer_rules(lib):
+    # E2TTT_FLAG_LN_AFFINE (4): the *_ln entry points need ln_weight / ln_bias
+    # (and the backward their gradients); the plain ones have none to give;
+    # without the flag the affine pointers must be NULL; ln arrays 16-byte aligned
+    fake = ctypes.c_void_p(16)
+    da = desc(flags=4)
+    d0 = desc()
+    args = [fake] * 12
+    assert lib.e2ttt_chunk_forward(ctypes.byref(da), *args, 1 << 40, 0, None) == 1
+    assert lib.e2ttt_chunk_forward_ln(ctypes.byref(da), None, fake, *args, 1 << 40, 0, None) == 1
+    assert lib.e2ttt_chunk_forward_ln(ctypes.byref(d0), fake, fake, *args, 1 << 40, 0, None) == 2
+    assert lib.e2ttt_chunk_forward_ln(ctypes.byref(da), ctypes.c_void_p(20), fake, *args,
+                                      1 << 40, 0, None) == 2
+    def bargs(dlw, dlb):   # ..., d_m_in, d_ln_weight, d_ln_bias, scratch, scratch_bytes, stream
+        return [fake] * 9 + [1 << 40] + [fake] * 11 + [dlw, dlb, fake, 1 << 40, None]
+    assert lib.e2ttt_chunk_backward_ln(ctypes.byref(da), fake, fake, *bargs(None, fake)) == 1
+    assert lib.e2ttt_chunk_backward_ln(ctypes.byref(d0), None, None, *bargs(fake, None)) == 2
+    assert lib.e2ttt_apply_ln(ctypes.byref(da), fake, None, fake, fake, fake, None) == 1
+    assert lib.e2ttt_apply(ctypes.byref(da), fake, fake, fake, None) == 1
+    # the scratch of an affine backward also holds the written rows and partial sums
+    sa = lib.e2ttt_backward_scratch_bytes(ctypes.byref(da))
+    s0 = lib.e2ttt_backward_scratch_bytes(ctypes.byref(d0))
+    assert sa >= s0 + 2 * 4 * 2048 * 64 * 4
 
 
 def test_status_strings(lib):

@@ -50,3 +50,17 @@ def test_fp32_evaluation_is_fp32_accurate():
     fo = fp32ref.forward(x, C=w.C, fw=w.fw, dh=w.dh)
     errs = [rel_l2(a, b) for a, b in zip(fo, ro)]
     assert all(1e-9 < e < 1e-5 for e in errs), errs
+
+
+@pytest.mark.parametrize("fw", [WL.FW_MLP, WL.FW_SWIGLU])
+def test_fp64_closed_form_with_affine_equals_the_oracle(fw):
+    from tests.test_ln_affine_oracle import problem
+    x, ln, g = problem(2, 2, 9, 4, 6, fw, 21 + fw)
+    pair = (ln["ln_a"], ln["ln_b"])
+    for a, b in zip(fp32ref.forward(x, C=4, fw=fw, dh=6, dtype=torch.float64, ln=pair),
+                    oracle.forward(**x, C=4, fw=fw, dh=6, **ln)):
+        assert rel_l2(a, b) < 1e-12
+    ref = oracle.backward(**x, **g, C=4, fw=fw, dh=6, **ln)
+    got = fp32ref.backward(dict(x, **g), C=4, fw=fw, dh=6, dtype=torch.float64, ln=pair)
+    for n, r in ref.items():
+        assert rel_l2(got[n], r) < 1e-12, n
