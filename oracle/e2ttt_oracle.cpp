@@ -13,6 +13,12 @@
 //     Flag bit 0 drops "x + LN(.)" so that f(x) is the bare matrix net.
 //     Optionally a learnable per-head LayerNorm affine (flag bit 2):
 //     f(x) = x + a * LN(y) + b with a, b in R^d, slow weights of the head.
+//   * Optionally (flag bit 3) the post-chunk L2 normalisation of the fast
+//     weights (App. B.1, after Zhang et al.): at every chunk end each row of
+//     each fast-weight matrix, taken over the matrix's input dimension, is
+//     rescaled to the norm that row has in the unit's initial weights w_in;
+//     the momentum is left as it is.  A row of norm zero is left as it is;
+//     a row whose target is zero becomes zero.
 //   * Inner loss L_t = 1/2 ||f_W(k_t) - v_t||^2 (Sec. 2, eq. (1); the paper
 //     names MSE without a constant, see the readings list in the design notes).
 //   * Per-token recurrence with gradients frozen at the chunk-start weights
@@ -212,8 +218,61 @@ void loss_grad(const Net& n, const T* W, const T* k, const T* v, T* gW, T* gk, T
 struct Problem {
   int B, H, T, C;
   Net net;
+  bool post_norm = false;   // L2-normalise the fast-weight rows at every chunk end
   long units() const { return (long)B * H; }
 };
+
+// Rows of the fast-weight matrices for the post-chunk normalisation: row r of
+// a matrix laid out [rows][cols] with the input index as the column (W x rule):
+// MLP W1 [dh][d], W2 [d][dh]; SwiGLU Wg, Wu [dh][d], Wd [d][dh].  Calls
+// f(offset of the row's first element, number of columns) for every row.
+template <class F>
+void for_each_row(const Net& n, F f) {
+  const int nmat = n.fw == 0 ? 2 : 3;
+  long off = 0;
+  for (int m = 0; m < nmat; ++m) {
+    const bool second = (m == nmat - 1);
+    const int rows = second ? n.d : n.dh, cols = second ? n.dh : n.d;
+    for (int r = 0; r < rows; ++r) f(off + (long)r * cols, cols);
+    off += (long)rows * cols;
+  }
+}
+
+double row_norm(const double* x, int cols) {
+  double s = 0.0;
+  for (int c = 0; c < cols; ++c) s += x[c] * x[c];
+  return std::sqrt(s);
+}
+
+// W <- every row rescaled from its norm to the norm of the same row of W_init.
+void post_chunk_normalise(const Net& n, const double* w_init, double* W) {
+  for_each_row(n, [&](long off, int cols) {
+    const double nr = row_norm(W + off, cols);
+    if (nr == 0.0) return;
+    const double s = row_norm(w_init + off, cols) / nr;
+    for (int c = 0; c < cols; ++c) W[off + c] *= s;
+  });
+}
+
+// Reverse of post_chunk_normalise at the pre-normalisation weights Wpre:
+// Wbar (the adjoint of the normalised rows) becomes the adjoint of Wpre, and
+// w_init_bar receives what flows into the targets (norm of w_init's rows):
+// with u = Wpre_r / |Wpre_r| and t_r = |w_init_r|, the normalised row is t_r u,
+// so  Wpre_r_bar = (t_r / |Wpre_r|) (Wbar_r - u <u, Wbar_r>)  and
+// w_init_r_bar += <u, Wbar_r> w_init_r / t_r.
+void post_chunk_normalise_bwd(const Net& n, const double* w_init, const double* Wpre, double* Wbar,
+                              double* w_init_bar) {
+  for_each_row(n, [&](long off, int cols) {
+    const double nr = row_norm(Wpre + off, cols);
+    if (nr == 0.0) return;                      // left as it was: identity
+    const double t = row_norm(w_init + off, cols);
+    double dot = 0.0;
+    for (int c = 0; c < cols; ++c) dot += Wpre[off + c] / nr * Wbar[off + c];
+    for (int c = 0; c < cols; ++c) Wbar[off + c] = t / nr * (Wbar[off + c] - Wpre[off + c] / nr * dot);
+    if (t > 0.0)
+      for (int c = 0; c < cols; ++c) w_init_bar[off + c] += dot * w_init[off + c] / t;
+  });
+}
 
 // Per-unit forward; optionally records the chunk-start states for the backward.
 void unit_forward(const Problem& pb, const double* q, const double* k, const double* v,
@@ -243,6 +302,7 @@ void unit_forward(const Problem& pb, const double* q, const double* k, const dou
         W[p] = g * W[p] + M[p];
       }
     }
+    if (pb.post_norm) post_chunk_normalise(n, w_in, W.data());
   }
   std::memcpy(w_out, W.data(), sizeof(double) * P);
   std::memcpy(m_out, M.data(), sizeof(double) * P);
@@ -273,7 +333,7 @@ void unit_backward(const Problem& pb, const double* q, const double* k, const do
   std::vector<double> Ws, Ms, Gs;        // token states W_t, M_t (t = 0..len) and G_t
   std::vector<double> gk(d), gv(d), fb(d), xb(d);
   std::vector<Dual> Wd(P), gWd(P), kd(d), vd(d), gkd(d), gvd(d), gad(d), gbd(d);
-  std::vector<double> Gbar;
+  std::vector<double> Gbar, winit_bar(P, 0.0);
   for (int c = NC - 1; c >= 0; --c) {
     const int s0 = c * C;
     const int len = (T - s0 < C) ? T - s0 : C;
@@ -300,6 +360,11 @@ void unit_backward(const Problem& pb, const double* q, const double* k, const do
         Wn[p] = g * Wp[p] + Mn[p];
       }
     }
+    // the chunk end was normalised: Wbar is the adjoint of the normalised
+    // weights, turned into that of the token loop's last state
+    if (pb.post_norm)
+      post_chunk_normalise_bwd(n, w_in, Ws.data() + (size_t)len * P, Wbar.data(),
+                               winit_bar.data());
     // reverse through the token loop
     Gbar.assign((size_t)len * P, 0.0);
     for (int i = len - 1; i >= 0; --i) {
@@ -350,6 +415,7 @@ void unit_backward(const Problem& pb, const double* q, const double* k, const do
     }
     for (long p = 0; p < P; ++p) Wbar[p] += Wob[p];
   }
+  for (long p = 0; p < P; ++p) Wbar[p] += winit_bar[p];   // w_in also sets the targets
   std::memcpy(d_w_in, Wbar.data(), sizeof(double) * P);
   std::memcpy(d_m_in, Mbar.data(), sizeof(double) * P);
 }
@@ -361,6 +427,7 @@ bool make_problem(Problem& pb, int B, int H, int T, int d, int dh, int C, int fw
   pb.net.d = d; pb.net.dh = dh; pb.net.fw = fw;
   pb.net.resln = (flags & 1) == 0;
   pb.net.eps = eps;
+  pb.post_norm = (flags & 8) != 0;
   return true;
 }
 

@@ -26,6 +26,7 @@ _LIB = os.path.join(_HERE, "libe2ttt_oracle.so")
 FW_MLP = 0
 FW_SWIGLU = 1
 FLAG_NO_RESIDUAL_LN = 1
+FLAG_POST_NORM = 8        # post-chunk L2 normalisation of the fast-weight rows
 
 _lib = None
 

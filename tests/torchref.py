@@ -39,10 +39,24 @@ def neg_grad(W, k, v, d, dh, fw, resln=True, eps=1e-5, create_graph=False):
     return -g
 
 
+def row_normalise(W, W_init, d, dh, fw):
+    """Every row of every matrix (over its input dimension) rescaled to the
+    norm of the same row of W_init, via torch.linalg.vector_norm (rows of norm
+    zero are left as they are)."""
+    out = []
+    for Wm, Im in zip(split(W, d, dh, fw), split(W_init, d, dh, fw)):
+        n = torch.linalg.vector_norm(Wm, dim=1, keepdim=True)
+        t = torch.linalg.vector_norm(Im, dim=1, keepdim=True)
+        safe = torch.where(n > 0, n, torch.ones_like(n))
+        out.append(torch.where(n > 0, Wm * (t / safe), Wm).reshape(-1))
+    return torch.cat(out)
+
+
 def chunked_forward(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=True, eps=1e-5,
-                    ln_a=None, ln_b=None):
+                    ln_a=None, ln_b=None, post_norm=False):
     """One unit: token recurrence with gradients at chunk-start weights
-    (paper eq. (7)), outputs f_{W_0}(q_t); differentiable end to end."""
+    (paper eq. (7)), outputs f_{W_0}(q_t); differentiable end to end.
+    post_norm: rows renormalised to w_in's row norms at every chunk end."""
     T = q.shape[0]
     W = w_in
     M = m_in if m_in is not None else torch.zeros_like(w_in)
@@ -58,4 +72,6 @@ def chunked_forward(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=T
             M = beta[t] * M + eta[t] * (-g)
             g_t = gamma[t] if gamma is not None else 1.0
             W = g_t * W + M
+        if post_norm:
+            W = row_normalise(W, w_in, d, dh, fw)
     return torch.stack(outs), W, M
