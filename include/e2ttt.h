@@ -113,6 +113,17 @@ typedef enum { E2TTT_DT_F32 = 0, E2TTT_DT_BF16 = 1 } e2ttt_dtype;
  * *_ln entry points below; the plain entry points return E2TTT_ERR_NULL_ARG
  * for it.  Not combinable with E2TTT_FLAG_NO_RESIDUAL_LN (E2TTT_ERR_BAD_SHAPE). */
 #define E2TTT_FLAG_LN_AFFINE 0x4u
+/* Post-chunk L2 normalisation of the fast weights (App. B.1, after LaCT): at
+ * every chunk end, after the update of Prop. 1, each row of each fast-weight
+ * matrix, taken over the matrix's input dimension (W1 / Wg / Wu: a hidden
+ * unit's d weights; W2 / Wd: an output's dh weights), is rescaled to the norm
+ * of the same row of the unit's initial weights w_in; a row of norm zero is
+ * left as it is, the momentum is not normalised.  Chunk-start states, outputs
+ * and w_out are then those of the normalised weights; the backward includes
+ * the normalisation and its targets' dependence on w_in.  (The paper gives no
+ * axis or target; this is the reading taken.  Off by default: with it the
+ * closed form no longer equals the plain token recurrence.) */
+#define E2TTT_FLAG_POST_NORM 0x8u
 
 typedef struct {
   int32_t B, H, T;      /* batch, heads, tokens                        */

@@ -37,6 +37,11 @@ struct Plan {
   size_t off_kw = 0, off_km = 0, off_carry = 0, off_sync = 0, off_xbuf = 0, off_w0 = 0;
   size_t ws_bytes = 0;
   size_t off_ckpt = 0, off_zk = 0, off_rk = 0, off_zq = 0, off_rq = 0, ws_bytes_save = 0;
+  // post-chunk normalisation: targets and exchange (forward), norms before it (saving)
+  size_t off_ntgt = 0, off_nx = 0, off_npre = 0;
+  long nrows = 0, ckpt_nc = 0;
+  bool post_norm = false;
+  bool w0b = false;       // the forward keeps W_0 per workgroup (long chunks re-forming operands)
   long ckpt_stride = 0;
   size_t off_as = 0;
   long as_stride = 0;
@@ -44,6 +49,7 @@ struct Plan {
   // backward scratch
   size_t off_kwb = 0, off_kmb = 0, off_carryb = 0, off_bsync = 0, off_bxbuf = 0, off_frz = 0;
   size_t off_zbar = 0, off_apart = 0;   // LayerNorm affine: written rows and partial sums
+  size_t off_rbar = 0, off_bnx = 0;      // post-chunk normalisation (backward)
   size_t scratch_bytes = 0;
   bool affine = false;
 };
@@ -97,7 +103,8 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
     return E2TTT_ERR_BAD_SHAPE;
   if (d.fw != E2TTT_FW_GELU_MLP && d.fw != E2TTT_FW_SWIGLU) return E2TTT_ERR_UNSUPPORTED;
   if (d.io != E2TTT_DT_F32 && d.io != E2TTT_DT_BF16) return E2TTT_ERR_UNSUPPORTED;
-  if (d.flags & ~(E2TTT_FLAG_NO_RESIDUAL_LN | E2TTT_FLAG_CHUNK_AVERAGED | E2TTT_FLAG_LN_AFFINE))
+  if (d.flags & ~(E2TTT_FLAG_NO_RESIDUAL_LN | E2TTT_FLAG_CHUNK_AVERAGED | E2TTT_FLAG_LN_AFFINE |
+                  E2TTT_FLAG_POST_NORM))
     return E2TTT_ERR_UNSUPPORTED;
   if (!(d.flags & E2TTT_FLAG_NO_RESIDUAL_LN) && !(d.ln_eps > 0.0f)) return E2TTT_ERR_BAD_SHAPE;
   // the affine belongs to the LayerNorm of the residual form
@@ -108,6 +115,7 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   if (U > INT_MAX || (long)d.T * d.d > (1L << 40) / U) return E2TTT_ERR_UNSUPPORTED;
   e2ttt_status st = select_config(d, pl.cfg);
   if (st != E2TTT_OK) return st;
+  pl.cfg.pn = (d.flags & E2TTT_FLAG_POST_NORM) ? 1 : 0;
   pl.U = U;
   pl.T = d.T;
   pl.NC = (d.T + d.chunk - 1) / d.chunk;
@@ -129,13 +137,24 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
               align_up((size_t)pl.npairs * ns * chain_xchg_floats(pl.cfg, false) * sizeof(float));
   // long chunks on bf16 whose products re-form W_0's operands from the state
   // (SwiGLU, and the MLP at head dim 128): the forward's per-workgroup copy of W_0
-  const bool w0b = pl.tpc > 1 && pl.cfg.bf && (pl.cfg.fw == E2TTT_FW_SWIGLU || d.d > 64);
+  pl.w0b = pl.tpc > 1 && pl.cfg.bf && (pl.cfg.fw == E2TTT_FW_SWIGLU || d.d > 64);
   pl.off_ckpt =
-      pl.off_w0 + (w0b ? align_up((size_t)nwg * chain_frz_floats(pl.cfg) * sizeof(float)) : 0);
+      pl.off_w0 + (pl.w0b ? align_up((size_t)nwg * chain_frz_floats(pl.cfg) * sizeof(float)) : 0);
+  pl.post_norm = (d.flags & E2TTT_FLAG_POST_NORM) != 0;
+  pl.nrows = (d.fw == E2TTT_FW_GELU_MLP ? 1L : 2L) * d.dh + d.d;
+  const size_t ngroups = (size_t)std::max(pl.npairs, 1L);
+  pl.off_ntgt = pl.off_ckpt;
+  pl.off_nx = pl.off_ntgt + (pl.post_norm ? align_up((size_t)U * pl.nrows * sizeof(float)) : 0);
+  pl.off_ckpt = pl.off_nx +
+                (pl.post_norm ? align_up(ngroups * ns * 2 * d.d * sizeof(float)) : 0);
   pl.ws_bytes = pl.off_ckpt;
   pl.ckpt_stride = chain_ckpt_bytes(pl.cfg);
+  // with the normalisation the backward also reads the final state (one more block)
+  pl.ckpt_nc = pl.NC + (pl.post_norm ? 1 : 0);
   const size_t tokd = tok * d.d;
-  pl.off_zk = pl.off_ckpt + align_up((size_t)U * pl.NC * ns * 2 * pl.ckpt_stride);
+  pl.off_npre = pl.off_ckpt + align_up((size_t)U * pl.ckpt_nc * ns * 2 * pl.ckpt_stride);
+  pl.off_zk = pl.off_npre +
+              (pl.post_norm ? align_up((size_t)U * pl.NC * pl.nrows * sizeof(float)) : 0);
   pl.off_rk = pl.off_zk + align_up(tokd);
   pl.off_zq = pl.off_rk + align_up(tok);
   pl.off_rq = pl.off_zq + align_up(tokd);
@@ -156,8 +175,12 @@ e2ttt_status make_plan(const e2ttt_desc* desc, Plan& pl) {
   pl.affine = (d.flags & E2TTT_FLAG_LN_AFFINE) != 0;
   pl.off_apart = pl.off_zbar + (pl.affine ? align_up(tokd) : 0);
   const long nb = (d.T + kAffineTokBlock - 1) / kAffineTokBlock;
-  pl.scratch_bytes =
+  pl.off_rbar =
       pl.off_apart + (pl.affine ? align_up((size_t)U * nb * 2 * d.d * sizeof(float)) : 0);
+  // one copy per rank (each accumulates its own rows)
+  pl.off_bnx = pl.off_rbar + (pl.post_norm ? align_up((size_t)U * ns * pl.nrows * sizeof(float)) : 0);
+  pl.scratch_bytes =
+      pl.off_bnx + (pl.post_norm ? align_up(ngroups * ns * 2 * d.d * sizeof(float)) : 0);
   return E2TTT_OK;
 }
 
@@ -375,6 +398,11 @@ e2ttt_status e2ttt_chunk_forward_ln(const e2ttt_desc* desc, const float* ln_weig
                  pl.U * pl.NC, sync, sync ? sync_words(np, pl.cfg.ns) : 0, averaged(desc)};
   hipError_t e = launch_coeff_fwd(c, s);
   if (e != hipSuccess) return E2TTT_ERR_HIP;
+  if (pl.post_norm) {
+    e = launch_norm_targets(w_in, at<float>(workspace, pl.off_ntgt), pl.U, desc->d, desc->dh,
+                            pl.cfg.fw == E2TTT_FW_GELU_MLP ? 2 : 3, pl.P, s);
+    if (e != hipSuccess) return E2TTT_ERR_HIP;
+  }
   ChainArgs a{};
   a.U = pl.U;
   a.q = q; a.k = k; a.v = v;
@@ -392,7 +420,7 @@ e2ttt_status e2ttt_chunk_forward_ln(const e2ttt_desc* desc, const float* ln_weig
     a.rq = at<float>(workspace, pl.off_rq);
   }
   a.xbuf = at<float>(workspace, pl.off_xbuf);
-  a.w0blk = pl.off_ckpt > pl.off_w0 ? at<float>(workspace, pl.off_w0) : nullptr;
+  a.w0blk = pl.w0b ? at<float>(workspace, pl.off_w0) : nullptr;
   a.sync = sync;
   a.npairs = np;
   a.wait_ticks = wait_ticks();
@@ -402,6 +430,12 @@ e2ttt_status e2ttt_chunk_forward_ln(const e2ttt_desc* desc, const float* ln_weig
   a.ln_a = ln_weight;
   a.ln_b = ln_bias;
   a.H = desc->H;
+  a.ckpt_nc = pl.ckpt_nc;
+  if (pl.post_norm) {
+    a.norm_tgt = at<float>(workspace, pl.off_ntgt);
+    a.nxbuf = at<float>(workspace, pl.off_nx);
+    a.norm_pre = save_for_backward ? at<float>(workspace, pl.off_npre) : nullptr;
+  }
   return finish(launch_chain_fwd(pl.cfg, a, s), s, sync);
 }
 
@@ -482,6 +516,13 @@ e2ttt_status e2ttt_chunk_backward_ln(const e2ttt_desc* desc, const float* ln_wei
   a.ln_b = ln_bias;
   a.H = desc->H;
   a.ln_zbar = pl.affine ? at<float>(scratch, pl.off_zbar) : nullptr;
+  a.ckpt_nc = pl.ckpt_nc;
+  if (pl.post_norm) {
+    a.norm_tgt = at<float>(workspace, pl.off_ntgt);
+    a.norm_pre = const_cast<float*>(at<float>(workspace, pl.off_npre));
+    a.norm_rbar = at<float>(scratch, pl.off_rbar);
+    a.nxbuf = at<float>(scratch, pl.off_bnx);
+  }
   hipError_t e = launch_chain_bwd(pl.cfg, a, s);
   if (e != hipSuccess) return E2TTT_ERR_HIP;
   CoeffBwdArgs cb{eta, beta, gamma, a.kwb, a.kmb, a.carryb, d_eta, d_beta, d_gamma,

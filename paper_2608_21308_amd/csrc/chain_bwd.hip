@@ -29,6 +29,18 @@
 #include "chain_common.h"
 #include "pair_xchg.h"
 
+// The instantiations with the post-chunk normalisation of the fast weights are
+// compiled in a translation unit of their own (chain_bwd_pn.hip defines this
+// as 1 and includes this file), in parallel with the plain ones.
+#ifndef E2TTT_CHAIN_PN
+#define E2TTT_CHAIN_PN 0
+#endif
+#if E2TTT_CHAIN_PN
+#define E2TTT_PN_NAME(f) f##_pn
+#else
+#define E2TTT_PN_NAME(f) f
+#endif
+
 namespace e2ttt {
 
 namespace {
@@ -351,7 +363,7 @@ __device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int le
 // Wb is reset to Wb_C; after the chunk's last processed tile (its first) the
 // transition Wb_0 = cw Wb_C + sum of contributions, Mb_0 = cm Wb_C + cb Mb_C
 // is applied once.
-template <class S, bool LONG>
+template <class S, bool LONG, bool PN>
 __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   using O = typename S::O;
   using E = typename S::E;
@@ -463,9 +475,121 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       else if (--r >= 0) kt = ntiles(r) - 1;
       const long row0 = u * T + s0;
       const int par = (int)(nch & 1);
+
+      // ---- reverse of the post-chunk normalisation at this chunk's end (the
+      // chunk's first tile processed).  The normalised row is W_r = t_r u_r
+      // (t_r its target norm, n_r its norm before, u_r the unit direction),
+      // so Wb_r, the adjoint of W_r, becomes that of the row before:
+      //   Wb_r <- (t_r / n_r) Wb_r - (W_r / n_r) (A_r / t_r),  A_r = <W_r, Wb_r>,
+      // and <u_r, Wb_r> = A_r / t_r is what flows into t_r (summed over the
+      // chunks, and applied to d_w_in at the unit's end).  W_r is the next
+      // chunk's checkpoint (the final state's for the last chunk).  A row the
+      // forward left alone (n_r = 0) keeps its adjoint; one sent to zero
+      // (t_r = 0) gets none.
+      if (PN && firstp) {
+        E2TTT_LANE_IDS;
+        const long R = (long)NF * dh + D;
+        const float* tg = E2TTT_ARG(norm_tgt) + u * R;
+        const float* npre = E2TTT_ARG(norm_pre) + (u * NC + rc) * R;
+        float* rbar = E2TTT_ARG(norm_rbar) + (u * S::NS + rank) * R;
+        const bool init = rc == NC - 1;
+        const char* ckN = static_cast<const char*>(E2TTT_ARG(ckpt)) +
+                          ((u * E2TTT_ARG(ckpt_nc) + rc + 1) * S::NS + rank) * 2 *
+                              E2TTT_ARG(ckpt_stride);
+        // first-layer rows: hidden unit j is the tile column of lanes c + 16 g
+#pragma unroll
+        for (int m = 0; m < NF; ++m) {
+          Q wn[NJB][NIB];
+          load_ckpt_mat<S>(wn, ckN, m, w, lane);
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            float A = 0.0f;
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+              const f32x4 x = quad_f32(wn[jj][ib]);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) A = fmaf(x[q], Wb.t[m][jj][ib][q], A);
+            }
+            A += __shfl_xor(A, 16);
+            A += __shfl_xor(A, 32);
+            const int j = j0 + 16 * (w * NJB + jj) + c;
+            float s1 = 1.0f, s2 = 0.0f, dot = 0.0f;
+            if (j < dh) {
+              const float t = tg[(long)m * dh + j], n = npre[(long)m * dh + j];
+              if (n > 0.0f) {
+                s1 = t / n;
+                if (t > 0.0f) { dot = A / t; s2 = dot / n; }
+              }
+              if (g == 0) rbar[(long)m * dh + j] = init ? dot : rbar[(long)m * dh + j] + dot;
+            }
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib)
+              Wb.t[m][jj][ib] = s1 * Wb.t[m][jj][ib] - s2 * quad_f32(wn[jj][ib]);
+          }
+        }
+        // second-layer rows: output i's weights span the lanes, the waves and
+        // the ranks; partial sums through LDS (Y's buffer, not yet staged)
+        // and, between ranks, the exchange, added in rank order on every rank
+        static_assert(S::CM >= NW + 2, "LDS room for the row sums");
+        float* part = yk;   // [NW][D] wave partials, then [2][D] row factors
+        Q wn[NJB][NIB];
+        load_ckpt_mat<S>(wn, ckN, SEC, w, lane);
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+          float A[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            const f32x4 x = quad_f32(wn[jj][ib]);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) A[q] = fmaf(x[q], Wb.t[SEC][jj][ib][q], A[q]);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float v = group16_sum(A[q]);
+            if (c == 0) part[w * D + 16 * ib + 4 * g + q] = v;
+          }
+        }
+        __syncthreads();
+        float A = 0.0f;
+        if (tid < D)
+          for (int ww = 0; ww < NW; ++ww) A += part[ww * D + tid];
+        if constexpr (S::NS > 1) {
+          float* nx = E2TTT_ARG(nxbuf);
+          if (tid < D) nx[((px.xs * S::NS + rank) * 2 + par) * D + tid] = A;
+          px.post();
+          px.wait_for(px.seq_now(), sword);
+          if (tid < D) {
+            A = 0.0f;
+            for (int rr = 0; rr < S::NS; ++rr) A += nx[((px.xs * S::NS + rr) * 2 + par) * D + tid];
+          }
+        }
+        if (tid < D) {
+          const float t = tg[(long)NF * dh + tid], n = npre[(long)NF * dh + tid];
+          float s1 = 1.0f, s2 = 0.0f, dot = 0.0f;
+          if (n > 0.0f) {
+            s1 = t / n;
+            if (t > 0.0f) { dot = A / t; s2 = dot / n; }
+          }
+          part[NW * D + tid] = s1;
+          part[(NW + 1) * D + tid] = s2;
+          rbar[(long)NF * dh + tid] = init ? dot : rbar[(long)NF * dh + tid] + dot;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+          const f32x4 s1 = *reinterpret_cast<const f32x4*>(&part[NW * D + 16 * ib + 4 * g]);
+          const f32x4 s2 = *reinterpret_cast<const f32x4*>(&part[(NW + 1) * D + 16 * ib + 4 * g]);
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj)
+            Wb.t[SEC][jj][ib] = s1 * Wb.t[SEC][jj][ib] - s2 * quad_f32(wn[jj][ib]);
+        }
+        __syncthreads();   // part (Y's buffer) is staged next
+      }
+
+      // the exchange sequence of this tile starts after the normalisation's
       const unsigned seq0 = px.seq_now();
       const char* ckW = static_cast<const char*>(E2TTT_ARG(ckpt)) +
-                        ((u * NC + rc) * S::NS + rank) * 2 * E2TTT_ARG(ckpt_stride);
+                        ((u * E2TTT_ARG(ckpt_nc) + rc) * S::NS + rank) * 2 * E2TTT_ARG(ckpt_stride);
       const char* ckM = ckW + E2TTT_ARG(ckpt_stride);
 
       // chunk-start weights W_0 (kept for the whole chunk) and momentum M_0
@@ -1240,6 +1364,44 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         flush_dkdq<S>(px.xs, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       __syncthreads();
     }
+    // w_in also sets the targets t_r = |w_in,r|: d_w_in,r += (sum over the
+    // chunks of A_r / t_r) w_in,r / t_r
+    if (PN) {
+      E2TTT_LANE_IDS;
+      const long R = (long)NF * dh + D;
+      const float* tg = E2TTT_ARG(norm_tgt) + u * R;
+      const float* rbar = E2TTT_ARG(norm_rbar) + (u * S::NS + rank) * R;
+      // the second-layer factors through LDS (each was written by thread tid)
+      if (tid < D) {
+        const float t = tg[(long)NF * dh + tid];
+        yk[tid] = t > 0.0f ? rbar[(long)NF * dh + tid] / t : 0.0f;
+      }
+      __syncthreads();
+      StateTiles<S> X;
+      load_state<S>(X, E2TTT_ARG(w_in) + u * a.P, dh, j0, w, g, c);
+#pragma unroll
+      for (int m = 0; m < NF; ++m)
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj) {
+          // the factor of column j, read by the lane that wrote it (g = 0, lane c)
+          const int j = j0 + 16 * (w * NJB + jj) + c;
+          float f = 0.0f;
+          if (g == 0 && j < dh) {
+            const float t = tg[(long)m * dh + j];
+            f = t > 0.0f ? rbar[(long)m * dh + j] / t : 0.0f;
+          }
+          f = __shfl(f, c);
+#pragma unroll
+          for (int ib = 0; ib < NIB; ++ib) Wb.t[m][jj][ib] += f * X.t[m][jj][ib];
+        }
+#pragma unroll
+      for (int ib = 0; ib < NIB; ++ib) {
+        const f32x4 f = *reinterpret_cast<const f32x4*>(&yk[16 * ib + 4 * g]);
+#pragma unroll
+        for (int jj = 0; jj < NJB; ++jj) Wb.t[SEC][jj][ib] += f * X.t[SEC][jj][ib];
+      }
+      __syncthreads();   // yk is staged by the next unit
+    }
     {
       E2TTT_LANE_IDS;
       store_state<S>(Wb, E2TTT_ARG(d_w_in) + u * a.P, dh, j0, w, g, c);
@@ -1248,10 +1410,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   }
 }
 
-template <class S, bool LONG>
+template <class S, bool LONG, bool PN>
 int occupancy() {
   int v = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_bwd_kernel<S, LONG>, S::NT, 0) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_bwd_kernel<S, LONG, PN>, S::NT, 0) !=
       hipSuccess)
     v = 0;
   return v;
@@ -1260,22 +1422,23 @@ int occupancy() {
 template <class S>
 int max_blocks_per_cu() {
   static int nb = [] {
-    // one launch geometry serves both instantiations
-    return std::min(occupancy<S, false>(), occupancy<S, true>());
+    // one launch geometry serves both chunk-length instantiations
+    constexpr bool PN = E2TTT_CHAIN_PN;
+    return std::min(occupancy<S, false, PN>(), occupancy<S, true, PN>());
   }();
   return nb;
 }
 
-template <class S, bool LONG>
+template <class S, bool LONG, bool PN>
 hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
   if constexpr (S::NS == 1) {
-    hipLaunchKernelGGL((chain_bwd_kernel<S, LONG>), dim3((unsigned)a.U), dim3(S::NT), 0, stream,
+    hipLaunchKernelGGL((chain_bwd_kernel<S, LONG, PN>), dim3((unsigned)a.U), dim3(S::NT), 0, stream,
                        a);
     return hipGetLastError();
   } else {
     ChainArgs b = a;
     void* args[] = {&b};
-    return hipLaunchCooperativeKernel((const void*)chain_bwd_kernel<S, LONG>,
+    return hipLaunchCooperativeKernel((const void*)chain_bwd_kernel<S, LONG, PN>,
                                       dim3((unsigned)(S::NS * a.npairs)), dim3(S::NT), args, 0,
                                       stream);
   }
@@ -1283,9 +1446,13 @@ hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
 
 template <class S>
 hipError_t launch(const ChainArgs& a, hipStream_t stream) {
-  if (a.C <= S::CM) return launch_as<S, false>(a, stream);
+  // the post-chunk normalisation is a separate instantiation, so that the
+  // kernels without it carry none of its registers
+  constexpr bool PN = E2TTT_CHAIN_PN;
+  if ((a.norm_tgt != nullptr) != PN) return hipErrorInvalidValue;
+  if (a.C <= S::CM) return launch_as<S, false, PN>(a, stream);
   if (!a.bfrz) return hipErrorInvalidValue;
-  return launch_as<S, true>(a, stream);
+  return launch_as<S, true, PN>(a, stream);
 }
 
 }  // namespace
@@ -1295,7 +1462,11 @@ hipError_t launch(const ChainArgs& a, hipStream_t stream) {
       cfg.bf == BF && cfg.ns == NS)                                                     \
     return launch<Shape<FW, D, NW, NJB, NTB, BF, NS>>(a, stream);
 
-hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream) {
+hipError_t E2TTT_PN_NAME(launch_chain_bwd)(const ChainConfig& cfg, const ChainArgs& a,
+                                      hipStream_t stream) {
+#if !E2TTT_CHAIN_PN
+  if (cfg.pn) return launch_chain_bwd_pn(cfg, a, stream);
+#endif
 #include "chain_variants.inc"
   return hipErrorInvalidValue;
 }
@@ -1306,7 +1477,10 @@ hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, hipStrea
       cfg.bf == BF && cfg.ns == NS)                                                     \
     return max_blocks_per_cu<Shape<FW, D, NW, NJB, NTB, BF, NS>>();
 
-int chain_bwd_blocks_per_cu(const ChainConfig& cfg) {
+int E2TTT_PN_NAME(chain_bwd_blocks_per_cu)(const ChainConfig& cfg) {
+#if !E2TTT_CHAIN_PN
+  if (cfg.pn) return chain_bwd_blocks_per_cu_pn(cfg);
+#endif
 #include "chain_variants.inc"
   return 0;
 }

@@ -29,6 +29,18 @@
 #include "chain_common.h"
 #include "pair_xchg.h"
 
+// The instantiations with the post-chunk normalisation of the fast weights are
+// compiled in a translation unit of their own (chain_fwd_pn.hip defines this
+// as 1 and includes this file), in parallel with the plain ones.
+#ifndef E2TTT_CHAIN_PN
+#define E2TTT_CHAIN_PN 0
+#endif
+#if E2TTT_CHAIN_PN
+#define E2TTT_PN_NAME(f) f##_pn
+#else
+#define E2TTT_PN_NAME(f) f
+#endif
+
 namespace e2ttt {
 
 namespace {
@@ -73,7 +85,7 @@ __device__ __forceinline__ float* fwd_slot(float* xbuf, long p, int rank, int pa
 
 // LONG: chunks longer than the CM-row tile (a separate instantiation, so that
 // the common case keeps W_0's operand copies dead between chunks).
-template <class S, bool LONG>
+template <class S, bool LONG, bool PN>
 __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   using O = typename S::O;
   using IO = IoT<S::BF>;
@@ -214,7 +226,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       }
       if (E2TTT_ARG(ckpt)) {
         char* cb = static_cast<char*>(E2TTT_ARG(ckpt)) +
-                   ((u * NC + rc) * S::NS + rank) * 2 * E2TTT_ARG(ckpt_stride);
+                   ((u * E2TTT_ARG(ckpt_nc) + rc) * S::NS + rank) * 2 * E2TTT_ARG(ckpt_stride);
         if constexpr (PRESPLIT) store_ckpt_q<S>(WS.hi, cb, w, lane);
         else store_ckpt<S>(W, cb, w, lane);
         store_ckpt<S>(M, cb + E2TTT_ARG(ckpt_stride), w, lane);
@@ -645,6 +657,77 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             }
       }
 
+      // ------------- post-chunk normalisation of the fast-weight rows (chunk end)
+      if (PN && !more) {
+        E2TTT_LANE_IDS;
+        constexpr int NF = NMAT - 1;
+        const long R = (long)NF * dh + D;
+        const float* tg = E2TTT_ARG(norm_tgt) + u * R;
+        float* npre = E2TTT_ARG(norm_pre) ? E2TTT_ARG(norm_pre) + (u * NC + rc) * R : nullptr;
+        // first-layer rows: hidden unit j's d weights are the tile column of
+        // lanes c, c + 16, c + 32, c + 48
+#pragma unroll
+        for (int m = 0; m < NF; ++m)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            float s2 = 0.0f;
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) s2 = fmaf(W.t[m][jj][ib][r], W.t[m][jj][ib][r], s2);
+            s2 += __shfl_xor(s2, 16);
+            s2 += __shfl_xor(s2, 32);
+            const int j = j0 + 16 * (w * NJB + jj) + c;
+            const float sc = (j < dh && s2 > 0.0f) ? tg[(long)m * dh + j] * rsq_f(s2) : 1.0f;
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) W.t[m][jj][ib] *= sc;
+            if (npre && g == 0 && j < dh) npre[(long)m * dh + j] = __builtin_sqrtf(s2);
+          }
+        // second-layer rows: output i's dh weights span the lanes, the waves and
+        // the ranks; partial sums through LDS (the Y_K buffer, free here) and,
+        // between ranks, the exchange, added in rank order on every rank
+        static_assert(S::CM >= S::NW + 1, "LDS room for the row sums");
+        float* part = sm.y;   // [NW][D] wave partials, then [D] scales
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float s2 = 0.0f;
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj)
+              s2 = fmaf(W.t[SEC][jj][ib][r], W.t[SEC][jj][ib][r], s2);
+            s2 = group16_sum(s2);
+            if (c == 0) part[w * D + 16 * ib + 4 * g + r] = s2;
+          }
+        __syncthreads();
+        float tot = 0.0f;
+        if (tid < D)
+          for (int ww = 0; ww < S::NW; ++ww) tot += part[ww * D + tid];
+        if constexpr (S::NS > 1) {
+          float* nx = E2TTT_ARG(nxbuf);
+          if (tid < D) nx[((px.xs * S::NS + rank) * 2 + par) * D + tid] = tot;
+          px.post();
+          px.wait_for(px.seq_now(), sm.word);
+          if (tid < D) {
+            tot = 0.0f;
+            for (int rr = 0; rr < S::NS; ++rr) tot += nx[((px.xs * S::NS + rr) * 2 + par) * D + tid];
+          }
+        }
+        if (tid < D) {
+          part[S::NW * D + tid] = tot > 0.0f ? tg[(long)NF * dh + tid] * rsq_f(tot) : 1.0f;
+          if (npre && rank == 0) npre[(long)NF * dh + tid] = __builtin_sqrtf(tot);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float sc = part[S::NW * D + 16 * ib + 4 * g + r];
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj) W.t[SEC][jj][ib][r] *= sc;
+          }
+      }
+
       // ------------------------------------------------- outputs (a7)
       {
         E2TTT_LANE_IDS;
@@ -720,16 +803,22 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
     {
       E2TTT_LANE_IDS;
+      // with the normalisation the backward also needs the final (normalised)
+      // weights: one more checkpoint block, W only
+      if (PN && E2TTT_ARG(ckpt))
+        store_ckpt<S>(W, static_cast<char*>(E2TTT_ARG(ckpt)) +
+                             ((u * E2TTT_ARG(ckpt_nc) + NC) * S::NS + rank) * 2 *
+                                 E2TTT_ARG(ckpt_stride), w, lane);
       store_state<S>(W, E2TTT_ARG(w_out) + u * a.P, dh, j0, w, g, c);
       store_state<S>(M, E2TTT_ARG(m_out) + u * a.P, dh, j0, w, g, c);
     }
   }
 }
 
-template <class S, bool LONG>
+template <class S, bool LONG, bool PN>
 int occupancy() {
   int v = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_fwd_kernel<S, LONG>, S::NT, 0) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, chain_fwd_kernel<S, LONG, PN>, S::NT, 0) !=
       hipSuccess)
     v = 0;
   return v;
@@ -738,22 +827,23 @@ int occupancy() {
 template <class S>
 int max_blocks_per_cu() {
   static int nb = [] {
-    // one launch geometry serves both instantiations
-    return std::min(occupancy<S, false>(), occupancy<S, true>());
+    // one launch geometry serves both chunk-length instantiations
+    constexpr bool PN = E2TTT_CHAIN_PN;
+    return std::min(occupancy<S, false, PN>(), occupancy<S, true, PN>());
   }();
   return nb;
 }
 
-template <class S, bool LONG>
+template <class S, bool LONG, bool PN>
 hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
   if constexpr (S::NS == 1) {
-    hipLaunchKernelGGL((chain_fwd_kernel<S, LONG>), dim3((unsigned)a.U), dim3(S::NT), 0, stream,
+    hipLaunchKernelGGL((chain_fwd_kernel<S, LONG, PN>), dim3((unsigned)a.U), dim3(S::NT), 0, stream,
                        a);
     return hipGetLastError();
   } else {
     ChainArgs b = a;
     void* args[] = {&b};
-    return hipLaunchCooperativeKernel((const void*)chain_fwd_kernel<S, LONG>,
+    return hipLaunchCooperativeKernel((const void*)chain_fwd_kernel<S, LONG, PN>,
                                       dim3((unsigned)(S::NS * a.npairs)), dim3(S::NT), args, 0,
                                       stream);
   }
@@ -761,10 +851,14 @@ hipError_t launch_as(const ChainArgs& a, hipStream_t stream) {
 
 template <class S>
 hipError_t launch(const ChainArgs& a, hipStream_t stream) {
-  if (a.C <= S::CM) return launch_as<S, false>(a, stream);
+  // the post-chunk normalisation is a separate instantiation, so that the
+  // kernels without it carry none of its registers
+  constexpr bool PN = E2TTT_CHAIN_PN;
+  if ((a.norm_tgt != nullptr) != PN) return hipErrorInvalidValue;
+  if (a.C <= S::CM) return launch_as<S, false, PN>(a, stream);
   // a long chunk whose products re-form W_0 from the state needs the W_0 blocks
   if (S::BF && (S::FW == 1 || S::D > 64) && !a.w0blk) return hipErrorInvalidValue;
-  return launch_as<S, true>(a, stream);
+  return launch_as<S, true, PN>(a, stream);
 }
 
 }  // namespace
@@ -774,7 +868,11 @@ hipError_t launch(const ChainArgs& a, hipStream_t stream) {
       cfg.bf == BF && cfg.ns == NS)                                                     \
     return launch<Shape<FW, D, NW, NJB, NTB, BF, NS>>(a, stream);
 
-hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream) {
+hipError_t E2TTT_PN_NAME(launch_chain_fwd)(const ChainConfig& cfg, const ChainArgs& a,
+                                      hipStream_t stream) {
+#if !E2TTT_CHAIN_PN
+  if (cfg.pn) return launch_chain_fwd_pn(cfg, a, stream);
+#endif
 #include "chain_variants.inc"
   return hipErrorInvalidValue;
 }
@@ -785,12 +883,16 @@ hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, hipStrea
       cfg.bf == BF && cfg.ns == NS)                                                     \
     return max_blocks_per_cu<Shape<FW, D, NW, NJB, NTB, BF, NS>>();
 
-int chain_fwd_blocks_per_cu(const ChainConfig& cfg) {
+int E2TTT_PN_NAME(chain_fwd_blocks_per_cu)(const ChainConfig& cfg) {
+#if !E2TTT_CHAIN_PN
+  if (cfg.pn) return chain_fwd_blocks_per_cu_pn(cfg);
+#endif
 #include "chain_variants.inc"
   return 0;
 }
 #undef E2TTT_CASE
 
+#if !E2TTT_CHAIN_PN
 long chain_ckpt_bytes(const ChainConfig& cfg) {
   const long nmat = (cfg.fw == 0) ? 2 : 3;
   return nmat * 16L * cfg.nw * cfg.njb * cfg.d * (cfg.bf ? 2 : 4);
@@ -802,5 +904,7 @@ long chain_saved_act_bytes(const ChainConfig& cfg) {
   // 8 bytes each on the bf16 path (bf16, fp16), 16 on the fp32 path
   return (long)cfg.ntb * cfg.njb * cfg.nw * 64 * (cfg.bf ? 2 * 8 : 2 * 16);
 }
+
+#endif  // !E2TTT_CHAIN_PN
 
 }  // namespace e2ttt

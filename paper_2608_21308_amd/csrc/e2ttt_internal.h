@@ -107,7 +107,18 @@ struct ChainArgs {
   // backward with the affine: the adjoint of a * e for every token row
   // [U][T][d] fp32, rows [rank share] written by each rank
   float* ln_zbar;
+  // post-chunk L2 normalisation of the fast-weight rows (nullable: off).
+  // Rows in packing order: the first-layer matrices' dh rows each, then the
+  // second layer's d rows, R = (NMAT - 1) dh + d per unit.
+  const float* norm_tgt;  // [U][R] target norms (the rows of w_in)
+  float* norm_pre;        // [U][NC][R] norms before the normalisation (forward, saving)
+  float* norm_rbar;       // [U][NS][R] backward: what flows into the targets, per rank
+  float* nxbuf;           // [groups][NS][2][d] second-layer row sums of each rank
+  long ckpt_nc;           // checkpoint blocks per unit: NC, or NC + 1 (the final state)
 };
+// Post-chunk normalisation: the target norms of every unit's rows from w_in.
+hipError_t launch_norm_targets(const float* w_in, float* tgt, long U, int d, int dh, int nmat,
+                               long P, hipStream_t stream);
 
 // The affine's gradients from the saved and written rows (ln_affine.hip):
 // per head h and column i, over the batch and all tokens,
@@ -140,6 +151,7 @@ struct ChainConfig {
   int ntb;    // 16-row token blocks per chunk
   int bf;     // 1: bf16 MFMA operands and io; 0: fp32
   int ns;     // workgroups per unit (1, or 2 with a cooperative launch)
+  int pn;     // 1: with the post-chunk normalisation of the fast weights
 };
 
 // Net evaluation at a given state (e2ttt_apply): per unit, T tokens of q at
@@ -165,6 +177,12 @@ hipError_t launch_coeff_bwd(const CoeffBwdArgs& a, hipStream_t stream);
 // Return hipErrorInvalidValue when no kernel exists for `cfg`.
 hipError_t launch_chain_fwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
 hipError_t launch_chain_bwd(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
+// the instantiations with the post-chunk normalisation (cfg.pn; the two above
+// forward to these)
+hipError_t launch_chain_fwd_pn(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
+hipError_t launch_chain_bwd_pn(const ChainConfig& cfg, const ChainArgs& a, hipStream_t stream);
+int chain_fwd_blocks_per_cu_pn(const ChainConfig& cfg);
+int chain_bwd_blocks_per_cu_pn(const ChainConfig& cfg);
 // Returns hipErrorInvalidValue for a head dim / io type / width without a kernel.
 hipError_t launch_apply(const ChainConfig& cfg, int fw, ApplyArgs a, hipStream_t stream);
 // Clears n words (a kernel, so that it may be captured in a graph).

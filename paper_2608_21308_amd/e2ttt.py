@@ -23,6 +23,7 @@ DT_BF16 = 1
 FLAG_NO_RESIDUAL_LN = 1
 FLAG_CHUNK_AVERAGED = 2
 FLAG_LN_AFFINE = 4
+FLAG_POST_NORM = 8       # post-chunk L2 normalisation of the fast-weight rows (App. B.1)
 
 STATUS = {0: "ok", 1: "null argument", 2: "bad shape", 3: "unsupported",
           4: "workspace too small", 5: "HIP error", 6: "device-side wait expired"}

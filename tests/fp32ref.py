@@ -59,9 +59,10 @@ def scalar_kernels(eta, beta, gamma):
 
 
 def closed_form_unit(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=True, eps=1e-5,
-                     ln_a=None, ln_b=None):
+                     ln_a=None, ln_b=None, post_norm=False):
     """One unit over all chunks: (outputs [T, d], W_T, M_T), differentiable;
-    ln_a, ln_b: the unit's LayerNorm affine [d], or None."""
+    ln_a, ln_b: the unit's LayerNorm affine [d], or None; post_norm: the rows
+    rescaled to w_in's row norms at every chunk end."""
     T = q.shape[0]
     W = w_in
     M = m_in if m_in is not None else torch.zeros_like(w_in)
@@ -80,6 +81,8 @@ def closed_form_unit(q, k, v, eta, beta, gamma, w_in, m_in, C, d, dh, fw, resln=
         (gm,) = torch.autograd.grad((km * per_tok).sum(), W0, create_graph=True)
         W = cw * W0 + cm * M0 - gw
         M = cb * M0 - gm
+        if post_norm:
+            W = torchref.row_normalise(W, w_in, d, dh, fw)
     return torch.cat(outs), W, M
 
 
@@ -101,7 +104,8 @@ def forward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32, ln=None):
             g = lambda n: None if x.get(n) is None else _t(x[n][b, h], dtype)
             la, lb = (None, None) if ln is None else (_t(ln[0][h], dtype), _t(ln[1][h], dtype))
             o, W, M = closed_form_unit(g("q"), g("k"), g("v"), g("eta"), g("beta"), g("gamma"),
-                                       g("w_in"), g("m_in"), C, d, dh, fw, resln, eps, la, lb)
+                                       g("w_in"), g("m_in"), C, d, dh, fw, resln, eps, la, lb,
+                                       post_norm=bool(flags & 8))
             outs.append(o.detach().double().numpy())
             ws.append(W.detach().double().numpy())
             ms.append(M.detach().double().numpy())
@@ -139,7 +143,8 @@ def backward(x, *, C, fw, dh, flags=0, eps=1e-5, dtype=torch.float32, ln=None):
                                        leaf["beta"], leaf["gamma"], leaf["w_in"], leaf["m_in"],
                                        C, d, dh, fw, resln, eps,
                                        None if ln is None else ta[h],
-                                       None if ln is None else tb[h])
+                                       None if ln is None else tb[h],
+                                       post_norm=bool(flags & 8))
             loss = (o * _t(x["d_out"][b, h], dtype)).sum()
             if x.get("d_w_out") is not None:
                 loss = loss + (W * _t(x["d_w_out"][b, h], dtype)).sum()

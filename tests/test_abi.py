@@ -48,9 +48,29 @@ def test_sizes(lib):
     assert lib.e2ttt_param_count(ctypes.byref(d)) == 3 * 64 * 172
 
 
+def test_post_norm_sizes(lib):
+    # E2TTT_FLAG_POST_NORM (8): the workspace adds the target norms, the
+    # exchange rows, one more checkpoint block per unit (the final state) and,
+    # when saving, the norms before each chunk end's normalisation; the
+    # backward scratch adds what flows into the targets and its exchange rows
+    for kw in (dict(), dict(fw=1, dh=172), dict(d=128, dh=512), dict(io=0, d=16, dh=64)):
+        d0, d8 = desc(**kw), desc(flags=8, **kw)
+        U, T, C = d0.B * d0.H, d0.T, d0.chunk
+        NC = (T + C - 1) // C
+        R = (1 if d0.fw == 0 else 2) * d0.dh + d0.d
+        ws0 = lib.e2ttt_workspace_bytes(ctypes.byref(d0), 1)
+        ws8 = lib.e2ttt_workspace_bytes(ctypes.byref(d8), 1)
+        assert ws8 >= ws0 + U * R * 4 + U * NC * R * 4, kw
+        assert lib.e2ttt_workspace_bytes(ctypes.byref(d8), 0) >= \
+            lib.e2ttt_workspace_bytes(ctypes.byref(d0), 0) + U * R * 4, kw
+        assert lib.e2ttt_backward_scratch_bytes(ctypes.byref(d8)) >= \
+            lib.e2ttt_backward_scratch_bytes(ctypes.byref(d0)) + U * R * 4, kw
+        assert lib.e2ttt_param_count(ctypes.byref(d8)) == lib.e2ttt_param_count(ctypes.byref(d0))
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(T=0), 2), (dict(B=-1), 2), (dict(chunk=0), 2), (dict(ln_eps=0.0), 2),
-    (dict(chunk=513), 3), (dict(fw=2), 3), (dict(io=7), 3), (dict(flags=8), 3),
+    (dict(chunk=513), 3), (dict(fw=2), 3), (dict(io=7), 3), (dict(flags=16), 3),
     (dict(flags=5), 2),
     (dict(d=32), 3), (dict(d=16), 3), (dict(dh=300), 3), (dict(fw=1, dh=200), 3),
     (dict(io=0, d=64), 3), (dict(io=0, d=16, dh=200), 3)])

@@ -1,7 +1,8 @@
 """The float32 reference that sizes the fp32 bars (tests/fp32ref.py) computes
 the same thing as the oracle: evaluated in float64 it reproduces the oracle's
 token recurrence (Prop. 1) to round-off, forward and backward, for both nets,
-ragged chunks, with and without the decay gate, and with the bare net."""
+ragged chunks, with and without the decay gate, with the bare net, and with
+the post-chunk normalisation of the fast weights (flag 8)."""
 import numpy as np
 import pytest
 import torch
@@ -14,7 +15,8 @@ from tests.gpu_util import rel_l2
 
 @pytest.mark.parametrize("fw", [WL.FW_MLP, WL.FW_SWIGLU])
 @pytest.mark.parametrize("T,C,flags,gamma", [(40, 16, 0, True), (23, 7, 0, False),
-                                             (30, 30, 1, True), (5, 1, 0, True)])
+                                             (30, 30, 1, True), (5, 1, 0, True),
+                                             (40, 16, 8, True), (23, 7, 9, False)])
 def test_fp64_closed_form_equals_the_oracle(fw, T, C, flags, gamma):
     w = WL.WORKLOADS[0].with_(fw=fw, B=1, H=2, T=T, C=C, dh=24, backward=True, seed=40 + T)
     x = WL.make_inputs(w)
