@@ -261,8 +261,9 @@ long chain_max_pairs(const ChainConfig& cfg, bool backward) {
 }
 
 long chain_xchg_floats(const ChainConfig& cfg, bool backward) {
-  // per rank: two parities of (Y_K, Y_Q) or (dYh, dk, dq), 16 ntb x d floats each
-  return 2L * (backward ? 3 : 2) * 16 * cfg.ntb * cfg.d;
+  // per rank, 16 ntb x d floats each: backward two parities of (dYh, dk, dq);
+  // forward at most two slots of Y_K and one of Y_Q
+  return (backward ? 6L : 3L) * 16 * cfg.ntb * cfg.d;
 }
 
 long chain_frz_floats(const ChainConfig& cfg) {

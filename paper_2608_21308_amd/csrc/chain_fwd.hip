@@ -77,10 +77,24 @@ struct FwdSmem {
   int word[2];
 };
 
-// Exchange slot of one rank for one parity: [Y_K | Y_Q], CM x D floats each.
-template <class S>
-__device__ __forceinline__ float* fwd_slot(float* xbuf, long p, int rank, int parity) {
-  return xbuf + (((p * S::NS + rank) * 2 + parity) * 2L) * S::CM * S::D;
+// Exchange slots of one rank: NPK slots of Y_K (one per parity) and one of
+// Y_Q, CM x D floats each.  A slot is rewritten only after every peer has
+// finished reading it, by the order of the waits, with one slot of Y_Q: a
+// peer reads a rank's Y_Q of tile n in its outputs phase, before it posts its
+// Y_K of tile n + 1 (whose post waits for those loads), and the rank writes
+// its Y_Q of tile n + 1 only after waiting for that post.  Likewise one slot
+// of Y_K where the peers load its rows right after their wait for it (before
+// posting their Y_Q of the same tile, which the rank waits for before the next
+// Y_K); where the row phases read Y_K from the slots later in the tile (after
+// that post), Y_K alternates between two slots.  Fewer slots keep the
+// exchange's working set in the XCD's L2.
+template <class S, int NPK>
+__device__ __forceinline__ float* fwd_slot_k(float* xbuf, long p, int rank, int parity) {
+  return xbuf + ((p * S::NS + rank) * (NPK + 1) + (NPK == 2 ? parity : 0)) * (long)S::CM * S::D;
+}
+template <class S, int NPK>
+__device__ __forceinline__ float* fwd_slot_q(float* xbuf, long p, int rank) {
+  return xbuf + ((p * S::NS + rank) * (NPK + 1) + NPK) * (long)S::CM * S::D;
 }
 
 // LONG: chunks longer than the CM-row tile (a separate instantiation, so that
@@ -117,6 +131,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
   // peers or wide rows that would hold too many registers, and each row
   // phase loads them where it adds them
   constexpr bool PEER_EARLY = NPEER * EPL <= 8 && S::D <= 64;
+  constexpr int NPK = PEER_EARLY ? 1 : 2;   // Y_K slots per rank
   __shared__ FwdSmem<S> sm;
   static_assert(sizeof(FwdSmem<S>) <= 160 * 1024, "LDS budget");
 
@@ -315,7 +330,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         jgemm_to_lds<S>(sm.alds, sm.w2, sm.y, w, g, c,   // Y_K (partial)
-                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) : nullptr);
+                        (S::NS > 1) ? fwd_slot_k<S, NPK>(E2TTT_ARG(xbuf), px.xs, rank, par) : nullptr);
       }
       px.post();                                          // seq0 + 1: Y_K
       // without a separate Q-side buffer, alds is rewritten below
@@ -378,7 +393,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
 #pragma unroll
         for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
-          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, other_rank(k, rank), par);
+          const float* peer = fwd_slot_k<S, NPK>(E2TTT_ARG(xbuf), px.xs, other_rank(k, rank), par);
 #pragma unroll
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * S::NW;
@@ -392,7 +407,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       {
         E2TTT_LANE_IDS;
         jgemm_to_lds<S>(aq, sm.w2, sm.yq, w, g, c,        // Y_Q (partial)
-                        (S::NS > 1) ? fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) + S::CM * D : nullptr);
+                        (S::NS > 1) ? fwd_slot_q<S, NPK>(E2TTT_ARG(xbuf), px.xs, rank) : nullptr);
       }
       px.post();                                          // seq0 + 2: Y_Q
       // the saved query side goes out after the post, so that the post's wait
@@ -445,7 +460,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
+              load_row_part<EPL>(pr, fwd_slot_k<S, NPK>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
                                          l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
@@ -535,7 +550,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
         E2TTT_LANE_IDS;
 #pragma unroll
         for (int k = 0; k < (PEER_EARLY ? NPEER : 0); ++k) {
-          const float* peer = fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, other_rank(k, rank), par) + S::CM * D;
+          const float* peer = fwd_slot_q<S, NPK>(E2TTT_ARG(xbuf), px.xs, other_rank(k, rank));
 #pragma unroll
           for (int it_ = 0; it_ < NITO; ++it_) {
             const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
@@ -756,7 +771,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_part<EPL>(pr, fwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par) + S::CM * D + t * D +
+              load_row_part<EPL>(pr, fwd_slot_q<S, NPK>(E2TTT_ARG(xbuf), px.xs, r) + t * D +
                                          l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
