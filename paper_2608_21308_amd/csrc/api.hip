@@ -261,9 +261,10 @@ long chain_max_pairs(const ChainConfig& cfg, bool backward) {
 }
 
 long chain_xchg_floats(const ChainConfig& cfg, bool backward) {
-  // per rank, 16 ntb x d floats each: backward two parities of (dYh, dk, dq);
-  // forward at most two slots of Y_K and one of Y_Q
-  return (backward ? 6L : 3L) * 16 * cfg.ntb * cfg.d;
+  // per rank, in units of 16 ntb x d floats: backward two parities of the fp32
+  // dYh partial and the dk, dq partials in the operand type (bf16: one unit for
+  // both); forward at most two slots of Y_K and one of Y_Q
+  return (backward ? (cfg.bf ? 4L : 6L) : 3L) * 16 * cfg.ntb * cfg.d;
 }
 
 long chain_frz_floats(const ChainConfig& cfg) {

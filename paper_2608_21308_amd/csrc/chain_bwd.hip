@@ -296,6 +296,29 @@ __device__ __forceinline__ void jacc_store_io(const JAcc<S>& out, void* dst, lon
   }
 }
 
+// Write the j-round output tiles to an E [CM][D] buffer (a slot's dk or dq
+// partial): dst[t][i] = out + extra(t, i), rounded to E.
+template <class S, class FX>
+__device__ __forceinline__ void jacc_store_part(const JAcc<S>& out, typename S::E* dst, FX extra,
+                                                int w, int g, int c) {
+  using L = BwdLayout<S>;
+  constexpr int NI = S::NIB / S::IBB;
+#pragma unroll
+  for (int a = 0; a < L::JIT; ++a) {
+    const int it = w + a * S::NW;
+    if (it < L::NITEM) {
+      const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * tb + 4 * g + r, i = 16 * (ib0 + b) + c;
+          dst[t * S::D + i] = S::O::to_e(out.v[a][b][r] + extra(t, i));
+        }
+    }
+  }
+}
+
 // Write the j-round output tiles to an fp32 [CM][D] buffer: dst[t][i] = out + extra(t, i).
 template <class S, class FX>
 __device__ __forceinline__ void jacc_store_f32(const JAcc<S>& out, float* dst, FX extra, int w,
@@ -318,10 +341,20 @@ __device__ __forceinline__ void jacc_store_f32(const JAcc<S>& out, float* dst, F
   }
 }
 
-// Exchange slot of one rank for one parity: [dYh | dk | dq] partials, CM x D floats each.
+// Exchange slot of one rank for one parity: the dYh partial (CM x D floats),
+// then the dk and dq partials (CM x D each) in the operand type E.  dk and dq
+// leave the kernel in the io type, which is E, so their partials travel in it
+// too (bf16 on the bf16 path: half the bytes, which keeps more of the slots in
+// the XCD's L2); they are widened and added in fp32 and rounded once more.
 template <class S>
 __device__ __forceinline__ float* bwd_slot(float* xbuf, long p, int rank, int parity) {
-  return xbuf + (((p * S::NS + rank) * 2 + parity) * 3L) * S::CM * S::D;
+  constexpr long PART = (long)S::CM * S::D * (1 + 2 * (long)sizeof(typename S::E) / 4);
+  return xbuf + ((p * S::NS + rank) * 2 + parity) * PART;
+}
+// The dk (sec = 1) or dq (sec = 2) partial of a slot.
+template <class S>
+__device__ __forceinline__ typename S::E* bwd_part(float* slot, int sec) {
+  return reinterpret_cast<typename S::E*>(slot + S::CM * S::D) + (sec - 1) * S::CM * S::D;
 }
 
 // dk and dq of one chunk from the ranks' partials, added in rank order (rank
@@ -341,16 +374,14 @@ __device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int le
     if (t >= tend) continue;
 #pragma unroll
     for (int sec = 1; sec <= 2; ++sec) {
-      float4 x = *reinterpret_cast<const float4*>(bwd_slot<S>(E2TTT_ARG(xbuf), p, 0, parity) +
-                                                  sec * S::CM * S::D + e);
+      f32x4 x = quad_f32(*reinterpret_cast<const typename S::O::Q*>(
+          bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, 0, parity), sec) + e));
 #pragma unroll
-      for (int rk = 1; rk < S::NS; ++rk) {
-        const float4 y = *reinterpret_cast<const float4*>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity) +
-                                                          sec * S::CM * S::D + e);
-        x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
-      }
+      for (int rk = 1; rk < S::NS; ++rk)
+        x += quad_f32(*reinterpret_cast<const typename S::O::Q*>(
+            bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec) + e));
       typename IO::T* d = (sec == 1) ? dk : dq;
-      IO::st4(d + e, f32x4{x.x, x.y, x.z, x.w});
+      IO::st4(d + e, x);
     }
   }
 }
@@ -1122,7 +1153,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         }
         const float ksign = (resln && rank == 0) ? -1.0f : 0.0f;
         if constexpr (S::NS > 1) {
-          jacc_store_f32<S>(dkacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) + S::CM * D,
+          jacc_store_part<S>(dkacc, bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par), 1),
                             [&](int t, int i) { return ksign * ek[t * D + i]; }, w, g, c);
         } else {
           jacc_store_io<S>(dkacc, E2TTT_ARG(dk), row0, len,
@@ -1294,7 +1325,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         }
         const float qsign = (resln && rank == 0) ? 1.0f : 0.0f;
         if constexpr (S::NS > 1) {
-          jacc_store_f32<S>(dqacc, bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par) + 2 * S::CM * D,
+          jacc_store_part<S>(dqacc, bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, rank, par), 2),
                             [&](int t, int i) { return qsign * O::from_e(xdo[t * S::LDD + i]); },
                             w, g, c);
         } else {
