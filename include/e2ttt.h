@@ -86,7 +86,8 @@ typedef enum {
  * and the results of that call are undefined.  The kernels record it in a
  * status word of the workspace (forward) or scratch (backward) buffer;
  * e2ttt_wait_status reads it.  With the environment variable
- * E2TTT_DEBUG_SYNC=1 every call also waits for its kernels and returns it. */
+ * E2TTT_DEBUG_SYNC=1 (read at every call) every call also waits for its
+ * kernels and returns it. */
 
 typedef enum { E2TTT_FW_GELU_MLP = 0, E2TTT_FW_SWIGLU = 1 } e2ttt_fw;
 

@@ -213,12 +213,10 @@ long long wait_ticks() {
   return std::min(us, 600000000LL) * 100;
 }
 
+// E2TTT_DEBUG_SYNC=1 (read at every call)
 bool debug_sync() {
-  static const bool on = [] {
-    const char* s = std::getenv("E2TTT_DEBUG_SYNC");
-    return s && s[0] == '1';
-  }();
-  return on;
+  const char* s = std::getenv("E2TTT_DEBUG_SYNC");
+  return s && s[0] == '1';
 }
 
 // With E2TTT_DEBUG_SYNC=1 every call waits for its kernels and, for the

@@ -37,6 +37,9 @@ def fwd_bwd(cfg, t, scratch):
 # GELU MLP dh 256 on two workgroups per unit; SwiGLU dh 172 on three
 @pytest.mark.parametrize("fw,dh", [(WL.FW_MLP, 256), (WL.FW_SWIGLU, 172)])
 def test_expired_waits_are_reported(fw, dh, monkeypatch):
+    # the status word as a caller reads it after asynchronous calls (without
+    # E2TTT_DEBUG_SYNC, which makes the call itself report the expiry: below)
+    monkeypatch.delenv("E2TTT_DEBUG_SYNC", raising=False)
     w = WL.WORKLOADS[3].with_(fw=fw, dh=dh, B=8, H=16, T=512, seed=3300 + dh)
     x = WL.make_inputs(w)
     cfg = config_of(w)
@@ -68,6 +71,24 @@ def test_expired_waits_are_reported(fw, dh, monkeypatch):
     if fw == WL.FW_MLP:   # (the SwiGLU + LN trajectory is chaotic over 8 chunks)
         assert all(e <= TOL["bf16"] for e in errs.values()), errs
     assert torch.isfinite(out.float()).all()
+
+
+def test_debug_sync_reports_the_expiry_from_the_call(monkeypatch):
+    # with E2TTT_DEBUG_SYNC=1 every call waits for its kernels and returns the
+    # status word itself: an expired wait is the call's E2TTT_ERR_DEVICE (6)
+    w = WL.WORKLOADS[3].with_(B=2, H=4, T=256, seed=3400)
+    x = WL.make_inputs(w)
+    cfg = config_of(w)
+    t = to_dev(x, "bf16")
+    monkeypatch.setenv("E2TTT_DEBUG_SYNC", "1")
+    out, _, _, _ = e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"],
+                                 t["w_in"], None)
+    assert torch.isfinite(out.float()).all()
+    monkeypatch.setenv("E2TTT_WAIT_LIMIT_US", "0")
+    with pytest.raises(e2ttt.E2TTTError) as err:
+        e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"], t["w_in"], None)
+    assert err.value.status == 6
+    torch.cuda.synchronize()
 
 
 def test_single_workgroup_units_have_no_waits():
