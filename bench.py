@@ -456,6 +456,13 @@ def main():
         res["long_chunk_forward"] = time_long_chunk(e2ttt, w, t, dev)
         res["gates"] = time_gates(e2ttt, w, dev)
         res["decode"] = time_decode(e2ttt, w, x, dev)
+        # the same decode loop for one layer at the paper's 1.3B shape (head dim
+        # 128, hidden 512, C 512), at the two batch sizes of its decode table
+        res["decode_paper_1p3b"] = {}
+        for b in (1, 8):
+            wp = WL.PAPER_1P3B.with_(B=b)
+            res["decode_paper_1p3b"]["B%d" % b] = time_decode(
+                e2ttt, wp, WL.make_inputs(wp, with_grads=False), dev)
         res["other_workloads"] = time_workloads(e2ttt, WL, dev)
         res["peaks_measured"] = measure_peaks(dev)
     if args.no_cpu_baseline:
