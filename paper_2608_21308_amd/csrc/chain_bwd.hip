@@ -789,43 +789,61 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
               wbq[m][jj][ib] = O::cvt(Wb.t[m][jj][ib]);
               mbq[m][jj][ib] = O::cvt(Mb.t[m][jj][ib]);
             }
+        // The products of token block (tb, jj) (dA, rW, rM, then hk, uW, uM of
+        // each first-layer matrix) are issued one item ahead of the arithmetic
+        // that uses them, in the same scheduling region, so that the matrix
+        // cores work on the next item while the VALU evaluates this one.
+        constexpr int NPR = 3 + 3 * NF, NITEM4 = NTB * NJB;
+        auto p4_products = [&](int tb, int jj, f32x4 (&r)[NPR]) {
+          E2TTT_LANE_IDS;
+#pragma unroll
+          for (int x = 0; x < NPR; ++x) r[x] = zero4();
+#pragma unroll
+          for (int p = 0; p < S::KS_D; ++p) {
+            auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
+            auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
+            typename O::Frag b2, bw, bm;
+#pragma unroll
+            for (int h = 0; h < S::NH; ++h) {
+              b2.h[h] = w2q[jj][S::NH * p + h];
+              bw.h[h] = wbq[SEC][jj][S::NH * p + h];
+              bm.h[h] = mbq[SEC][jj][S::NH * p + h];
+            }
+            r[0] = O::mma(r[0], fy, b2);
+            r[1] = O::mma(r[1], fy, bw);
+            r[2] = O::mma(r[2], fy, bm);
+#pragma unroll
+            for (int m = 0; m < NF; ++m) {
+#pragma unroll
+              for (int h = 0; h < S::NH; ++h) {
+                b2.h[h] = w1q[m][jj][S::NH * p + h];
+                bw.h[h] = wbq[m][jj][S::NH * p + h];
+                bm.h[h] = mbq[m][jj][S::NH * p + h];
+              }
+              r[3 + m] = O::mma(r[3 + m], fk, b2);
+              r[3 + NF + m] = O::mma(r[3 + NF + m], fk, bw);
+              r[3 + 2 * NF + m] = O::mma(r[3 + 2 * NF + m], fk, bm);
+            }
+          }
+        };
+        f32x4 pcur[NPR], pnext[NPR];
+        p4_products(0, 0, pcur);
+        sched_fence();
 #pragma unroll
         for (int tb = 0; tb < NTB; ++tb) {
           E2TTT_LANE_IDS;
           float kwp[4] = {0.0f, 0.0f, 0.0f, 0.0f}, kmp[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
           for (int jj = 0; jj < NJB; ++jj) {
-            f32x4 dA = zero4(), rW = zero4(), rM = zero4();
+            const int it4 = tb * NJB + jj;
+            if (it4 + 1 < NITEM4) p4_products((it4 + 1) / NJB, (it4 + 1) % NJB, pnext);
+            const f32x4 dA = pcur[0], rW = pcur[1], rM = pcur[2];
             f32x4 uW[NF], uM[NF], hk[NF];
 #pragma unroll
-            for (int m = 0; m < NF; ++m) { uW[m] = zero4(); uM[m] = zero4(); hk[m] = zero4(); }
-#pragma unroll
-            for (int p = 0; p < S::KS_D; ++p) {
-              auto fy = lds_frag<S::BF>(dyl, S::LDD, 16 * tb + c, p * S::KC, g);
-              auto fk = lds_frag<S::BF>(xk, S::LDD, 16 * tb + c, p * S::KC, g);
-              typename O::Frag b2, bw, bm;
-#pragma unroll
-              for (int h = 0; h < S::NH; ++h) {
-                b2.h[h] = w2q[jj][S::NH * p + h];
-                bw.h[h] = wbq[SEC][jj][S::NH * p + h];
-                bm.h[h] = mbq[SEC][jj][S::NH * p + h];
-              }
-              dA = O::mma(dA, fy, b2);
-              rW = O::mma(rW, fy, bw);
-              rM = O::mma(rM, fy, bm);
-#pragma unroll
-              for (int m = 0; m < NF; ++m) {
-#pragma unroll
-                for (int h = 0; h < S::NH; ++h) {
-                  b2.h[h] = w1q[m][jj][S::NH * p + h];
-                  bw.h[h] = wbq[m][jj][S::NH * p + h];
-                  bm.h[h] = mbq[m][jj][S::NH * p + h];
-                }
-                hk[m] = O::mma(hk[m], fk, b2);
-                uW[m] = O::mma(uW[m], fk, bw);
-                uM[m] = O::mma(uM[m], fk, bm);
-              }
-              sched_fence();   // one K-step's operands live at a time
+            for (int m = 0; m < NF; ++m) {
+              hk[m] = pcur[3 + m];
+              uW[m] = pcur[3 + NF + m];
+              uM[m] = pcur[3 + 2 * NF + m];
             }
             f32x4 dH[NF], dAh, hh[NF], Af;
 #pragma unroll
@@ -873,6 +891,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             }
             dAhq[tb][jj] = O::cvt(dAh);
             Akq[tb][jj] = O::cvt(Af);
+            if (it4 + 1 < NITEM4) {
+#pragma unroll
+              for (int x = 0; x < NPR; ++x) pcur[x] = pnext[x];
+            }
             sched_fence();
           }
           // per-wave row partials of dK^W, dK^M for this token block: after the
