@@ -51,6 +51,7 @@ struct BwdLayout {
   static constexpr int JH = (S::DHK > 128) ? 2 : 1;     // hidden halves per j-round
   static constexpr int JWD = S::DHK / JH;                // hidden width of one half
   static constexpr int LDJ = JWD + S::O::PAD;
+  static_assert(!S::BF || LDJ % 16 == 4, "bf16 j-round quad rows 4 (mod 16) quads apart");
   static_assert(JWD % S::KC == 0, "half width must be a multiple of the K-step");
   static_assert(JWD % (16 * S::NJB) == 0, "a wave's hidden slice must lie in one half");
   static constexpr int TD = S::CM * S::LDD * (int)sizeof(E);   // [t][i]
@@ -104,6 +105,74 @@ struct JAcc {
   }
 };
 
+// j-round operands.  Both operands of a j-round (activations [t][j], weights
+// [i][j]) come from accumulator-layout tiles: lane (g, c) of a wave holds rows
+// 4 g .. 4 g + 3 of a 16-row block at one hidden column.  On the bf16 path
+// that quad is stored with one 8-byte write, quad (block b, row quad q, hidden
+// column k) at quad offset (4 b + q) LDJ + k (the bytes of a [16 NB][LDJ]
+// array), and a lane's operand fragment (row c of block b, contraction indices
+// k0 + 16 h + 4 g + 0..3 for h = 0, 1, the order lds_frag reads) comes back
+// through two transposing LDS reads (ds_read_b64_tr_b16: within each group of
+// 16 lanes, lane c receives element c mod 4 of the quads addressed by lanes
+// 4 r + c / 4, r = 0..3; measured on the MI355X).  With LDJ = 4 (mod 16) the
+// stores (16 lanes on 16 consecutive quads) and the reads (four quad rows, four
+// consecutive quads each) fall on 32 distinct banks.  On the fp32 path the
+// arrays stay row-major, one element per store.
+template <class S>
+__device__ __forceinline__ void jq_put(typename S::E* buf, int blk, int g, int k,
+                                       const typename S::O::Q& v) {
+  using L = BwdLayout<S>;
+  if constexpr (S::BF) {
+    *reinterpret_cast<typename S::O::Q*>(buf + ((4 * blk + g) * L::LDJ + k) * 4) = v;
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) buf[(16 * blk + 4 * g + r) * L::LDJ + k] = v[r];
+  }
+}
+// A lane's read position in block blk of a j-round operand array (formed once
+// per block; the K-steps then add constant offsets).
+template <class S>
+__device__ __forceinline__ const typename S::E* jq_lane(const typename S::E* buf, int blk, int g,
+                                                        int c) {
+  using L = BwdLayout<S>;
+  if constexpr (S::BF) return buf + ((4 * blk + (c & 3)) * L::LDJ + 4 * g + (c >> 2)) * 4;
+  else return buf + (16 * blk + c) * L::LDJ + 4 * g;
+}
+// The operand fragment at K-step offset k0 from a lane's read position.
+template <class S>
+__device__ __forceinline__ typename S::O::Frag jq_frag(const typename S::E* pos, int k0) {
+  typename S::O::Frag f;
+  if constexpr (S::BF) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s4* lds_s4;
+#pragma unroll
+    for (int h = 0; h < S::O::NH; ++h) {
+      typename S::E* p = const_cast<typename S::E*>(pos) + (k0 + 16 * h) * 4;
+      f.h[h] = __builtin_bit_cast(typename S::O::Q, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)p));
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < S::O::NH; ++h)
+      f.h[h] = *reinterpret_cast<const typename S::O::Q*>(pos + k0 + 16 * h);
+  }
+  return f;
+}
+// Zero quads at hidden columns [k_lo, JWD) of nb_a + nb_w 16-row blocks of two
+// operand arrays (columns no wave owns must read as zero).
+template <class S>
+__device__ __forceinline__ void jq_zero_cols(typename S::E* a, int nb_a, typename S::E* b, int nb_w,
+                                             int k_lo) {
+  using L = BwdLayout<S>;
+  const int nz = L::JWD - k_lo;
+  const typename S::O::Q z = S::O::cvt(zero4());
+#pragma unroll 1
+  for (int idx = threadIdx.x; idx < 4 * (nb_a + nb_w) * nz; idx += S::NT) {
+    const int rq = idx / nz, k = k_lo + idx % nz;
+    if (rq < 4 * nb_a) jq_put<S>(a, rq / 4, rq % 4, k, z);
+    else jq_put<S>(b, (rq - 4 * nb_a) / 4, (rq - 4 * nb_a) % 4, k, z);
+  }
+}
+
 // j-round: out[t][i] (+)= rowscale[t] * sum_j Act[t][j] Wt[i][j] over the full
 // hidden range.  Act and Wt are register tiles of every wave: act(tb, jj) is
 // the tile (rows t, column j) and wt(ib, jj) the tile (rows i, column j).
@@ -122,17 +191,8 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
   for (int half = 0; half < L::JH; ++half) {
     // columns of this half beyond the padded hidden width belong to no wave;
     // they may hold the previous half's values and must read as zero
-    constexpr int NT = S::NT;
     const int validw = S::DHP - half * L::JWD;
-    if (validw < L::JWD) {
-      const int nz = L::JWD - validw;
-#pragma unroll 1
-      for (int idx = threadIdx.x; idx < (S::CM + S::D) * nz; idx += NT) {
-        const int rw = idx / nz, col = validw + idx % nz;
-        if (rw < S::CM) ja[rw * L::LDJ + col] = O::to_e(0.0f);
-        else jw[(rw - S::CM) * L::LDJ + col] = O::to_e(0.0f);
-      }
-    }
+    if (validw < L::JWD) jq_zero_cols<S>(ja, S::NTB, jw, S::NIB, validw);
     const int col0 = 16 * w * S::NJB - half * L::JWD;   // this wave's first column in the half
     if (col0 >= 0 && col0 < L::JWD) {
 #pragma unroll
@@ -140,18 +200,10 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
         const int col = col0 + 16 * jj + c;
         if (WRITE_ACT || L::JH > 1) {
 #pragma unroll
-          for (int tb = 0; tb < S::NTB; ++tb) {
-            const auto v = as_quad<S>(act(tb, jj));
-#pragma unroll
-            for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = v[r];
-          }
+          for (int tb = 0; tb < S::NTB; ++tb) jq_put<S>(ja, tb, g, col, as_quad<S>(act(tb, jj)));
         }
 #pragma unroll
-        for (int ib = 0; ib < S::NIB; ++ib) {
-          const auto v = as_quad<S>(wt(ib, jj));
-#pragma unroll
-          for (int r = 0; r < 4; ++r) jw[(16 * ib + 4 * g + r) * L::LDJ + col] = v[r];
-        }
+        for (int ib = 0; ib < S::NIB; ++ib) jq_put<S>(jw, ib, g, col, as_quad<S>(wt(ib, jj)));
       }
     }
     __syncthreads();
@@ -160,12 +212,16 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
       const int it = w + a * S::NW;
       if (it < L::NITEM) {
         const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+        const typename S::E* pa = jq_lane<S>(ja, tb, g, c);
+        const typename S::E* pb[S::IBB];
+#pragma unroll
+        for (int b = 0; b < S::IBB; ++b) pb[b] = jq_lane<S>(jw, ib0 + b, g, c);
 #pragma unroll
         for (int p = 0; p < L::JWD / S::KC; ++p) {
-          auto af = lds_frag<S::BF>(ja, L::LDJ, 16 * tb + c, p * S::KC, g);
+          auto af = jq_frag<S>(pa, p * S::KC);
 #pragma unroll
           for (int b = 0; b < S::IBB; ++b) {
-            auto bf = lds_frag<S::BF>(jw, L::LDJ, 16 * (ib0 + b) + c, p * S::KC, g);
+            auto bf = jq_frag<S>(pb[b], p * S::KC);
             tmp.v[a][b] = O::mma(tmp.v[a][b], af, bf);
           }
         }
@@ -206,34 +262,20 @@ __device__ __forceinline__ void jround2(JAcc<S>& out, const float* rs1, const fl
   // padding columns beyond the hidden width read as zero
   constexpr int NZ = L::JWD - S::DHP;
   if constexpr (NZ > 0) {
-#pragma unroll 1
-    for (int idx = threadIdx.x; idx < (S::CM + 2 * S::D) * NZ; idx += S::NT) {
-      const int rw = idx / NZ, col = S::DHP + idx % NZ;
-      if (rw < S::CM) ja[rw * L::LDJ + col] = O::to_e(0.0f);
-      else if (rw < S::CM + S::D) jw[(rw - S::CM) * L::LDJ + col] = O::to_e(0.0f);
-      else jw2[(rw - S::CM - S::D) * L::LDJ + col] = O::to_e(0.0f);
-    }
+    jq_zero_cols<S>(ja, S::NTB, jw, S::NIB, S::DHP);
+    jq_zero_cols<S>(jw2, 0, jw2, S::NIB, S::DHP);
   }
 #pragma unroll
   for (int jj = 0; jj < S::NJB; ++jj) {
     const int col = 16 * (w * S::NJB + jj) + c;
     if constexpr (WRITE_ACT) {
 #pragma unroll
-      for (int tb = 0; tb < S::NTB; ++tb) {
-        const auto v = as_quad<S>(act(tb, jj));
-#pragma unroll
-        for (int r = 0; r < 4; ++r) ja[(16 * tb + 4 * g + r) * L::LDJ + col] = v[r];
-      }
+      for (int tb = 0; tb < S::NTB; ++tb) jq_put<S>(ja, tb, g, col, as_quad<S>(act(tb, jj)));
     }
 #pragma unroll
     for (int ib = 0; ib < S::NIB; ++ib) {
-      const auto v1 = as_quad<S>(wt1(ib, jj));
-      const auto v2 = as_quad<S>(wt2(ib, jj));
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        jw[(16 * ib + 4 * g + r) * L::LDJ + col] = v1[r];
-        jw2[(16 * ib + 4 * g + r) * L::LDJ + col] = v2[r];
-      }
+      jq_put<S>(jw, ib, g, col, as_quad<S>(wt1(ib, jj)));
+      jq_put<S>(jw2, ib, g, col, as_quad<S>(wt2(ib, jj)));
     }
   }
   __syncthreads();
@@ -242,13 +284,21 @@ __device__ __forceinline__ void jround2(JAcc<S>& out, const float* rs1, const fl
     const int it = w + a * S::NW;
     if (it < L::NITEM) {
       const int tb = it / NI, ib0 = (it % NI) * S::IBB;
+      const typename S::E* pa = jq_lane<S>(ja, tb, g, c);
+      const typename S::E* pb1[S::IBB];
+      const typename S::E* pb2[S::IBB];
+#pragma unroll
+      for (int b = 0; b < S::IBB; ++b) {
+        pb1[b] = jq_lane<S>(jw, ib0 + b, g, c);
+        pb2[b] = jq_lane<S>(jw2, ib0 + b, g, c);
+      }
 #pragma unroll
       for (int p = 0; p < L::JWD / S::KC; ++p) {
-        auto af = lds_frag<S::BF>(ja, L::LDJ, 16 * tb + c, p * S::KC, g);
+        auto af = jq_frag<S>(pa, p * S::KC);
 #pragma unroll
         for (int b = 0; b < S::IBB; ++b) {
-          auto b1 = lds_frag<S::BF>(jw, L::LDJ, 16 * (ib0 + b) + c, p * S::KC, g);
-          auto b2 = lds_frag<S::BF>(jw2, L::LDJ, 16 * (ib0 + b) + c, p * S::KC, g);
+          auto b1 = jq_frag<S>(pb1[b], p * S::KC);
+          auto b2 = jq_frag<S>(pb2[b], p * S::KC);
           t1.v[a][b] = O::mma(t1.v[a][b], af, b1);
           t2.v[a][b] = O::mma(t2.v[a][b], af, b2);
         }
@@ -882,9 +932,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int m = 0; m < NF; ++m) hh_at(m, tb, jj, lane) = hh[m];
             if constexpr (DH_LDS) {
-#pragma unroll
-              for (int q = 0; q < 4; ++q)
-                ja[(16 * tb + 4 * g + q) * L::LDJ + 16 * (w * NJB + jj) + c] = O::to_e(dH[0][q]);
+              jq_put<S>(ja, tb, g, 16 * (w * NJB + jj) + c, O::cvt(dH[0]));
             } else {
 #pragma unroll
               for (int m = 0; m < NF; ++m) dHq[m][tb][jj] = O::cvt(dH[m]);
