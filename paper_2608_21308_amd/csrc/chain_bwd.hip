@@ -105,74 +105,6 @@ struct JAcc {
   }
 };
 
-// j-round operands.  Both operands of a j-round (activations [t][j], weights
-// [i][j]) come from accumulator-layout tiles: lane (g, c) of a wave holds rows
-// 4 g .. 4 g + 3 of a 16-row block at one hidden column.  On the bf16 path
-// that quad is stored with one 8-byte write, quad (block b, row quad q, hidden
-// column k) at quad offset (4 b + q) LDJ + k (the bytes of a [16 NB][LDJ]
-// array), and a lane's operand fragment (row c of block b, contraction indices
-// k0 + 16 h + 4 g + 0..3 for h = 0, 1, the order lds_frag reads) comes back
-// through two transposing LDS reads (ds_read_b64_tr_b16: within each group of
-// 16 lanes, lane c receives element c mod 4 of the quads addressed by lanes
-// 4 r + c / 4, r = 0..3; measured on the MI355X).  With LDJ = 4 (mod 16) the
-// stores (16 lanes on 16 consecutive quads) and the reads (four quad rows, four
-// consecutive quads each) fall on 32 distinct banks.  On the fp32 path the
-// arrays stay row-major, one element per store.
-template <class S>
-__device__ __forceinline__ void jq_put(typename S::E* buf, int blk, int g, int k,
-                                       const typename S::O::Q& v) {
-  using L = BwdLayout<S>;
-  if constexpr (S::BF) {
-    *reinterpret_cast<typename S::O::Q*>(buf + ((4 * blk + g) * L::LDJ + k) * 4) = v;
-  } else {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) buf[(16 * blk + 4 * g + r) * L::LDJ + k] = v[r];
-  }
-}
-// A lane's read position in block blk of a j-round operand array (formed once
-// per block; the K-steps then add constant offsets).
-template <class S>
-__device__ __forceinline__ const typename S::E* jq_lane(const typename S::E* buf, int blk, int g,
-                                                        int c) {
-  using L = BwdLayout<S>;
-  if constexpr (S::BF) return buf + ((4 * blk + (c & 3)) * L::LDJ + 4 * g + (c >> 2)) * 4;
-  else return buf + (16 * blk + c) * L::LDJ + 4 * g;
-}
-// The operand fragment at K-step offset k0 from a lane's read position.
-template <class S>
-__device__ __forceinline__ typename S::O::Frag jq_frag(const typename S::E* pos, int k0) {
-  typename S::O::Frag f;
-  if constexpr (S::BF) {
-    typedef short s4 __attribute__((ext_vector_type(4)));
-    typedef __attribute__((address_space(3))) s4* lds_s4;
-#pragma unroll
-    for (int h = 0; h < S::O::NH; ++h) {
-      typename S::E* p = const_cast<typename S::E*>(pos) + (k0 + 16 * h) * 4;
-      f.h[h] = __builtin_bit_cast(typename S::O::Q, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)p));
-    }
-  } else {
-#pragma unroll
-    for (int h = 0; h < S::O::NH; ++h)
-      f.h[h] = *reinterpret_cast<const typename S::O::Q*>(pos + k0 + 16 * h);
-  }
-  return f;
-}
-// Zero quads at hidden columns [k_lo, JWD) of nb_a + nb_w 16-row blocks of two
-// operand arrays (columns no wave owns must read as zero).
-template <class S>
-__device__ __forceinline__ void jq_zero_cols(typename S::E* a, int nb_a, typename S::E* b, int nb_w,
-                                             int k_lo) {
-  using L = BwdLayout<S>;
-  const int nz = L::JWD - k_lo;
-  const typename S::O::Q z = S::O::cvt(zero4());
-#pragma unroll 1
-  for (int idx = threadIdx.x; idx < 4 * (nb_a + nb_w) * nz; idx += S::NT) {
-    const int rq = idx / nz, k = k_lo + idx % nz;
-    if (rq < 4 * nb_a) jq_put<S>(a, rq / 4, rq % 4, k, z);
-    else jq_put<S>(b, (rq - 4 * nb_a) / 4, (rq - 4 * nb_a) % 4, k, z);
-  }
-}
-
 // j-round: out[t][i] (+)= rowscale[t] * sum_j Act[t][j] Wt[i][j] over the full
 // hidden range.  Act and Wt are register tiles of every wave: act(tb, jj) is
 // the tile (rows t, column j) and wt(ib, jj) the tile (rows i, column j).
@@ -192,7 +124,7 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
     // columns of this half beyond the padded hidden width belong to no wave;
     // they may hold the previous half's values and must read as zero
     const int validw = S::DHP - half * L::JWD;
-    if (validw < L::JWD) jq_zero_cols<S>(ja, S::NTB, jw, S::NIB, validw);
+    if (validw < L::JWD) jq_zero_cols<S, L::LDJ, L::JWD>(ja, S::NTB, jw, S::NIB, validw);
     const int col0 = 16 * w * S::NJB - half * L::JWD;   // this wave's first column in the half
     if (col0 >= 0 && col0 < L::JWD) {
 #pragma unroll
@@ -200,10 +132,10 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
         const int col = col0 + 16 * jj + c;
         if (WRITE_ACT || L::JH > 1) {
 #pragma unroll
-          for (int tb = 0; tb < S::NTB; ++tb) jq_put<S>(ja, tb, g, col, as_quad<S>(act(tb, jj)));
+          for (int tb = 0; tb < S::NTB; ++tb) jq_put<S, L::LDJ>(ja, tb, g, col, as_quad<S>(act(tb, jj)));
         }
 #pragma unroll
-        for (int ib = 0; ib < S::NIB; ++ib) jq_put<S>(jw, ib, g, col, as_quad<S>(wt(ib, jj)));
+        for (int ib = 0; ib < S::NIB; ++ib) jq_put<S, L::LDJ>(jw, ib, g, col, as_quad<S>(wt(ib, jj)));
       }
     }
     __syncthreads();
@@ -212,10 +144,10 @@ __device__ __forceinline__ void jround(JAcc<S>& out, const float* rowscale, type
       const int it = w + a * S::NW;
       if (it < L::NITEM) {
         const int tb = it / NI, ib0 = (it % NI) * S::IBB;
-        const typename S::E* pa = jq_lane<S>(ja, tb, g, c);
+        const typename S::E* pa = jq_lane<S, L::LDJ>(ja, tb, g, c);
         const typename S::E* pb[S::IBB];
 #pragma unroll
-        for (int b = 0; b < S::IBB; ++b) pb[b] = jq_lane<S>(jw, ib0 + b, g, c);
+        for (int b = 0; b < S::IBB; ++b) pb[b] = jq_lane<S, L::LDJ>(jw, ib0 + b, g, c);
 #pragma unroll
         for (int p = 0; p < L::JWD / S::KC; ++p) {
           auto af = jq_frag<S>(pa, p * S::KC);
@@ -262,20 +194,20 @@ __device__ __forceinline__ void jround2(JAcc<S>& out, const float* rs1, const fl
   // padding columns beyond the hidden width read as zero
   constexpr int NZ = L::JWD - S::DHP;
   if constexpr (NZ > 0) {
-    jq_zero_cols<S>(ja, S::NTB, jw, S::NIB, S::DHP);
-    jq_zero_cols<S>(jw2, 0, jw2, S::NIB, S::DHP);
+    jq_zero_cols<S, L::LDJ, L::JWD>(ja, S::NTB, jw, S::NIB, S::DHP);
+    jq_zero_cols<S, L::LDJ, L::JWD>(jw2, 0, jw2, S::NIB, S::DHP);
   }
 #pragma unroll
   for (int jj = 0; jj < S::NJB; ++jj) {
     const int col = 16 * (w * S::NJB + jj) + c;
     if constexpr (WRITE_ACT) {
 #pragma unroll
-      for (int tb = 0; tb < S::NTB; ++tb) jq_put<S>(ja, tb, g, col, as_quad<S>(act(tb, jj)));
+      for (int tb = 0; tb < S::NTB; ++tb) jq_put<S, L::LDJ>(ja, tb, g, col, as_quad<S>(act(tb, jj)));
     }
 #pragma unroll
     for (int ib = 0; ib < S::NIB; ++ib) {
-      jq_put<S>(jw, ib, g, col, as_quad<S>(wt1(ib, jj)));
-      jq_put<S>(jw2, ib, g, col, as_quad<S>(wt2(ib, jj)));
+      jq_put<S, L::LDJ>(jw, ib, g, col, as_quad<S>(wt1(ib, jj)));
+      jq_put<S, L::LDJ>(jw2, ib, g, col, as_quad<S>(wt2(ib, jj)));
     }
   }
   __syncthreads();
@@ -284,13 +216,13 @@ __device__ __forceinline__ void jround2(JAcc<S>& out, const float* rs1, const fl
     const int it = w + a * S::NW;
     if (it < L::NITEM) {
       const int tb = it / NI, ib0 = (it % NI) * S::IBB;
-      const typename S::E* pa = jq_lane<S>(ja, tb, g, c);
+      const typename S::E* pa = jq_lane<S, L::LDJ>(ja, tb, g, c);
       const typename S::E* pb1[S::IBB];
       const typename S::E* pb2[S::IBB];
 #pragma unroll
       for (int b = 0; b < S::IBB; ++b) {
-        pb1[b] = jq_lane<S>(jw, ib0 + b, g, c);
-        pb2[b] = jq_lane<S>(jw2, ib0 + b, g, c);
+        pb1[b] = jq_lane<S, L::LDJ>(jw, ib0 + b, g, c);
+        pb2[b] = jq_lane<S, L::LDJ>(jw2, ib0 + b, g, c);
       }
 #pragma unroll
       for (int p = 0; p < L::JWD / S::KC; ++p) {
@@ -932,7 +864,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int m = 0; m < NF; ++m) hh_at(m, tb, jj, lane) = hh[m];
             if constexpr (DH_LDS) {
-              jq_put<S>(ja, tb, g, 16 * (w * NJB + jj) + c, O::cvt(dH[0]));
+              jq_put<S, L::LDJ>(ja, tb, g, 16 * (w * NJB + jj) + c, O::cvt(dH[0]));
             } else {
 #pragma unroll
               for (int m = 0; m < NF; ++m) dHq[m][tb][jj] = O::cvt(dH[m]);

@@ -495,7 +495,75 @@ struct F32TileRegs {
   }
 };
 
-// Y[t][i] = sum_j A[t][j] Wt[i][j]  (j-contraction, both operands in LDS),
+// Operands of the contractions over the hidden index (the forward's Y = A W2^T,
+// the backward's j-rounds).  Both operands (activations [t][j], weights [i][j])
+// come from accumulator-layout tiles: lane (g, c) of a wave holds rows
+// 4 g .. 4 g + 3 of a 16-row block at one hidden column.  On the bf16 path
+// that quad is stored with one 8-byte write, quad (block b, row quad q, hidden
+// column k) at quad offset (4 b + q) LD + k (the bytes of a [16 NB][LD]
+// array), and a lane's operand fragment (row c of block b, contraction indices
+// k0 + 16 h + 4 g + 0..3 for h = 0, 1, the order lds_frag reads) comes back
+// through two transposing LDS reads (ds_read_b64_tr_b16: within each group of
+// 16 lanes, lane c receives element c mod 4 of the quads addressed by lanes
+// 4 r + c / 4, r = 0..3; measured on the MI355X).  With LD = 4 (mod 16) the
+// stores (16 lanes on 16 consecutive quads) and the reads (four quad rows, four
+// consecutive quads each) fall on 32 distinct banks.  On the fp32 path the
+// arrays stay row-major, one element per store.
+template <class S, int LD>
+__device__ __forceinline__ void jq_put(typename S::E* buf, int blk, int g, int k,
+                                       const typename S::O::Q& v) {
+  static_assert(!S::BF || LD % 16 == 4, "bf16 quad rows 4 (mod 16) quads apart");
+  if constexpr (S::BF) {
+    *reinterpret_cast<typename S::O::Q*>(buf + ((4 * blk + g) * LD + k) * 4) = v;
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) buf[(16 * blk + 4 * g + r) * LD + k] = v[r];
+  }
+}
+// A lane's read position in block blk of a j-round operand array (formed once
+// per block; the K-steps then add constant offsets).
+template <class S, int LD>
+__device__ __forceinline__ const typename S::E* jq_lane(const typename S::E* buf, int blk, int g,
+                                                        int c) {
+  if constexpr (S::BF) return buf + ((4 * blk + (c & 3)) * LD + 4 * g + (c >> 2)) * 4;
+  else return buf + (16 * blk + c) * LD + 4 * g;
+}
+// The operand fragment at K-step offset k0 from a lane's read position.
+template <class S>
+__device__ __forceinline__ typename S::O::Frag jq_frag(const typename S::E* pos, int k0) {
+  typename S::O::Frag f;
+  if constexpr (S::BF) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s4* lds_s4;
+#pragma unroll
+    for (int h = 0; h < S::O::NH; ++h) {
+      typename S::E* p = const_cast<typename S::E*>(pos) + (k0 + 16 * h) * 4;
+      f.h[h] = __builtin_bit_cast(typename S::O::Q, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)p));
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < S::O::NH; ++h)
+      f.h[h] = *reinterpret_cast<const typename S::O::Q*>(pos + k0 + 16 * h);
+  }
+  return f;
+}
+// Zero quads at hidden columns [k_lo, KW) of nb_a + nb_w 16-row blocks of two
+// operand arrays (columns no wave owns must read as zero).
+template <class S, int LD, int KW>
+__device__ __forceinline__ void jq_zero_cols(typename S::E* a, int nb_a, typename S::E* b, int nb_w,
+                                             int k_lo) {
+  const int nz = KW - k_lo;
+  const typename S::O::Q z = S::O::cvt(zero4());
+#pragma unroll 1
+  for (int idx = threadIdx.x; idx < 4 * (nb_a + nb_w) * nz; idx += S::NT) {
+    const int rq = idx / nz, k = k_lo + idx % nz;
+    if (rq < 4 * nb_a) jq_put<S, LD>(a, rq / 4, rq % 4, k, z);
+    else jq_put<S, LD>(b, (rq - 4 * nb_a) / 4, (rq - 4 * nb_a) % 4, k, z);
+  }
+}
+
+// Y[t][i] = sum_j A[t][j] Wt[i][j]  (j-contraction, both operands in LDS as
+// quads, stored with jq_put<S, S::LDH>),
 // written to y (fp32 [CM][D]) and, when given, in the same layout to `slot`
 // in global memory.  Work is split into (token block, head block pair) items
 // over the waves.
@@ -509,12 +577,16 @@ __device__ __forceinline__ void jgemm_to_lds(const typename S::E* A, const typen
     f32x4 acc[S::IBB];
 #pragma unroll
     for (int b = 0; b < S::IBB; ++b) acc[b] = zero4();
+    const typename S::E* pa = jq_lane<S, S::LDH>(A, tb, g, c);
+    const typename S::E* pb[S::IBB];
+#pragma unroll
+    for (int b = 0; b < S::IBB; ++b) pb[b] = jq_lane<S, S::LDH>(Wt, ib0 + b, g, c);
 #pragma unroll
     for (int p = 0; p < S::KS_H; ++p) {
-      auto af = lds_frag<S::BF>(A, S::LDH, 16 * tb + c, p * S::KC, g);
+      auto af = jq_frag<S>(pa, p * S::KC);
 #pragma unroll
       for (int b = 0; b < S::IBB; ++b) {
-        auto bf = lds_frag<S::BF>(Wt, S::LDH, 16 * (ib0 + b) + c, p * S::KC, g);
+        auto bf = jq_frag<S>(pb[b], p * S::KC);
         acc[b] = S::O::mma(acc[b], af, bf);
       }
     }

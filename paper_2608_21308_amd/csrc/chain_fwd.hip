@@ -152,15 +152,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 
   // hidden columns [DHP, DHK) of the j-operands stay zero for the whole run
   if constexpr (S::DHK > S::DHP) {
-    E2TTT_LANE_IDS;
-    constexpr int NZ = S::DHK - S::DHP;
-    for (int idx = tid; idx < S::CM * NZ; idx += S::NT) {
-      sm.alds[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
-      if constexpr (FwdSmem<S>::Q2)
-        sm.alds2[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
-    }
-    for (int idx = tid; idx < D * NZ; idx += S::NT)
-      sm.w2[(idx / NZ) * S::LDH + S::DHP + idx % NZ] = O::to_e(0.0f);
+    jq_zero_cols<S, S::LDH, S::DHK>(sm.alds, S::NTB, sm.w2, S::NIB, S::DHP);
+    if constexpr (FwdSmem<S>::Q2) jq_zero_cols<S, S::LDH, S::DHK>(sm.alds2, S::NTB, sm.alds2, 0, S::DHP);
   }
 
   // inputs of the next chunk, loaded one chunk ahead
@@ -250,12 +243,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
       for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-        for (int ib = 0; ib < NIB; ++ib) {
-          const auto q = as_quad<S>(PRESPLIT ? WS.hi[SEC][jj][ib] : O::cvt(W.t[SEC][jj][ib]));
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-            sm.w2[(16 * ib + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = q[rr];
-        }
+        for (int ib = 0; ib < NIB; ++ib)
+          jq_put<S, S::LDH>(sm.w2, ib, g, 16 * (w * NJB + jj) + c,
+                            as_quad<S>(PRESPLIT ? WS.hi[SEC][jj][ib] : O::cvt(W.t[SEC][jj][ib])));
       }
       opaque_state<S>(W);
       opaque_state<S>(M);
@@ -319,9 +309,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           H[tb][jj] = d1;
           if constexpr (S::FW == 1) Hu[tb][jj] = d2;
           AK[tb][jj] = O::cvt(act);
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-            sm.alds[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = O::to_e(act[rr]);
+          jq_put<S, S::LDH>(sm.alds, tb, g, 16 * (w * NJB + jj) + c, AK[tb][jj]);
           sched_fence();
         }
       }
@@ -373,9 +361,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
             }
           }
           const auto aquad = O::cvt(act);
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-            aq[(16 * tb + 4 * g + rr) * S::LDH + 16 * (w * NJB + jj) + c] = aquad[rr];
+          jq_put<S, S::LDH>(aq, tb, g, 16 * (w * NJB + jj) + c, aquad);
           if constexpr (S::FW == 0) {   // stored after the Y_Q post below
             qsa[tb][jj] = aquad;
             qsd[tb][jj] = d1;
