@@ -337,13 +337,84 @@ __device__ __forceinline__ void store_row16(typename S::E* dst, const uint4& x) 
   }
 }
 
+// Operands of the contractions over the hidden index (the forward's Y = A W2^T,
+// the backward's j-rounds).  Both operands (activations [t][j], weights [i][j])
+// come from accumulator-layout tiles: lane (g, c) of a wave holds rows
+// 4 g .. 4 g + 3 of a 16-row block at one hidden column.  On the bf16 path
+// that quad is stored with one 8-byte write, quad (block b, row quad q, hidden
+// column k) at quad offset (4 b + q) LD + k (the bytes of a [16 NB][LD]
+// array), and a lane's operand fragment (row c of block b, contraction indices
+// k0 + 16 h + 4 g + 0..3 for h = 0, 1, the order lds_frag reads) comes back
+// through two transposing LDS reads (ds_read_b64_tr_b16: within each group of
+// 16 lanes, lane c receives element c mod 4 of the quads addressed by lanes
+// 4 r + c / 4, r = 0..3; measured on the MI355X).  With LD = 4 (mod 16) the
+// stores (16 lanes on 16 consecutive quads) and the reads (four quad rows, four
+// consecutive quads each) fall on 32 distinct banks.  On the fp32 path the
+// arrays stay row-major, one element per store.
+template <class S, int LD>
+__device__ __forceinline__ void jq_put(typename S::E* buf, int blk, int g, int k,
+                                       const typename S::O::Q& v) {
+  static_assert(!S::BF || LD % 16 == 4, "bf16 quad rows 4 (mod 16) quads apart");
+  if constexpr (S::BF) {
+    *reinterpret_cast<typename S::O::Q*>(buf + ((4 * blk + g) * LD + k) * 4) = v;
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) buf[(16 * blk + 4 * g + r) * LD + k] = v[r];
+  }
+}
+// A lane's read position in block blk of a j-round operand array (formed once
+// per block; the K-steps then add constant offsets).
+template <class S, int LD>
+__device__ __forceinline__ const typename S::E* jq_lane(const typename S::E* buf, int blk, int g,
+                                                        int c) {
+  if constexpr (S::BF) return buf + ((4 * blk + (c & 3)) * LD + 4 * g + (c >> 2)) * 4;
+  else return buf + (16 * blk + c) * LD + 4 * g;
+}
+// The operand fragment at K-step offset k0 from a lane's read position.
+template <class S>
+__device__ __forceinline__ typename S::O::Frag jq_frag(const typename S::E* pos, int k0) {
+  typename S::O::Frag f;
+  if constexpr (S::BF) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s4* lds_s4;
+#pragma unroll
+    for (int h = 0; h < S::O::NH; ++h) {
+      typename S::E* p = const_cast<typename S::E*>(pos) + (k0 + 16 * h) * 4;
+      f.h[h] = __builtin_bit_cast(typename S::O::Q, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)p));
+    }
+  } else {
+#pragma unroll
+    for (int h = 0; h < S::O::NH; ++h)
+      f.h[h] = *reinterpret_cast<const typename S::O::Q*>(pos + k0 + 16 * h);
+  }
+  return f;
+}
+// Zero quads at hidden columns [k_lo, KW) of nb_a + nb_w 16-row blocks of two
+// operand arrays (columns no wave owns must read as zero).
+template <class S, int LD, int KW>
+__device__ __forceinline__ void jq_zero_cols(typename S::E* a, int nb_a, typename S::E* b, int nb_w,
+                                             int k_lo) {
+  const int nz = KW - k_lo;
+  const typename S::O::Q z = S::O::cvt(zero4());
+#pragma unroll 1
+  for (int idx = threadIdx.x; idx < 4 * (nb_a + nb_w) * nz; idx += S::NT) {
+    const int rq = idx / nz, k = k_lo + idx % nz;
+    if (rq < 4 * nb_a) jq_put<S, LD>(a, rq / 4, rq % 4, k, z);
+    else jq_put<S, LD>(b, (rq - 4 * nb_a) / 4, (rq - 4 * nb_a) % 4, k, z);
+  }
+}
+
 // [i][t] operands (rows i = head index, columns t = token, the contraction
-// index of the state updates) keep each row's 4-element quads permuted:
-// element (i, t) sits at quad (t / 4) ^ ((i / 16) mod 4) of row i.  The row
-// phases write these arrays one element per lane with 16 lanes on rows 4
-// apart; unpermuted, those rows fall on 4 LDS banks (a 4-way conflict on every
-// such store), permuted on 16.  Fragment reads stay single paired loads: the
-// permutation only moves the lane's quad within its K-step.
+// index of the state updates).  On the bf16 path they use the quad layout of
+// the hidden-index operands above with the token as the K index: quad (head
+// block b, head quad q, token t) holds heads 16 b + 4 q .. + 3 of token t, so
+// a row phase that holds four consecutive head indices of one token writes
+// them with one 8-byte store, and a fragment comes back through the
+// transposing reads.  On the fp32 path each row's 4-element quads are
+// permuted instead: element (i, t) sits at quad (t / 4) ^ ((i / 16) mod 4) of
+// row i, so that the element stores of 16 lanes on rows 4 apart fall on 16
+// LDS banks rather than 4; fragment reads stay single paired loads (the
+// permutation only moves the lane's quad within its K-step).
 template <class S>
 __device__ __forceinline__ int it_idx(int i, int t) {
   return i * S::LDC + ((((t >> 2) ^ (i >> 4)) & 3) | ((t >> 2) & ~3)) * 4 + (t & 3);
@@ -351,7 +422,8 @@ __device__ __forceinline__ int it_idx(int i, int t) {
 template <class S>
 __device__ __forceinline__ typename S::O::Frag it_frag(const typename S::E* base, int row, int k0,
                                                        int g) {
-  return lds_frag<S::BF>(base, S::LDC, row, k0, g ^ ((row >> 4) & 3));
+  if constexpr (S::BF) return jq_frag<S>(jq_lane<S, S::LDC>(base, row >> 4, g, row & 15), k0);
+  else return lds_frag<S::BF>(base, S::LDC, row, k0, g ^ ((row >> 4) & 3));
 }
 
 // Row-phase stores: a lane holds EPL consecutive head indices i0 .. i0+EPL-1
@@ -378,18 +450,19 @@ __device__ __forceinline__ void store_row_ti(typename S::E* dst, int ld, int t, 
 template <class S, int EPL>
 __device__ __forceinline__ void store_row_it(typename S::E* dst, int t, int i0,
                                              const float (&v)[EPL], float sc = 1.0f) {
-  static_assert(16 % EPL == 0, "a lane's head indices must lie in one 16-row block");
-  const int b = it_idx<S>(i0, t);
-  if constexpr (S::BF && EPL % 2 == 0) {
-    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-    typedef __attribute__((ext_vector_type(2))) float f32x2;
+  static_assert(16 % EPL == 0 || EPL % 16 == 0, "a lane's head indices in whole 16-row blocks");
+  if constexpr (S::BF && EPL % 4 == 0) {
+    // bf16: four consecutive head indices of one token are one quad of the
+    // transposed-read layout: one 8-byte store each
 #pragma unroll
-    for (int q = 0; q < EPL; q += 2) {
-      const bf16x2 pr = __builtin_convertvector(f32x2{sc * v[q], sc * v[q + 1]}, bf16x2);
-      dst[b + q * S::LDC] = pr[0];
-      dst[b + (q + 1) * S::LDC] = pr[1];
+    for (int k = 0; k < EPL / 4; ++k) {
+      const int i = i0 + 4 * k;
+      jq_put<S, S::LDC>(dst, i >> 4, (i >> 2) & 3, t,
+                        S::O::cvt(f32x4{sc * v[4 * k], sc * v[4 * k + 1], sc * v[4 * k + 2],
+                                        sc * v[4 * k + 3]}));
     }
   } else {
+    const int b = it_idx<S>(i0, t);
 #pragma unroll
     for (int q = 0; q < EPL; ++q) dst[b + q * S::LDC] = S::O::to_e(sc * v[q]);
   }
@@ -413,6 +486,17 @@ __device__ __forceinline__ void store_row_io(typename IO::T* dst, const float (&
 template <class S>
 __device__ __forceinline__ void transpose_to_it(typename S::E* dst, const typename S::E* src,
                                                 int tid) {
+  if constexpr (S::BF) {
+    // bf16: a row quad of [t][i] (four consecutive head indices of one token)
+    // is a quad of the transposed-read layout as it stands: copied whole
+#pragma unroll 1
+    for (int idx = tid; idx < S::CM * (S::D / 4); idx += S::NT) {
+      const int t = idx / (S::D / 4), i = 4 * (idx % (S::D / 4));
+      jq_put<S, S::LDC>(dst, i >> 4, (i >> 2) & 3, t,
+                        *reinterpret_cast<const typename S::O::Q*>(src + t * S::LDD + i));
+    }
+    return;
+  }
 #pragma unroll 1
   for (int idx = tid; idx < S::D * (S::CM / 4); idx += S::NT) {
     const int i = idx % S::D, t0 = 4 * (idx / S::D);
@@ -494,73 +578,6 @@ struct F32TileRegs {
       if (tid + k * S::NT < NV) reinterpret_cast<float4*>(dst)[tid + k * S::NT] = v[k];
   }
 };
-
-// Operands of the contractions over the hidden index (the forward's Y = A W2^T,
-// the backward's j-rounds).  Both operands (activations [t][j], weights [i][j])
-// come from accumulator-layout tiles: lane (g, c) of a wave holds rows
-// 4 g .. 4 g + 3 of a 16-row block at one hidden column.  On the bf16 path
-// that quad is stored with one 8-byte write, quad (block b, row quad q, hidden
-// column k) at quad offset (4 b + q) LD + k (the bytes of a [16 NB][LD]
-// array), and a lane's operand fragment (row c of block b, contraction indices
-// k0 + 16 h + 4 g + 0..3 for h = 0, 1, the order lds_frag reads) comes back
-// through two transposing LDS reads (ds_read_b64_tr_b16: within each group of
-// 16 lanes, lane c receives element c mod 4 of the quads addressed by lanes
-// 4 r + c / 4, r = 0..3; measured on the MI355X).  With LD = 4 (mod 16) the
-// stores (16 lanes on 16 consecutive quads) and the reads (four quad rows, four
-// consecutive quads each) fall on 32 distinct banks.  On the fp32 path the
-// arrays stay row-major, one element per store.
-template <class S, int LD>
-__device__ __forceinline__ void jq_put(typename S::E* buf, int blk, int g, int k,
-                                       const typename S::O::Q& v) {
-  static_assert(!S::BF || LD % 16 == 4, "bf16 quad rows 4 (mod 16) quads apart");
-  if constexpr (S::BF) {
-    *reinterpret_cast<typename S::O::Q*>(buf + ((4 * blk + g) * LD + k) * 4) = v;
-  } else {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) buf[(16 * blk + 4 * g + r) * LD + k] = v[r];
-  }
-}
-// A lane's read position in block blk of a j-round operand array (formed once
-// per block; the K-steps then add constant offsets).
-template <class S, int LD>
-__device__ __forceinline__ const typename S::E* jq_lane(const typename S::E* buf, int blk, int g,
-                                                        int c) {
-  if constexpr (S::BF) return buf + ((4 * blk + (c & 3)) * LD + 4 * g + (c >> 2)) * 4;
-  else return buf + (16 * blk + c) * LD + 4 * g;
-}
-// The operand fragment at K-step offset k0 from a lane's read position.
-template <class S>
-__device__ __forceinline__ typename S::O::Frag jq_frag(const typename S::E* pos, int k0) {
-  typename S::O::Frag f;
-  if constexpr (S::BF) {
-    typedef short s4 __attribute__((ext_vector_type(4)));
-    typedef __attribute__((address_space(3))) s4* lds_s4;
-#pragma unroll
-    for (int h = 0; h < S::O::NH; ++h) {
-      typename S::E* p = const_cast<typename S::E*>(pos) + (k0 + 16 * h) * 4;
-      f.h[h] = __builtin_bit_cast(typename S::O::Q, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)p));
-    }
-  } else {
-#pragma unroll
-    for (int h = 0; h < S::O::NH; ++h)
-      f.h[h] = *reinterpret_cast<const typename S::O::Q*>(pos + k0 + 16 * h);
-  }
-  return f;
-}
-// Zero quads at hidden columns [k_lo, KW) of nb_a + nb_w 16-row blocks of two
-// operand arrays (columns no wave owns must read as zero).
-template <class S, int LD, int KW>
-__device__ __forceinline__ void jq_zero_cols(typename S::E* a, int nb_a, typename S::E* b, int nb_w,
-                                             int k_lo) {
-  const int nz = KW - k_lo;
-  const typename S::O::Q z = S::O::cvt(zero4());
-#pragma unroll 1
-  for (int idx = threadIdx.x; idx < 4 * (nb_a + nb_w) * nz; idx += S::NT) {
-    const int rq = idx / nz, k = k_lo + idx % nz;
-    if (rq < 4 * nb_a) jq_put<S, LD>(a, rq / 4, rq % 4, k, z);
-    else jq_put<S, LD>(b, (rq - 4 * nb_a) / 4, (rq - 4 * nb_a) % 4, k, z);
-  }
-}
 
 // Y[t][i] = sum_j A[t][j] Wt[i][j]  (j-contraction, both operands in LDS as
 // quads, stored with jq_put<S, S::LDH>),
