@@ -177,10 +177,13 @@ def test_split_workspace_sizes(lib):
     ws_save = lib.e2ttt_workspace_bytes(ctypes.byref(d), 1)
     sc = lib.e2ttt_backward_scratch_bytes(ctypes.byref(d))
     tok = U * T * 4
-    assert ws >= 2 * tok + U * NC * 3 * 4 + 128 * 2 * 2 * 2 * 64 * 64 * 4
+    # forward slots per rank: two Y_K parities and one Y_Q, fp32 [C][d] each
+    assert ws >= 2 * tok + U * NC * 3 * 4 + 128 * 2 * 3 * 64 * 64 * 4
     # checkpoints of W and M (bf16, both ranks) plus Z and 1/sigma of both passes
     assert ws_save - ws >= U * NC * 2 * 2 * 64 * 256 * 2 + 2 * (tok * 64 + tok)
-    assert sc >= 2 * (2 * tok + U * NC * 3 * 4) + 128 * 2 * 2 * 3 * 64 * 64 * 4
+    # backward slots per rank: two parities of the fp32 dYh partial and of the
+    # bf16 dk, dq partials
+    assert sc >= 2 * (2 * tok + U * NC * 3 * 4) + 128 * 2 * 2 * (64 * 64 * 4 + 2 * 64 * 64 * 2)
 
 
 def test_gate_argument_errors(lib):
