@@ -278,8 +278,10 @@ __device__ __forceinline__ void jacc_store_io(const JAcc<S>& out, void* dst, lon
   }
 }
 
-// Write the j-round output tiles to an E [CM][D] buffer (a slot's dk or dq
-// partial): dst[t][i] = out + extra(t, i), rounded to E.
+// Write the j-round output tiles to a slot's dk or dq partial: out + extra(t, i),
+// rounded to E, in accumulator order: the quad at quad offset (t / 4) D + i
+// holds rows 4 (t / 4) .. + 3 of column i (one 8- or 16-byte store per tile
+// and lane instead of four element stores).
 template <class S, class FX>
 __device__ __forceinline__ void jacc_store_part(const JAcc<S>& out, typename S::E* dst, FX extra,
                                                 int w, int g, int c) {
@@ -291,12 +293,13 @@ __device__ __forceinline__ void jacc_store_part(const JAcc<S>& out, typename S::
     if (it < L::NITEM) {
       const int tb = it / NI, ib0 = (it % NI) * S::IBB;
 #pragma unroll
-      for (int b = 0; b < S::IBB; ++b)
+      for (int b = 0; b < S::IBB; ++b) {
+        const int i = 16 * (ib0 + b) + c;
+        f32x4 v;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = 16 * tb + 4 * g + r, i = 16 * (ib0 + b) + c;
-          dst[t * S::D + i] = S::O::to_e(out.v[a][b][r] + extra(t, i));
-        }
+        for (int r = 0; r < 4; ++r) v[r] = out.v[a][b][r] + extra(16 * tb + 4 * g + r, i);
+        *reinterpret_cast<typename S::O::Q*>(dst + ((4 * tb + g) * S::D + i) * 4) = S::O::cvt(v);
+      }
     }
   }
 }
@@ -340,20 +343,25 @@ __device__ __forceinline__ typename S::E* bwd_part(float* slot, int sec) {
 }
 
 // dk and dq of one chunk from the ranks' partials, added in rank order (rank
-// 0's carries the -eh and dO terms), rows [rlo, min(CM, rlo + RPW)) below len.
+// 0's carries the -eh and dO terms), rows [rlo, min(CM, rlo + RPW)) below len
+// (rlo and RPW are multiples of 4).  An item is one row quad of one column:
+// one quad load per rank, four element stores, each coalesced over the wave's
+// 64 consecutive columns.
 template <class S>
 __device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int len, int rlo,
                                            int tid) {
   using IO = IoT<S::BF>;
   constexpr int RPW = row_share<S>();
-  constexpr int NV = RPW * S::D / 4;
+  static_assert(RPW % 4 == 0, "row shares in whole row quads");
+  constexpr int NV = (RPW / 4) * S::D;
   const int tend = min(len, min(S::CM, rlo + RPW));
   typename IO::T* dk = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dk)) + row0 * S::D;
   typename IO::T* dq = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dq)) + row0 * S::D;
 #pragma unroll 1
   for (int v = tid; v < NV; v += S::NT) {
-    const int e = rlo * S::D + 4 * v, t = e / S::D;
-    if (t >= tend) continue;
+    const int tq = rlo / 4 + v / S::D, i = v % S::D;
+    if (4 * tq >= tend) continue;
+    const long e = ((long)tq * S::D + i) * 4;
 #pragma unroll
     for (int sec = 1; sec <= 2; ++sec) {
       f32x4 x = quad_f32(*reinterpret_cast<const typename S::O::Q*>(
@@ -363,7 +371,9 @@ __device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int le
         x += quad_f32(*reinterpret_cast<const typename S::O::Q*>(
             bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec) + e));
       typename IO::T* d = (sec == 1) ? dk : dq;
-      IO::st4(d + e, x);
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (4 * tq + r < tend) IO::st(d + (4 * tq + r) * S::D + i, x[r]);
     }
   }
 }
