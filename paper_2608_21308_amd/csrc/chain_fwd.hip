@@ -384,7 +384,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * S::NW;
             if (t0 < S::CM)
-              load_row_part<EPL>(pyv[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+              load_row_xchg<EPL>(pyv[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
           }
         }
       } else {
@@ -446,7 +446,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_part<EPL>(pr, fwd_slot_k<S, NPK>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
+              load_row_xchg<EPL>(pr, fwd_slot_k<S, NPK>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
                                          l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
@@ -541,7 +541,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int it_ = 0; it_ < NITO; ++it_) {
             const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
             if (t0 < rhi)
-              load_row_part<EPL>(pyq[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+              load_row_xchg<EPL>(pyq[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
           }
         }
       } else {
@@ -711,7 +711,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           px.wait_for(px.seq_now(), sm.word);
           if (tid < D) {
             tot = 0.0f;
-            for (int rr = 0; rr < S::NS; ++rr) tot += nx[((px.xs * S::NS + rr) * 2 + par) * D + tid];
+            for (int rr = 0; rr < S::NS; ++rr) tot += ld_xchg(&nx[((px.xs * S::NS + rr) * 2 + par) * D + tid]);
           }
         }
         if (tid < D) {
@@ -757,7 +757,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_part<EPL>(pr, fwd_slot_q<S, NPK>(E2TTT_ARG(xbuf), px.xs, r) + t * D +
+              load_row_xchg<EPL>(pr, fwd_slot_q<S, NPK>(E2TTT_ARG(xbuf), px.xs, r) + t * D +
                                          l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];

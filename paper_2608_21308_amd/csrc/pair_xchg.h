@@ -13,11 +13,16 @@
 // plain stores of the data, s_waitcnt vmcnt(0) (the stores have reached L2,
 // the L1 being write-through), a workgroup barrier, then a device-scope store
 // of the flag; the wait is: a device-scope poll of the peers' flags, a
-// barrier, then an invalidation of this CU's L1 (buffer_inv sc0) before plain
-// loads of the peers' data.  At kernel start the ranks swap their hardware XCC
-// ids with device-scope accesses; if they differ (another dispatch order),
-// every post and wait of that group uses agent-scope release / acquire fences
-// instead, which are coherent across XCDs but write back and invalidate the L2.
+// barrier, then device-scope loads of the peers' data (ld_xchg: they skip
+// this CU's L1 and read the shared L2).  Plain loads would not do: measured on
+// the MI355X, a plain load keeps returning a line that another CU of the same
+// XCD has since overwritten, also after the workgroup-scope invalidate
+// (buffer_inv sc0); the agent-scope invalidate (buffer_inv sc1) makes them
+// correct but drops L2 contents the chain kernels still use, which doubled
+// their time.  At kernel start the ranks swap their hardware XCC ids with
+// device-scope accesses; if they differ (another dispatch order), every post
+// and wait of that group also uses the agent-scope release / acquire fences,
+// which write back and invalidate the L2 for the other XCD.
 //
 // Every wait is bounded (by default kTimeoutTicks of the 100 MHz real-time
 // counter; the host passes the limit with the launch).  A
@@ -194,9 +199,43 @@ template <int NS> struct PairX {
     __syncthreads();
     if (was_dead) return;
     if (s_word[0] == 0) dead = true;
-    if (same_xcc) asm volatile("buffer_inv sc0" ::: "memory");
-    else __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (!same_xcc) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
 };
+
+// Loads of data that another workgroup of the launch has written (exchange
+// slots, norm partials): relaxed device-scope atomic loads, 8 bytes each
+// (global_load_dwordx2 sc1), which never hit a stale line in this CU's L1.
+template <class T>
+__device__ __forceinline__ T ld_xchg(const T* p) {
+  static_assert(sizeof(T) % 8 == 0 || sizeof(T) == 4, "4 bytes or whole 8-byte words");
+  if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(
+        T, __hip_atomic_load(reinterpret_cast<const unsigned*>(p), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT));
+  } else {
+    struct W { unsigned long long w[sizeof(T) / 8]; } x;
+#pragma unroll
+    for (int k = 0; k < (int)(sizeof(T) / 8); ++k)
+      x.w[k] = __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p) + k,
+                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return __builtin_bit_cast(T, x);
+  }
+}
+// EPL consecutive floats of an exchange row (8-byte aligned when EPL is even).
+template <int EPL>
+__device__ __forceinline__ void load_row_xchg(float (&dst)[EPL], const float* src) {
+  if constexpr (EPL % 2 == 0) {
+#pragma unroll
+    for (int k = 0; k < EPL / 2; ++k) {
+      const float2 v = ld_xchg(reinterpret_cast<const float2*>(src) + k);
+      dst[2 * k] = v.x;
+      dst[2 * k + 1] = v.y;
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) dst[q] = ld_xchg(src + q);
+  }
+}
 
 }  // namespace e2ttt
