@@ -989,7 +989,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
 
       // ------------------------------------- P7: LayerNorm second order
-      prefetch_q(u, rc, kc);
       {
         E2TTT_LANE_IDS;
         using IOT = typename IoT<S::BF>::T;
@@ -1089,6 +1088,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
                   }
         }
       }
+      // the output branch's tiles, issued after the row steps above: issued
+      // before them, the wait for the peers' rows (whose count of later memory
+      // operations the compiler loses over the flush loop) waited for these
+      // loads from HBM as well
+      prefetch_q(u, rc, kc);
       __syncthreads();
 
       // ---------- P8: Hh += (Yh W2) act'(H); accumulate into Wb; dk = r1 - eh + Hh W1
