@@ -1093,6 +1093,23 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       // operations the compiler loses over the flush loop) waited for these
       // loads from HBM as well
       prefetch_q(u, rc, kc);
+      // MLP: A_Q and GELU'(H_Q) as the forward formed them (its query side at
+      // W_0, GELU' packed), in flight during P8
+      Q Aqq[NTB][NJB];
+      typename DerivQ<S::BF>::T D1p[SW ? 1 : NTB][SW ? 1 : NJB];
+      if constexpr (!SW) {
+        E2TTT_LANE_IDS;
+        const SavedAct<S> sv(static_cast<char*>(E2TTT_ARG(asave)) +
+                             (((u * NC + rc) * TPC + kc) * S::NS + rank) * E2TTT_ARG(as_stride));
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+          for (int jj = 0; jj < NJB; ++jj) {
+            const int qi = SavedAct<S>::idx(tb, jj, w, lane);
+            Aqq[tb][jj] = ld_stream(sv.aq() + qi);
+            D1p[tb][jj] = ld_stream(sv.d1q() + qi);
+          }
+      }
       __syncthreads();
 
       // ---------- P8: Hh += (Yh W2) act'(H); accumulate into Wb; dk = r1 - eh + Hh W1
@@ -1186,23 +1203,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         E* ybq = yh;                                     // Yb_Q [t][i]
         E* ybqt = dyt;                                   // Yb_Q^T [i][t]
         E* xqt = yht;                                    // Q^T [i][t]
-        f32x4 D1q[NF][NTB][NJB];   // act'(H_Q) factors, as D1 above
-        Q Aqq[NTB][NJB];
-        if constexpr (!SW) {
-          // A_Q and GELU'(H_Q) as the forward formed them (its query side at
-          // W_0), loaded now so that they arrive under the staging and the
-          // Yb_Q row phase below
-          const SavedAct<S> sv(static_cast<char*>(E2TTT_ARG(asave)) +
-                               (((u * NC + rc) * TPC + kc) * S::NS + rank) * E2TTT_ARG(as_stride));
-#pragma unroll
-          for (int tb = 0; tb < NTB; ++tb)
-#pragma unroll
-            for (int jj = 0; jj < NJB; ++jj) {
-              const int qi = SavedAct<S>::idx(tb, jj, w, lane);
-              Aqq[tb][jj] = ld_stream(sv.aq() + qi);
-              D1q[0][tb][jj] = DerivQ<S::BF>::unpack(ld_stream(sv.d1q() + qi));
-            }
-        }
+        // act'(H_Q) factors, as D1 above (SwiGLU: recomputed below; the MLP's
+        // GELU'(H_Q) was loaded packed with A_Q at the end of P7)
+        f32x4 D1q[SW ? NF : 1][SW ? NTB : 1][SW ? NJB : 1];
         pQ.store(xq, tid);
         pD.store(xdo, tid);
         pZq.store(yk, tid);                             // Z_Q (or Y_Q)
@@ -1297,10 +1300,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
                 ab = O::mma(ab, af, bf);
               }
               f32x4 hb[NF];
+              if constexpr (SW) {
 #pragma unroll
-              for (int q = 0; q < 4; ++q) {
+                for (int q = 0; q < 4; ++q)
 #pragma unroll
-                for (int m = 0; m < NF; ++m) hb[m][q] = ab[q] * D1q[m][tb][jj][q];
+                  for (int m = 0; m < NF; ++m) hb[m][q] = ab[q] * D1q[m][tb][jj][q];
+              } else {
+                const f32x4 d1 = DerivQ<S::BF>::unpack(D1p[tb][jj]);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) hb[0][q] = ab[q] * d1[q];
               }
 #pragma unroll
               for (int m = 0; m < NF; ++m) Hbq[m][tb][jj] = O::cvt(hb[m]);
