@@ -164,7 +164,14 @@ template <int NS> struct PairX {
 
   // Publish everything this workgroup stored before the call.  All threads call.
   __device__ void post() {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // vmcnt(0) through the builtin (encoding 0x0F70: vmcnt 0, expcnt and
+    // lgkmcnt unconstrained), which the compiler's own wait tracking sees: an
+    // inline-asm wait leaves it believing that loads issued before the post
+    // are still in flight, and the first use of one then waits for every
+    // memory operation issued after the post as well.  The empty asm keeps
+    // the compiler from moving stores below the wait.
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
     ++seq;
     if (threadIdx.x == 0 && !dead) {
