@@ -989,6 +989,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
 
       // ------------------------------------- P7: LayerNorm second order
+      // every earlier memory operation complete (the first row step waits for
+      // the peers' rows, issued before the flush, anyway): stated through the
+      // builtin, so that the compiler knows it and the second row step does
+      // not wait again, for the tile loads issued between the steps
+      __builtin_amdgcn_s_waitcnt(0x0F70);
       {
         E2TTT_LANE_IDS;
         using IOT = typename IoT<S::BF>::T;
@@ -1086,13 +1091,14 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           store_row_ti<S, EPL>(yh, S::LDD, t, l16 * EPL, yhv);
           store_row_it<S, EPL>(yht, t, l16 * EPL, yhv);
                   }
+          // the output branch's tiles, issued after the first row step: issued
+          // before it, the wait for the peers' rows (whose count of later
+          // memory operations the compiler loses over the flush loop) waited
+          // for these loads from HBM as well; issued here, they drain from the
+          // memory pipeline while the next row step computes
+          if (it_ == 0) prefetch_q(u, rc, kc);
         }
       }
-      // the output branch's tiles, issued after the row steps above: issued
-      // before them, the wait for the peers' rows (whose count of later memory
-      // operations the compiler loses over the flush loop) waited for these
-      // loads from HBM as well
-      prefetch_q(u, rc, kc);
       // MLP: A_Q and GELU'(H_Q) as the forward formed them (its query side at
       // W_0, GELU' packed), in flight during P8
       Q Aqq[NTB][NJB];
