@@ -361,15 +361,15 @@ __device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int le
   for (int v = tid; v < NV; v += S::NT) {
     const int tq = rlo / 4 + v / S::D, i = v % S::D;
     if (4 * tq >= tend) continue;
-    const long e = ((long)tq * S::D + i) * 4;
+    const int eq = tq * S::D + i;   // quad index
 #pragma unroll
     for (int sec = 1; sec <= 2; ++sec) {
-      f32x4 x = quad_f32(ld_xchg(reinterpret_cast<const typename S::O::Q*>(
-          bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, 0, parity), sec) + e)));
+      f32x4 x = quad_f32(ld_xchg(E2TTT_ARG(xbuf), reinterpret_cast<const typename S::O::Q*>(
+          bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, 0, parity), sec)), eq));
 #pragma unroll
       for (int rk = 1; rk < S::NS; ++rk)
-        x += quad_f32(ld_xchg(reinterpret_cast<const typename S::O::Q*>(
-            bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec) + e)));
+        x += quad_f32(ld_xchg(E2TTT_ARG(xbuf), reinterpret_cast<const typename S::O::Q*>(
+            bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec)), eq));
       typename IO::T* d = (sec == 1) ? dk : dq;
 #pragma unroll
       for (int r = 0; r < 4; ++r)
@@ -583,7 +583,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           px.wait_for(px.seq_now(), sword);
           if (tid < D) {
             A = 0.0f;
-            for (int rr = 0; rr < S::NS; ++rr) A += ld_xchg(&nx[((px.xs * S::NS + rr) * 2 + par) * D + tid]);
+            for (int rr = 0; rr < S::NS; ++rr)
+              A += ld_xchg(nx, nx + ((px.xs * S::NS + rr) * 2 + par) * D, tid);
           }
         }
         if (tid < D) {
@@ -981,7 +982,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           for (int it_ = 0; it_ < P7IT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * NW;
             if (t0 < S::CM)
-              load_row_xchg<EPL>(pdyh[it_][k], dyh_peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+              load_row_xchg<EPL>(pdyh[it_][k], E2TTT_ARG(xbuf), dyh_peer,
+                                 (t0 + (lane >> 4)) * D + l16 * EPL);
           }
         }
         if (pend_s0 >= 0)
@@ -1023,8 +1025,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_xchg<EPL>(pr, bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
-                                         l16 * EPL);
+              load_row_xchg<EPL>(pr, E2TTT_ARG(xbuf),
+                                 bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par), t * D + l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) dyhv[q] = (r == 0) ? pr[q] : dyhv[q] + pr[q];
             }

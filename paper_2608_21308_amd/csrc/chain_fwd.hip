@@ -251,7 +251,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       opaque_state<S>(M);
       }
       __syncthreads();
-      if (r < NC) prefetch(u, r, kt);              // the next tile (r, kt advanced above)
+      // the next tile (r, kt advanced above): at head dim 64 issued inside the
+      // K-side below, after its first token block, so that it drains from the
+      // memory pipeline under the others; the head-dim-128 kernels have no
+      // registers to hold it there
+      constexpr bool PF_IN_K = S::D <= 64;
+      if (!PF_IN_K && r < NC) prefetch(u, r, kt);
 
       // operand of the chunk's products (W_0: W is not updated before the chunk end
       // on the fp32 path, nor before the transition below on the others)
@@ -310,6 +315,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           if constexpr (S::FW == 1) Hu[tb][jj] = d2;
           AK[tb][jj] = O::cvt(act);
           jq_put<S, S::LDH>(sm.alds, tb, g, 16 * (w * NJB + jj) + c, AK[tb][jj]);
+          if (PF_IN_K && tb == 0 && jj == NJB - 1 && r < NC) prefetch(u, r, kt);
           sched_fence();
         }
       }
@@ -384,7 +390,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int it_ = 0; it_ < NIT; ++it_) {
             const int t0 = 4 * w + it_ * 4 * S::NW;
             if (t0 < S::CM)
-              load_row_xchg<EPL>(pyv[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+              load_row_xchg<EPL>(pyv[it_][k], E2TTT_ARG(xbuf), peer,
+                                 (t0 + (lane >> 4)) * D + l16 * EPL);
           }
         }
       } else {
@@ -446,8 +453,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_xchg<EPL>(pr, fwd_slot_k<S, NPK>(E2TTT_ARG(xbuf), px.xs, r, par) + t * D +
-                                         l16 * EPL);
+              load_row_xchg<EPL>(pr, E2TTT_ARG(xbuf),
+                                 fwd_slot_k<S, NPK>(E2TTT_ARG(xbuf), px.xs, r, par),
+                                 t * D + l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
             }
@@ -541,7 +549,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           for (int it_ = 0; it_ < NITO; ++it_) {
             const int t0 = rlo + 4 * w + it_ * 4 * S::NW;
             if (t0 < rhi)
-              load_row_xchg<EPL>(pyq[it_][k], peer + (t0 + (lane >> 4)) * D + l16 * EPL);
+              load_row_xchg<EPL>(pyq[it_][k], E2TTT_ARG(xbuf), peer,
+                                 (t0 + (lane >> 4)) * D + l16 * EPL);
           }
         }
       } else {
@@ -711,7 +720,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           px.wait_for(px.seq_now(), sm.word);
           if (tid < D) {
             tot = 0.0f;
-            for (int rr = 0; rr < S::NS; ++rr) tot += ld_xchg(&nx[((px.xs * S::NS + rr) * 2 + par) * D + tid]);
+            for (int rr = 0; rr < S::NS; ++rr)
+              tot += ld_xchg(nx, nx + ((px.xs * S::NS + rr) * 2 + par) * D, tid);
           }
         }
         if (tid < D) {
@@ -757,8 +767,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
 #pragma unroll
             for (int r = 0; r < S::NS; ++r) {
               float pr[EPL];
-              load_row_xchg<EPL>(pr, fwd_slot_q<S, NPK>(E2TTT_ARG(xbuf), px.xs, r) + t * D +
-                                         l16 * EPL);
+              load_row_xchg<EPL>(pr, E2TTT_ARG(xbuf), fwd_slot_q<S, NPK>(E2TTT_ARG(xbuf), px.xs, r),
+                                 t * D + l16 * EPL);
 #pragma unroll
               for (int q = 0; q < EPL; ++q) yv[q] = (r == 0) ? pr[q] : yv[q] + pr[q];
             }

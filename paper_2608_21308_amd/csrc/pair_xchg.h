@@ -211,38 +211,47 @@ template <int NS> struct PairX {
 };
 
 // Loads of data that another workgroup of the launch has written (exchange
-// slots, norm partials): relaxed device-scope atomic loads, 8 bytes each
-// (global_load_dwordx2 sc1), which never hit a stale line in this CU's L1.
+// slots, norm partials): buffer loads with the device-scope bit (sc1), which
+// never hit a stale line in this CU's L1, one instruction of up to 16 bytes.
+// `buf` is the exchange buffer (the kernel argument: one scalar descriptor
+// for every slot; 0x00020000 is the descriptor's fourth word for raw buffer
+// access on this GPU family), `base` the wave's slot in it (its byte offset
+// goes into the instruction's scalar offset) and `off` the lane's element
+// offset from `base`.  Offsets stay far below 2 GiB (the buffers hold a few
+// C x d partials per workgroup).
 template <class T>
-__device__ __forceinline__ T ld_xchg(const T* p) {
-  static_assert(sizeof(T) % 8 == 0 || sizeof(T) == 4, "4 bytes or whole 8-byte words");
+__device__ __forceinline__ T ld_xchg(const void* buf, const T* base, int off) {
+  static_assert(sizeof(T) == 4 || sizeof(T) == 8 || sizeof(T) == 16, "4, 8 or 16 bytes");
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(buf), 0, 0x7fffffff, 0x00020000);
+  constexpr int kSc1 = 16;   // cache-policy operand: the device-scope bit
+  const int sbyte = (int)(reinterpret_cast<const char*>(base) - static_cast<const char*>(buf));
+  const int vbyte = off * (int)sizeof(T);
   if constexpr (sizeof(T) == 4) {
-    return __builtin_bit_cast(
-        T, __hip_atomic_load(reinterpret_cast<const unsigned*>(p), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT));
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, vbyte, sbyte, kSc1));
+  } else if constexpr (sizeof(T) == 8) {
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b64(r, vbyte, sbyte, kSc1));
   } else {
-    struct W { unsigned long long w[sizeof(T) / 8]; } x;
-#pragma unroll
-    for (int k = 0; k < (int)(sizeof(T) / 8); ++k)
-      x.w[k] = __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p) + k,
-                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return __builtin_bit_cast(T, x);
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b128(r, vbyte, sbyte, kSc1));
   }
 }
-// EPL consecutive floats of an exchange row (8-byte aligned when EPL is even).
+// EPL consecutive floats of an exchange row at element offset `off` from the
+// slot `base` in `buf` (16-byte aligned when EPL is a multiple of 4).
 template <int EPL>
-__device__ __forceinline__ void load_row_xchg(float (&dst)[EPL], const float* src) {
-  if constexpr (EPL % 2 == 0) {
+__device__ __forceinline__ void load_row_xchg(float (&dst)[EPL], const void* buf,
+                                              const float* base, int off) {
+  if constexpr (EPL % 4 == 0) {
 #pragma unroll
-    for (int k = 0; k < EPL / 2; ++k) {
-      const float2 v = ld_xchg(reinterpret_cast<const float2*>(src) + k);
-      dst[2 * k] = v.x;
-      dst[2 * k + 1] = v.y;
+    for (int k = 0; k < EPL / 4; ++k) {
+      const float4 v = ld_xchg(buf, reinterpret_cast<const float4*>(base), off / 4 + k);
+      dst[4 * k] = v.x; dst[4 * k + 1] = v.y; dst[4 * k + 2] = v.z; dst[4 * k + 3] = v.w;
     }
   } else {
 #pragma unroll
-    for (int q = 0; q < EPL; ++q) dst[q] = ld_xchg(src + q);
+    for (int q = 0; q < EPL; ++q) dst[q] = ld_xchg(buf, base, off + q);
   }
 }
+
+
 
 }  // namespace e2ttt
