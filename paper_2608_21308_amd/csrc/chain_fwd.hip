@@ -251,12 +251,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
       opaque_state<S>(M);
       }
       __syncthreads();
-      // the next tile (r, kt advanced above): at head dim 64 issued inside the
-      // K-side below, after its first token block, so that it drains from the
-      // memory pipeline under the others; the head-dim-128 kernels have no
-      // registers to hold it there
-      constexpr bool PF_IN_K = S::D <= 64;
-      if (!PF_IN_K && r < NC) prefetch(u, r, kt);
+      if (r < NC) prefetch(u, r, kt);              // the next tile (r, kt advanced above)
 
       // operand of the chunk's products (W_0: W is not updated before the chunk end
       // on the fp32 path, nor before the transition below on the others)
@@ -315,7 +310,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_fwd_kernel(ChainArgs a) {
           if constexpr (S::FW == 1) Hu[tb][jj] = d2;
           AK[tb][jj] = O::cvt(act);
           jq_put<S, S::LDH>(sm.alds, tb, g, 16 * (w * NJB + jj) + c, AK[tb][jj]);
-          if (PF_IN_K && tb == 0 && jj == NJB - 1 && r < NC) prefetch(u, r, kt);
           sched_fence();
         }
       }
