@@ -274,8 +274,9 @@ e2ttt_status e2ttt_gates_backward(const e2ttt_gate_params* params, int64_t n,
  * results are undefined), E2TTT_OK otherwise (always for descriptors that run
  * one workgroup per unit).  Each call clears its buffer's word when it starts.
  * The wait limit is 2 s; the environment variable E2TTT_WAIT_LIMIT_US (a
- * decimal count of microseconds, read at every call) sets another, which lets
- * a test make waits give up without any kernel failing.
+ * decimal count of microseconds, read at every call) sets another; a limit of
+ * 0 makes every wait give up before it reads the peer's flag, which lets a
+ * test force the expiry without any kernel failing.
  */
 e2ttt_status e2ttt_wait_status(const e2ttt_desc* desc, const void* workspace,
                                const void* scratch, void* stream);

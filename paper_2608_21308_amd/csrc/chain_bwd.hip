@@ -346,36 +346,62 @@ __device__ __forceinline__ typename S::E* bwd_part(float* slot, int sec) {
 // 0's carries the -eh and dO terms), rows [rlo, min(CM, rlo + RPW)) below len
 // (rlo and RPW are multiples of 4).  An item is one row quad of one column:
 // one quad load per rank, four element stores, each coalesced over the wave's
-// 64 consecutive columns.
+// 64 consecutive columns.  load() reads and adds the partials, store() writes
+// the rows, so that the stores can go out later than the loads.
+template <class S>
+struct FlushDkDq {
+  static constexpr int RPW = row_share<S>();
+  static_assert(RPW % 4 == 0, "row shares in whole row quads");
+  static constexpr int NV = (RPW / 4) * S::D;
+  static constexpr int NPT = (NV + S::NT - 1) / S::NT;   // items per thread
+  f32x4 x[NPT][2];
+
+  __device__ __forceinline__ void load(long p, int parity, int tid) {
+#pragma unroll
+    for (int a = 0; a < NPT; ++a) {
+      // the item's quad; items past the rank's share or the tile (the last
+      // rank's share may extend beyond CM rows) read quad 0 and are not stored
+      const int qi = q0 + tid + a * S::NT;
+      const int qs = (tid + a * S::NT < NV && qi < (S::CM / 4) * S::D) ? qi : 0;
+#pragma unroll
+      for (int sec = 1; sec <= 2; ++sec) {
+        x[a][sec - 1] = zero4();
+#pragma unroll
+        for (int rk = 0; rk < S::NS; ++rk)
+          x[a][sec - 1] += quad_f32(ld_xchg(E2TTT_ARG(xbuf),
+              reinterpret_cast<const typename S::O::Q*>(
+                  bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec)), qs));
+      }
+    }
+  }
+  __device__ __forceinline__ void store(long row0, int len, int rlo, int tid) const {
+    using IO = IoT<S::BF>;
+    const int tend = min(len, min(S::CM, rlo + RPW));
+    typename IO::T* dk = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dk)) + row0 * S::D;
+    typename IO::T* dq = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dq)) + row0 * S::D;
+#pragma unroll
+    for (int a = 0; a < NPT; ++a) {
+      const int v = tid + a * S::NT;
+      const int tq = rlo / 4 + v / S::D, i = v % S::D;
+      if (v >= NV || 4 * tq >= tend) continue;
+#pragma unroll
+      for (int sec = 1; sec <= 2; ++sec) {
+        typename IO::T* d = (sec == 1) ? dk : dq;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (4 * tq + r < tend) IO::st(d + (4 * tq + r) * S::D + i, x[a][sec - 1][r]);
+      }
+    }
+  }
+  int q0 = 0;   // quad index of the rank's first row quad, set with the loads
+};
 template <class S>
 __device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int len, int rlo,
                                            int tid) {
-  using IO = IoT<S::BF>;
-  constexpr int RPW = row_share<S>();
-  static_assert(RPW % 4 == 0, "row shares in whole row quads");
-  constexpr int NV = (RPW / 4) * S::D;
-  const int tend = min(len, min(S::CM, rlo + RPW));
-  typename IO::T* dk = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dk)) + row0 * S::D;
-  typename IO::T* dq = reinterpret_cast<typename IO::T*>(E2TTT_ARG(dq)) + row0 * S::D;
-#pragma unroll 1
-  for (int v = tid; v < NV; v += S::NT) {
-    const int tq = rlo / 4 + v / S::D, i = v % S::D;
-    if (4 * tq >= tend) continue;
-    const int eq = tq * S::D + i;   // quad index
-#pragma unroll
-    for (int sec = 1; sec <= 2; ++sec) {
-      f32x4 x = quad_f32(ld_xchg(E2TTT_ARG(xbuf), reinterpret_cast<const typename S::O::Q*>(
-          bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, 0, parity), sec)), eq));
-#pragma unroll
-      for (int rk = 1; rk < S::NS; ++rk)
-        x += quad_f32(ld_xchg(E2TTT_ARG(xbuf), reinterpret_cast<const typename S::O::Q*>(
-            bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec)), eq));
-      typename IO::T* d = (sec == 1) ? dk : dq;
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (4 * tq + r < tend) IO::st(d + (4 * tq + r) * S::D + i, x[r]);
-    }
-  }
+  FlushDkDq<S> f;
+  f.q0 = (rlo / 4) * S::D;
+  f.load(p, parity, tid);
+  f.store(row0, len, rlo, tid);
 }
 
 // LONG: chunks longer than the CM-row tile.  Their tiles are processed last
@@ -964,6 +990,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
       __syncthreads();
       constexpr int P7IT = (S::CM + 4 * NW - 1) / (4 * NW);
+      FlushDkDq<S> flush;
       float pdyh[S::NS > 1 && PEER_EARLY ? P7IT : 1][S::NS > 1 ? NPEER : 1][EPL];
       if constexpr (S::NS > 1) {
         E2TTT_LANE_IDS;
@@ -986,8 +1013,12 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
                                  (t0 + (lane >> 4)) * D + l16 * EPL);
           }
         }
-        if (pend_s0 >= 0)
-          flush_dkdq<S>(px.xs, pend_par, u * T + pend_s0, pend_len, rlo, tid);
+        // the previous chunk's dk / dq: partials read now (their latency
+        // overlaps the peers' rows'), rows written after P7's first row step
+        if (pend_s0 >= 0) {
+          flush.q0 = (rlo / 4) * S::D;
+          flush.load(px.xs, pend_par, tid);
+        }
       }
 
       // ------------------------------------- P7: LayerNorm second order
@@ -1098,7 +1129,10 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           // memory operations the compiler loses over the flush loop) waited
           // for these loads from HBM as well; issued here, they drain from the
           // memory pipeline while the next row step computes
-          if (it_ == 0) prefetch_q(u, rc, kc);
+          if (it_ == 0) {
+            prefetch_q(u, rc, kc);
+            if (S::NS > 1 && pend_s0 >= 0) flush.store(u * T + pend_s0, pend_len, rlo, tid);
+          }
         }
       }
       // MLP: A_Q and GELU'(H_Q) as the forward formed them (its query side at

@@ -25,7 +25,8 @@
 // which write back and invalidate the L2 for the other XCD.
 //
 // Every wait is bounded (by default kTimeoutTicks of the 100 MHz real-time
-// counter; the host passes the limit with the launch).  A
+// counter; the host passes the limit with the launch; a limit of zero makes
+// every wait give up before it reads a flag).  A
 // rank whose wait expires sets the status word, poisons its own flag so that
 // the others stop waiting too, and skips all later waits, so the grid always
 // drains; the results of that launch are then undefined and the status word
@@ -146,8 +147,12 @@ template <int NS> struct PairX {
       for (int k = 0; k < NS - 1; ++k) {
         const unsigned* xp = sync + kSyncLine * (1 + NS * ngroups + NS * p + other_rank(k, rank));
         unsigned o = 0;
-        while ((o = ld_dev(xp)) == 0u) {
-          if (__builtin_amdgcn_s_memrealtime() - t0 > limit) break;
+        // a limit of zero gives up at once, whatever the peer has written (a
+        // host-forced expiry); otherwise the flag is read first
+        if (limit > 0) {
+          while ((o = ld_dev(xp)) == 0u) {
+            if (__builtin_amdgcn_s_memrealtime() - t0 > limit) break;
+          }
         }
         if (o != id) same = 0;
         if (o == 0u) alive = 0;
@@ -192,6 +197,7 @@ template <int NS> struct PairX {
       int ok = 1;
 #pragma unroll
       for (int k = 0; k < NS - 1; ++k) {
+        if (ok && limit <= 0) ok = 0;   // zero limit: give up at once, as at init
         if (ok) {
           unsigned f;
           while ((f = ld_dev(peer[k])) < target) {

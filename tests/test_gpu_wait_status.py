@@ -48,7 +48,7 @@ def test_expired_waits_are_reported(fw, dh, monkeypatch):
     # normal limit: no expiry
     _, _, _, ws, _ = fwd_bwd(cfg, t, scratch)
     assert e2ttt.wait_status(cfg, workspace=ws, scratch=scratch) == 0
-    # zero limit: a wait whose peer has not posted yet gives up at once
+    # zero limit: every wait gives up at once
     monkeypatch.setenv("E2TTT_WAIT_LIMIT_US", "0")
     _, _, _, ws0, _ = fwd_bwd(cfg, t, scratch)
     st_f = e2ttt.wait_status(cfg, workspace=ws0)
