@@ -642,16 +642,15 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
                         ((u * E2TTT_ARG(ckpt_nc) + rc) * S::NS + rank) * 2 * E2TTT_ARG(ckpt_stride);
       const char* ckM = ckW + E2TTT_ARG(ckpt_stride);
 
-      // chunk-start weights W_0 (kept for the whole chunk) and momentum M_0
-      // (for the carry adjoints), issued first so that P0 and P3 hide them
+      // chunk-start weights W_0 (kept for the whole chunk), issued first so
+      // that P0 and P3 hide them; momentum M_0 (for the carry adjoints after
+      // P3) follows after P0, so that the two bursts of loads each drain under
+      // a phase
       Q w0q[NMAT][NJB][NIB], m0q[NMAT][NJB][NIB];
       {
         E2TTT_LANE_IDS;
 #pragma unroll
-        for (int m = 0; m < NMAT; ++m) {
-          load_ckpt_mat<S>(w0q[m], ckW, m, w, lane);
-          load_ckpt_mat<S>(m0q[m], ckM, m, w, lane);
-        }
+        for (int m = 0; m < NMAT; ++m) load_ckpt_mat<S>(w0q[m], ckW, m, w, lane);
       }
 
       // ---------------------------------------------------------- P0: stage
@@ -669,6 +668,11 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         if (tid < 3) scar[tid] = pcar;
       }
       __syncthreads();
+      {
+        E2TTT_LANE_IDS;
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m) load_ckpt_mat<S>(m0q[m], ckM, m, w, lane);
+      }
 
       // --------------------- P3: e, dY (first order, from the saved LN output)
       E* dyl = reinterpret_cast<E*>(rr + L::TDX);   // dY [t][i]
