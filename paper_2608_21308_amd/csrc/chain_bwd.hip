@@ -1002,7 +1002,7 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
 #pragma unroll 1
         for (int v = tid; v < S::CM * D / 4; v += S::NT)
           reinterpret_cast<float4*>(mine)[v] = reinterpret_cast<const float4*>(dyh)[v];
-        px.post();                                  // seq0 + 1: dYh partial
+        px.post();                                  // seq0 + 1: dYh partial, previous tile's dk, dq
         px.wait_for(seq0 + 1, sword);               // the peers'
         // the peers' rows of every P7 step, loaded before the global stores
         // below (which would otherwise order each step's loads after them)
@@ -1448,19 +1448,24 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
             }
       }
       }
+      // The dk, dq partials stored above go out with the next post (the next
+      // tile's dYh post, or the one after the unit's last tile): the peers
+      // read them only after that post anyway, and a post here would wait
+      // for every memory operation in flight (the next tile's loads among
+      // them).  The barrier guards the LDS regions that the next tile's
+      // staging rewrites.
+      __syncthreads();
       if constexpr (S::NS > 1) {
-        px.post();                                  // seq0 + 2: dk, dq partials
         pend_s0 = s0;
         pend_len = len;
         pend_par = par;
-      } else {
-        __syncthreads();
       }
     }
 
     if constexpr (S::NS > 1) {
       E2TTT_LANE_IDS;
-      px.wait_for(px.seq_now(), sword);             // the peers' last post
+      px.post();                                    // the last tile's dk, dq partials
+      px.wait_for(px.seq_now(), sword);             // the peers'
       if (pend_s0 >= 0)
         flush_dkdq<S>(px.xs, pend_par, u * T + pend_s0, pend_len, rlo, tid);
       __syncthreads();
