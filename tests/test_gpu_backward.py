@@ -163,6 +163,22 @@ def test_backward_swiglu_more_units_than_resident_groups():
         assert_tol(errors(g, sub, [u], C=w.C), "bf16", "bwd swiglu B8 H16 bare unit %d" % u)
 
 
+def test_backward_mlp_pairs_take_several_units():
+    # the headline MLP net (two workgroups per unit) with twice as many units
+    # as the device holds pairs at once: each pair runs two units in turn, so
+    # the exchange sequence carries over from one unit to the next (the last
+    # tile's dk/dq partials are posted after the unit's chunk loop); ragged
+    # last chunk; oracle on units of both turns, checked unit by unit
+    w = WL.WORKLOADS[3].with_(B=8, H=32, T=130, C=64)
+    x = WL.make_inputs(w)
+    g = gpu_fwd_bwd(w, x)
+    units = [0, 127, 128, 255]
+    ref = oracle_bwd(w, WL.make_inputs(w, units=units))
+    for i, u in enumerate(units):
+        sub = {n: None if r is None else r[:, i:i + 1] for n, r in ref.items()}
+        assert_tol(errors(g, sub, [u], C=w.C), "bf16", "bwd mlp B8 H32 unit %d" % u)
+
+
 def test_backward_swiglu_literal_net_workload():
     w = WL.WORKLOADS[2]
     x = WL.make_inputs(w)
