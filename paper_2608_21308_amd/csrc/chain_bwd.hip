@@ -346,17 +346,26 @@ __device__ __forceinline__ typename S::E* bwd_part(float* slot, int sec) {
 // 0's carries the -eh and dO terms), rows [rlo, min(CM, rlo + RPW)) below len
 // (rlo and RPW are multiples of 4).  An item is one row quad of one column:
 // one quad load per rank, four element stores, each coalesced over the wave's
-// 64 consecutive columns.  load() reads and adds the partials, store() writes
-// the rows, so that the stores can go out later than the loads.
+// 64 consecutive columns.  load() issues every rank's partial quads and
+// store() widens, adds and writes them, so that the loads travel while the
+// caller works in between: a partial added as soon as it is loaded would
+// wait for each load in turn, and every such wait also waits for whatever
+// memory operations were issued before it.  The raw quads take as many
+// registers as the sums with two ranks; with more ranks, load() adds them
+// itself once all are in flight.
 template <class S>
 struct FlushDkDq {
+  using Q = typename S::O::Q;
   static constexpr int RPW = row_share<S>();
   static_assert(RPW % 4 == 0, "row shares in whole row quads");
   static constexpr int NV = (RPW / 4) * S::D;
   static constexpr int NPT = (NV + S::NT - 1) / S::NT;   // items per thread
-  f32x4 x[NPT][2];
+  static constexpr bool RAW = S::NS <= 2;                // sums formed in store()
+  Q raw[RAW ? NPT : 1][2][RAW ? S::NS : 1];
+  f32x4 x[RAW ? 1 : NPT][2];
 
   __device__ __forceinline__ void load(long p, int parity, int tid) {
+    Q q[NPT][2][S::NS];
 #pragma unroll
     for (int a = 0; a < NPT; ++a) {
       // the item's quad; items past the rank's share or the tile (the last
@@ -364,14 +373,26 @@ struct FlushDkDq {
       const int qi = q0 + tid + a * S::NT;
       const int qs = (tid + a * S::NT < NV && qi < (S::CM / 4) * S::D) ? qi : 0;
 #pragma unroll
-      for (int sec = 1; sec <= 2; ++sec) {
-        x[a][sec - 1] = zero4();
+      for (int sec = 1; sec <= 2; ++sec)
 #pragma unroll
         for (int rk = 0; rk < S::NS; ++rk)
-          x[a][sec - 1] += quad_f32(ld_xchg(E2TTT_ARG(xbuf),
-              reinterpret_cast<const typename S::O::Q*>(
-                  bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec)), qs));
-      }
+          q[a][sec - 1][rk] = ld_xchg(E2TTT_ARG(xbuf),
+              reinterpret_cast<const Q*>(bwd_part<S>(bwd_slot<S>(E2TTT_ARG(xbuf), p, rk, parity), sec)),
+              qs);
+    }
+    if constexpr (RAW) {
+#pragma unroll
+      for (int a = 0; a < NPT; ++a)
+#pragma unroll
+        for (int sec = 0; sec < 2; ++sec)
+#pragma unroll
+          for (int rk = 0; rk < S::NS; ++rk) raw[a][sec][rk] = q[a][sec][rk];
+    } else {
+      sched_fence();   // every load issued before the first sum waits for one
+#pragma unroll
+      for (int a = 0; a < NPT; ++a)
+#pragma unroll
+        for (int sec = 0; sec < 2; ++sec) x[a][sec] = sum_quads(q[a][sec]);
     }
   }
   __device__ __forceinline__ void store(long row0, int len, int rlo, int tid) const {
@@ -387,11 +408,21 @@ struct FlushDkDq {
 #pragma unroll
       for (int sec = 1; sec <= 2; ++sec) {
         typename IO::T* d = (sec == 1) ? dk : dq;
+        f32x4 xs;
+        if constexpr (RAW) xs = sum_quads(raw[a][sec - 1]);
+        else xs = x[a][sec - 1];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (4 * tq + r < tend) IO::st(d + (4 * tq + r) * S::D + i, x[a][sec - 1][r]);
+          if (4 * tq + r < tend) IO::st(d + (4 * tq + r) * S::D + i, xs[r]);
       }
     }
+  }
+  // the ranks' partials widened and added in rank order, from zero
+  static __device__ __forceinline__ f32x4 sum_quads(const Q (&qr)[S::NS]) {
+    f32x4 acc = zero4();
+#pragma unroll
+    for (int rk = 0; rk < S::NS; ++rk) acc += quad_f32(qr[rk]);
+    return acc;
   }
   int q0 = 0;   // quad index of the rank's first row quad, set with the loads
 };
