@@ -244,7 +244,7 @@ def oracle_state_at(x, w, r, flags=0):
 
 
 @pytest.mark.parametrize("cfg_idx,units,starts", [(2, None, [0, 1, 3, 8, 17, 24, 31]),
-                                                  (4, [5], [0, 1, 50, 100, 300, 511])])
+                                                  (4, [0, 5, 10, 15], [0, 1, 50, 100, 300, 511])])
 def test_swiglu_ln_chunk_windows(cfg_idx, units, starts):
     # One chunk at a time from the oracle's own chunk-start state.  The bound
     # is 2e-2, widened only where the chunk itself is ill-conditioned: the
