@@ -1088,14 +1088,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
           } else if constexpr (S::NS > 1) {
             // every rank's partial from its slot (this rank's too), added in
             // rank order as sum_ranks does: the same sum on every rank
-#pragma unroll
-            for (int r = 0; r < S::NS; ++r) {
-              float pr[EPL];
-              load_row_xchg<EPL>(pr, E2TTT_ARG(xbuf),
-                                 bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par), t * D + l16 * EPL);
-#pragma unroll
-              for (int q = 0; q < EPL; ++q) dyhv[q] = (r == 0) ? pr[q] : dyhv[q] + pr[q];
-            }
+            sum_rows_xchg<S::NS, EPL>(dyhv, E2TTT_ARG(xbuf),
+                                      [&](int r) { return bwd_slot<S>(E2TTT_ARG(xbuf), px.xs, r, par); },
+                                      t * D + l16 * EPL);
           }
           if (resln) {
             float z[EPL], dyv[EPL], zh[EPL];
@@ -1458,25 +1453,40 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         // Wb = Wb_C + this tile's contributions: move them to the second block
         // and restore Wb_C, or (the chunk's last tile processed) apply the
         // transition with all of them
+        // The blocks' tiles are read four at a time, all before any is used:
+        // one at a time, each read would wait for the one before it.
         const float cw = scar[0], cm = scar[1], cbv = scar[2];
+        constexpr int NE = NMAT * NJB * NIB, NBAT = 4;
 #pragma unroll
-        for (int m = 0; m < NMAT; ++m)
+        for (int e0 = 0; e0 < NE; e0 += NBAT) {
+          f32x4 f[NBAT], pc[NBAT];
 #pragma unroll
-          for (int jj = 0; jj < NJB; ++jj)
+          for (int k = 0; k < NBAT; ++k) {
+            if (e0 + k < NE) {
+              const long idx = (long)(e0 + k) * S::NT + tid;
+              f[k] = frz[idx];
+              pc[k] = firstp ? zero4() : frz[NB + idx];
+            }
+          }
+          sched_fence();
 #pragma unroll
-            for (int ib = 0; ib < NIB; ++ib) {
-              const long idx = ((m * NJB + jj) * NIB + ib) * S::NT + tid;
-              const f32x4 f = frz[idx];
-              const f32x4 dacc = firstp ? Wb.t[m][jj][ib] - f : frz[NB + idx] + (Wb.t[m][jj][ib] - f);
+          for (int k = 0; k < NBAT; ++k) {
+            const int e = e0 + k;
+            if (e < NE) {
+              const int m = e / (NJB * NIB), jj = (e / NIB) % NJB, ib = e % NIB;
+              const long idx = (long)e * S::NT + tid;
+              const f32x4 dacc = firstp ? Wb.t[m][jj][ib] - f[k] : pc[k] + (Wb.t[m][jj][ib] - f[k]);
               if (lastp) {
-                Wb.t[m][jj][ib] = cw * f + dacc;
-                Mb.t[m][jj][ib] = cm * f + cbv * Mb.t[m][jj][ib];
+                Wb.t[m][jj][ib] = cw * f[k] + dacc;
+                Mb.t[m][jj][ib] = cm * f[k] + cbv * Mb.t[m][jj][ib];
               } else {
                 frz[NB + idx] = dacc;
-                Wb.t[m][jj][ib] = f;
+                Wb.t[m][jj][ib] = f[k];
               }
-              sched_fence();
             }
+          }
+          sched_fence();
+        }
       }
       }
       // The dk, dq partials stored above go out with the next post (the next
