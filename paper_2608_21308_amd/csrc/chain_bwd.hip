@@ -437,12 +437,12 @@ __device__ __forceinline__ void flush_dkdq(long p, int parity, long row0, int le
 
 // LONG: chunks longer than the CM-row tile.  Their tiles are processed last
 // to first; every tile's P4 needs the adjoint state at the chunk end (Wb_C,
-// Mb_C) while P8 and P9 add the tile's contributions to Wb.  So Wb_C is kept
-// in a per-workgroup fp32 buffer from the chunk's first processed tile on; at
-// the end of each tile the contribution Wb - Wb_C moves to a second buffer and
-// Wb is reset to Wb_C; after the chunk's last processed tile (its first) the
-// transition Wb_0 = cw Wb_C + sum of contributions, Mb_0 = cm Wb_C + cb Mb_C
-// is applied once.
+// Mb_C) as its product operands, while P8 and P9 add the tile's contributions
+// to the adjoint of W_0.  So the chunk's first processed tile (its last) keeps
+// the operand copies of Wb_C and Mb_C in a per-workgroup buffer, applies the
+// transition Wb_0 = cw Wb_C (+ contributions), Mb_0 = cm Wb_C + cb Mb_C right
+// after its P4 as a one-tile chunk does, and every tile adds its contributions
+// to Wb; the chunk's other tiles take their P4 operands from the buffer.
 template <class S, bool LONG, bool PN>
 __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   using O = typename S::O;
@@ -486,7 +486,9 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
   const int TL = LONG ? S::CM : C;                       // tokens per tile
   auto ntiles = [&](int rc) { return LONG ? (min(T, (rc + 1) * C) - rc * C + TL - 1) / TL : 1; };
   constexpr int NB = NMAT * NJB * NIB * S::NT;            // float4 per frozen block
-  f32x4* const frz = LONG ? reinterpret_cast<f32x4*>(E2TTT_ARG(bfrz)) + (long)blockIdx.x * 2 * NB : nullptr;
+  // LONG: the operand copies of Wb_C, then of Mb_C (NB quads each, register-tile order)
+  Q* const frz = LONG ? reinterpret_cast<Q*>(reinterpret_cast<f32x4*>(E2TTT_ARG(bfrz)) + (long)blockIdx.x * 2 * NB)
+                      : nullptr;
 
   PairX<S::NS> px;
   px.init(a.sync, a.npairs, sword, a.wait_ticks);
@@ -549,7 +551,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       const int cend = LONG ? min(T, (r + 1) * C) : 0;
       const int len = LONG ? min(TL, cend - s0) : min(C, T - s0);
       const bool firstp = !LONG || s0 + TL >= cend;   // the chunk's first tile processed (its last)
-      const bool lastp = !LONG || kt == 0;            // the chunk's last tile processed (its first)
       const int rc = r, kc = kt;                      // this tile
       if (kt > 0) --kt;
       else if (--r >= 0) kt = ntiles(r) - 1;
@@ -793,14 +794,17 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         pcm = wave_sum(pcm);
         pcb = wave_sum(pcb);
         if (lane == 0) { cbp[w * 4 + 0] = pcw; cbp[w * 4 + 1] = pcm; cbp[w * 4 + 2] = pcb; }
-        if constexpr (LONG) {   // keep Wb_C for the chunk's other tiles
+        if constexpr (LONG) {   // Wb_C, Mb_C operands for the chunk's other tiles
 #pragma unroll
           for (int m = 0; m < NMAT; ++m)
 #pragma unroll
             for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-              for (int ib = 0; ib < NIB; ++ib)
-                frz[((m * NJB + jj) * NIB + ib) * S::NT + tid] = Wb.t[m][jj][ib];
+              for (int ib = 0; ib < NIB; ++ib) {
+                const long idx = ((m * NJB + jj) * NIB + ib) * S::NT + tid;
+                frz[idx] = O::cvt(Wb.t[m][jj][ib]);
+                frz[NB + idx] = O::cvt(Mb.t[m][jj][ib]);
+              }
         }
       }
 
@@ -834,15 +838,29 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         const auto& w2q = w0q[SEC];
         opaque_state<S>(Wb);
         opaque_state<S>(Mb);
+        if (LONG && !firstp) {   // Wb, Mb hold the chunk's W_0 adjoints by now
+          E2TTT_LANE_IDS;
 #pragma unroll
-        for (int m = 0; m < NMAT; ++m)
+          for (int m = 0; m < NMAT; ++m)
 #pragma unroll
-          for (int jj = 0; jj < NJB; ++jj)
+            for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-            for (int ib = 0; ib < NIB; ++ib) {
-              wbq[m][jj][ib] = O::cvt(Wb.t[m][jj][ib]);
-              mbq[m][jj][ib] = O::cvt(Mb.t[m][jj][ib]);
-            }
+              for (int ib = 0; ib < NIB; ++ib) {
+                const long idx = ((m * NJB + jj) * NIB + ib) * S::NT + tid;
+                wbq[m][jj][ib] = frz[idx];
+                mbq[m][jj][ib] = frz[NB + idx];
+              }
+        } else {
+#pragma unroll
+          for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+            for (int jj = 0; jj < NJB; ++jj)
+#pragma unroll
+              for (int ib = 0; ib < NIB; ++ib) {
+                wbq[m][jj][ib] = O::cvt(Wb.t[m][jj][ib]);
+                mbq[m][jj][ib] = O::cvt(Mb.t[m][jj][ib]);
+              }
+        }
         // The products of token block (tb, jj) (dA, rW, rM, then hk, uW, uM of
         // each first-layer matrix) are issued one item ahead of the arithmetic
         // that uses them, in the same scheduling region, so that the matrix
@@ -999,8 +1017,8 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
       }
 
       // ------------------------------------ P5: adjoint state transition
-      // (LONG: once per chunk, after its last tile processed)
-      if constexpr (!LONG) {
+      // (LONG: once per chunk, at its first tile processed)
+      if (!LONG || firstp) {
         const float cw = scar[0], cm = scar[1], cbv = scar[2];
 #pragma unroll
         for (int m = 0; m < NMAT; ++m)
@@ -1448,45 +1466,6 @@ __global__ void __launch_bounds__(S::NT, 1) chain_bwd_kernel(ChainArgs a) {
         float sacc = 0.0f;
         for (int ww = 0; ww < NW; ++ww) sacc += cbp[ww * 4 + tid];
         carryb_slot[(u * NC + rc) * 3 + tid] = sacc;
-      }
-      if constexpr (LONG) {
-        // Wb = Wb_C + this tile's contributions: move them to the second block
-        // and restore Wb_C, or (the chunk's last tile processed) apply the
-        // transition with all of them
-        // The blocks' tiles are read four at a time, all before any is used:
-        // one at a time, each read would wait for the one before it.
-        const float cw = scar[0], cm = scar[1], cbv = scar[2];
-        constexpr int NE = NMAT * NJB * NIB, NBAT = 4;
-#pragma unroll
-        for (int e0 = 0; e0 < NE; e0 += NBAT) {
-          f32x4 f[NBAT], pc[NBAT];
-#pragma unroll
-          for (int k = 0; k < NBAT; ++k) {
-            if (e0 + k < NE) {
-              const long idx = (long)(e0 + k) * S::NT + tid;
-              f[k] = frz[idx];
-              pc[k] = firstp ? zero4() : frz[NB + idx];
-            }
-          }
-          sched_fence();
-#pragma unroll
-          for (int k = 0; k < NBAT; ++k) {
-            const int e = e0 + k;
-            if (e < NE) {
-              const int m = e / (NJB * NIB), jj = (e / NIB) % NJB, ib = e % NIB;
-              const long idx = (long)e * S::NT + tid;
-              const f32x4 dacc = firstp ? Wb.t[m][jj][ib] - f[k] : pc[k] + (Wb.t[m][jj][ib] - f[k]);
-              if (lastp) {
-                Wb.t[m][jj][ib] = cw * f[k] + dacc;
-                Mb.t[m][jj][ib] = cm * f[k] + cbv * Mb.t[m][jj][ib];
-              } else {
-                frz[NB + idx] = dacc;
-                Wb.t[m][jj][ib] = f[k];
-              }
-            }
-          }
-          sched_fence();
-        }
       }
       }
       // The dk, dq partials stored above go out with the next post (the next

@@ -263,13 +263,13 @@ __device__ __forceinline__ void load_row_xchg(float (&dst)[EPL], const void* buf
 // Sum, in rank order from rank 0 (so every rank forms the same sum), of the
 // NS ranks' exchange rows: EPL consecutive floats at element offset `off` of
 // each rank's slot, slot(r) giving rank r's.  The loads go out a batch of
-// ranks at a time (up to 16 floats in flight per lane) before any is added:
+// ranks at a time (up to 32 floats in flight per lane) before any is added:
 // a row added as soon as it arrives would wait for each load in turn, and each
 // such wait also covers every memory operation issued before it.
 template <int NS, int EPL, class SLOT>
 __device__ __forceinline__ void sum_rows_xchg(float (&acc)[EPL], const void* buf, SLOT slot,
                                               int off) {
-  constexpr int RB = (16 / EPL < 1) ? 1 : ((16 / EPL > NS) ? NS : 16 / EPL);
+  constexpr int RB = (32 / EPL < 1) ? 1 : ((32 / EPL > NS) ? NS : 32 / EPL);
 #pragma unroll
   for (int r0 = 0; r0 < NS; r0 += RB) {
     float pr[RB][EPL];
