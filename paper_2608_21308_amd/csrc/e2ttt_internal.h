@@ -75,10 +75,11 @@ struct ChainArgs {
   // layout: SavedAct in chain_common.h)
   void* asave;
   long as_stride;       // bytes per (unit, chunk tile, rank) block
-  // backward of chunks longer than one tile: per workgroup, the adjoint state
-  // at the chunk end and the sum of the tiles' contributions to its update
-  // (fp32, in the register-tile order of the state), two blocks of
-  // chain_frz_floats(cfg) floats each
+  // backward of chunks longer than one tile: per workgroup, the MFMA operand
+  // copies of the adjoint state at the chunk end (that of W, then that of M,
+  // in the operand type and the register-tile order of the state), kept by
+  // the chunk's first processed tile for its other tiles; room for two blocks
+  // of chain_frz_floats(cfg) floats (the fp32 path fills both, bf16 half)
   float* bfrz;
   // forward of chunks longer than one tile with operands re-formed from the
   // state (SwiGLU on bf16): per workgroup, the chunk-start weights W_0 (fp32,
@@ -191,7 +192,8 @@ hipError_t launch_zero_words(unsigned* p, long n, hipStream_t stream);
 long chain_max_pairs(const ChainConfig& cfg, bool backward);
 // Bytes of one checkpoint block (W or M of one unit's workgroup at one chunk start).
 long chain_ckpt_bytes(const ChainConfig& cfg);
-// floats of one workgroup's frozen adjoint-state block (long-chunk backward)
+// floats of one workgroup's fp32 state block (register-tile order): the unit of
+// the long-chunk buffers bfrz and w0blk
 long chain_frz_floats(const ChainConfig& cfg);
 // Bytes of one saved-activation block (one unit's workgroup, one chunk); 0 when
 // the backward recomputes the activations instead (SwiGLU).
