@@ -168,8 +168,8 @@ def test_backward_mlp_pairs_take_several_units():
     # as the device holds pairs at once: each pair runs two units in turn, so
     # the exchange sequence carries over from one unit to the next (the last
     # tile's dk/dq partials are posted after the unit's chunk loop); ragged
-    # last chunk; oracle on units of both turns, checked unit by unit
-    w = WL.WORKLOADS[3].with_(B=8, H=32, T=130, C=64)
+    # last chunk (58 tokens); oracle on units of both turns, checked unit by unit
+    w = WL.WORKLOADS[3].with_(B=8, H=32, T=250, C=64)
     x = WL.make_inputs(w)
     g = gpu_fwd_bwd(w, x)
     units = [0, 127, 128, 255]
