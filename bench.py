@@ -91,8 +91,8 @@ def cpu_baseline(w, seconds_hint: float = 20.0) -> dict:
 
 def time_long_chunk(e2ttt, w, t, dev, reps: int = 10) -> dict:
     """Forward (no saving) of the same layer at chunk 64 and at the paper's
-    chunk 512 (64-token tiles at the chunk-start weights): HIP events around
-    back-to-back calls."""
+    chunk 512 (64-token tiles at the chunk-start weights), and the fwd+bwd
+    step at chunk 512: HIP events around back-to-back calls."""
     import torch
     res = {}
     for C in (w.C, 512):
@@ -117,6 +117,36 @@ def time_long_chunk(e2ttt, w, t, dev, reps: int = 10) -> dict:
         ms = ev[0].elapsed_time(ev[1]) / reps
         res["C%d_fwd_ms" % C] = ms
         res["C%d_tokens_per_s" % C] = w.B * w.T / (ms * 1e-3)
+    # the training step (forward saving for the backward, then the backward) at
+    # chunk 512, as the headline step is timed at the workload's chunk
+    cfg = e2ttt.Config(w.B, w.H, w.T, w.d, w.dh, 512, w.fw, e2ttt.DT_BF16)
+    ws = e2ttt.alloc_workspace(cfg, True, dev)
+    scratch = torch.empty(e2ttt.backward_scratch_bytes(cfg), dtype=torch.uint8, device=dev)
+    out = torch.empty_like(t["q"])
+    wo, mo = torch.empty_like(t["w_in"]), torch.empty_like(t["w_in"])
+    grads = dict(dq=torch.empty_like(t["q"]), dk=torch.empty_like(t["k"]), dv=torch.empty_like(t["v"]),
+                 d_eta=torch.empty_like(t["eta"]), d_beta=torch.empty_like(t["beta"]),
+                 d_gamma=torch.empty_like(t["gamma"]), d_w_in=torch.empty_like(t["w_in"]),
+                 d_m_in=torch.empty_like(t["w_in"]))
+
+    def step():
+        e2ttt.forward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"], t["w_in"], None,
+                      out=out, w_out=wo, m_out=mo, workspace=ws, save_for_backward=True)
+        e2ttt.backward(cfg, t["q"], t["k"], t["v"], t["eta"], t["beta"], t["gamma"], t["w_in"], None,
+                       ws, t["d_out"], grads=grads, scratch=scratch)
+
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        step()
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    res["C512_step_ms"] = ms
+    res["C512_step_tokens_per_s"] = w.B * w.T / (ms * 1e-3)
     return res
 
 
