@@ -360,6 +360,9 @@ def main():
                     help="time only the headline step (no averaged-rule, gate or decode timings)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this size (for counter calibration)")
+    ap.add_argument("--workloads-only", action="store_true",
+                    help="time only the other workloads and the paper's 1.3B shape (for a kernel "
+                         "trace of their kernels); prints their timings as one JSON object")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the chunk update shards over (batch, head) units "
@@ -368,6 +371,11 @@ def main():
 
     import torch
     from paper_2608_21308_amd import e2ttt, workloads as WL
+
+    if args.workloads_only:
+        print(json.dumps({"other_workloads": time_workloads(e2ttt, WL, torch.device("cuda:0")),
+                          "source_hash": source_hash()}), flush=True)
+        return
 
     w = WL.WORKLOADS[3]
     x = WL.make_inputs(w)

@@ -100,8 +100,29 @@ struct LongScalars {
   float carry[3];                                // (g~_0, beta_1 S_1, b~_0)
 };
 
-__device__ __forceinline__ void long_scalars(const float* eta, const float* beta,
-                                             const float* gamma, long base, int len, int lane,
+// One lane's token of every segment of a long chunk (eta, beta, gamma, with
+// the neutral values 0, 1, 1 past the chunk's end).  Every load goes out at
+// once, from an index clamped to the chunk's first token so that it stays in
+// bounds; the segment walks below then run on registers (loads issued segment
+// by segment would each wait a full memory round trip).
+struct LongInputs {
+  float e[kMaxSeg], b[kMaxSeg], g[kMaxSeg];
+};
+__device__ __forceinline__ void long_inputs(const float* eta, const float* beta,
+                                            const float* gamma, long base, int len, int lane,
+                                            LongInputs& x) {
+#pragma unroll
+  for (int seg = 0; seg < kMaxSeg; ++seg) {
+    const bool valid = seg * 64 + lane < len;
+    const long i = valid ? base + seg * 64 + lane : base;
+    const float e = eta[i], b = beta[i], g = gamma ? gamma[i] : 1.0f;
+    x.e[seg] = valid ? e : 0.0f;
+    x.b[seg] = valid ? b : 1.0f;
+    x.g[seg] = valid ? g : 1.0f;
+  }
+}
+
+__device__ __forceinline__ void long_scalars(const LongInputs& x, int len, int lane,
                                              LongScalars& o) {
   float cb = 1.0f, cg = 1.0f;           // products of beta, gamma over the later segments
   float s_next = 0.0f, b_next = 1.0f;   // S and beta at the next segment's first token
@@ -109,11 +130,9 @@ __device__ __forceinline__ void long_scalars(const float* eta, const float* beta
 #pragma unroll
   for (int seg = kMaxSeg - 1; seg >= 0; --seg) {
     if (seg >= nseg) continue;          // uniform
-    const long sb = base + seg * 64;
     const int n = min(64, len - seg * 64);
-    const bool valid = lane < n;
-    const float b = valid ? beta[sb + lane] : 1.0f;
-    const float gm = (valid && gamma) ? gamma[sb + lane] : 1.0f;
+    const float b = x.b[seg];
+    const float gm = x.g[seg];
     float pb = b, pg = gm;
 #pragma unroll
     for (int k = 1; k < 64; k <<= 1) {
@@ -150,15 +169,17 @@ __device__ __forceinline__ void long_scalars(const float* eta, const float* beta
 }
 
 __device__ void coeff_fwd_long(const CoeffFwdArgs& a, long wid, long base, int len, int lane) {
+  LongInputs x;
+  long_inputs(a.eta, a.beta, a.gamma, base, len, lane, x);
   LongScalars o;
-  long_scalars(a.eta, a.beta, a.gamma, base, len, lane, o);
+  long_scalars(x, len, lane, o);
   const int nseg = (len + 63) / 64;
 #pragma unroll
   for (int seg = 0; seg < kMaxSeg; ++seg) {
     if (seg >= nseg) break;
     const long sb = base + seg * 64;
     if (lane < min(64, len - seg * 64)) {
-      const float e = a.eta[sb + lane];
+      const float e = x.e[seg];
       a.kw[sb + lane] = e * o.S[seg];
       a.km[sb + lane] = e * o.bt[seg];
     }
@@ -229,10 +250,45 @@ __global__ void __launch_bounds__(256) coeff_fwd_kernel(CoeffFwdArgs a) {
 // (every scan is ascending); each segment's scans start from the previous
 // segment's last values (S-hat, Y, Z, and the previous token's beta, gamma and
 // K^M eta), which enter lane 0 as x_0 = a_0 + b_0 x_{-1}.
+// Token t's adjoints of K^W and K^M summed over the ns workgroup slots, in
+// slot order from slot 0.  The slot loop runs to the largest ns with every
+// load issued (slot index clamped to ns - 1, in bounds) and the surplus
+// slots added as zeros, so the loads go out together instead of one slot
+// per memory round trip.
+constexpr int kMaxSlots = 8;
+__device__ __forceinline__ void sum_slots(const CoeffBwdArgs& a, long t, bool valid, float& kw,
+                                          float& km) {
+  float w[kMaxSlots], m[kMaxSlots];
+#pragma unroll
+  for (int sl = 0; sl < kMaxSlots; ++sl) {
+    const long o = (long)min(sl, a.ns - 1) * a.tok_slot + t;
+    w[sl] = a.kwb[o];
+    m[sl] = a.kmb[o];
+  }
+  kw = 0.0f;
+  km = 0.0f;
+#pragma unroll
+  for (int sl = 0; sl < kMaxSlots; ++sl) {
+    if (valid && sl < a.ns) {
+      kw += w[sl];
+      km += m[sl];
+    }
+  }
+}
+
 __device__ void coeff_bwd_long(const CoeffBwdArgs& a, long wid, long base, int len, int lane,
                                float cwb, float cmb, float cbb) {
+  LongInputs x;
+  long_inputs(a.eta, a.beta, a.gamma, base, len, lane, x);
+  // the token adjoints of every segment, summed over the workgroup slots
+  float kwv[kMaxSeg], kmv[kMaxSeg];
+#pragma unroll
+  for (int seg = 0; seg < kMaxSeg; ++seg) {
+    const bool valid = seg * 64 + lane < len;
+    sum_slots(a, valid ? base + seg * 64 + lane : base, valid, kwv[seg], kmv[seg]);
+  }
   LongScalars o;
-  long_scalars(a.eta, a.beta, a.gamma, base, len, lane, o);
+  long_scalars(x, len, lane, o);
   const int nseg = (len + 63) / 64;
   float sh_last = 0.0f, kme_last = 0.0f, b_last = 1.0f, g_last = 1.0f, y_last = 0.0f,
         z_last = 0.0f;
@@ -242,16 +298,10 @@ __device__ void coeff_bwd_long(const CoeffBwdArgs& a, long wid, long base, int l
     const long sb = base + seg * 64;
     const int n = min(64, len - seg * 64);
     const bool valid = lane < n;
-    const float e = valid ? a.eta[sb + lane] : 0.0f;
-    const float b = valid ? a.beta[sb + lane] : 1.0f;
-    const float gm = (valid && a.gamma) ? a.gamma[sb + lane] : 1.0f;
-    float kwb = 0.0f, kmb = 0.0f;
-    for (int sl = 0; sl < a.ns; ++sl) {
-      if (valid) {
-        kwb += a.kwb[sl * a.tok_slot + sb + lane];
-        kmb += a.kmb[sl * a.tok_slot + sb + lane];
-      }
-    }
+    const float e = x.e[seg];
+    const float b = x.b[seg];
+    const float gm = x.g[seg];
+    const float kwb = kwv[seg], kmb = kmv[seg];
     const float S = o.S[seg], bt = o.bt[seg], gt = o.gt[seg];
     const bool t0 = seg == 0 && lane == 0;            // the chunk's first token
     const float etab = kwb * S + kmb * bt;
@@ -286,6 +336,9 @@ __device__ void coeff_bwd_long(const CoeffBwdArgs& a, long wid, long base, int l
   }
 }
 
+// LONGC: chunks longer than one wave's 64 tokens (a separate instantiation,
+// so that the short-chunk kernel keeps its small register footprint).
+template <bool LONGC>
 __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
   const long wid = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (wid >= a.nwork) return;
@@ -297,15 +350,23 @@ __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
   const long base = u * a.T + s0;
   const bool valid = lane < len;
   // the chain kernel leaves one partial per workgroup of a unit; sum them
-  float kwb = 0.0f, kmb = 0.0f, cwb = 0.0f, cmb = 0.0f, cbb = 0.0f;
-  for (int sl = 0; sl < a.ns; ++sl) {
-    if (valid) {
-      kwb += a.kwb[sl * a.tok_slot + base + lane];
-      kmb += a.kmb[sl * a.tok_slot + base + lane];
+  float kwb, kmb, cwb = 0.0f, cmb = 0.0f, cbb = 0.0f;
+  sum_slots(a, valid ? base + lane : base, valid, kwb, kmb);
+  float cv[kMaxSlots][3];
+#pragma unroll
+  for (int sl = 0; sl < kMaxSlots; ++sl) {
+    const long o = (long)min(sl, a.ns - 1) * a.chk_slot + wid * 3;
+    cv[sl][0] = a.carryb[o];
+    cv[sl][1] = a.carryb[o + 1];
+    cv[sl][2] = a.carryb[o + 2];
+  }
+#pragma unroll
+  for (int sl = 0; sl < kMaxSlots; ++sl) {
+    if (sl < a.ns) {
+      cwb += cv[sl][0];
+      cmb += cv[sl][1];
+      cbb += cv[sl][2];
     }
-    cwb += a.carryb[sl * a.chk_slot + wid * 3 + 0];
-    cmb += a.carryb[sl * a.chk_slot + wid * 3 + 1];
-    cbb += a.carryb[sl * a.chk_slot + wid * 3 + 2];
   }
   if (a.averaged) {
     const float inv = 1.0f / (float)len;
@@ -323,7 +384,7 @@ __global__ void __launch_bounds__(256) coeff_bwd_kernel(CoeffBwdArgs a) {
     }
     return;
   }
-  if (len > 64) {
+  if (LONGC && len > 64) {
     coeff_bwd_long(a, wid, base, len, lane, cwb, cmb, cbb);
     return;
   }
@@ -375,8 +436,12 @@ hipError_t launch_coeff_fwd(const CoeffFwdArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_coeff_bwd(const CoeffBwdArgs& a, hipStream_t stream) {
+  if (a.ns < 1 || a.ns > kMaxSlots) return hipErrorInvalidValue;
   const unsigned blocks = (unsigned)((a.nwork + 3) / 4);
-  hipLaunchKernelGGL(coeff_bwd_kernel, dim3(blocks), dim3(256), 0, stream, a);
+  if (a.C > 64)
+    hipLaunchKernelGGL(coeff_bwd_kernel<true>, dim3(blocks), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(coeff_bwd_kernel<false>, dim3(blocks), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
